@@ -1,0 +1,412 @@
+// SMetric matching/routing oracle: the plain, sequential CPU definition of what the
+// request -> KV-holder matching hot path computes.
+//
+// TEST INFRASTRUCTURE ONLY. Nothing in the product library links, loads or calls this
+// file; only the test suite, the smoke check and the CPU-baseline leg of the benchmark
+// do. It shares no code, header, table or constant generator with the GPU library.
+//
+// Paper: "SMetric: Rethink LLM Scheduling for Serving Agents with Balanced
+// Session-centric Scheduling" (arXiv 2607.08565).
+//
+// Steps, each written for obviousness rather than speed:
+//   hash_blocks  block split + chained 64-bit block keys            (Sec. 3.1, App. A; reading SMH64-v1)
+//   index_*      global block index: set of (key, instance) entries  (Sec. 4.1 "kvc"; readings on insert/evict)
+//   match        per-request, per-instance longest matched prefix     (Sec. 4.1 score template: c_i)
+//   route        stick-or-balance rule with SLO checks and Eq. (1)    (Sec. 4.2 pseudocode, parts (a)-(c))
+//
+// Where the paper is silent (hash function, tie-breaks, integer units, batch semantics,
+// eviction order) the choices are the readings recorded with the design notes; each is
+// named at the point of use below.
+//
+// Parity status: the hash constants are pinned to published SplitMix64 output; the
+// hash itself is pinned only by its structural properties (chained prefix identity,
+// closed-form == sequential), since the paper specifies no hash.  Match is pinned by a
+// hash-free brute-force longest-common-prefix model, route by hand-built decision tables
+// and closed forms of Eq. (1), insert/evict by a brute-force dictionary model.
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <tuple>
+#include <unordered_map>
+#include <vector>
+
+namespace {
+
+constexpr int ORC_OK = 0;
+constexpr int ORC_EINVAL = -1;
+constexpr int ORC_EFULL = -2;
+
+constexpr uint64_t KEY_EMPTY = 0;           // reserved: never a key
+constexpr uint64_t KEY_TOMB = ~uint64_t(0);  // reserved: never a key
+constexpr uint32_t SESSION_LIMIT = 1u << 24;
+constexpr uint32_t EPOCH_LIMIT = 1u << 22;
+
+// ---------------------------------------------------------------------------------
+// SplitMix64 (Steele, Lea, Flood, "Fast splittable pseudorandom number generators",
+// OOPSLA 2014): a Weyl-sequence state advanced by the golden-ratio increment, passed
+// through a two-multiply xor-shift finaliser.
+// ---------------------------------------------------------------------------------
+uint64_t splitmix_finalise(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+uint64_t splitmix_next(uint64_t &state) {
+  state += 0x9E3779B97F4A7C15ull;
+  return splitmix_finalise(state);
+}
+
+// Reading SMH64-v1 (the paper fixes only "block granularity" and chained block hashes
+// whose sequence identifies a prefix, Sec. 3.1 and App. A):
+//   constants from SplitMix64 seeded with `seed`:
+//     K_t = low 32 bits of output t (t < B);  M = output B with its low bit set;
+//     s_init = output B+1
+//   d_j   = sum_{k < B/2} (x[2k] + K[2k] mod 2^32) * (x[2k+1] + K[2k+1] mod 2^32)  mod 2^64
+//           (the NH digest of UMAC, Black et al., CRYPTO 1999)
+//   e_j   = F(d_j + j)           F = SplitMix64 finaliser, j = block index in the prompt
+//   s_j   = M * s_{j-1} + e_j    (s_{-1} = s_init)
+//   key_j = F(s_j), with 0 -> 1 and 2^64-1 -> 2^64-2 (both values are reserved markers)
+struct HashConsts {
+  std::vector<uint32_t> K;
+  uint64_t M = 0;
+  uint64_t s_init = 0;
+};
+
+HashConsts make_consts(uint64_t seed, int B) {
+  HashConsts hc;
+  uint64_t st = seed;
+  for (int t = 0; t < B; ++t) hc.K.push_back(uint32_t(splitmix_next(st)));
+  hc.M = splitmix_next(st) | 1ull;
+  hc.s_init = splitmix_next(st);
+  return hc;
+}
+
+uint64_t nh_digest(const int32_t *x, int B, const HashConsts &hc) {
+  uint64_t d = 0;
+  for (int k = 0; k < B / 2; ++k) {
+    uint32_t a = uint32_t(x[2 * k]) + hc.K[2 * k];
+    uint32_t b = uint32_t(x[2 * k + 1]) + hc.K[2 * k + 1];
+    d += uint64_t(a) * uint64_t(b);
+  }
+  return d;
+}
+
+uint64_t remap_key(uint64_t k) {
+  if (k == KEY_EMPTY) return 1;
+  if (k == KEY_TOMB) return KEY_TOMB - 1;
+  return k;
+}
+
+// ---------------------------------------------------------------------------------
+// Global block index. The paper's router consults "kvc" for each instance's local
+// prefix hit (Sec. 4.1) without describing the structure; here it is the plain set of
+// entries (key, instance), each carrying the producing session and the last epoch
+// (batch id) that touched it.
+// ---------------------------------------------------------------------------------
+struct Entry {
+  uint32_t session;
+  uint32_t epoch;
+};
+
+struct Index {
+  uint64_t capacity = 0;
+  int32_t n_inst = 0;
+  uint64_t n = 0;
+  int32_t status = ORC_OK;
+  std::unordered_map<uint64_t, std::map<int32_t, Entry>> m;
+
+  void set_status(int32_t e) {
+    if (status == ORC_OK) status = e;
+  }
+};
+
+// Request r owns keys[blk_off[r] .. blk_off[r+1]); the range must lie in [0, n_blocks].
+bool range_ok(const int64_t *blk_off, int32_t r, int64_t n_blocks) {
+  return blk_off[r] >= 0 && blk_off[r] <= blk_off[r + 1] && blk_off[r + 1] <= n_blocks;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Parameters of the route step, in integer units (nanoseconds of prefill time).
+// Sec. 4.2 (c) load model; Eq. (1); Sec. 4.1 TTFT SLO b + a*L; SLACK and HIT_RATIO as
+// rationals (slack_den == 0 means SLACK = +infinity).
+typedef struct orc_params {
+  int64_t c_lin;   // ns per new token          (c_linear / PREFILL_RATE)
+  int64_t c_att;   // ns per new token^2        (c_attn / PREFILL_RATE)
+  int64_t slo_b;   // ns                         TTFT budget b
+  int64_t slo_a;   // ns per prompt token        TTFT budget a
+  int32_t slack_num, slack_den;
+  int32_t hit_num, hit_den;
+  int32_t block_size;
+} orc_params;
+
+// Block split and chained keys (reading SMH64-v1 above). blk_off_out gets R+1 entries:
+// request r owns keys[blk_off[r] .. blk_off[r+1]); only full blocks are hashed.
+int orc_hash_blocks(const int32_t *tokens, const int64_t *tok_off, int32_t n_req, int32_t B,
+                    uint64_t seed, int64_t *blk_off_out, uint64_t *keys_out) {
+  if (B < 2 || B > 256 || (B & 1) || n_req < 0) return ORC_EINVAL;
+  HashConsts hc = make_consts(seed, B);
+  blk_off_out[0] = 0;
+  for (int32_t r = 0; r < n_req; ++r) {
+    int64_t len = tok_off[r + 1] - tok_off[r];
+    if (len < 0) return ORC_EINVAL;
+    blk_off_out[r + 1] = blk_off_out[r] + len / B;
+  }
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int32_t *x = tokens + tok_off[r];
+    int64_t nb = blk_off_out[r + 1] - blk_off_out[r];
+    uint64_t s = hc.s_init;
+    for (int64_t j = 0; j < nb; ++j) {
+      uint64_t d = nh_digest(x + j * B, B, hc);
+      uint64_t e = splitmix_finalise(d + uint64_t(j));
+      s = hc.M * s + e;
+      keys_out[blk_off_out[r] + j] = remap_key(splitmix_finalise(s));
+    }
+  }
+  return ORC_OK;
+}
+
+// Exposes the constants for the SplitMix64 pins.
+int orc_hash_consts(uint64_t seed, int32_t B, uint32_t *K_out, uint64_t *M_out,
+                    uint64_t *s_init_out) {
+  if (B < 2 || B > 256 || (B & 1)) return ORC_EINVAL;
+  HashConsts hc = make_consts(seed, B);
+  for (int t = 0; t < B; ++t) K_out[t] = hc.K[t];
+  *M_out = hc.M;
+  *s_init_out = hc.s_init;
+  return ORC_OK;
+}
+
+uint64_t orc_splitmix_next(uint64_t *state) { return splitmix_next(*state); }
+
+void *orc_index_new(uint64_t capacity, int32_t n_inst) {
+  if (n_inst < 1 || n_inst > 65536) return nullptr;
+  Index *ix = new Index;
+  ix->capacity = capacity;
+  ix->n_inst = n_inst;
+  return ix;
+}
+
+void orc_index_free(void *h) { delete static_cast<Index *>(h); }
+
+uint64_t orc_index_size(void *h) { return static_cast<Index *>(h)->n; }
+int32_t orc_index_status(void *h) { return static_cast<Index *>(h)->status; }
+
+// Post-route insert: every full block of request r goes on inst[r] (the routed target).
+// Reading: an existing (key, instance) entry keeps its producer session and takes
+// epoch = max(old, epoch); a new one records session[r] -- for pairs repeated inside one
+// batch that is the session of the lowest request index, because requests are applied
+// in order. The call is all-or-nothing: invalid contents (instance out of range,
+// session >= 2^24, a reserved key value, inconsistent offsets) give EINVAL, and a batch
+// whose distinct new entries would push the entry count past the capacity gives EFULL;
+// either way the index is left unchanged and the status word records the first error.
+int orc_index_insert(void *h, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                     int64_t n_blocks, const int32_t *inst, const uint32_t *session,
+                     uint32_t epoch) {
+  Index &ix = *static_cast<Index *>(h);
+  if (n_req < 0 || n_blocks < 0 || epoch >= EPOCH_LIMIT) return ORC_EINVAL;
+  int64_t n_pairs = 0;
+  bool ranges = true;
+  for (int32_t r = 0; r < n_req; ++r) {
+    if (!range_ok(blk_off, r, n_blocks)) ranges = false;
+    else n_pairs += blk_off[r + 1] - blk_off[r];
+  }
+  if (!ranges || n_pairs > n_blocks) {
+    ix.set_status(ORC_EINVAL);
+    return ORC_EINVAL;
+  }
+  for (int32_t r = 0; r < n_req; ++r) {
+    bool bad = inst[r] < 0 || inst[r] >= ix.n_inst || session[r] >= SESSION_LIMIT;
+    for (int64_t b = blk_off[r]; b < blk_off[r + 1] && !bad; ++b)
+      bad = keys[b] == KEY_EMPTY || keys[b] == KEY_TOMB;
+    if (bad && blk_off[r + 1] > blk_off[r]) {
+      ix.set_status(ORC_EINVAL);
+      return ORC_EINVAL;
+    }
+  }
+  // Count distinct (key, instance) pairs that are not yet in the index.
+  std::map<std::pair<uint64_t, int32_t>, bool> fresh;
+  for (int32_t r = 0; r < n_req; ++r)
+    for (int64_t b = blk_off[r]; b < blk_off[r + 1]; ++b) {
+      auto it = ix.m.find(keys[b]);
+      bool present = it != ix.m.end() && it->second.count(inst[r]);
+      if (!present) fresh[{keys[b], inst[r]}] = true;
+    }
+  if (ix.n + fresh.size() > ix.capacity) {
+    ix.set_status(ORC_EFULL);
+    return ORC_EFULL;
+  }
+  for (int32_t r = 0; r < n_req; ++r)
+    for (int64_t b = blk_off[r]; b < blk_off[r + 1]; ++b) {
+      std::map<int32_t, Entry> &holders = ix.m[keys[b]];
+      auto it = holders.find(inst[r]);
+      if (it == holders.end()) {
+        holders[inst[r]] = Entry{session[r], epoch};
+        ix.n += 1;
+      } else {
+        it->second.epoch = std::max(it->second.epoch, epoch);
+      }
+    }
+  return ORC_OK;
+}
+
+// LRU eviction of a fraction f = num/den of the entries. Reading: remove exactly
+// ceil(f * N) entries, the smallest under the total order (epoch, key, instance).
+int orc_index_evict(void *h, uint32_t num, uint32_t den) {
+  Index &ix = *static_cast<Index *>(h);
+  if (den == 0 || num > den) return ORC_EINVAL;
+  uint64_t m = uint64_t((static_cast<unsigned __int128>(ix.n) * num + den - 1) / den);
+  std::vector<std::tuple<uint32_t, uint64_t, int32_t>> all;
+  all.reserve(ix.n);
+  for (auto &kv : ix.m)
+    for (auto &he : kv.second) all.emplace_back(he.second.epoch, kv.first, he.first);
+  std::sort(all.begin(), all.end());
+  for (uint64_t t = 0; t < m && t < all.size(); ++t) {
+    uint64_t key = std::get<1>(all[t]);
+    int32_t i = std::get<2>(all[t]);
+    auto it = ix.m.find(key);
+    it->second.erase(i);
+    if (it->second.empty()) ix.m.erase(it);
+    ix.n -= 1;
+  }
+  return ORC_OK;
+}
+
+// All entries sorted by (key, instance). vals = instance << 48 | epoch << 24 | session.
+uint64_t orc_index_dump(void *h, uint64_t *keys, uint64_t *vals, uint64_t cap) {
+  Index &ix = *static_cast<Index *>(h);
+  std::vector<std::tuple<uint64_t, int32_t, uint32_t, uint32_t>> all;
+  for (auto &kv : ix.m)
+    for (auto &he : kv.second)
+      all.emplace_back(kv.first, he.first, he.second.epoch, he.second.session);
+  std::sort(all.begin(), all.end());
+  for (uint64_t t = 0; t < all.size() && t < cap; ++t) {
+    keys[t] = std::get<0>(all[t]);
+    vals[t] = (uint64_t(std::get<1>(all[t])) << 48) | (uint64_t(std::get<2>(all[t])) << 24) |
+              uint64_t(std::get<3>(all[t]));
+  }
+  return all.size();
+}
+
+// c[r][i] = the number of leading blocks of request r whose keys are all held by
+// instance i: the local prefix hit of the paper's score template (Sec. 4.1), measured
+// at block granularity (Sec. 3.1). The walk follows the prompt block by block and drops
+// an instance at its first missing block ("first miss"), so a block cached without its
+// ancestors never counts.
+int orc_match(void *h, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+              int64_t n_blocks, int32_t *matched) {
+  Index &ix = *static_cast<Index *>(h);
+  if (n_req < 0 || n_blocks < 0) return ORC_EINVAL;
+  const int32_t I = ix.n_inst;
+  int rc = ORC_OK;
+  for (int32_t r = 0; r < n_req; ++r) {
+    int32_t *c = matched + int64_t(r) * I;
+    if (!range_ok(blk_off, r, n_blocks)) {  // a request with a bad range matches nothing
+      for (int32_t i = 0; i < I; ++i) c[i] = 0;
+      ix.set_status(ORC_EINVAL);
+      rc = ORC_EINVAL;
+      continue;
+    }
+    int64_t nb = blk_off[r + 1] - blk_off[r];
+    std::vector<bool> alive(I, true);
+    int32_t n_alive = I;
+    for (int32_t i = 0; i < I; ++i) c[i] = int32_t(nb);
+    for (int64_t j = 0; j < nb && n_alive > 0; ++j) {
+      auto it = ix.m.find(keys[blk_off[r] + j]);
+      for (int32_t i = 0; i < I; ++i) {
+        if (!alive[i]) continue;
+        bool held = it != ix.m.end() && it->second.count(i);
+        if (!held) {
+          alive[i] = false;
+          c[i] = int32_t(j);
+          --n_alive;
+        }
+      }
+    }
+  }
+  return rc;
+}
+
+// Route one batch (Sec. 4.2 pseudocode (a)-(c), Eq. (1)). All requests see the same
+// load snapshot q (reading: batched routing). Integer form, exact in 128-bit:
+//   n_i      = L - B*c[i]                      new tokens on instance i
+//   cost2(n) = 2*C_LIN*n + C_ATT*n*(2L - n)    = 2 * Eq. (1)
+//   est2(i)  = 2*q[i] + cost2(n_i)              = 2 * estimate_load
+//   meets(i) : est2(i)*SLACK_den <= SLACK_num * 2*(b + a*L)   (always true for SLACK = inf)
+//   cached   : B*c[prev] * HIT_den > HIT_num * hist            (strict, as in session_cached)
+//   prev     = argmax c, lowest instance id on ties
+//   balance  = argmin over (est2(i), (i - start) mod I), start = (rr_base + r) mod I
+// branch: 0 first turn, 1 session evicted, 2 stick, 3 last-resort stick (no instance
+// meets the deadline), 4 migrate; 255 = request with out-of-domain inputs (target -1).
+int orc_route(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
+              const int32_t *hist_len, const int32_t *turn, const int64_t *q,
+              const orc_params *p, uint64_t rr_base, int32_t *target, uint8_t *branch) {
+  typedef __int128 i128;
+  const int64_t LIM32 = int64_t(1) << 32;
+  if (n_req < 0 || I < 1 || I > 65536) return ORC_EINVAL;
+  if (p->c_lin < 0 || p->c_lin > LIM32 || p->c_att < 0 || p->c_att > LIM32 || p->slo_b < 0 ||
+      p->slo_b > LIM32 || p->slo_a < 0 || p->slo_a > LIM32 || p->slack_num < 0 ||
+      p->slack_den < 0 || p->hit_num < 0 || p->hit_den <= 0 || p->hit_num >= p->hit_den ||
+      p->block_size < 2 || p->block_size > 256 || (p->block_size & 1))
+    return ORC_EINVAL;
+  const int64_t B = p->block_size;
+  bool q_ok = true;
+  for (int32_t i = 0; i < I; ++i)
+    if (q[i] < 0 || q[i] >= (int64_t(1) << 62)) q_ok = false;
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int32_t *c = matched + int64_t(r) * I;
+    const int64_t L = prompt_len[r];
+    bool ok = q_ok && L >= 0 && L <= (int64_t(1) << 24) && hist_len[r] >= 0 && turn[r] >= 0;
+    for (int32_t i = 0; ok && i < I; ++i) ok = c[i] >= 0 && c[i] <= L / B;
+    if (!ok) {
+      target[r] = -1;
+      branch[r] = 255;
+      continue;
+    }
+    auto est2 = [&](int32_t i) -> i128 {
+      i128 n = L - B * c[i];
+      return i128(2) * q[i] + i128(2) * p->c_lin * n + i128(p->c_att) * n * (i128(2) * L - n);
+    };
+    const i128 bound2 = i128(2) * (i128(p->slo_b) + i128(p->slo_a) * L);
+    auto meets = [&](int32_t i) -> bool {
+      if (p->slack_den == 0) return true;
+      return est2(i) * p->slack_den <= i128(p->slack_num) * bound2;
+    };
+    int32_t prev = 0;
+    for (int32_t i = 1; i < I; ++i)
+      if (c[i] > c[prev]) prev = i;
+    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    int32_t best = start;
+    for (int32_t k = 1; k < I; ++k) {
+      int32_t i = (start + k) % I;
+      if (est2(i) < est2(best)) best = i;  // strict: the earlier rotation position wins ties
+    }
+    const bool none_meets = !meets(best);  // best has the minimum estimated load
+    const bool cached =
+        i128(B) * c[prev] * p->hit_den > i128(p->hit_num) * hist_len[r];
+    if (turn[r] == 0) {
+      target[r] = best;
+      branch[r] = 0;
+    } else if (!cached) {
+      target[r] = best;
+      branch[r] = 1;
+    } else if (meets(prev)) {
+      target[r] = prev;
+      branch[r] = 2;
+    } else if (none_meets) {
+      target[r] = prev;
+      branch[r] = 3;
+    } else {
+      target[r] = best;
+      branch[r] = 4;
+    }
+  }
+  return ORC_OK;
+}
+
+}  // extern "C"
