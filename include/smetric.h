@@ -1,0 +1,254 @@
+/*
+ * smetric.h -- C ABI of libsmetric.so: batched request -> KV-holder matching and routing
+ * for SMetric's balanced session-centric scheduler, on one MI355X (gfx950).
+ *
+ * Paper: "SMetric: Rethink LLM Scheduling for Serving Agents with Balanced
+ * Session-centric Scheduling" (arXiv 2607.08565).  The router scores each instance i by
+ * the request's local KV$ prefix hit c_i and its load (Sec. 4.1, the scoring template),
+ * and SMetric's rule (Sec. 4.2, pseudocode parts (a)-(c), Eq. (1)) sticks a follow-up
+ * request to the instance with the largest hit or balances it by estimated load.  This
+ * library computes, for a batch of prompts:
+ *   smetric_hash_blocks   block split + chained 64-bit block keys       (Sec. 3.1, App. A)
+ *   smetric_match         c[r][i] = longest prefix of request r, in blocks, held by
+ *                         instance i in the global block index           (Sec. 4.1)
+ *   smetric_route         the stick / balance / migrate decision          (Sec. 4.2, Eq. (1))
+ *   smetric_index_insert  post-route insert of every full block on the target
+ *   smetric_index_evict   LRU eviction of a fraction of the entries
+ *
+ * Conventions (all entry points):
+ *  - Pointers are DEVICE pointers owned by the caller unless marked (host).  The library
+ *    never allocates device memory: the index lives in one caller-provided buffer and
+ *    scratch space in a caller-provided workspace whose size a *_bytes call reports.
+ *  - Work is enqueued on `stream` and the call returns before it completes, except where
+ *    a call is marked "synchronizes", which waits for `stream` before returning.
+ *  - Return value: SMETRIC_OK or a negative code.  Errors visible on the host (null
+ *    pointers, out-of-range scalars, short workspace) are returned at once and nothing is
+ *    enqueued.  Errors in device-resident inputs are found by the kernels: they never
+ *    read or write out of bounds, and they record the first such error in the index's
+ *    sticky status word (read it with smetric_index_stats) or in `status` (hash).
+ *  - Not thread-safe per index: calls on one index must be ordered on one stream.
+ *  - Reserved key values: 0 and 2^64-1 never appear as block keys.
+ */
+#ifndef SMETRIC_H
+#define SMETRIC_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  SMETRIC_OK = 0,
+  SMETRIC_EINVAL = -1,     /* bad argument or bad device-resident input           */
+  SMETRIC_EFULL = -2,      /* insert would exceed the index capacity (no change)  */
+  SMETRIC_EHIP = -3,       /* a HIP runtime call failed                           */
+  SMETRIC_EWORKSPACE = -4, /* workspace missing or too small                      */
+  SMETRIC_EINTERNAL = -5   /* an internal bound was hit (should not happen)       */
+};
+
+/* Library version as (major << 16 | minor). */
+int smetric_version(void);
+
+/* ---------------------------------------------------------------------------------
+ * Block split (Sec. 3.1: reuse is measured at KV$-block granularity; App. A: a prompt
+ * is a sequence of block hashes).  Request r's tokens are tokens[tok_off[r] ..
+ * tok_off[r+1]); its blocks are its first floor(len/B) B-token pieces, the trailing
+ * partial block is never hashed.
+ *
+ * smetric_block_offsets (host only, no GPU work): tok_off (host, int64[n_req+1]) ->
+ * blk_off (host, int64[n_req+1], blk_off[0] = 0, exclusive prefix sum of floor(len/B)),
+ * *n_blocks (host) = blk_off[n_req].  EINVAL if a length is negative or B is not an even
+ * number in [2, 256].
+ * --------------------------------------------------------------------------------- */
+int smetric_block_offsets(const int64_t *tok_off, int32_t n_req, int32_t block_size,
+                          int64_t *blk_off, int64_t *n_blocks);
+
+/* Chained 64-bit block keys (the paper fixes only that a prompt is identified by its
+ * chained block hashes; the function is the SMH64-v1 reading):
+ *   constants from SplitMix64 (Steele, Lea, Flood, OOPSLA 2014) seeded with `seed`:
+ *     K_t = low 32 bits of output t for t < B, M = output B with its low bit set,
+ *     s_init = output B+1;
+ *   d_j   = sum_{k<B/2} (x[2k]+K[2k] mod 2^32) * (x[2k+1]+K[2k+1] mod 2^32) mod 2^64
+ *           (the NH digest of UMAC), x = the block's tokens as uint32;
+ *   e_j   = F(d_j + j), F = the SplitMix64 finaliser, j = block index in the request;
+ *   s_j   = M * s_{j-1} + e_j mod 2^64, s_{-1} = s_init;
+ *   key_j = F(s_j), then 0 -> 1 and 2^64-1 -> 2^64-2.
+ * key_j depends on exactly the first (j+1)*B tokens, so equal key sequences mean equal
+ * prompt prefixes (up to 64-bit collisions).
+ *
+ *   tokens   int32[n_tokens]          token IDs (any values; used as uint32 bit patterns)
+ *   tok_off  int64[n_req+1]           request r = tokens[tok_off[r] .. tok_off[r+1])
+ *   blk_off  int64[n_req+1]           output range of request r in keys; must satisfy
+ *                                     blk_off[r+1]-blk_off[r] = floor(len_r / B)
+ *                                     (smetric_block_offsets computes it)
+ *   keys     uint64[n_blocks] (out)   keys[blk_off[r] + j] = key_j of request r
+ *   status   int32[1] or NULL         set to SMETRIC_EINVAL (if it is still 0) when a
+ *                                     request's offsets are inconsistent or out of range;
+ *                                     that request's keys are not written.  The caller
+ *                                     clears it.
+ * Host errors: EINVAL for n_req < 0, n_tokens < 0, n_blocks < 0, bad block_size, or a
+ * null pointer with n_req > 0.
+ */
+int smetric_hash_blocks(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_off,
+                        const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
+                        int32_t block_size, uint64_t seed, uint64_t *keys, int32_t *status,
+                        hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Global block index: the router's view of every instance's local KV$ (the paper's
+ * "kvc", Sec. 4.1, which the router "already knows"; its structure is not described).
+ * Semantically a set of entries (key, instance), each with the producing session
+ * (24 bits) and the epoch (22 bits) of its last insert.  Physically: an open-addressing
+ * table in HBM of 128-byte buckets (8 keys, then 8 values) with linear bucket probing;
+ * keys held by more than a threshold of instances keep a holder bitmap in a side pool.
+ * --------------------------------------------------------------------------------- */
+typedef struct smetric_index {
+  /* set by smetric_index_init / smetric_index_attach; treat as read-only */
+  void *mem;               /* caller's device buffer holding the whole index        */
+  uint64_t mem_bytes;
+  uint64_t capacity;       /* maximum number of live entries                        */
+  int32_t n_instances;     /* instances are 0 .. n_instances-1, n_instances <= 65536 */
+  int32_t bitmap_words;    /* ceil(n_instances / 64)                                */
+  int32_t spill_threshold; /* keys with more holders use a bitmap record             */
+  int32_t reserved0;
+  uint64_t n_buckets;
+  uint64_t n_records;      /* bitmap records in the side pool                       */
+  uint64_t *slots;         /* n_buckets * 16 words                                  */
+  uint64_t *pool;          /* n_records * bitmap_words words                        */
+  void *hdr;               /* device counters: entry count, status, pool use        */
+} smetric_index;
+
+/* Device bytes needed for an index of `capacity` entries over `n_instances` instances.
+ * EINVAL if capacity == 0 or n_instances is not in [1, 65536]. */
+int smetric_index_bytes(uint64_t capacity, int32_t n_instances, uint64_t *bytes /* host */);
+
+/* Lays the index out in `mem` (>= smetric_index_bytes) and clears it on `stream`.
+ * `idx` (host) is filled in.  EINVAL on bad sizes, EHIP if the clear cannot launch. */
+int smetric_index_init(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
+                       int32_t n_instances, hipStream_t stream);
+
+/* Like init but leaves the buffer's contents alone: re-attaches an index whose bytes
+ * were copied from another buffer laid out with the same capacity and n_instances
+ * (a snapshot / restore of the whole index is a plain copy of mem_bytes). */
+int smetric_index_attach(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
+                         int32_t n_instances);
+
+/* Entry count and sticky status (0 or the first device-detected error).  Synchronizes.
+ * Pass reset_status != 0 to clear the status afterwards. */
+int smetric_index_stats(const smetric_index *idx, uint64_t *n_entries /* host */,
+                        int32_t *status /* host */, int32_t reset_status, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Match: c[r][i] = the largest m such that instance i holds the keys of blocks 0..m-1 of
+ * request r -- the request's local prefix hit on instance i, in blocks (Sec. 4.1: c_i is
+ * the prefix hit length of the prompt in instance i's local KV$; Sec. 3.1: measured at
+ * block granularity).  An instance drops out at its first missing block, so a cached
+ * block whose ancestors are gone does not count.
+ *
+ *   keys     uint64[n_blocks]          from smetric_hash_blocks
+ *   blk_off  int64[n_req+1]            request r's keys are keys[blk_off[r] .. blk_off[r+1])
+ *   matched  int32[n_req * n_instances] (out), row-major: matched[r * n_instances + i]
+ * A request whose range is decreasing or leaves [0, n_blocks] gets an all-zero row and
+ * sets status EINVAL.  Reads the index; writes only `matched` and the status word.
+ */
+int smetric_match(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
+                  int32_t n_req, int64_t n_blocks, int32_t *matched, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Route (Sec. 4.2 pseudocode (a) routing, (b) SLO checks, (c) load model; Eq. (1)).
+ * All requests of the batch see the same load snapshot q.  Exact integer arithmetic in
+ * nanoseconds of prefill time (PREFILL_RATE folded into the coefficients):
+ *   n_i      = L - B*c[i]                                   new tokens on instance i
+ *   est2(i)  = 2*q[i] + 2*c_lin*n_i + c_att*n_i*(2L - n_i)  = 2 * estimate_load
+ *   meets(i) : est2(i) * slack_den <= slack_num * 2*(slo_b + slo_a*L)
+ *              (always true when slack_den == 0, i.e. SLACK = +inf)
+ *   prev     = argmax_i c[i], lowest instance on ties
+ *   cached   : B*c[prev] * hit_den > hit_num * hist         (session_cached, strict)
+ *   balance  = argmin over (est2(i), (i - start) mod I), start = (rr_base + r) mod I
+ *              (the round-robin tie-break of rr_argmin)
+ *   turn == 0                    -> balance, branch 0 (first turn)
+ *   !cached                      -> balance, branch 1 (session evicted from local tier)
+ *   meets(prev)                  -> prev,    branch 2 (stick)
+ *   no instance meets            -> prev,    branch 3 (last-resort stick)
+ *   otherwise                    -> balance, branch 4 (SLO migration)
+ *
+ *   matched   int32[n_req * n_instances]   from smetric_match
+ *   prompt_len, hist_len, turn  int32[n_req]  L, est_hit in tokens (the previous prompt's
+ *                                             length), turn (0 = first)
+ *   q         int64[n_instances]           queued prefill per instance, ns
+ *   params    (host)                       see smetric_params
+ *   target    int32[n_req] (out), branch uint8[n_req] (out)
+ * A request with inputs outside the domain (L < 0 or L > 2^24, hist < 0, turn < 0, some
+ * c[i] < 0 or > L/B, some q[i] < 0 or >= 2^62) gets target -1, branch 255.
+ * Host errors: EINVAL for n_req < 0, n_instances outside [1, 65536], parameters outside
+ * their documented ranges.
+ * --------------------------------------------------------------------------------- */
+typedef struct smetric_params {
+  int64_t c_lin;      /* ns per new token,  in [0, 2^32]  (c_linear / PREFILL_RATE) */
+  int64_t c_att;      /* ns per token^2,    in [0, 2^32]  (c_attn / PREFILL_RATE)   */
+  int64_t slo_b;      /* TTFT budget b, ns, in [0, 2^32]                            */
+  int64_t slo_a;      /* TTFT budget a, ns per prompt token, in [0, 2^32]           */
+  int32_t slack_num;  /* SLACK = slack_num / slack_den, both >= 0; den 0 = +inf     */
+  int32_t slack_den;
+  int32_t hit_num;    /* HIT_RATIO = hit_num / hit_den, 0 <= num < den              */
+  int32_t hit_den;
+  int32_t block_size; /* B, even, in [2, 256]                                       */
+} smetric_params;
+
+enum { SMETRIC_FIRST_TURN = 0, SMETRIC_EVICTED = 1, SMETRIC_STICK = 2, SMETRIC_LAST_RESORT = 3,
+       SMETRIC_MIGRATE = 4, SMETRIC_INVALID = 255 };
+
+int smetric_route(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                  const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                  const int64_t *q, const smetric_params *params /* host */, uint64_t rr_base,
+                  int32_t *target, uint8_t *branch, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Post-route insert: every full block of request r goes on instance[r] (the routed
+ * target caches the whole prompt it prefills, Sec. 2 and 4.2).  An existing (key,
+ * instance) entry keeps its session and takes epoch = max(old, epoch); a new entry
+ * records session[r], and a pair repeated within the batch takes the session of the
+ * lowest request index.  All-or-nothing: a bad device-resident input (a request range
+ * outside [0, n_blocks], total pairs > n_blocks, instance outside [0, n_instances),
+ * session >= 2^24, a reserved key) sets status EINVAL, and a batch whose distinct new
+ * entries would exceed the capacity sets status EFULL; either way the index is
+ * unchanged.
+ *
+ *   keys, blk_off     as for smetric_match (request ranges must not overlap)
+ *   instance          int32[n_req]     target instance per request
+ *   session           uint32[n_req]    producing session per request, < 2^24
+ *   epoch             host, < 2^22     batch id / recency stamp
+ *   workspace         >= smetric_index_insert_ws_bytes(n_blocks) bytes, 256-B aligned
+ * Host errors: EINVAL (bad scalars), EWORKSPACE (workspace too small).
+ * --------------------------------------------------------------------------------- */
+int smetric_index_insert_ws_bytes(int64_t n_blocks, uint64_t *ws_bytes /* host */);
+int smetric_index_insert(smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
+                         int32_t n_req, int64_t n_blocks, const int32_t *instance,
+                         const uint32_t *session, uint32_t epoch, void *workspace,
+                         uint64_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * LRU eviction of a fraction frac_num/frac_den of the entries (the paper's local tier
+ * evicts; its policy is not specified): removes exactly ceil(N * num / den) entries, the
+ * smallest under the total order (epoch, key, instance), then rebuilds the table.
+ * Synchronizes.  EINVAL if frac_den == 0 or frac_num > frac_den.
+ * Dump: all entries sorted by (key, instance) into keys_out / vals_out (device,
+ * `cap` each), vals = instance << 48 | epoch << 24 | session; *n_out (host) = entry
+ * count (entries beyond cap are not written).  Synchronizes.
+ * Both take a workspace of >= smetric_index_evict_ws_bytes(idx) bytes.
+ * --------------------------------------------------------------------------------- */
+int smetric_index_evict_ws_bytes(const smetric_index *idx, uint64_t *ws_bytes /* host */);
+int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32_t frac_den,
+                        void *workspace, uint64_t ws_bytes, hipStream_t stream);
+int smetric_index_dump(const smetric_index *idx, uint64_t *keys_out, uint64_t *vals_out,
+                       uint64_t cap, void *workspace, uint64_t ws_bytes,
+                       uint64_t *n_out /* host */, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SMETRIC_H */

@@ -1,0 +1,103 @@
+// Internal definitions shared by the libsmetric kernels: index layout in HBM, entry
+// value packing, bucket hashing, and small wavefront helpers.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "smetric.h"
+
+namespace smk {
+
+constexpr uint64_t KEY_EMPTY = 0;
+constexpr uint64_t KEY_TOMB = ~uint64_t(0);
+constexpr int SLOTS = 8;                 // slots per 128-byte bucket: 8 keys then 8 values
+constexpr int BUCKET_WORDS = 2 * SLOTS;  // u64 words per bucket
+constexpr uint32_t SESSION_LIMIT = 1u << 24;
+constexpr uint32_t EPOCH_LIMIT = 1u << 22;
+
+// Entry value (64 bits): instance:16 | kind:2 | epoch:22 | session:24.
+// HEADER values hold a pool record index in the low 46 bits instead.
+enum Kind : uint32_t { PLAIN = 0, HEADER = 1, MEMBER = 2 };
+
+__host__ __device__ inline uint64_t make_val(uint32_t inst, uint32_t kind, uint32_t epoch,
+                                             uint32_t session) {
+  return (uint64_t(inst) << 48) | (uint64_t(kind) << 46) | (uint64_t(epoch) << 24) |
+         uint64_t(session);
+}
+__host__ __device__ inline uint32_t val_inst(uint64_t v) { return uint32_t(v >> 48); }
+__host__ __device__ inline uint32_t val_kind(uint64_t v) { return uint32_t(v >> 46) & 3u; }
+__host__ __device__ inline uint32_t val_epoch(uint64_t v) { return uint32_t(v >> 24) & 0x3FFFFFu; }
+__host__ __device__ inline uint64_t val_rec(uint64_t v) { return v & ((uint64_t(1) << 46) - 1); }
+__host__ __device__ inline uint64_t header_val(uint64_t rec) { return (uint64_t(HEADER) << 46) | rec; }
+// value with the kind bits cleared: the dump layout inst << 48 | epoch << 24 | session
+__host__ __device__ inline uint64_t val_plain(uint64_t v) { return v & ~(uint64_t(3) << 46); }
+
+// Device-resident counters, first 256 bytes of the index buffer.
+struct IndexHdr {
+  unsigned long long n_entries;
+  int status;
+  unsigned int pad0;
+  unsigned long long rec_used;  // bitmap records handed out (may exceed n_records: exhausted)
+  unsigned long long pad[29];
+};
+static_assert(sizeof(IndexHdr) == 256, "header size");
+
+// Index view passed by value to kernels.
+struct DevIndex {
+  uint64_t *slots;
+  uint64_t n_buckets;
+  uint64_t *pool;
+  uint64_t n_records;
+  IndexHdr *hdr;
+  uint64_t capacity;
+  int32_t n_inst;
+  int32_t words;      // bitmap words per record
+  int32_t threshold;  // spill threshold T
+};
+
+inline DevIndex dev_view(const smetric_index *ix) {
+  DevIndex d;
+  d.slots = ix->slots;
+  d.n_buckets = ix->n_buckets;
+  d.pool = ix->pool;
+  d.n_records = ix->n_records;
+  d.hdr = static_cast<IndexHdr *>(ix->hdr);
+  d.capacity = ix->capacity;
+  d.n_inst = ix->n_instances;
+  d.words = ix->bitmap_words;
+  d.threshold = ix->spill_threshold;
+  return d;
+}
+
+// Bucket of a key: a multiplicative mix of the key mapped onto [0, n_buckets) with a
+// 64x64 high product (keys from the hash are already uniform; the mix protects against
+// structured caller keys).
+__host__ __device__ inline uint64_t mix64(uint64_t k) {
+  k ^= k >> 32;
+  k *= 0xD6E8FEB86659FD93ull;
+  k ^= k >> 32;
+  return k;
+}
+__device__ inline uint64_t home_bucket(uint64_t key, uint64_t n_buckets) {
+  return __umul64hi(mix64(key), n_buckets);
+}
+// Bucket chain for a member entry (key, inst) of a key that uses a bitmap record.
+__device__ inline uint64_t member_bucket(uint64_t key, uint32_t inst, uint64_t n_buckets) {
+  return __umul64hi(mix64(key ^ ((uint64_t(inst) + 1) * 0x9E3779B97F4A7C15ull)), n_buckets);
+}
+
+__device__ inline void set_status(IndexHdr *h, int err) {
+  atomicCAS(&h->status, 0, err);
+}
+
+// Sizing shared by host code.
+inline int32_t bitmap_words_for(int32_t n_inst) { return (n_inst + 63) / 64; }
+inline int32_t threshold_for(int32_t n_inst) {
+  int32_t t = (n_inst + 127) / 128;
+  return t < 8 ? 8 : t;
+}
+
+inline int hip_rc(hipError_t e) { return e == hipSuccess ? SMETRIC_OK : SMETRIC_EHIP; }
+
+}  // namespace smk

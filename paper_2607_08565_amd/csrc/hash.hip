@@ -1,0 +1,238 @@
+// Block split + chained 64-bit block keys (K1).
+//
+// Paper: a prompt is identified at KV$-block granularity by its chained block hashes
+// (Sec. 3.1; App. A).  The function is the SMH64-v1 reading stated in smetric.h:
+// SplitMix64 constants, the NH digest of each block, a position salt, an affine chain
+// s_j = M s_{j-1} + e_j and a finalised key.
+//
+// Mapping to gfx950: one 64-lane wavefront per request walks it in tiles of 64 blocks.
+//  * B = 16 (the fast path): tokens are read as 16-byte vectors, lane l of load u taking
+//    tokens [256u + 4l, 256u + 4l + 4) of the tile, so every load instruction covers 1 KB
+//    of contiguous HBM.  Four lanes share a block; each forms the NH products of its two
+//    token pairs and a quad reduction (DPP quad permutes) yields the block digest.
+//  * other even B: lane l digests block l of the tile sequentially.
+//  Digests go through LDS so that lane l then owns block l of the tile; the chain is an
+//  inclusive scan of affine maps x -> M x + e_l across the wavefront (Kogge-Stone with
+//  the uniform multipliers M^1..M^32), seeded with the carry from the previous tile.
+//  Because the chain is affine, this scan equals the sequential definition exactly.
+#include "common.h"
+
+namespace smk {
+namespace {
+
+constexpr uint64_t GOLDEN = 0x9E3779B97F4A7C15ull;
+
+__device__ __forceinline__ uint64_t finalise(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+// Output t (0-based) of the SplitMix64 stream seeded with `seed`: the Weyl state after
+// t+1 steps is seed + (t+1) * golden, so outputs can be formed independently.
+__device__ __forceinline__ uint64_t splitmix_out(uint64_t seed, uint64_t t) {
+  return finalise(seed + (t + 1) * GOLDEN);
+}
+
+__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int d) {
+  int lo = __shfl_up(int(uint32_t(v)), d, 64);
+  int hi = __shfl_up(int(uint32_t(v >> 32)), d, 64);
+  return (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo);
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  int lo = __builtin_amdgcn_mov_dpp(int(uint32_t(v)), CTRL, 0xF, 0xF, false);
+  int hi = __builtin_amdgcn_mov_dpp(int(uint32_t(v >> 32)), CTRL, 0xF, 0xF, false);
+  return (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo);
+}
+
+__device__ __forceinline__ uint64_t remap(uint64_t k) {
+  if (k == KEY_EMPTY) return 1;
+  if (k == KEY_TOMB) return KEY_TOMB - 1;
+  return k;
+}
+
+struct ChainConsts {
+  uint64_t M;
+  uint64_t s_init;
+  uint64_t Mpow[6];  // M^1, M^2, M^4, ..., M^32
+  uint64_t Mlane;    // M^(lane+1)
+};
+
+__device__ ChainConsts chain_consts(uint64_t seed, int B) {
+  ChainConsts c;
+  c.M = splitmix_out(seed, B) | 1ull;
+  c.s_init = splitmix_out(seed, B + 1);
+  uint64_t p = c.M;
+  for (int k = 0; k < 6; ++k) {
+    c.Mpow[k] = p;
+    p *= p;
+  }
+  // M^(lane+1) by binary exponentiation
+  uint32_t e = (threadIdx.x & 63) + 1;
+  uint64_t r = 1, b = c.M;
+  while (e) {
+    if (e & 1) r *= b;
+    b *= b;
+    e >>= 1;
+  }
+  c.Mlane = r;
+  return c;
+}
+
+// Given lane l's block digest for block j = j0 + l (valid when l < n_valid), finish the
+// tile: salt, chain scan from `carry`, finalise, store.  Returns the chain state after
+// the tile's last block (meaningful when the tile is full).
+__device__ __forceinline__ uint64_t finish_tile(uint64_t d, int64_t j0, int n_valid, uint64_t carry,
+                                                const ChainConsts &cc, uint64_t *out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t j = j0 + lane;
+  uint64_t v = lane < n_valid ? finalise(d + uint64_t(j)) : 0;
+#pragma unroll
+  for (int k = 0; k < 6; ++k) {
+    const int dist = 1 << k;
+    uint64_t t = shfl_up64(v, dist);
+    if (lane >= dist) v += cc.Mpow[k] * t;
+  }
+  const uint64_t s = cc.Mlane * carry + v;  // s_j = M^(l+1) carry + sum_k M^(l-k) e_k
+  if (lane < n_valid) out[lane] = remap(finalise(s));
+  return uint64_t(__shfl(int64_t(s), 63, 64));
+}
+
+__device__ __forceinline__ bool request_ok(const int64_t *tok_off, const int64_t *blk_off, int r,
+                                           int64_t n_tokens, int64_t n_blocks, int B, int64_t &t0,
+                                           int64_t &b0, int64_t &nb) {
+  t0 = tok_off[r];
+  const int64_t t1 = tok_off[r + 1];
+  b0 = blk_off[r];
+  const int64_t b1 = blk_off[r + 1];
+  nb = b1 - b0;
+  return t0 >= 0 && t0 <= t1 && t1 <= n_tokens && b0 >= 0 && b0 <= b1 && b1 <= n_blocks &&
+         nb == (t1 - t0) / B;
+}
+
+constexpr int WAVES = 4;
+
+// B = 16 fast path.
+__global__ __launch_bounds__(64 * WAVES) void hash16_kernel(const int32_t *__restrict__ tokens,
+                                                            int64_t n_tokens,
+                                                            const int64_t *__restrict__ tok_off,
+                                                            const int64_t *__restrict__ blk_off,
+                                                            int32_t n_req, int64_t n_blocks,
+                                                            uint64_t seed,
+                                                            uint64_t *__restrict__ keys,
+                                                            int32_t *status) {
+  __shared__ uint64_t dig[WAVES][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * WAVES + wave;
+  if (r >= n_req) return;
+  int64_t t0, b0, nb;
+  if (!request_ok(tok_off, blk_off, r, n_tokens, n_blocks, 16, t0, b0, nb)) {
+    if (lane == 0 && status) atomicCAS(status, 0, SMETRIC_EINVAL);
+    return;
+  }
+  const ChainConsts cc = chain_consts(seed, 16);
+  // this lane's four offset constants: K[4q .. 4q+3], q = lane % 4
+  const int q = lane & 3;
+  const uint32_t k0 = uint32_t(splitmix_out(seed, 4 * q + 0));
+  const uint32_t k1 = uint32_t(splitmix_out(seed, 4 * q + 1));
+  const uint32_t k2 = uint32_t(splitmix_out(seed, 4 * q + 2));
+  const uint32_t k3 = uint32_t(splitmix_out(seed, 4 * q + 3));
+  const int32_t *x = tokens + t0;
+  uint64_t carry = cc.s_init;
+  for (int64_t j0 = 0; j0 < nb; j0 += 64) {
+    const int n_valid = int(nb - j0 < 64 ? nb - j0 : 64);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int blk = 16 * u + (lane >> 2);  // block within the tile
+      uint64_t part = 0;
+      if (blk < n_valid) {
+        int4 v;
+        __builtin_memcpy(&v, x + (j0 + blk) * 16 + 4 * q, 16);
+        part = uint64_t(uint32_t(v.x) + k0) * uint64_t(uint32_t(v.y) + k1) +
+               uint64_t(uint32_t(v.z) + k2) * uint64_t(uint32_t(v.w) + k3);
+      }
+      part += dpp64<0xB1>(part);  // quad_perm [1,0,3,2]
+      part += dpp64<0x4E>(part);  // quad_perm [2,3,0,1]
+      if (q == 0) dig[wave][blk] = part;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    const uint64_t d = dig[wave][lane];
+    carry = finish_tile(d, j0, n_valid, carry, cc, keys + b0 + j0);
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// Any even B in [2, 256].
+__global__ __launch_bounds__(64 * WAVES) void hash_generic_kernel(
+    const int32_t *__restrict__ tokens, int64_t n_tokens, const int64_t *__restrict__ tok_off,
+    const int64_t *__restrict__ blk_off, int32_t n_req, int64_t n_blocks, int B, uint64_t seed,
+    uint64_t *__restrict__ keys, int32_t *status) {
+  __shared__ uint32_t K[256];
+  for (int t = threadIdx.x; t < B; t += blockDim.x) K[t] = uint32_t(splitmix_out(seed, t));
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * WAVES + wave;
+  if (r >= n_req) return;
+  int64_t t0, b0, nb;
+  if (!request_ok(tok_off, blk_off, r, n_tokens, n_blocks, B, t0, b0, nb)) {
+    if (lane == 0 && status) atomicCAS(status, 0, SMETRIC_EINVAL);
+    return;
+  }
+  const ChainConsts cc = chain_consts(seed, B);
+  const int32_t *x = tokens + t0;
+  uint64_t carry = cc.s_init;
+  for (int64_t j0 = 0; j0 < nb; j0 += 64) {
+    const int n_valid = int(nb - j0 < 64 ? nb - j0 : 64);
+    uint64_t d = 0;
+    if (lane < n_valid) {
+      const int32_t *b = x + (j0 + lane) * B;
+      for (int k = 0; k < B / 2; ++k)
+        d += uint64_t(uint32_t(b[2 * k]) + K[2 * k]) * uint64_t(uint32_t(b[2 * k + 1]) + K[2 * k + 1]);
+    }
+    carry = finish_tile(d, j0, n_valid, carry, cc, keys + b0 + j0);
+  }
+}
+
+}  // namespace
+}  // namespace smk
+
+using namespace smk;
+
+extern "C" int smetric_hash_blocks(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_off,
+                                   const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
+                                   int32_t block_size, uint64_t seed, uint64_t *keys,
+                                   int32_t *status, hipStream_t stream) {
+  if (n_req < 0 || n_tokens < 0 || n_blocks < 0 || block_size < 2 || block_size > 256 ||
+      (block_size & 1))
+    return SMETRIC_EINVAL;
+  if (n_req == 0) return SMETRIC_OK;
+  if (!tok_off || !blk_off || (n_tokens > 0 && !tokens) || (n_blocks > 0 && !keys))
+    return SMETRIC_EINVAL;
+  const dim3 grid((n_req + WAVES - 1) / WAVES), block(64 * WAVES);
+  if (block_size == 16)
+    hipLaunchKernelGGL(hash16_kernel, grid, block, 0, stream, tokens, n_tokens, tok_off, blk_off,
+                       n_req, n_blocks, seed, keys, status);
+  else
+    hipLaunchKernelGGL(hash_generic_kernel, grid, block, 0, stream, tokens, n_tokens, tok_off,
+                       blk_off, n_req, n_blocks, int(block_size), seed, keys, status);
+  return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_block_offsets(const int64_t *tok_off, int32_t n_req, int32_t block_size,
+                                     int64_t *blk_off, int64_t *n_blocks) {
+  if (n_req < 0 || block_size < 2 || block_size > 256 || (block_size & 1) || !tok_off ||
+      !blk_off || !n_blocks)
+    return SMETRIC_EINVAL;
+  blk_off[0] = 0;
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int64_t len = tok_off[r + 1] - tok_off[r];
+    if (len < 0) return SMETRIC_EINVAL;
+    blk_off[r + 1] = blk_off[r] + len / block_size;
+  }
+  *n_blocks = blk_off[n_req];
+  return SMETRIC_OK;
+}
+
+extern "C" int smetric_version(void) { return (0 << 16) | 1; }

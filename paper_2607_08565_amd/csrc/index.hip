@@ -1,0 +1,709 @@
+// Global block index in HBM: layout, insert (K2 + K7), evict (K6), dump, stats.
+//
+// Paper: the router consults each instance's local KV$ contents ("kvc", Sec. 4.1) to get
+// the prefix hit c_i; the structure is not described.  The index here is the set of
+// entries (key, instance) with the producing session and the last epoch; after a batch
+// is routed every full block of each prompt is entered on its target (the target's
+// prefill caches the prompt, Sec. 2 and 4.2), and a fraction of the oldest entries can be
+// evicted (local tiers evict, Sec. 2 and 4.2 "session_cached").
+//
+// Layout of the caller's buffer:
+//   [0, 256)                 IndexHdr: entry count, sticky status, pool use
+//   slots                    n_buckets x 128 B: keys[8] then values[8]
+//   pool                     n_records x bitmap_words x 8 B: holder bitmaps
+// A key normally owns one PLAIN slot per holder in its home chain (linear probing over
+// buckets from home_bucket(key)).  When a key gains more than T holders its plain slots
+// are replaced by one HEADER slot pointing at a bitmap record, and every holder becomes a
+// MEMBER slot found from member_bucket(key, inst); probes of the key then read one
+// bucket line plus the bitmap instead of walking T+ slots.  If the pool runs out, keys
+// simply stay plain.  Slots are only ever claimed (EMPTY -> key by compare-and-swap) or
+// turned into tombstones, so every slot of a key lies before the first EMPTY slot of its
+// chain; eviction rebuilds the table from the surviving entries.
+//
+// Insert pipeline (no sort, no host synchronisation):
+//   clear      scratch dedupe table
+//   probe      per pair (r, j): validate; find (key, target) -> refresh position, or
+//              enter the pair in the dedupe table keyed by (key, instance), keeping the
+//              lowest request index (atomic min), and list each distinct new pair once
+//   check      one thread: first error -> EINVAL/EFULL, nothing changes; else count
+//   refresh    epoch = max(old, epoch) for existing entries
+//   place      each distinct new pair claims a slot; the thread whose slot becomes the
+//              key's (T+1)-th plain slot -- unique, since claims fill a chain in order --
+//              queues the key for conversion
+//   spill      queued keys get a bitmap record, member slots, a header and tombstones
+#include <hipcub/hipcub.hpp>
+
+#include "common.h"
+
+namespace smk {
+namespace {
+
+constexpr int TB = 256;
+constexpr int MAX_GRID = 4096;
+
+inline uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+inline int grid_for(uint64_t n) {
+  const uint64_t g = (n + TB - 1) / TB;
+  return int(g < 1 ? 1 : (g > MAX_GRID ? MAX_GRID : g));
+}
+
+__global__ void fill_kernel(uint64_t *p, uint64_t n_words, uint64_t value) {
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_words; i += stride) p[i] = value;
+}
+
+__global__ void set_int_kernel(int *p, int v) { *p = v; }
+
+int fill(void *p, uint64_t bytes, uint64_t value, hipStream_t s) {
+  const uint64_t n = bytes / 8;
+  if (n == 0) return SMETRIC_OK;
+  hipLaunchKernelGGL(fill_kernel, dim3(grid_for(n)), dim3(TB), 0, s, static_cast<uint64_t *>(p), n, value);
+  return hip_rc(hipGetLastError());
+}
+
+struct Layout {
+  int32_t words, threshold;
+  uint64_t n_records, n_buckets, slots_off, pool_off, bytes;
+};
+
+bool layout_for(uint64_t capacity, int32_t n_inst, Layout &L) {
+  if (capacity == 0 || capacity > (uint64_t(1) << 40) || n_inst < 1 || n_inst > 65536) return false;
+  L.words = bitmap_words_for(n_inst);
+  L.threshold = threshold_for(n_inst);
+  uint64_t rec = capacity / 256;
+  if (rec < 64) rec = 64;
+  const uint64_t rec_max = capacity / uint64_t(L.threshold + 1) + 1;
+  if (rec > rec_max) rec = rec_max;
+  L.n_records = rec;
+  // slots: live entries plus headers/tombstones of converted keys, at <= 3/4 occupancy
+  const uint64_t slots = capacity + uint64_t(L.threshold) * rec;
+  L.n_buckets = (slots * 4 / 3 + SLOTS - 1) / SLOTS + 1;
+  L.slots_off = sizeof(IndexHdr);
+  L.pool_off = L.slots_off + L.n_buckets * BUCKET_WORDS * 8;
+  L.bytes = round_up(L.pool_off + L.n_records * uint64_t(L.words) * 8, 256);
+  return true;
+}
+
+int attach(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity, int32_t n_inst) {
+  Layout L;
+  if (!idx || !mem || !layout_for(capacity, n_inst, L) || mem_bytes < L.bytes ||
+      (reinterpret_cast<uintptr_t>(mem) & 255))
+    return SMETRIC_EINVAL;
+  char *base = static_cast<char *>(mem);
+  idx->mem = mem;
+  idx->mem_bytes = mem_bytes;
+  idx->capacity = capacity;
+  idx->n_instances = n_inst;
+  idx->bitmap_words = L.words;
+  idx->spill_threshold = L.threshold;
+  idx->reserved0 = 0;
+  idx->n_buckets = L.n_buckets;
+  idx->n_records = L.n_records;
+  idx->slots = reinterpret_cast<uint64_t *>(base + L.slots_off);
+  idx->pool = reinterpret_cast<uint64_t *>(base + L.pool_off);
+  idx->hdr = base;
+  return SMETRIC_OK;
+}
+
+// ---------------------------------------------------------------------------------
+// Table primitives
+// ---------------------------------------------------------------------------------
+struct Found {
+  int64_t slot;  // bucket * SLOTS + s, or -1
+  uint64_t val;
+};
+
+// Find the entry (key, inst), looking through a bitmap record when the key has one.
+__device__ Found find_entry(const DevIndex &ix, uint64_t key, uint32_t inst) {
+  uint64_t b = home_bucket(key, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    for (int s = 0; s < SLOTS; ++s) {
+      const uint64_t k = bk[s];
+      if (k == KEY_EMPTY) return Found{-1, 0};
+      if (k != key) continue;
+      const uint64_t v = bk[SLOTS + s];
+      const uint32_t kind = val_kind(v);
+      if (kind == PLAIN && val_inst(v) == inst) return Found{int64_t(b * SLOTS + s), v};
+      if (kind == HEADER) {
+        const uint64_t w = ix.pool[val_rec(v) * uint64_t(ix.words) + (inst >> 6)];
+        if (!((w >> (inst & 63)) & 1)) return Found{-1, 0};
+        uint64_t m = member_bucket(key, inst, ix.n_buckets);
+        for (uint64_t st2 = 0; st2 < ix.n_buckets; ++st2) {
+          const uint64_t *mk = ix.slots + m * BUCKET_WORDS;
+          for (int t = 0; t < SLOTS; ++t) {
+            const uint64_t k2 = mk[t];
+            if (k2 == KEY_EMPTY) return Found{-1, 0};
+            if (k2 != key) continue;
+            const uint64_t v2 = mk[SLOTS + t];
+            if (val_kind(v2) == MEMBER && val_inst(v2) == inst) return Found{int64_t(m * SLOTS + t), v2};
+          }
+          m = (m + 1 == ix.n_buckets) ? 0 : m + 1;
+        }
+        return Found{-1, 0};
+      }
+    }
+    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+  }
+  return Found{-1, 0};
+}
+
+// Claim the first EMPTY slot of the chain starting at bucket b.  `same` counts slots
+// holding `key` seen before the claimed one.  Returns the slot or -1 if none.
+__device__ int64_t claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, uint32_t &same) {
+  same = 0;
+  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+    uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    for (int s = 0; s < SLOTS; ++s) {
+      uint64_t k = __hip_atomic_load(&bk[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (k == KEY_EMPTY) {
+        k = atomicCAS(reinterpret_cast<unsigned long long *>(&bk[s]), KEY_EMPTY, key);
+        if (k == KEY_EMPTY) return int64_t(b * SLOTS + s);
+      }
+      if (k == key) ++same;
+    }
+    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+  }
+  return -1;
+}
+
+__device__ __forceinline__ uint64_t *val_ptr(const DevIndex &ix, int64_t slot) {
+  return ix.slots + (slot / SLOTS) * BUCKET_WORDS + SLOTS + (slot % SLOTS);
+}
+__device__ __forceinline__ uint64_t *key_ptr(const DevIndex &ix, int64_t slot) {
+  return ix.slots + (slot / SLOTS) * BUCKET_WORDS + (slot % SLOTS);
+}
+
+// Find whether `key` has a bitmap record (its HEADER lies before the chain's first EMPTY).
+__device__ int64_t find_header(const DevIndex &ix, uint64_t key) {
+  uint64_t b = home_bucket(key, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    for (int s = 0; s < SLOTS; ++s) {
+      const uint64_t k = __hip_atomic_load(&bk[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (k == KEY_EMPTY) return -1;
+      if (k == key && val_kind(bk[SLOTS + s]) == HEADER) return int64_t(b * SLOTS + s);
+    }
+    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+  }
+  return -1;
+}
+
+// Enter a distinct new entry.  Returns false only if the table has no free slot.
+// *trigger is set when the slot is the key's (T+1)-th plain slot.
+__device__ bool place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32_t epoch,
+                          uint32_t sess, bool &trigger) {
+  trigger = false;
+  const int64_t hs = find_header(ix, key);
+  uint32_t same;
+  if (hs >= 0) {
+    const uint64_t rec = val_rec(*val_ptr(ix, hs));
+    atomicOr(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
+             1ull << (inst & 63));
+    const int64_t s = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, same);
+    if (s < 0) return false;
+    *val_ptr(ix, s) = make_val(inst, MEMBER, epoch, sess);
+    return true;
+  }
+  const int64_t s = claim_slot(ix, home_bucket(key, ix.n_buckets), key, same);
+  if (s < 0) return false;
+  *val_ptr(ix, s) = make_val(inst, PLAIN, epoch, sess);
+  trigger = same == uint32_t(ix.threshold);
+  return true;
+}
+
+// Replace the plain slots of `key` by a bitmap record (one thread per key).
+__device__ bool spill_key(const DevIndex &ix, uint64_t key) {
+  const unsigned long long rec = atomicAdd(reinterpret_cast<unsigned long long *>(&ix.hdr->rec_used), 1ull);
+  if (rec >= ix.n_records) return true;  // pool exhausted: the key stays plain
+  uint64_t *bm = ix.pool + rec * uint64_t(ix.words);
+  int64_t first = -1;
+  uint64_t b = home_bucket(key, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+    uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    bool end = false;
+    for (int s = 0; s < SLOTS; ++s) {
+      const uint64_t k = bk[s];
+      if (k == KEY_EMPTY) {
+        end = true;
+        break;
+      }
+      if (k != key) continue;
+      const uint64_t v = bk[SLOTS + s];
+      if (val_kind(v) != PLAIN) continue;
+      const uint32_t inst = val_inst(v);
+      bm[inst >> 6] |= 1ull << (inst & 63);
+      uint32_t same;
+      const int64_t m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, same);
+      if (m < 0) return false;
+      *val_ptr(ix, m) = make_val(inst, MEMBER, val_epoch(v), uint32_t(v & 0xFFFFFF));
+      if (first < 0) {
+        first = int64_t(b * SLOTS + s);
+        bk[SLOTS + s] = header_val(rec);
+      } else {
+        bk[s] = KEY_TOMB;
+      }
+    }
+    if (end) break;
+    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+  }
+  return true;
+}
+
+// ---------------------------------------------------------------------------------
+// Insert
+// ---------------------------------------------------------------------------------
+struct WsHdr {
+  unsigned long long n_new;    // distinct new pairs listed
+  unsigned long long n_pairs;  // pairs over all request ranges
+  unsigned long long n_trig;   // keys queued for conversion
+  int err;                     // first input error seen by the probe
+  int abort;                   // set by the check: leave the index unchanged
+  unsigned long long pad[28];
+};
+static_assert(sizeof(WsHdr) == 256, "ws header size");
+
+struct InsWs {
+  WsHdr *hdr;
+  uint64_t *pos;    // per block: slot + 1 of an entry to refresh, 0 = none
+  uint64_t *dkey;   // dedupe table keys
+  uint64_t *dw2;    // dedupe table: inst << 32 | lowest request index, ~0 = free
+  uint64_t *list;   // dedupe slots of distinct new pairs
+  uint64_t *trig;   // keys queued for conversion
+  uint64_t n_dedupe;
+  uint64_t list_cap;  // entries in list and trig (= n_blocks)
+};
+
+uint64_t dedupe_size(int64_t n_blocks) {
+  uint64_t n = 64;
+  while (n < 2 * uint64_t(n_blocks)) n <<= 1;
+  return n;
+}
+
+uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
+  const uint64_t n = uint64_t(n_blocks < 1 ? 1 : n_blocks);
+  const uint64_t nd = dedupe_size(n_blocks);
+  uint64_t off = 0;
+  auto take = [&](uint64_t bytes) {
+    const uint64_t o = off;
+    off = round_up(off + bytes, 256);
+    return o;
+  };
+  const uint64_t o_hdr = take(sizeof(WsHdr));
+  const uint64_t o_pos = take(8 * n);
+  const uint64_t o_dkey = take(8 * nd);
+  const uint64_t o_dw2 = take(8 * nd);
+  const uint64_t o_list = take(8 * n);
+  const uint64_t o_trig = take(8 * n);
+  if (ws) {
+    char *b = static_cast<char *>(base);
+    ws->hdr = reinterpret_cast<WsHdr *>(b + o_hdr);
+    ws->pos = reinterpret_cast<uint64_t *>(b + o_pos);
+    ws->dkey = reinterpret_cast<uint64_t *>(b + o_dkey);
+    ws->dw2 = reinterpret_cast<uint64_t *>(b + o_dw2);
+    ws->list = reinterpret_cast<uint64_t *>(b + o_list);
+    ws->trig = reinterpret_cast<uint64_t *>(b + o_trig);
+    ws->n_dedupe = nd;
+    ws->list_cap = n;
+  }
+  return off;
+}
+
+__device__ __forceinline__ void ws_error(WsHdr *h, int e) { atomicCAS(&h->err, 0, e); }
+
+// Returns true when this call created the dedupe entry (first sighting of the pair).
+__device__ bool dedupe_pair(const InsWs &ws, uint64_t key, uint32_t inst, uint32_t r) {
+  const uint64_t mine = (uint64_t(inst) << 32) | r;
+  uint64_t h = mix64(key ^ ((uint64_t(inst) + 1) * 0xC2B2AE3D27D4EB4Full)) & (ws.n_dedupe - 1);
+  for (uint64_t step = 0; step < ws.n_dedupe; ++step, h = (h + 1) & (ws.n_dedupe - 1)) {
+    uint64_t k = __hip_atomic_load(&ws.dkey[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (k == KEY_EMPTY) k = atomicCAS(reinterpret_cast<unsigned long long *>(&ws.dkey[h]), KEY_EMPTY, key);
+    if (k != KEY_EMPTY && k != key) continue;
+    // this slot's key is `key`; its owner instance is decided by the second word
+    uint64_t w = __hip_atomic_load(&ws.dw2[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while (true) {
+      if (w == ~uint64_t(0)) {
+        const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&ws.dw2[h]), ~0ull, mine);
+        if (prev == ~uint64_t(0)) {
+          const unsigned long long at = atomicAdd(&ws.hdr->n_new, 1ull);
+          if (at < ws.list_cap) ws.list[at] = h;  // more pairs than blocks: rejected by the check
+          return true;
+        }
+        w = prev;
+        continue;
+      }
+      if ((w >> 32) == inst) {
+        atomicMin(reinterpret_cast<unsigned long long *>(&ws.dw2[h]), mine);
+        return false;
+      }
+      break;  // another instance's pair: keep probing
+    }
+  }
+  ws_error(ws.hdr, SMETRIC_EINTERNAL);
+  return false;
+}
+
+constexpr int IW = 4;  // waves per workgroup in per-request kernels
+
+__device__ __forceinline__ bool range_of(const int64_t *blk_off, int r, int64_t n_blocks, int64_t &b0,
+                                         int64_t &nb) {
+  b0 = blk_off[r];
+  const int64_t b1 = blk_off[r + 1];
+  nb = b1 - b0;
+  return b0 >= 0 && b0 <= b1 && b1 <= n_blocks;
+}
+
+__global__ __launch_bounds__(64 * IW) void ins_probe_kernel(DevIndex ix, InsWs ws, const uint64_t *keys,
+                                                            const int64_t *blk_off, int32_t n_req,
+                                                            int64_t n_blocks, const int32_t *instance,
+                                                            const uint32_t *session, uint32_t epoch) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * IW + wave;
+  if (r >= n_req) return;
+  int64_t b0, nb;
+  if (!range_of(blk_off, r, n_blocks, b0, nb)) {
+    if (lane == 0) ws_error(ws.hdr, SMETRIC_EINVAL);
+    return;
+  }
+  if (nb == 0) return;
+  if (lane == 0) atomicAdd(&ws.hdr->n_pairs, (unsigned long long)nb);
+  const int32_t inst = instance[r];
+  const uint32_t sess = session[r];
+  if (inst < 0 || inst >= ix.n_inst || sess >= SESSION_LIMIT) {
+    if (lane == 0) ws_error(ws.hdr, SMETRIC_EINVAL);
+    return;
+  }
+  for (int64_t j = lane; j < nb; j += 64) {
+    const uint64_t key = keys[b0 + j];
+    if (key == KEY_EMPTY || key == KEY_TOMB) {
+      ws_error(ws.hdr, SMETRIC_EINVAL);
+      ws.pos[b0 + j] = 0;
+      continue;
+    }
+    const Found f = find_entry(ix, key, uint32_t(inst));
+    if (f.slot >= 0) {
+      ws.pos[b0 + j] = val_epoch(f.val) < epoch ? uint64_t(f.slot) + 1 : 0;
+    } else {
+      ws.pos[b0 + j] = 0;
+      dedupe_pair(ws, key, uint32_t(inst), uint32_t(r));
+    }
+  }
+}
+
+__global__ void ins_check_kernel(DevIndex ix, InsWs ws, int64_t n_blocks) {
+  WsHdr *h = ws.hdr;
+  int e = h->err;
+  if (e == 0 && h->n_pairs > (unsigned long long)n_blocks) e = SMETRIC_EINVAL;
+  if (e == 0 && ix.hdr->n_entries + h->n_new > ix.capacity) e = SMETRIC_EFULL;
+  if (e != 0) {
+    h->abort = 1;
+    set_status(ix.hdr, e);
+  } else {
+    ix.hdr->n_entries += h->n_new;
+  }
+}
+
+__global__ __launch_bounds__(64 * IW) void ins_refresh_kernel(DevIndex ix, InsWs ws, const int64_t *blk_off,
+                                                              int32_t n_req, int64_t n_blocks,
+                                                              uint32_t epoch) {
+  if (ws.hdr->abort) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * IW + wave;
+  if (r >= n_req) return;
+  int64_t b0, nb;
+  if (!range_of(blk_off, r, n_blocks, b0, nb)) return;
+  for (int64_t j = lane; j < nb; j += 64) {
+    const uint64_t p = ws.pos[b0 + j];
+    if (!p) continue;
+    uint64_t *vp = val_ptr(ix, int64_t(p - 1));
+    const uint64_t v = *vp;
+    if (val_epoch(v) < epoch) *vp = (v & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+  }
+}
+
+__global__ void ins_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session, uint32_t epoch) {
+  if (ws.hdr->abort) return;
+  const uint64_t n = ws.hdr->n_new;
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint64_t h = ws.list[i];
+    const uint64_t key = ws.dkey[h], w = ws.dw2[h];
+    const uint32_t inst = uint32_t(w >> 32), r = uint32_t(w);
+    bool trig;
+    if (!place_new(ix, key, inst, epoch, session[r], trig)) {
+      set_status(ix.hdr, SMETRIC_EINTERNAL);
+      continue;
+    }
+    if (trig) ws.trig[atomicAdd(&ws.hdr->n_trig, 1ull)] = key;
+  }
+}
+
+__global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned long long *n_trig,
+                             const int *abort_flag) {
+  if (abort_flag && *abort_flag) return;
+  const uint64_t n = *n_trig;
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
+    if (!spill_key(ix, trig[i])) set_status(ix.hdr, SMETRIC_EINTERNAL);
+}
+
+// ---------------------------------------------------------------------------------
+// Evict / dump
+// ---------------------------------------------------------------------------------
+__global__ void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals, unsigned long long *count,
+                              uint64_t cap) {
+  const uint64_t n_slots = ix.n_buckets * SLOTS;
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_slots; i += stride) {
+    const uint64_t b = i / SLOTS, s = i % SLOTS;
+    const uint64_t k = ix.slots[b * BUCKET_WORDS + s];
+    if (k == KEY_EMPTY || k == KEY_TOMB) continue;
+    const uint64_t v = ix.slots[b * BUCKET_WORDS + SLOTS + s];
+    if (val_kind(v) == HEADER) continue;
+    const unsigned long long at = atomicAdd(count, 1ull);
+    if (at < cap) {
+      keys[at] = k;
+      vals[at] = val_plain(v);
+    }
+  }
+}
+
+// Rebuild: enter entries [lo, hi) of (keys, vals) into a cleared table.
+__global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const uint64_t *vals, uint64_t lo,
+                                     uint64_t hi, uint64_t *trig, unsigned long long *n_trig) {
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = lo + uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < hi; i += stride) {
+    const uint64_t v = vals[i];
+    bool t;
+    if (!place_new(ix, keys[i], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), t)) {
+      set_status(ix.hdr, SMETRIC_EINTERNAL);
+      continue;
+    }
+    if (t) trig[atomicAdd(n_trig, 1ull)] = keys[i];
+  }
+}
+
+__global__ void set_counts_kernel(IndexHdr *h, unsigned long long n_entries) {
+  h->n_entries = n_entries;
+  h->rec_used = 0;
+}
+
+struct EvictWs {
+  unsigned long long *count;  // 2 counters
+  uint64_t *ka, *va, *kb, *vb;
+  void *temp;
+  size_t temp_bytes;
+};
+
+size_t sort_temp_bytes(uint64_t n) {
+  size_t tb = 0;
+  hipcub::DoubleBuffer<uint64_t> k(nullptr, nullptr), v(nullptr, nullptr);
+  if (hipcub::DeviceRadixSort::SortPairs(nullptr, tb, k, v, int(n < 1 ? 1 : n), 0, 64, 0) != hipSuccess) return 0;
+  return tb;
+}
+
+uint64_t evict_ws_layout(uint64_t cap, EvictWs *ws, void *base) {
+  const uint64_t n = cap < 1 ? 1 : cap;
+  const size_t tb = sort_temp_bytes(n);
+  uint64_t off = 0;
+  auto take = [&](uint64_t bytes) {
+    const uint64_t o = off;
+    off = round_up(off + bytes, 256);
+    return o;
+  };
+  const uint64_t o_cnt = take(256), o_ka = take(8 * n), o_va = take(8 * n), o_kb = take(8 * n),
+                 o_vb = take(8 * n), o_tmp = take(tb);
+  if (ws) {
+    char *b = static_cast<char *>(base);
+    ws->count = reinterpret_cast<unsigned long long *>(b + o_cnt);
+    ws->ka = reinterpret_cast<uint64_t *>(b + o_ka);
+    ws->va = reinterpret_cast<uint64_t *>(b + o_va);
+    ws->kb = reinterpret_cast<uint64_t *>(b + o_kb);
+    ws->vb = reinterpret_cast<uint64_t *>(b + o_vb);
+    ws->temp = b + o_tmp;
+    ws->temp_bytes = tb;
+  }
+  return off;
+}
+
+int read_hdr(const smetric_index *idx, IndexHdr *out, hipStream_t s) {
+  if (hipMemcpyAsync(out, idx->hdr, sizeof(IndexHdr), hipMemcpyDeviceToHost, s) != hipSuccess) return SMETRIC_EHIP;
+  return hip_rc(hipStreamSynchronize(s));
+}
+
+// Gather all entries and sort them by (key, instance), or by (epoch, key, instance) when
+// by_epoch.  Stable LSD passes: instance, then key, then (optionally) epoch.  On return
+// the sorted keys/values are in (*keys_out, *vals_out).
+int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, bool by_epoch, uint64_t **keys_out,
+                  uint64_t **vals_out, hipStream_t s) {
+  const DevIndex ix = dev_view(idx);
+  int rc = fill(ws.count, 256, 0, s);
+  if (rc) return rc;
+  const uint64_t n_slots = ix.n_buckets * SLOTS;
+  hipLaunchKernelGGL(gather_kernel, dim3(grid_for(n_slots)), dim3(TB), 0, s, ix, ws.ka, ws.va, ws.count, n);
+  if ((rc = hip_rc(hipGetLastError()))) return rc;
+  unsigned long long got = 0;
+  if (hipMemcpyAsync(&got, ws.count, 8, hipMemcpyDeviceToHost, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+    return SMETRIC_EHIP;
+  if (got != n) return SMETRIC_EINTERNAL;
+  if (n > 1) {
+    size_t tb = ws.temp_bytes;
+    hipcub::DoubleBuffer<uint64_t> vk(ws.va, ws.vb), kv(ws.ka, ws.kb);
+    // 1) by instance (value bits 48..63)
+    if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, vk, kv, int(n), 48, 64, s) != hipSuccess) return SMETRIC_EHIP;
+    // 2) stably by key
+    hipcub::DoubleBuffer<uint64_t> k2(kv.Current(), kv.Alternate()), v2(vk.Current(), vk.Alternate());
+    if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, k2, v2, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
+    if (by_epoch) {
+      // 3) stably by epoch (value bits 24..45)
+      hipcub::DoubleBuffer<uint64_t> v3(v2.Current(), v2.Alternate()), k3(k2.Current(), k2.Alternate());
+      if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, v3, k3, int(n), 24, 46, s) != hipSuccess) return SMETRIC_EHIP;
+      *keys_out = k3.Current();
+      *vals_out = v3.Current();
+    } else {
+      *keys_out = k2.Current();
+      *vals_out = v2.Current();
+    }
+  } else {
+    *keys_out = ws.ka;
+    *vals_out = ws.va;
+  }
+  return SMETRIC_OK;
+}
+
+}  // namespace
+}  // namespace smk
+
+using namespace smk;
+
+extern "C" int smetric_index_bytes(uint64_t capacity, int32_t n_instances, uint64_t *bytes) {
+  Layout L;
+  if (!bytes || !layout_for(capacity, n_instances, L)) return SMETRIC_EINVAL;
+  *bytes = L.bytes;
+  return SMETRIC_OK;
+}
+
+extern "C" int smetric_index_attach(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
+                                    int32_t n_instances) {
+  return attach(idx, mem, mem_bytes, capacity, n_instances);
+}
+
+extern "C" int smetric_index_init(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
+                                  int32_t n_instances, hipStream_t stream) {
+  int rc = attach(idx, mem, mem_bytes, capacity, n_instances);
+  if (rc) return rc;
+  Layout L;
+  layout_for(capacity, n_instances, L);
+  return fill(mem, L.bytes, 0, stream);
+}
+
+extern "C" int smetric_index_stats(const smetric_index *idx, uint64_t *n_entries, int32_t *status,
+                                   int32_t reset_status, hipStream_t stream) {
+  if (!idx || !idx->hdr) return SMETRIC_EINVAL;
+  IndexHdr h;
+  int rc = read_hdr(idx, &h, stream);
+  if (rc) return rc;
+  if (n_entries) *n_entries = h.n_entries;
+  if (status) *status = h.status;
+  if (reset_status) {
+    hipLaunchKernelGGL(set_int_kernel, dim3(1), dim3(1), 0, stream, &static_cast<IndexHdr *>(idx->hdr)->status, 0);
+    if ((rc = hip_rc(hipGetLastError()))) return rc;
+    rc = hip_rc(hipStreamSynchronize(stream));
+  }
+  return rc;
+}
+
+extern "C" int smetric_index_insert_ws_bytes(int64_t n_blocks, uint64_t *ws_bytes) {
+  if (n_blocks < 0 || !ws_bytes) return SMETRIC_EINVAL;
+  *ws_bytes = insert_ws_layout(n_blocks, nullptr, nullptr);
+  return SMETRIC_OK;
+}
+
+extern "C" int smetric_index_insert(smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
+                                    int32_t n_req, int64_t n_blocks, const int32_t *instance,
+                                    const uint32_t *session, uint32_t epoch, void *workspace,
+                                    uint64_t ws_bytes, hipStream_t stream) {
+  if (!idx || !idx->slots || n_req < 0 || n_blocks < 0 || epoch >= EPOCH_LIMIT) return SMETRIC_EINVAL;
+  if (n_req == 0) return SMETRIC_OK;
+  if (!blk_off || !instance || !session || (n_blocks > 0 && !keys)) return SMETRIC_EINVAL;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) ||
+      ws_bytes < insert_ws_layout(n_blocks, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  InsWs ws;
+  insert_ws_layout(n_blocks, &ws, workspace);
+  const DevIndex ix = dev_view(idx);
+  int rc;
+  if ((rc = fill(ws.hdr, sizeof(WsHdr), 0, stream))) return rc;
+  if ((rc = fill(ws.dkey, 8 * ws.n_dedupe, 0, stream))) return rc;
+  if ((rc = fill(ws.dw2, 8 * ws.n_dedupe, ~uint64_t(0), stream))) return rc;
+  const dim3 rgrid((n_req + IW - 1) / IW), rblock(64 * IW);
+  hipLaunchKernelGGL(ins_probe_kernel, rgrid, rblock, 0, stream, ix, ws, keys, blk_off, n_req, n_blocks, instance,
+                     session, epoch);
+  hipLaunchKernelGGL(ins_check_kernel, dim3(1), dim3(1), 0, stream, ix, ws, n_blocks);
+  hipLaunchKernelGGL(ins_refresh_kernel, rgrid, rblock, 0, stream, ix, ws, blk_off, n_req, n_blocks, epoch);
+  hipLaunchKernelGGL(ins_place_kernel, dim3(grid_for(uint64_t(n_blocks))), dim3(TB), 0, stream, ix, ws, session, epoch);
+  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort);
+  return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_index_evict_ws_bytes(const smetric_index *idx, uint64_t *ws_bytes) {
+  if (!idx || !ws_bytes) return SMETRIC_EINVAL;
+  *ws_bytes = evict_ws_layout(idx->capacity, nullptr, nullptr);
+  return SMETRIC_OK;
+}
+
+extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32_t frac_den, void *workspace,
+                                   uint64_t ws_bytes, hipStream_t stream) {
+  if (!idx || !idx->slots || frac_den == 0 || frac_num > frac_den) return SMETRIC_EINVAL;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) ||
+      ws_bytes < evict_ws_layout(idx->capacity, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  EvictWs ws;
+  evict_ws_layout(idx->capacity, &ws, workspace);
+  IndexHdr h;
+  int rc = read_hdr(idx, &h, stream);
+  if (rc) return rc;
+  const uint64_t n = h.n_entries;
+  const uint64_t m = uint64_t((static_cast<unsigned __int128>(n) * frac_num + frac_den - 1) / frac_den);
+  if (m == 0) return SMETRIC_OK;
+  uint64_t *keys, *vals;
+  if ((rc = gather_sorted(idx, ws, n, true, &keys, &vals, stream))) return rc;
+  // rebuild from the survivors [m, n)
+  const DevIndex ix = dev_view(idx);
+  if ((rc = fill(ix.slots, ix.n_buckets * BUCKET_WORDS * 8, 0, stream))) return rc;
+  if ((rc = fill(ix.pool, ix.n_records * uint64_t(ix.words) * 8, 0, stream))) return rc;
+  hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m));
+  // the alternate sort buffers are free now: one holds the conversion queue
+  uint64_t *trig = (keys == ws.ka) ? ws.kb : ws.ka;
+  unsigned long long *n_trig = ws.count + 1;
+  hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n - m)), dim3(TB), 0, stream, ix, keys, vals, m, n, trig,
+                     n_trig);
+  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr);
+  if ((rc = hip_rc(hipGetLastError()))) return rc;
+  return hip_rc(hipStreamSynchronize(stream));
+}
+
+extern "C" int smetric_index_dump(const smetric_index *idx, uint64_t *keys_out, uint64_t *vals_out, uint64_t cap,
+                                  void *workspace, uint64_t ws_bytes, uint64_t *n_out, hipStream_t stream) {
+  if (!idx || !idx->slots || !n_out || (cap > 0 && (!keys_out || !vals_out))) return SMETRIC_EINVAL;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) ||
+      ws_bytes < evict_ws_layout(idx->capacity, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  EvictWs ws;
+  evict_ws_layout(idx->capacity, &ws, workspace);
+  IndexHdr h;
+  int rc = read_hdr(idx, &h, stream);
+  if (rc) return rc;
+  const uint64_t n = h.n_entries;
+  *n_out = n;
+  if (n == 0) return SMETRIC_OK;
+  uint64_t *keys, *vals;
+  if ((rc = gather_sorted(idx, ws, n, false, &keys, &vals, stream))) return rc;
+  const uint64_t c = n < cap ? n : cap;
+  if (c) {
+    if (hipMemcpyAsync(keys_out, keys, 8 * c, hipMemcpyDeviceToDevice, stream) != hipSuccess ||
+        hipMemcpyAsync(vals_out, vals, 8 * c, hipMemcpyDeviceToDevice, stream) != hipSuccess)
+      return SMETRIC_EHIP;
+  }
+  return hip_rc(hipStreamSynchronize(stream));
+}

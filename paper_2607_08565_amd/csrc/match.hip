@@ -1,0 +1,369 @@
+// Index probe + first-miss reduction (K3 + K4).
+//
+// Paper: the router scores instance i by c_i, the prefix hit length of the request's
+// prompt in instance i's local KV$ (Sec. 4.1, scoring template), measured at KV$-block
+// granularity (Sec. 3.1).  Here c[r][i] = the number of leading blocks of request r
+// whose keys instance i holds; an instance drops out at its first missing block.
+//
+// Mapping to gfx950: one wavefront per request.  The request is walked in chunks of 64
+// blocks; lane l probes block j0+l (one 128-byte bucket line per probe, more only when
+// a chain spills into the next bucket), collecting the block's holder set as one of
+//   NONE, LIST (<= 8 plain holders, kept in registers), HOT (bitmap record in the pool)
+//   or LONG (more plain holders than fit the list; re-walked on demand).
+// The alive set then shrinks block by block:
+//   * NARROW (<= 64 alive): lane t keeps alive instance a_t; per chunk and per alive
+//     instance, every lane tests membership in its own block and one ballot finds the
+//     first missing block.  This is the common case (a session's private blocks).
+//   * WIDE (more alive, e.g. a shared system prefix): the alive bitmap lives in registers,
+//     WPL 64-bit words per lane; holder bitmaps of 8 blocks are fetched ahead, then
+//     ANDed in block order.  Once <= 64 remain the wave switches to NARROW.
+// The output row is zeroed first; an instance is written again only when it drops after
+// block 0 or survives to the end.
+#include "common.h"
+
+namespace smk {
+namespace {
+
+constexpr int MW = 4;        // waves per workgroup
+constexpr int LIST_MAX = 8;  // plain holders kept per probe
+enum HKind : uint32_t { H_NONE = 0, H_LIST = 1, H_HOT = 2, H_LONG = 3 };
+
+struct Holders {
+  uint32_t kind;
+  uint32_t h[LIST_MAX];  // LIST members (0xFFFFFFFF when unused)
+  uint64_t rec;          // HOT: pool record
+};
+
+__device__ __forceinline__ void load_keys(const uint64_t *bk, uint64_t k[SLOTS]) {
+  const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(bk);
+#pragma unroll
+  for (int i = 0; i < SLOTS / 2; ++i) {
+    ulonglong2 v = p[i];
+    k[2 * i] = v.x;
+    k[2 * i + 1] = v.y;
+  }
+}
+
+// Walk key's chain and collect its holders.
+__device__ Holders probe(const DevIndex &ix, uint64_t key) {
+  Holders H;
+  H.kind = H_NONE;
+  H.rec = 0;
+#pragma unroll
+  for (int i = 0; i < LIST_MAX; ++i) H.h[i] = 0xFFFFFFFFu;
+  uint32_t cnt = 0;
+  uint64_t b = home_bucket(key, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    uint64_t k[SLOTS];
+    load_keys(bk, k);
+    uint32_t mm = 0, em = 0;
+#pragma unroll
+    for (int s = 0; s < SLOTS; ++s) {
+      mm |= uint32_t(k[s] == key) << s;
+      em |= uint32_t(k[s] == KEY_EMPTY) << s;
+    }
+    if (em) mm &= (em & (0u - em)) - 1u;  // only slots before the first empty one
+    while (mm) {
+      const int s = __builtin_ctz(mm);
+      mm &= mm - 1;
+      const uint64_t v = bk[SLOTS + s];
+      const uint32_t kind = val_kind(v);
+      if (kind == HEADER) {
+        H.kind = H_HOT;
+        H.rec = val_rec(v);
+        return H;
+      }
+      if (kind == PLAIN) {
+        const uint32_t inst = val_inst(v);
+#pragma unroll
+        for (int i = 0; i < LIST_MAX; ++i)
+          if (cnt == uint32_t(i)) H.h[i] = inst;
+        ++cnt;
+      }
+    }
+    if (em) break;
+    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+  }
+  H.kind = cnt == 0 ? H_NONE : (cnt <= LIST_MAX ? H_LIST : H_LONG);
+  return H;
+}
+
+// Is (key, inst) a plain entry?  Used for LONG holder sets only.
+__device__ bool chain_has(const DevIndex &ix, uint64_t key, uint32_t inst) {
+  uint64_t b = home_bucket(key, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    for (int s = 0; s < SLOTS; ++s) {
+      const uint64_t k = bk[s];
+      if (k == KEY_EMPTY) return false;
+      if (k == key) {
+        const uint64_t v = bk[SLOTS + s];
+        if (val_kind(v) == PLAIN && val_inst(v) == inst) return true;
+      }
+    }
+    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+  }
+  return false;
+}
+
+// OR into `m` the bits of every plain holder of `key` that fall in word w.
+__device__ uint64_t chain_word(const DevIndex &ix, uint64_t key, int w) {
+  uint64_t m = 0;
+  uint64_t b = home_bucket(key, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    for (int s = 0; s < SLOTS; ++s) {
+      const uint64_t k = bk[s];
+      if (k == KEY_EMPTY) return m;
+      if (k == key) {
+        const uint64_t v = bk[SLOTS + s];
+        if (val_kind(v) == PLAIN && int(val_inst(v) >> 6) == w) m |= uint64_t(1) << (val_inst(v) & 63);
+      }
+    }
+    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+  }
+  return m;
+}
+
+__device__ __forceinline__ bool holds(const DevIndex &ix, const Holders &H, uint64_t key, uint32_t a) {
+  switch (H.kind) {
+    case H_LIST: {
+      bool hit = false;
+#pragma unroll
+      for (int i = 0; i < LIST_MAX; ++i) hit |= H.h[i] == a;
+      return hit;
+    }
+    case H_HOT:
+      return (ix.pool[H.rec * uint64_t(ix.words) + (a >> 6)] >> (a & 63)) & 1;
+    case H_LONG:
+      return chain_has(ix, key, a);
+    default:
+      return false;
+  }
+}
+
+__device__ __forceinline__ uint64_t rdl64(uint64_t v, int src) {
+  const uint32_t lo = __builtin_amdgcn_readlane(uint32_t(v), src);
+  const uint32_t hi = __builtin_amdgcn_readlane(uint32_t(v >> 32), src);
+  return (uint64_t(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+
+// Holder word w of block `src` (a lane of the current chunk) in WIDE mode.
+__device__ __forceinline__ uint64_t holder_word(const DevIndex &ix, uint32_t kind, uint64_t rec,
+                                                const uint32_t hl[LIST_MAX], uint64_t key, int w) {
+  if (w >= ix.words) return 0;
+  if (kind == H_HOT) return ix.pool[rec * uint64_t(ix.words) + w];
+  if (kind == H_LIST) {
+    uint64_t m = 0;
+#pragma unroll
+    for (int i = 0; i < LIST_MAX; ++i)
+      if (hl[i] != 0xFFFFFFFFu && int(hl[i] >> 6) == w) m |= uint64_t(1) << (hl[i] & 63);
+    return m;
+  }
+  if (kind == H_LONG) return chain_word(ix, key, w);
+  return 0;
+}
+
+template <int WPL>
+__global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
+                                                        const int64_t *__restrict__ blk_off,
+                                                        int32_t n_req, int64_t n_blocks,
+                                                        int32_t *__restrict__ matched) {
+  __shared__ int32_t nlist[MW][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * MW + wave;
+  if (r >= n_req) return;
+  const int I = ix.n_inst;
+  int32_t *row = matched + int64_t(r) * I;
+  for (int i = lane; i < I; i += 64) row[i] = 0;
+  const int64_t b0 = blk_off[r], b1 = blk_off[r + 1];
+  if (!(b0 >= 0 && b0 <= b1 && b1 <= n_blocks)) {
+    if (lane == 0) set_status(ix.hdr, SMETRIC_EINVAL);
+    return;
+  }
+  const int64_t nb = b1 - b0;
+  if (nb == 0) return;
+
+  enum { M_ALL, M_NARROW, M_WIDE, M_DONE };
+  int mode = M_ALL;
+  int my_inst = -1;   // NARROW: this lane's alive instance
+  uint64_t A[WPL];    // WIDE: alive words lane + 64 t
+#pragma unroll
+  for (int t = 0; t < WPL; ++t) A[t] = 0;
+
+  for (int64_t j0 = 0; j0 < nb && mode != M_DONE; j0 += 64) {
+    const int64_t j = j0 + lane;
+    const bool valid = j < nb;
+    const uint64_t key = valid ? keys[b0 + j] : 0;
+    Holders H;
+    if (valid) {
+      H = probe(ix, key);
+    } else {
+      H.kind = H_NONE;
+      H.rec = 0;
+#pragma unroll
+      for (int i = 0; i < LIST_MAX; ++i) H.h[i] = 0xFFFFFFFFu;
+    }
+    int jj = 0;
+    if (mode == M_ALL) {
+      // block 0 fixes the first alive set; everyone else already has c = 0
+      const uint32_t kind0 = __builtin_amdgcn_readfirstlane(H.kind);
+      if (kind0 == H_NONE) return;
+      if (kind0 == H_LIST) {
+#pragma unroll
+        for (int i = 0; i < LIST_MAX; ++i) {
+          const uint32_t v = __builtin_amdgcn_readlane(H.h[i], 0);
+          if (lane == i) my_inst = v == 0xFFFFFFFFu ? -1 : int(v);
+        }
+        mode = M_NARROW;
+      } else {
+        const uint64_t rec0 = rdl64(H.rec, 0), key0 = rdl64(key, 0);
+        uint32_t hl0[LIST_MAX];
+#pragma unroll
+        for (int i = 0; i < LIST_MAX; ++i) hl0[i] = 0xFFFFFFFFu;
+#pragma unroll
+        for (int t = 0; t < WPL; ++t) A[t] = holder_word(ix, kind0, rec0, hl0, key0, lane + 64 * t);
+        mode = M_WIDE;
+      }
+      jj = 1;
+    }
+
+    if (mode == M_WIDE) {
+      // block by block, G blocks' holder words fetched ahead of the AND chain
+      constexpr int G = WPL >= 8 ? 1 : 8 / WPL;
+      while (jj < 64 && mode == M_WIDE) {
+        uint64_t hw[G][WPL];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const int src = jj + g < 64 ? jj + g : 63;
+          const uint32_t kind = __builtin_amdgcn_readlane(H.kind, src);
+          const uint64_t rec = rdl64(H.rec, src);
+          const uint64_t k = rdl64(key, src);
+          uint32_t hl[LIST_MAX];
+#pragma unroll
+          for (int i = 0; i < LIST_MAX; ++i) hl[i] = __builtin_amdgcn_readlane(H.h[i], src);
+#pragma unroll
+          for (int t = 0; t < WPL; ++t)
+            hw[g][t] = (jj + g < 64 && j0 + jj + g < nb) ? holder_word(ix, kind, rec, hl, k, lane + 64 * t) : 0;
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const int64_t jb = j0 + jj + g;
+          if (jj + g < 64) {
+#pragma unroll
+            for (int t = 0; t < WPL; ++t) {
+              const uint64_t n = A[t] & hw[g][t];
+              uint64_t d = A[t] & ~n;
+              A[t] = n;
+              const int w = lane + 64 * t;
+              while (d) {  // blocks past the end count as misses: survivors get nb
+                const int bit = __builtin_ctzll(d);
+                d &= d - 1;
+                row[w * 64 + bit] = int32_t(jb < nb ? jb : nb);
+              }
+            }
+          }
+        }
+        jj += G;
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int t = 0; t < WPL; ++t) cnt += __popcll(A[t]);
+        const uint32_t n_alive = wave_sum(cnt);
+        if (n_alive == 0) {
+          mode = M_DONE;
+        } else if (n_alive <= 64) {
+          // hand the survivors to lanes: exclusive prefix of per-lane counts
+          uint32_t pre = cnt;
+#pragma unroll
+          for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t t = __shfl_up(pre, d, 64);
+            if (lane >= d) pre += t;
+          }
+          pre -= cnt;
+#pragma unroll
+          for (int t = 0; t < WPL; ++t) {
+            uint64_t a = A[t];
+            while (a) {
+              const int bit = __builtin_ctzll(a);
+              a &= a - 1;
+              nlist[wave][pre++] = (lane + 64 * t) * 64 + bit;
+            }
+          }
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+          my_inst = lane < int(n_alive) ? nlist[wave][lane] : -1;
+          __builtin_amdgcn_wave_barrier();
+          mode = M_NARROW;
+        }
+      }
+    }
+
+    if (mode == M_NARROW && jj < 64) {
+      // every alive instance: first block of the chunk (at or after jj) it does not hold
+      uint64_t alive = __ballot(my_inst >= 0);
+      while (alive) {
+        const int t = __builtin_ctzll(alive);
+        alive &= alive - 1;
+        const uint32_t a = __builtin_amdgcn_readlane(uint32_t(my_inst), t);
+        const bool held = lane < jj || (valid && holds(ix, H, key, a));
+        const uint64_t miss = __ballot(!held);
+        if (miss) {
+          const int f = __builtin_ctzll(miss);
+          if (lane == t) {
+            row[a] = int32_t(j0 + f < nb ? j0 + f : nb);
+            my_inst = -1;
+          }
+        }
+      }
+      if (!__ballot(my_inst >= 0)) mode = M_DONE;
+    }
+  }
+  // survivors of a request whose block count is a multiple of 64
+  if (mode == M_NARROW) {
+    if (my_inst >= 0) row[my_inst] = int32_t(nb);
+  } else if (mode == M_WIDE) {
+#pragma unroll
+    for (int t = 0; t < WPL; ++t) {
+      uint64_t a = A[t];
+      const int w = lane + 64 * t;
+      while (a) {
+        const int bit = __builtin_ctzll(a);
+        a &= a - 1;
+        row[w * 64 + bit] = int32_t(nb);
+      }
+    }
+  }
+}
+
+}  // namespace
+}  // namespace smk
+
+using namespace smk;
+
+extern "C" int smetric_match(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
+                             int32_t n_req, int64_t n_blocks, int32_t *matched, hipStream_t stream) {
+  if (!idx || n_req < 0 || n_blocks < 0) return SMETRIC_EINVAL;
+  if (n_req == 0) return SMETRIC_OK;
+  if (!blk_off || !matched || (n_blocks > 0 && !keys) || !idx->slots) return SMETRIC_EINVAL;
+  const DevIndex ix = dev_view(idx);
+  const dim3 grid((n_req + MW - 1) / MW), block(64 * MW);
+  const int wpl = (ix.words + 63) / 64;
+  if (wpl <= 1)
+    hipLaunchKernelGGL(match_kernel<1>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
+  else if (wpl <= 2)
+    hipLaunchKernelGGL(match_kernel<2>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
+  else if (wpl <= 4)
+    hipLaunchKernelGGL(match_kernel<4>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
+  else if (wpl <= 8)
+    hipLaunchKernelGGL(match_kernel<8>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
+  else
+    hipLaunchKernelGGL(match_kernel<16>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
+  return hip_rc(hipGetLastError());
+}

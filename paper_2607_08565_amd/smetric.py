@@ -1,0 +1,233 @@
+"""Thin ctypes binding of libsmetric.so (C ABI in include/smetric.h).
+
+Argument marshalling only: device tensors are passed by data pointer, the stream is
+torch's current stream, and every step runs in the library's HIP kernels.  Importing
+this module loads the library and raises if it has not been built -- there is no CPU
+fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+import torch
+
+from .workload import BLOCK, DEFAULT_SEED
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsmetric.so")
+
+OK, EINVAL, EFULL, EHIP, EWORKSPACE, EINTERNAL = 0, -1, -2, -3, -4, -5
+FIRST_TURN, EVICTED, STICK, LAST_RESORT, MIGRATE, INVALID = 0, 1, 2, 3, 4, 255
+
+
+class SmetricError(RuntimeError):
+    def __init__(self, fn: str, rc: int):
+        super().__init__(f"{fn} returned {rc}")
+        self.rc = rc
+
+
+class _Index(C.Structure):
+    _fields_ = [
+        ("mem", C.c_void_p), ("mem_bytes", C.c_uint64), ("capacity", C.c_uint64),
+        ("n_instances", C.c_int32), ("bitmap_words", C.c_int32), ("spill_threshold", C.c_int32),
+        ("reserved0", C.c_int32), ("n_buckets", C.c_uint64), ("n_records", C.c_uint64),
+        ("slots", C.c_void_p), ("pool", C.c_void_p), ("hdr", C.c_void_p),
+    ]
+
+
+class _Params(C.Structure):
+    _fields_ = [
+        ("c_lin", C.c_int64), ("c_att", C.c_int64), ("slo_b", C.c_int64), ("slo_a", C.c_int64),
+        ("slack_num", C.c_int32), ("slack_den", C.c_int32), ("hit_num", C.c_int32),
+        ("hit_den", C.c_int32), ("block_size", C.c_int32),
+    ]
+
+
+def _load() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build the HIP library first (__graft_entry__.build())")
+    lib = C.CDLL(LIB_PATH)
+    P, I32, I64, U64, U32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_uint32
+    PIX = C.POINTER(_Index)
+    sig = {
+        "smetric_version": [],
+        "smetric_block_offsets": [P, I32, I32, P, P],
+        "smetric_hash_blocks": [P, I64, P, P, I32, I64, I32, U64, P, P, P],
+        "smetric_index_bytes": [U64, I32, P],
+        "smetric_index_init": [PIX, P, U64, U64, I32, P],
+        "smetric_index_attach": [PIX, P, U64, U64, I32],
+        "smetric_index_stats": [PIX, P, P, I32, P],
+        "smetric_match": [PIX, P, P, I32, I64, P, P],
+        "smetric_route": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
+        "smetric_index_insert_ws_bytes": [I64, P],
+        "smetric_index_insert": [PIX, P, P, I32, I64, P, P, U32, P, U64, P],
+        "smetric_index_evict_ws_bytes": [PIX, P],
+        "smetric_index_evict": [PIX, U32, U32, P, U64, P],
+        "smetric_index_dump": [PIX, P, P, U64, P, U64, P, P],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = C.c_int
+    return lib
+
+
+_lib = _load()
+EXPORTED = (
+    "smetric_version", "smetric_block_offsets", "smetric_hash_blocks", "smetric_index_bytes",
+    "smetric_index_init", "smetric_index_attach", "smetric_index_stats", "smetric_match",
+    "smetric_route", "smetric_index_insert_ws_bytes", "smetric_index_insert",
+    "smetric_index_evict_ws_bytes", "smetric_index_evict", "smetric_index_dump",
+)
+
+
+def _check(fn: str, rc: int):
+    if rc != OK:
+        raise SmetricError(fn, rc)
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype, name: str) -> C.c_void_p:
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dtype != dtype or not t.is_contiguous():
+        raise TypeError(f"{name}: expected a contiguous {dtype} CUDA tensor")
+    return C.c_void_p(t.data_ptr())
+
+
+def version() -> int:
+    return _lib.smetric_version()
+
+
+def block_offsets(tok_off, block_size: int = BLOCK):
+    """Host helper: (blk_off int64[R+1] numpy, n_blocks)."""
+    tok_off = np.ascontiguousarray(np.asarray(tok_off, np.int64))
+    R = len(tok_off) - 1
+    blk_off = np.zeros(R + 1, np.int64)
+    nb = C.c_int64()
+    _check("smetric_block_offsets", _lib.smetric_block_offsets(
+        tok_off.ctypes.data_as(C.c_void_p), R, block_size, blk_off.ctypes.data_as(C.c_void_p), C.byref(nb)))
+    return blk_off, int(nb.value)
+
+
+def hash_blocks(tokens: torch.Tensor, tok_off: torch.Tensor, blk_off: torch.Tensor, n_blocks: int,
+                block_size: int = BLOCK, seed: int = DEFAULT_SEED, keys: torch.Tensor | None = None,
+                status: torch.Tensor | None = None) -> torch.Tensor:
+    R = tok_off.numel() - 1
+    if keys is None:
+        keys = torch.empty(max(n_blocks, 1), dtype=torch.uint64, device=tokens.device)
+    _check("smetric_hash_blocks", _lib.smetric_hash_blocks(
+        _dev(tokens, torch.int32, "tokens"), tokens.numel(), _dev(tok_off, torch.int64, "tok_off"),
+        _dev(blk_off, torch.int64, "blk_off"), R, n_blocks, block_size, C.c_uint64(seed),
+        _dev(keys, torch.uint64, "keys"), _dev(status, torch.int32, "status") if status is not None else None,
+        _stream()))
+    return keys
+
+
+def route(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
+          q: torch.Tensor, params: dict, rr_base: int = 0, target: torch.Tensor | None = None,
+          branch: torch.Tensor | None = None):
+    R, I = matched.shape
+    dev = matched.device
+    target = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if target is None else target
+    branch = torch.empty(max(R, 1), dtype=torch.uint8, device=dev) if branch is None else branch
+    p = _Params(**params)
+    _check("smetric_route", _lib.smetric_route(
+        _dev(matched, torch.int32, "matched"), R, I, _dev(prompt_len, torch.int32, "prompt_len"),
+        _dev(hist_len, torch.int32, "hist_len"), _dev(turn, torch.int32, "turn"), _dev(q, torch.int64, "q"),
+        C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
+        _stream()))
+    return target[:R], branch[:R]
+
+
+def insert_ws_bytes(n_blocks: int) -> int:
+    b = C.c_uint64()
+    _check("smetric_index_insert_ws_bytes", _lib.smetric_index_insert_ws_bytes(n_blocks, C.byref(b)))
+    return int(b.value)
+
+
+def index_bytes(capacity: int, n_instances: int) -> int:
+    b = C.c_uint64()
+    _check("smetric_index_bytes", _lib.smetric_index_bytes(C.c_uint64(capacity), n_instances, C.byref(b)))
+    return int(b.value)
+
+
+class Index:
+    """Global block index in one device buffer (torch-allocated)."""
+
+    def __init__(self, capacity: int, n_instances: int, device="cuda", mem: torch.Tensor | None = None):
+        self.capacity, self.n_instances = capacity, n_instances
+        nbytes = index_bytes(capacity, n_instances)
+        self.mem = torch.empty(nbytes, dtype=torch.uint8, device=device) if mem is None else mem
+        self.c = _Index()
+        _check("smetric_index_init", _lib.smetric_index_init(
+            C.byref(self.c), C.c_void_p(self.mem.data_ptr()), nbytes, C.c_uint64(capacity), n_instances, _stream()))
+        self._ws = None
+
+    @property
+    def ref(self):
+        return C.byref(self.c)
+
+    def _workspace(self, nbytes: int) -> torch.Tensor:
+        if self._ws is None or self._ws.numel() < nbytes:
+            self._ws = torch.empty(nbytes, dtype=torch.uint8, device=self.mem.device)
+        return self._ws
+
+    def stats(self, reset_status: bool = False):
+        n, st = C.c_uint64(), C.c_int32()
+        _check("smetric_index_stats", _lib.smetric_index_stats(self.ref, C.byref(n), C.byref(st), int(reset_status),
+                                                               _stream()))
+        return int(n.value), int(st.value)
+
+    def match(self, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int,
+              matched: torch.Tensor | None = None) -> torch.Tensor:
+        R = blk_off.numel() - 1
+        if matched is None:
+            matched = torch.empty((max(R, 1), self.n_instances), dtype=torch.int32, device=keys.device)
+        _check("smetric_match", _lib.smetric_match(
+            self.ref, _dev(keys, torch.uint64, "keys"), _dev(blk_off, torch.int64, "blk_off"), R, n_blocks,
+            _dev(matched, torch.int32, "matched"), _stream()))
+        return matched[:R]
+
+    def insert(self, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int, instance: torch.Tensor,
+               session: torch.Tensor, epoch: int, workspace: torch.Tensor | None = None):
+        R = blk_off.numel() - 1
+        need = insert_ws_bytes(n_blocks)
+        ws = self._workspace(need) if workspace is None else workspace
+        _check("smetric_index_insert", _lib.smetric_index_insert(
+            self.ref, _dev(keys, torch.uint64, "keys"), _dev(blk_off, torch.int64, "blk_off"), R, n_blocks,
+            _dev(instance, torch.int32, "instance"), _dev(session, torch.int32, "session")
+            if session.dtype == torch.int32 else _dev(session, torch.uint32, "session"),
+            C.c_uint32(epoch), C.c_void_p(ws.data_ptr()), ws.numel(), _stream()))
+
+    def evict_ws_bytes(self) -> int:
+        b = C.c_uint64()
+        _check("smetric_index_evict_ws_bytes", _lib.smetric_index_evict_ws_bytes(self.ref, C.byref(b)))
+        return int(b.value)
+
+    def evict(self, num: int, den: int):
+        ws = self._workspace(self.evict_ws_bytes())
+        _check("smetric_index_evict", _lib.smetric_index_evict(self.ref, C.c_uint32(num), C.c_uint32(den),
+                                                               C.c_void_p(ws.data_ptr()), ws.numel(), _stream()))
+
+    def dump(self):
+        """All entries sorted by (key, instance) as host numpy (keys, vals)."""
+        n, _ = self.stats()
+        keys = torch.empty(max(n, 1), dtype=torch.uint64, device=self.mem.device)
+        vals = torch.empty(max(n, 1), dtype=torch.uint64, device=self.mem.device)
+        ws = self._workspace(self.evict_ws_bytes())
+        got = C.c_uint64()
+        _check("smetric_index_dump", _lib.smetric_index_dump(
+            self.ref, C.c_void_p(keys.data_ptr()), C.c_void_p(vals.data_ptr()), C.c_uint64(n),
+            C.c_void_p(ws.data_ptr()), ws.numel(), C.byref(got), _stream()))
+        assert int(got.value) == n
+        return keys[:n].cpu().numpy(), vals[:n].cpu().numpy()
+
+    def snapshot(self) -> torch.Tensor:
+        return self.mem.clone()
+
+    def restore(self, snap: torch.Tensor):
+        self.mem.copy_(snap)

@@ -1,0 +1,47 @@
+"""The C-ABI library loads on the CPU and exports every entry point include/*.h declares
+(no GPU work is launched)."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"^\s*(?:int|void|uint64_t|int32_t)\s+(smetric_\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
+
+
+def test_header_declares_the_hot_path_calls():
+    names = declared_symbols()
+    for must in ("smetric_hash_blocks", "smetric_match", "smetric_route", "smetric_index_insert",
+                 "smetric_index_evict"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2607_08565_amd import smetric as S
+    lib = ctypes.CDLL(S.LIB_PATH)
+    missing = [n for n in declared_symbols() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(S.EXPORTED) == set(declared_symbols())
+
+
+def test_host_side_errors_without_gpu():
+    from paper_2607_08565_amd import smetric as S
+    assert S.version() >= 1
+    with pytest.raises(S.SmetricError):
+        S.index_bytes(0, 8)
+    with pytest.raises(S.SmetricError):
+        S.index_bytes(100, 65537)
+    with pytest.raises(S.SmetricError):
+        S.block_offsets([0, 10], 15)
+    blk, nb = S.block_offsets([0, 15, 31, 100, 100], 16)
+    assert blk.tolist() == [0, 0, 1, 5, 5] and nb == 5
+    assert S.insert_ws_bytes(1000) > 16 * 1000

@@ -1,0 +1,241 @@
+"""GPU (HIP library, through the C ABI) vs the CPU oracle, element by element.
+
+Bit-exact for every block key, matched-prefix length, target, branch and the sorted
+index dump.  Sizes keep the oracle at seconds while spanning several 64-block tiles,
+ragged tails, shared prefixes held by more instances than a holder list keeps (bitmap
+records), pool exhaustion, eviction with orphaned descendants, and the degenerate cases
+(empty prompts, empty batches, one instance)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_08565_amd import workload as W
+from tests.parity import Pair, run_sessions, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu(dev):
+    yield
+
+
+def _rand_prompts(rng, n, lo, hi, vocab=W.VOCAB):
+    lens = rng.integers(lo, hi, n)
+    toks = rng.integers(0, vocab, int(lens.sum()), dtype=np.int32)
+    off = np.zeros(n + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    return toks, off
+
+
+@pytest.mark.parametrize("B", [16, 2, 8, 32, 256])
+def test_hash_parity_ragged(B):
+    rng = np.random.default_rng(B)
+    toks, off = _rand_prompts(rng, 37, 0, 5000)
+    # extremes: empty, one token short of a block, exactly one block, a multi-tile prompt
+    extra = [0, B - 1, B, 64 * B * 3 + B * 5 + 3]
+    for L in extra:
+        toks = np.concatenate([toks, rng.integers(-2**31, 2**31 - 1, L, dtype=np.int64).astype(np.int32)])
+        off = np.append(off, off[-1] + L)
+    pair = Pair(1024, 4, seed=int(rng.integers(0, 2**63)), block=B)
+    say(f"hash B={B} blocks={int((np.diff(off) // B).sum())}")
+    pair.hash_both(toks, off)
+
+
+def test_hash_long_prompt_many_tiles():
+    rng = np.random.default_rng(1)
+    toks, off = _rand_prompts(rng, 3, 131072 - 7, 131072 + 1)
+    Pair(16, 1).hash_both(toks, off)
+
+
+def test_hash_bad_offsets_flag_status_without_writing():
+    from paper_2607_08565_amd import smetric as S
+    toks = to_dev(np.arange(64, dtype=np.int32))
+    tok_off = to_dev(np.array([0, 32, 64], np.int64))
+    blk_off = to_dev(np.array([0, 3, 4], np.int64))  # request 0 claims 3 blocks of a 2-block prompt
+    keys = to_dev(np.full(4, 7, np.uint64))
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    S.hash_blocks(toks, tok_off, blk_off, 4, 16, 5, keys=keys, status=status)
+    got = keys.cpu().numpy()
+    assert int(status.item()) == S.EINVAL
+    assert got[:3].tolist() == [7, 7, 7]  # the bad request wrote nothing
+    _, ok = oracle.hash_blocks(np.arange(64, dtype=np.int32)[32:], [0, 32], 16, 5)
+    assert got[3] == ok[0]
+
+
+def test_config0_open_loop_full():
+    """configs[0] at full size: 8 instances, 64 sessions x 4 turns."""
+    pair, br = run_sessions(W.config0(), 4, capacity=200_000)
+    assert set(br.tolist()) >= {0, 2}
+
+
+def test_config1_scaled_closed_loop():
+    wl = W.config1(n_sess=192, n_turns=8, l0=1024, app=(64, 1536), cap=16384, prefix_len=512)
+    pair, br = run_sessions(wl, 8, capacity=2_000_000)
+    say("branches", np.bincount(br, minlength=5).tolist())
+
+
+def test_config2_scaled_prev_counts():
+    wl = W.config2(n_sess=48, n_turns=10, l0=4096, app=(128, 3000), cap=40000, prefix_len=2048)
+    run_sessions(wl, 10, capacity=2_000_000)
+
+
+def test_config3_scaled_with_eviction():
+    """One shared prefix held by every instance (bitmap records, WIDE alive sets of 128),
+    divergent tails, 5 % LRU eviction after every batch (orphaned descendants)."""
+    wl = W.config3(n_sess=160, n_turns=5, prefix_len=4096, tail=(256, 3000), app=512)
+    run_sessions(wl, 5, capacity=400_000, evict=(1, 20))
+
+
+def test_many_instances_wide_words():
+    """I = 5000 (two bitmap words per lane) and a prefix shared by 300 instances."""
+    rng = np.random.default_rng(5)
+    I = 5000
+    pre = rng.integers(0, W.VOCAB, 2048, dtype=np.int32)
+    pair = Pair(2_000_000, I)
+    prompts = [np.concatenate([pre[: rng.integers(100, 2048)], rng.integers(0, W.VOCAB, rng.integers(0, 900), dtype=np.int32)])
+               for _ in range(300)]
+    off = np.zeros(301, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    toks = np.concatenate(prompts)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+    inst = rng.choice(I, 300, replace=False).astype(np.int32)
+    assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, inst, np.arange(300), 1) == 0
+    pair.compare_index("insert")
+    q = np.concatenate([pre, rng.integers(0, W.VOCAB, 500, dtype=np.int32)])
+    batch = W.Batch(tokens=np.concatenate([q, q[:1000]]), tok_off=np.array([0, len(q), len(q) + 1000]),
+                    prompt_len=np.array([len(q), 1000], np.int32), hist_len=np.array([1024, 0], np.int32),
+                    turn=np.array([1, 0], np.int32), session=np.array([9, 10], np.uint32),
+                    q=rng.integers(0, 50, I) * W.Q_UNIT_NS, rr_base=17, epoch=2)
+    pair.step(batch, what="I=5000")
+
+
+def test_max_instances():
+    rng = np.random.default_rng(6)
+    I = 65536
+    pre = rng.integers(0, W.VOCAB, 512, dtype=np.int32)
+    pair = Pair(200_000, I)
+    R = 80
+    prompts = [np.concatenate([pre, rng.integers(0, W.VOCAB, 100, dtype=np.int32)]) for _ in range(R)]
+    off = np.zeros(R + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(np.concatenate(prompts), off)
+    inst = np.concatenate([rng.choice(I, R - 2, replace=False), [0, I - 1]]).astype(np.int32)
+    assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, inst, np.arange(R), 3) == 0
+    pair.compare_index("insert")
+    b = W.Batch(tokens=prompts[0][:600], tok_off=np.array([0, 600]), prompt_len=np.array([600], np.int32),
+                hist_len=np.array([512], np.int32), turn=np.array([1], np.int32), session=np.array([1], np.uint32),
+                q=np.zeros(I, np.int64), rr_base=0, epoch=4)
+    pair.step(b, what="I=65536")
+
+
+def test_hot_keys_pool_exhaustion_and_long_lists():
+    """More hot keys than bitmap records: the rest keep long plain holder lists."""
+    rng = np.random.default_rng(7)
+    I, R = 16, 12 * 16
+    pair = Pair(3000, I)  # 64 records only
+    streams = [rng.integers(0, W.VOCAB, 16 * 150, dtype=np.int32) for _ in range(12)]
+    prompts = [streams[r % 12][: 16 * rng.integers(100, 150)] for r in range(R)]
+    off = np.zeros(R + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(np.concatenate(prompts), off)
+    inst = np.array([r // 12 for r in range(R)], np.int32)  # each stream on all 16 instances
+    assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, inst, np.arange(R), 1) == 0
+    pair.compare_index("insert")
+    b = W.Batch(tokens=np.concatenate(streams[:4]), tok_off=np.arange(5) * 16 * 150,
+                prompt_len=np.full(4, 2400, np.int32), hist_len=np.full(4, 1600, np.int32),
+                turn=np.ones(4, np.int32), session=np.arange(4, dtype=np.uint32), q=np.zeros(I, np.int64), epoch=2)
+    pair.step(b, what="hot")
+
+
+def test_duplicate_pairs_in_batch_take_lowest_request():
+    rng = np.random.default_rng(8)
+    pair = Pair(10_000, 4)
+    p = rng.integers(0, W.VOCAB, 800, dtype=np.int32)
+    prompts = [p[:800], p[:400], p[:800], p[:640]]
+    off = np.zeros(5, np.int64)
+    off[1:] = np.cumsum([len(x) for x in prompts])
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(np.concatenate(prompts), off)
+    assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, [2, 2, 2, 1], [50, 40, 30, 20], 5) == 0
+    pair.compare_index("dups")
+    assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, [2, 3, 2, 1], [9, 8, 7, 6], 3) == 0
+    pair.compare_index("older epoch")
+
+
+def test_efull_and_einval_leave_index_unchanged():
+    rng = np.random.default_rng(9)
+    pair = Pair(100, 3)
+    toks, off = _rand_prompts(rng, 4, 300, 700)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+    half = np.array([0, nb // 2])
+    rc = pair.insert_both(d_keys, to_dev(half), nb, okeys, half, [1], [1], 1)
+    assert rc == 0
+    pair.compare_index("first")
+    rc = pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, [0, 1, 2, 0], [1, 2, 3, 4], 2)
+    assert rc == oracle.EFULL
+    pair.compare_index("efull")
+    # instance out of range -> EINVAL, unchanged (status stays the first error: EFULL)
+    rc = pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, [0, 5, 1, 1], [1, 2, 3, 4], 3)
+    assert rc == oracle.EINVAL
+    pair.compare_index("einval")
+    _, st = pair.gix.stats(reset_status=True)
+    assert st == oracle.EFULL and pair.gix.stats()[1] == 0
+
+
+def test_match_bad_range_and_empty_requests():
+    rng = np.random.default_rng(10)
+    pair = Pair(10_000, 5)
+    toks, off = _rand_prompts(rng, 3, 200, 400)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+    pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, [0, 1, 2], [1, 2, 3], 1)
+    bad = np.array([0, blk_off[1], blk_off[1] - 1, nb, nb], np.int64)  # request 1 decreasing, 3 empty
+    gm = pair.gix.match(d_keys, to_dev(bad), nb).cpu().numpy()
+    om = pair.oix.match(okeys, bad, nb)
+    assert np.array_equal(gm, om)
+    assert pair.gix.stats()[1] == oracle.EINVAL == pair.oix.status
+
+
+def test_empty_batch_and_single_instance():
+    from paper_2607_08565_amd import smetric as S
+    pair = Pair(1000, 1)
+    b = W.Batch(tokens=np.zeros(0, np.int32), tok_off=np.zeros(1, np.int64), prompt_len=np.zeros(0, np.int32),
+                hist_len=np.zeros(0, np.int32), turn=np.zeros(0, np.int32), session=np.zeros(0, np.uint32),
+                q=np.zeros(1, np.int64))
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(b.tokens, b.tok_off)
+    assert nb == 0
+    rng = np.random.default_rng(11)
+    toks, off = _rand_prompts(rng, 5, 0, 100)
+    b = W.Batch(tokens=toks, tok_off=off, prompt_len=np.diff(off).astype(np.int32), hist_len=np.zeros(5, np.int32),
+                turn=np.array([0, 1, 2, 0, 1], np.int32), session=np.arange(5, dtype=np.uint32), q=np.array([7], np.int64))
+    pair.step(b, what="I=1 a")
+    pair.step(b, what="I=1 b")
+    assert S.version() >= 1
+
+
+def test_route_edge_parameters():
+    """SLACK = inf / 0, HIT_RATIO 0, c_att = 0, and out-of-domain requests (branch 255)."""
+    rng = np.random.default_rng(12)
+    R, I = 300, 40
+    m = rng.integers(0, 60, (R, I)).astype(np.int32)
+    L = rng.integers(0, 1200, R).astype(np.int32)
+    m = np.minimum(m, (L // 16)[:, None]).astype(np.int32)
+    m[5, 3] = -1
+    m[6, 0] = L[6] // 16 + 1
+    hist = rng.integers(0, 1200, R).astype(np.int32)
+    hist[7] = -1
+    turn = rng.integers(0, 3, R).astype(np.int32)
+    turn[8] = -2
+    L[9] = -5
+    q = rng.integers(0, 200, I).astype(np.int64) * W.Q_UNIT_NS
+    from paper_2607_08565_amd import smetric as S
+    for over in ({}, dict(slack_num=0, slack_den=0), dict(slack_num=0, slack_den=1), dict(hit_num=0, hit_den=7),
+                 dict(c_att=0, c_lin=1), dict(slack_num=3, slack_den=2, c_att=4)):
+        p = dict(W.DEFAULT_PARAMS, **over)
+        for rr in (0, 123456789):
+            gt, gb = S.route(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), p, rr)
+            ot, ob = oracle.route(m, L, hist, turn, q, p, rr)
+            assert np.array_equal(gt.cpu().numpy(), ot) and np.array_equal(gb.cpu().numpy(), ob), over
+    assert set(ob[[5, 6, 7, 8, 9]].tolist()) == {255}
+    with pytest.raises(S.SmetricError):
+        S.route(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), dict(W.DEFAULT_PARAMS, hit_num=2, hit_den=2))
