@@ -1,0 +1,299 @@
+"""Benchmark: one step = hash -> match -> route -> insert over one routing batch.
+
+Workload (the throughput configuration): 1,024 instances, 16,384 requests per batch,
+prompt lengths lognormal(median 24,576, sigma 0.6) clipped to [1,024, 131,072], 70 % of
+each prompt's blocks being its session's prior turn (placed on a home instance before
+the run), 64 shared 4,096-token prefixes chosen Zipf(1.2), loads Poisson(50) x 20 ms,
+and an index padded with never-matching filler entries to ~200M entries.  Every timed
+step routes a batch of distinct sessions, so all steps have the same statistics; the
+tokens of every batch are resident in HBM before timing starts.
+
+Prints one JSON line (see the fields at the end of main()).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "requests routed/sec + prompt tokens matched/sec; achieved HBM GB/s vs peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=6)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--n-req", type=int, default=16384)
+    ap.add_argument("--n-inst", type=int, default=1024)
+    ap.add_argument("--index-entries", type=int, default=200_000_000, help="entries at the start of timing")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle time budget for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM bytes per launch (rocprofv3 FETCH_SIZE/WRITE_SIZE), if present")
+    return ap.parse_args()
+
+
+class Setup:
+    """Resident inputs, the pre-populated index and reusable output buffers."""
+
+    def __init__(self, args):
+        import torch
+
+        from paper_2607_08565_amd import smetric as S
+        from paper_2607_08565_amd import workload as W
+
+        self.S, self.W, self.torch = S, W, torch
+        self.args = args
+        self.n_batches = args.warmup + args.steps
+        self.tw = W.ThroughputWorkload(n_req=args.n_req, n_inst=args.n_inst)
+        t0 = time.time()
+        self.host = [self.tw.batch(b) for b in range(self.n_batches)]
+        log(f"[setup] generated {self.n_batches} batches in {time.time() - t0:.1f}s")
+        self.dev = []
+        for tb in self.host:
+            b = tb.batch
+            blk_off, nb = S.block_offsets(b.tok_off)
+            self.dev.append(dict(
+                tokens=torch.from_numpy(b.tokens).cuda(), tok_off=torch.from_numpy(b.tok_off).cuda(),
+                blk_off=torch.from_numpy(blk_off).cuda(), blk_off_h=blk_off, n_blocks=nb,
+                prompt_len=torch.from_numpy(b.prompt_len).cuda(), hist_len=torch.from_numpy(b.hist_len).cuda(),
+                turn=torch.from_numpy(b.turn).cuda(), session=torch.from_numpy(b.session).cuda(),
+                q=torch.from_numpy(b.q).cuda()))
+        max_blocks = max(d["n_blocks"] for d in self.dev)
+        self.keys = torch.empty(max_blocks, dtype=torch.uint64, device="cuda")
+        self.matched = torch.empty((args.n_req, args.n_inst), dtype=torch.int32, device="cuda")
+        self.target = torch.empty(args.n_req, dtype=torch.int32, device="cuda")
+        self.branch = torch.empty(args.n_req, dtype=torch.uint8, device="cuda")
+        self.ws = torch.empty(S.insert_ws_bytes(max_blocks), dtype=torch.uint8, device="cuda")
+        # index: the prior turns of every batch's sessions, then filler
+        growth = 30_000_000 * self.n_batches
+        self.capacity = args.index_entries + growth
+        self.index = S.Index(self.capacity, args.n_inst)
+        t0 = time.time()
+        for b, (tb, d) in enumerate(zip(self.host, self.dev)):
+            self._prepopulate(tb, d)
+        n, st = self.index.stats()
+        assert st == 0, f"index status {st} after prior turns"
+        self.prior_entries = n
+        self._filler(max(args.index_entries - n, 0))
+        n, st = self.index.stats()
+        assert st == 0, f"index status {st} after filler"
+        self.start_entries = n
+        log(f"[setup] index: {self.prior_entries} prior-turn entries + filler = {n} entries "
+            f"({self.index.mem.numel() / 2**30:.2f} GiB, capacity {self.capacity}) in {time.time() - t0:.1f}s")
+
+    def _prepopulate(self, tb, d):
+        torch, S = self.torch, self.S
+        keys = S.hash_blocks(d["tokens"], d["tok_off"], d["blk_off"], d["n_blocks"], keys=self.keys)
+        prior_blocks = (tb.prior_len // self.W.BLOCK).astype(np.int64)
+        starts = d["blk_off_h"][:-1]
+        pos = np.repeat(starts - np.concatenate([[0], np.cumsum(prior_blocks)[:-1]]), prior_blocks) + np.arange(
+            int(prior_blocks.sum()))
+        pk = keys.view(torch.int64)[torch.from_numpy(pos).cuda()].view(torch.uint64).contiguous()
+        poff = np.zeros(len(prior_blocks) + 1, np.int64)
+        poff[1:] = np.cumsum(prior_blocks)
+        self.index.insert(pk, torch.from_numpy(poff).cuda(), int(poff[-1]), torch.from_numpy(tb.home).cuda(),
+                          d["session"], 0, workspace=self.ws)
+
+    def _filler(self, n: int):
+        torch = self.torch
+        per = 64
+        chunk = 16_000_000
+        done, c = 0, 0
+        while done < n:
+            m = min(chunk, n - done)
+            m -= m % per if m >= per else 0
+            m = max(m, 1)
+            keys, inst, sess = self.tw.filler(m, chunk=c)
+            R = (m + per - 1) // per
+            off = np.minimum(np.arange(R + 1, dtype=np.int64) * per, m)
+            self.index.insert(torch.from_numpy(keys).cuda(), torch.from_numpy(off).cuda(), m,
+                              torch.from_numpy(inst[::per][:R].copy()).cuda(),
+                              torch.from_numpy(sess[:R].copy()).cuda(), 0, workspace=self.ws)
+            done += m
+            c += 1
+
+    def step(self, b: int, ev=None):
+        """The timed unit: all four calls on the current stream."""
+        S, d, tb = self.S, self.dev[b], self.host[b]
+        rec = (lambda k: ev[k].record()) if ev is not None else (lambda k: None)
+        rec(0)
+        S.hash_blocks(d["tokens"], d["tok_off"], d["blk_off"], d["n_blocks"], keys=self.keys)
+        rec(1)
+        self.index.match(self.keys, d["blk_off"], d["n_blocks"], matched=self.matched)
+        rec(2)
+        S.route(self.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], self.W.DEFAULT_PARAMS,
+                tb.batch.rr_base, target=self.target, branch=self.branch)
+        rec(3)
+        self.index.insert(self.keys, d["blk_off"], d["n_blocks"], self.target, d["session"], tb.batch.epoch,
+                          workspace=self.ws)
+        rec(4)
+
+
+def algorithmic_bytes(setup, b, matched, I):
+    """Bytes the method itself must move for batch b (see the design notes):
+    hash: 4 B per token read + 8 B per block key written;
+    match: per probed block 8 B key + one 64 B bucket burst, I/8 B of holder bitmap per
+    probed block of a widely shared prefix, 4 B per (request, instance) written."""
+    tb = setup.host[b]
+    bt = tb.batch
+    n_tok = int(bt.tok_off[-1])
+    n_blk = int(setup.dev[b]["n_blocks"])
+    nb = np.diff(setup.dev[b]["blk_off_h"])
+    cmax = matched.max(axis=1)
+    probes = np.minimum(cmax + 1, nb)  # blocks up to and including the first block nobody holds
+    hot = np.minimum(probes, np.minimum(256, nb))  # blocks of the shared 4,096-token prefix
+    R = len(nb)
+    hash_b = 4 * n_tok + 8 * n_blk
+    match_b = int(probes.sum()) * (8 + 64) + int(hot.sum()) * (I // 8) + 4 * R * I
+    return dict(tokens=n_tok, blocks=n_blk, probes=int(probes.sum()), hot_probes=int(hot.sum()),
+                hash=hash_b, match=match_b, route=4 * R * I + 8 * I + 12 * R + 5 * R)
+
+
+def cpu_baseline(setup, budget_s: float, gpu_out):
+    """The oracle, as it stands, on a bounded sample of batch 0: the first n requests,
+    against the exact restriction of the index to their keys (their own prior turns and
+    every prior turn's copy of the shared prefixes they use; filler never matches).
+    Also checks the GPU's batch-0 outputs for those requests bit for bit."""
+    import oracle
+
+    W = setup.W
+    tw, hosts = setup.tw, setup.host
+    tb0 = hosts[0]
+    b0 = tb0.batch
+    params = W.DEFAULT_PARAMS
+    prefix_len = len(tw.prefixes[0])
+
+    def run(n):
+        R = n
+        toks = b0.tokens[: b0.tok_off[R]]
+        tok_off = b0.tok_off[: R + 1]
+        ix = oracle.Index(1 << 40, tw.n_inst)
+        # shared prefixes used by the sample, held by every session placed with them
+        used = set(tb0.prefix_of[:R].tolist())
+        for p in sorted(used):
+            pre = tw.prefixes[p]
+            pb, pk = oracle.hash_blocks(pre, [0, len(pre)], W.BLOCK, W.DEFAULT_SEED)
+            for tb in hosts:
+                sel = np.nonzero(tb.prefix_of == p)[0]
+                for s in sel:
+                    m = int(min(tb.prior_len[s], prefix_len) // W.BLOCK)
+                    m = min(m, int(tb.batch.prompt_len[s]) // W.BLOCK)
+                    if m:
+                        ix.insert(pk[:m], [0, m], [tb.home[s]], [tb.batch.session[s]], 0)
+        # the sample's own prior turns
+        blk_off, keys = oracle.hash_blocks(toks, tok_off, W.BLOCK, W.DEFAULT_SEED)
+        prior = (tb0.prior_len[:R] // W.BLOCK).astype(np.int64)
+        pos = np.concatenate([np.arange(blk_off[r], blk_off[r] + prior[r]) for r in range(R)])
+        poff = np.zeros(R + 1, np.int64)
+        poff[1:] = np.cumsum(prior)
+        ix.insert(keys[pos], poff, tb0.home[:R], b0.session[:R], 0)
+        # timed: hash + match + route + insert, exactly the GPU step's work for n requests
+        t0 = time.perf_counter()
+        blk_off, keys = oracle.hash_blocks(toks, tok_off, W.BLOCK, W.DEFAULT_SEED)
+        m = ix.match(keys, blk_off)
+        tgt, br = oracle.route(m, b0.prompt_len[:R], b0.hist_len[:R], b0.turn[:R], b0.q, params, b0.rr_base)
+        ix.insert(keys, blk_off, tgt, b0.session[:R], b0.epoch)
+        dt = time.perf_counter() - t0
+        return dt, keys, m, tgt, br
+
+    dt, *_ = run(8)
+    n = int(max(8, min(setup.args.n_req, 8 * budget_s / max(dt, 1e-6))))
+    dt, keys, m, tgt, br = run(n)
+    g_keys, g_m, g_t, g_b = gpu_out
+    nk = len(keys)
+    parity = (np.array_equal(g_keys[:nk], keys) and np.array_equal(g_m[:n], m) and np.array_equal(g_t[:n], tgt)
+              and np.array_equal(g_b[:n], br))
+    return dict(value=n / dt, unit="requests/s", cores=1, kind="oracle",
+                sample=f"first {n} requests of batch 0 (of {setup.args.n_req}), hash+match+route+insert, "
+                       f"index restricted to their keys, single thread, {dt:.1f} s"), parity, n
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the matching/routing path is "
+                                   "not sharded across GPUs in this build (pass --gpus 1)"}))
+        sys.exit(2)
+    import torch
+
+    torch.cuda.set_device(0)
+    setup = Setup(args)
+    S = setup.S
+    # warmup (untimed); batch 0's outputs are kept for the sampled oracle check
+    gpu_out = None
+    for b in range(args.warmup):
+        setup.step(b)
+        if b == 0:
+            torch.cuda.synchronize()
+            nb0 = setup.dev[0]["n_blocks"]
+            gpu_out = (setup.keys[:nb0].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
+                       setup.branch.cpu().numpy())
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    mats = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        setup.step(args.warmup + k, evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    names = ["hash", "match", "route", "insert"]
+    per = {n: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
+           for i, n in enumerate(names)}
+    n, st = setup.index.stats()
+    assert st == 0, f"index status {st}"
+    # algorithmic bytes for the last timed batch (match outputs still in the buffer)
+    last = args.warmup + args.steps - 1
+    alg = algorithmic_bytes(setup, last, setup.matched.cpu().numpy(), args.n_inst)
+    R = args.n_req
+    tokens = float(np.mean([setup.host[args.warmup + k].batch.n_tokens for k in range(args.steps)]))
+    ms_step = wall * 1e3 / args.steps
+    gbs = {"hash": alg["hash"] / per["hash"] / 1e6, "match": alg["match"] / per["match"] / 1e6}
+    dominant = max(("hash", "match", "route"), key=lambda k: per[k])
+    traffic = None
+    if os.path.exists(args.traffic):
+        tr = json.load(open(args.traffic))
+        traffic = tr.get(dominant)
+    roof = {"bound": "hbm", "kernel": dominant, "achieved": round(gbs.get(dominant, 0.0), 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(gbs.get(dominant, 0.0) / HBM_PEAK_GBS, 4), "traffic": traffic}
+    path_gbs = (alg["hash"] + alg["match"]) / (per["hash"] + per["match"]) / 1e6
+    out = {
+        "metric": METRIC, "value": round(R / (ms_step / 1e3), 1), "unit": "requests/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": f"throughput: {args.n_inst} instances, {R} requests/batch, lognormal(24576, 0.6) "
+                               f"prompts in [1024, 131072], 70% prior-turn blocks, 64 Zipf(1.2) 4096-token prefixes, "
+                               f"{setup.start_entries} index entries at start",
+                   "n_instances": args.n_inst, "requests_per_batch": R, "block_size": 16,
+                   "index_entries_start": setup.start_entries, "index_entries_end": n,
+                   "index_capacity": setup.capacity, "tokens_per_batch": int(tokens)},
+        "prompt_tokens_matched_per_s": round(tokens / ((per["hash"] + per["match"]) / 1e3), 1),
+        "kernel_ms": {k: round(v, 4) for k, v in per.items()},
+        "algorithmic_GBs": {k: round(v, 1) for k, v in gbs.items()},
+        "hash_probe_path": {"GBs": round(path_gbs, 1), "frac_of_peak": round(path_gbs / HBM_PEAK_GBS, 4),
+                            "bytes": alg["hash"] + alg["match"], "probes": alg["probes"]},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        cb, parity, n_s = cpu_baseline(setup, args.cpu_seconds, gpu_out)
+        out["cpu_baseline"] = cb
+        out["sampled_parity"] = {"requests": n_s, "bit_exact": bool(parity)}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

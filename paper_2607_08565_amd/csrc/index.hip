@@ -490,7 +490,8 @@ __global__ void set_counts_kernel(IndexHdr *h, unsigned long long n_entries) {
 
 struct EvictWs {
   unsigned long long *count;  // 2 counters
-  uint64_t *ka, *va, *kb, *vb;
+  uint64_t *ka, *va, *kb, *vb;  // entries and their sort ping-pong buffers
+  uint64_t *ea, *eb, *ia, *ib;  // epoch sort keys and the permutation they carry
   void *temp;
   size_t temp_bytes;
 };
@@ -512,7 +513,8 @@ uint64_t evict_ws_layout(uint64_t cap, EvictWs *ws, void *base) {
     return o;
   };
   const uint64_t o_cnt = take(256), o_ka = take(8 * n), o_va = take(8 * n), o_kb = take(8 * n),
-                 o_vb = take(8 * n), o_tmp = take(tb);
+                 o_vb = take(8 * n), o_ea = take(8 * n), o_eb = take(8 * n), o_ia = take(8 * n),
+                 o_ib = take(8 * n), o_tmp = take(tb);
   if (ws) {
     char *b = static_cast<char *>(base);
     ws->count = reinterpret_cast<unsigned long long *>(b + o_cnt);
@@ -520,6 +522,10 @@ uint64_t evict_ws_layout(uint64_t cap, EvictWs *ws, void *base) {
     ws->va = reinterpret_cast<uint64_t *>(b + o_va);
     ws->kb = reinterpret_cast<uint64_t *>(b + o_kb);
     ws->vb = reinterpret_cast<uint64_t *>(b + o_vb);
+    ws->ea = reinterpret_cast<uint64_t *>(b + o_ea);
+    ws->eb = reinterpret_cast<uint64_t *>(b + o_eb);
+    ws->ia = reinterpret_cast<uint64_t *>(b + o_ia);
+    ws->ib = reinterpret_cast<uint64_t *>(b + o_ib);
     ws->temp = b + o_tmp;
     ws->temp_bytes = tb;
   }
@@ -531,9 +537,31 @@ int read_hdr(const smetric_index *idx, IndexHdr *out, hipStream_t s) {
   return hip_rc(hipStreamSynchronize(s));
 }
 
+__global__ void epoch_keys_kernel(const uint64_t *vals, uint64_t *ep, uint64_t *idx, uint64_t n) {
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+    ep[i] = val_epoch(vals[i]);
+    idx[i] = i;
+  }
+}
+
+__global__ void permute_kernel(const uint64_t *keys, const uint64_t *vals, const uint64_t *idx, uint64_t *keys_out,
+                               uint64_t *vals_out, uint64_t n) {
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint64_t j = idx[i];
+    keys_out[i] = keys[j];
+    vals_out[i] = vals[j];
+  }
+}
+
 // Gather all entries and sort them by (key, instance), or by (epoch, key, instance) when
-// by_epoch.  Stable LSD passes: instance, then key, then (optionally) epoch.  On return
-// the sorted keys/values are in (*keys_out, *vals_out).
+// by_epoch.  Stable LSD radix passes, each over the full 64-bit sort word (restricting a
+// pass to a bit range gave wrong orders for some inputs with the installed rocPRIM):
+//   1) by the value word (instance << 48 | epoch << 24 | session);
+//   2) stably by key -- (key, instance) is unique, so this is (key, instance) order;
+//   3) (by_epoch) stably by epoch, carrying the permutation, then a gather.
+// On return the sorted keys/values are in (*keys_out, *vals_out).
 int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, bool by_epoch, uint64_t **keys_out,
                   uint64_t **vals_out, hipStream_t s) {
   const DevIndex ix = dev_view(idx);
@@ -546,29 +574,27 @@ int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, bool 
   if (hipMemcpyAsync(&got, ws.count, 8, hipMemcpyDeviceToHost, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
     return SMETRIC_EHIP;
   if (got != n) return SMETRIC_EINTERNAL;
-  if (n > 1) {
-    size_t tb = ws.temp_bytes;
-    hipcub::DoubleBuffer<uint64_t> vk(ws.va, ws.vb), kv(ws.ka, ws.kb);
-    // 1) by instance (value bits 48..63)
-    if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, vk, kv, int(n), 48, 64, s) != hipSuccess) return SMETRIC_EHIP;
-    // 2) stably by key
-    hipcub::DoubleBuffer<uint64_t> k2(kv.Current(), kv.Alternate()), v2(vk.Current(), vk.Alternate());
-    if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, k2, v2, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
-    if (by_epoch) {
-      // 3) stably by epoch (value bits 24..45)
-      hipcub::DoubleBuffer<uint64_t> v3(v2.Current(), v2.Alternate()), k3(k2.Current(), k2.Alternate());
-      if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, v3, k3, int(n), 24, 46, s) != hipSuccess) return SMETRIC_EHIP;
-      *keys_out = k3.Current();
-      *vals_out = v3.Current();
-    } else {
-      *keys_out = k2.Current();
-      *vals_out = v2.Current();
-    }
-  } else {
-    *keys_out = ws.ka;
-    *vals_out = ws.va;
-  }
-  return SMETRIC_OK;
+  *keys_out = ws.ka;
+  *vals_out = ws.va;
+  if (n <= 1) return SMETRIC_OK;
+  size_t tb = ws.temp_bytes;
+  hipcub::DoubleBuffer<uint64_t> vk(ws.va, ws.vb), kv(ws.ka, ws.kb);
+  if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, vk, kv, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
+  hipcub::DoubleBuffer<uint64_t> k2(kv.Current(), kv.Alternate()), v2(vk.Current(), vk.Alternate());
+  tb = ws.temp_bytes;
+  if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, k2, v2, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
+  *keys_out = k2.Current();
+  *vals_out = v2.Current();
+  if (!by_epoch) return SMETRIC_OK;
+  hipLaunchKernelGGL(epoch_keys_kernel, dim3(grid_for(n)), dim3(TB), 0, s, v2.Current(), ws.ea, ws.ia, n);
+  hipcub::DoubleBuffer<uint64_t> e(ws.ea, ws.eb), x(ws.ia, ws.ib);
+  tb = ws.temp_bytes;
+  if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, e, x, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
+  hipLaunchKernelGGL(permute_kernel, dim3(grid_for(n)), dim3(TB), 0, s, k2.Current(), v2.Current(), x.Current(),
+                     k2.Alternate(), v2.Alternate(), n);
+  *keys_out = k2.Alternate();
+  *vals_out = v2.Alternate();
+  return hip_rc(hipGetLastError());
 }
 
 }  // namespace
@@ -674,7 +700,7 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   if ((rc = fill(ix.pool, ix.n_records * uint64_t(ix.words) * 8, 0, stream))) return rc;
   hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m));
   // the alternate sort buffers are free now: one holds the conversion queue
-  uint64_t *trig = (keys == ws.ka) ? ws.kb : ws.ka;
+  uint64_t *trig = ws.ea;  // free once the sorted entries are in place
   unsigned long long *n_trig = ws.count + 1;
   hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n - m)), dim3(TB), 0, stream, ix, keys, vals, m, n, trig,
                      n_trig);
