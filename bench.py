@@ -77,7 +77,8 @@ class Setup:
         self.matched = torch.empty((args.n_req, args.n_inst), dtype=torch.int32, device="cuda")
         self.target = torch.empty(args.n_req, dtype=torch.int32, device="cuda")
         self.branch = torch.empty(args.n_req, dtype=torch.uint8, device="cuda")
-        self.ws = torch.empty(S.insert_ws_bytes(max_blocks), dtype=torch.uint8, device="cuda")
+        self.filler_chunk = 16_000_000
+        self.ws = torch.empty(S.insert_ws_bytes(max(max_blocks, self.filler_chunk)), dtype=torch.uint8, device="cuda")
         # index: the prior turns of every batch's sessions, then filler
         growth = 30_000_000 * self.n_batches
         self.capacity = args.index_entries + growth
@@ -111,7 +112,7 @@ class Setup:
     def _filler(self, n: int):
         torch = self.torch
         per = 64
-        chunk = 16_000_000
+        chunk = self.filler_chunk
         done, c = 0, 0
         while done < n:
             m = min(chunk, n - done)
