@@ -91,6 +91,27 @@ __device__ inline void set_status(IndexHdr *h, int err) {
   atomicCAS(&h->status, 0, err);
 }
 
+// The 8 keys of bucket b, read as four 16-byte vectors, and the masks of slots equal to
+// `key` and of EMPTY slots.  Within a bucket occupied slots form a prefix (claims take
+// the first EMPTY slot of a chain and slots never become EMPTY again), so `match`
+// is restricted to the slots before the first EMPTY one.
+struct BucketScan {
+  uint32_t match, empty;
+};
+__device__ __forceinline__ BucketScan scan_bucket(const uint64_t *bk, uint64_t key) {
+  const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(bk);
+  BucketScan r{0, 0};
+#pragma unroll
+  for (int i = 0; i < SLOTS / 2; ++i) {
+    const ulonglong2 v = p[i];
+    r.match |= (uint32_t(v.x == key) << (2 * i)) | (uint32_t(v.y == key) << (2 * i + 1));
+    r.empty |= (uint32_t(v.x == KEY_EMPTY) << (2 * i)) | (uint32_t(v.y == KEY_EMPTY) << (2 * i + 1));
+  }
+  if (r.empty) r.match &= (r.empty & (0u - r.empty)) - 1u;
+  return r;
+}
+__device__ __forceinline__ uint64_t next_bucket(uint64_t b, uint64_t n) { return b + 1 == n ? 0 : b + 1; }
+
 // Sizing shared by host code.
 inline int32_t bitmap_words_for(int32_t n_inst) { return (n_inst + 63) / 64; }
 inline int32_t threshold_for(int32_t n_inst) {

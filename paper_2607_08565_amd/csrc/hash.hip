@@ -111,7 +111,7 @@ __device__ __forceinline__ bool request_ok(const int64_t *tok_off, const int64_t
          nb == (t1 - t0) / B;
 }
 
-constexpr int WAVES = 4;
+constexpr int WAVES = 1;
 
 // B = 16 fast path.
 __global__ __launch_bounds__(64 * WAVES) void hash16_kernel(const int32_t *__restrict__ tokens,

@@ -114,79 +114,99 @@ struct Found {
 };
 
 // Find the entry (key, inst), looking through a bitmap record when the key has one.
+__device__ Found find_member(const DevIndex &ix, uint64_t key, uint32_t inst) {
+  uint64_t m = member_bucket(key, inst, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step, m = next_bucket(m, ix.n_buckets)) {
+    const uint64_t *mk = ix.slots + m * BUCKET_WORDS;
+    const BucketScan sc = scan_bucket(mk, key);
+    uint32_t mm = sc.match;
+    while (mm) {
+      const int t = __builtin_ctz(mm);
+      mm &= mm - 1;
+      const uint64_t v = mk[SLOTS + t];
+      if (val_kind(v) == MEMBER && val_inst(v) == inst) return Found{int64_t(m * SLOTS + t), v};
+    }
+    if (sc.empty) break;
+  }
+  return Found{-1, 0};
+}
+
 __device__ Found find_entry(const DevIndex &ix, uint64_t key, uint32_t inst) {
   uint64_t b = home_bucket(key, ix.n_buckets);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
+  for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
     const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
-    for (int s = 0; s < SLOTS; ++s) {
-      const uint64_t k = bk[s];
-      if (k == KEY_EMPTY) return Found{-1, 0};
-      if (k != key) continue;
+    const BucketScan sc = scan_bucket(bk, key);
+    uint32_t mm = sc.match;
+    while (mm) {
+      const int s = __builtin_ctz(mm);
+      mm &= mm - 1;
       const uint64_t v = bk[SLOTS + s];
       const uint32_t kind = val_kind(v);
       if (kind == PLAIN && val_inst(v) == inst) return Found{int64_t(b * SLOTS + s), v};
       if (kind == HEADER) {
         const uint64_t w = ix.pool[val_rec(v) * uint64_t(ix.words) + (inst >> 6)];
         if (!((w >> (inst & 63)) & 1)) return Found{-1, 0};
-        uint64_t m = member_bucket(key, inst, ix.n_buckets);
-        for (uint64_t st2 = 0; st2 < ix.n_buckets; ++st2) {
-          const uint64_t *mk = ix.slots + m * BUCKET_WORDS;
-          for (int t = 0; t < SLOTS; ++t) {
-            const uint64_t k2 = mk[t];
-            if (k2 == KEY_EMPTY) return Found{-1, 0};
-            if (k2 != key) continue;
-            const uint64_t v2 = mk[SLOTS + t];
-            if (val_kind(v2) == MEMBER && val_inst(v2) == inst) return Found{int64_t(m * SLOTS + t), v2};
-          }
-          m = (m + 1 == ix.n_buckets) ? 0 : m + 1;
-        }
-        return Found{-1, 0};
+        return find_member(ix, key, inst);
       }
     }
-    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+    if (sc.empty) break;
   }
   return Found{-1, 0};
-}
-
-// Claim the first EMPTY slot of the chain starting at bucket b.  `same` counts slots
-// holding `key` seen before the claimed one.  Returns the slot or -1 if none.
-__device__ int64_t claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, uint32_t &same) {
-  same = 0;
-  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
-    uint64_t *bk = ix.slots + b * BUCKET_WORDS;
-    for (int s = 0; s < SLOTS; ++s) {
-      uint64_t k = __hip_atomic_load(&bk[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (k == KEY_EMPTY) {
-        k = atomicCAS(reinterpret_cast<unsigned long long *>(&bk[s]), KEY_EMPTY, key);
-        if (k == KEY_EMPTY) return int64_t(b * SLOTS + s);
-      }
-      if (k == key) ++same;
-    }
-    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
-  }
-  return -1;
 }
 
 __device__ __forceinline__ uint64_t *val_ptr(const DevIndex &ix, int64_t slot) {
   return ix.slots + (slot / SLOTS) * BUCKET_WORDS + SLOTS + (slot % SLOTS);
 }
-__device__ __forceinline__ uint64_t *key_ptr(const DevIndex &ix, int64_t slot) {
-  return ix.slots + (slot / SLOTS) * BUCKET_WORDS + (slot % SLOTS);
-}
 
-// Find whether `key` has a bitmap record (its HEADER lies before the chain's first EMPTY).
-__device__ int64_t find_header(const DevIndex &ix, uint64_t key) {
-  uint64_t b = home_bucket(key, ix.n_buckets);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
-    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
-    for (int s = 0; s < SLOTS; ++s) {
-      const uint64_t k = __hip_atomic_load(&bk[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (k == KEY_EMPTY) return -1;
-      if (k == key && val_kind(bk[SLOTS + s]) == HEADER) return int64_t(b * SLOTS + s);
+// Walk the chain from bucket b and claim its first EMPTY slot for `key`.  With
+// want_header, stop instead at a HEADER slot of `key` (the key has a bitmap record).
+// `same` counts slots holding `key` ahead of the claimed one.  Plain loads may see a
+// stale EMPTY; the compare-and-swap then fails and returns the slot's real key, and
+// slots never return to EMPTY, so the count is exact.
+struct Claim {
+  int64_t slot;    // claimed slot, or -1
+  int64_t header;  // HEADER slot of key when found, else -1
+  uint32_t same;
+};
+__device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool want_header) {
+  Claim c{-1, -1, 0};
+  for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
+    uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    const BucketScan sc = scan_bucket(bk, key);
+    if (want_header) {
+      uint32_t mm = sc.match;
+      while (mm) {
+        const int s = __builtin_ctz(mm);
+        mm &= mm - 1;
+        if (val_kind(bk[SLOTS + s]) == HEADER) {
+          c.header = int64_t(b * SLOTS + s);
+          return c;
+        }
+      }
     }
-    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
+    if (!sc.empty) {
+      c.same += __popc(sc.match);
+      continue;
+    }
+    // slots before the first EMPTY are final; try the EMPTY ones in order
+    const int first = __builtin_ctz(sc.empty);
+    c.same += __popc(sc.match & ((1u << first) - 1u));
+    for (int s = first; s < SLOTS; ++s) {
+      const uint64_t k = atomicCAS(reinterpret_cast<unsigned long long *>(&bk[s]), KEY_EMPTY, key);
+      if (k == KEY_EMPTY) {
+        c.slot = int64_t(b * SLOTS + s);
+        return c;
+      }
+      if (k == key) {
+        if (want_header && val_kind(__hip_atomic_load(&bk[SLOTS + s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == HEADER) {
+          c.header = int64_t(b * SLOTS + s);  // cannot happen: headers predate this kernel
+          return c;
+        }
+        ++c.same;
+      }
+    }
   }
-  return -1;
+  return c;
 }
 
 // Enter a distinct new entry.  Returns false only if the table has no free slot.
@@ -194,21 +214,19 @@ __device__ int64_t find_header(const DevIndex &ix, uint64_t key) {
 __device__ bool place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32_t epoch,
                           uint32_t sess, bool &trigger) {
   trigger = false;
-  const int64_t hs = find_header(ix, key);
-  uint32_t same;
-  if (hs >= 0) {
-    const uint64_t rec = val_rec(*val_ptr(ix, hs));
+  const Claim c = claim_slot(ix, home_bucket(key, ix.n_buckets), key, true);
+  if (c.header >= 0) {
+    const uint64_t rec = val_rec(*val_ptr(ix, c.header));
     atomicOr(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
              1ull << (inst & 63));
-    const int64_t s = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, same);
-    if (s < 0) return false;
-    *val_ptr(ix, s) = make_val(inst, MEMBER, epoch, sess);
+    const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, false);
+    if (m.slot < 0) return false;
+    *val_ptr(ix, m.slot) = make_val(inst, MEMBER, epoch, sess);
     return true;
   }
-  const int64_t s = claim_slot(ix, home_bucket(key, ix.n_buckets), key, same);
-  if (s < 0) return false;
-  *val_ptr(ix, s) = make_val(inst, PLAIN, epoch, sess);
-  trigger = same == uint32_t(ix.threshold);
+  if (c.slot < 0) return false;
+  *val_ptr(ix, c.slot) = make_val(inst, PLAIN, epoch, sess);
+  trigger = c.same == uint32_t(ix.threshold);
   return true;
 }
 
@@ -233,10 +251,9 @@ __device__ bool spill_key(const DevIndex &ix, uint64_t key) {
       if (val_kind(v) != PLAIN) continue;
       const uint32_t inst = val_inst(v);
       bm[inst >> 6] |= 1ull << (inst & 63);
-      uint32_t same;
-      const int64_t m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, same);
-      if (m < 0) return false;
-      *val_ptr(ix, m) = make_val(inst, MEMBER, val_epoch(v), uint32_t(v & 0xFFFFFF));
+      const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, false);
+      if (m.slot < 0) return false;
+      *val_ptr(ix, m.slot) = make_val(inst, MEMBER, val_epoch(v), uint32_t(v & 0xFFFFFF));
       if (first < 0) {
         first = int64_t(b * SLOTS + s);
         bk[SLOTS + s] = header_val(rec);
@@ -311,8 +328,9 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
 
 __device__ __forceinline__ void ws_error(WsHdr *h, int e) { atomicCAS(&h->err, 0, e); }
 
-// Returns true when this call created the dedupe entry (first sighting of the pair).
-__device__ bool dedupe_pair(const InsWs &ws, uint64_t key, uint32_t inst, uint32_t r) {
+// Returns the dedupe slot when this call created the entry (first sighting of the
+// pair), else -1; the caller lists created slots with one atomic per wavefront.
+__device__ int64_t dedupe_pair(const InsWs &ws, uint64_t key, uint32_t inst, uint32_t r) {
   const uint64_t mine = (uint64_t(inst) << 32) | r;
   uint64_t h = mix64(key ^ ((uint64_t(inst) + 1) * 0xC2B2AE3D27D4EB4Full)) & (ws.n_dedupe - 1);
   for (uint64_t step = 0; step < ws.n_dedupe; ++step, h = (h + 1) & (ws.n_dedupe - 1)) {
@@ -324,26 +342,37 @@ __device__ bool dedupe_pair(const InsWs &ws, uint64_t key, uint32_t inst, uint32
     while (true) {
       if (w == ~uint64_t(0)) {
         const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&ws.dw2[h]), ~0ull, mine);
-        if (prev == ~uint64_t(0)) {
-          const unsigned long long at = atomicAdd(&ws.hdr->n_new, 1ull);
-          if (at < ws.list_cap) ws.list[at] = h;  // more pairs than blocks: rejected by the check
-          return true;
-        }
+        if (prev == ~uint64_t(0)) return int64_t(h);
         w = prev;
         continue;
       }
       if ((w >> 32) == inst) {
         atomicMin(reinterpret_cast<unsigned long long *>(&ws.dw2[h]), mine);
-        return false;
+        return -1;
       }
       break;  // another instance's pair: keep probing
     }
   }
   ws_error(ws.hdr, SMETRIC_EINTERNAL);
-  return false;
+  return -1;
 }
 
-constexpr int IW = 4;  // waves per workgroup in per-request kernels
+// Append `h` (when >= 0) to the list: one atomicAdd per wavefront for all its lanes.
+__device__ __forceinline__ void append_wave(unsigned long long *counter, uint64_t *list, uint64_t cap, int64_t h) {
+  const uint64_t want = __ballot(h >= 0);
+  if (!want) return;
+  const int lane = threadIdx.x & 63;
+  const int leader = __builtin_ctzll(want);
+  unsigned long long base = 0;
+  if (lane == leader) base = atomicAdd(counter, (unsigned long long)__popcll(want));
+  base = __shfl(base, leader, 64);
+  if (h >= 0) {
+    const unsigned long long at = base + __popcll(want & ((uint64_t(1) << lane) - 1));
+    if (at < cap) list[at] = uint64_t(h);  // more pairs than blocks: rejected by the check
+  }
+}
+
+constexpr int IW = 1;  // waves per workgroup in per-request kernels
 
 __device__ __forceinline__ bool range_of(const int64_t *blk_off, int r, int64_t n_blocks, int64_t &b0,
                                          int64_t &nb) {
@@ -373,20 +402,25 @@ __global__ __launch_bounds__(64 * IW) void ins_probe_kernel(DevIndex ix, InsWs w
     if (lane == 0) ws_error(ws.hdr, SMETRIC_EINVAL);
     return;
   }
-  for (int64_t j = lane; j < nb; j += 64) {
-    const uint64_t key = keys[b0 + j];
-    if (key == KEY_EMPTY || key == KEY_TOMB) {
-      ws_error(ws.hdr, SMETRIC_EINVAL);
-      ws.pos[b0 + j] = 0;
-      continue;
+  for (int64_t j0 = 0; j0 < nb; j0 += 64) {
+    const int64_t j = j0 + lane;
+    int64_t fresh = -1;
+    if (j < nb) {
+      const uint64_t key = keys[b0 + j];
+      if (key == KEY_EMPTY || key == KEY_TOMB) {
+        ws_error(ws.hdr, SMETRIC_EINVAL);
+        ws.pos[b0 + j] = 0;
+      } else {
+        const Found f = find_entry(ix, key, uint32_t(inst));
+        if (f.slot >= 0) {
+          ws.pos[b0 + j] = val_epoch(f.val) < epoch ? uint64_t(f.slot) + 1 : 0;
+        } else {
+          ws.pos[b0 + j] = 0;
+          fresh = dedupe_pair(ws, key, uint32_t(inst), uint32_t(r));
+        }
+      }
     }
-    const Found f = find_entry(ix, key, uint32_t(inst));
-    if (f.slot >= 0) {
-      ws.pos[b0 + j] = val_epoch(f.val) < epoch ? uint64_t(f.slot) + 1 : 0;
-    } else {
-      ws.pos[b0 + j] = 0;
-      dedupe_pair(ws, key, uint32_t(inst), uint32_t(r));
-    }
+    append_wave(&ws.hdr->n_new, ws.list, ws.list_cap, fresh);
   }
 }
 
@@ -425,26 +459,35 @@ __global__ void ins_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
   if (ws.hdr->abort) return;
   const uint64_t n = ws.hdr->n_new;
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
-    const uint64_t h = ws.list[i];
-    const uint64_t key = ws.dkey[h], w = ws.dw2[h];
-    const uint32_t inst = uint32_t(w >> 32), r = uint32_t(w);
-    bool trig;
-    if (!place_new(ix, key, inst, epoch, session[r], trig)) {
-      set_status(ix.hdr, SMETRIC_EINTERNAL);
-      continue;
+  const uint64_t first = uint64_t(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u);
+  for (uint64_t i0 = first; i0 < n; i0 += stride) {  // whole wavefronts iterate together
+    const uint64_t i = i0 + (threadIdx.x & 63);
+    int64_t tk = -1;
+    if (i < n) {
+      const uint64_t h = ws.list[i];
+      const uint64_t key = ws.dkey[h];
+      const uint64_t w = ws.dw2[h];
+      const uint32_t inst = uint32_t(w >> 32), r = uint32_t(w);
+      bool trig;
+      if (!place_new(ix, key, inst, epoch, session[r], trig)) set_status(ix.hdr, SMETRIC_EINTERNAL);
+      else if (trig) tk = int64_t(i);
     }
-    if (trig) ws.trig[atomicAdd(&ws.hdr->n_trig, 1ull)] = key;
+    append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by list index
   }
 }
 
+// Convert the queued keys.  trig holds indexes: key = keys[via[idx]] when `via` is
+// given (insert: positions in the dedupe list), else keys[idx] (rebuild).
 __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned long long *n_trig,
-                             const int *abort_flag) {
+                             const int *abort_flag, const uint64_t *keys, const uint64_t *via) {
   if (abort_flag && *abort_flag) return;
   const uint64_t n = *n_trig;
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
-    if (!spill_key(ix, trig[i])) set_status(ix.hdr, SMETRIC_EINTERNAL);
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint64_t t = trig[i];
+    const uint64_t key = via ? keys[via[t]] : keys[t];
+    if (!spill_key(ix, key)) set_status(ix.hdr, SMETRIC_EINTERNAL);
+  }
 }
 
 // ---------------------------------------------------------------------------------
@@ -470,16 +513,20 @@ __global__ void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals, unsig
 
 // Rebuild: enter entries [lo, hi) of (keys, vals) into a cleared table.
 __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const uint64_t *vals, uint64_t lo,
-                                     uint64_t hi, uint64_t *trig, unsigned long long *n_trig) {
+                                     uint64_t hi, uint64_t *trig, unsigned long long *n_trig, uint64_t cap) {
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = lo + uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < hi; i += stride) {
-    const uint64_t v = vals[i];
-    bool t;
-    if (!place_new(ix, keys[i], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), t)) {
-      set_status(ix.hdr, SMETRIC_EINTERNAL);
-      continue;
+  const uint64_t first = lo + uint64_t(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u);
+  for (uint64_t i0 = first; i0 < hi; i0 += stride) {  // whole wavefronts iterate together
+    const uint64_t i = i0 + (threadIdx.x & 63);
+    int64_t tk = -1;
+    if (i < hi) {
+      const uint64_t v = vals[i];
+      bool t;
+      if (!place_new(ix, keys[i], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), t))
+        set_status(ix.hdr, SMETRIC_EINTERNAL);
+      else if (t) tk = int64_t(i);
     }
-    if (t) trig[atomicAdd(n_trig, 1ull)] = keys[i];
+    append_wave(n_trig, trig, cap, tk);
   }
 }
 
@@ -668,7 +715,8 @@ extern "C" int smetric_index_insert(smetric_index *idx, const uint64_t *keys, co
   hipLaunchKernelGGL(ins_check_kernel, dim3(1), dim3(1), 0, stream, ix, ws, n_blocks);
   hipLaunchKernelGGL(ins_refresh_kernel, rgrid, rblock, 0, stream, ix, ws, blk_off, n_req, n_blocks, epoch);
   hipLaunchKernelGGL(ins_place_kernel, dim3(grid_for(uint64_t(n_blocks))), dim3(TB), 0, stream, ix, ws, session, epoch);
-  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort);
+  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
+                     ws.dkey, ws.list);
   return hip_rc(hipGetLastError());
 }
 
@@ -703,8 +751,8 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   uint64_t *trig = ws.ea;  // free once the sorted entries are in place
   unsigned long long *n_trig = ws.count + 1;
   hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n - m)), dim3(TB), 0, stream, ix, keys, vals, m, n, trig,
-                     n_trig);
-  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr);
+                     n_trig, idx->capacity);
+  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   return hip_rc(hipStreamSynchronize(stream));
 }

@@ -24,7 +24,7 @@
 namespace smk {
 namespace {
 
-constexpr int MW = 4;        // waves per workgroup
+constexpr int MW = 1;        // waves per workgroup
 constexpr int LIST_MAX = 8;  // plain holders kept per probe
 enum HKind : uint32_t { H_NONE = 0, H_LIST = 1, H_HOT = 2, H_LONG = 3 };
 

@@ -65,7 +65,7 @@ def test_hash_bad_offsets_flag_status_without_writing():
 
 
 def test_config0_open_loop_full():
-    """configs[0] at full size: 8 instances, 64 sessions x 4 turns."""
+    """The tiny trace at full size: 8 instances, 64 sessions x 4 turns."""
     pair, br = run_sessions(W.config0(), 4, capacity=200_000)
     assert set(br.tolist()) >= {0, 2}
 
