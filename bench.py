@@ -144,6 +144,15 @@ class Setup:
         rec(4)
 
 
+def kernel_sources_hash() -> str:
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2607_08565_amd", "csrc", "*"))):
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
 def algorithmic_bytes(setup, b, matched, I):
     """Bytes the method itself must move for batch b (see the design notes):
     hash: 4 B per token read + 8 B per block key written;
@@ -268,7 +277,8 @@ def main():
     traffic = None
     if os.path.exists(args.traffic):
         tr = json.load(open(args.traffic))
-        traffic = tr.get(dominant)
+        if tr.get("sources_sha256_16") == kernel_sources_hash():  # counters of the current kernels only
+            traffic = tr.get(dominant)
     roof = {"bound": "hbm", "kernel": dominant, "achieved": round(gbs.get(dominant, 0.0), 1), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(gbs.get(dominant, 0.0) / HBM_PEAK_GBS, 4), "traffic": traffic}
     path_gbs = (alg["hash"] + alg["match"]) / (per["hash"] + per["match"]) / 1e6
