@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--index-entries", type=int, default=200_000_000, help="entries at the start of timing")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle time budget for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--direct", action="store_true",
+                    help="match and insert probe the index themselves instead of sharing one region-ordered probe")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (rocprofv3 FETCH_SIZE/WRITE_SIZE), if present")
     return ap.parse_args()
@@ -79,6 +81,7 @@ class Setup:
         self.branch = torch.empty(args.n_req, dtype=torch.uint8, device="cuda")
         self.filler_chunk = 16_000_000
         self.ws = torch.empty(S.insert_ws_bytes(max(max_blocks, self.filler_chunk)), dtype=torch.uint8, device="cuda")
+        self.probe_state = torch.empty(S.probe_ws_bytes(max_blocks), dtype=torch.uint8, device="cuda")
         # index: the prior turns of every batch's sessions, then filler
         growth = 30_000_000 * self.n_batches
         self.capacity = args.index_entries + growth
@@ -127,21 +130,34 @@ class Setup:
             done += m
             c += 1
 
+    CALLS = ("hash", "probe", "match", "route", "insert")
+
     def step(self, b: int, ev=None):
-        """The timed unit: all four calls on the current stream."""
+        """The timed unit: every call of the path on the current stream."""
         S, d, tb = self.S, self.dev[b], self.host[b]
         rec = (lambda k: ev[k].record()) if ev is not None else (lambda k: None)
+        nb = d["n_blocks"]
         rec(0)
-        S.hash_blocks(d["tokens"], d["tok_off"], d["blk_off"], d["n_blocks"], keys=self.keys)
+        S.hash_blocks(d["tokens"], d["tok_off"], d["blk_off"], nb, keys=self.keys)
         rec(1)
-        self.index.match(self.keys, d["blk_off"], d["n_blocks"], matched=self.matched)
+        if not self.args.direct:
+            self.index.probe(self.keys, d["blk_off"], nb, state=self.probe_state)
         rec(2)
+        if self.args.direct:
+            self.index.match(self.keys, d["blk_off"], nb, matched=self.matched)
+        else:
+            self.index.match_probed(self.probe_state, self.keys, d["blk_off"], nb, matched=self.matched)
+        rec(3)
         S.route(self.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], self.W.DEFAULT_PARAMS,
                 tb.batch.rr_base, target=self.target, branch=self.branch)
-        rec(3)
-        self.index.insert(self.keys, d["blk_off"], d["n_blocks"], self.target, d["session"], tb.batch.epoch,
-                          workspace=self.ws)
         rec(4)
+        if self.args.direct:
+            self.index.insert(self.keys, d["blk_off"], nb, self.target, d["session"], tb.batch.epoch,
+                              workspace=self.ws)
+        else:
+            self.index.insert_probed(self.probe_state, self.args.n_req, nb, self.target, d["session"],
+                                     tb.batch.epoch, workspace=self.ws)
+        rec(5)
 
 
 def kernel_sources_hash() -> str:
@@ -169,8 +185,13 @@ def algorithmic_bytes(setup, b, matched, I):
     R = len(nb)
     hash_b = 4 * n_tok + 8 * n_blk
     match_b = int(probes.sum()) * (8 + 64) + int(hot.sum()) * (I // 8) + 4 * R * I
+    # the shared probe answers every block once (the insert needs all of them):
+    # 8 B key + one 64 B bucket burst in, an 8 B descriptor out
+    probe_b = n_blk * (8 + 64 + 8)
+    # the match that follows it reads one 8 B descriptor per necessary block
+    scan_b = int(probes.sum()) * 8 + int(hot.sum()) * (I // 8) + 4 * R * I
     return dict(tokens=n_tok, blocks=n_blk, probes=int(probes.sum()), hot_probes=int(hot.sum()),
-                hash=hash_b, match=match_b, route=4 * R * I + 8 * I + 12 * R + 5 * R)
+                hash=hash_b, match=match_b, probe=probe_b, match_scan=scan_b, route=4 * R * I + 8 * I + 12 * R + 5 * R)
 
 
 def cpu_baseline(setup, budget_s: float, gpu_out):
@@ -253,7 +274,7 @@ def main():
             gpu_out = (setup.keys[:nb0].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
                        setup.branch.cpu().numpy())
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     mats = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -261,9 +282,8 @@ def main():
         setup.step(args.warmup + k, evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    names = ["hash", "match", "route", "insert"]
     per = {n: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
-           for i, n in enumerate(names)}
+           for i, n in enumerate(Setup.CALLS)}
     n, st = setup.index.stats()
     assert st == 0, f"index status {st}"
     # algorithmic bytes for the last timed batch (match outputs still in the buffer)
@@ -272,8 +292,14 @@ def main():
     R = args.n_req
     tokens = float(np.mean([setup.host[args.warmup + k].batch.n_tokens for k in range(args.steps)]))
     ms_step = wall * 1e3 / args.steps
-    gbs = {"hash": alg["hash"] / per["hash"] / 1e6, "match": alg["match"] / per["match"] / 1e6}
-    dominant = max(("hash", "match", "route"), key=lambda k: per[k])
+    probe_match_ms = per["probe"] + per["match"]
+    gbs = {"hash": alg["hash"] / per["hash"] / 1e6}
+    if args.direct:
+        gbs["match"] = alg["match"] / per["match"] / 1e6
+    else:
+        gbs["probe"] = alg["probe"] / per["probe"] / 1e6
+        gbs["match"] = alg["match_scan"] / per["match"] / 1e6
+    dominant = max(("hash", "probe", "match", "route"), key=lambda k: per[k])
     traffic = None
     if os.path.exists(args.traffic):
         tr = json.load(open(args.traffic))
@@ -281,7 +307,7 @@ def main():
             traffic = tr.get(dominant)
     roof = {"bound": "hbm", "kernel": dominant, "achieved": round(gbs.get(dominant, 0.0), 1), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(gbs.get(dominant, 0.0) / HBM_PEAK_GBS, 4), "traffic": traffic}
-    path_gbs = (alg["hash"] + alg["match"]) / (per["hash"] + per["match"]) / 1e6
+    path_gbs = (alg["hash"] + alg["match"]) / (per["hash"] + probe_match_ms) / 1e6
     out = {
         "metric": METRIC, "value": round(R / (ms_step / 1e3), 1), "unit": "requests/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
@@ -292,7 +318,8 @@ def main():
                    "n_instances": args.n_inst, "requests_per_batch": R, "block_size": 16,
                    "index_entries_start": setup.start_entries, "index_entries_end": n,
                    "index_capacity": setup.capacity, "tokens_per_batch": int(tokens)},
-        "prompt_tokens_matched_per_s": round(tokens / ((per["hash"] + per["match"]) / 1e3), 1),
+        "path": "direct" if args.direct else "region-ordered probe",
+        "prompt_tokens_matched_per_s": round(tokens / ((per["hash"] + probe_match_ms) / 1e3), 1),
         "kernel_ms": {k: round(v, 4) for k, v in per.items()},
         "algorithmic_GBs": {k: round(v, 1) for k, v in gbs.items()},
         "hash_probe_path": {"GBs": round(path_gbs, 1), "frac_of_peak": round(path_gbs / HBM_PEAK_GBS, 4),

@@ -158,6 +158,37 @@ int smetric_match(const smetric_index *idx, const uint64_t *keys, const int64_t 
                   int32_t n_req, int64_t n_blocks, int32_t *matched, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------
+ * Region-ordered probe: the same question as smetric_match (which instances hold each
+ * block's key, Sec. 4.1), asked once per block of a batch and answered into a probe
+ * state that both smetric_match_probed and smetric_index_insert_probed consume, so the
+ * post-route insert needs no second lookup.  Blocks are first partitioned by table
+ * region and probed region by region, which keeps the random reads of the index inside
+ * a small window of HBM at any moment.
+ *
+ * smetric_probe_ws_bytes: bytes of the probe state for n_blocks (< 2^32) blocks.
+ * smetric_probe: requests must tile the keys: blk_off[0] = 0, non-decreasing,
+ *   blk_off[n_req] = n_blocks; otherwise the probe state is marked invalid and the
+ *   consumers report EINVAL.  `probe` is caller device memory (256-byte aligned) that the
+ *   caller keeps unchanged until the consumers have run; the index must not change in
+ *   between (the descriptors describe its state at probe time).
+ * smetric_match_probed: exactly smetric_match's output (Sec. 4.1), read from the probe
+ *   state; an invalid probe state gives all-zero rows and status EINVAL.
+ * smetric_index_insert_probed: exactly smetric_index_insert's effect (same validation,
+ *   all-or-nothing, EINVAL/EFULL in the status word) for the probed batch, with
+ *   instance/session per request as there; an invalid probe state gives EINVAL.
+ * Host errors: EINVAL (bad scalars, n_blocks >= 2^32), EWORKSPACE (short buffers).
+ * --------------------------------------------------------------------------------- */
+int smetric_probe_ws_bytes(int64_t n_blocks, uint64_t *bytes /* host */);
+int smetric_probe(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                  int64_t n_blocks, void *probe, uint64_t probe_bytes, hipStream_t stream);
+int smetric_match_probed(const smetric_index *idx, const void *probe, uint64_t probe_bytes,
+                         const uint64_t *keys, const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
+                         int32_t *matched, hipStream_t stream);
+int smetric_index_insert_probed(smetric_index *idx, const void *probe, uint64_t probe_bytes, int32_t n_req,
+                                int64_t n_blocks, const int32_t *instance, const uint32_t *session,
+                                uint32_t epoch, void *workspace, uint64_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
  * Route (Sec. 4.2 pseudocode (a) routing, (b) SLO checks, (c) load model; Eq. (1)).
  * All requests of the batch see the same load snapshot q.  Exact integer arithmetic in
  * nanoseconds of prefill time (PREFILL_RATE folded into the coefficients):

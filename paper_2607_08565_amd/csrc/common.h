@@ -82,9 +82,22 @@ __host__ __device__ inline uint64_t mix64(uint64_t k) {
 __device__ inline uint64_t home_bucket(uint64_t key, uint64_t n_buckets) {
   return __umul64hi(mix64(key), n_buckets);
 }
-// Bucket chain for a member entry (key, inst) of a key that uses a bitmap record.
+// Table regions: the bucket range split into NREG equal parts.  Probes, refreshes and
+// claims are issued region by region so the pages live at any moment stay few.
+constexpr int NREG = 256;
+__device__ __forceinline__ uint32_t region_of(uint64_t key, uint64_t n_buckets) {
+  return uint32_t(home_bucket(key, n_buckets) * NREG / n_buckets);
+}
+
+// Bucket chain for a member entry (key, inst) of a key that uses a bitmap record: a
+// pseudo-random bucket inside the region of the key's home bucket, so member lookups
+// issued in region order stay inside the same window of the table.
 __device__ inline uint64_t member_bucket(uint64_t key, uint32_t inst, uint64_t n_buckets) {
-  return __umul64hi(mix64(key ^ ((uint64_t(inst) + 1) * 0x9E3779B97F4A7C15ull)), n_buckets);
+  const uint64_t h = mix64(key ^ ((uint64_t(inst) + 1) * 0x9E3779B97F4A7C15ull));
+  if (n_buckets < uint64_t(4 * NREG)) return __umul64hi(h, n_buckets);
+  const uint64_t g = region_of(key, n_buckets);
+  const uint64_t lo = g * n_buckets / NREG, hi = (g + 1) * n_buckets / NREG;
+  return lo + __umul64hi(h, hi - lo);
 }
 
 __device__ inline void set_status(IndexHdr *h, int err) {
@@ -111,6 +124,74 @@ __device__ __forceinline__ BucketScan scan_bucket(const uint64_t *bk, uint64_t k
   return r;
 }
 __device__ __forceinline__ uint64_t next_bucket(uint64_t b, uint64_t n) { return b + 1 == n ? 0 : b + 1; }
+
+// Holder descriptor of one probed block (64 bits): kind:2 | instance:16 | x:46.
+//   NONE  no entry holds the key
+//   ONE   one plain holder: instance, x = its slot index
+//   MANY  two or more plain holders: re-walk the chain when needed
+//   HOT   bitmap record: x = record index
+enum DescKind : uint32_t { D_NONE = 0, D_ONE = 1, D_MANY = 2, D_HOT = 3 };
+constexpr uint64_t DESC_X_MASK = (uint64_t(1) << 46) - 1;
+__host__ __device__ inline uint64_t make_desc(uint32_t kind, uint32_t inst, uint64_t x) {
+  return (uint64_t(kind) << 62) | (uint64_t(inst & 0xFFFF) << 46) | (x & DESC_X_MASK);
+}
+__host__ __device__ inline uint32_t desc_kind(uint64_t d) { return uint32_t(d >> 62); }
+__host__ __device__ inline uint32_t desc_inst(uint64_t d) { return uint32_t(d >> 46) & 0xFFFFu; }
+__host__ __device__ inline uint64_t desc_x(uint64_t d) { return d & DESC_X_MASK; }
+
+// Work split of the region-ordered kernels: a fixed grid of FLAT_WG workgroups whose
+// iterations advance through the region-ordered arrays together (iteration t covers
+// items [t * FLAT_WG * 256, (t + 1) * FLAT_WG * 256)), so the live window of the table
+// slides; PART_WG workgroups partition contiguous chunks of blocks.
+constexpr int FLAT_WG = 2048;
+constexpr int PART_WG = 1024;
+constexpr int WG_THREADS = 256;
+inline uint64_t flat_span() { return uint64_t(FLAT_WG) * WG_THREADS; }
+// items one workgroup of the fixed grid handles at most (its output segment size)
+inline uint64_t flat_segment(uint64_t n) { return (n + flat_span() - 1) / flat_span() * WG_THREADS; }
+
+// Probe state shared by smetric_probe and the calls that consume it.
+struct ProbeHdr {
+  int err;                          // first input error (EINVAL) found while partitioning
+  int pad0;
+  unsigned long long n;             // number of blocks probed (0 when invalid)
+};
+struct ProbeView {
+  ProbeHdr *hdr;
+  uint32_t *req_of;     // block order: request of each block
+  uint32_t *inv;        // block order: position of the block in region order
+  uint32_t *hist;       // [NREG][PART_WG] blocks of each region in each partition chunk
+  uint64_t *base;       // [NREG][PART_WG] first region-order position of each (region, chunk)
+  uint64_t *part_key;   // region order: key
+  uint64_t *part_br;    // region order: block index | request << 32
+  uint64_t *desc_p;     // region order: holder descriptor
+  uint64_t cap;         // blocks the buffer holds
+};
+inline uint64_t probe_layout(int64_t n_blocks, ProbeView *v, void *base) {
+  const uint64_t n = uint64_t(n_blocks < 1 ? 1 : n_blocks);
+  uint64_t off = 0;
+  auto take = [&](uint64_t bytes) {
+    const uint64_t o = off;
+    off = (off + bytes + 255) / 256 * 256;
+    return o;
+  };
+  const uint64_t o_hdr = take(sizeof(ProbeHdr)), o_req = take(4 * n), o_inv = take(4 * n),
+                 o_hist = take(4ull * NREG * PART_WG), o_base = take(8ull * NREG * PART_WG), o_k = take(8 * n),
+                 o_br = take(8 * n), o_dp = take(8 * n);
+  if (v) {
+    char *b = static_cast<char *>(base);
+    v->hdr = reinterpret_cast<ProbeHdr *>(b + o_hdr);
+    v->req_of = reinterpret_cast<uint32_t *>(b + o_req);
+    v->inv = reinterpret_cast<uint32_t *>(b + o_inv);
+    v->hist = reinterpret_cast<uint32_t *>(b + o_hist);
+    v->base = reinterpret_cast<uint64_t *>(b + o_base);
+    v->part_key = reinterpret_cast<uint64_t *>(b + o_k);
+    v->part_br = reinterpret_cast<uint64_t *>(b + o_br);
+    v->desc_p = reinterpret_cast<uint64_t *>(b + o_dp);
+    v->cap = n;
+  }
+  return off;
+}
 
 // Sizing shared by host code.
 inline int32_t bitmap_words_for(int32_t n_inst) { return (n_inst + 63) / 64; }

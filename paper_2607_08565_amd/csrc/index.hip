@@ -163,13 +163,19 @@ __device__ __forceinline__ uint64_t *val_ptr(const DevIndex &ix, int64_t slot) {
 // `same` counts slots holding `key` ahead of the claimed one.  Plain loads may see a
 // stale EMPTY; the compare-and-swap then fails and returns the slot's real key, and
 // slots never return to EMPTY, so the count is exact.
+// With max_same, the walk gives up (capped) once it has seen max_same slots of `key`
+// ahead of any free slot: that key is about to get a bitmap record, and its remaining
+// new holders are entered after the conversion instead of piling up plain slots that
+// would all turn into tombstones.
 struct Claim {
   int64_t slot;    // claimed slot, or -1
   int64_t header;  // HEADER slot of key when found, else -1
   uint32_t same;
+  bool capped;
 };
-__device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool want_header) {
-  Claim c{-1, -1, 0};
+__device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool want_header,
+                            uint32_t max_same = 0xFFFFFFFFu) {
+  Claim c{-1, -1, 0, false};
   for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
     uint64_t *bk = ix.slots + b * BUCKET_WORDS;
     const BucketScan sc = scan_bucket(bk, key);
@@ -186,12 +192,20 @@ __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool w
     }
     if (!sc.empty) {
       c.same += __popc(sc.match);
+      if (c.same >= max_same) {
+        c.capped = true;
+        return c;
+      }
       continue;
     }
     // slots before the first EMPTY are final; try the EMPTY ones in order
     const int first = __builtin_ctz(sc.empty);
     c.same += __popc(sc.match & ((1u << first) - 1u));
     for (int s = first; s < SLOTS; ++s) {
+      if (c.same >= max_same) {
+        c.capped = true;
+        return c;
+      }
       const uint64_t k = atomicCAS(reinterpret_cast<unsigned long long *>(&bk[s]), KEY_EMPTY, key);
       if (k == KEY_EMPTY) {
         c.slot = int64_t(b * SLOTS + s);
@@ -209,25 +223,29 @@ __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool w
   return c;
 }
 
-// Enter a distinct new entry.  Returns false only if the table has no free slot.
-// *trigger is set when the slot is the key's (T+1)-th plain slot.
-__device__ bool place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32_t epoch,
-                          uint32_t sess, bool &trigger) {
+// Enter a distinct new entry.  Returns PLACED, DEFERRED (capped: enter it again after the
+// key's conversion, uncapped) or FAILED (no free slot).  trigger is set when the slot is
+// the key's (T+1)-th plain slot, the last one a key gets before its conversion.
+enum Placed { PLACED = 0, DEFERRED = 1, FAILED = 2 };
+__device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32_t epoch, uint32_t sess,
+                         bool &trigger, bool capped) {
   trigger = false;
-  const Claim c = claim_slot(ix, home_bucket(key, ix.n_buckets), key, true);
+  const Claim c = claim_slot(ix, home_bucket(key, ix.n_buckets), key, true,
+                             capped ? uint32_t(ix.threshold) + 1 : 0xFFFFFFFFu);
   if (c.header >= 0) {
     const uint64_t rec = val_rec(*val_ptr(ix, c.header));
     atomicOr(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
              1ull << (inst & 63));
     const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, false);
-    if (m.slot < 0) return false;
+    if (m.slot < 0) return FAILED;
     *val_ptr(ix, m.slot) = make_val(inst, MEMBER, epoch, sess);
-    return true;
+    return PLACED;
   }
-  if (c.slot < 0) return false;
+  if (c.capped) return DEFERRED;
+  if (c.slot < 0) return FAILED;
   *val_ptr(ix, c.slot) = make_val(inst, PLAIN, epoch, sess);
   trigger = c.same == uint32_t(ix.threshold);
-  return true;
+  return PLACED;
 }
 
 // Replace the plain slots of `key` by a bitmap record (one thread per key).
@@ -276,7 +294,10 @@ struct WsHdr {
   unsigned long long n_trig;   // keys queued for conversion
   int err;                     // first input error seen by the probe
   int abort;                   // set by the check: leave the index unchanged
-  unsigned long long pad[28];
+  unsigned long long n_cand;   // pairs absent before the batch (region-ordered insert)
+  unsigned long long n_dd;     // dedupe slots in use (a power of two)
+  unsigned long long n_def;    // new pairs deferred until their key's conversion
+  unsigned long long pad[25];
 };
 static_assert(sizeof(WsHdr) == 256, "ws header size");
 
@@ -287,8 +308,13 @@ struct InsWs {
   uint64_t *dw2;    // dedupe table: inst << 32 | lowest request index, ~0 = free
   uint64_t *list;   // dedupe slots of distinct new pairs
   uint64_t *trig;   // keys queued for conversion
+  uint64_t *def;    // list positions of deferred new pairs
+  uint64_t *cand;   // region-ordered insert: positions of absent pairs, one segment per workgroup
+  uint32_t *cand_cnt;  // entries in each workgroup's candidate segment
+  uint32_t *list_cnt;  // entries in each workgroup's new-pair segment
   uint64_t n_dedupe;
-  uint64_t list_cap;  // entries in list and trig (= n_blocks)
+  uint64_t list_cap;  // entries in list and trig
+  uint64_t seg;       // segment length of the region-ordered insert
 };
 
 uint64_t dedupe_size(int64_t n_blocks) {
@@ -300,6 +326,8 @@ uint64_t dedupe_size(int64_t n_blocks) {
 uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
   const uint64_t n = uint64_t(n_blocks < 1 ? 1 : n_blocks);
   const uint64_t nd = dedupe_size(n_blocks);
+  const uint64_t seg = flat_segment(n), seg_n = seg * FLAT_WG;
+  const uint64_t nl = seg_n > n ? seg_n : n;
   uint64_t off = 0;
   auto take = [&](uint64_t bytes) {
     const uint64_t o = off;
@@ -310,8 +338,12 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
   const uint64_t o_pos = take(8 * n);
   const uint64_t o_dkey = take(8 * nd);
   const uint64_t o_dw2 = take(8 * nd);
-  const uint64_t o_list = take(8 * n);
-  const uint64_t o_trig = take(8 * n);
+  const uint64_t o_list = take(8 * nl);
+  const uint64_t o_trig = take(8 * nl);
+  const uint64_t o_def = take(8 * nl);
+  const uint64_t o_cand = take(8 * seg_n);
+  const uint64_t o_cc = take(4 * FLAT_WG);
+  const uint64_t o_lc = take(4 * FLAT_WG);
   if (ws) {
     char *b = static_cast<char *>(base);
     ws->hdr = reinterpret_cast<WsHdr *>(b + o_hdr);
@@ -320,8 +352,13 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
     ws->dw2 = reinterpret_cast<uint64_t *>(b + o_dw2);
     ws->list = reinterpret_cast<uint64_t *>(b + o_list);
     ws->trig = reinterpret_cast<uint64_t *>(b + o_trig);
+    ws->def = reinterpret_cast<uint64_t *>(b + o_def);
+    ws->cand = reinterpret_cast<uint64_t *>(b + o_cand);
+    ws->cand_cnt = reinterpret_cast<uint32_t *>(b + o_cc);
+    ws->list_cnt = reinterpret_cast<uint32_t *>(b + o_lc);
     ws->n_dedupe = nd;
-    ws->list_cap = n;
+    ws->list_cap = nl;
+    ws->seg = seg;
   }
   return off;
 }
@@ -330,10 +367,10 @@ __device__ __forceinline__ void ws_error(WsHdr *h, int e) { atomicCAS(&h->err, 0
 
 // Returns the dedupe slot when this call created the entry (first sighting of the
 // pair), else -1; the caller lists created slots with one atomic per wavefront.
-__device__ int64_t dedupe_pair(const InsWs &ws, uint64_t key, uint32_t inst, uint32_t r) {
+__device__ int64_t dedupe_pair(const InsWs &ws, uint64_t nd, uint64_t key, uint32_t inst, uint32_t r) {
   const uint64_t mine = (uint64_t(inst) << 32) | r;
-  uint64_t h = mix64(key ^ ((uint64_t(inst) + 1) * 0xC2B2AE3D27D4EB4Full)) & (ws.n_dedupe - 1);
-  for (uint64_t step = 0; step < ws.n_dedupe; ++step, h = (h + 1) & (ws.n_dedupe - 1)) {
+  uint64_t h = mix64(key ^ ((uint64_t(inst) + 1) * 0xC2B2AE3D27D4EB4Full)) & (nd - 1);
+  for (uint64_t step = 0; step < nd; ++step, h = (h + 1) & (nd - 1)) {
     uint64_t k = __hip_atomic_load(&ws.dkey[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (k == KEY_EMPTY) k = atomicCAS(reinterpret_cast<unsigned long long *>(&ws.dkey[h]), KEY_EMPTY, key);
     if (k != KEY_EMPTY && k != key) continue;
@@ -416,7 +453,7 @@ __global__ __launch_bounds__(64 * IW) void ins_probe_kernel(DevIndex ix, InsWs w
           ws.pos[b0 + j] = val_epoch(f.val) < epoch ? uint64_t(f.slot) + 1 : 0;
         } else {
           ws.pos[b0 + j] = 0;
-          fresh = dedupe_pair(ws, key, uint32_t(inst), uint32_t(r));
+          fresh = dedupe_pair(ws, ws.n_dedupe, key, uint32_t(inst), uint32_t(r));
         }
       }
     }
@@ -462,17 +499,20 @@ __global__ void ins_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
   const uint64_t first = uint64_t(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u);
   for (uint64_t i0 = first; i0 < n; i0 += stride) {  // whole wavefronts iterate together
     const uint64_t i = i0 + (threadIdx.x & 63);
-    int64_t tk = -1;
+    int64_t tk = -1, df = -1;
     if (i < n) {
       const uint64_t h = ws.list[i];
       const uint64_t key = ws.dkey[h];
       const uint64_t w = ws.dw2[h];
       const uint32_t inst = uint32_t(w >> 32), r = uint32_t(w);
       bool trig;
-      if (!place_new(ix, key, inst, epoch, session[r], trig)) set_status(ix.hdr, SMETRIC_EINTERNAL);
+      const int pl = place_new(ix, key, inst, epoch, session[r], trig, true);
+      if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+      else if (pl == DEFERRED) df = int64_t(i);
       else if (trig) tk = int64_t(i);
     }
     append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by list index
+    append_wave(&ws.hdr->n_def, ws.def, ws.list_cap, df);
   }
 }
 
@@ -487,6 +527,147 @@ __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned l
     const uint64_t t = trig[i];
     const uint64_t key = via ? keys[via[t]] : keys[t];
     if (!spill_key(ix, key)) set_status(ix.hdr, SMETRIC_EINTERNAL);
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// Region-ordered insert, from the descriptors of smetric_probe
+// ---------------------------------------------------------------------------------
+// classify: per probed block (region order), is (key, target) already an entry?  The
+// descriptor answers it for NONE and ONE; HOT needs the bitmap bit and the member slot
+// (inside the key's region), MANY a chain walk.  Existing -> refresh position; absent ->
+// candidate, appended to this workgroup's segment (LDS counter, no global atomics).
+// All FLAT_WG workgroups advance through the region order together.
+__global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeView pv, InsWs ws,
+                                                           const int32_t *instance, const uint32_t *session) {
+  __shared__ unsigned int lc;
+  if (threadIdx.x == 0) lc = 0;
+  __syncthreads();
+  const uint64_t n = pv.hdr->n;
+  if (pv.hdr->err) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      ws_error(ws.hdr, SMETRIC_EINVAL);
+      ws.cand_cnt[0] = 0;
+    }
+    if (threadIdx.x == 0) ws.cand_cnt[blockIdx.x] = 0;
+    return;
+  }
+  uint64_t *seg = ws.cand + uint64_t(blockIdx.x) * ws.seg;
+  const uint64_t span = uint64_t(gridDim.x) * TB;
+  for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += span) {
+    const uint64_t key = pv.part_key[i];
+    const uint32_t r = uint32_t(pv.part_br[i] >> 32);
+    const int32_t t = instance[r];
+    const uint32_t sess = session[r];
+    uint64_t pos = 0;
+    if (t < 0 || t >= ix.n_inst || sess >= SESSION_LIMIT || key == KEY_EMPTY || key == KEY_TOMB) {
+      ws_error(ws.hdr, SMETRIC_EINVAL);
+    } else {
+      const uint64_t d = pv.desc_p[i];
+      const uint32_t kind = desc_kind(d);
+      int64_t slot = -1;
+      if (kind == D_ONE) {
+        if (desc_inst(d) == uint32_t(t)) slot = int64_t(desc_x(d));
+      } else if (kind == D_HOT) {
+        const uint64_t w = ix.pool[desc_x(d) * uint64_t(ix.words) + (uint32_t(t) >> 6)];
+        if ((w >> (t & 63)) & 1) slot = find_member(ix, key, uint32_t(t)).slot;
+      } else if (kind == D_MANY) {
+        slot = find_entry(ix, key, uint32_t(t)).slot;
+      }
+      if (slot >= 0) pos = uint64_t(slot) + 1;
+      else seg[atomicAdd(&lc, 1u)] = i;
+    }
+    ws.pos[i] = pos;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) ws.cand_cnt[blockIdx.x] = lc;
+}
+
+// total candidates -> size of the dedupe table: the least power of two >= 2 x candidates
+__global__ void insp_size_kernel(InsWs ws) {
+  unsigned long long c = 0;
+  for (int w = 0; w < FLAT_WG; ++w) c += ws.cand_cnt[w];
+  ws.hdr->n_cand = c;
+  uint64_t nd = 64;
+  while (nd < 2 * c && nd < ws.n_dedupe) nd <<= 1;
+  ws.hdr->n_dd = nd;
+}
+
+__global__ void insp_clear_kernel(InsWs ws) {
+  const uint64_t nd = ws.hdr->n_dd;
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t h = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; h < nd; h += stride) {
+    ws.dkey[h] = KEY_EMPTY;
+    ws.dw2[h] = ~uint64_t(0);
+  }
+}
+
+// workgroup w deduplicates its candidate segment into its new-pair segment
+__global__ __launch_bounds__(TB) void insp_dedupe_kernel(ProbeView pv, InsWs ws, const int32_t *instance) {
+  __shared__ unsigned int lc;
+  if (threadIdx.x == 0) lc = 0;
+  __syncthreads();
+  const uint64_t nd = ws.hdr->n_dd;
+  const uint32_t n = ws.cand_cnt[blockIdx.x];
+  const uint64_t *in = ws.cand + uint64_t(blockIdx.x) * ws.seg;
+  uint64_t *out = ws.list + uint64_t(blockIdx.x) * ws.seg;
+  for (uint32_t k = threadIdx.x; k < n; k += TB) {
+    const uint64_t i = in[k];
+    const uint32_t r = uint32_t(pv.part_br[i] >> 32);
+    const int64_t h = dedupe_pair(ws, nd, pv.part_key[i], uint32_t(instance[r]), r);
+    if (h >= 0) out[atomicAdd(&lc, 1u)] = uint64_t(h);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) ws.list_cnt[blockIdx.x] = lc;
+}
+
+__global__ void insp_check_kernel(DevIndex ix, InsWs ws) {
+  unsigned long long c = 0;
+  for (int w = 0; w < FLAT_WG; ++w) c += ws.list_cnt[w];
+  WsHdr *h = ws.hdr;
+  h->n_new = c;
+  const int e = h->err != 0 ? h->err : (ix.hdr->n_entries + c > ix.capacity ? SMETRIC_EFULL : 0);
+  if (e != 0) {
+    h->abort = 1;
+    set_status(ix.hdr, e);
+  } else {
+    ix.hdr->n_entries += c;
+  }
+}
+
+__global__ __launch_bounds__(TB) void insp_refresh_kernel(DevIndex ix, ProbeView pv, InsWs ws, uint32_t epoch) {
+  if (ws.hdr->abort) return;
+  const uint64_t n = pv.hdr->n;
+  const uint64_t span = uint64_t(gridDim.x) * TB;
+  for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += span) {
+    const uint64_t p = ws.pos[i];
+    if (!p) continue;
+    uint64_t *vp = val_ptr(ix, int64_t(p - 1));
+    const uint64_t v = *vp;
+    if (val_epoch(v) < epoch) *vp = (v & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+  }
+}
+
+// workgroup w enters its new-pair segment (in region order, like every segment)
+__global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
+                                                        uint32_t epoch) {
+  if (ws.hdr->abort) return;
+  const uint32_t n = ws.list_cnt[blockIdx.x];
+  const uint64_t base = uint64_t(blockIdx.x) * ws.seg;
+  for (uint32_t k0 = 0; k0 < n; k0 += TB) {  // whole workgroups iterate together
+    const uint32_t k = k0 + threadIdx.x;
+    int64_t tk = -1, df = -1;
+    if (k < n) {
+      const uint64_t h = ws.list[base + k];
+      const uint64_t key = ws.dkey[h], w = ws.dw2[h];
+      bool trig;
+      const int pl = place_new(ix, key, uint32_t(w >> 32), epoch, session[uint32_t(w)], trig, true);
+      if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+      else if (pl == DEFERRED) df = int64_t(base + k);
+      else if (trig) tk = int64_t(base + k);
+    }
+    append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by list position
+    append_wave(&ws.hdr->n_def, ws.def, ws.list_cap, df);
   }
 }
 
@@ -513,20 +694,49 @@ __global__ void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals, unsig
 
 // Rebuild: enter entries [lo, hi) of (keys, vals) into a cleared table.
 __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const uint64_t *vals, uint64_t lo,
-                                     uint64_t hi, uint64_t *trig, unsigned long long *n_trig, uint64_t cap) {
+                                     uint64_t hi, uint64_t *trig, unsigned long long *n_trig, uint64_t *def,
+                                     unsigned long long *n_def, uint64_t cap) {
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
   const uint64_t first = lo + uint64_t(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u);
   for (uint64_t i0 = first; i0 < hi; i0 += stride) {  // whole wavefronts iterate together
     const uint64_t i = i0 + (threadIdx.x & 63);
-    int64_t tk = -1;
+    int64_t tk = -1, df = -1;
     if (i < hi) {
       const uint64_t v = vals[i];
       bool t;
-      if (!place_new(ix, keys[i], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), t))
-        set_status(ix.hdr, SMETRIC_EINTERNAL);
+      const int pl = place_new(ix, keys[i], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), t, true);
+      if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+      else if (pl == DEFERRED) df = int64_t(i);
       else if (t) tk = int64_t(i);
     }
     append_wave(n_trig, trig, cap, tk);
+    append_wave(n_def, def, cap, df);
+  }
+}
+
+// Enter the deferred pairs once their keys are converted (or, with the pool exhausted,
+// as further plain slots).  Items index `keys` (and `vals`) directly, or through
+// `via` into the dedupe table (insert: session of the lowest request).
+__global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsigned long long *n_items,
+                                const int *abort_flag, const uint64_t *via, const uint64_t *dkey, const uint64_t *dw2,
+                                const uint32_t *session, uint32_t epoch, const uint64_t *keys,
+                                const uint64_t *vals) {
+  if (abort_flag && *abort_flag) return;
+  const uint64_t n = *n_items;
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const uint64_t t = items[i];
+    bool trig;
+    int pl;
+    if (via) {
+      const uint64_t h = via[t];
+      const uint64_t w = dw2[h];
+      pl = place_new(ix, dkey[h], uint32_t(w >> 32), epoch, session[uint32_t(w)], trig, false);
+    } else {
+      const uint64_t v = vals[t];
+      pl = place_new(ix, keys[t], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), trig, false);
+    }
+    if (pl != PLACED) set_status(ix.hdr, SMETRIC_EINTERNAL);
   }
 }
 
@@ -536,7 +746,7 @@ __global__ void set_counts_kernel(IndexHdr *h, unsigned long long n_entries) {
 }
 
 struct EvictWs {
-  unsigned long long *count;  // 2 counters
+  unsigned long long *count;  // gathered entries, conversion queue, deferred pairs
   uint64_t *ka, *va, *kb, *vb;  // entries and their sort ping-pong buffers
   uint64_t *ea, *eb, *ia, *ib;  // epoch sort keys and the permutation they carry
   void *temp;
@@ -717,6 +927,8 @@ extern "C" int smetric_index_insert(smetric_index *idx, const uint64_t *keys, co
   hipLaunchKernelGGL(ins_place_kernel, dim3(grid_for(uint64_t(n_blocks))), dim3(TB), 0, stream, ix, ws, session, epoch);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
                      ws.dkey, ws.list);
+  hipLaunchKernelGGL(deferred_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,
+                     ws.list, ws.dkey, ws.dw2, session, epoch, nullptr, nullptr);
   return hip_rc(hipGetLastError());
 }
 
@@ -750,9 +962,13 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   // the alternate sort buffers are free now: one holds the conversion queue
   uint64_t *trig = ws.ea;  // free once the sorted entries are in place
   unsigned long long *n_trig = ws.count + 1;
+  uint64_t *def = ws.ia;  // free as well
+  unsigned long long *n_def = ws.count + 2;
   hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n - m)), dim3(TB), 0, stream, ix, keys, vals, m, n, trig,
-                     n_trig, idx->capacity);
+                     n_trig, def, n_def, idx->capacity);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr);
+  hipLaunchKernelGGL(deferred_kernel, dim3(64), dim3(TB), 0, stream, ix, def, n_def, nullptr, nullptr, nullptr,
+                     nullptr, nullptr, 0u, keys, vals);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   return hip_rc(hipStreamSynchronize(stream));
 }
@@ -780,4 +996,39 @@ extern "C" int smetric_index_dump(const smetric_index *idx, uint64_t *keys_out, 
       return SMETRIC_EHIP;
   }
   return hip_rc(hipStreamSynchronize(stream));
+}
+
+extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe, uint64_t probe_bytes,
+                                           int32_t n_req, int64_t n_blocks, const int32_t *instance,
+                                           const uint32_t *session, uint32_t epoch, void *workspace,
+                                           uint64_t ws_bytes, hipStream_t stream) {
+  if (!idx || !idx->slots || n_req < 0 || n_blocks < 0 || n_blocks >= (int64_t(1) << 32) || epoch >= EPOCH_LIMIT)
+    return SMETRIC_EINVAL;
+  if (n_req == 0) return SMETRIC_OK;
+  if (!instance || !session) return SMETRIC_EINVAL;
+  if (!probe || (reinterpret_cast<uintptr_t>(probe) & 255) || probe_bytes < probe_layout(n_blocks, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) ||
+      ws_bytes < insert_ws_layout(n_blocks, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  ProbeView pv;
+  probe_layout(n_blocks, &pv, const_cast<void *>(probe));
+  InsWs ws;
+  insert_ws_layout(n_blocks, &ws, workspace);
+  const DevIndex ix = dev_view(idx);
+  int rc;
+  if ((rc = fill(ws.hdr, sizeof(WsHdr), 0, stream))) return rc;
+  const dim3 flat(FLAT_WG), blk(TB);
+  hipLaunchKernelGGL(insp_classify_kernel, flat, blk, 0, stream, ix, pv, ws, instance, session);
+  hipLaunchKernelGGL(insp_size_kernel, dim3(1), dim3(1), 0, stream, ws);
+  hipLaunchKernelGGL(insp_clear_kernel, dim3(grid_for(2 * uint64_t(n_blocks))), blk, 0, stream, ws);
+  hipLaunchKernelGGL(insp_dedupe_kernel, flat, blk, 0, stream, pv, ws, instance);
+  hipLaunchKernelGGL(insp_check_kernel, dim3(1), dim3(1), 0, stream, ix, ws);
+  hipLaunchKernelGGL(insp_refresh_kernel, flat, blk, 0, stream, ix, pv, ws, epoch);
+  hipLaunchKernelGGL(insp_place_kernel, flat, blk, 0, stream, ix, ws, session, epoch);
+  hipLaunchKernelGGL(spill_kernel, dim3(64), blk, 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
+                     ws.dkey, ws.list);
+  hipLaunchKernelGGL(deferred_kernel, dim3(64), blk, 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,
+                     ws.list, ws.dkey, ws.dw2, session, epoch, nullptr, nullptr);
+  return hip_rc(hipGetLastError());
 }

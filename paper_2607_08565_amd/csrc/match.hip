@@ -171,11 +171,41 @@ __device__ __forceinline__ uint64_t holder_word(const DevIndex &ix, uint32_t kin
   return 0;
 }
 
-template <int WPL>
+// Holder set of a block from its probe descriptor; MANY re-walks the chain.
+__device__ __forceinline__ Holders decode(const DevIndex &ix, uint64_t d, uint64_t key) {
+  Holders H;
+  H.kind = H_NONE;
+  H.rec = 0;
+#pragma unroll
+  for (int i = 0; i < LIST_MAX; ++i) H.h[i] = 0xFFFFFFFFu;
+  switch (desc_kind(d)) {
+    case D_ONE:
+      H.kind = H_LIST;
+      H.h[0] = desc_inst(d);
+      break;
+    case D_HOT:
+      H.kind = H_HOT;
+      H.rec = desc_x(d);
+      break;
+    case D_MANY:
+      H = probe(ix, key);
+      break;
+    default:
+      break;
+  }
+  return H;
+}
+
+// DESC = false: probe each block's chain here (early exit after the first all-miss
+// chunk).  DESC = true: read the descriptors written by the region-ordered probe.
+template <int WPL, bool DESC>
 __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
                                                         const int64_t *__restrict__ blk_off,
                                                         int32_t n_req, int64_t n_blocks,
-                                                        int32_t *__restrict__ matched) {
+                                                        int32_t *__restrict__ matched,
+                                                        const uint64_t *__restrict__ desc,
+                                                        const uint32_t *__restrict__ inv,
+                                                        const ProbeHdr *__restrict__ ph) {
   __shared__ int32_t nlist[MW][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * MW + wave;
@@ -184,7 +214,7 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
   int32_t *row = matched + int64_t(r) * I;
   for (int i = lane; i < I; i += 64) row[i] = 0;
   const int64_t b0 = blk_off[r], b1 = blk_off[r + 1];
-  if (!(b0 >= 0 && b0 <= b1 && b1 <= n_blocks)) {
+  if (!(b0 >= 0 && b0 <= b1 && b1 <= n_blocks) || (DESC && ph->err)) {
     if (lane == 0) set_status(ix.hdr, SMETRIC_EINVAL);
     return;
   }
@@ -201,10 +231,17 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
   for (int64_t j0 = 0; j0 < nb && mode != M_DONE; j0 += 64) {
     const int64_t j = j0 + lane;
     const bool valid = j < nb;
-    const uint64_t key = valid ? keys[b0 + j] : 0;
     Holders H;
+    uint64_t key = 0;
     if (valid) {
-      H = probe(ix, key);
+      if (DESC) {
+        const uint64_t d = desc[inv[b0 + j]];
+        if (desc_kind(d) == D_MANY) key = keys[b0 + j];
+        H = decode(ix, d, key);
+      } else {
+        key = keys[b0 + j];
+        H = probe(ix, key);
+      }
     } else {
       H.kind = H_NONE;
       H.rec = 0;
@@ -342,6 +379,26 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
   }
 }
 
+template <bool DESC>
+int launch_match(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                 int64_t n_blocks, int32_t *matched, const uint64_t *desc, const uint32_t *inv, const ProbeHdr *ph,
+                 hipStream_t stream) {
+  const DevIndex ix = dev_view(idx);
+  const dim3 grid((n_req + MW - 1) / MW), block(64 * MW);
+  const int wpl = (ix.words + 63) / 64;
+  if (wpl <= 1)
+    hipLaunchKernelGGL((match_kernel<1, DESC>), grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched, desc, inv, ph);
+  else if (wpl <= 2)
+    hipLaunchKernelGGL((match_kernel<2, DESC>), grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched, desc, inv, ph);
+  else if (wpl <= 4)
+    hipLaunchKernelGGL((match_kernel<4, DESC>), grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched, desc, inv, ph);
+  else if (wpl <= 8)
+    hipLaunchKernelGGL((match_kernel<8, DESC>), grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched, desc, inv, ph);
+  else
+    hipLaunchKernelGGL((match_kernel<16, DESC>), grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched, desc, inv, ph);
+  return hip_rc(hipGetLastError());
+}
+
 }  // namespace
 }  // namespace smk
 
@@ -352,18 +409,18 @@ extern "C" int smetric_match(const smetric_index *idx, const uint64_t *keys, con
   if (!idx || n_req < 0 || n_blocks < 0) return SMETRIC_EINVAL;
   if (n_req == 0) return SMETRIC_OK;
   if (!blk_off || !matched || (n_blocks > 0 && !keys) || !idx->slots) return SMETRIC_EINVAL;
-  const DevIndex ix = dev_view(idx);
-  const dim3 grid((n_req + MW - 1) / MW), block(64 * MW);
-  const int wpl = (ix.words + 63) / 64;
-  if (wpl <= 1)
-    hipLaunchKernelGGL(match_kernel<1>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
-  else if (wpl <= 2)
-    hipLaunchKernelGGL(match_kernel<2>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
-  else if (wpl <= 4)
-    hipLaunchKernelGGL(match_kernel<4>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
-  else if (wpl <= 8)
-    hipLaunchKernelGGL(match_kernel<8>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
-  else
-    hipLaunchKernelGGL(match_kernel<16>, grid, block, 0, stream, ix, keys, blk_off, n_req, n_blocks, matched);
-  return hip_rc(hipGetLastError());
+  return launch_match<false>(idx, keys, blk_off, n_req, n_blocks, matched, nullptr, nullptr, nullptr, stream);
+}
+
+extern "C" int smetric_match_probed(const smetric_index *idx, const void *probe, uint64_t probe_bytes,
+                                    const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                                    int64_t n_blocks, int32_t *matched, hipStream_t stream) {
+  if (!idx || n_req < 0 || n_blocks < 0 || n_blocks >= (int64_t(1) << 32)) return SMETRIC_EINVAL;
+  if (n_req == 0) return SMETRIC_OK;
+  if (!blk_off || !matched || (n_blocks > 0 && !keys) || !idx->slots) return SMETRIC_EINVAL;
+  if (!probe || (reinterpret_cast<uintptr_t>(probe) & 255) || probe_bytes < probe_layout(n_blocks, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  ProbeView pv;
+  probe_layout(n_blocks, &pv, const_cast<void *>(probe));
+  return launch_match<true>(idx, keys, blk_off, n_req, n_blocks, matched, pv.desc_p, pv.inv, pv.hdr, stream);
 }

@@ -66,6 +66,10 @@ def _load() -> C.CDLL:
         "smetric_index_evict_ws_bytes": [PIX, P],
         "smetric_index_evict": [PIX, U32, U32, P, U64, P],
         "smetric_index_dump": [PIX, P, P, U64, P, U64, P, P],
+        "smetric_probe_ws_bytes": [I64, P],
+        "smetric_probe": [PIX, P, P, I32, I64, P, U64, P],
+        "smetric_match_probed": [PIX, P, U64, P, P, I32, I64, P, P],
+        "smetric_index_insert_probed": [PIX, P, U64, I32, I64, P, P, U32, P, U64, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -80,6 +84,7 @@ EXPORTED = (
     "smetric_index_init", "smetric_index_attach", "smetric_index_stats", "smetric_match",
     "smetric_route", "smetric_index_insert_ws_bytes", "smetric_index_insert",
     "smetric_index_evict_ws_bytes", "smetric_index_evict", "smetric_index_dump",
+    "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
 )
 
 
@@ -146,6 +151,12 @@ def route(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tenso
 def insert_ws_bytes(n_blocks: int) -> int:
     b = C.c_uint64()
     _check("smetric_index_insert_ws_bytes", _lib.smetric_index_insert_ws_bytes(n_blocks, C.byref(b)))
+    return int(b.value)
+
+
+def probe_ws_bytes(n_blocks: int) -> int:
+    b = C.c_uint64()
+    _check("smetric_probe_ws_bytes", _lib.smetric_probe_ws_bytes(n_blocks, C.byref(b)))
     return int(b.value)
 
 
@@ -225,6 +236,36 @@ class Index:
             C.c_void_p(ws.data_ptr()), ws.numel(), C.byref(got), _stream()))
         assert int(got.value) == n
         return keys[:n].cpu().numpy(), vals[:n].cpu().numpy()
+
+    # region-ordered path: probe once, then match and insert from the probe state
+    def probe(self, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int, state: torch.Tensor | None = None):
+        R = blk_off.numel() - 1
+        need = probe_ws_bytes(n_blocks)
+        if state is None or state.numel() < need:
+            state = torch.empty(need, dtype=torch.uint8, device=keys.device)
+        _check("smetric_probe", _lib.smetric_probe(
+            self.ref, _dev(keys, torch.uint64, "keys"), _dev(blk_off, torch.int64, "blk_off"), R, n_blocks,
+            C.c_void_p(state.data_ptr()), state.numel(), _stream()))
+        return state
+
+    def match_probed(self, state: torch.Tensor, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int,
+                     matched: torch.Tensor | None = None) -> torch.Tensor:
+        R = blk_off.numel() - 1
+        if matched is None:
+            matched = torch.empty((max(R, 1), self.n_instances), dtype=torch.int32, device=keys.device)
+        _check("smetric_match_probed", _lib.smetric_match_probed(
+            self.ref, C.c_void_p(state.data_ptr()), state.numel(), _dev(keys, torch.uint64, "keys"),
+            _dev(blk_off, torch.int64, "blk_off"), R, n_blocks, _dev(matched, torch.int32, "matched"), _stream()))
+        return matched[:R]
+
+    def insert_probed(self, state: torch.Tensor, n_req: int, n_blocks: int, instance: torch.Tensor,
+                      session: torch.Tensor, epoch: int, workspace: torch.Tensor | None = None):
+        ws = self._workspace(insert_ws_bytes(n_blocks)) if workspace is None else workspace
+        sess = _dev(session, torch.int32, "session") if session.dtype == torch.int32 else _dev(session, torch.uint32, "session")
+        _check("smetric_index_insert_probed", _lib.smetric_index_insert_probed(
+            self.ref, C.c_void_p(state.data_ptr()), state.numel(), n_req, n_blocks,
+            _dev(instance, torch.int32, "instance"), sess, C.c_uint32(epoch), C.c_void_p(ws.data_ptr()), ws.numel(),
+            _stream()))
 
     def snapshot(self) -> torch.Tensor:
         return self.mem.clone()

@@ -65,12 +65,18 @@ class Pair:
         bad = np.nonzero(gv != ov)[0]
         assert len(bad) == 0, f"{what}: {len(bad)} dumped values differ, e.g. {[(hex(gv[i]), hex(ov[i])) for i in bad[:3]]}"
 
-    def step(self, batch: W.Batch, params=None, rr_base=None, check_dump=True, what=""):
-        """hash -> match -> route -> insert at target; returns (targets, branches)."""
+    def step(self, batch: W.Batch, params=None, rr_base=None, check_dump=True, what="", probed=False):
+        """hash -> match -> route -> insert at target; returns (targets, branches).
+        probed: the region-ordered path (probe once; match and insert from the probe state)."""
         params = params or W.DEFAULT_PARAMS
         rr = batch.rr_base if rr_base is None else rr_base
         d_boff, nb, d_keys, okeys, blk_off = self.hash_both(batch.tokens, batch.tok_off)
-        gm = self.gix.match(d_keys, d_boff, nb)
+        state = None
+        if probed:
+            state = self.gix.probe(d_keys, d_boff, nb)
+            gm = self.gix.match_probed(state, d_keys, d_boff, nb)
+        else:
+            gm = self.gix.match(d_keys, d_boff, nb)
         om = self.oix.match(okeys, blk_off)
         g = gm.cpu().numpy()
         bad = np.argwhere(g != om)
@@ -81,7 +87,12 @@ class Pair:
         gt, gb = gt.cpu().numpy(), gb.cpu().numpy()
         assert np.array_equal(gt, ot), f"{what}: targets differ at {np.nonzero(gt != ot)[0][:5]}"
         assert np.array_equal(gb, ob), f"{what}: branches differ at {np.nonzero(gb != ob)[0][:5]}"
-        rc = self.insert_both(d_keys, d_boff, nb, okeys, blk_off, ot, batch.session, batch.epoch)
+        if probed:
+            self.gix.insert_probed(state, batch.n_req, nb, to_dev(np.asarray(ot, np.int32)),
+                                   to_dev(np.asarray(batch.session, np.uint32)), batch.epoch)
+            rc = self.oix.insert(okeys, blk_off, ot, batch.session, batch.epoch)
+        else:
+            rc = self.insert_both(d_keys, d_boff, nb, okeys, blk_off, ot, batch.session, batch.epoch)
         assert rc == 0, f"{what}: oracle insert rc {rc}"
         if check_dump:
             self.compare_index(what)
@@ -89,7 +100,7 @@ class Pair:
 
 
 def run_sessions(wl: W.SessionWorkload, n_batches: int, capacity: int, evict: tuple[int, int] | None = None,
-                 placement_epoch_offset: int = 0):
+                 probed: bool = False):
     """Batch t = turn t of every session.  Open-loop workloads (with a placement) first
     enter turn t-1 on its placed instance; closed-loop ones rely on the post-route insert."""
     pair = Pair(capacity, wl.n_inst)
@@ -102,7 +113,7 @@ def run_sessions(wl: W.SessionWorkload, n_batches: int, capacity: int, evict: tu
             assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, wl.placement[t - 1], prevb.session, t - 1) == 0
         b = wl.batch(t, prev_targets)
         say(f"  batch {t}: R={b.n_req} tokens={b.n_tokens}")
-        tg, br = pair.step(b, what=f"batch {t}")
+        tg, br = pair.step(b, what=f"batch {t}", probed=probed)
         branches.append(br)
         prev_targets = tg
         if evict is not None:

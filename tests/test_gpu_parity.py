@@ -64,28 +64,32 @@ def test_hash_bad_offsets_flag_status_without_writing():
     assert got[3:].tolist() == ok.tolist()  # the good one is unaffected
 
 
-def test_config0_open_loop_full():
+@pytest.mark.parametrize("probed", [False, True])
+def test_config0_open_loop_full(probed):
     """The tiny trace at full size: 8 instances, 64 sessions x 4 turns."""
-    pair, br = run_sessions(W.config0(), 4, capacity=200_000)
+    pair, br = run_sessions(W.config0(), 4, capacity=200_000, probed=probed)
     assert set(br.tolist()) >= {0, 2}
 
 
-def test_config1_scaled_closed_loop():
+@pytest.mark.parametrize("probed", [False, True])
+def test_config1_scaled_closed_loop(probed):
     wl = W.config1(n_sess=192, n_turns=8, l0=1024, app=(64, 1536), cap=16384, prefix_len=512)
-    pair, br = run_sessions(wl, 8, capacity=2_000_000)
+    pair, br = run_sessions(wl, 8, capacity=2_000_000, probed=probed)
     say("branches", np.bincount(br, minlength=5).tolist())
 
 
-def test_config2_scaled_prev_counts():
+@pytest.mark.parametrize("probed", [False, True])
+def test_config2_scaled_prev_counts(probed):
     wl = W.config2(n_sess=48, n_turns=10, l0=4096, app=(128, 3000), cap=40000, prefix_len=2048)
-    run_sessions(wl, 10, capacity=2_000_000)
+    run_sessions(wl, 10, capacity=2_000_000, probed=probed)
 
 
-def test_config3_scaled_with_eviction():
+@pytest.mark.parametrize("probed", [False, True])
+def test_config3_scaled_with_eviction(probed):
     """One shared prefix held by every instance (bitmap records, WIDE alive sets of 128),
     divergent tails, 5 % LRU eviction after every batch (orphaned descendants)."""
     wl = W.config3(n_sess=160, n_turns=5, prefix_len=4096, tail=(256, 3000), app=512)
-    run_sessions(wl, 5, capacity=400_000, evict=(1, 20))
+    run_sessions(wl, 5, capacity=400_000, evict=(1, 20), probed=probed)
 
 
 def test_many_instances_wide_words():
@@ -109,6 +113,7 @@ def test_many_instances_wide_words():
                     turn=np.array([1, 0], np.int32), session=np.array([9, 10], np.uint32),
                     q=rng.integers(0, 50, I) * W.Q_UNIT_NS, rr_base=17, epoch=2)
     pair.step(batch, what="I=5000")
+    pair.step(batch, what="I=5000 probed", probed=True)
 
 
 def test_max_instances():
@@ -128,6 +133,7 @@ def test_max_instances():
                 hist_len=np.array([512], np.int32), turn=np.array([1], np.int32), session=np.array([1], np.uint32),
                 q=np.zeros(I, np.int64), rr_base=0, epoch=4)
     pair.step(b, what="I=65536")
+    pair.step(b, what="I=65536 probed", probed=True)
 
 
 def test_hot_keys_pool_exhaustion_and_long_lists():
@@ -147,6 +153,7 @@ def test_hot_keys_pool_exhaustion_and_long_lists():
                 prompt_len=np.full(4, 2400, np.int32), hist_len=np.full(4, 1600, np.int32),
                 turn=np.ones(4, np.int32), session=np.arange(4, dtype=np.uint32), q=np.zeros(I, np.int64), epoch=2)
     pair.step(b, what="hot")
+    pair.step(b, what="hot probed", probed=True)
 
 
 def test_duplicate_pairs_in_batch_take_lowest_request():
@@ -210,6 +217,7 @@ def test_empty_batch_and_single_instance():
                 turn=np.array([0, 1, 2, 0, 1], np.int32), session=np.arange(5, dtype=np.uint32), q=np.array([7], np.int64))
     pair.step(b, what="I=1 a")
     pair.step(b, what="I=1 b")
+    pair.step(b, what="I=1 c", probed=True)
     assert S.version() >= 1
 
 
@@ -239,3 +247,23 @@ def test_route_edge_parameters():
     assert set(ob[[5, 6, 7, 8, 9]].tolist()) == {255}
     with pytest.raises(S.SmetricError):
         S.route(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), dict(W.DEFAULT_PARAMS, hit_num=2, hit_den=2))
+
+
+def test_probed_path_rejects_untiled_requests():
+    """The region-ordered path needs requests that tile the keys; otherwise every row is
+    zero, the status is EINVAL and the insert changes nothing."""
+    rng = np.random.default_rng(13)
+    pair = Pair(10_000, 4)
+    toks, off = _rand_prompts(rng, 3, 200, 400)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+    pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, [0, 1, 2], [1, 2, 3], 1)
+    before = pair.gix.dump()
+    gapped = to_dev(np.array([0, blk_off[1], blk_off[2], nb - 1], np.int64))  # last block uncovered
+    state = pair.gix.probe(d_keys, gapped, nb)
+    m = pair.gix.match_probed(state, d_keys, gapped, nb).cpu().numpy()
+    assert not m.any()
+    pair.gix.insert_probed(state, 3, nb, to_dev(np.array([1, 1, 1], np.int32)), to_dev(np.array([5, 6, 7], np.uint32)), 2)
+    n, st = pair.gix.stats()
+    assert st == oracle.EINVAL
+    after = pair.gix.dump()
+    assert all(np.array_equal(a, b) for a, b in zip(before, after))
