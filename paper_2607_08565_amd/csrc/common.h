@@ -155,13 +155,14 @@ struct ProbeHdr {
   int err;                          // first input error (EINVAL) found while partitioning
   int pad0;
   unsigned long long n;             // number of blocks probed (0 when invalid)
+  unsigned long long tot[NREG];     // blocks per region
 };
 struct ProbeView {
   ProbeHdr *hdr;
   uint32_t *req_of;     // block order: request of each block
   uint32_t *inv;        // block order: position of the block in region order
-  uint32_t *hist;       // [NREG][PART_WG] blocks of each region in each partition chunk
-  uint64_t *base;       // [NREG][PART_WG] first region-order position of each (region, chunk)
+  uint32_t *hist;       // [PART_WG][NREG] blocks of each region in each partition chunk
+  uint64_t *base;       // [PART_WG][NREG] first region-order position of each (chunk, region)
   uint64_t *part_key;   // region order: key
   uint64_t *part_br;    // region order: block index | request << 32
   uint64_t *desc_p;     // region order: holder descriptor

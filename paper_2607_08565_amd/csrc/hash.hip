@@ -5,16 +5,20 @@
 // SplitMix64 constants, the NH digest of each block, a position salt, an affine chain
 // s_j = M s_{j-1} + e_j and a finalised key.
 //
-// Mapping to gfx950: one 64-lane wavefront per request walks it in tiles of 64 blocks.
-//  * B = 16 (the fast path): tokens are read as 16-byte vectors, lane l of load u taking
-//    tokens [256u + 4l, 256u + 4l + 4) of the tile, so every load instruction covers 1 KB
-//    of contiguous HBM.  Four lanes share a block; each forms the NH products of its two
-//    token pairs and a quad reduction (DPP quad permutes) yields the block digest.
-//  * other even B: lane l digests block l of the tile sequentially.
+// Mapping to gfx950: requests are cut into tiles of 64 blocks.
+//  * B = 16 (the fast path): one workgroup of four wavefronts per request, wavefront w
+//    taking tiles w, w + 4, ... and loading its next tile while it hashes the current one,
+//    so long prompts do not serialise on one wavefront.  Tokens are read as 16-byte
+//    vectors, lane l of load u taking tokens [256u + 4l, 256u + 4l + 4) of the tile, so
+//    every load instruction covers 1 KB of contiguous HBM.  Four lanes share a block;
+//    each forms the NH products of its two token pairs and a quad reduction (DPP quad
+//    permutes) yields the block digest.
+//  * other even B: one wavefront per request; lane l digests block l of the tile.
 //  Digests go through LDS so that lane l then owns block l of the tile; the chain is an
 //  inclusive scan of affine maps x -> M x + e_l across the wavefront (Kogge-Stone with
-//  the uniform multipliers M^1..M^32), seeded with the carry from the previous tile.
-//  Because the chain is affine, this scan equals the sequential definition exactly.
+//  the uniform multipliers M^1..M^32).  A tile's carry-in composes the affine maps of
+//  the tiles before it.  Because the chain is affine, this equals the sequential
+//  definition exactly.
 #include "common.h"
 
 namespace smk {
@@ -111,27 +115,49 @@ __device__ __forceinline__ bool request_ok(const int64_t *tok_off, const int64_t
          nb == (t1 - t0) / B;
 }
 
-constexpr int WAVES = 1;
+constexpr int WAVES = 1;  // wavefronts per workgroup of the generic kernel
 
-// B = 16 fast path.
-__global__ __launch_bounds__(64 * WAVES) void hash16_kernel(const int32_t *__restrict__ tokens,
-                                                            int64_t n_tokens,
-                                                            const int64_t *__restrict__ tok_off,
-                                                            const int64_t *__restrict__ blk_off,
-                                                            int32_t n_req, int64_t n_blocks,
-                                                            uint64_t seed,
-                                                            uint64_t *__restrict__ keys,
-                                                            int32_t *status) {
-  __shared__ uint64_t dig[WAVES][64];
+// B = 16 fast path: one workgroup of NW wavefronts per request.  Step k covers tiles
+// [k NW, k NW + NW): wavefront w digests tile k NW + w and scans it from a zero state;
+// the tiles' aggregates meet in LDS, and wavefront w's carry-in is the step's carry
+// advanced through the aggregates of the tiles before its own (x -> M^64 x + agg, as
+// every tile before the request's last is full).  Each wavefront loads its next tile's
+// tokens before working on the current one.
+constexpr int NW = 4;
+
+struct Tile16 {
+  int4 v[4];
+};
+
+__device__ __forceinline__ void load_tile16(const int32_t *x, int64_t tile, int64_t nb, int q, int lane, Tile16 &t) {
+  const int64_t j0 = tile * 64;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int blk = 16 * u + (lane >> 2);
+    if (j0 + blk < nb) __builtin_memcpy(&t.v[u], x + (j0 + blk) * 16 + 4 * q, 16);
+    else t.v[u] = make_int4(0, 0, 0, 0);
+  }
+}
+
+__global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restrict__ tokens,
+                                                         int64_t n_tokens,
+                                                         const int64_t *__restrict__ tok_off,
+                                                         const int64_t *__restrict__ blk_off,
+                                                         int32_t n_req, int64_t n_blocks,
+                                                         uint64_t seed,
+                                                         uint64_t *__restrict__ keys,
+                                                         int32_t *status) {
+  __shared__ uint64_t dig[NW][64];
+  __shared__ uint64_t agg[NW];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int r = blockIdx.x * WAVES + wave;
-  if (r >= n_req) return;
+  const int r = blockIdx.x;
   int64_t t0, b0, nb;
   if (!request_ok(tok_off, blk_off, r, n_tokens, n_blocks, 16, t0, b0, nb)) {
-    if (lane == 0 && status) atomicCAS(status, 0, SMETRIC_EINVAL);
-    return;
+    if (threadIdx.x == 0 && status) atomicCAS(status, 0, SMETRIC_EINVAL);
+    return;  // the whole workgroup leaves before any barrier
   }
   const ChainConsts cc = chain_consts(seed, 16);
+  const uint64_t M64 = cc.Mpow[5] * cc.Mpow[5];
   // this lane's four offset constants: K[4q .. 4q+3], q = lane % 4
   const int q = lane & 3;
   const uint32_t k0 = uint32_t(splitmix_out(seed, 4 * q + 0));
@@ -139,28 +165,46 @@ __global__ __launch_bounds__(64 * WAVES) void hash16_kernel(const int32_t *__res
   const uint32_t k2 = uint32_t(splitmix_out(seed, 4 * q + 2));
   const uint32_t k3 = uint32_t(splitmix_out(seed, 4 * q + 3));
   const int32_t *x = tokens + t0;
-  uint64_t carry = cc.s_init;
-  for (int64_t j0 = 0; j0 < nb; j0 += 64) {
-    const int n_valid = int(nb - j0 < 64 ? nb - j0 : 64);
+  const int64_t n_tiles = (nb + 63) / 64;
+  uint64_t carry = cc.s_init;  // chain state before the step's first block
+  Tile16 cur, nxt;
+  load_tile16(x, wave, nb, q, lane, cur);
+  for (int64_t step0 = 0; step0 < n_tiles; step0 += NW) {
+    const int64_t tile = step0 + wave;
+    load_tile16(x, tile + NW, nb, q, lane, nxt);
+    const int64_t j0 = tile * 64;
+    const int64_t left = nb - j0;
+    const int n_valid = int(left <= 0 ? 0 : (left < 64 ? left : 64));
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int blk = 16 * u + (lane >> 2);  // block within the tile
-      uint64_t part = 0;
-      if (blk < n_valid) {
-        int4 v;
-        __builtin_memcpy(&v, x + (j0 + blk) * 16 + 4 * q, 16);
-        part = uint64_t(uint32_t(v.x) + k0) * uint64_t(uint32_t(v.y) + k1) +
-               uint64_t(uint32_t(v.z) + k2) * uint64_t(uint32_t(v.w) + k3);
-      }
+      const int4 v = cur.v[u];
+      uint64_t part = uint64_t(uint32_t(v.x) + k0) * uint64_t(uint32_t(v.y) + k1) +
+                      uint64_t(uint32_t(v.z) + k2) * uint64_t(uint32_t(v.w) + k3);
       part += dpp64<0xB1>(part);  // quad_perm [1,0,3,2]
       part += dpp64<0x4E>(part);  // quad_perm [2,3,0,1]
-      if (q == 0) dig[wave][blk] = part;
+      if (q == 0) dig[wave][16 * u + (lane >> 2)] = part;
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    const uint64_t d = dig[wave][lane];
-    carry = finish_tile(d, j0, n_valid, carry, cc, keys + b0 + j0);
-    __builtin_amdgcn_wave_barrier();
+    // local inclusive scan of the tile's affine maps from state 0
+    uint64_t v = lane < n_valid ? finalise(dig[wave][lane] + uint64_t(j0 + lane)) : 0;
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+      const int dist = 1 << k;
+      const uint64_t t = shfl_up64(v, dist);
+      if (lane >= dist) v += cc.Mpow[k] * t;
+    }
+    if (lane == 63) agg[wave] = v;
+    __syncthreads();
+    uint64_t c = carry;
+    for (int w = 0; w < wave; ++w) c = M64 * c + agg[w];
+    if (lane < n_valid) keys[b0 + j0 + lane] = remap(finalise(cc.Mlane * c + v));
+    uint64_t next = carry;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) next = M64 * next + agg[w];
+    carry = next;  // used only when every tile of this step was full
+    __syncthreads();
+    cur = nxt;
   }
 }
 
@@ -212,7 +256,7 @@ extern "C" int smetric_hash_blocks(const int32_t *tokens, int64_t n_tokens, cons
     return SMETRIC_EINVAL;
   const dim3 grid((n_req + WAVES - 1) / WAVES), block(64 * WAVES);
   if (block_size == 16)
-    hipLaunchKernelGGL(hash16_kernel, grid, block, 0, stream, tokens, n_tokens, tok_off, blk_off,
+    hipLaunchKernelGGL(hash16_kernel, dim3(n_req), dim3(64 * NW), 0, stream, tokens, n_tokens, tok_off, blk_off,
                        n_req, n_blocks, seed, keys, status);
   else
     hipLaunchKernelGGL(hash_generic_kernel, grid, block, 0, stream, tokens, n_tokens, tok_off,

@@ -301,15 +301,29 @@ struct WsHdr {
 };
 static_assert(sizeof(WsHdr) == 256, "ws header size");
 
+// Dedupe table slot: the pair's key and (inst + 1) << 32 | lowest request index, both in
+// one 16-byte slot so a pair costs one line; all-zero = free.
+struct DSlot {
+  uint64_t key;
+  uint64_t w2;
+};
+__device__ __forceinline__ uint32_t dd_inst(uint64_t w2) { return uint32_t(w2 >> 32) - 1; }
+__device__ __forceinline__ uint32_t dd_req(uint64_t w2) { return uint32_t(w2); }
+
+// Candidate of the region-ordered insert: an absent pair, as it enters the dedupe.
+struct Cand {
+  uint64_t key;
+  uint64_t w2;  // same encoding as DSlot::w2
+};
+
 struct InsWs {
   WsHdr *hdr;
   uint64_t *pos;    // per block: slot + 1 of an entry to refresh, 0 = none
-  uint64_t *dkey;   // dedupe table keys
-  uint64_t *dw2;    // dedupe table: inst << 32 | lowest request index, ~0 = free
+  DSlot *dd;        // dedupe table
   uint64_t *list;   // dedupe slots of distinct new pairs
   uint64_t *trig;   // keys queued for conversion
   uint64_t *def;    // list positions of deferred new pairs
-  uint64_t *cand;   // region-ordered insert: positions of absent pairs, one segment per workgroup
+  Cand *cand;       // region-ordered insert: absent pairs, one segment per workgroup
   uint32_t *cand_cnt;  // entries in each workgroup's candidate segment
   uint32_t *list_cnt;  // entries in each workgroup's new-pair segment
   uint64_t n_dedupe;
@@ -336,24 +350,22 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
   };
   const uint64_t o_hdr = take(sizeof(WsHdr));
   const uint64_t o_pos = take(8 * n);
-  const uint64_t o_dkey = take(8 * nd);
-  const uint64_t o_dw2 = take(8 * nd);
+  const uint64_t o_dd = take(16 * nd);
   const uint64_t o_list = take(8 * nl);
   const uint64_t o_trig = take(8 * nl);
   const uint64_t o_def = take(8 * nl);
-  const uint64_t o_cand = take(8 * seg_n);
+  const uint64_t o_cand = take(16 * seg_n);
   const uint64_t o_cc = take(4 * FLAT_WG);
   const uint64_t o_lc = take(4 * FLAT_WG);
   if (ws) {
     char *b = static_cast<char *>(base);
     ws->hdr = reinterpret_cast<WsHdr *>(b + o_hdr);
     ws->pos = reinterpret_cast<uint64_t *>(b + o_pos);
-    ws->dkey = reinterpret_cast<uint64_t *>(b + o_dkey);
-    ws->dw2 = reinterpret_cast<uint64_t *>(b + o_dw2);
+    ws->dd = reinterpret_cast<DSlot *>(b + o_dd);
     ws->list = reinterpret_cast<uint64_t *>(b + o_list);
     ws->trig = reinterpret_cast<uint64_t *>(b + o_trig);
     ws->def = reinterpret_cast<uint64_t *>(b + o_def);
-    ws->cand = reinterpret_cast<uint64_t *>(b + o_cand);
+    ws->cand = reinterpret_cast<Cand *>(b + o_cand);
     ws->cand_cnt = reinterpret_cast<uint32_t *>(b + o_cc);
     ws->list_cnt = reinterpret_cast<uint32_t *>(b + o_lc);
     ws->n_dedupe = nd;
@@ -367,24 +379,24 @@ __device__ __forceinline__ void ws_error(WsHdr *h, int e) { atomicCAS(&h->err, 0
 
 // Returns the dedupe slot when this call created the entry (first sighting of the
 // pair), else -1; the caller lists created slots with one atomic per wavefront.
-__device__ int64_t dedupe_pair(const InsWs &ws, uint64_t nd, uint64_t key, uint32_t inst, uint32_t r) {
-  const uint64_t mine = (uint64_t(inst) << 32) | r;
-  uint64_t h = mix64(key ^ ((uint64_t(inst) + 1) * 0xC2B2AE3D27D4EB4Full)) & (nd - 1);
+__device__ int64_t dedupe_pair(const InsWs &ws, uint64_t nd, uint64_t key, uint64_t mine) {
+  uint64_t h = mix64(key ^ ((mine >> 32) * 0xC2B2AE3D27D4EB4Full)) & (nd - 1);
   for (uint64_t step = 0; step < nd; ++step, h = (h + 1) & (nd - 1)) {
-    uint64_t k = __hip_atomic_load(&ws.dkey[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (k == KEY_EMPTY) k = atomicCAS(reinterpret_cast<unsigned long long *>(&ws.dkey[h]), KEY_EMPTY, key);
+    DSlot *d = ws.dd + h;
+    uint64_t k = __hip_atomic_load(&d->key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (k == KEY_EMPTY) k = atomicCAS(reinterpret_cast<unsigned long long *>(&d->key), KEY_EMPTY, key);
     if (k != KEY_EMPTY && k != key) continue;
     // this slot's key is `key`; its owner instance is decided by the second word
-    uint64_t w = __hip_atomic_load(&ws.dw2[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint64_t w = __hip_atomic_load(&d->w2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     while (true) {
-      if (w == ~uint64_t(0)) {
-        const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&ws.dw2[h]), ~0ull, mine);
-        if (prev == ~uint64_t(0)) return int64_t(h);
+      if (w == 0) {
+        const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&d->w2), 0ull, mine);
+        if (prev == 0) return int64_t(h);
         w = prev;
         continue;
       }
-      if ((w >> 32) == inst) {
-        atomicMin(reinterpret_cast<unsigned long long *>(&ws.dw2[h]), mine);
+      if ((w >> 32) == (mine >> 32)) {
+        if (mine < w) atomicMin(reinterpret_cast<unsigned long long *>(&d->w2), mine);
         return -1;
       }
       break;  // another instance's pair: keep probing
@@ -453,7 +465,7 @@ __global__ __launch_bounds__(64 * IW) void ins_probe_kernel(DevIndex ix, InsWs w
           ws.pos[b0 + j] = val_epoch(f.val) < epoch ? uint64_t(f.slot) + 1 : 0;
         } else {
           ws.pos[b0 + j] = 0;
-          fresh = dedupe_pair(ws, ws.n_dedupe, key, uint32_t(inst), uint32_t(r));
+          fresh = dedupe_pair(ws, ws.n_dedupe, key, ((uint64_t(inst) + 1) << 32) | uint32_t(r));
         }
       }
     }
@@ -501,12 +513,9 @@ __global__ void ins_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
     const uint64_t i = i0 + (threadIdx.x & 63);
     int64_t tk = -1, df = -1;
     if (i < n) {
-      const uint64_t h = ws.list[i];
-      const uint64_t key = ws.dkey[h];
-      const uint64_t w = ws.dw2[h];
-      const uint32_t inst = uint32_t(w >> 32), r = uint32_t(w);
+      const DSlot d = ws.dd[ws.list[i]];
       bool trig;
-      const int pl = place_new(ix, key, inst, epoch, session[r], trig, true);
+      const int pl = place_new(ix, d.key, dd_inst(d.w2), epoch, session[dd_req(d.w2)], trig, true);
       if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
       else if (pl == DEFERRED) df = int64_t(i);
       else if (trig) tk = int64_t(i);
@@ -516,16 +525,16 @@ __global__ void ins_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
   }
 }
 
-// Convert the queued keys.  trig holds indexes: key = keys[via[idx]] when `via` is
+// Convert the queued keys.  trig holds indexes: key = dd[via[idx]].key when `dd` is
 // given (insert: positions in the dedupe list), else keys[idx] (rebuild).
 __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned long long *n_trig,
-                             const int *abort_flag, const uint64_t *keys, const uint64_t *via) {
+                             const int *abort_flag, const uint64_t *keys, const DSlot *dd, const uint64_t *via) {
   if (abort_flag && *abort_flag) return;
   const uint64_t n = *n_trig;
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
   for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
     const uint64_t t = trig[i];
-    const uint64_t key = via ? keys[via[t]] : keys[t];
+    const uint64_t key = dd ? dd[via[t]].key : keys[t];
     if (!spill_key(ix, key)) set_status(ix.hdr, SMETRIC_EINTERNAL);
   }
 }
@@ -552,7 +561,7 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
     if (threadIdx.x == 0) ws.cand_cnt[blockIdx.x] = 0;
     return;
   }
-  uint64_t *seg = ws.cand + uint64_t(blockIdx.x) * ws.seg;
+  Cand *seg = ws.cand + uint64_t(blockIdx.x) * ws.seg;
   const uint64_t span = uint64_t(gridDim.x) * TB;
   for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += span) {
     const uint64_t key = pv.part_key[i];
@@ -575,7 +584,7 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
         slot = find_entry(ix, key, uint32_t(t)).slot;
       }
       if (slot >= 0) pos = uint64_t(slot) + 1;
-      else seg[atomicAdd(&lc, 1u)] = i;
+      else seg[atomicAdd(&lc, 1u)] = Cand{key, ((uint64_t(t) + 1) << 32) | r};
     }
     ws.pos[i] = pos;
   }
@@ -583,47 +592,58 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
   if (threadIdx.x == 0) ws.cand_cnt[blockIdx.x] = lc;
 }
 
-// total candidates -> size of the dedupe table: the least power of two >= 2 x candidates
-__global__ void insp_size_kernel(InsWs ws) {
+// Sum of the FLAT_WG per-workgroup counts, by one workgroup of TB threads.
+__device__ unsigned long long sum_counts(const uint32_t *cnt) {
+  __shared__ unsigned long long part[TB / 64];
   unsigned long long c = 0;
-  for (int w = 0; w < FLAT_WG; ++w) c += ws.cand_cnt[w];
+  for (int w = threadIdx.x; w < FLAT_WG; w += TB) c += cnt[w];
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = c;
+  __syncthreads();
+  unsigned long long all = 0;
+#pragma unroll
+  for (int i = 0; i < TB / 64; ++i) all += part[i];
+  return all;
+}
+
+// total candidates -> size of the dedupe table: the least power of two >= 1.5 x candidates
+__global__ __launch_bounds__(TB) void insp_size_kernel(InsWs ws) {
+  const unsigned long long c = sum_counts(ws.cand_cnt);
+  if (threadIdx.x != 0) return;
   ws.hdr->n_cand = c;
   uint64_t nd = 64;
-  while (nd < 2 * c && nd < ws.n_dedupe) nd <<= 1;
+  while (nd < c + c / 2 && nd < ws.n_dedupe) nd <<= 1;
   ws.hdr->n_dd = nd;
 }
 
-__global__ void insp_clear_kernel(InsWs ws) {
-  const uint64_t nd = ws.hdr->n_dd;
+__global__ void dd_clear_kernel(DSlot *dd, uint64_t n, const unsigned long long *n_dev) {
+  const uint64_t nd = n_dev ? *n_dev : n;
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t h = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; h < nd; h += stride) {
-    ws.dkey[h] = KEY_EMPTY;
-    ws.dw2[h] = ~uint64_t(0);
-  }
+  for (uint64_t h = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; h < nd; h += stride) dd[h] = DSlot{0, 0};
 }
 
 // workgroup w deduplicates its candidate segment into its new-pair segment
-__global__ __launch_bounds__(TB) void insp_dedupe_kernel(ProbeView pv, InsWs ws, const int32_t *instance) {
+__global__ __launch_bounds__(TB) void insp_dedupe_kernel(InsWs ws) {
   __shared__ unsigned int lc;
   if (threadIdx.x == 0) lc = 0;
   __syncthreads();
   const uint64_t nd = ws.hdr->n_dd;
   const uint32_t n = ws.cand_cnt[blockIdx.x];
-  const uint64_t *in = ws.cand + uint64_t(blockIdx.x) * ws.seg;
+  const Cand *in = ws.cand + uint64_t(blockIdx.x) * ws.seg;
   uint64_t *out = ws.list + uint64_t(blockIdx.x) * ws.seg;
   for (uint32_t k = threadIdx.x; k < n; k += TB) {
-    const uint64_t i = in[k];
-    const uint32_t r = uint32_t(pv.part_br[i] >> 32);
-    const int64_t h = dedupe_pair(ws, nd, pv.part_key[i], uint32_t(instance[r]), r);
+    const Cand c = in[k];
+    const int64_t h = dedupe_pair(ws, nd, c.key, c.w2);
     if (h >= 0) out[atomicAdd(&lc, 1u)] = uint64_t(h);
   }
   __syncthreads();
   if (threadIdx.x == 0) ws.list_cnt[blockIdx.x] = lc;
 }
 
-__global__ void insp_check_kernel(DevIndex ix, InsWs ws) {
-  unsigned long long c = 0;
-  for (int w = 0; w < FLAT_WG; ++w) c += ws.list_cnt[w];
+__global__ __launch_bounds__(TB) void insp_check_kernel(DevIndex ix, InsWs ws) {
+  const unsigned long long c = sum_counts(ws.list_cnt);
+  if (threadIdx.x != 0) return;
   WsHdr *h = ws.hdr;
   h->n_new = c;
   const int e = h->err != 0 ? h->err : (ix.hdr->n_entries + c > ix.capacity ? SMETRIC_EFULL : 0);
@@ -658,10 +678,9 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
     const uint32_t k = k0 + threadIdx.x;
     int64_t tk = -1, df = -1;
     if (k < n) {
-      const uint64_t h = ws.list[base + k];
-      const uint64_t key = ws.dkey[h], w = ws.dw2[h];
+      const DSlot d = ws.dd[ws.list[base + k]];
       bool trig;
-      const int pl = place_new(ix, key, uint32_t(w >> 32), epoch, session[uint32_t(w)], trig, true);
+      const int pl = place_new(ix, d.key, dd_inst(d.w2), epoch, session[dd_req(d.w2)], trig, true);
       if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
       else if (pl == DEFERRED) df = int64_t(base + k);
       else if (trig) tk = int64_t(base + k);
@@ -716,9 +735,9 @@ __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const ui
 
 // Enter the deferred pairs once their keys are converted (or, with the pool exhausted,
 // as further plain slots).  Items index `keys` (and `vals`) directly, or through
-// `via` into the dedupe table (insert: session of the lowest request).
+// `via` into the dedupe table `dd` (insert: session of the lowest request).
 __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsigned long long *n_items,
-                                const int *abort_flag, const uint64_t *via, const uint64_t *dkey, const uint64_t *dw2,
+                                const int *abort_flag, const uint64_t *via, const DSlot *dd,
                                 const uint32_t *session, uint32_t epoch, const uint64_t *keys,
                                 const uint64_t *vals) {
   if (abort_flag && *abort_flag) return;
@@ -729,9 +748,8 @@ __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsign
     bool trig;
     int pl;
     if (via) {
-      const uint64_t h = via[t];
-      const uint64_t w = dw2[h];
-      pl = place_new(ix, dkey[h], uint32_t(w >> 32), epoch, session[uint32_t(w)], trig, false);
+      const DSlot d = dd[via[t]];
+      pl = place_new(ix, d.key, dd_inst(d.w2), epoch, session[dd_req(d.w2)], trig, false);
     } else {
       const uint64_t v = vals[t];
       pl = place_new(ix, keys[t], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), trig, false);
@@ -917,8 +935,8 @@ extern "C" int smetric_index_insert(smetric_index *idx, const uint64_t *keys, co
   const DevIndex ix = dev_view(idx);
   int rc;
   if ((rc = fill(ws.hdr, sizeof(WsHdr), 0, stream))) return rc;
-  if ((rc = fill(ws.dkey, 8 * ws.n_dedupe, 0, stream))) return rc;
-  if ((rc = fill(ws.dw2, 8 * ws.n_dedupe, ~uint64_t(0), stream))) return rc;
+  hipLaunchKernelGGL(dd_clear_kernel, dim3(grid_for(ws.n_dedupe)), dim3(TB), 0, stream, ws.dd, ws.n_dedupe,
+                     nullptr);
   const dim3 rgrid((n_req + IW - 1) / IW), rblock(64 * IW);
   hipLaunchKernelGGL(ins_probe_kernel, rgrid, rblock, 0, stream, ix, ws, keys, blk_off, n_req, n_blocks, instance,
                      session, epoch);
@@ -926,9 +944,9 @@ extern "C" int smetric_index_insert(smetric_index *idx, const uint64_t *keys, co
   hipLaunchKernelGGL(ins_refresh_kernel, rgrid, rblock, 0, stream, ix, ws, blk_off, n_req, n_blocks, epoch);
   hipLaunchKernelGGL(ins_place_kernel, dim3(grid_for(uint64_t(n_blocks))), dim3(TB), 0, stream, ix, ws, session, epoch);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
-                     ws.dkey, ws.list);
+                     nullptr, ws.dd, ws.list);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,
-                     ws.list, ws.dkey, ws.dw2, session, epoch, nullptr, nullptr);
+                     ws.list, ws.dd, session, epoch, nullptr, nullptr);
   return hip_rc(hipGetLastError());
 }
 
@@ -966,9 +984,9 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   unsigned long long *n_def = ws.count + 2;
   hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n - m)), dim3(TB), 0, stream, ix, keys, vals, m, n, trig,
                      n_trig, def, n_def, idx->capacity);
-  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr);
+  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr, nullptr);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), dim3(TB), 0, stream, ix, def, n_def, nullptr, nullptr, nullptr,
-                     nullptr, nullptr, 0u, keys, vals);
+                     nullptr, 0u, keys, vals);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   return hip_rc(hipStreamSynchronize(stream));
 }
@@ -1020,15 +1038,16 @@ extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe
   if ((rc = fill(ws.hdr, sizeof(WsHdr), 0, stream))) return rc;
   const dim3 flat(FLAT_WG), blk(TB);
   hipLaunchKernelGGL(insp_classify_kernel, flat, blk, 0, stream, ix, pv, ws, instance, session);
-  hipLaunchKernelGGL(insp_size_kernel, dim3(1), dim3(1), 0, stream, ws);
-  hipLaunchKernelGGL(insp_clear_kernel, dim3(grid_for(2 * uint64_t(n_blocks))), blk, 0, stream, ws);
-  hipLaunchKernelGGL(insp_dedupe_kernel, flat, blk, 0, stream, pv, ws, instance);
-  hipLaunchKernelGGL(insp_check_kernel, dim3(1), dim3(1), 0, stream, ix, ws);
+  hipLaunchKernelGGL(insp_size_kernel, dim3(1), blk, 0, stream, ws);
+  hipLaunchKernelGGL(dd_clear_kernel, dim3(grid_for(ws.n_dedupe)), blk, 0, stream, ws.dd, ws.n_dedupe,
+                     &ws.hdr->n_dd);
+  hipLaunchKernelGGL(insp_dedupe_kernel, flat, blk, 0, stream, ws);
+  hipLaunchKernelGGL(insp_check_kernel, dim3(1), blk, 0, stream, ix, ws);
   hipLaunchKernelGGL(insp_refresh_kernel, flat, blk, 0, stream, ix, pv, ws, epoch);
   hipLaunchKernelGGL(insp_place_kernel, flat, blk, 0, stream, ix, ws, session, epoch);
   hipLaunchKernelGGL(spill_kernel, dim3(64), blk, 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
-                     ws.dkey, ws.list);
+                     nullptr, ws.dd, ws.list);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), blk, 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,
-                     ws.list, ws.dkey, ws.dw2, session, epoch, nullptr, nullptr);
+                     ws.list, ws.dd, session, epoch, nullptr, nullptr);
   return hip_rc(hipGetLastError());
 }

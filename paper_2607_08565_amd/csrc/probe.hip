@@ -11,11 +11,12 @@
 // with no global atomics:
 //   requests  one wavefront per request checks the tiling and records each block's request
 //   count     PART_WG workgroups, one contiguous chunk of blocks each: LDS histogram of
-//             regions -> one column of the [region][chunk] matrix
-//   scan      per region, running offsets over chunks -> first position of every
-//             (region, chunk) pair
-//   scatter   each chunk again: LDS ranks per region -> (key, block | request << 32) at
-//             its region-order position, and the inverse index block -> position
+//             regions -> one row of the [chunk][region] matrix, plus region totals
+//   scan      one workgroup per region: its first position, then running offsets over
+//             chunks -> first position of every (chunk, region) pair
+//   scatter   each chunk again, one tile at a time: regrouped by region in LDS, then
+//             (key, block | request << 32) written as one contiguous run per region at its
+//             region-order position, and the inverse index block -> position
 //   probe     a fixed grid of FLAT_WG workgroups walks the region-ordered keys; all
 //             workgroups advance through the regions together, so the live window slides
 //             through the table.  One 128-byte bucket read per chain step (keys and values
@@ -50,7 +51,36 @@ __device__ __forceinline__ void chunk_of(uint64_t n, uint64_t &lo, uint64_t &hi)
   const uint64_t c = (n + PART_WG - 1) / PART_WG;
   lo = uint64_t(blockIdx.x) * c;
   hi = lo + c < n ? lo + c : n;
+  if (lo > n) lo = n;
 }
+
+// Exclusive scan of one value per thread over a TB-thread workgroup; `wt` holds TB / 64
+// wave totals.  Every thread returns its prefix; *total gets the sum.
+__device__ __forceinline__ uint32_t wg_exclusive_scan(uint32_t v, uint32_t *wt, uint32_t *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wt[wave] = x;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < TB / 64; ++i) {
+    const uint32_t t = wt[i];
+    before += i < wave ? t : 0;
+    all += t;
+  }
+  __syncthreads();  // wt may be reused by the caller
+  *total = all;
+  return before + x - v;
+}
+
+// Items per thread and per tile of the partition loops: U independent loads in flight.
+constexpr int U = 8;
+constexpr int TILE = U * TB;
 
 __global__ __launch_bounds__(TB) void part_count_kernel(DevIndex ix, ProbeView pv, const uint64_t *__restrict__ keys,
                                                         uint64_t n) {
@@ -59,57 +89,116 @@ __global__ __launch_bounds__(TB) void part_count_kernel(DevIndex ix, ProbeView p
   __syncthreads();
   uint64_t lo, hi;
   chunk_of(n, lo, hi);
-  for (uint64_t b = lo + threadIdx.x; b < hi; b += TB) atomicAdd(&h[region_of(keys[b], ix.n_buckets)], 1u);
-  __syncthreads();
-  for (int g = threadIdx.x; g < NREG; g += TB) pv.hist[uint64_t(g) * PART_WG + blockIdx.x] = h[g];
-}
-
-// one thread per region: region totals, their exclusive scan, then per-chunk offsets
-__global__ __launch_bounds__(NREG) void part_scan_kernel(ProbeView pv, uint64_t n) {
-  __shared__ unsigned long long tot[NREG];
-  const int g = threadIdx.x;
-  const uint32_t *row = pv.hist + uint64_t(g) * PART_WG;
-  unsigned long long t = 0;
-  for (int w = 0; w < PART_WG; ++w) t += row[w];
-  tot[g] = t;
-  __syncthreads();
-  if (g == 0) {
-    unsigned long long acc = 0;
-    for (int i = 0; i < NREG; ++i) {
-      const unsigned long long c = tot[i];
-      tot[i] = acc;
-      acc += c;
+  for (uint64_t t0 = lo; t0 < hi; t0 += TILE) {
+    uint64_t k[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint64_t b = t0 + u * TB + threadIdx.x;
+      k[u] = b < hi ? keys[b] : 0;
     }
-    pv.hdr->n = pv.hdr->err ? 0 : acc;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (t0 + u * TB + threadIdx.x < hi) atomicAdd(&h[region_of(k[u], ix.n_buckets)], 1u);
   }
   __syncthreads();
-  unsigned long long acc = tot[g];
-  uint64_t *out = pv.base + uint64_t(g) * PART_WG;
-  for (int w = 0; w < PART_WG; ++w) {
-    out[w] = acc;
-    acc += row[w];
+  for (int g = threadIdx.x; g < NREG; g += TB) {
+    const unsigned int c = h[g];
+    pv.hist[uint64_t(blockIdx.x) * NREG + g] = c;
+    if (c) atomicAdd(&pv.hdr->tot[g], (unsigned long long)c);
   }
 }
 
+// Workgroup g: first position of region g (sum of the totals before it), then the
+// running offsets of its chunks.
+static_assert(PART_WG == 4 * TB, "each thread of the scan covers 4 chunks");
+__global__ __launch_bounds__(TB) void part_scan_kernel(ProbeView pv) {
+  __shared__ uint32_t wt[TB / 64];
+  __shared__ unsigned long long red[TB / 64];
+  const int g = blockIdx.x, t = threadIdx.x;
+  unsigned long long v = 0;
+  for (int i = t; i < g; i += TB) v += pv.hdr->tot[i];
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  if ((t & 63) == 0) red[t >> 6] = v;
+  __syncthreads();
+  unsigned long long off = 0;
+#pragma unroll
+  for (int i = 0; i < TB / 64; ++i) off += red[i];
+  uint32_t c[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) c[j] = pv.hist[uint64_t(4 * t + j) * NREG + g];
+  uint32_t total;
+  uint32_t acc = wg_exclusive_scan(c[0] + c[1] + c[2] + c[3], wt, &total);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    pv.base[uint64_t(4 * t + j) * NREG + g] = off + acc;
+    acc += c[j];
+  }
+  if (g == NREG - 1 && t == 0) pv.hdr->n = pv.hdr->err ? 0 : off + total;
+}
+
+// Workgroup w moves its chunk into region order one tile at a time: LDS counts and ranks
+// per region, the tile regrouped by region in LDS, then each region's part written as one
+// contiguous run after the previous tile's.
+static_assert(NREG == TB, "one region per thread in the tile scan");
 __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView pv, const uint64_t *__restrict__ keys,
                                                           uint64_t n) {
-  __shared__ unsigned long long base[NREG];
-  __shared__ unsigned int rank[NREG];
+  __shared__ unsigned long long run[NREG];
+  __shared__ uint32_t cnt[NREG], tstart[NREG], wt[TB / 64];
+  __shared__ uint64_t skey[TILE], sbr[TILE];
+  __shared__ uint16_t sg[TILE];
   if (pv.hdr->err) return;
-  for (int g = threadIdx.x; g < NREG; g += TB) {
-    base[g] = pv.base[uint64_t(g) * PART_WG + blockIdx.x];
-    rank[g] = 0;
-  }
+  const int t = threadIdx.x;
+  run[t] = pv.base[uint64_t(blockIdx.x) * NREG + t];
+  cnt[t] = 0;
   __syncthreads();
   uint64_t lo, hi;
   chunk_of(n, lo, hi);
-  for (uint64_t b = lo + threadIdx.x; b < hi; b += TB) {
-    const uint64_t key = keys[b];
-    const uint32_t g = region_of(key, ix.n_buckets);
-    const uint64_t pos = base[g] + atomicAdd(&rank[g], 1u);
-    pv.part_key[pos] = key;
-    pv.part_br[pos] = b | (uint64_t(pv.req_of[b]) << 32);
-    pv.inv[b] = uint32_t(pos);
+  for (uint64_t t0 = lo; t0 < hi; t0 += TILE) {
+    uint64_t k[U];
+    uint32_t r[U], g[U], rk[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint64_t b = t0 + u * TB + t;
+      k[u] = b < hi ? keys[b] : 0;
+      r[u] = b < hi ? pv.req_of[b] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      g[u] = region_of(k[u], ix.n_buckets);
+      rk[u] = t0 + u * TB + t < hi ? atomicAdd(&cnt[g[u]], 1u) : 0;
+    }
+    __syncthreads();
+    uint32_t total;
+    tstart[t] = wg_exclusive_scan(cnt[t], wt, &total);
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint64_t b = t0 + u * TB + t;
+      if (b < hi) {
+        const uint32_t p = tstart[g[u]] + rk[u];
+        skey[p] = k[u];
+        sbr[p] = b | (uint64_t(r[u]) << 32);
+        sg[p] = uint16_t(g[u]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t p = u * TB + t;
+      if (p < total) {
+        const uint32_t gg = sg[p];
+        const uint64_t pos = run[gg] + (p - tstart[gg]);
+        const uint64_t br = sbr[p];
+        pv.part_key[pos] = skey[p];
+        pv.part_br[pos] = br;
+        pv.inv[uint32_t(br)] = uint32_t(pos);
+      }
+    }
+    __syncthreads();
+    run[t] += cnt[t];
+    cnt[t] = 0;
+    __syncthreads();
   }
 }
 
@@ -178,12 +267,12 @@ extern "C" int smetric_probe(const smetric_index *idx, const uint64_t *keys, con
   probe_layout(n_blocks, &pv, probe);
   const DevIndex ix = dev_view(idx);
   const uint64_t n = uint64_t(n_blocks);
-  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(64), 0, stream, reinterpret_cast<uint64_t *>(pv.hdr),
+  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hdr),
                      uint64_t(sizeof(ProbeHdr) / 8));
   if (n_req > 0)
     hipLaunchKernelGGL(req_of_kernel, dim3(n_req), dim3(64), 0, stream, pv, blk_off, n_req, n_blocks);
   hipLaunchKernelGGL(part_count_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
-  hipLaunchKernelGGL(part_scan_kernel, dim3(1), dim3(NREG), 0, stream, pv, n);
+  hipLaunchKernelGGL(part_scan_kernel, dim3(NREG), dim3(TB), 0, stream, pv);
   hipLaunchKernelGGL(part_scatter_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
   hipLaunchKernelGGL(probe_kernel, dim3(FLAT_WG), dim3(TB), 0, stream, ix, pv);
   return hip_rc(hipGetLastError());
