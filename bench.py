@@ -160,6 +160,18 @@ class Setup:
         rec(5)
 
 
+# kernels each timed call launches, in order (names as rocprofv3 reports them)
+CALL_KERNELS = {
+    "hash": ["hash16_kernel"],
+    "probe": ["zero_kernel", "req_of_kernel", "part_count_kernel", "part_scan_kernel", "part_scatter_kernel",
+              "probe_kernel"],
+    "match": ["match_kernel<1, true>"],
+    "route": ["route_kernel"],
+    "insert": ["fill_kernel", "insp_classify_kernel", "insp_size_kernel", "dd_clear_kernel", "insp_dedupe_kernel",
+               "insp_check_kernel", "insp_refresh_kernel", "insp_place_kernel", "spill_kernel", "deferred_kernel"],
+}
+
+
 def kernel_sources_hash() -> str:
     import glob
     import hashlib
@@ -274,6 +286,7 @@ def main():
             gpu_out = (setup.keys[:nb0].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
                        setup.branch.cpu().numpy())
     torch.cuda.synchronize()
+    n_before, _ = setup.index.stats()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     mats = []
     torch.cuda.synchronize()
@@ -300,13 +313,24 @@ def main():
         gbs["probe"] = alg["probe"] / per["probe"] / 1e6
         gbs["match"] = alg["match_scan"] / per["match"] / 1e6
     dominant = max(("hash", "probe", "match", "route"), key=lambda k: per[k])
-    traffic = None
-    if os.path.exists(args.traffic):
-        tr = json.load(open(args.traffic))
-        if tr.get("sources_sha256_16") == kernel_sources_hash():  # counters of the current kernels only
-            traffic = tr.get(dominant)
-    roof = {"bound": "hbm", "kernel": dominant, "achieved": round(gbs.get(dominant, 0.0), 1), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(gbs.get(dominant, 0.0) / HBM_PEAK_GBS, 4), "traffic": traffic}
+    tr = {}
+    if os.path.exists(args.traffic) and not args.direct:
+        t = json.load(open(args.traffic))
+        if t.get("sources_sha256_16") == kernel_sources_hash():  # counters of the current kernels only
+            tr = t
+    launches = (lambda c: None if args.direct else CALL_KERNELS[c])
+    roof = {"bound": "hbm", "kernel": dominant, "launches": launches(dominant),
+            "achieved": round(gbs.get(dominant, 0.0), 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs.get(dominant, 0.0) / HBM_PEAK_GBS, 4),
+            "traffic": round(tr[dominant]) if dominant in tr else None}
+    # the post-route insert: one bucket burst per pair, 16 B per new entry, 8 B per refresh
+    new_pairs = (n - n_before) / args.steps
+    n_blk = alg["blocks"]
+    ins_b = 64 * n_blk + 16 * new_pairs + 8 * (n_blk - new_pairs)
+    ins_gbs = ins_b / per["insert"] / 1e6
+    insert = {"kernel": "insert", "launches": launches("insert"), "new_pairs": int(new_pairs),
+              "achieved": round(ins_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+              "frac": round(ins_gbs / HBM_PEAK_GBS, 4), "traffic": round(tr["insert"]) if "insert" in tr else None}
     path_gbs = (alg["hash"] + alg["match"]) / (per["hash"] + probe_match_ms) / 1e6
     out = {
         "metric": METRIC, "value": round(R / (ms_step / 1e3), 1), "unit": "requests/s", "n_gpus": 1,
@@ -325,6 +349,7 @@ def main():
         "hash_probe_path": {"GBs": round(path_gbs, 1), "frac_of_peak": round(path_gbs / HBM_PEAK_GBS, 4),
                             "bytes": alg["hash"] + alg["match"], "probes": alg["probes"]},
         "roofline": roof,
+        "roofline_insert": insert,
     }
     if not args.no_cpu_baseline:
         cb, parity, n_s = cpu_baseline(setup, args.cpu_seconds, gpu_out)

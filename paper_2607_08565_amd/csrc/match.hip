@@ -228,14 +228,19 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
 #pragma unroll
   for (int t = 0; t < WPL; ++t) A[t] = 0;
 
+  // DESC: the next chunk's descriptors are loaded while the current one is processed
+  uint64_t d_cur = 0;
+  if (DESC && lane < nb) d_cur = desc[inv[b0 + lane]];
   for (int64_t j0 = 0; j0 < nb && mode != M_DONE; j0 += 64) {
     const int64_t j = j0 + lane;
     const bool valid = j < nb;
+    uint64_t d_next = 0;
+    if (DESC && j + 64 < nb) d_next = desc[inv[b0 + j + 64]];
     Holders H;
     uint64_t key = 0;
     if (valid) {
       if (DESC) {
-        const uint64_t d = desc[inv[b0 + j]];
+        const uint64_t d = d_cur;
         if (desc_kind(d) == D_MANY) key = keys[b0 + j];
         H = decode(ix, d, key);
       } else {
@@ -361,6 +366,7 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
       }
       if (!__ballot(my_inst >= 0)) mode = M_DONE;
     }
+    d_cur = d_next;
   }
   // survivors of a request whose block count is a multiple of 64
   if (mode == M_NARROW) {
