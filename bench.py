@@ -265,6 +265,45 @@ def cpu_baseline(setup, budget_s: float, gpu_out):
                        f"index restricted to their keys, single thread, {dt:.1f} s"), parity, n
 
 
+def measure_variants(setup, b: int, reps: int = 20):
+    """Route variants on the match rows of batch b (still in the output buffer), each
+    event-timed over `reps` calls on the current stream."""
+    import torch
+
+    S, W, d, tb = setup.S, setup.W, setup.dev[b], setup.host[b]
+    R, I = setup.matched.shape
+    slack, n_run = setup.tw.decode_state(b)
+    d_slack, d_run = torch.from_numpy(slack).cuda(), torch.from_numpy(n_run).cuda()
+    tgt = torch.empty(R, dtype=torch.int32, device="cuda")
+    br = torch.empty(R, dtype=torch.uint8, device="cuda")
+    call = lambda: S.route_coloc(setup.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], d_slack, d_run,
+                                 W.DEFAULT_PARAMS, tb.batch.rr_base, target=tgt, branch=br)
+    call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    alg = 4 * R * I + (8 + 8 + 4) * I + 12 * R + 5 * R  # c rows; q, slack, n_running; per-request in/out
+    out = {"route_coloc": {"rule": "PD colocation (App. B): TPOT filter, LMetric score, no last resort",
+                           "ms": round(ms, 4), "algorithmic_GBs": round(alg / ms / 1e6, 1),
+                           "branches": np.bincount(br.cpu().numpy(), minlength=6).tolist()}}
+    return out, dict(route_coloc=(slack, n_run, tgt.cpu().numpy(), br.cpu().numpy(), b))
+
+
+def variants_parity(setup, inputs) -> dict:
+    """The variants' whole-batch outputs against the oracle (CPU-baseline leg only)."""
+    import oracle
+
+    slack, n_run, gt, gb, b = inputs["route_coloc"]
+    bt = setup.host[b].batch
+    ot, ob = oracle.route_coloc(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, bt.turn, bt.q, slack, n_run,
+                                setup.W.DEFAULT_PARAMS, bt.rr_base)
+    return {"route_coloc": {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb))}}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -351,10 +390,13 @@ def main():
         "roofline": roof,
         "roofline_insert": insert,
     }
+    variants, var_inputs = measure_variants(setup, last)
+    out["variants"] = variants
     if not args.no_cpu_baseline:
         cb, parity, n_s = cpu_baseline(setup, args.cpu_seconds, gpu_out)
         out["cpu_baseline"] = cb
         out["sampled_parity"] = {"requests": n_s, "bit_exact": bool(parity)}
+        out["sampled_parity"]["variants"] = variants_parity(setup, var_inputs)
     print(json.dumps(out), flush=True)
 
 

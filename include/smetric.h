@@ -12,6 +12,7 @@
  *   smetric_match         c[r][i] = longest prefix of request r, in blocks, held by
  *                         instance i in the global block index           (Sec. 4.1)
  *   smetric_route         the stick / balance / migrate decision          (Sec. 4.2, Eq. (1))
+ *   smetric_route_coloc   the same decision under PD colocation           (App. B)
  *   smetric_index_insert  post-route insert of every full block on the target
  *   smetric_index_evict   LRU eviction of a fraction of the entries
  *
@@ -230,12 +231,37 @@ typedef struct smetric_params {
 } smetric_params;
 
 enum { SMETRIC_FIRST_TURN = 0, SMETRIC_EVICTED = 1, SMETRIC_STICK = 2, SMETRIC_LAST_RESORT = 3,
-       SMETRIC_MIGRATE = 4, SMETRIC_INVALID = 255 };
+       SMETRIC_MIGRATE = 4, SMETRIC_MIGRATE_TPOT = 5, SMETRIC_INVALID = 255 };
 
 int smetric_route(const int32_t *matched, int32_t n_req, int32_t n_instances,
                   const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
                   const int64_t *q, const smetric_params *params /* host */, uint64_t rr_base,
                   int32_t *target, uint8_t *branch, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Route under PD colocation (App. B pseudocode): the rule above with three changes.
+ *   * TPOT filter: a colocated instance also decodes, and the new request's prefill
+ *     stalls its live decodes for prefill_cost(req, c[i]) (Eq. (1)); instance i is a
+ *     candidate iff that stall fits the smallest slack of its live decodes:
+ *     2 C_LIN n + C_ATT n (2L - n) <= 2 tpot_slack[i].  When no instance passes, every
+ *     instance is a candidate.
+ *   * stick to prev iff turn != 0, prev caches the session, prev meets the TTFT check and
+ *     prev is a candidate; there is no last-resort stick.
+ *   * balance: argmin over the candidates of LMetric's multiplicative score
+ *     est2(i) * n_running[i] (estimated load times the instance's request count), ties to
+ *     the rotation order of smetric_route.
+ *   tpot_slack  int64[n_instances]  smallest slack of the instance's live decodes, ns of
+ *               prefill time; any value >= 2^62 means no live decode (always passes)
+ *   n_running   int32[n_instances]  requests at the instance (>= 0)
+ * Other arguments, domains and errors as smetric_route; a negative n_running makes every
+ * request out of domain.  Branches: FIRST_TURN, EVICTED, STICK, MIGRATE (prev misses the
+ * TTFT check), MIGRATE_TPOT (prev fails the TPOT filter while another instance passes).
+ * --------------------------------------------------------------------------------- */
+int smetric_route_coloc(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                        const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                        const int64_t *q, const int64_t *tpot_slack, const int32_t *n_running,
+                        const smetric_params *params /* host */, uint64_t rr_base, int32_t *target,
+                        uint8_t *branch, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------
  * Post-route insert: every full block of request r goes on instance[r] (the routed

@@ -74,6 +74,8 @@ def _load():
     lib.orc_index_dump.restype = C.c_uint64
     lib.orc_match.argtypes = [P, P, P, C.c_int32, C.c_int64, P]
     lib.orc_route.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P]
+    lib.orc_route_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
+                                    P, P]
     _lib = lib
     return lib
 
@@ -203,4 +205,33 @@ def route(matched, prompt_len, hist_len, turn, q, params: dict, rr_base: int = 0
                            _ptr(target), _ptr(branch))
     if rc != OK:
         raise ValueError(f"orc_route rc={rc}")
+    return target[:R], branch[:R]
+
+
+# Per-instance decode slack at or above this value means "no live decode" (App. B's
+# all() over an empty set is true).
+NO_DECODE = 1 << 62
+
+
+def route_coloc(matched, prompt_len, hist_len, turn, q, slack, n_run, params: dict, rr_base: int = 0):
+    """The rule under PD colocation (App. B pseudocode). slack: int64[I] smallest slack of the
+    instance's live decodes in ns (>= NO_DECODE: none); n_run: int32[I] requests at the
+    instance. Returns (target int32[R], branch uint8[R]); raises on invalid parameters."""
+    matched = _arr(matched, np.int32)
+    R, I = matched.shape
+    prompt_len = _arr(prompt_len, np.int32)
+    hist_len = _arr(hist_len, np.int32)
+    turn = _arr(turn, np.int32)
+    q = _arr(q, np.int64)
+    slack = _arr(slack, np.int64)
+    n_run = _arr(n_run, np.int32)
+    p = _Params(**params)
+    target = np.zeros(max(R, 1), np.int32)
+    branch = np.zeros(max(R, 1), np.uint8)
+    rc = _load().orc_route_coloc(_ptr(matched) if matched.size else None, R, I,
+                                 _ptr(prompt_len) if R else None, _ptr(hist_len) if R else None,
+                                 _ptr(turn) if R else None, _ptr(q), _ptr(slack), _ptr(n_run), C.byref(p),
+                                 C.c_uint64(rr_base), _ptr(target), _ptr(branch))
+    if rc != OK:
+        raise ValueError(f"orc_route_coloc rc={rc}")
     return target[:R], branch[:R]

@@ -13,6 +13,7 @@
 //   index_*      global block index: set of (key, instance) entries  (Sec. 4.1 "kvc"; readings on insert/evict)
 //   match        per-request, per-instance longest matched prefix     (Sec. 4.1 score template: c_i)
 //   route        stick-or-balance rule with SLO checks and Eq. (1)    (Sec. 4.2 pseudocode, parts (a)-(c))
+//   route_coloc  the same rule under PD colocation                    (App. B pseudocode)
 //
 // Where the paper is silent (hash function, tie-breaks, integer units, batch semantics,
 // eviction order) the choices are the readings recorded with the design notes; each is
@@ -404,6 +405,98 @@ int orc_route(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *p
     } else {
       target[r] = best;
       branch[r] = 4;
+    }
+  }
+  return ORC_OK;
+}
+
+// Route under PD colocation, App. B pseudocode: the Sec. 4.2 rule with two changes.
+//   meets_tpot(i): the request's prefill stalls i's live decodes by prefill_cost(c[i]);
+//     it must fit the smallest decode slack at i:  cost2(i) <= 2 * slack[i], with cost2
+//     as above; slack[i] >= 2^62 means no live decode (always passes).
+//   cand = instances meeting it; when none does, every instance.
+//   stick to prev iff turn != 0, session_cached(prev), meets_ttft(prev) and prev in cand;
+//   otherwise balance: argmin over cand of (est2(i) * n_run[i], (i - start) mod I), the
+//   multiplicative score of LMetric (estimate_load times the instance's request count).
+//   There is no last-resort clause.
+// branch: 0 first turn, 1 session evicted, 2 stick, 4 migrate (prev misses the TTFT check),
+// 5 migrate (prev fails the TPOT filter while another instance passes); 255 out of domain
+// (additionally some n_run[i] < 0).
+int orc_route_coloc(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
+                    const int32_t *hist_len, const int32_t *turn, const int64_t *q,
+                    const int64_t *slack, const int32_t *n_run, const orc_params *p, uint64_t rr_base,
+                    int32_t *target, uint8_t *branch) {
+  typedef __int128 i128;
+  const int64_t LIM32 = int64_t(1) << 32;
+  if (n_req < 0 || I < 1 || I > 65536) return ORC_EINVAL;
+  if (p->c_lin < 0 || p->c_lin > LIM32 || p->c_att < 0 || p->c_att > LIM32 || p->slo_b < 0 ||
+      p->slo_b > LIM32 || p->slo_a < 0 || p->slo_a > LIM32 || p->slack_num < 0 ||
+      p->slack_den < 0 || p->hit_num < 0 || p->hit_den <= 0 || p->hit_num >= p->hit_den ||
+      p->block_size < 2 || p->block_size > 256 || (p->block_size & 1))
+    return ORC_EINVAL;
+  const int64_t B = p->block_size;
+  const int64_t NO_DECODE = int64_t(1) << 62;
+  bool inst_ok = true;
+  for (int32_t i = 0; i < I; ++i)
+    if (q[i] < 0 || q[i] >= (int64_t(1) << 62) || n_run[i] < 0) inst_ok = false;
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int32_t *c = matched + int64_t(r) * I;
+    const int64_t L = prompt_len[r];
+    bool ok = inst_ok && L >= 0 && L <= (int64_t(1) << 24) && hist_len[r] >= 0 && turn[r] >= 0;
+    for (int32_t i = 0; ok && i < I; ++i) ok = c[i] >= 0 && c[i] <= L / B;
+    if (!ok) {
+      target[r] = -1;
+      branch[r] = 255;
+      continue;
+    }
+    auto cost2 = [&](int32_t i) -> i128 {  // 2 x prefill_cost(req, c[i]), Eq. (1)
+      i128 n = L - B * c[i];
+      return i128(2) * p->c_lin * n + i128(p->c_att) * n * (i128(2) * L - n);
+    };
+    auto est2 = [&](int32_t i) -> i128 { return i128(2) * q[i] + cost2(i); };
+    auto meets_tpot = [&](int32_t i) -> bool {
+      return slack[i] >= NO_DECODE || cost2(i) <= i128(2) * slack[i];
+    };
+    const i128 bound2 = i128(2) * (i128(p->slo_b) + i128(p->slo_a) * L);
+    auto meets_ttft = [&](int32_t i) -> bool {
+      if (p->slack_den == 0) return true;
+      return est2(i) * p->slack_den <= i128(p->slack_num) * bound2;
+    };
+    std::vector<bool> in_cand(I);
+    bool any = false;
+    for (int32_t i = 0; i < I; ++i) {
+      in_cand[i] = meets_tpot(i);
+      any = any || in_cand[i];
+    }
+    if (!any)
+      for (int32_t i = 0; i < I; ++i) in_cand[i] = true;
+    int32_t prev = 0;
+    for (int32_t i = 1; i < I; ++i)
+      if (c[i] > c[prev]) prev = i;
+    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    int32_t best = -1;
+    for (int32_t k = 0; k < I; ++k) {
+      const int32_t i = (start + k) % I;
+      if (!in_cand[i]) continue;
+      // strict: the earlier rotation position wins ties
+      if (best < 0 || est2(i) * n_run[i] < est2(best) * n_run[best]) best = i;
+    }
+    const bool cached = i128(B) * c[prev] * p->hit_den > i128(p->hit_num) * hist_len[r];
+    if (turn[r] == 0) {
+      target[r] = best;
+      branch[r] = 0;
+    } else if (!cached) {
+      target[r] = best;
+      branch[r] = 1;
+    } else if (!meets_ttft(prev)) {
+      target[r] = best;
+      branch[r] = 4;
+    } else if (!in_cand[prev]) {
+      target[r] = best;
+      branch[r] = 5;
+    } else {
+      target[r] = prev;
+      branch[r] = 2;
     }
   }
   return ORC_OK;

@@ -61,6 +61,7 @@ def _load() -> C.CDLL:
         "smetric_index_stats": [PIX, P, P, I32, P],
         "smetric_match": [PIX, P, P, I32, I64, P, P],
         "smetric_route": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
+        "smetric_route_coloc": [P, I32, I32, P, P, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_index_insert_ws_bytes": [I64, P],
         "smetric_index_insert": [PIX, P, P, I32, I64, P, P, U32, P, U64, P],
         "smetric_index_evict_ws_bytes": [PIX, P],
@@ -85,6 +86,7 @@ EXPORTED = (
     "smetric_route", "smetric_index_insert_ws_bytes", "smetric_index_insert",
     "smetric_index_evict_ws_bytes", "smetric_index_evict", "smetric_index_dump",
     "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
+    "smetric_route_coloc",
 )
 
 
@@ -147,6 +149,28 @@ def route(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tenso
         _stream()))
     return target[:R], branch[:R]
 
+
+
+# Decode slack at or above this value means "no live decode" (smetric_route_coloc).
+NO_DECODE = 1 << 62
+
+
+def route_coloc(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
+                q: torch.Tensor, tpot_slack: torch.Tensor, n_running: torch.Tensor, params: dict, rr_base: int = 0,
+                target: torch.Tensor | None = None, branch: torch.Tensor | None = None):
+    """smetric_route_coloc: the decision under PD colocation (App. B)."""
+    R, I = matched.shape
+    dev = matched.device
+    target = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if target is None else target
+    branch = torch.empty(max(R, 1), dtype=torch.uint8, device=dev) if branch is None else branch
+    p = _Params(**params)
+    _check("smetric_route_coloc", _lib.smetric_route_coloc(
+        _dev(matched, torch.int32, "matched"), R, I, _dev(prompt_len, torch.int32, "prompt_len"),
+        _dev(hist_len, torch.int32, "hist_len"), _dev(turn, torch.int32, "turn"), _dev(q, torch.int64, "q"),
+        _dev(tpot_slack, torch.int64, "tpot_slack"), _dev(n_running, torch.int32, "n_running"),
+        C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
+        _stream()))
+    return target[:R], branch[:R]
 
 def insert_ws_bytes(n_blocks: int) -> int:
     b = C.c_uint64()

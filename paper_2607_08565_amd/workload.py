@@ -37,7 +37,11 @@ DEFAULT_PARAMS = dict(
 )
 
 # Named RNG streams.
-S_TOK, S_LEN, S_PREFIX, S_PLACE, S_LOAD, S_FILL, S_PREFIXTOK = range(7)
+S_TOK, S_LEN, S_PREFIX, S_PLACE, S_LOAD, S_FILL, S_PREFIXTOK, S_DECODE = range(8)
+
+# Per-instance decode state for the colocated rule: the value of a slack meaning "no live
+# decode" (any value >= it).
+NO_DECODE = 1 << 62
 
 
 def _rng(cfg: int, stream: int, *extra: int) -> np.random.Generator:
@@ -267,6 +271,18 @@ class ThroughputWorkload:
                       turn=np.ones(R, np.int32), session=(np.arange(R, dtype=np.int64) + b * R).astype(np.uint32),
                       q=q, rr_base=b * R, epoch=1 + b)
         return ThroughputBatch(batch=batch, home=home, prior_len=prior_len, prefix_of=prefix_of)
+
+    def decode_state(self, b: int, idle_frac: float = 0.3, max_slack_ns: int = 3_000_000_000,
+                     mean_running: float = 8.0):
+        """Colocated fleet at batch b: per instance the smallest slack of its live decodes
+        (ns; NO_DECODE for the idle_frac of instances without decodes, else uniform in
+        [0, max_slack_ns)) and its request count (Poisson(mean_running))."""
+        rd = _rng(self.cfg, S_DECODE, b)
+        idle = rd.random(self.n_inst) < idle_frac
+        slack = rd.integers(0, max_slack_ns, size=self.n_inst).astype(np.int64)
+        slack[idle] = NO_DECODE
+        n_run = rd.poisson(mean_running, size=self.n_inst).astype(np.int32)
+        return slack, n_run
 
     def filler(self, n: int, chunk: int = 0):
         """n filler entries: random 64-bit keys (reserved values 0 and 2^64-1 excluded),

@@ -1,0 +1,119 @@
+"""GPU route variants (through the C ABI) vs the CPU oracle, bit for bit: the rule under
+PD colocation (App. B).  Random batches cover every branch, both sides of the TPOT
+filter (instances without decodes, slacks around the prefill stall, slacks nobody meets),
+idle instances (score 0), instance counts that are not multiples of the 64-lane wave,
+128-bit extremes and out-of-domain inputs; one case routes the matched rows of a real
+session workload."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_08565_amd import workload as W
+from tests.parity import Pair, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu(dev):
+    yield
+
+
+def _coloc_inputs(rng, R, I, L_hi=4000):
+    L = rng.integers(0, L_hi, R).astype(np.int32)
+    m = rng.integers(0, L_hi // 16 + 1, (R, I)).astype(np.int32)
+    m = np.minimum(m, (L // 16)[:, None]).astype(np.int32)
+    hist = rng.integers(0, L_hi, R).astype(np.int32)
+    turn = rng.integers(0, 3, R).astype(np.int32)
+    q = (rng.integers(0, 200, I) * W.Q_UNIT_NS).astype(np.int64)
+    # slacks: a third without decodes, a third around typical stalls, the rest anywhere
+    kind = rng.integers(0, 3, I)
+    slack = np.where(kind == 0, oracle.NO_DECODE,
+                     np.where(kind == 1, rng.integers(0, 4 * 10**8, I), rng.integers(-10**9, 10**10, I))).astype(np.int64)
+    n_run = rng.integers(0, 40, I).astype(np.int32)
+    return m, L, hist, turn, q, slack, n_run
+
+
+def _both(S, m, L, hist, turn, q, slack, n_run, p, rr):
+    gt, gb = S.route_coloc(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), to_dev(slack),
+                           to_dev(n_run), p, rr)
+    ot, ob = oracle.route_coloc(m, L, hist, turn, q, slack, n_run, p, rr)
+    gt, gb = gt.cpu().numpy(), gb.cpu().numpy()
+    bad = np.nonzero((gt != ot) | (gb != ob))[0]
+    assert len(bad) == 0, f"{len(bad)} decisions differ, first {bad[:5]}: gpu {gt[bad[:3]]}/{gb[bad[:3]]} oracle {ot[bad[:3]]}/{ob[bad[:3]]}"
+    return ot, ob
+
+
+@pytest.mark.parametrize("I", [1, 3, 64, 65, 1000, 5000])
+def test_coloc_random_parity(I):
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(100 + I)
+    R = 1500 if I <= 1000 else 300
+    m, L, hist, turn, q, slack, n_run = _coloc_inputs(rng, R, I)
+    seen = set()
+    for over in ({}, dict(slack_num=0, slack_den=1), dict(slack_num=1, slack_den=0), dict(c_att=0, c_lin=1),
+                 dict(slack_num=3, slack_den=2, hit_num=0, hit_den=5)):
+        p = dict(W.DEFAULT_PARAMS, **over)
+        for rr in (0, 987654321):
+            _, ob = _both(S, m, L, hist, turn, q, slack, n_run, p, rr)
+            seen |= set(ob.tolist())
+    # every slack below any stall: the filter is dropped
+    _both(S, m, L, hist, turn, q, np.full(I, -1, np.int64), n_run, W.DEFAULT_PARAMS, 5)
+    # an idle fleet: every score is 0
+    _both(S, m, L, hist, turn, q, slack, np.zeros(I, np.int32), W.DEFAULT_PARAMS, 5)
+    say(f"  I={I}: branches seen {sorted(seen)}")
+    assert {0, 1, 2, 4} <= seen
+    if I in (64, 1000, 5000):
+        assert 5 in seen
+
+
+def test_coloc_extremes_and_out_of_domain():
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(7)
+    R, I = 200, 70
+    L = np.full(R, 1 << 24, np.int32)
+    L[:50] = rng.integers(0, 1 << 24, 50)
+    m = rng.integers(0, (1 << 24) // 256 + 1, (R, I)).astype(np.int32)
+    m = np.minimum(m, (L // 256)[:, None]).astype(np.int32)
+    hist = rng.integers(0, 1 << 24, R).astype(np.int32)
+    turn = rng.integers(0, 2, R).astype(np.int32)
+    q = rng.integers((1 << 62) - 10**6, 1 << 62, I).astype(np.int64)
+    slack = rng.integers(-(1 << 62), 1 << 62, I).astype(np.int64)
+    slack[::5] = np.iinfo(np.int64).max
+    n_run = rng.integers(0, 2**31 - 1, I).astype(np.int32)
+    big = dict(W.DEFAULT_PARAMS, c_lin=1 << 32, c_att=1 << 32, slo_b=1 << 32, slo_a=1 << 32, block_size=256,
+               slack_num=2**31 - 1, slack_den=1)
+    _both(S, m, L, hist, turn, q, slack, n_run, big, 2**64 - 1)
+    # out of domain: c above L / B, negative turn, and a negative request count (all requests)
+    m2 = m.copy()
+    m2[3, 1] = L[3] // 256 + 1
+    t2 = turn.copy()
+    t2[4] = -1
+    _, ob = _both(S, m2, L, hist, t2, q, slack, n_run, big, 0)
+    assert ob[3] == 255 and ob[4] == 255
+    n_bad = n_run.copy()
+    n_bad[10] = -1
+    _, ob = _both(S, m, L, hist, turn, q, slack, n_bad, big, 0)
+    assert set(ob.tolist()) == {255}
+
+
+def test_coloc_on_matched_rows_of_a_session_workload():
+    """Route the real c rows of a scaled mid-fleet workload (closed loop) under colocation."""
+    from paper_2607_08565_amd import smetric as S
+    wl = W.config1(n_sess=256, n_turns=3)
+    pair = Pair(4_000_000, wl.n_inst)
+    rng = np.random.default_rng(3)
+    prev = None
+    for t in range(3):
+        b = wl.batch(t, prev)
+        d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(b.tokens, b.tok_off)
+        gm = pair.gix.match(d_keys, d_boff, nb)
+        om = pair.oix.match(okeys, blk_off)
+        assert np.array_equal(gm.cpu().numpy(), om)
+        slack = rng.integers(0, 2 * 10**9, wl.n_inst).astype(np.int64)
+        slack[rng.random(wl.n_inst) < 0.3] = oracle.NO_DECODE
+        n_run = rng.integers(0, 30, wl.n_inst).astype(np.int32)
+        ot, ob = _both(S, om, b.prompt_len, b.hist_len, b.turn, b.q, slack, n_run, W.DEFAULT_PARAMS, b.rr_base)
+        say(f"  batch {t}: branches {np.bincount(ob, minlength=6).tolist()}")
+        pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, ot, b.session, b.epoch)
+        prev = ot
