@@ -290,7 +290,30 @@ def measure_variants(setup, b: int, reps: int = 20):
     out = {"route_coloc": {"rule": "PD colocation (App. B): TPOT filter, LMetric score, no last resort",
                            "ms": round(ms, 4), "algorithmic_GBs": round(alg / ms / 1e6, 1),
                            "branches": np.bincount(br.cpu().numpy(), minlength=6).tolist()}}
-    return out, dict(route_coloc=(slack, n_run, tgt.cpu().numpy(), br.cpu().numpy(), b))
+    inputs = dict(route_coloc=(slack, n_run, tgt.cpu().numpy(), br.cpu().numpy(), b))
+    # online load update: one wavefront routes the batch in order
+    snap_t, _ = S.route(setup.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], W.DEFAULT_PARAMS,
+                        tb.batch.rr_base)
+    snap_t = snap_t.cpu().numpy()
+    q_out = torch.empty(I, dtype=torch.int64, device="cuda")
+    ws = torch.empty(S.route_seq_ws_bytes(R), dtype=torch.uint8, device="cuda")
+    call = lambda: S.route_seq(setup.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], W.DEFAULT_PARAMS,
+                               tb.batch.rr_base, target=tgt, branch=br, q_out=q_out, workspace=ws)
+    call()
+    seq_reps = max(2, reps // 4)
+    e0.record()
+    for _ in range(seq_reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / seq_reps
+    st = tgt.cpu().numpy()
+    out["route_seq"] = {"rule": "Sec. 4.2 rule, each request sees the queue updated by the earlier ones",
+                        "ms": round(ms, 4), "requests_per_s": round(R / (ms / 1e3), 1),
+                        "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist(),
+                        "targets_differing_from_batch_snapshot": int((st != snap_t).sum())}
+    inputs["route_seq"] = (st, br.cpu().numpy(), q_out.cpu().numpy(), b)
+    return out, inputs
 
 
 def variants_parity(setup, inputs) -> dict:
@@ -301,7 +324,14 @@ def variants_parity(setup, inputs) -> dict:
     bt = setup.host[b].batch
     ot, ob = oracle.route_coloc(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, bt.turn, bt.q, slack, n_run,
                                 setup.W.DEFAULT_PARAMS, bt.rr_base)
-    return {"route_coloc": {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb))}}
+    res = {"route_coloc": {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb))}}
+    gt, gb, gq, b = inputs["route_seq"]
+    bt = setup.host[b].batch
+    ot, ob, oq = oracle.route_seq(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, bt.turn, bt.q,
+                                  setup.W.DEFAULT_PARAMS, bt.rr_base)
+    res["route_seq"] = {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb)
+                                                                    and np.array_equal(oq, gq))}
+    return res
 
 
 def main():

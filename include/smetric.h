@@ -12,6 +12,7 @@
  *   smetric_match         c[r][i] = longest prefix of request r, in blocks, held by
  *                         instance i in the global block index           (Sec. 4.1)
  *   smetric_route         the stick / balance / migrate decision          (Sec. 4.2, Eq. (1))
+ *   smetric_route_seq     the same decision, requests routed one at a time (Sec. 4.2 (a))
  *   smetric_route_coloc   the same decision under PD colocation           (App. B)
  *   smetric_index_insert  post-route insert of every full block on the target
  *   smetric_index_evict   LRU eviction of a fraction of the entries
@@ -239,7 +240,29 @@ int smetric_route(const int32_t *matched, int32_t n_req, int32_t n_instances,
                   int32_t *target, uint8_t *branch, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------
- * Route under PD colocation (App. B pseudocode): the rule above with three changes.
+ * Route with the online load update: the rule of smetric_route, but requests are routed
+ * one at a time in index order and each routed request's prefill joins its target's
+ * queue before the next is routed (Sec. 4.2 (a): q is the prefill queued when the request
+ * arrives; prefill_cost is Eq. (1) with the request's hit on the target):
+ *   q_r[i] = q[i] + sum over r' < r routed to i of prefill_cost(r', c[r'][i]).
+ * A parallel pass first records what does not depend on the loads (domain, prev,
+ * session_cached, the prefill cost on prev, the deadline); then one wavefront walks the
+ * batch with the running loads kept doubled in 128 bits (exact).
+ *   q_out      int64[n_instances] (out, optional: NULL) final loads in ns, rounded down
+ *   workspace  >= smetric_route_seq_ws_bytes(n_req) bytes (64 per request), 256-B aligned
+ * Other arguments, domains, branches and errors as smetric_route, and n_instances must be
+ * <= 4096 (EINVAL otherwise); EWORKSPACE for a short workspace.  Out-of-domain requests
+ * (branch 255) add no load.
+ * --------------------------------------------------------------------------------- */
+int smetric_route_seq_ws_bytes(int32_t n_req, uint64_t *ws_bytes /* host */);
+int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                      const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                      const int64_t *q, const smetric_params *params /* host */, uint64_t rr_base,
+                      int32_t *target, uint8_t *branch, int64_t *q_out, void *workspace,
+                      uint64_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Route under PD colocation (App. B pseudocode): smetric_route's rule with three changes.
  *   * TPOT filter: a colocated instance also decodes, and the new request's prefill
  *     stalls its live decodes for prefill_cost(req, c[i]) (Eq. (1)); instance i is a
  *     candidate iff that stall fits the smallest slack of its live decodes:

@@ -74,6 +74,7 @@ def _load():
     lib.orc_index_dump.restype = C.c_uint64
     lib.orc_match.argtypes = [P, P, P, C.c_int32, C.c_int64, P]
     lib.orc_route.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P]
+    lib.orc_route_seq.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P, P]
     lib.orc_route_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
                                     P, P]
     _lib = lib
@@ -235,3 +236,25 @@ def route_coloc(matched, prompt_len, hist_len, turn, q, slack, n_run, params: di
     if rc != OK:
         raise ValueError(f"orc_route_coloc rc={rc}")
     return target[:R], branch[:R]
+
+
+def route_seq(matched, prompt_len, hist_len, turn, q, params: dict, rr_base: int = 0):
+    """Requests routed one at a time, each seeing the queue updated by the earlier ones.
+    Returns (target int32[R], branch uint8[R], q_after int64[I] in ns, rounded down)."""
+    matched = _arr(matched, np.int32)
+    R, I = matched.shape
+    prompt_len = _arr(prompt_len, np.int32)
+    hist_len = _arr(hist_len, np.int32)
+    turn = _arr(turn, np.int32)
+    q = _arr(q, np.int64)
+    p = _Params(**params)
+    target = np.zeros(max(R, 1), np.int32)
+    branch = np.zeros(max(R, 1), np.uint8)
+    q_out = np.zeros(I, np.int64)
+    rc = _load().orc_route_seq(_ptr(matched) if matched.size else None, R, I,
+                               _ptr(prompt_len) if R else None, _ptr(hist_len) if R else None,
+                               _ptr(turn) if R else None, _ptr(q), C.byref(p), C.c_uint64(rr_base),
+                               _ptr(target), _ptr(branch), _ptr(q_out))
+    if rc != OK:
+        raise ValueError(f"orc_route_seq rc={rc}")
+    return target[:R], branch[:R], q_out

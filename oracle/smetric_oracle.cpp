@@ -13,6 +13,7 @@
 //   index_*      global block index: set of (key, instance) entries  (Sec. 4.1 "kvc"; readings on insert/evict)
 //   match        per-request, per-instance longest matched prefix     (Sec. 4.1 score template: c_i)
 //   route        stick-or-balance rule with SLO checks and Eq. (1)    (Sec. 4.2 pseudocode, parts (a)-(c))
+//   route_seq    the same rule with the queue updated after every decision (Sec. 4.2 (a))
 //   route_coloc  the same rule under PD colocation                    (App. B pseudocode)
 //
 // Where the paper is silent (hash function, tie-breaks, integer units, batch semantics,
@@ -26,6 +27,7 @@
 // and closed forms of Eq. (1), insert/evict by a brute-force dictionary model.
 
 #include <algorithm>
+#include <climits>
 #include <cstdint>
 #include <cstring>
 #include <map>
@@ -407,6 +409,92 @@ int orc_route(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *p
       branch[r] = 4;
     }
   }
+  return ORC_OK;
+}
+
+// Route with the paper's online load semantics (Sec. 4.2 (a), where q is the queued
+// prefill at the moment each request is routed): requests are routed one at a time in index
+// order, and after each decision the request's prefill joins its target's queue,
+//   q[target] += prefill_cost(req, c[target])        (Eq. (1)),
+// so request r sees q plus the costs of every earlier request of the batch routed to each
+// instance.  The decision for each request is orc_route's with that q; loads are kept
+// doubled (2q, exact with Eq. (1)'s n/2 term) in 128 bits.  Out-of-domain requests add no
+// load.  q_out (optional) gets the final loads in ns, rounded down.
+int orc_route_seq(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
+                  const int32_t *hist_len, const int32_t *turn, const int64_t *q, const orc_params *p,
+                  uint64_t rr_base, int32_t *target, uint8_t *branch, int64_t *q_out) {
+  typedef __int128 i128;
+  const int64_t LIM32 = int64_t(1) << 32;
+  if (n_req < 0 || I < 1 || I > 65536) return ORC_EINVAL;
+  if (p->c_lin < 0 || p->c_lin > LIM32 || p->c_att < 0 || p->c_att > LIM32 || p->slo_b < 0 ||
+      p->slo_b > LIM32 || p->slo_a < 0 || p->slo_a > LIM32 || p->slack_num < 0 ||
+      p->slack_den < 0 || p->hit_num < 0 || p->hit_den <= 0 || p->hit_num >= p->hit_den ||
+      p->block_size < 2 || p->block_size > 256 || (p->block_size & 1))
+    return ORC_EINVAL;
+  const int64_t B = p->block_size;
+  bool q_ok = true;
+  std::vector<i128> q2(I);
+  for (int32_t i = 0; i < I; ++i) {
+    if (q[i] < 0 || q[i] >= (int64_t(1) << 62)) q_ok = false;
+    q2[i] = i128(2) * q[i];
+  }
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int32_t *c = matched + int64_t(r) * I;
+    const int64_t L = prompt_len[r];
+    bool ok = q_ok && L >= 0 && L <= (int64_t(1) << 24) && hist_len[r] >= 0 && turn[r] >= 0;
+    for (int32_t i = 0; ok && i < I; ++i) ok = c[i] >= 0 && c[i] <= L / B;
+    if (!ok) {
+      target[r] = -1;
+      branch[r] = 255;
+      continue;
+    }
+    auto cost2 = [&](int32_t i) -> i128 {  // 2 x prefill_cost(req, c[i])
+      i128 n = L - B * c[i];
+      return i128(2) * p->c_lin * n + i128(p->c_att) * n * (i128(2) * L - n);
+    };
+    auto est2 = [&](int32_t i) -> i128 { return q2[i] + cost2(i); };
+    const i128 bound2 = i128(2) * (i128(p->slo_b) + i128(p->slo_a) * L);
+    auto meets = [&](int32_t i) -> bool {
+      if (p->slack_den == 0) return true;
+      return est2(i) * p->slack_den <= i128(p->slack_num) * bound2;
+    };
+    int32_t prev = 0;
+    for (int32_t i = 1; i < I; ++i)
+      if (c[i] > c[prev]) prev = i;
+    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    int32_t best = start;
+    for (int32_t k = 1; k < I; ++k) {
+      int32_t i = (start + k) % I;
+      if (est2(i) < est2(best)) best = i;
+    }
+    const bool cached = i128(B) * c[prev] * p->hit_den > i128(p->hit_num) * hist_len[r];
+    int32_t t;
+    uint8_t br;
+    if (turn[r] == 0) {
+      t = best;
+      br = 0;
+    } else if (!cached) {
+      t = best;
+      br = 1;
+    } else if (meets(prev)) {
+      t = prev;
+      br = 2;
+    } else if (!meets(best)) {
+      t = prev;
+      br = 3;
+    } else {
+      t = best;
+      br = 4;
+    }
+    target[r] = t;
+    branch[r] = br;
+    q2[t] += cost2(t);  // the request's prefill joins its target's queue
+  }
+  if (q_out)
+    for (int32_t i = 0; i < I; ++i) {
+      const i128 v = q2[i] / 2;
+      q_out[i] = v > i128(INT64_MAX) ? INT64_MAX : int64_t(v);
+    }
   return ORC_OK;
 }
 

@@ -220,6 +220,254 @@ __global__ __launch_bounds__(64 * RW) void route_coloc_kernel(
   branch[r] = br;
 }
 
+// ---------------------------------------------------------------------------------
+// Online load update (Sec. 4.2 (a): q is what is queued when each request is routed).
+//   prep  one wavefront per request, in parallel: what does not depend on the loads --
+//         domain check, prev = argmax c, c[prev], session_cached -- into a 16-byte record.
+//   seq   ONE wavefront routes the batch in index order; the running loads 2q[i] live in
+//         LDS as 128-bit integers, together with their minimum.  Per request:
+//           * cached follow-up whose prev meets its deadline: stick (no scan);
+//           * cached follow-up with min(2q) + cost(prev) past the deadline: no instance can
+//             meet it (prev has the largest hit, so the smallest cost), last-resort stick
+//             (no scan);
+//           * otherwise the row is scanned for the argmin with the current loads.
+//         Rows (for <= 1024 instances) and records are loaded D requests ahead into
+//         registers, so HBM latency overlaps the requests in between.
+// ---------------------------------------------------------------------------------
+constexpr int SEQ_MAX_I = 4096;  // 64 KB of LDS for the loads
+
+struct SeqRec {
+  int32_t prev;    // argmax c, lowest id
+  int32_t flags;   // bit 0: in domain (apart from q), bit 1: session cached, bit 2: follow-up
+  int32_t L;       // prompt length
+  int32_t pad;
+  i128 cost_prev;  // 2 x prefill_cost(req, c[prev]), Eq. (1)
+  i128 cost_rest;  // 2 x prefill_cost at the largest hit of any other instance: a lower
+                   // bound of every other instance's cost (Eq. (1) falls as the hit grows)
+  i128 bound;      // SLACK_num x 2 (b + a L): i meets its deadline iff est2(i) SLACK_den <= bound
+};
+
+__global__ __launch_bounds__(64 * RW) void route_seq_prep_kernel(const int32_t *__restrict__ matched, int32_t n_req,
+                                                                 int32_t I, const int32_t *__restrict__ prompt_len,
+                                                                 const int32_t *__restrict__ hist_len,
+                                                                 const int32_t *__restrict__ turn, RouteParams p,
+                                                                 SeqRec *__restrict__ rec) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * RW + wave;
+  if (r >= n_req) return;
+  const int32_t *c = matched + int64_t(r) * I;
+  const int64_t L = prompt_len[r];
+  const int32_t hist = hist_len[r], tr = turn[r];
+  bool ok = L >= 0 && L <= (int64_t(1) << 24) && hist >= 0 && tr >= 0;
+  const int64_t max_c = ok ? L / p.B : -1;
+  int32_t bc = -1, bi = 0x7FFFFFFF;
+  for (int32_t i = lane; i < I; i += 64) {
+    const int32_t ci = c[i];
+    if (ci < 0 || ci > max_c) ok = false;
+    if (ci > bc) {
+      bc = ci;
+      bi = i;
+    }
+  }
+  ok = __ballot(!ok) == 0;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const int32_t oc = __shfl_xor(bc, m, 64), oi = __shfl_xor(bi, m, 64);
+    if (oc > bc || (oc == bc && oi < bi)) {
+      bc = oc;
+      bi = oi;
+    }
+  }
+  // the largest hit of any instance but prev (none: no other instance)
+  int32_t c2 = -1;
+  for (int32_t i = lane; i < I; i += 64)
+    if (i != bi) c2 = c[i] > c2 ? c[i] : c2;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const int32_t o = __shfl_xor(c2, m, 64);
+    c2 = o > c2 ? o : c2;
+  }
+  if (lane != 0) return;
+  const bool cached = ok && i128(p.B) * bc * p.hit_den > i128(p.hit_num) * hist;
+  SeqRec out;
+  out.prev = ok ? bi : 0;
+  out.flags = int32_t(ok) | (int32_t(cached) << 1) | (int32_t(tr != 0) << 2);
+  out.L = ok ? int32_t(L) : 0;
+  out.pad = 0;
+  out.cost_prev = ok ? est2(p, L, bc, 0) : i128(0);
+  // one instance: nothing else to bound, any value will do
+  out.cost_rest = ok ? est2(p, L, c2 < 0 ? bc : c2, 0) : i128(0);
+  out.bound = i128(p.slack_num) * (i128(2) * (i128(p.slo_b) + i128(p.slo_a) * (ok ? L : 0)));
+  rec[r] = out;
+}
+
+template <int K>
+struct SeqRow {
+  int32_t v[K];  // c[r][lane + 64 k] (K = 0: read on demand)
+  SeqRec rec;
+};
+
+template <int K>
+__device__ __forceinline__ void seq_load(const int32_t *__restrict__ matched, int32_t I, int32_t r, int32_t n_req,
+                                         const SeqRec *__restrict__ recs, SeqRow<K> &row) {
+  // Unconditional, clamped loads keep this straight-line code, so the compiler can wait
+  // for exactly the loads a request needs; lanes past the last instance are never read.
+  const int lane = threadIdx.x;
+  const int32_t rr = r < n_req ? r : n_req - 1;
+  const int32_t *c = matched + int64_t(rr) * I;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int i = lane + 64 * k;
+    row.v[k] = c[i < I ? i : I - 1];
+  }
+  // Vector loads on purpose: as scalar loads (the index is uniform) they would complete
+  // out of order, and every later wait on LDS or on the current request's scalars would
+  // also wait for these prefetches.
+  int32_t rv = rr;
+  asm volatile("" : "+v"(rv));
+  row.rec = recs[rv];
+}
+
+// Minimum of the running loads (every lane gets it).
+__device__ __forceinline__ i128 seq_qmin(const i128 *q2, int32_t I) {
+  i128 m = q2[0];
+  for (int32_t i = threadIdx.x; i < I; i += 64) m = q2[i] < m ? q2[i] : m;
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) {
+    const i128 o = shfl_xor128(m, s);
+    m = o < m ? o : m;
+  }
+  return m;
+}
+
+__device__ __forceinline__ int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Decide request r.  Every branch below is on wavefront-uniform values (read with
+// readfirstlane), and every lane performs the identical stores, so the code has no divergent
+// regions: the compiler can then wait for exactly the prefetched loads it uses.
+template <int K>
+__device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *__restrict__ matched, int32_t r,
+                                           int32_t I, const RouteParams &p, uint64_t rr_base, bool q_ok, i128 *q2,
+                                           i128 &qmin, int32_t *__restrict__ target, uint8_t *__restrict__ branch) {
+  const int lane = threadIdx.x;
+  const int32_t flags = uni(row.rec.flags);
+  if (!q_ok || !(flags & 1)) {
+    target[r] = -1;
+    branch[r] = SMETRIC_INVALID;
+    return;
+  }
+  const int32_t prev = uni(row.rec.prev);
+  const bool cached = flags & 2, follow_up = flags & 4;
+  const bool slack_inf = p.slack_den == 0;
+  const i128 cost_prev = row.rec.cost_prev, bound = row.rec.bound;  // uniform across lanes
+  const bool meets_prev = slack_inf || (q2[prev] + cost_prev) * p.slack_den <= bound;
+  int32_t t;
+  uint8_t br;
+  i128 cost_t;
+  if (follow_up && cached && meets_prev) {
+    t = prev;
+    br = SMETRIC_STICK;
+    cost_t = cost_prev;
+  } else if (follow_up && cached && !slack_inf && (qmin + row.rec.cost_rest) * p.slack_den > bound) {
+    // prev misses its deadline, and every other instance i has est2(i) >= min(2q) +
+    // cost_rest: nobody can meet it
+    t = prev;
+    br = SMETRIC_LAST_RESORT;
+    cost_t = cost_prev;
+  } else {
+    const int64_t L = uni(row.rec.L);
+    const int32_t tr = follow_up ? 1 : 0;
+    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    const int32_t *c = matched + int64_t(r) * I;
+    MinSD best{0, 0x7FFFFFFF};
+    if (K > 0) {
+#pragma unroll
+      for (int k = 0; k < (K > 0 ? K : 1); ++k) {
+        const int32_t i = lane + 64 * k;
+        const int32_t ii = i < I ? i : I - 1;
+        const i128 e = q2[ii] + est2(p, L, row.v[k], 0);
+        min_sd(best, e, i < I ? (i >= start ? i - start : i - start + I) : 0x7FFFFFFF);
+      }
+    } else {
+      for (int32_t i = lane; i < I; i += 64)
+        min_sd(best, q2[i] + est2(p, L, c[i], 0), i >= start ? i - start : i - start + I);
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) min_sd(best, shfl_xor128(best.s, m), __shfl_xor(best.d, m, 64));
+    const int32_t bal = (start + uni(best.d)) % I;
+    if (tr == 0) {
+      t = bal;
+      br = SMETRIC_FIRST_TURN;
+    } else if (!cached) {
+      t = bal;
+      br = SMETRIC_EVICTED;
+    } else if (!slack_inf && best.s * p.slack_den > bound) {
+      t = prev;
+      br = SMETRIC_LAST_RESORT;
+    } else {
+      t = bal;
+      br = SMETRIC_MIGRATE;
+    }
+    int32_t ct;
+    if (K > 0) {
+      int32_t v = 0;
+#pragma unroll
+      for (int k = 0; k < (K > 0 ? K : 1); ++k)
+        if (k == t / 64) v = row.v[k];
+      ct = uni(__shfl(v, t % 64, 64));
+    } else {
+      ct = uni(c[t]);
+    }
+    cost_t = t == prev ? cost_prev : est2(p, L, ct, 0);
+  }
+  // One wavefront does every LDS access, and its LDS operations complete in program
+  // order, so the next request reads this update without a fence (a fence here would also
+  // wait for the rows prefetched for later requests).  All lanes store the same values.
+  const i128 old = q2[t];
+  target[r] = t;
+  branch[r] = br;
+  q2[t] = old + cost_t;  // the request's prefill joins its target's queue
+  if (old == qmin && cost_t != 0) qmin = seq_qmin(q2, I);
+}
+
+template <int K, int D>
+__global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict__ matched, int32_t n_req,
+                                                       int32_t I, const int64_t *__restrict__ q, RouteParams p,
+                                                       uint64_t rr_base, const SeqRec *__restrict__ recs,
+                                                       int32_t *__restrict__ target, uint8_t *__restrict__ branch,
+                                                       int64_t *__restrict__ q_out) {
+  __shared__ i128 q2[SEQ_MAX_I];
+  const int lane = threadIdx.x;
+  bool q_ok = true;
+  for (int32_t i = lane; i < I; i += 64) {
+    const int64_t qi = q[i];
+    if (qi < 0 || qi >= (int64_t(1) << 62)) q_ok = false;
+    q2[i] = i128(2) * qi;
+  }
+  q_ok = __ballot(!q_ok) == 0;
+  __syncthreads();
+  i128 qmin = seq_qmin(q2, I);
+  SeqRow<K> ring[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) seq_load<K>(matched, I, d, n_req, recs, ring[d]);
+  for (int32_t r0 = 0; r0 < n_req; r0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int32_t r = r0 + d;
+      if (r < n_req) {
+        seq_decide<K>(ring[d], matched, r, I, p, rr_base, q_ok, q2, qmin, target, branch);
+        seq_load<K>(matched, I, r + D, n_req, recs, ring[d]);
+      }
+    }
+  }
+  __syncthreads();
+  if (q_out)
+    for (int32_t i = lane; i < I; i += 64) {
+      const i128 v = q2[i] >> 1;
+      q_out[i] = v > i128(INT64_MAX) ? INT64_MAX : int64_t(v);
+    }
+}
+
 int route_params(const smetric_params *params, int32_t n_req, int32_t n_instances, RouteParams &rp) {
   if (!params || n_req < 0 || n_instances < 1 || n_instances > 65536) return SMETRIC_EINVAL;
   const smetric_params &P = *params;
@@ -265,5 +513,44 @@ extern "C" int smetric_route_coloc(const int32_t *matched, int32_t n_req, int32_
   hipLaunchKernelGGL(route_coloc_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
                      n_instances, prompt_len, hist_len, turn, q, tpot_slack, n_running, rp, rr_base, target,
                      branch);
+  return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_route_seq_ws_bytes(int32_t n_req, uint64_t *ws_bytes) {
+  if (n_req < 0 || !ws_bytes) return SMETRIC_EINVAL;
+  *ws_bytes = (uint64_t(n_req < 1 ? 1 : n_req) * sizeof(SeqRec) + 255) / 256 * 256;
+  return SMETRIC_OK;
+}
+
+extern "C" int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                                 const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                                 const int64_t *q, const smetric_params *params, uint64_t rr_base,
+                                 int32_t *target, uint8_t *branch, int64_t *q_out, void *workspace,
+                                 uint64_t ws_bytes, hipStream_t stream) {
+  RouteParams rp;
+  if (int rc = route_params(params, n_req, n_instances, rp)) return rc;
+  if (n_instances > SEQ_MAX_I) return SMETRIC_EINVAL;
+  if (!q) return SMETRIC_EINVAL;
+  if (n_req > 0 && (!matched || !prompt_len || !hist_len || !turn || !target || !branch)) return SMETRIC_EINVAL;
+  uint64_t need = 0;
+  smetric_route_seq_ws_bytes(n_req, &need);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) || ws_bytes < need) return SMETRIC_EWORKSPACE;
+  SeqRec *recs = static_cast<SeqRec *>(workspace);
+  if (n_req > 0)
+    hipLaunchKernelGGL(route_seq_prep_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
+                       n_instances, prompt_len, hist_len, turn, rp, recs);
+  const int kk = (n_instances + 63) / 64;
+#define SEQ_LAUNCH(K, D)                                                                                       \
+  hipLaunchKernelGGL((route_seq_kernel<K, D>), dim3(1), dim3(64), 0, stream, matched, n_req, n_instances,         \
+                     q, rp, rr_base, recs, target, branch, q_out)
+  // prefetch depth D: D * (K + 4) vector loads in flight (K row words and a 64-byte
+  // record per request) stay within the 63 the wait counter tracks
+  if (kk <= 1) SEQ_LAUNCH(1, 8);
+  else if (kk <= 2) SEQ_LAUNCH(2, 8);
+  else if (kk <= 4) SEQ_LAUNCH(4, 7);
+  else if (kk <= 8) SEQ_LAUNCH(8, 5);
+  else if (kk <= 16) SEQ_LAUNCH(16, 3);
+  else SEQ_LAUNCH(0, 8);
+#undef SEQ_LAUNCH
   return hip_rc(hipGetLastError());
 }

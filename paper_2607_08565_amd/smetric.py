@@ -62,6 +62,8 @@ def _load() -> C.CDLL:
         "smetric_match": [PIX, P, P, I32, I64, P, P],
         "smetric_route": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_route_coloc": [P, I32, I32, P, P, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
+        "smetric_route_seq_ws_bytes": [I32, P],
+        "smetric_route_seq": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P, U64, P],
         "smetric_index_insert_ws_bytes": [I64, P],
         "smetric_index_insert": [PIX, P, P, I32, I64, P, P, U32, P, U64, P],
         "smetric_index_evict_ws_bytes": [PIX, P],
@@ -86,7 +88,7 @@ EXPORTED = (
     "smetric_route", "smetric_index_insert_ws_bytes", "smetric_index_insert",
     "smetric_index_evict_ws_bytes", "smetric_index_evict", "smetric_index_dump",
     "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
-    "smetric_route_coloc",
+    "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq",
 )
 
 
@@ -150,6 +152,34 @@ def route(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tenso
     return target[:R], branch[:R]
 
 
+
+def route_seq_ws_bytes(n_req: int) -> int:
+    b = C.c_uint64(0)
+    _check("smetric_route_seq_ws_bytes", _lib.smetric_route_seq_ws_bytes(n_req, C.byref(b)))
+    return b.value
+
+
+def route_seq(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
+              q: torch.Tensor, params: dict, rr_base: int = 0, target: torch.Tensor | None = None,
+              branch: torch.Tensor | None = None, q_out: torch.Tensor | None = None,
+              workspace: torch.Tensor | None = None):
+    """smetric_route_seq: requests routed one at a time, each seeing the earlier ones' load.
+    Returns (target, branch, q_out)."""
+    R, I = matched.shape
+    dev = matched.device
+    target = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if target is None else target
+    branch = torch.empty(max(R, 1), dtype=torch.uint8, device=dev) if branch is None else branch
+    q_out = torch.empty(I, dtype=torch.int64, device=dev) if q_out is None else q_out
+    need = route_seq_ws_bytes(R)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    p = _Params(**params)
+    _check("smetric_route_seq", _lib.smetric_route_seq(
+        _dev(matched, torch.int32, "matched"), R, I, _dev(prompt_len, torch.int32, "prompt_len"),
+        _dev(hist_len, torch.int32, "hist_len"), _dev(turn, torch.int32, "turn"), _dev(q, torch.int64, "q"),
+        C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
+        _dev(q_out, torch.int64, "q_out"), _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
+    return target[:R], branch[:R], q_out
 
 # Decode slack at or above this value means "no live decode" (smetric_route_coloc).
 NO_DECODE = 1 << 62

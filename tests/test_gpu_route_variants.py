@@ -117,3 +117,87 @@ def test_coloc_on_matched_rows_of_a_session_workload():
         say(f"  batch {t}: branches {np.bincount(ob, minlength=6).tolist()}")
         pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, ot, b.session, b.epoch)
         prev = ot
+
+
+# ---------------------------------------------------------------------------------
+# Online load update (requests routed one at a time)
+# ---------------------------------------------------------------------------------
+def _seq_both(S, m, L, hist, turn, q, p, rr):
+    gt, gb, gq = S.route_seq(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), p, rr)
+    ot, ob, oq = oracle.route_seq(m, L, hist, turn, q, p, rr)
+    gt, gb, gq = gt.cpu().numpy(), gb.cpu().numpy(), gq.cpu().numpy()
+    bad = np.nonzero((gt != ot) | (gb != ob))[0]
+    assert len(bad) == 0, f"{len(bad)} decisions differ, first {bad[:5]}: gpu {gt[bad[:3]]}/{gb[bad[:3]]} oracle {ot[bad[:3]]}/{ob[bad[:3]]}"
+    assert np.array_equal(gq, oq), "final loads differ"
+    return ot, ob
+
+
+@pytest.mark.parametrize("I", [1, 3, 64, 65, 1000, 1024, 1025, 4096])
+def test_seq_random_parity(I):
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(200 + I)
+    R = 3000 if I <= 1025 else 800
+    m, L, hist, turn, q, _, _ = _coloc_inputs(rng, R, I)
+    seen = set()
+    for over in ({}, dict(slack_num=0, slack_den=1), dict(slack_num=1, slack_den=0), dict(c_att=0, c_lin=1),
+                 dict(slack_num=3, slack_den=2, hit_num=0, hit_den=5)):
+        p = dict(W.DEFAULT_PARAMS, **over)
+        for rr in (0, 987654321):
+            _, ob = _seq_both(S, m, L, hist, turn, q, p, rr)
+            seen |= set(ob.tolist())
+    say(f"  I={I}: branches seen {sorted(seen)}")
+    assert {0, 1, 2, 3} <= seen
+    if I > 1:
+        assert 4 in seen
+
+
+def test_seq_extremes_invalid_and_limits():
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(8)
+    R, I = 300, 70
+    L = np.full(R, 1 << 24, np.int32)
+    L[:50] = rng.integers(0, 1 << 24, 50)
+    m = np.minimum(rng.integers(0, (1 << 24) // 256 + 1, (R, I)), (L // 256)[:, None]).astype(np.int32)
+    hist = rng.integers(0, 1 << 24, R).astype(np.int32)
+    turn = rng.integers(0, 2, R).astype(np.int32)
+    q = rng.integers((1 << 62) - 10**6, 1 << 62, I).astype(np.int64)
+    big = dict(W.DEFAULT_PARAMS, c_lin=1 << 32, c_att=1 << 32, slo_b=1 << 32, slo_a=1 << 32, block_size=256,
+               slack_num=2**31 - 1, slack_den=1)
+    _seq_both(S, m, L, hist, turn, q, big, 2**64 - 1)  # loads far beyond 2^64 (saturated q_out)
+    m2, t2 = m.copy(), turn.copy()
+    m2[3, 1] = L[3] // 256 + 1
+    t2[4] = -1
+    _, ob = _seq_both(S, m2, L, hist, t2, q, big, 0)
+    assert ob[3] == 255 and ob[4] == 255
+    qb = q.copy()
+    qb[0] = -1
+    _, ob = _seq_both(S, m, L, hist, turn, qb, big, 0)
+    assert set(ob.tolist()) == {255}
+    with pytest.raises(S.SmetricError):
+        S.route_seq(to_dev(np.zeros((2, 4097), np.int32)), to_dev(np.zeros(2, np.int32)),
+                    to_dev(np.zeros(2, np.int32)), to_dev(np.zeros(2, np.int32)), to_dev(np.zeros(4097, np.int64)),
+                    W.DEFAULT_PARAMS)
+    # an empty batch leaves the loads as they were
+    gt, gb, gq = S.route_seq(to_dev(np.zeros((0, 5), np.int32)), to_dev(np.zeros(0, np.int32)),
+                             to_dev(np.zeros(0, np.int32)), to_dev(np.zeros(0, np.int32)),
+                             to_dev(np.arange(5, dtype=np.int64)), W.DEFAULT_PARAMS)
+    assert gq.cpu().numpy().tolist() == list(range(5))
+
+
+def test_seq_on_matched_rows_of_a_session_workload():
+    """Online routing of the real c rows of a scaled long-context workload, closed loop."""
+    from paper_2607_08565_amd import smetric as S
+    wl = W.config2(n_sess=128, n_turns=3, l0=4096, app=(512, 2048), prefix_len=2048)
+    pair = Pair(4_000_000, wl.n_inst)
+    prev = None
+    for t in range(3):
+        b = wl.batch(t, prev)
+        d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(b.tokens, b.tok_off)
+        om = pair.oix.match(okeys, blk_off)
+        assert np.array_equal(pair.gix.match(d_keys, d_boff, nb).cpu().numpy(), om)
+        ot, ob = _seq_both(S, om, b.prompt_len, b.hist_len, b.turn, b.q, W.DEFAULT_PARAMS, b.rr_base)
+        bt, _ = oracle.route(om, b.prompt_len, b.hist_len, b.turn, b.q, W.DEFAULT_PARAMS, b.rr_base)
+        say(f"  batch {t}: branches {np.bincount(ob, minlength=5).tolist()}, "
+            f"{int((bt != ot).sum())} of {len(ot)} targets differ from the batch-snapshot rule")
+        pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, ot, b.session, b.epoch)
+        prev = ot
