@@ -313,6 +313,34 @@ def measure_variants(setup, b: int, reps: int = 20):
                         "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist(),
                         "targets_differing_from_batch_snapshot": int((st != snap_t).sum())}
     inputs["route_seq"] = (st, br.cpu().numpy(), q_out.cpu().numpy(), b)
+    # session reconstruction from block hashes on a multi-session trace
+    tr = W.session_trace(n_users=1024, sessions_per_user=4, turns=8)
+    blk_off, nb = S.block_offsets(tr.tok_off)
+    d_tok, d_toff, d_boff = (torch.from_numpy(tr.tokens).cuda(), torch.from_numpy(tr.tok_off).cuda(),
+                             torch.from_numpy(blk_off).cuda())
+    d_user, d_turn = torch.from_numpy(tr.user).cuda(), torch.from_numpy(tr.turn).cuda()
+    keys = S.hash_blocks(d_tok, d_toff, d_boff, nb)
+    par = torch.empty(tr.n_req, dtype=torch.int32, device="cuda")
+    ses = torch.empty(tr.n_req, dtype=torch.int32, device="cuda")
+    ws = torch.empty(S.sessions_ws_bytes(tr.n_req), dtype=torch.uint8, device="cuda")
+    call = lambda: S.sessions(keys, d_boff, nb, d_user, d_turn, parent=par, session=ses, workspace=ws)
+    call()
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    gp, gs = par.cpu().numpy(), ses.cpu().numpy()
+    keep = ~tr.compacted
+    out["sessions"] = {"rule": "App. A: follow-up = same user, turn + 1, block-hash prefix",
+                       "trace": f"{len(np.unique(tr.user))} users x 4 sessions x 8 turns, {tr.n_req} requests, "
+                                f"{nb} blocks, 5% compactions, 3% retries",
+                       "ms": round(ms, 4), "requests_per_s": round(tr.n_req / (ms / 1e3), 1),
+                       "blocks_per_s": round(nb / (ms / 1e3), 1), "linked": int((gp >= 0).sum()),
+                       "sessions_found": int(len(np.unique(gs))), "true_sessions": int(len(np.unique(tr.true_session))),
+                       "parent_agreement_excluding_compactions": round(float((gp[keep] == tr.true_parent[keep]).mean()), 6)}
+    inputs["sessions"] = (tr, blk_off, gp, gs)
     return out, inputs
 
 
@@ -331,6 +359,10 @@ def variants_parity(setup, inputs) -> dict:
                                   setup.W.DEFAULT_PARAMS, bt.rr_base)
     res["route_seq"] = {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb)
                                                                     and np.array_equal(oq, gq))}
+    tr, blk_off, gp, gs = inputs["sessions"]
+    ob, ok = oracle.hash_blocks(tr.tokens, tr.tok_off, setup.W.BLOCK, setup.W.DEFAULT_SEED)
+    op, os_ = oracle.sessions(ok, ob, tr.user, tr.turn)
+    res["sessions"] = {"requests": int(tr.n_req), "bit_exact": bool(np.array_equal(op, gp) and np.array_equal(os_, gs))}
     return res
 
 

@@ -14,6 +14,7 @@
  *   smetric_route         the stick / balance / migrate decision          (Sec. 4.2, Eq. (1))
  *   smetric_route_seq     the same decision, requests routed one at a time (Sec. 4.2 (a))
  *   smetric_route_coloc   the same decision under PD colocation           (App. B)
+ *   smetric_sessions      session reconstruction from block hashes        (App. A)
  *   smetric_index_insert  post-route insert of every full block on the target
  *   smetric_index_evict   LRU eviction of a fraction of the entries
  *
@@ -238,6 +239,32 @@ int smetric_route(const int32_t *matched, int32_t n_req, int32_t n_instances,
                   const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
                   const int64_t *q, const smetric_params *params /* host */, uint64_t rr_base,
                   int32_t *target, uint8_t *branch, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Session reconstruction from block hashes (App. A): request r follows an earlier request
+ * p of the same user when turn[r] = turn[p] + 1 and r's block-key sequence starts with p's
+ * (each turn extends its parent's prompt); chained, such requests form a session.
+ * Readings: requests are given in arrival order (index order); when several earlier
+ * requests qualify, the most recent is the parent; the empty sequence (a prompt shorter
+ * than one block) is a prefix of every sequence; session[r] is the index of the first
+ * request of r's chain.  Keys must be chained, as smetric_hash_blocks produces them (key j
+ * determines blocks 0..j): "p's sequence is a prefix of r's" is then the single test
+ * key_r[nb_p - 1] == key_p[nb_p - 1].
+ *   keys, blk_off  block keys, CSR by request (n_req + 1 offsets)
+ *   user           uint32[n_req]   opaque user id
+ *   turn           int32[n_req]    turn number within its session (>= 0)
+ *   parent         int32[n_req] (out)  parent request, or -1
+ *   session        int32[n_req] (out)  index of the chain's first request
+ *   status         int32 (device, optional: NULL) set to EINVAL if some request has a bad
+ *                  key range or a negative turn; such a request gets parent -1, session -1
+ *                  and is nobody's parent
+ *   workspace      >= smetric_sessions_ws_bytes(n_req) bytes (~32 per request), 256-B aligned
+ * Host errors: EINVAL (bad scalars, null pointers), EWORKSPACE.
+ * --------------------------------------------------------------------------------- */
+int smetric_sessions_ws_bytes(int32_t n_req, uint64_t *ws_bytes /* host */);
+int smetric_sessions(const uint64_t *keys, const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
+                     const uint32_t *user, const int32_t *turn, int32_t *parent, int32_t *session,
+                     int32_t *status, void *workspace, uint64_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------
  * Route with the online load update: the rule of smetric_route, but requests are routed

@@ -74,6 +74,7 @@ def _load():
     lib.orc_index_dump.restype = C.c_uint64
     lib.orc_match.argtypes = [P, P, P, C.c_int32, C.c_int64, P]
     lib.orc_route.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P]
+    lib.orc_sessions.argtypes = [P, P, C.c_int32, C.c_int64, P, P, P, P]
     lib.orc_route_seq.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P, P]
     lib.orc_route_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
                                     P, P]
@@ -258,3 +259,19 @@ def route_seq(matched, prompt_len, hist_len, turn, q, params: dict, rr_base: int
     if rc != OK:
         raise ValueError(f"orc_route_seq rc={rc}")
     return target[:R], branch[:R], q_out
+
+
+def sessions(keys, blk_off, user, turn):
+    """App. A session reconstruction.  Returns (parent int32[R], session int32[R])."""
+    keys = _arr(keys, np.uint64)
+    blk_off = _arr(blk_off, np.int64)
+    user = _arr(user, np.uint32)
+    turn = _arr(turn, np.int32)
+    R = len(blk_off) - 1
+    parent = np.zeros(max(R, 1), np.int32)
+    session = np.zeros(max(R, 1), np.int32)
+    rc = _load().orc_sessions(_ptr(keys) if len(keys) else None, _ptr(blk_off), R, int(len(keys)),
+                              _ptr(user) if R else None, _ptr(turn) if R else None, _ptr(parent), _ptr(session))
+    if rc != OK:
+        raise ValueError(f"orc_sessions rc={rc}")
+    return parent[:R], session[:R]

@@ -14,6 +14,7 @@
 //   match        per-request, per-instance longest matched prefix     (Sec. 4.1 score template: c_i)
 //   route        stick-or-balance rule with SLO checks and Eq. (1)    (Sec. 4.2 pseudocode, parts (a)-(c))
 //   route_seq    the same rule with the queue updated after every decision (Sec. 4.2 (a))
+//   sessions     session reconstruction from block hashes              (App. A)
 //   route_coloc  the same rule under PD colocation                    (App. B pseudocode)
 //
 // Where the paper is silent (hash function, tie-breaks, integer units, batch semantics,
@@ -408,6 +409,44 @@ int orc_route(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *p
       target[r] = best;
       branch[r] = 4;
     }
+  }
+  return ORC_OK;
+}
+
+// Session reconstruction, App. A: a request is the follow-up of an earlier request of
+// the same user when (1) its turn is larger by exactly one and (2) its block-hash sequence
+// starts with the other's.  Readings: requests are given in arrival order (index order);
+// when several earlier requests qualify, the most recent is the parent; the empty
+// sequence is a prefix of every sequence; a request's session is the index of the first
+// request of its chain (a request without parent starts one).  A request with a bad key
+// range gets parent -1, session -1 and is nobody's parent.
+int orc_sessions(const uint64_t *keys, const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
+                 const uint32_t *user, const int32_t *turn, int32_t *parent, int32_t *session) {
+  if (n_req < 0 || n_blocks < 0) return ORC_EINVAL;
+  std::vector<bool> ok(n_req);
+  for (int32_t r = 0; r < n_req; ++r)
+    ok[r] = blk_off[r] >= 0 && blk_off[r] <= blk_off[r + 1] && blk_off[r + 1] <= n_blocks && turn[r] >= 0;
+  std::unordered_map<uint32_t, std::vector<int32_t>> by_user;  // earlier requests of each user
+  for (int32_t r = 0; r < n_req; ++r) {
+    parent[r] = -1;
+    session[r] = -1;
+    if (!ok[r]) continue;
+    std::vector<int32_t> &earlier = by_user[user[r]];
+    const int64_t nr = blk_off[r + 1] - blk_off[r];
+    for (int32_t k = int32_t(earlier.size()) - 1; k >= 0; --k) {  // most recent first
+      const int32_t p = earlier[k];
+      if (turn[p] + int64_t(1) != turn[r]) continue;
+      const int64_t np = blk_off[p + 1] - blk_off[p];
+      if (np > nr) continue;
+      bool prefix = true;
+      for (int64_t j = 0; prefix && j < np; ++j) prefix = keys[blk_off[p] + j] == keys[blk_off[r] + j];
+      if (prefix) {
+        parent[r] = p;
+        break;
+      }
+    }
+    session[r] = parent[r] >= 0 ? session[parent[r]] : r;
+    earlier.push_back(r);
   }
   return ORC_OK;
 }

@@ -63,6 +63,8 @@ def _load() -> C.CDLL:
         "smetric_route": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_route_coloc": [P, I32, I32, P, P, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_route_seq_ws_bytes": [I32, P],
+        "smetric_sessions_ws_bytes": [I32, P],
+        "smetric_sessions": [P, P, I32, I64, P, P, P, P, P, P, U64, P],
         "smetric_route_seq": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P, U64, P],
         "smetric_index_insert_ws_bytes": [I64, P],
         "smetric_index_insert": [PIX, P, P, I32, I64, P, P, U32, P, U64, P],
@@ -88,7 +90,8 @@ EXPORTED = (
     "smetric_route", "smetric_index_insert_ws_bytes", "smetric_index_insert",
     "smetric_index_evict_ws_bytes", "smetric_index_evict", "smetric_index_dump",
     "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
-    "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq",
+    "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq", "smetric_sessions_ws_bytes",
+    "smetric_sessions",
 )
 
 
@@ -180,6 +183,30 @@ def route_seq(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.T
         C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
         _dev(q_out, torch.int64, "q_out"), _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
     return target[:R], branch[:R], q_out
+
+def sessions_ws_bytes(n_req: int) -> int:
+    b = C.c_uint64(0)
+    _check("smetric_sessions_ws_bytes", _lib.smetric_sessions_ws_bytes(n_req, C.byref(b)))
+    return b.value
+
+
+def sessions(keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int, user: torch.Tensor, turn: torch.Tensor,
+             parent: torch.Tensor | None = None, session: torch.Tensor | None = None,
+             status: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+    """smetric_sessions: App. A session reconstruction.  Returns (parent, session)."""
+    R = blk_off.numel() - 1
+    dev = blk_off.device
+    parent = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if parent is None else parent
+    session = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if session is None else session
+    need = sessions_ws_bytes(R)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    _check("smetric_sessions", _lib.smetric_sessions(
+        _dev(keys, torch.uint64, "keys"), _dev(blk_off, torch.int64, "blk_off"), R, n_blocks,
+        _dev(user, torch.uint32, "user"), _dev(turn, torch.int32, "turn"), _dev(parent, torch.int32, "parent"),
+        _dev(session, torch.int32, "session"), _dev(status, torch.int32, "status") if status is not None else None,
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
+    return parent[:R], session[:R]
 
 # Decode slack at or above this value means "no live decode" (smetric_route_coloc).
 NO_DECODE = 1 << 62

@@ -37,7 +37,7 @@ DEFAULT_PARAMS = dict(
 )
 
 # Named RNG streams.
-S_TOK, S_LEN, S_PREFIX, S_PLACE, S_LOAD, S_FILL, S_PREFIXTOK, S_DECODE = range(8)
+S_TOK, S_LEN, S_PREFIX, S_PLACE, S_LOAD, S_FILL, S_PREFIXTOK, S_DECODE, S_TRACE = range(9)
 
 # Per-instance decode state for the colocated rule: the value of a slack meaning "no live
 # decode" (any value >= it).
@@ -292,3 +292,69 @@ class ThroughputWorkload:
         inst = rf.integers(0, self.n_inst, size=n).astype(np.int32)
         sess = np.full(n, (1 << 24) - 1, np.uint32)
         return keys, inst, sess
+
+
+@dataclass
+class Trace:
+    """An anonymised multi-session trace: requests in arrival order with their tokens,
+    user and turn, plus the generator's ground truth (never an input of the method)."""
+    tokens: np.ndarray      # int32, CSR by request
+    tok_off: np.ndarray     # int64[R+1]
+    user: np.ndarray        # uint32[R]
+    turn: np.ndarray        # int32[R]
+    true_session: np.ndarray  # int32[R] generator's session id
+    true_parent: np.ndarray   # int32[R] generator's previous request of the session (-1: none)
+    compacted: np.ndarray     # bool[R] prompt rewritten (no prefix relation to the previous turn)
+
+    @property
+    def n_req(self) -> int:
+        return len(self.tok_off) - 1
+
+
+def session_trace(n_users: int = 64, sessions_per_user: int = 4, turns: int = 6, l0: int = 2048,
+                  prefix_len: int = 1024, app: tuple[int, int] = (256, 2048), p_compact: float = 0.05,
+                  p_retry: float = 0.03, compact_len: int = 1024, seed: int = 0) -> Trace:
+    """Synthetic trace with the shapes App. A relies on: each user runs several sessions,
+    all starting with the user's own system prefix; each turn's prompt extends the previous
+    one (reply + tool output, App. A) by U{app} tokens; a compaction turn (probability
+    p_compact) replaces the prompt with a fresh summary of compact_len tokens; a retry
+    (probability p_retry) resends a turn's exact prompt.  Sessions start at uniform times and
+    their turns are spaced by exponential gaps; requests are sorted by arrival."""
+    rg = _rng(9, S_TRACE, seed)
+    prompts, users, turns_l, sess, parents, comp, times = [], [], [], [], [], [], []
+    sid = 0
+    for u in range(n_users):
+        sys_prefix = uniform_tokens(rg, prefix_len)
+        for _ in range(sessions_per_user):
+            t_now = rg.uniform(0.0, 1000.0)
+            prompt = np.concatenate([sys_prefix, uniform_tokens(rg, max(l0 - prefix_len, 0))])
+            prev_idx = -1
+            for t in range(turns):
+                is_comp = False
+                if t > 0:
+                    if rg.random() < p_compact:
+                        prompt = uniform_tokens(rg, compact_len)
+                        is_comp = True
+                    prompt = np.concatenate([prompt, uniform_tokens(rg, int(rg.integers(app[0], app[1] + 1)))])
+                reps = 2 if rg.random() < p_retry else 1
+                parent_of_turn = prev_idx  # a retry has the same parent as the original
+                for _k in range(reps):
+                    prompts.append(prompt)
+                    users.append(u)
+                    turns_l.append(t)
+                    sess.append(sid)
+                    parents.append(parent_of_turn)  # generator-local index, remapped below
+                    comp.append(is_comp)
+                    times.append(t_now)
+                    prev_idx = len(prompts) - 1  # the next turn follows the latest send
+                    t_now += rg.exponential(5.0) + 1e-6
+            sid += 1
+    order = np.argsort(np.asarray(times), kind="stable")
+    rank = np.empty(len(order), np.int64)
+    rank[order] = np.arange(len(order))
+    toks, off = _csr([prompts[i] for i in order])
+    par = np.asarray(parents, np.int64)[order]
+    par = np.where(par >= 0, rank[np.maximum(par, 0)], -1).astype(np.int32)
+    return Trace(tokens=toks, tok_off=off, user=np.asarray(users, np.uint32)[order],
+                 turn=np.asarray(turns_l, np.int32)[order], true_session=np.asarray(sess, np.int32)[order],
+                 true_parent=par, compacted=np.asarray(comp, bool)[order])
