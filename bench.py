@@ -313,6 +313,34 @@ def measure_variants(setup, b: int, reps: int = 20):
                         "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist(),
                         "targets_differing_from_batch_snapshot": int((st != snap_t).sum())}
     inputs["route_seq"] = (st, br.cpu().numpy(), q_out.cpu().numpy(), b)
+    # the Sec. 5.4 ablation's load-aware filter, load = queued prefill + 100 ms per running request
+    load = d["q"] + d_run.to(torch.int64) * 100_000_000
+    call = lambda: S.route_loadaware(setup.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], load, (1, 2),
+                                     W.DEFAULT_PARAMS, tb.batch.rr_base, target=tgt, branch=br)
+    call()
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    la_t = tgt.cpu().numpy()
+    out["route_loadaware"] = {"rule": "Sec. 5.4 ablation: stick unless prev's load > 1.5 x mean",
+                              "ms": round(ms, 4), "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist()}
+    inputs["route_loadaware"] = (load.cpu().numpy(), la_t, br.cpu().numpy(), b)
+    # load imbalance (Sec. 4.1) of the batch-snapshot and the load-aware decisions: arrivals
+    # spread over 10 min, each request running 20 s, 30 s windows
+    rng = np.random.default_rng(b)
+    t0 = np.sort(rng.integers(0, 600_000, R)).astype(np.int64)
+    d_t0 = torch.from_numpy(t0).cuda()
+    d_t1 = d_t0 + 20_000
+    imb = {}
+    for name, tg in (("smetric_batch", snap_t), ("loadaware", la_t)):
+        gs, gm, _ = S.imbalance(torch.from_numpy(tg.astype(np.int32)).cuda(), d_t0, d_t1, I, 30_000, 21)
+        gs, gm = gs.cpu().numpy(), gm.cpu().numpy()
+        ratio = gm * I / np.maximum(gs, 1)
+        imb[name] = {"median": round(float(np.median(ratio[gs > 0])), 3), "max": round(float(ratio.max()), 3)}
+    out["imbalance_30s_windows"] = imb
     # session reconstruction from block hashes on a multi-session trace
     tr = W.session_trace(n_users=1024, sessions_per_user=4, turns=8)
     blk_off, nb = S.block_offsets(tr.tok_off)
@@ -359,6 +387,11 @@ def variants_parity(setup, inputs) -> dict:
                                   setup.W.DEFAULT_PARAMS, bt.rr_base)
     res["route_seq"] = {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb)
                                                                     and np.array_equal(oq, gq))}
+    load, gt, gb, b = inputs["route_loadaware"]
+    bt = setup.host[b].batch
+    ot, ob = oracle.route_loadaware(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, bt.turn, bt.q, load,
+                                    (1, 2), setup.W.DEFAULT_PARAMS, bt.rr_base)
+    res["route_loadaware"] = {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb))}
     tr, blk_off, gp, gs = inputs["sessions"]
     ob, ok = oracle.hash_blocks(tr.tokens, tr.tok_off, setup.W.BLOCK, setup.W.DEFAULT_SEED)
     op, os_ = oracle.sessions(ok, ob, tr.user, tr.turn)

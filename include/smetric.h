@@ -15,6 +15,8 @@
  *   smetric_route_seq     the same decision, requests routed one at a time (Sec. 4.2 (a))
  *   smetric_route_coloc   the same decision under PD colocation           (App. B)
  *   smetric_sessions      session reconstruction from block hashes        (App. A)
+ *   smetric_route_loadaware  the Sec. 5.4 ablation's load-aware filter
+ *   smetric_imbalance     per-window max / mean load                      (Sec. 4.1)
  *   smetric_index_insert  post-route insert of every full block on the target
  *   smetric_index_evict   LRU eviction of a fraction of the entries
  *
@@ -239,6 +241,42 @@ int smetric_route(const int32_t *matched, int32_t n_req, int32_t n_instances,
                   const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
                   const int64_t *q, const smetric_params *params /* host */, uint64_t rr_base,
                   int32_t *target, uint8_t *branch, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * The load-aware filter of the Sec. 5.4 ablation ("overloading migration"): the basic
+ * session-centric rule sticks a cached follow-up (turn != 0 and session_cached(prev), as in
+ * smetric_route) to prev = argmax c; the filter makes it leave prev when prev's load
+ * exceeds the cluster mean by the margin m = margin_num / margin_den:
+ *     load[prev] * n_instances * margin_den > (sum of loads) * (margin_den + margin_num)
+ * (margin_den == 0: never leaves -- the basic rule).  Leaving, first turns and evicted
+ * sessions take smetric_route's balance target.
+ *   load  int64[n_instances]  queued prefill plus ongoing decode (any unit), in [0, 2^62)
+ * Other arguments, domains and errors as smetric_route (a load outside its range makes
+ * every request out of domain).  Branches: FIRST_TURN, EVICTED, STICK, MIGRATE (overloaded).
+ * --------------------------------------------------------------------------------- */
+int smetric_route_loadaware(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                            const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                            const int64_t *q, const int64_t *load, int32_t margin_num, int32_t margin_den,
+                            const smetric_params *params /* host */, uint64_t rr_base, int32_t *target,
+                            uint8_t *branch, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Load imbalance per time window (the metric of the Sec. 4.1 analysis: an instance's load
+ * is its average number of running requests in a window; the imbalance is the maximum load
+ * over the mean).  For window w = [w window, (w+1) window) and instance i, the sum over
+ * requests r on i of the overlap of [t0[r], t1[r]) with the window (= average running
+ * requests x window length, exact in integers):
+ *   out_sum[w] = sum over instances, out_max[w] = maximum over instances
+ * so the imbalance is out_max[w] * n_instances / out_sum[w].
+ *   inst int32[n_req], t0/t1 int64[n_req]  instance and running interval (integer time unit)
+ *   n_bad (device int64, out)  requests skipped: instance outside [0, n_instances) or t1 < t0
+ *   workspace >= smetric_imbalance_ws_bytes(n_instances, n_windows) bytes, 256-B aligned
+ * Host errors: EINVAL (bad scalars, window * (n_windows + 1) >= 2^62), EWORKSPACE.
+ * --------------------------------------------------------------------------------- */
+int smetric_imbalance_ws_bytes(int32_t n_instances, int32_t n_windows, uint64_t *ws_bytes /* host */);
+int smetric_imbalance(const int32_t *inst, const int64_t *t0, const int64_t *t1, int64_t n_req, int32_t n_instances,
+                      int64_t window, int32_t n_windows, int64_t *out_sum, int64_t *out_max, int64_t *n_bad,
+                      void *workspace, uint64_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------
  * Session reconstruction from block hashes (App. A): request r follows an earlier request

@@ -74,6 +74,9 @@ def _load():
     lib.orc_index_dump.restype = C.c_uint64
     lib.orc_match.argtypes = [P, P, P, C.c_int32, C.c_int64, P]
     lib.orc_route.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P]
+    lib.orc_route_loadaware.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, C.c_int32, C.c_int32,
+                                        C.POINTER(_Params), C.c_uint64, P, P]
+    lib.orc_imbalance.argtypes = [P, P, P, C.c_int64, C.c_int32, C.c_int64, C.c_int32, P, P, P]
     lib.orc_sessions.argtypes = [P, P, C.c_int32, C.c_int64, P, P, P, P]
     lib.orc_route_seq.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P, P]
     lib.orc_route_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
@@ -275,3 +278,38 @@ def sessions(keys, blk_off, user, turn):
     if rc != OK:
         raise ValueError(f"orc_sessions rc={rc}")
     return parent[:R], session[:R]
+
+
+def route_loadaware(matched, prompt_len, hist_len, turn, q, load, margin: tuple[int, int], params: dict,
+                    rr_base: int = 0):
+    """Sec. 5.4 ablation: session stickiness with the load-aware filter (leave prev when its load
+    exceeds the mean by margin = num/den; den 0 = never).  Returns (target, branch)."""
+    matched = _arr(matched, np.int32)
+    R, I = matched.shape
+    prompt_len, hist_len, turn = _arr(prompt_len, np.int32), _arr(hist_len, np.int32), _arr(turn, np.int32)
+    q, load = _arr(q, np.int64), _arr(load, np.int64)
+    p = _Params(**params)
+    target = np.zeros(max(R, 1), np.int32)
+    branch = np.zeros(max(R, 1), np.uint8)
+    rc = _load().orc_route_loadaware(_ptr(matched) if matched.size else None, R, I,
+                                     _ptr(prompt_len) if R else None, _ptr(hist_len) if R else None,
+                                     _ptr(turn) if R else None, _ptr(q), _ptr(load), int(margin[0]), int(margin[1]),
+                                     C.byref(p), C.c_uint64(rr_base), _ptr(target), _ptr(branch))
+    if rc != OK:
+        raise ValueError(f"orc_route_loadaware rc={rc}")
+    return target[:R], branch[:R]
+
+
+def imbalance(inst, t0, t1, n_inst: int, window: int, n_windows: int):
+    """Per-window (sum, max) of instance loads (running requests x window length).
+    Returns (sum int64[W], max int64[W], n_bad)."""
+    inst, t0, t1 = _arr(inst, np.int32), _arr(t0, np.int64), _arr(t1, np.int64)
+    out_sum = np.zeros(max(n_windows, 1), np.int64)
+    out_max = np.zeros(max(n_windows, 1), np.int64)
+    bad = C.c_int64(0)
+    rc = _load().orc_imbalance(_ptr(inst) if len(inst) else None, _ptr(t0) if len(t0) else None,
+                               _ptr(t1) if len(t1) else None, len(inst), n_inst, window, n_windows,
+                               _ptr(out_sum), _ptr(out_max), C.byref(bad))
+    if rc != OK:
+        raise ValueError(f"orc_imbalance rc={rc}")
+    return out_sum[:n_windows], out_max[:n_windows], bad.value

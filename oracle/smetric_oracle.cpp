@@ -15,6 +15,8 @@
 //   route        stick-or-balance rule with SLO checks and Eq. (1)    (Sec. 4.2 pseudocode, parts (a)-(c))
 //   route_seq    the same rule with the queue updated after every decision (Sec. 4.2 (a))
 //   sessions     session reconstruction from block hashes              (App. A)
+//   route_loadaware  the Sec. 5.4 ablation's load-aware filter        (Sec. 5.4)
+//   imbalance    per-window max / mean load                            (Sec. 4.1 analysis)
 //   route_coloc  the same rule under PD colocation                    (App. B pseudocode)
 //
 // Where the paper is silent (hash function, tie-breaks, integer units, batch semantics,
@@ -410,6 +412,99 @@ int orc_route(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *p
       branch[r] = 4;
     }
   }
+  return ORC_OK;
+}
+
+// Load-aware filter (the Sec. 5.4 ablation's "overloading migration"): the basic
+// session-centric rule sticks a cached follow-up to prev = argmax c; with the filter it
+// leaves prev when prev's load (queued prefill plus ongoing decode, a caller input)
+// exceeds the cluster mean by the margin m = m_num / m_den:
+//   overloaded  <=>  load[prev] * I * m_den > (sum of loads) * (m_den + m_num).
+// Leaving, and the first-turn / evicted cases, balance exactly as orc_route (argmin of
+// est2 with the rotation tie-break).  m_den == 0 means an infinite margin (never leave:
+// the basic rule).  branch: 0 first turn, 1 evicted, 2 stick, 4 migrate (overloaded);
+// 255 out of domain (also: some load[i] < 0 or >= 2^62).
+int orc_route_loadaware(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
+                        const int32_t *hist_len, const int32_t *turn, const int64_t *q, const int64_t *load,
+                        int32_t m_num, int32_t m_den, const orc_params *p, uint64_t rr_base, int32_t *target,
+                        uint8_t *branch) {
+  typedef __int128 i128;
+  if (m_num < 0 || m_den < 0) return ORC_EINVAL;
+  std::vector<uint8_t> br0(n_req > 0 ? n_req : 1);
+  std::vector<int32_t> t0(n_req > 0 ? n_req : 1);
+  // the balance target of every request is orc_route's (first-turn requests balance)
+  std::vector<int32_t> zero_turn(n_req > 0 ? n_req : 1, 0);
+  int rc = orc_route(matched, n_req, I, prompt_len, hist_len, n_req ? zero_turn.data() : turn, q, p, rr_base,
+                     t0.data(), br0.data());
+  if (rc != ORC_OK) return rc;
+  bool load_ok = true;
+  i128 sum = 0;
+  for (int32_t i = 0; i < I; ++i) {
+    if (load[i] < 0 || load[i] >= (int64_t(1) << 62)) load_ok = false;
+    sum += load[i];
+  }
+  const int64_t B = p->block_size;
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int32_t *c = matched + int64_t(r) * I;
+    if (br0[r] == 255 || turn[r] < 0 || !load_ok) {
+      target[r] = -1;
+      branch[r] = 255;
+      continue;
+    }
+    int32_t prev = 0;
+    for (int32_t i = 1; i < I; ++i)
+      if (c[i] > c[prev]) prev = i;
+    const bool cached = i128(B) * c[prev] * p->hit_den > i128(p->hit_num) * hist_len[r];
+    const bool overloaded = m_den != 0 && i128(load[prev]) * I * m_den > sum * (i128(m_den) + m_num);
+    if (turn[r] == 0) {
+      target[r] = t0[r];
+      branch[r] = 0;
+    } else if (!cached) {
+      target[r] = t0[r];
+      branch[r] = 1;
+    } else if (!overloaded) {
+      target[r] = prev;
+      branch[r] = 2;
+    } else {
+      target[r] = t0[r];
+      branch[r] = 4;
+    }
+  }
+  return ORC_OK;
+}
+
+// Load imbalance, Sec. 4.1 analysis: an instance's load in a window is its average number
+// of running requests over the window; the imbalance is the maximum load over the mean.
+// Here per window w = [w W, (w+1) W) (times in integer units, e.g. ms): for each request
+// with instance i and running interval [t0, t1), its overlap with the window is added to
+// instance i's load (so load = average running requests x W, exact in integers); out_sum[w]
+// = the sum over instances, out_max[w] = the maximum (imbalance = out_max I / out_sum).
+// Requests with i outside [0, I) or t1 < t0 are skipped and counted in *n_bad.
+int orc_imbalance(const int32_t *inst, const int64_t *t0, const int64_t *t1, int64_t n_req, int32_t I,
+                  int64_t window, int32_t n_windows, int64_t *out_sum, int64_t *out_max, int64_t *n_bad) {
+  if (n_req < 0 || I < 1 || window <= 0 || n_windows < 0) return ORC_EINVAL;
+  std::vector<int64_t> cell(size_t(n_windows) * I, 0);
+  int64_t bad = 0;
+  for (int64_t r = 0; r < n_req; ++r) {
+    if (inst[r] < 0 || inst[r] >= I || t1[r] < t0[r]) {
+      ++bad;
+      continue;
+    }
+    for (int32_t w = 0; w < n_windows; ++w) {
+      const int64_t lo = std::max(t0[r], int64_t(w) * window), hi = std::min(t1[r], int64_t(w + 1) * window);
+      if (hi > lo) cell[size_t(w) * I + inst[r]] += hi - lo;
+    }
+  }
+  for (int32_t w = 0; w < n_windows; ++w) {
+    int64_t s = 0, m = 0;
+    for (int32_t i = 0; i < I; ++i) {
+      s += cell[size_t(w) * I + i];
+      m = std::max(m, cell[size_t(w) * I + i]);
+    }
+    out_sum[w] = s;
+    out_max[w] = m;
+  }
+  *n_bad = bad;
   return ORC_OK;
 }
 

@@ -41,6 +41,10 @@ __device__ __forceinline__ i128 shfl_xor128(i128 v, int m) {
   return (i128(hi2) << 64) | i128(lo2);
 }
 
+// RULE 0: SMetric (Sec. 4.2).  RULE 1: the Sec. 5.4 ablation's load-aware filter -- a
+// cached follow-up sticks unless prev's load exceeds the mean by the margin m_num/m_den:
+// load[prev] * I * m_den > (sum of loads) * (m_den + m_num); m_den == 0: never leaves.
+template <int RULE>
 __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restrict__ matched,
                                                         int32_t n_req, int32_t I,
                                                         const int32_t *__restrict__ prompt_len,
@@ -49,7 +53,9 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
                                                         const int64_t *__restrict__ q,
                                                         RouteParams p, uint64_t rr_base,
                                                         int32_t *__restrict__ target,
-                                                        uint8_t *__restrict__ branch) {
+                                                        uint8_t *__restrict__ branch,
+                                                        const int64_t *__restrict__ load = nullptr,
+                                                        int32_t m_num = 0, int32_t m_den = 0) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * RW + wave;
   if (r >= n_req) return;
@@ -63,10 +69,16 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
   int32_t best_c = -1, best_ci = 0x7FFFFFFF;  // argmax c, lowest id
   i128 best_e = 0;
   int32_t best_d = 0x7FFFFFFF;                // argmin (est2, rotation distance)
+  i128 load_sum = 0;                          // RULE 1
   for (int32_t i = lane; i < I; i += 64) {
     const int32_t ci = c[i];
     const int64_t qi = q[i];
     if (ci < 0 || ci > max_c || qi < 0 || qi >= (int64_t(1) << 62)) ok = false;
+    if (RULE == 1) {
+      const int64_t li = load[i];
+      if (li < 0 || li >= (int64_t(1) << 62)) ok = false;
+      load_sum += li;
+    }
     if (ci > best_c) {
       best_c = ci;
       best_ci = i;
@@ -92,6 +104,7 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
       best_e = oe;
       best_d = od;
     }
+    if (RULE == 1) load_sum += shfl_xor128(load_sum, m);
   }
   if (lane != 0) return;
   if (!ok) {
@@ -109,6 +122,14 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
   const bool cached = i128(p.B) * c[prev] * p.hit_den > i128(p.hit_num) * hist;
   int32_t t;
   uint8_t br;
+  if (RULE == 1) {
+    const bool over = m_den != 0 && i128(load[prev]) * I * m_den > load_sum * (i128(m_den) + m_num);
+    t = (tr != 0 && cached && !over) ? prev : bal;
+    br = tr == 0 ? SMETRIC_FIRST_TURN : !cached ? SMETRIC_EVICTED : !over ? SMETRIC_STICK : SMETRIC_MIGRATE;
+    target[r] = t;
+    branch[r] = br;
+    return;
+  }
   if (tr == 0) {
     t = bal;
     br = SMETRIC_FIRST_TURN;
@@ -495,8 +516,24 @@ extern "C" int smetric_route(const int32_t *matched, int32_t n_req, int32_t n_in
   if (int rc = route_params(params, n_req, n_instances, rp)) return rc;
   if (n_req == 0) return SMETRIC_OK;
   if (!matched || !prompt_len || !hist_len || !turn || !q || !target || !branch) return SMETRIC_EINVAL;
-  hipLaunchKernelGGL(route_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
-                     n_instances, prompt_len, hist_len, turn, q, rp, rr_base, target, branch);
+  hipLaunchKernelGGL(route_kernel<0>, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
+                     n_instances, prompt_len, hist_len, turn, q, rp, rr_base, target, branch, nullptr, 0, 0);
+  return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_route_loadaware(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                                       const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                                       const int64_t *q, const int64_t *load, int32_t margin_num,
+                                       int32_t margin_den, const smetric_params *params, uint64_t rr_base,
+                                       int32_t *target, uint8_t *branch, hipStream_t stream) {
+  RouteParams rp;
+  if (int rc = route_params(params, n_req, n_instances, rp)) return rc;
+  if (margin_num < 0 || margin_den < 0) return SMETRIC_EINVAL;
+  if (n_req == 0) return SMETRIC_OK;
+  if (!matched || !prompt_len || !hist_len || !turn || !q || !load || !target || !branch) return SMETRIC_EINVAL;
+  hipLaunchKernelGGL(route_kernel<1>, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
+                     n_instances, prompt_len, hist_len, turn, q, rp, rr_base, target, branch, load, margin_num,
+                     margin_den);
   return hip_rc(hipGetLastError());
 }
 

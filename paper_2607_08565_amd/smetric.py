@@ -63,6 +63,9 @@ def _load() -> C.CDLL:
         "smetric_route": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_route_coloc": [P, I32, I32, P, P, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_route_seq_ws_bytes": [I32, P],
+        "smetric_route_loadaware": [P, I32, I32, P, P, P, P, P, I32, I32, C.POINTER(_Params), U64, P, P, P],
+        "smetric_imbalance_ws_bytes": [I32, I32, P],
+        "smetric_imbalance": [P, P, P, I64, I32, I64, I32, P, P, P, P, U64, P],
         "smetric_sessions_ws_bytes": [I32, P],
         "smetric_sessions": [P, P, I32, I64, P, P, P, P, P, P, U64, P],
         "smetric_route_seq": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P, U64, P],
@@ -91,7 +94,7 @@ EXPORTED = (
     "smetric_index_evict_ws_bytes", "smetric_index_evict", "smetric_index_dump",
     "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
     "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq", "smetric_sessions_ws_bytes",
-    "smetric_sessions",
+    "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
 )
 
 
@@ -183,6 +186,41 @@ def route_seq(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.T
         C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
         _dev(q_out, torch.int64, "q_out"), _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
     return target[:R], branch[:R], q_out
+
+def route_loadaware(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
+                    q: torch.Tensor, load: torch.Tensor, margin: tuple[int, int], params: dict, rr_base: int = 0,
+                    target: torch.Tensor | None = None, branch: torch.Tensor | None = None):
+    """smetric_route_loadaware: the Sec. 5.4 ablation's load-aware filter."""
+    R, I = matched.shape
+    dev = matched.device
+    target = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if target is None else target
+    branch = torch.empty(max(R, 1), dtype=torch.uint8, device=dev) if branch is None else branch
+    p = _Params(**params)
+    _check("smetric_route_loadaware", _lib.smetric_route_loadaware(
+        _dev(matched, torch.int32, "matched"), R, I, _dev(prompt_len, torch.int32, "prompt_len"),
+        _dev(hist_len, torch.int32, "hist_len"), _dev(turn, torch.int32, "turn"), _dev(q, torch.int64, "q"),
+        _dev(load, torch.int64, "load"), int(margin[0]), int(margin[1]), C.byref(p), C.c_uint64(rr_base),
+        _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"), _stream()))
+    return target[:R], branch[:R]
+
+
+def imbalance(inst: torch.Tensor, t0: torch.Tensor, t1: torch.Tensor, n_inst: int, window: int, n_windows: int,
+              workspace: torch.Tensor | None = None):
+    """smetric_imbalance: per-window (sum, max) of instance loads.  Returns (sum, max, n_bad)."""
+    dev = inst.device
+    b = C.c_uint64(0)
+    _check("smetric_imbalance_ws_bytes", _lib.smetric_imbalance_ws_bytes(n_inst, n_windows, C.byref(b)))
+    if workspace is None or workspace.numel() < b.value:
+        workspace = torch.empty(b.value, dtype=torch.uint8, device=dev)
+    out_sum = torch.empty(max(n_windows, 1), dtype=torch.int64, device=dev)
+    out_max = torch.empty(max(n_windows, 1), dtype=torch.int64, device=dev)
+    n_bad = torch.empty(1, dtype=torch.int64, device=dev)
+    _check("smetric_imbalance", _lib.smetric_imbalance(
+        _dev(inst, torch.int32, "inst"), _dev(t0, torch.int64, "t0"), _dev(t1, torch.int64, "t1"), inst.numel(),
+        n_inst, window, n_windows, _dev(out_sum, torch.int64, "out_sum"), _dev(out_max, torch.int64, "out_max"),
+        _dev(n_bad, torch.int64, "n_bad"), _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
+    return out_sum[:n_windows], out_max[:n_windows], n_bad
+
 
 def sessions_ws_bytes(n_req: int) -> int:
     b = C.c_uint64(0)

@@ -201,3 +201,47 @@ def test_seq_on_matched_rows_of_a_session_workload():
             f"{int((bt != ot).sum())} of {len(ot)} targets differ from the batch-snapshot rule")
         pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, ot, b.session, b.epoch)
         prev = ot
+
+
+# ---------------------------------------------------------------------------------
+# Sec. 5.4 ablation: load-aware filter; Sec. 4.1 load-imbalance metric
+# ---------------------------------------------------------------------------------
+@pytest.mark.parametrize("I", [1, 3, 64, 65, 1000, 5000])
+def test_loadaware_random_parity(I):
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(300 + I)
+    R = 1500 if I <= 1000 else 300
+    m, L, hist, turn, q, _, _ = _coloc_inputs(rng, R, I)
+    load = rng.integers(0, 10**9, I).astype(np.int64)
+    seen = set()
+    for margin in ((1, 2), (0, 1), (1, 0), (7, 3)):
+        for rr in (0, 12345):
+            gt, gb = S.route_loadaware(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), to_dev(load),
+                                       margin, W.DEFAULT_PARAMS, rr)
+            ot, ob = oracle.route_loadaware(m, L, hist, turn, q, load, margin, W.DEFAULT_PARAMS, rr)
+            assert np.array_equal(gt.cpu().numpy(), ot) and np.array_equal(gb.cpu().numpy(), ob), (margin, rr)
+            seen |= set(ob.tolist())
+    assert {0, 1, 2} <= seen
+    if I > 1:
+        assert 4 in seen
+    # a load outside its range: every request out of domain
+    bad = load.copy()
+    bad[0] = -1
+    gt, gb = S.route_loadaware(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), to_dev(bad), (1, 2),
+                               W.DEFAULT_PARAMS)
+    assert set(gb.cpu().numpy().tolist()) == {255}
+
+
+@pytest.mark.parametrize("I,W_", [(1, 1), (7, 5), (64, 100), (1000, 37)])
+def test_imbalance_parity(I, W_):
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(I * 31 + W_)
+    R = 20000
+    inst = rng.integers(-2, I + 2, R).astype(np.int32)  # some out of range
+    t0 = rng.integers(-500, 120 * W_, R).astype(np.int64)
+    t1 = t0 + rng.integers(-5, 400, R)  # some negative durations, some zero
+    window = 100
+    gs, gm, gb = S.imbalance(to_dev(inst), to_dev(t0), to_dev(t1), I, window, W_)
+    os_, om, ob = oracle.imbalance(inst, t0, t1, I, window, W_)
+    assert np.array_equal(gs.cpu().numpy(), os_) and np.array_equal(gm.cpu().numpy(), om)
+    assert int(gb.item()) == ob
