@@ -180,8 +180,10 @@ int smetric_match(const smetric_index *idx, const uint64_t *keys, const int64_t 
  *   state; an invalid probe state gives all-zero rows and status EINVAL.
  * smetric_index_insert_probed: exactly smetric_index_insert's effect (same validation,
  *   all-or-nothing, EINVAL/EFULL in the status word) for the probed batch, with
- *   instance/session per request as there; an invalid probe state gives EINVAL.
- * Host errors: EINVAL (bad scalars, n_blocks >= 2^32), EWORKSPACE (short buffers).
+ *   instance/session per request as there; an invalid probe state gives EINVAL.  Its
+ *   batch must have n_blocks < 2^31.
+ * Host errors: EINVAL (bad scalars, n_blocks >= 2^32; >= 2^31 for the insert), EWORKSPACE
+ * (short buffers).
  * --------------------------------------------------------------------------------- */
 int smetric_probe_ws_bytes(int64_t n_blocks, uint64_t *bytes /* host */);
 int smetric_probe(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,

@@ -297,7 +297,9 @@ struct WsHdr {
   unsigned long long n_cand;   // pairs absent before the batch (region-ordered insert)
   unsigned long long n_dd;     // dedupe slots in use (a power of two)
   unsigned long long n_def;    // new pairs deferred until their key's conversion
-  unsigned long long pad[25];
+  unsigned long long n_dup;    // region-ordered insert: candidates whose key an earlier one claimed
+  unsigned long long n_dd2;    // region-ordered insert: pair-table slots in use (a power of two)
+  unsigned long long pad[23];
 };
 static_assert(sizeof(WsHdr) == 256, "ws header size");
 
@@ -316,6 +318,21 @@ struct Cand {
   uint64_t w2;  // same encoding as DSlot::w2
 };
 
+// Key-only claim table of the region-ordered insert: the first candidate of a key claims
+// the slot, later ones count themselves in `extra`.
+struct KSlot {
+  uint64_t key;
+  unsigned long long extra;
+};
+
+// Distinct new pair of the region-ordered insert.  h >= 0: its key repeats among the
+// candidates and dd[h] holds the pair's final (lowest) request.
+struct NewPair {
+  uint64_t key;
+  uint64_t w2;
+  int64_t h;
+};
+
 struct InsWs {
   WsHdr *hdr;
   uint64_t *pos;    // per block: slot + 1 of an entry to refresh, 0 = none
@@ -324,7 +341,11 @@ struct InsWs {
   uint64_t *trig;   // keys queued for conversion
   uint64_t *def;    // list positions of deferred new pairs
   Cand *cand;       // region-ordered insert: absent pairs, one segment per workgroup
+  uint32_t *cand_h;    // region-ordered insert: key-table slot of each candidate
+  KSlot *kt;           // region-ordered insert: key claims
+  NewPair *np;         // region-ordered insert: distinct new pairs, one segment per workgroup
   uint32_t *cand_cnt;  // entries in each workgroup's candidate segment
+  uint32_t *dup_cnt;   // repeated-key candidates seen by each workgroup
   uint32_t *list_cnt;  // entries in each workgroup's new-pair segment
   uint64_t n_dedupe;
   uint64_t list_cap;  // entries in list and trig
@@ -354,8 +375,12 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
   const uint64_t o_list = take(8 * nl);
   const uint64_t o_trig = take(8 * nl);
   const uint64_t o_def = take(8 * nl);
-  const uint64_t o_cand = take(16 * seg_n);
+  const uint64_t o_cand = take(sizeof(Cand) * seg_n);
+  const uint64_t o_ch = take(4 * seg_n);
+  const uint64_t o_kt = take(sizeof(KSlot) * nd);
+  const uint64_t o_np = take(sizeof(NewPair) * seg_n);
   const uint64_t o_cc = take(4 * FLAT_WG);
+  const uint64_t o_dc = take(4 * FLAT_WG);
   const uint64_t o_lc = take(4 * FLAT_WG);
   if (ws) {
     char *b = static_cast<char *>(base);
@@ -366,6 +391,10 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
     ws->trig = reinterpret_cast<uint64_t *>(b + o_trig);
     ws->def = reinterpret_cast<uint64_t *>(b + o_def);
     ws->cand = reinterpret_cast<Cand *>(b + o_cand);
+    ws->cand_h = reinterpret_cast<uint32_t *>(b + o_ch);
+    ws->kt = reinterpret_cast<KSlot *>(b + o_kt);
+    ws->np = reinterpret_cast<NewPair *>(b + o_np);
+    ws->dup_cnt = reinterpret_cast<uint32_t *>(b + o_dc);
     ws->cand_cnt = reinterpret_cast<uint32_t *>(b + o_cc);
     ws->list_cnt = reinterpret_cast<uint32_t *>(b + o_lc);
     ws->n_dedupe = nd;
@@ -525,16 +554,18 @@ __global__ void ins_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
   }
 }
 
-// Convert the queued keys.  trig holds indexes: key = dd[via[idx]].key when `dd` is
-// given (insert: positions in the dedupe list), else keys[idx] (rebuild).
+// Convert the queued keys.  trig holds indexes: key = np[idx].key when `np` is given
+// (region-ordered insert: new-pair positions), dd[via[idx]].key when `dd` is (insert:
+// positions in the dedupe list), else keys[idx] (rebuild).
 __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned long long *n_trig,
-                             const int *abort_flag, const uint64_t *keys, const DSlot *dd, const uint64_t *via) {
+                             const int *abort_flag, const uint64_t *keys, const DSlot *dd, const uint64_t *via,
+                             const NewPair *np) {
   if (abort_flag && *abort_flag) return;
   const uint64_t n = *n_trig;
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
   for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
     const uint64_t t = trig[i];
-    const uint64_t key = dd ? dd[via[t]].key : keys[t];
+    const uint64_t key = np ? np[t].key : (dd ? dd[via[t]].key : keys[t]);
     if (!spill_key(ix, key)) set_status(ix.hdr, SMETRIC_EINTERNAL);
   }
 }
@@ -607,7 +638,7 @@ __device__ unsigned long long sum_counts(const uint32_t *cnt) {
   return all;
 }
 
-// total candidates -> size of the dedupe table: the least power of two >= 1.5 x candidates
+// total candidates -> size of the key table: the least power of two >= 1.5 x candidates
 __global__ __launch_bounds__(TB) void insp_size_kernel(InsWs ws) {
   const unsigned long long c = sum_counts(ws.cand_cnt);
   if (threadIdx.x != 0) return;
@@ -617,25 +648,94 @@ __global__ __launch_bounds__(TB) void insp_size_kernel(InsWs ws) {
   ws.hdr->n_dd = nd;
 }
 
+// repeated-key candidates -> size of the pair table: a key seen m >= 2 times puts m <= 2 (m - 1)
+// candidates there, so 1.5 x 2 x repeats slots keep it at most 2/3 full
+__global__ __launch_bounds__(TB) void insp_size2_kernel(InsWs ws) {
+  const unsigned long long c = sum_counts(ws.dup_cnt);
+  if (threadIdx.x != 0) return;
+  ws.hdr->n_dup = c;
+  uint64_t nd = 64;
+  while (nd < 3 * c && nd < ws.n_dedupe) nd <<= 1;
+  ws.hdr->n_dd2 = nd;
+}
+
 __global__ void dd_clear_kernel(DSlot *dd, uint64_t n, const unsigned long long *n_dev) {
   const uint64_t nd = n_dev ? *n_dev : n;
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
   for (uint64_t h = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; h < nd; h += stride) dd[h] = DSlot{0, 0};
 }
 
-// workgroup w deduplicates its candidate segment into its new-pair segment
-__global__ __launch_bounds__(TB) void insp_dedupe_kernel(InsWs ws) {
+__global__ void kt_clear_kernel(KSlot *kt, const unsigned long long *n_dev) {
+  const uint64_t nd = *n_dev;
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t h = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; h < nd; h += stride) kt[h] = KSlot{0, 0};
+}
+
+// Claim the candidate's key alone: one compare-and-swap for the first candidate of a key,
+// an increment of the slot's count for every later one.  Returns the slot.
+__device__ uint32_t claim_key(const InsWs &ws, uint64_t nd, uint64_t key, bool &repeat) {
+  uint64_t h = mix64(key ^ 0x5851F42D4C957F2Dull) & (nd - 1);
+  for (uint64_t step = 0; step < nd; ++step, h = (h + 1) & (nd - 1)) {
+    KSlot *k = ws.kt + h;
+    // a plain load first: occupied slots are passed without an atomic
+    uint64_t cur = __hip_atomic_load(&k->key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (cur == KEY_EMPTY) {
+      cur = atomicCAS(reinterpret_cast<unsigned long long *>(&k->key), KEY_EMPTY, key);
+      if (cur == KEY_EMPTY) {
+        repeat = false;
+        return uint32_t(h);
+      }
+    }
+    if (cur == key) {
+      atomicAdd(&k->extra, 1ull);
+      repeat = true;
+      return uint32_t(h);
+    }
+  }
+  ws_error(ws.hdr, SMETRIC_EINTERNAL);
+  repeat = false;
+  return 0;
+}
+
+// workgroup w claims the keys of its candidate segment
+__global__ __launch_bounds__(TB) void insp_keyclaim_kernel(InsWs ws) {
   __shared__ unsigned int lc;
   if (threadIdx.x == 0) lc = 0;
   __syncthreads();
   const uint64_t nd = ws.hdr->n_dd;
   const uint32_t n = ws.cand_cnt[blockIdx.x];
-  const Cand *in = ws.cand + uint64_t(blockIdx.x) * ws.seg;
-  uint64_t *out = ws.list + uint64_t(blockIdx.x) * ws.seg;
+  const uint64_t base = uint64_t(blockIdx.x) * ws.seg;
+  uint32_t mine = 0;
   for (uint32_t k = threadIdx.x; k < n; k += TB) {
-    const Cand c = in[k];
-    const int64_t h = dedupe_pair(ws, nd, c.key, c.w2);
-    if (h >= 0) out[atomicAdd(&lc, 1u)] = uint64_t(h);
+    bool repeat;
+    ws.cand_h[base + k] = claim_key(ws, nd, ws.cand[base + k].key, repeat);
+    mine += repeat;
+  }
+  if (mine) atomicAdd(&lc, mine);
+  __syncthreads();
+  if (threadIdx.x == 0) ws.dup_cnt[blockIdx.x] = lc;
+}
+
+// workgroup w turns its candidate segment into its new-pair segment: a candidate whose key
+// no other candidate has is a distinct new pair as it stands; the others go through the
+// (key, instance) pair table, where the lowest request index wins
+__global__ __launch_bounds__(TB) void insp_dedupe_kernel(InsWs ws) {
+  __shared__ unsigned int lc;
+  if (threadIdx.x == 0) lc = 0;
+  __syncthreads();
+  const uint64_t nd2 = ws.hdr->n_dd2;
+  const uint32_t n = ws.cand_cnt[blockIdx.x];
+  const uint64_t base = uint64_t(blockIdx.x) * ws.seg;
+  for (uint32_t k = threadIdx.x; k < n; k += TB) {
+    const Cand c = ws.cand[base + k];
+    const unsigned long long extra = ws.kt[ws.cand_h[base + k]].extra;
+    int64_t h = -1;
+    bool fresh = true;
+    if (extra != 0) {
+      h = dedupe_pair(ws, nd2, c.key, c.w2);
+      fresh = h >= 0;
+    }
+    if (fresh) ws.np[base + atomicAdd(&lc, 1u)] = NewPair{c.key, c.w2, h};
   }
   __syncthreads();
   if (threadIdx.x == 0) ws.list_cnt[blockIdx.x] = lc;
@@ -678,9 +778,10 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
     const uint32_t k = k0 + threadIdx.x;
     int64_t tk = -1, df = -1;
     if (k < n) {
-      const DSlot d = ws.dd[ws.list[base + k]];
+      const NewPair e = ws.np[base + k];
+      const uint64_t w2 = e.h >= 0 ? ws.dd[e.h].w2 : e.w2;  // a repeated pair's lowest request
       bool trig;
-      const int pl = place_new(ix, d.key, dd_inst(d.w2), epoch, session[dd_req(d.w2)], trig, true);
+      const int pl = place_new(ix, e.key, dd_inst(w2), epoch, session[dd_req(w2)], trig, true);
       if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
       else if (pl == DEFERRED) df = int64_t(base + k);
       else if (trig) tk = int64_t(base + k);
@@ -739,7 +840,7 @@ __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const ui
 __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsigned long long *n_items,
                                 const int *abort_flag, const uint64_t *via, const DSlot *dd,
                                 const uint32_t *session, uint32_t epoch, const uint64_t *keys,
-                                const uint64_t *vals) {
+                                const uint64_t *vals, const NewPair *np) {
   if (abort_flag && *abort_flag) return;
   const uint64_t n = *n_items;
   const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
@@ -747,7 +848,11 @@ __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsign
     const uint64_t t = items[i];
     bool trig;
     int pl;
-    if (via) {
+    if (np) {
+      const NewPair e = np[t];
+      const uint64_t w2 = e.h >= 0 ? dd[e.h].w2 : e.w2;
+      pl = place_new(ix, e.key, dd_inst(w2), epoch, session[dd_req(w2)], trig, false);
+    } else if (via) {
       const DSlot d = dd[via[t]];
       pl = place_new(ix, d.key, dd_inst(d.w2), epoch, session[dd_req(d.w2)], trig, false);
     } else {
@@ -944,9 +1049,9 @@ extern "C" int smetric_index_insert(smetric_index *idx, const uint64_t *keys, co
   hipLaunchKernelGGL(ins_refresh_kernel, rgrid, rblock, 0, stream, ix, ws, blk_off, n_req, n_blocks, epoch);
   hipLaunchKernelGGL(ins_place_kernel, dim3(grid_for(uint64_t(n_blocks))), dim3(TB), 0, stream, ix, ws, session, epoch);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
-                     nullptr, ws.dd, ws.list);
+                     nullptr, ws.dd, ws.list, nullptr);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), dim3(TB), 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,
-                     ws.list, ws.dd, session, epoch, nullptr, nullptr);
+                     ws.list, ws.dd, session, epoch, nullptr, nullptr, nullptr);
   return hip_rc(hipGetLastError());
 }
 
@@ -984,9 +1089,10 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   unsigned long long *n_def = ws.count + 2;
   hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n - m)), dim3(TB), 0, stream, ix, keys, vals, m, n, trig,
                      n_trig, def, n_def, idx->capacity);
-  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr, nullptr);
+  hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr, nullptr,
+                     nullptr);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), dim3(TB), 0, stream, ix, def, n_def, nullptr, nullptr, nullptr,
-                     nullptr, 0u, keys, vals);
+                     nullptr, 0u, keys, vals, nullptr);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   return hip_rc(hipStreamSynchronize(stream));
 }
@@ -1020,7 +1126,7 @@ extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe
                                            int32_t n_req, int64_t n_blocks, const int32_t *instance,
                                            const uint32_t *session, uint32_t epoch, void *workspace,
                                            uint64_t ws_bytes, hipStream_t stream) {
-  if (!idx || !idx->slots || n_req < 0 || n_blocks < 0 || n_blocks >= (int64_t(1) << 32) || epoch >= EPOCH_LIMIT)
+  if (!idx || !idx->slots || n_req < 0 || n_blocks < 0 || n_blocks >= (int64_t(1) << 31) || epoch >= EPOCH_LIMIT)
     return SMETRIC_EINVAL;
   if (n_req == 0) return SMETRIC_OK;
   if (!instance || !session) return SMETRIC_EINVAL;
@@ -1039,15 +1145,18 @@ extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe
   const dim3 flat(FLAT_WG), blk(TB);
   hipLaunchKernelGGL(insp_classify_kernel, flat, blk, 0, stream, ix, pv, ws, instance, session);
   hipLaunchKernelGGL(insp_size_kernel, dim3(1), blk, 0, stream, ws);
+  hipLaunchKernelGGL(kt_clear_kernel, dim3(grid_for(ws.n_dedupe)), blk, 0, stream, ws.kt, &ws.hdr->n_dd);
+  hipLaunchKernelGGL(insp_keyclaim_kernel, flat, blk, 0, stream, ws);
+  hipLaunchKernelGGL(insp_size2_kernel, dim3(1), blk, 0, stream, ws);
   hipLaunchKernelGGL(dd_clear_kernel, dim3(grid_for(ws.n_dedupe)), blk, 0, stream, ws.dd, ws.n_dedupe,
-                     &ws.hdr->n_dd);
+                     &ws.hdr->n_dd2);
   hipLaunchKernelGGL(insp_dedupe_kernel, flat, blk, 0, stream, ws);
   hipLaunchKernelGGL(insp_check_kernel, dim3(1), blk, 0, stream, ix, ws);
   hipLaunchKernelGGL(insp_refresh_kernel, flat, blk, 0, stream, ix, pv, ws, epoch);
   hipLaunchKernelGGL(insp_place_kernel, flat, blk, 0, stream, ix, ws, session, epoch);
   hipLaunchKernelGGL(spill_kernel, dim3(64), blk, 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
-                     nullptr, ws.dd, ws.list);
+                     nullptr, nullptr, nullptr, ws.np);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), blk, 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,
-                     ws.list, ws.dd, session, epoch, nullptr, nullptr);
+                     nullptr, ws.dd, session, epoch, nullptr, nullptr, ws.np);
   return hip_rc(hipGetLastError());
 }

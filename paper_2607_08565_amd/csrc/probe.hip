@@ -202,48 +202,97 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
   }
 }
 
-// Holder descriptor of `key`: one chain walk, each step one 128-byte bucket read.
-__device__ uint64_t describe(const DevIndex &ix, uint64_t key) {
-  uint64_t b = home_bucket(key, ix.n_buckets);
-  uint32_t cnt = 0, first_inst = 0;
-  uint64_t first_slot = 0;
-  for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
-    const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + b * BUCKET_WORDS);
-    ulonglong2 kk[SLOTS / 2], vv[SLOTS / 2];
-#pragma unroll
-    for (int i = 0; i < SLOTS / 2; ++i) kk[i] = p[i];
-#pragma unroll
-    for (int i = 0; i < SLOTS / 2; ++i) vv[i] = p[SLOTS / 2 + i];
-    bool end = false;
-#pragma unroll
-    for (int s = 0; s < SLOTS; ++s) {
-      const uint64_t k = (s & 1) ? kk[s / 2].y : kk[s / 2].x;
-      const uint64_t v = (s & 1) ? vv[s / 2].y : vv[s / 2].x;
-      end |= k == KEY_EMPTY;
-      if (!end && k == key) {
-        const uint32_t kind = val_kind(v);
-        if (kind == HEADER) return make_desc(D_HOT, 0, val_rec(v));
-        if (kind == PLAIN) {
-          if (cnt == 0) {
-            first_inst = val_inst(v);
-            first_slot = b * SLOTS + s;
-          }
-          ++cnt;
-        }
-      }
-    }
-    if (end) break;
-  }
-  if (cnt == 0) return make_desc(D_NONE, 0, 0);
-  if (cnt == 1) return make_desc(D_ONE, first_inst, first_slot);
-  return make_desc(D_MANY, 0, 0);
+// Holder descriptor of a key, built one 128-byte bucket (keys and values at once) per
+// chain step.
+struct DescWalk {
+  uint64_t key, b, first_slot;
+  uint32_t cnt, first_inst;
+  bool done;
+  uint64_t out;
+};
+
+__device__ __forceinline__ void desc_begin(const DevIndex &ix, uint64_t key, DescWalk &w) {
+  w.key = key;
+  w.b = home_bucket(key, ix.n_buckets);
+  w.cnt = 0;
+  w.first_inst = 0;
+  w.first_slot = 0;
+  w.done = false;
+  w.out = 0;
 }
 
+__device__ __forceinline__ void desc_load(const DevIndex &ix, const DescWalk &w, ulonglong2 kk[SLOTS / 2],
+                                          ulonglong2 vv[SLOTS / 2]) {
+  const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + w.b * BUCKET_WORDS);
+#pragma unroll
+  for (int i = 0; i < SLOTS / 2; ++i) kk[i] = p[i];
+#pragma unroll
+  for (int i = 0; i < SLOTS / 2; ++i) vv[i] = p[SLOTS / 2 + i];
+}
+
+// Fold one bucket of the chain into the walk; sets done (and out) when the chain ends.
+__device__ __forceinline__ void desc_step(const DevIndex &ix, DescWalk &w, const ulonglong2 kk[SLOTS / 2],
+                                          const ulonglong2 vv[SLOTS / 2]) {
+  bool end = false;
+#pragma unroll
+  for (int s = 0; s < SLOTS; ++s) {
+    const uint64_t k = (s & 1) ? kk[s / 2].y : kk[s / 2].x;
+    const uint64_t v = (s & 1) ? vv[s / 2].y : vv[s / 2].x;
+    end |= k == KEY_EMPTY;
+    if (!end && k == w.key) {
+      const uint32_t kind = val_kind(v);
+      if (kind == HEADER && !w.done) {
+        w.out = make_desc(D_HOT, 0, val_rec(v));
+        w.done = true;
+      }
+      if (kind == PLAIN) {
+        if (w.cnt == 0) {
+          w.first_inst = val_inst(v);
+          w.first_slot = w.b * SLOTS + s;
+        }
+        ++w.cnt;
+      }
+    }
+  }
+  if (w.done) return;
+  if (end) {
+    w.done = true;
+    w.out = w.cnt == 0 ? make_desc(D_NONE, 0, 0)
+                       : (w.cnt == 1 ? make_desc(D_ONE, w.first_inst, w.first_slot) : make_desc(D_MANY, 0, 0));
+    return;
+  }
+  w.b = next_bucket(w.b, ix.n_buckets);
+}
+
+__device__ __forceinline__ uint64_t desc_finish(const DevIndex &ix, DescWalk &w) {
+  for (uint64_t step = 1; step < ix.n_buckets && !w.done; ++step) {
+    ulonglong2 kk[SLOTS / 2], vv[SLOTS / 2];
+    desc_load(ix, w, kk, vv);
+    desc_step(ix, w, kk, vv);
+  }
+  return w.out;
+}
+
+// Each thread describes two keys of the same iteration (i and i + TB); both first buckets
+// are requested before either is examined, so every lane keeps two lines in flight.  The
+// rare chains longer than one bucket are finished one key at a time.
 __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
   const uint64_t n = pv.hdr->n;
-  const uint64_t span = uint64_t(gridDim.x) * TB;
-  for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += span)
-    pv.desc_p[i] = describe(ix, pv.part_key[i]);
+  const uint64_t span = uint64_t(gridDim.x) * 2 * TB;
+  for (uint64_t i = uint64_t(blockIdx.x) * 2 * TB + threadIdx.x; i < n; i += span) {
+    const uint64_t j = i + TB;
+    const bool has_j = j < n;
+    DescWalk a, b;
+    desc_begin(ix, pv.part_key[i], a);
+    desc_begin(ix, has_j ? pv.part_key[j] : pv.part_key[i], b);
+    ulonglong2 ka[SLOTS / 2], va[SLOTS / 2], kb[SLOTS / 2], vb[SLOTS / 2];
+    desc_load(ix, a, ka, va);
+    desc_load(ix, b, kb, vb);
+    desc_step(ix, a, ka, va);
+    desc_step(ix, b, kb, vb);
+    pv.desc_p[i] = desc_finish(ix, a);
+    if (has_j) pv.desc_p[j] = desc_finish(ix, b);
+  }
 }
 
 }  // namespace
