@@ -81,6 +81,9 @@ __device__ __forceinline__ uint32_t wg_exclusive_scan(uint32_t v, uint32_t *wt, 
 // Items per thread and per tile of the partition loops: U independent loads in flight.
 constexpr int U = 8;
 constexpr int TILE = U * TB;
+// The scatter uses tiles of UW * TB blocks, so that each region's run per tile is longer.
+constexpr int UW = 16;
+constexpr int TILE_W = UW * TB;
 
 __global__ __launch_bounds__(TB) void part_count_kernel(DevIndex ix, ProbeView pv, const uint64_t *__restrict__ keys,
                                                         uint64_t n) {
@@ -140,51 +143,55 @@ __global__ __launch_bounds__(TB) void part_scan_kernel(ProbeView pv) {
 // Workgroup w moves its chunk into region order one tile at a time: LDS counts and ranks
 // per region, the tile regrouped by region in LDS, then each region's part written as one
 // contiguous run after the previous tile's.
-static_assert(NREG == TB, "one region per thread in the tile scan");
+static_assert(NREG <= TB && NREG <= 256, "one region per thread, region ids in a byte");
 __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView pv, const uint64_t *__restrict__ keys,
                                                           uint64_t n) {
   __shared__ unsigned long long run[NREG];
   __shared__ uint32_t cnt[NREG], tstart[NREG], wt[TB / 64];
-  __shared__ uint64_t skey[TILE], sbr[TILE];
-  __shared__ uint16_t sg[TILE];
+  __shared__ uint64_t skey[TILE_W], sbr[TILE_W];
+  __shared__ uint8_t sg[TILE_W];
   if (pv.hdr->err) return;
   const int t = threadIdx.x;
-  run[t] = pv.base[uint64_t(blockIdx.x) * NREG + t];
-  cnt[t] = 0;
+  if (t < NREG) {
+    run[t] = pv.base[uint64_t(blockIdx.x) * NREG + t];
+    cnt[t] = 0;
+  }
   __syncthreads();
   uint64_t lo, hi;
   chunk_of(n, lo, hi);
-  for (uint64_t t0 = lo; t0 < hi; t0 += TILE) {
-    uint64_t k[U];
-    uint32_t r[U], g[U], rk[U];
+  for (uint64_t t0 = lo; t0 < hi; t0 += TILE_W) {
+    uint64_t k[UW];
+    uint32_t r[UW], rk[UW];
+    uint8_t g[UW];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < UW; ++u) {
       const uint64_t b = t0 + u * TB + t;
       k[u] = b < hi ? keys[b] : 0;
       r[u] = b < hi ? pv.req_of[b] : 0;
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      g[u] = region_of(k[u], ix.n_buckets);
+    for (int u = 0; u < UW; ++u) {
+      g[u] = uint8_t(region_of(k[u], ix.n_buckets));
       rk[u] = t0 + u * TB + t < hi ? atomicAdd(&cnt[g[u]], 1u) : 0;
     }
     __syncthreads();
     uint32_t total;
-    tstart[t] = wg_exclusive_scan(cnt[t], wt, &total);
+    const uint32_t before = wg_exclusive_scan(t < NREG ? cnt[t] : 0u, wt, &total);
+    if (t < NREG) tstart[t] = before;
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < UW; ++u) {
       const uint64_t b = t0 + u * TB + t;
       if (b < hi) {
         const uint32_t p = tstart[g[u]] + rk[u];
         skey[p] = k[u];
         sbr[p] = b | (uint64_t(r[u]) << 32);
-        sg[p] = uint16_t(g[u]);
+        sg[p] = g[u];
       }
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < UW; ++u) {
       const uint32_t p = u * TB + t;
       if (p < total) {
         const uint32_t gg = sg[p];
@@ -196,8 +203,10 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
       }
     }
     __syncthreads();
-    run[t] += cnt[t];
-    cnt[t] = 0;
+    if (t < NREG) {
+      run[t] += cnt[t];
+      cnt[t] = 0;
+    }
     __syncthreads();
   }
 }
