@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--direct", action="store_true",
                     help="match and insert probe the index themselves instead of sharing one region-ordered probe")
+    ap.add_argument("--pipelined", action="store_true",
+                    help="two streams: the next batch's hash and partition run beside the current batch's insert "
+                         "(default: one batch at a time on one stream, so each kernel's duration is its own)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (rocprofv3 FETCH_SIZE/WRITE_SIZE), if present")
     return ap.parse_args()
@@ -76,12 +79,16 @@ class Setup:
                 q=torch.from_numpy(b.q).cuda()))
         max_blocks = max(d["n_blocks"] for d in self.dev)
         self.keys = torch.empty(max_blocks, dtype=torch.uint64, device="cuda")
+        self.keys2 = [self.keys, torch.empty(max_blocks, dtype=torch.uint64, device="cuda")]
         self.matched = torch.empty((args.n_req, args.n_inst), dtype=torch.int32, device="cuda")
         self.target = torch.empty(args.n_req, dtype=torch.int32, device="cuda")
         self.branch = torch.empty(args.n_req, dtype=torch.uint8, device="cuda")
         self.filler_chunk = 16_000_000
         self.ws = torch.empty(S.insert_ws_bytes(max(max_blocks, self.filler_chunk)), dtype=torch.uint8, device="cuda")
         self.probe_state = torch.empty(S.probe_ws_bytes(max_blocks), dtype=torch.uint8, device="cuda")
+        self.state2 = [self.probe_state, torch.empty(S.probe_ws_bytes(max_blocks), dtype=torch.uint8, device="cuda")]
+        # default-priority streams: front = hash + partition, back = lookup .. insert
+        self.sA, self.sB = torch.cuda.Stream(), torch.cuda.Stream()
         # index: the prior turns of every batch's sessions, then filler
         growth = 30_000_000 * self.n_batches
         self.capacity = args.index_entries + growth
@@ -131,6 +138,76 @@ class Setup:
             c += 1
 
     CALLS = ("hash", "probe", "match", "route", "insert")
+    PCALLS = ("hash", "partition", "lookup", "match", "route", "insert")
+
+    def front(self, b: int, ev=None):
+        """Batch b's hash and partition: they read no index contents."""
+        S, d, p = self.S, self.dev[b], b % 2
+        rec = (lambda k, i: ev[k][i].record()) if ev is not None else (lambda k, i: None)
+        nb = d["n_blocks"]
+        rec("hash", 0)
+        S.hash_blocks(d["tokens"], d["tok_off"], d["blk_off"], nb, keys=self.keys2[p])
+        rec("hash", 1)
+        rec("partition", 0)
+        self.index.probe_partition(self.keys2[p], d["blk_off"], nb, state=self.state2[p])
+        rec("partition", 1)
+
+    def back(self, b: int, ev=None, before_insert=None):
+        """Batch b's lookup, match, route and insert."""
+        S, d, tb, p = self.S, self.dev[b], self.host[b], b % 2
+        rec = (lambda k, i: ev[k][i].record()) if ev is not None else (lambda k, i: None)
+        nb = d["n_blocks"]
+        rec("lookup", 0)
+        self.index.probe_lookup(self.state2[p], nb)
+        rec("lookup", 1)
+        rec("match", 0)
+        self.index.match_probed(self.state2[p], self.keys2[p], d["blk_off"], nb, matched=self.matched)
+        rec("match", 1)
+        rec("route", 0)
+        S.route(self.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], self.W.DEFAULT_PARAMS,
+                tb.batch.rr_base, target=self.target, branch=self.branch)
+        rec("route", 1)
+        if before_insert is not None:
+            before_insert()
+        rec("insert", 0)
+        self.index.insert_probed(self.state2[p], self.args.n_req, nb, self.target, d["session"], tb.batch.epoch,
+                                 workspace=self.ws)
+        rec("insert", 1)
+
+    def run_pipelined(self, b0: int, n: int, evs=None, after_back=None):
+        """Batches b0 .. b0+n-1 on two streams: batch b+1's front (hash, partition) starts
+        when batch b's insert does and runs beside it; back(b+1) waits for front(b+1) and,
+        on its own stream, for insert(b).  front(b+1) reuses the keys and probe-state
+        buffers of batch b-1, whose back has finished before insert(b) starts."""
+        torch = self.torch
+        done_front, at_insert = {}, {}
+
+        def do_front(b):
+            with torch.cuda.stream(self.sA):
+                if b - 1 in at_insert:
+                    self.sA.wait_event(at_insert[b - 1])
+                self.front(b, evs[b - b0] if evs else None)
+                e = torch.cuda.Event()
+                e.record(self.sA)
+                done_front[b] = e
+
+        def do_back(b):
+            def mark():
+                e = torch.cuda.Event()
+                e.record(self.sB)
+                at_insert[b] = e
+
+            with torch.cuda.stream(self.sB):
+                self.sB.wait_event(done_front[b])
+                self.back(b, evs[b - b0] if evs else None, before_insert=mark)
+
+        do_front(b0)
+        for k in range(n):
+            do_back(b0 + k)
+            if after_back is not None:
+                after_back(b0 + k)
+            if k + 1 < n:
+                do_front(b0 + k + 1)
 
     def step(self, b: int, ev=None):
         """The timed unit: every call of the path on the current stream."""
@@ -410,27 +487,47 @@ def main():
     torch.cuda.set_device(0)
     setup = Setup(args)
     S = setup.S
+    pipelined = args.pipelined and not args.direct
     # warmup (untimed); batch 0's outputs are kept for the sampled oracle check
     gpu_out = None
-    for b in range(args.warmup):
-        setup.step(b)
+
+    def capture(b):
+        nonlocal gpu_out
         if b == 0:
             torch.cuda.synchronize()
             nb0 = setup.dev[0]["n_blocks"]
-            gpu_out = (setup.keys[:nb0].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
+            gpu_out = (setup.keys2[0][:nb0].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
                        setup.branch.cpu().numpy())
+
+    if pipelined:
+        setup.run_pipelined(0, args.warmup, after_back=capture)
+    else:
+        for b in range(args.warmup):
+            setup.step(b)
+            capture(b)
     torch.cuda.synchronize()
     n_before, _ = setup.index.stats()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
-    mats = []
+    if pipelined:
+        evs = [{c: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for c in Setup.PCALLS} for _ in range(args.steps)]
+    else:
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
-        setup.step(args.warmup + k, evs[k])
+    if pipelined:
+        setup.run_pipelined(args.warmup, args.steps, evs)
+    else:
+        for k in range(args.steps):
+            setup.step(args.warmup + k, evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = {n: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
-           for i, n in enumerate(Setup.CALLS)}
+    if pipelined:
+        per = {c: float(np.mean([evs[k][c][0].elapsed_time(evs[k][c][1]) for k in range(args.steps)]))
+               for c in Setup.PCALLS}
+        per["probe"] = per["partition"] + per["lookup"]
+    else:
+        per = {n: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
+               for i, n in enumerate(Setup.CALLS)}
     n, st = setup.index.stats()
     assert st == 0, f"index status {st}"
     # algorithmic bytes for the last timed batch (match outputs still in the buffer)
@@ -476,7 +573,9 @@ def main():
                    "n_instances": args.n_inst, "requests_per_batch": R, "block_size": 16,
                    "index_entries_start": setup.start_entries, "index_entries_end": n,
                    "index_capacity": setup.capacity, "tokens_per_batch": int(tokens)},
-        "path": "direct" if args.direct else "region-ordered probe",
+        "path": ("direct" if args.direct else "region-ordered probe") + (
+            "; next batch's hash + partition overlap this batch's insert (2 streams)" if pipelined else
+            "; one batch at a time"),
         "prompt_tokens_matched_per_s": round(tokens / ((per["hash"] + probe_match_ms) / 1e3), 1),
         "kernel_ms": {k: round(v, 4) for k, v in per.items()},
         "algorithmic_GBs": {k: round(v, 1) for k, v in gbs.items()},

@@ -188,6 +188,18 @@ int smetric_match(const smetric_index *idx, const uint64_t *keys, const int64_t 
 int smetric_probe_ws_bytes(int64_t n_blocks, uint64_t *bytes /* host */);
 int smetric_probe(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
                   int64_t n_blocks, void *probe, uint64_t probe_bytes, hipStream_t stream);
+/* smetric_probe in two halves, for pipelining consecutive batches:
+ *   smetric_probe_partition  validates the tiling and orders the batch's blocks by table
+ *                            region; it reads only the index geometry, never its contents, so it
+ *                            may run while an earlier batch still inserts into the index;
+ *   smetric_probe_lookup     reads the index (the descriptors then describe the index as it is
+ *                            when this runs), after smetric_probe_partition on the same state.
+ * smetric_probe = smetric_probe_partition followed by smetric_probe_lookup on one stream. */
+int smetric_probe_partition(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
+                            int32_t n_req, int64_t n_blocks, void *probe, uint64_t probe_bytes,
+                            hipStream_t stream);
+int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes, int64_t n_blocks,
+                         hipStream_t stream);
 int smetric_match_probed(const smetric_index *idx, const void *probe, uint64_t probe_bytes,
                          const uint64_t *keys, const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
                          int32_t *matched, hipStream_t stream);

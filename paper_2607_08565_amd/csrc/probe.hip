@@ -315,15 +315,24 @@ extern "C" int smetric_probe_ws_bytes(int64_t n_blocks, uint64_t *bytes) {
   return SMETRIC_OK;
 }
 
-extern "C" int smetric_probe(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
-                             int64_t n_blocks, void *probe, uint64_t probe_bytes, hipStream_t stream) {
+namespace {
+int probe_args(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+               int64_t n_blocks, void *probe, uint64_t probe_bytes) {
   if (!idx || !idx->slots || n_req < 0 || n_blocks < 0 || n_blocks >= (int64_t(1) << 32)) return SMETRIC_EINVAL;
   if (!blk_off || (n_blocks > 0 && !keys) || (n_req == 0 && n_blocks != 0)) return SMETRIC_EINVAL;
   if (!probe || (reinterpret_cast<uintptr_t>(probe) & 255) || probe_bytes < probe_layout(n_blocks, nullptr, nullptr))
     return SMETRIC_EWORKSPACE;
+  return SMETRIC_OK;
+}
+}  // namespace
+
+extern "C" int smetric_probe_partition(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
+                                       int32_t n_req, int64_t n_blocks, void *probe, uint64_t probe_bytes,
+                                       hipStream_t stream) {
+  if (int rc = probe_args(idx, keys, blk_off, n_req, n_blocks, probe, probe_bytes)) return rc;
   ProbeView pv;
   probe_layout(n_blocks, &pv, probe);
-  const DevIndex ix = dev_view(idx);
+  const DevIndex ix = dev_view(idx);  // geometry only: the table's contents are not read here
   const uint64_t n = uint64_t(n_blocks);
   hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hdr),
                      uint64_t(sizeof(ProbeHdr) / 8));
@@ -332,6 +341,22 @@ extern "C" int smetric_probe(const smetric_index *idx, const uint64_t *keys, con
   hipLaunchKernelGGL(part_count_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
   hipLaunchKernelGGL(part_scan_kernel, dim3(NREG), dim3(TB), 0, stream, pv);
   hipLaunchKernelGGL(part_scatter_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
-  hipLaunchKernelGGL(probe_kernel, dim3(FLAT_WG), dim3(TB), 0, stream, ix, pv);
   return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes, int64_t n_blocks,
+                                    hipStream_t stream) {
+  if (!idx || !idx->slots || n_blocks < 0 || n_blocks >= (int64_t(1) << 32)) return SMETRIC_EINVAL;
+  if (!probe || (reinterpret_cast<uintptr_t>(probe) & 255) || probe_bytes < probe_layout(n_blocks, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  ProbeView pv;
+  probe_layout(n_blocks, &pv, probe);
+  hipLaunchKernelGGL(probe_kernel, dim3(FLAT_WG), dim3(TB), 0, stream, dev_view(idx), pv);
+  return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_probe(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                             int64_t n_blocks, void *probe, uint64_t probe_bytes, hipStream_t stream) {
+  if (int rc = smetric_probe_partition(idx, keys, blk_off, n_req, n_blocks, probe, probe_bytes, stream)) return rc;
+  return smetric_probe_lookup(idx, probe, probe_bytes, n_blocks, stream);
 }

@@ -76,6 +76,8 @@ def _load() -> C.CDLL:
         "smetric_index_dump": [PIX, P, P, U64, P, U64, P, P],
         "smetric_probe_ws_bytes": [I64, P],
         "smetric_probe": [PIX, P, P, I32, I64, P, U64, P],
+        "smetric_probe_partition": [PIX, P, P, I32, I64, P, U64, P],
+        "smetric_probe_lookup": [PIX, P, U64, I64, P],
         "smetric_match_probed": [PIX, P, U64, P, P, I32, I64, P, P],
         "smetric_index_insert_probed": [PIX, P, U64, I32, I64, P, P, U32, P, U64, P],
     }
@@ -95,6 +97,7 @@ EXPORTED = (
     "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
     "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq", "smetric_sessions_ws_bytes",
     "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
+    "smetric_probe_partition", "smetric_probe_lookup",
 )
 
 
@@ -365,6 +368,24 @@ class Index:
         _check("smetric_probe", _lib.smetric_probe(
             self.ref, _dev(keys, torch.uint64, "keys"), _dev(blk_off, torch.int64, "blk_off"), R, n_blocks,
             C.c_void_p(state.data_ptr()), state.numel(), _stream()))
+        return state
+
+    def probe_partition(self, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int,
+                        state: torch.Tensor | None = None):
+        """First half of probe(): reads only the index geometry (may overlap an earlier insert)."""
+        R = blk_off.numel() - 1
+        need = probe_ws_bytes(n_blocks)
+        if state is None or state.numel() < need:
+            state = torch.empty(need, dtype=torch.uint8, device=keys.device)
+        _check("smetric_probe_partition", _lib.smetric_probe_partition(
+            self.ref, _dev(keys, torch.uint64, "keys"), _dev(blk_off, torch.int64, "blk_off"), R, n_blocks,
+            C.c_void_p(state.data_ptr()), state.numel(), _stream()))
+        return state
+
+    def probe_lookup(self, state: torch.Tensor, n_blocks: int):
+        """Second half of probe(): reads the index."""
+        _check("smetric_probe_lookup", _lib.smetric_probe_lookup(
+            self.ref, C.c_void_p(state.data_ptr()), state.numel(), n_blocks, _stream()))
         return state
 
     def match_probed(self, state: torch.Tensor, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int,

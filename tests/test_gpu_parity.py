@@ -92,6 +92,53 @@ def test_config3_scaled_with_eviction(probed):
     run_sessions(wl, 5, capacity=400_000, evict=(1, 20), probed=probed)
 
 
+def test_partition_overlaps_previous_insert():
+    """Two streams: batch t+1's hash and partition run while batch t's insert is still
+    queued on the other stream (the partition reads the index geometry only); lookup waits
+    for both.  Every matched row, target, branch and the final dump equal the oracle's."""
+    from paper_2607_08565_amd import smetric as S
+    wl = W.config1(n_sess=192, n_turns=6, l0=1024, app=(64, 1536), cap=16384, prefix_len=512)
+    pair = Pair(2_000_000, wl.n_inst)
+    sA, sB = torch.cuda.Stream(), torch.cuda.Stream()
+    keys = [torch.empty(1 << 20, dtype=torch.uint64, device="cuda") for _ in range(2)]
+    states = [None, None]
+    prev_t, held = None, []
+    for t in range(6):
+        b = wl.batch(t, prev_t)
+        blk_off, nb = S.block_offsets(b.tok_off)
+        assert nb <= keys[0].numel()
+        d_tok, d_toff, d_boff = to_dev(b.tokens), to_dev(b.tok_off), to_dev(blk_off)
+        held.append((d_tok, d_toff, d_boff))  # read on other streams: keep them alive to the end
+        p = t % 2
+        # keys[p] and states[p] were last read by batch t-2, finished at t-1's synchronize below
+        sA.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(sA):
+            S.hash_blocks(d_tok, d_toff, d_boff, nb, keys=keys[p])
+            states[p] = pair.gix.probe_partition(keys[p], d_boff, nb, state=states[p])
+            front = torch.cuda.Event()
+            front.record(sA)
+        _, okeys = oracle.hash_blocks(b.tokens, b.tok_off, W.BLOCK, W.DEFAULT_SEED)
+        with torch.cuda.stream(sB):
+            sB.wait_event(front)
+            pair.gix.probe_lookup(states[p], nb)
+            gm = pair.gix.match_probed(states[p], keys[p], d_boff, nb)
+            gt, gb = S.route(gm, to_dev(b.prompt_len), to_dev(b.hist_len), to_dev(b.turn), to_dev(b.q),
+                             W.DEFAULT_PARAMS, b.rr_base)
+            sB.synchronize()
+            om = pair.oix.match(okeys, blk_off)
+            ot, ob = oracle.route(om, b.prompt_len, b.hist_len, b.turn, b.q, W.DEFAULT_PARAMS, b.rr_base)
+            assert np.array_equal(gm.cpu().numpy(), om), f"batch {t}: matched rows differ"
+            assert np.array_equal(gt.cpu().numpy(), ot) and np.array_equal(gb.cpu().numpy(), ob), f"batch {t}"
+            # the insert stays queued on sB while the loop builds, hashes and partitions t+1 on sA
+            pair.gix.insert_probed(states[p], b.n_req, nb, to_dev(np.asarray(ot, np.int32)),
+                                   to_dev(np.asarray(b.session, np.uint32)), b.epoch)
+        assert pair.oix.insert(okeys, blk_off, ot, b.session, b.epoch) == 0
+        prev_t = ot
+        say(f"  batch {t}: R={b.n_req} blocks={nb}")
+    torch.cuda.synchronize()
+    pair.compare_index("after the pipelined batches")
+
+
 def test_many_instances_wide_words():
     """I = 5000 (two bitmap words per lane) and a prefix shared by 300 instances."""
     rng = np.random.default_rng(5)
