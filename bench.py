@@ -243,9 +243,10 @@ CALL_KERNELS = {
     "probe": ["zero_kernel", "req_of_kernel", "part_count_kernel", "part_scan_kernel", "part_scatter_kernel",
               "probe_kernel"],
     "match": ["match_kernel<1, true>"],
-    "route": ["route_kernel"],
-    "insert": ["fill_kernel", "insp_classify_kernel", "insp_size_kernel", "dd_clear_kernel", "insp_dedupe_kernel",
-               "insp_check_kernel", "insp_refresh_kernel", "insp_place_kernel", "spill_kernel", "deferred_kernel"],
+    "route": ["route_kernel<0>"],
+    "insert": ["fill_kernel", "insp_classify_kernel", "insp_size_kernel", "kt_clear_kernel", "insp_keyclaim_kernel",
+               "insp_size2_kernel", "dd_clear_kernel", "insp_dedupe_kernel", "insp_check_kernel", "insp_refresh_kernel",
+               "insp_place_kernel", "spill_kernel", "deferred_kernel"],
 }
 
 
