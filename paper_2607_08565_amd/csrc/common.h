@@ -83,8 +83,9 @@ __device__ inline uint64_t home_bucket(uint64_t key, uint64_t n_buckets) {
   return __umul64hi(mix64(key), n_buckets);
 }
 // Table regions: the bucket range split into NREG equal parts.  Probes, refreshes and
-// claims are issued region by region so the pages live at any moment stay few.
-constexpr int NREG = 256;
+// claims are issued region by region so the pages live at any moment stay within the
+// translation caches' reach (~2 GiB); few regions keep the partition's runs long.
+constexpr int NREG = 16;
 __device__ __forceinline__ uint32_t region_of(uint64_t key, uint64_t n_buckets) {
   return uint32_t(home_bucket(key, n_buckets) * NREG / n_buckets);
 }

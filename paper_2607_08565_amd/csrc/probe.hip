@@ -5,10 +5,10 @@
 // same question per block -- which instances hold this key -- so it is asked once.
 //
 // Mapping to gfx950.  Probes are random 128-byte reads over a table of several GB.  On
-// MI355X such reads run ~5x faster when the workgroups in flight stay inside a window of
-// a GB or less than when they roam the whole table (the translation caches keep up), so
-// the batch's blocks are first partitioned by table region (NREG equal bucket ranges),
-// with no global atomics:
+// MI355X such reads run at ~44 G lines/s while the lines in flight stay inside ~2 GiB and
+// drop to 10-14 G lines/s over 4-9 GiB (the reach of the address-translation caches), so
+// the batch's blocks are first partitioned by table region (NREG equal bucket ranges, each
+// well inside that reach), with no global atomics:
 //   requests  one wavefront per request checks the tiling and records each block's request
 //   count     PART_WG workgroups, one contiguous chunk of blocks each: LDS histogram of
 //             regions -> one row of the [chunk][region] matrix, plus region totals
