@@ -228,14 +228,31 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
 #pragma unroll
   for (int t = 0; t < WPL; ++t) A[t] = 0;
 
-  // DESC: the next chunk's descriptors are loaded while the current one is processed
-  uint64_t d_cur = 0;
-  if (DESC && lane < nb) d_cur = desc[inv[b0 + lane]];
+  // DESC: descriptors are fetched PF chunks at a time -- positions, then all PF gathers
+  // at once -- since a chunk's own work rarely touches memory and the walk is otherwise
+  // one round trip per chunk
+  constexpr int PF = DESC ? 8 : 1;
+  uint64_t dq[PF];
+  int left = 0;
   for (int64_t j0 = 0; j0 < nb && mode != M_DONE; j0 += 64) {
     const int64_t j = j0 + lane;
     const bool valid = j < nb;
-    uint64_t d_next = 0;
-    if (DESC && j + 64 < nb) d_next = desc[inv[b0 + j + 64]];
+    if (DESC && left == 0) {
+      // indexes clamped to the request's last block, so that the loads need no branches
+      // (a branch around a load makes the compiler wait for it on the spot)
+      uint32_t at[PF];
+#pragma unroll
+      for (int k = 0; k < PF; ++k) at[k] = inv[b0 + (j + 64 * k < nb ? j + 64 * k : nb - 1)];
+#pragma unroll
+      for (int k = 0; k < PF; ++k) dq[k] = desc[at[k]];
+#pragma unroll
+      for (int k = 0; k < PF; ++k) dq[k] = j + 64 * k < nb ? dq[k] : 0;
+      left = PF;
+    }
+    const uint64_t d_cur = dq[0];
+#pragma unroll
+    for (int k = 0; k + 1 < PF; ++k) dq[k] = dq[k + 1];
+    --left;
     Holders H;
     uint64_t key = 0;
     if (valid) {
@@ -282,18 +299,37 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
       constexpr int G = WPL >= 8 ? 1 : 8 / WPL;
       while (jj < 64 && mode == M_WIDE) {
         uint64_t hw[G][WPL];
+        uint32_t kinds[G];
+        // bitmap words of all G blocks requested at once, with no branch around the loads
+        // (a non-HOT block reads record 0, always present, and discards it), so the
+        // group costs one round trip
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           const int src = jj + g < 64 ? jj + g : 63;
-          const uint32_t kind = __builtin_amdgcn_readlane(H.kind, src);
-          const uint64_t rec = rdl64(H.rec, src);
-          const uint64_t k = rdl64(key, src);
-          uint32_t hl[LIST_MAX];
+          const bool in = jj + g < 64 && j0 + jj + g < nb;
+          kinds[g] = in ? __builtin_amdgcn_readlane(H.kind, src) : uint32_t(H_NONE);
+          const uint64_t rec = kinds[g] == H_HOT ? rdl64(H.rec, src) : 0;
 #pragma unroll
-          for (int i = 0; i < LIST_MAX; ++i) hl[i] = __builtin_amdgcn_readlane(H.h[i], src);
+          for (int t = 0; t < WPL; ++t) {
+            const int w = lane + 64 * t;
+            hw[g][t] = ix.pool[rec * uint64_t(ix.words) + uint64_t(w < ix.words ? w : 0)];
+          }
+        }
 #pragma unroll
-          for (int t = 0; t < WPL; ++t)
-            hw[g][t] = (jj + g < 64 && j0 + jj + g < nb) ? holder_word(ix, kind, rec, hl, k, lane + 64 * t) : 0;
+        for (int g = 0; g < G; ++g) {
+          if (kinds[g] == H_HOT) {
+#pragma unroll
+            for (int t = 0; t < WPL; ++t)
+              if (lane + 64 * t >= ix.words) hw[g][t] = 0;
+          } else {
+            const int src = jj + g < 64 ? jj + g : 63;
+            const uint64_t k = rdl64(key, src);
+            uint32_t hl[LIST_MAX];
+#pragma unroll
+            for (int i = 0; i < LIST_MAX; ++i) hl[i] = __builtin_amdgcn_readlane(H.h[i], src);
+#pragma unroll
+            for (int t = 0; t < WPL; ++t) hw[g][t] = holder_word(ix, kinds[g], 0, hl, k, lane + 64 * t);
+          }
         }
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -366,7 +402,6 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
       }
       if (!__ballot(my_inst >= 0)) mode = M_DONE;
     }
-    d_cur = d_next;
   }
   // survivors of a request whose block count is a multiple of 64
   if (mode == M_NARROW) {
