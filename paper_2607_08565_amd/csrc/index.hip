@@ -573,11 +573,37 @@ __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned l
 // ---------------------------------------------------------------------------------
 // Region-ordered insert, from the descriptors of smetric_probe
 // ---------------------------------------------------------------------------------
+// find_member with each bucket read whole (keys and values in one 128-byte request), so
+// a chain step is one round trip.
+__device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t inst) {
+  uint64_t m = member_bucket(key, inst, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step, m = next_bucket(m, ix.n_buckets)) {
+    const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + m * BUCKET_WORDS);
+    ulonglong2 kk[SLOTS / 2], vv[SLOTS / 2];
+#pragma unroll
+    for (int i = 0; i < SLOTS / 2; ++i) kk[i] = p[i];
+#pragma unroll
+    for (int i = 0; i < SLOTS / 2; ++i) vv[i] = p[SLOTS / 2 + i];
+    bool end = false;
+#pragma unroll
+    for (int s = 0; s < SLOTS; ++s) {
+      const uint64_t k = (s & 1) ? kk[s / 2].y : kk[s / 2].x;
+      const uint64_t v = (s & 1) ? vv[s / 2].y : vv[s / 2].x;
+      end |= k == KEY_EMPTY;
+      if (!end && k == key && val_kind(v) == MEMBER && val_inst(v) == inst) return Found{int64_t(m * SLOTS + s), v};
+    }
+    if (end) break;
+  }
+  return Found{-1, 0};
+}
+
 // classify: per probed block (region order), is (key, target) already an entry?  The
 // descriptor answers it for NONE and ONE; HOT needs the bitmap bit and the member slot
 // (inside the key's region), MANY a chain walk.  Existing -> refresh position; absent ->
 // candidate, appended to this workgroup's segment (LDS counter, no global atomics).
-// All FLAT_WG workgroups advance through the region order together.
+// All FLAT_WG workgroups advance through the region order together.  Each thread takes
+// CU positions per round (the same positions as a plain grid-stride loop, so segments
+// keep their bound), with every load of the round issued before any result is used.
 __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeView pv, InsWs ws,
                                                            const int32_t *instance, const uint32_t *session) {
   __shared__ unsigned int lc;
@@ -593,31 +619,55 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
     return;
   }
   Cand *seg = ws.cand + uint64_t(blockIdx.x) * ws.seg;
+  constexpr int CU = 4;
   const uint64_t span = uint64_t(gridDim.x) * TB;
-  for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += span) {
-    const uint64_t key = pv.part_key[i];
-    const uint32_t r = uint32_t(pv.part_br[i] >> 32);
-    const int32_t t = instance[r];
-    const uint32_t sess = session[r];
-    uint64_t pos = 0;
-    if (t < 0 || t >= ix.n_inst || sess >= SESSION_LIMIT || key == KEY_EMPTY || key == KEY_TOMB) {
-      ws_error(ws.hdr, SMETRIC_EINVAL);
-    } else {
-      const uint64_t d = pv.desc_p[i];
-      const uint32_t kind = desc_kind(d);
-      int64_t slot = -1;
-      if (kind == D_ONE) {
-        if (desc_inst(d) == uint32_t(t)) slot = int64_t(desc_x(d));
-      } else if (kind == D_HOT) {
-        const uint64_t w = ix.pool[desc_x(d) * uint64_t(ix.words) + (uint32_t(t) >> 6)];
-        if ((w >> (t & 63)) & 1) slot = find_member(ix, key, uint32_t(t)).slot;
-      } else if (kind == D_MANY) {
-        slot = find_entry(ix, key, uint32_t(t)).slot;
-      }
-      if (slot >= 0) pos = uint64_t(slot) + 1;
-      else seg[atomicAdd(&lc, 1u)] = Cand{key, ((uint64_t(t) + 1) << 32) | r};
+  for (uint64_t i0 = uint64_t(blockIdx.x) * TB + threadIdx.x; i0 < n; i0 += CU * span) {
+    // positions past the end read the last position (in bounds) and are dropped below
+    uint64_t key[CU], d[CU];
+    uint32_t r[CU];
+#pragma unroll
+    for (int u = 0; u < CU; ++u) {
+      const uint64_t i = i0 + u * span < n ? i0 + u * span : n - 1;
+      key[u] = pv.part_key[i];
+      r[u] = uint32_t(pv.part_br[i] >> 32);
+      d[u] = pv.desc_p[i];
     }
-    ws.pos[i] = pos;
+    int32_t t[CU];
+    uint32_t sess[CU];
+#pragma unroll
+    for (int u = 0; u < CU; ++u) {
+      t[u] = instance[r[u]];
+      sess[u] = session[r[u]];
+    }
+    // HOT: the target's bitmap word (a block of another kind reads record 0, always present)
+    uint64_t hw[CU];
+#pragma unroll
+    for (int u = 0; u < CU; ++u) {
+      const bool hot = desc_kind(d[u]) == D_HOT && t[u] >= 0 && t[u] < ix.n_inst;
+      hw[u] = ix.pool[(hot ? desc_x(d[u]) : 0) * uint64_t(ix.words) + (hot ? uint32_t(t[u]) >> 6 : 0u)];
+    }
+#pragma unroll
+    for (int u = 0; u < CU; ++u) {
+      const uint64_t i = i0 + u * span;
+      if (i >= n) break;
+      uint64_t pos = 0;
+      if (t[u] < 0 || t[u] >= ix.n_inst || sess[u] >= SESSION_LIMIT || key[u] == KEY_EMPTY || key[u] == KEY_TOMB) {
+        ws_error(ws.hdr, SMETRIC_EINVAL);
+      } else {
+        const uint32_t kind = desc_kind(d[u]);
+        int64_t slot = -1;
+        if (kind == D_ONE) {
+          if (desc_inst(d[u]) == uint32_t(t[u])) slot = int64_t(desc_x(d[u]));
+        } else if (kind == D_HOT) {
+          if ((hw[u] >> (t[u] & 63)) & 1) slot = find_member_line(ix, key[u], uint32_t(t[u])).slot;
+        } else if (kind == D_MANY) {
+          slot = find_entry(ix, key[u], uint32_t(t[u])).slot;
+        }
+        if (slot >= 0) pos = uint64_t(slot) + 1;
+        else seg[atomicAdd(&lc, 1u)] = Cand{key[u], ((uint64_t(t[u]) + 1) << 32) | r[u]};
+      }
+      ws.pos[i] = pos;
+    }
   }
   __syncthreads();
   if (threadIdx.x == 0) ws.cand_cnt[blockIdx.x] = lc;
