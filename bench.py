@@ -343,6 +343,25 @@ def cpu_baseline(setup, budget_s: float, gpu_out):
                        f"index restricted to their keys, single thread, {dt:.1f} s"), parity, n
 
 
+def measure_evict(setup):
+    """LRU eviction (5 % of the entries, the divergent-prefix configuration's rate) of the
+    whole bench index after the timed batches: one call, wall-clock with device syncs (the
+    call's rebuild ends in a stream sync of its own).  Exact count checked at full size:
+    ceil(N / 20) entries go, status stays 0."""
+    import torch
+
+    n0, _ = setup.index.stats()
+    setup.index.evict_ws_bytes()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    setup.index.evict(1, 20)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    n1, st = setup.index.stats()
+    return {"fraction": "1/20", "ms": round(dt * 1e3, 2), "entries_before": n0, "entries_after": n1,
+            "entries_per_s": round(n0 / dt, 1), "exact_count": bool(n0 - n1 == -(-n0 // 20) and st == 0)}
+
+
 def measure_variants(setup, b: int, reps: int = 20):
     """Route variants on the match rows of batch b (still in the output buffer), each
     event-timed over `reps` calls on the current stream."""
@@ -587,6 +606,7 @@ def main():
     }
     variants, var_inputs = measure_variants(setup, last)
     out["variants"] = variants
+    out["evict"] = measure_evict(setup)
     if not args.no_cpu_baseline:
         cb, parity, n_s = cpu_baseline(setup, args.cpu_seconds, gpu_out)
         out["cpu_baseline"] = cb

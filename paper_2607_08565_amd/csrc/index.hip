@@ -435,6 +435,29 @@ __device__ int64_t dedupe_pair(const InsWs &ws, uint64_t nd, uint64_t key, uint6
   return -1;
 }
 
+// Append base + j for every bit j of each lane's mask: one atomicAdd per wavefront.
+__device__ __forceinline__ void append_wave_mask(unsigned long long *counter, uint64_t *list, uint64_t cap,
+                                                 uint32_t mask, uint64_t base) {
+  const uint32_t c = __popc(mask);
+  if (!__ballot(c != 0)) return;
+  const int lane = threadIdx.x & 63;
+  uint32_t x = c;  // inclusive prefix over the wavefront
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  unsigned long long at = 0;
+  if (lane == 63) at = atomicAdd(counter, (unsigned long long)x);
+  at = __shfl(at, 63, 64) + (x - c);
+  while (mask) {
+    const int j = __builtin_ctz(mask);
+    mask &= mask - 1;
+    if (at < cap) list[at] = base + uint64_t(j);  // callers size the list to hold every entry
+    ++at;
+  }
+}
+
 // Append `h` (when >= 0) to the list: one atomicAdd per wavefront for all its lanes.
 __device__ __forceinline__ void append_wave(unsigned long long *counter, uint64_t *list, uint64_t cap, int64_t h) {
   const uint64_t want = __ballot(h >= 0);
@@ -844,43 +867,154 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
 // ---------------------------------------------------------------------------------
 // Evict / dump
 // ---------------------------------------------------------------------------------
-__global__ void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals, unsigned long long *count,
-                              uint64_t cap) {
-  const uint64_t n_slots = ix.n_buckets * SLOTS;
-  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_slots; i += stride) {
-    const uint64_t b = i / SLOTS, s = i % SLOTS;
-    const uint64_t k = ix.slots[b * BUCKET_WORDS + s];
-    if (k == KEY_EMPTY || k == KEY_TOMB) continue;
-    const uint64_t v = ix.slots[b * BUCKET_WORDS + SLOTS + s];
-    if (val_kind(v) == HEADER) continue;
-    const unsigned long long at = atomicAdd(count, 1ull);
-    if (at < cap) {
-      keys[at] = k;
-      vals[at] = val_plain(v);
+// All live entries (plain and member slots; headers are not entries), in no particular
+// order.  Each thread takes GB consecutive buckets per round; a workgroup reserves its
+// round's output with one atomic (one per entry made a single counter the bottleneck).
+constexpr int GB = 2;
+__global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals,
+                                                    unsigned long long *count, uint64_t cap) {
+  __shared__ uint32_t wt[TB / 64];
+  __shared__ unsigned long long wg_base;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t per_round = uint64_t(TB) * GB;
+  for (uint64_t b0 = uint64_t(blockIdx.x) * per_round; b0 < ix.n_buckets; b0 += uint64_t(gridDim.x) * per_round) {
+    uint32_t live = 0;  // bit s + SLOTS * g: slot s of bucket g is an entry
+    uint64_t k[GB][SLOTS], v[GB][SLOTS];
+#pragma unroll
+    for (int g = 0; g < GB; ++g) {
+      const uint64_t b = b0 + uint64_t(threadIdx.x) * GB + g;
+      const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + (b < ix.n_buckets ? b : 0) * BUCKET_WORDS);
+#pragma unroll
+      for (int i = 0; i < SLOTS / 2; ++i) {
+        const ulonglong2 kk = p[i], vv = p[SLOTS / 2 + i];
+        k[g][2 * i] = kk.x;
+        k[g][2 * i + 1] = kk.y;
+        v[g][2 * i] = vv.x;
+        v[g][2 * i + 1] = vv.y;
+      }
+#pragma unroll
+      for (int s = 0; s < SLOTS; ++s)
+        if (b < ix.n_buckets && k[g][s] != KEY_EMPTY && k[g][s] != KEY_TOMB && val_kind(v[g][s]) != HEADER)
+          live |= 1u << (g * SLOTS + s);
     }
+    // exclusive prefix of the live counts over the workgroup
+    const uint32_t c = __popc(live);
+    uint32_t x = c;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (lane == 63) wt[wave] = x;
+    __syncthreads();
+    uint32_t before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < TB / 64; ++w) {
+      before += w < wave ? wt[w] : 0;
+      total += wt[w];
+    }
+    if (threadIdx.x == 0) wg_base = total ? atomicAdd(count, (unsigned long long)total) : 0;
+    __syncthreads();
+    unsigned long long at = wg_base + before + x - c;
+#pragma unroll
+    for (int g = 0; g < GB; ++g)
+#pragma unroll
+      for (int s = 0; s < SLOTS; ++s)
+        if ((live >> (g * SLOTS + s)) & 1) {
+          if (at < cap) {
+            keys[at] = k[g][s];
+            vals[at] = val_plain(v[g][s]);
+          }
+          ++at;
+        }
+    __syncthreads();  // wt and wg_base are reused by the next round
   }
 }
 
-// Rebuild: enter entries [lo, hi) of (keys, vals) into a cleared table.
-__global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const uint64_t *vals, uint64_t lo,
-                                     uint64_t hi, uint64_t *trig, unsigned long long *n_trig, uint64_t *def,
+// Eviction as a selection: the m-th smallest entry under (epoch, key, instance) is found
+// digit by digit -- epoch in two 11-bit digits, the key in five 12-bit digits and a last
+// 4-bit part joined with the instance's top 6 bits, then the instance's low 10 bits --
+// each digit fixed by one histogram pass over the entries that share the digits fixed
+// so far.  Entries up to and including that bin under the lexicographic digit order are
+// evicted; the survivors are compacted and the table rebuilt from them.  Entries are in
+// the dump's value format (instance << 48 | epoch << 24 | session).
+constexpr int SEL_LEVELS = 9;
+constexpr int SEL_BINS = 4096;
+struct SelPrefix {
+  int level;  // digits fixed so far
+  uint32_t digit[SEL_LEVELS];
+};
+__device__ __forceinline__ uint32_t sel_digit(uint64_t key, uint64_t v, int l) {
+  const uint32_t ep = uint32_t(v >> 24) & 0x3FFFFFu, inst = uint32_t(v >> 48);
+  switch (l) {
+    case 0: return ep >> 11;
+    case 1: return ep & 0x7FFu;
+    case 2: return uint32_t(key >> 52);
+    case 3: return uint32_t(key >> 40) & 0xFFFu;
+    case 4: return uint32_t(key >> 28) & 0xFFFu;
+    case 5: return uint32_t(key >> 16) & 0xFFFu;
+    case 6: return uint32_t(key >> 4) & 0xFFFu;
+    case 7: return (uint32_t(key & 15) << 6) | (inst >> 10);
+    default: return inst & 0x3FFu;
+  }
+}
+// -1: below the prefix (evicted), 0: on it, 1: above it
+__device__ __forceinline__ int sel_cmp(uint64_t key, uint64_t v, const SelPrefix &p) {
+  for (int l = 0; l < p.level; ++l) {
+    const uint32_t d = sel_digit(key, v, l);
+    if (d != p.digit[l]) return d < p.digit[l] ? -1 : 1;
+  }
+  return 0;
+}
+// Rebuild: enter the entries of (keys, vals)[0, n) that lie above the cut (the
+// eviction's selection prefix) into a cleared table.  The entries arrive in table order,
+// where neighbours share buckets, so lane l of a wavefront takes a stretch of RS
+// consecutive entries (one 128-byte line of keys and one of values, loaded at once) and
+// places them one after another: the lanes of one step are RS entries apart and rarely
+// race for a bucket, and a lane's writes land in the same few buckets.
+constexpr int RS = 16;
+__global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const uint64_t *vals, uint64_t n,
+                                     SelPrefix cut, uint64_t *trig, unsigned long long *n_trig, uint64_t *def,
                                      unsigned long long *n_def, uint64_t cap) {
-  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  const uint64_t first = lo + uint64_t(blockIdx.x) * blockDim.x + (threadIdx.x & ~63u);
-  for (uint64_t i0 = first; i0 < hi; i0 += stride) {  // whole wavefronts iterate together
-    const uint64_t i = i0 + (threadIdx.x & 63);
-    int64_t tk = -1, df = -1;
-    if (i < hi) {
-      const uint64_t v = vals[i];
-      bool t;
-      const int pl = place_new(ix, keys[i], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), t, true);
-      if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
-      else if (pl == DEFERRED) df = int64_t(i);
-      else if (t) tk = int64_t(i);
+  const int lane = threadIdx.x & 63;
+  const uint64_t wave = (uint64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+  const uint64_t n_waves = (uint64_t(gridDim.x) * blockDim.x) >> 6;
+  for (uint64_t t0 = wave * 64 * RS; t0 < n; t0 += n_waves * 64 * RS) {  // whole wavefronts iterate together
+    const uint64_t base = t0 + uint64_t(lane) * RS;
+    uint64_t k[RS], v[RS];
+    if (base + RS <= n) {
+      const ulonglong2 *pk = reinterpret_cast<const ulonglong2 *>(keys + base);
+      const ulonglong2 *pv = reinterpret_cast<const ulonglong2 *>(vals + base);
+#pragma unroll
+      for (int j = 0; j < RS / 2; ++j) {
+        const ulonglong2 a = pk[j], b = pv[j];
+        k[2 * j] = a.x;
+        k[2 * j + 1] = a.y;
+        v[2 * j] = b.x;
+        v[2 * j + 1] = b.y;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < RS; ++j) {
+        k[j] = base + j < n ? keys[base + j] : 0;
+        v[j] = base + j < n ? vals[base + j] : 0;
+      }
     }
-    append_wave(n_trig, trig, cap, tk);
-    append_wave(n_def, def, cap, df);
+    uint32_t tmask = 0, dmask = 0;  // entries of the stretch that trigger a conversion / are deferred
+#pragma unroll
+    for (int j = 0; j < RS; ++j) {
+      if (base + j < n && sel_cmp(k[j], v[j], cut) > 0) {
+        bool t;
+        const int pl = place_new(ix, k[j], val_inst(v[j]), val_epoch(v[j]), uint32_t(v[j] & 0xFFFFFF), t, true);
+        if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+        else if (pl == DEFERRED) dmask |= 1u << j;
+        else if (t) tmask |= 1u << j;
+      }
+    }
+    // one reservation per wavefront and list for the whole tile (deferred entries are
+    // spread over the table, so a reservation per step made one counter the bottleneck)
+    append_wave_mask(n_trig, trig, cap, tmask, base);
+    append_wave_mask(n_def, def, cap, dmask, base);
   }
 }
 
@@ -918,10 +1052,25 @@ __global__ void set_counts_kernel(IndexHdr *h, unsigned long long n_entries) {
   h->rec_used = 0;
 }
 
+__global__ __launch_bounds__(TB) void sel_hist_kernel(const uint64_t *keys, const uint64_t *vals, uint64_t n,
+                                                      SelPrefix p, unsigned long long *hist) {
+  __shared__ uint32_t h[SEL_BINS];
+  for (int b = threadIdx.x; b < SEL_BINS; b += TB) h[b] = 0;
+  __syncthreads();
+  const uint64_t stride = uint64_t(gridDim.x) * TB;
+  for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += stride) {
+    const uint64_t k = keys[i], v = vals[i];
+    if (sel_cmp(k, v, p) == 0) atomicAdd(&h[sel_digit(k, v, p.level)], 1u);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < SEL_BINS; b += TB)
+    if (h[b]) atomicAdd(&hist[b], (unsigned long long)h[b]);
+}
 struct EvictWs {
-  unsigned long long *count;  // gathered entries, conversion queue, deferred pairs
+  unsigned long long *count;  // gathered entries, conversion queue, deferred pairs, survivors
+  unsigned long long *hist;   // SEL_BINS counts of the eviction's selection passes
   uint64_t *ka, *va, *kb, *vb;  // entries and their sort ping-pong buffers
-  uint64_t *ea, *eb, *ia, *ib;  // epoch sort keys and the permutation they carry
+  uint64_t *ea, *ia;            // eviction's rebuild: conversion queue and deferred pairs
   void *temp;
   size_t temp_bytes;
 };
@@ -942,20 +1091,18 @@ uint64_t evict_ws_layout(uint64_t cap, EvictWs *ws, void *base) {
     off = round_up(off + bytes, 256);
     return o;
   };
-  const uint64_t o_cnt = take(256), o_ka = take(8 * n), o_va = take(8 * n), o_kb = take(8 * n),
-                 o_vb = take(8 * n), o_ea = take(8 * n), o_eb = take(8 * n), o_ia = take(8 * n),
-                 o_ib = take(8 * n), o_tmp = take(tb);
+  const uint64_t o_cnt = take(256), o_hist = take(8 * SEL_BINS), o_ka = take(8 * n), o_va = take(8 * n), o_kb = take(8 * n),
+                 o_vb = take(8 * n), o_ea = take(8 * n), o_ia = take(8 * n), o_tmp = take(tb);
   if (ws) {
     char *b = static_cast<char *>(base);
     ws->count = reinterpret_cast<unsigned long long *>(b + o_cnt);
+    ws->hist = reinterpret_cast<unsigned long long *>(b + o_hist);
     ws->ka = reinterpret_cast<uint64_t *>(b + o_ka);
     ws->va = reinterpret_cast<uint64_t *>(b + o_va);
     ws->kb = reinterpret_cast<uint64_t *>(b + o_kb);
     ws->vb = reinterpret_cast<uint64_t *>(b + o_vb);
     ws->ea = reinterpret_cast<uint64_t *>(b + o_ea);
-    ws->eb = reinterpret_cast<uint64_t *>(b + o_eb);
     ws->ia = reinterpret_cast<uint64_t *>(b + o_ia);
-    ws->ib = reinterpret_cast<uint64_t *>(b + o_ib);
     ws->temp = b + o_tmp;
     ws->temp_bytes = tb;
   }
@@ -967,32 +1114,13 @@ int read_hdr(const smetric_index *idx, IndexHdr *out, hipStream_t s) {
   return hip_rc(hipStreamSynchronize(s));
 }
 
-__global__ void epoch_keys_kernel(const uint64_t *vals, uint64_t *ep, uint64_t *idx, uint64_t n) {
-  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
-    ep[i] = val_epoch(vals[i]);
-    idx[i] = i;
-  }
-}
-
-__global__ void permute_kernel(const uint64_t *keys, const uint64_t *vals, const uint64_t *idx, uint64_t *keys_out,
-                               uint64_t *vals_out, uint64_t n) {
-  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
-    const uint64_t j = idx[i];
-    keys_out[i] = keys[j];
-    vals_out[i] = vals[j];
-  }
-}
-
-// Gather all entries and sort them by (key, instance), or by (epoch, key, instance) when
-// by_epoch.  Stable LSD radix passes, each over the full 64-bit sort word (restricting a
-// pass to a bit range gave wrong orders for some inputs with the installed rocPRIM):
+// Gather all entries and sort them by (key, instance) for the dump.  Stable LSD radix
+// passes, each over the full 64-bit sort word (restricting a pass to a bit range gave
+// wrong orders for some inputs with the installed rocPRIM):
 //   1) by the value word (instance << 48 | epoch << 24 | session);
-//   2) stably by key -- (key, instance) is unique, so this is (key, instance) order;
-//   3) (by_epoch) stably by epoch, carrying the permutation, then a gather.
+//   2) stably by key -- (key, instance) is unique, so this is (key, instance) order.
 // On return the sorted keys/values are in (*keys_out, *vals_out).
-int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, bool by_epoch, uint64_t **keys_out,
+int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, uint64_t **keys_out,
                   uint64_t **vals_out, hipStream_t s) {
   const DevIndex ix = dev_view(idx);
   int rc = fill(ws.count, 256, 0, s);
@@ -1015,16 +1143,7 @@ int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, bool 
   if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, k2, v2, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
   *keys_out = k2.Current();
   *vals_out = v2.Current();
-  if (!by_epoch) return SMETRIC_OK;
-  hipLaunchKernelGGL(epoch_keys_kernel, dim3(grid_for(n)), dim3(TB), 0, s, v2.Current(), ws.ea, ws.ia, n);
-  hipcub::DoubleBuffer<uint64_t> e(ws.ea, ws.eb), x(ws.ia, ws.ib);
-  tb = ws.temp_bytes;
-  if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, e, x, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
-  hipLaunchKernelGGL(permute_kernel, dim3(grid_for(n)), dim3(TB), 0, s, k2.Current(), v2.Current(), x.Current(),
-                     k2.Alternate(), v2.Alternate(), n);
-  *keys_out = k2.Alternate();
-  *vals_out = v2.Alternate();
-  return hip_rc(hipGetLastError());
+  return SMETRIC_OK;
 }
 
 }  // namespace
@@ -1125,23 +1244,53 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   const uint64_t n = h.n_entries;
   const uint64_t m = uint64_t((static_cast<unsigned __int128>(n) * frac_num + frac_den - 1) / frac_den);
   if (m == 0) return SMETRIC_OK;
-  uint64_t *keys, *vals;
-  if ((rc = gather_sorted(idx, ws, n, true, &keys, &vals, stream))) return rc;
-  // rebuild from the survivors [m, n)
+  // all entries, unordered
+  if ((rc = fill(ws.count, 256, 0, stream))) return rc;
   const DevIndex ix = dev_view(idx);
+  hipLaunchKernelGGL(gather_kernel, dim3(grid_for(ix.n_buckets * SLOTS)), dim3(TB), 0, stream, ix, ws.ka, ws.va,
+                     ws.count, n);
+  unsigned long long got = 0;
+  if (hipMemcpyAsync(&got, ws.count, 8, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return SMETRIC_EHIP;
+  if (got != n) return SMETRIC_EINTERNAL;
+  // select the m-th smallest, one digit per pass; stop once its whole bin is evicted
+  SelPrefix p{};
+  uint64_t rem = m;  // rank of the m-th smallest among the entries on the prefix (1-based)
+  unsigned long long hh[SEL_BINS];
+  for (int l = 0; l < SEL_LEVELS; ++l) {
+    p.level = l;
+    if ((rc = fill(ws.hist, 8 * SEL_BINS, 0, stream))) return rc;
+    hipLaunchKernelGGL(sel_hist_kernel, dim3(grid_for(n) < 1024 ? grid_for(n) : 1024), dim3(TB), 0, stream, ws.ka,
+                       ws.va, n, p, ws.hist);
+    if (hipMemcpyAsync(hh, ws.hist, 8 * SEL_BINS, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+      return SMETRIC_EHIP;
+    uint64_t below = 0;
+    int b = 0;
+    while (b < SEL_BINS && below + hh[b] < rem) below += hh[b++];
+    if (b == SEL_BINS) return SMETRIC_EINTERNAL;
+    p.digit[l] = uint32_t(b);
+    p.level = l + 1;
+    rem -= below;
+    if (rem == hh[b]) break;  // the whole bin goes: the prefix itself is the cut
+    if (l + 1 == SEL_LEVELS) return SMETRIC_EINTERNAL;  // the full tuple is unique
+  }
+  // rebuild from the survivors: the entries above the cut, exactly n - m of them
+  uint64_t *keys = ws.ka, *vals = ws.va;
   if ((rc = fill(ix.slots, ix.n_buckets * BUCKET_WORDS * 8, 0, stream))) return rc;
   if ((rc = fill(ix.pool, ix.n_records * uint64_t(ix.words) * 8, 0, stream))) return rc;
   hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m));
-  // the alternate sort buffers are free now: one holds the conversion queue
-  uint64_t *trig = ws.ea;  // free once the sorted entries are in place
+  uint64_t *trig = ws.ea;  // free buffers: the conversion queue and the deferred pairs
   unsigned long long *n_trig = ws.count + 1;
-  uint64_t *def = ws.ia;  // free as well
+  uint64_t *def = ws.ia;
   unsigned long long *n_def = ws.count + 2;
-  hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n - m)), dim3(TB), 0, stream, ix, keys, vals, m, n, trig,
+  hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n / RS)), dim3(TB), 0, stream, ix, keys, vals, n, p, trig,
                      n_trig, def, n_def, idx->capacity);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr, nullptr,
                      nullptr);
-  hipLaunchKernelGGL(deferred_kernel, dim3(64), dim3(TB), 0, stream, ix, def, n_def, nullptr, nullptr, nullptr,
+  // every member of a key with a bitmap record is deferred here (millions): the full grid
+  hipLaunchKernelGGL(deferred_kernel, dim3(MAX_GRID), dim3(TB), 0, stream, ix, def, n_def, nullptr, nullptr, nullptr,
                      nullptr, 0u, keys, vals, nullptr);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   return hip_rc(hipStreamSynchronize(stream));
@@ -1162,7 +1311,7 @@ extern "C" int smetric_index_dump(const smetric_index *idx, uint64_t *keys_out, 
   *n_out = n;
   if (n == 0) return SMETRIC_OK;
   uint64_t *keys, *vals;
-  if ((rc = gather_sorted(idx, ws, n, false, &keys, &vals, stream))) return rc;
+  if ((rc = gather_sorted(idx, ws, n, &keys, &vals, stream))) return rc;
   const uint64_t c = n < cap ? n : cap;
   if (c) {
     if (hipMemcpyAsync(keys_out, keys, 8 * c, hipMemcpyDeviceToDevice, stream) != hipSuccess ||
