@@ -149,6 +149,12 @@ __device__ __forceinline__ uint64_t rdl64(uint64_t v, int src) {
   return (uint64_t(hi) << 32) | lo;
 }
 
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+  const uint32_t lo = uint32_t(__shfl(int(uint32_t(v)), src, 64));
+  const uint32_t hi = uint32_t(__shfl(int(uint32_t(v >> 32)), src, 64));
+  return (uint64_t(hi) << 32) | lo;
+}
+
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
@@ -224,9 +230,16 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
   enum { M_ALL, M_NARROW, M_WIDE, M_DONE };
   int mode = M_ALL;
   int my_inst = -1;   // NARROW: this lane's alive instance
-  uint64_t A[WPL];    // WIDE: alive words lane + 64 t
+  uint64_t A[WPL];    // WIDE: alive words lane + 64 t (WPL = 1: word wl, in every lane group)
 #pragma unroll
   for (int t = 0; t < WPL; ++t) A[t] = 0;
+  // WPL = 1 (at most 4,096 instances): the wavefront is cut into groups of lpb lanes (the
+  // least power of two >= the bitmap's words); lane (sub, wl) handles word wl of the
+  // group's block, so one load instruction fetches the words of bpl = 64 / lpb blocks
+  // (4 at 1,024 instances) and every lane group keeps a copy of the alive words.
+  const int words = ix.words;
+  const int lpb = WPL > 1 ? 64 : (words <= 1 ? 1 : 1 << (32 - __builtin_clz(uint32_t(words - 1))));
+  const int bpl = 64 / lpb, sub = lane / lpb, wl = lane % lpb;
 
   // DESC: descriptors are fetched PF chunks at a time -- positions, then all PF gathers
   // at once -- since a chunk's own work rarely touches memory and the walk is otherwise
@@ -253,9 +266,12 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
 #pragma unroll
     for (int k = 0; k + 1 < PF; ++k) dq[k] = dq[k + 1];
     --left;
+    // DESC, NARROW, and every descriptor of the chunk NONE or ONE (a session's private
+    // blocks, the common case): "held by a" is read off the descriptor, nothing decoded
+    const bool simple = DESC && mode == M_NARROW && !__ballot(valid && desc_kind(d_cur) >= D_MANY);
     Holders H;
     uint64_t key = 0;
-    if (valid) {
+    if (valid && !simple) {
       if (DESC) {
         const uint64_t d = d_cur;
         if (desc_kind(d) == D_MANY) key = keys[b0 + j];
@@ -287,14 +303,97 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
         uint32_t hl0[LIST_MAX];
 #pragma unroll
         for (int i = 0; i < LIST_MAX; ++i) hl0[i] = 0xFFFFFFFFu;
+        if constexpr (WPL == 1) {
+          A[0] = holder_word(ix, kind0, rec0, hl0, key0, wl);
+        } else {
 #pragma unroll
-        for (int t = 0; t < WPL; ++t) A[t] = holder_word(ix, kind0, rec0, hl0, key0, lane + 64 * t);
+          for (int t = 0; t < WPL; ++t) A[t] = holder_word(ix, kind0, rec0, hl0, key0, lane + 64 * t);
+        }
         mode = M_WIDE;
       }
       jj = 1;
     }
 
-    if (mode == M_WIDE) {
+    if (WPL == 1 && mode == M_WIDE) {
+      // groups of GQ loads (GQ x bpl blocks, one round trip); the words of each block are
+      // then ANDed in block order, each fetched from its lane group with a shuffle
+      constexpr int GQ = 8;
+      while (jj < 64 && mode == M_WIDE) {
+        uint64_t hq[GQ];
+        uint32_t kq[GQ];
+#pragma unroll
+        for (int q = 0; q < GQ; ++q) {
+          const int b = jj + q * bpl + sub;
+          const int src = b < 64 ? b : 63;
+          const uint32_t kd = uint32_t(__shfl(int(H.kind), src, 64));
+          const uint64_t rc = shfl64(H.rec, src);
+          kq[q] = (b < 64 && j0 + b < nb) ? kd : uint32_t(H_NONE);
+          // no branch around the load: a non-HOT block reads record 0 (always present)
+          hq[q] = ix.pool[(kq[q] == H_HOT ? rc : 0) * uint64_t(words) + uint64_t(wl < words ? wl : 0)];
+        }
+#pragma unroll
+        for (int q = 0; q < GQ; ++q) {
+          if (kq[q] != H_HOT || wl >= words) hq[q] = 0;
+          if (__ballot(kq[q] == H_LIST || kq[q] == H_LONG)) {  // rare: plain holders
+            const int b = jj + q * bpl + sub;
+            const int src = b < 64 ? b : 63;
+            uint32_t hl[LIST_MAX];
+#pragma unroll
+            for (int i = 0; i < LIST_MAX; ++i) hl[i] = uint32_t(__shfl(int(H.h[i]), src, 64));
+            const uint64_t k = shfl64(key, src);
+            if (kq[q] == H_LIST || kq[q] == H_LONG) hq[q] = holder_word(ix, kq[q], 0, hl, k, wl);
+          }
+        }
+        const int nblk = GQ * bpl < 64 - jj ? GQ * bpl : 64 - jj;
+#pragma unroll
+        for (int q = 0; q < GQ; ++q) {
+          for (int s2 = 0; s2 < bpl; ++s2) {
+            const int t = q * bpl + s2;
+            if (t >= nblk) break;
+            const uint64_t x = shfl64(hq[q], s2 * lpb + wl);
+            const uint64_t n = A[0] & x;
+            uint64_t d = A[0] & ~n;
+            A[0] = n;
+            const int64_t jb = j0 + jj + t;
+            if (sub == 0) {
+              while (d) {  // blocks past the end count as misses: survivors get nb
+                const int bit = __builtin_ctzll(d);
+                d &= d - 1;
+                row[wl * 64 + bit] = int32_t(jb < nb ? jb : nb);
+              }
+            }
+          }
+        }
+        jj += nblk;
+        const uint32_t cnt = sub == 0 ? uint32_t(__popcll(A[0])) : 0u;
+        const uint32_t n_alive = wave_sum(cnt);
+        if (n_alive == 0) {
+          mode = M_DONE;
+        } else if (n_alive <= 64) {
+          // hand the survivors to lanes: exclusive prefix of the lead group's counts
+          uint32_t pre = cnt;
+#pragma unroll
+          for (int d = 1; d < 64; d <<= 1) {
+            const uint32_t t = __shfl_up(pre, d, 64);
+            if (lane >= d) pre += t;
+          }
+          pre -= cnt;
+          uint64_t a = sub == 0 ? A[0] : 0;
+          while (a) {
+            const int bit = __builtin_ctzll(a);
+            a &= a - 1;
+            nlist[wave][pre++] = wl * 64 + bit;
+          }
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+          my_inst = lane < int(n_alive) ? nlist[wave][lane] : -1;
+          __builtin_amdgcn_wave_barrier();
+          mode = M_NARROW;
+        }
+      }
+    }
+
+    if (WPL > 1 && mode == M_WIDE) {
       // block by block, G blocks' holder words fetched ahead of the AND chain
       constexpr int G = WPL >= 8 ? 1 : 8 / WPL;
       while (jj < 64 && mode == M_WIDE) {
@@ -386,11 +485,13 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
     if (mode == M_NARROW && jj < 64) {
       // every alive instance: first block of the chunk (at or after jj) it does not hold
       uint64_t alive = __ballot(my_inst >= 0);
+      // simple chunks: the lane's single holder, or none (-1)
+      const int32_t one = (valid && desc_kind(d_cur) == D_ONE) ? int32_t(desc_inst(d_cur)) : -1;
       while (alive) {
         const int t = __builtin_ctzll(alive);
         alive &= alive - 1;
         const uint32_t a = __builtin_amdgcn_readlane(uint32_t(my_inst), t);
-        const bool held = lane < jj || (valid && holds(ix, H, key, a));
+        const bool held = lane < jj || (simple ? one == int32_t(a) : (valid && holds(ix, H, key, a)));
         const uint64_t miss = __ballot(!held);
         if (miss) {
           const int f = __builtin_ctzll(miss);
@@ -409,8 +510,8 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
   } else if (mode == M_WIDE) {
 #pragma unroll
     for (int t = 0; t < WPL; ++t) {
-      uint64_t a = A[t];
-      const int w = lane + 64 * t;
+      uint64_t a = (WPL > 1 || sub == 0) ? A[t] : 0;  // WPL = 1: the lead lane group's copy
+      const int w = WPL > 1 ? lane + 64 * t : wl;
       while (a) {
         const int bit = __builtin_ctzll(a);
         a &= a - 1;

@@ -163,6 +163,37 @@ def test_many_instances_wide_words():
     pair.step(batch, what="I=5000 probed", probed=True)
 
 
+@pytest.mark.parametrize("I", [130, 300, 1000, 4000])
+def test_wide_mode_bitmap_widths(I):
+    """Bitmap rows of 3, 5, 16 and 63 words (lane groups of 4, 8, 16 and 64 lanes, the odd
+    widths with padding lanes): a prefix held by most instances to different depths, so the
+    alive set shrinks block by block through the wide mode and hands over to the narrow
+    one; many requests, each probing the prefix to its own length."""
+    rng = np.random.default_rng(I)
+    pre = rng.integers(0, W.VOCAB, 4096, dtype=np.int32)
+    pair = Pair(3_000_000, I)
+    n_hold = int(0.8 * I)
+    prompts = [np.concatenate([pre[: rng.integers(64, 4096)], rng.integers(0, W.VOCAB, rng.integers(0, 600), dtype=np.int32)])
+               for _ in range(n_hold)]
+    off = np.zeros(n_hold + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(np.concatenate(prompts), off)
+    inst = rng.choice(I, n_hold, replace=False).astype(np.int32)
+    assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, inst, np.arange(n_hold), 1) == 0
+    R = 48
+    qs = [np.concatenate([pre[: rng.integers(16, 4096)], rng.integers(0, W.VOCAB, rng.integers(0, 2000), dtype=np.int32)])
+          for _ in range(R)]
+    toff = np.zeros(R + 1, np.int64)
+    toff[1:] = np.cumsum([len(x) for x in qs])
+    batch = W.Batch(tokens=np.concatenate(qs), tok_off=toff, prompt_len=np.diff(toff).astype(np.int32),
+                    hist_len=rng.integers(0, 4096, R).astype(np.int32), turn=rng.integers(0, 3, R).astype(np.int32),
+                    session=np.arange(R, dtype=np.uint32) + 5000, q=rng.integers(0, 50, I) * W.Q_UNIT_NS,
+                    rr_base=3, epoch=2)
+    say(f"I={I}: {n_hold} holders, {nb} blocks inserted")
+    pair.step(batch, what=f"I={I}", check_dump=False)
+    pair.step(batch, what=f"I={I} probed", probed=True)
+
+
 def test_max_instances():
     rng = np.random.default_rng(6)
     I = 65536
