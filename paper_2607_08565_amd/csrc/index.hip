@@ -936,7 +936,7 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
 // 4-bit part joined with the instance's top 6 bits, then the instance's low 10 bits --
 // each digit fixed by one histogram pass over the entries that share the digits fixed
 // so far.  Entries up to and including that bin under the lexicographic digit order are
-// evicted; the survivors are compacted and the table rebuilt from them.  Entries are in
+// evicted, and the table is rebuilt from the entries above it.  Entries are in
 // the dump's value format (instance << 48 | epoch << 24 | session).
 constexpr int SEL_LEVELS = 9;
 constexpr int SEL_BINS = 4096;
