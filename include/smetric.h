@@ -328,7 +328,7 @@ int smetric_sessions(const uint64_t *keys, const int64_t *blk_off, int32_t n_req
  * session_cached, the prefill cost on prev, the deadline); then one wavefront walks the
  * batch with the running loads kept doubled in 128 bits (exact).
  *   q_out      int64[n_instances] (out, optional: NULL) final loads in ns, rounded down
- *   workspace  >= smetric_route_seq_ws_bytes(n_req) bytes (64 per request), 256-B aligned
+ *   workspace  >= smetric_route_seq_ws_bytes(n_req) bytes (80 per request), 256-B aligned
  * Other arguments, domains, branches and errors as smetric_route, and n_instances must be
  * <= 4096 (EINVAL otherwise); EWORKSPACE for a short workspace.  Out-of-domain requests
  * (branch 255) add no load.

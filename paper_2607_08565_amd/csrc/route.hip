@@ -243,8 +243,10 @@ __global__ __launch_bounds__(64 * RW) void route_coloc_kernel(
 
 // ---------------------------------------------------------------------------------
 // Online load update (Sec. 4.2 (a): q is what is queued when each request is routed).
-//   prep  one wavefront per request, in parallel: what does not depend on the loads --
-//         domain check, prev = argmax c, c[prev], session_cached -- into a 16-byte record.
+//   prep  one wavefront per request, in parallel: what does not depend on the running
+//         loads -- domain check, prev = argmax c, session_cached, the costs on prev and at
+//         the best other hit, the deadline, and the smallest other est2 on the starting
+//         loads -- into an 80-byte record.
 //   seq   ONE wavefront routes the batch in index order; the running loads 2q[i] live in
 //         LDS as 128-bit integers, together with their minimum.  Per request:
 //           * cached follow-up whose prev meets its deadline: stick (no scan);
@@ -266,12 +268,16 @@ struct SeqRec {
   i128 cost_rest;  // 2 x prefill_cost at the largest hit of any other instance: a lower
                    // bound of every other instance's cost (Eq. (1) falls as the hit grows)
   i128 bound;      // SLACK_num x 2 (b + a L): i meets its deadline iff est2(i) SLACK_den <= bound
+  i128 m0;         // min over i != prev of est2(i) on the loads the batch starts with: a lower
+                   // bound of every other instance's est2 at any later point (loads only grow)
 };
+constexpr int64_t SEQ_NO_OTHER = int64_t(1) << 60;  // m0 with no other instance (x 2^30: never meets)
 
 __global__ __launch_bounds__(64 * RW) void route_seq_prep_kernel(const int32_t *__restrict__ matched, int32_t n_req,
                                                                  int32_t I, const int32_t *__restrict__ prompt_len,
                                                                  const int32_t *__restrict__ hist_len,
-                                                                 const int32_t *__restrict__ turn, RouteParams p,
+                                                                 const int32_t *__restrict__ turn,
+                                                                 const int64_t *__restrict__ q, RouteParams p,
                                                                  SeqRec *__restrict__ rec) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * RW + wave;
@@ -308,6 +314,21 @@ __global__ __launch_bounds__(64 * RW) void route_seq_prep_kernel(const int32_t *
     const int32_t o = __shfl_xor(c2, m, 64);
     c2 = o > c2 ? o : c2;
   }
+  // the smallest est2 of any other instance on the starting loads (the row is in range
+  // whenever ok; a load outside [0, 2^62) makes the whole batch invalid later)
+  i128 m0 = i128(SEQ_NO_OTHER) << 30;
+  if (ok)
+    for (int32_t i = lane; i < I; i += 64)
+      if (i != bi) {
+        const int64_t qi = q[i];
+        const i128 e = est2(p, L, c[i], qi < 0 || qi >= (int64_t(1) << 62) ? 0 : qi);
+        m0 = e < m0 ? e : m0;
+      }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const i128 o = shfl_xor128(m0, m);
+    m0 = o < m0 ? o : m0;
+  }
   if (lane != 0) return;
   const bool cached = ok && i128(p.B) * bc * p.hit_den > i128(p.hit_num) * hist;
   SeqRec out;
@@ -319,6 +340,7 @@ __global__ __launch_bounds__(64 * RW) void route_seq_prep_kernel(const int32_t *
   // one instance: nothing else to bound, any value will do
   out.cost_rest = ok ? est2(p, L, c2 < 0 ? bc : c2, 0) : i128(0);
   out.bound = i128(p.slack_num) * (i128(2) * (i128(p.slo_b) + i128(p.slo_a) * (ok ? L : 0)));
+  out.m0 = m0;
   rec[r] = out;
 }
 
@@ -363,6 +385,17 @@ __device__ __forceinline__ i128 seq_qmin(const i128 *q2, int32_t I) {
 
 __device__ __forceinline__ int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// readlane returns int: each word goes through uint32_t, or a set bit 31 of a low word
+// would sign-extend into the word above it
+__device__ __forceinline__ i128 readlane128(i128 v, int l) {
+  const uint64_t lo = uint64_t(v), hi = uint64_t(v >> 64);
+  const uint32_t w0 = uint32_t(__builtin_amdgcn_readlane(uint32_t(lo), l));
+  const uint32_t w1 = uint32_t(__builtin_amdgcn_readlane(uint32_t(lo >> 32), l));
+  const uint32_t w2 = uint32_t(__builtin_amdgcn_readlane(uint32_t(hi), l));
+  const uint32_t w3 = uint32_t(__builtin_amdgcn_readlane(uint32_t(hi >> 32), l));
+  return (i128((uint64_t(w3) << 32) | w2) << 64) | i128((uint64_t(w1) << 32) | w0);
+}
+
 // Decide request r.  Every branch below is on wavefront-uniform values (read with
 // readfirstlane), and every lane performs the identical stores, so the code has no divergent
 // regions: the compiler can then wait for exactly the prefetched loads it uses.
@@ -389,9 +422,10 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
     t = prev;
     br = SMETRIC_STICK;
     cost_t = cost_prev;
-  } else if (follow_up && cached && !slack_inf && (qmin + row.rec.cost_rest) * p.slack_den > bound) {
+  } else if (follow_up && cached && !slack_inf &&
+             ((qmin + row.rec.cost_rest) * p.slack_den > bound || row.rec.m0 * p.slack_den > bound)) {
     // prev misses its deadline, and every other instance i has est2(i) >= min(2q) +
-    // cost_rest: nobody can meet it
+    // cost_rest and est2(i) >= m0: nobody can meet it
     t = prev;
     br = SMETRIC_LAST_RESORT;
     cost_t = cost_prev;
@@ -451,6 +485,38 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
   if (old == qmin && cost_t != 0) qmin = seq_qmin(q2, I);
 }
 
+// Requests [rs, re) one at a time, rows and records prefetched D requests ahead.
+template <int K, int D>
+__device__ __forceinline__ void seq_exact_block(const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
+                                                const RouteParams &p, uint64_t rr_base, bool q_ok,
+                                                const SeqRec *__restrict__ recs, i128 *q2, i128 &qmin,
+                                                int32_t *__restrict__ target, uint8_t *__restrict__ branch,
+                                                int32_t rs, int32_t re) {
+  SeqRow<K> ring[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) seq_load<K>(matched, I, rs + d, n_req, recs, ring[d]);
+  for (int32_t r0 = rs; r0 < re; r0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int32_t r = r0 + d;
+      if (r < re) {
+        seq_decide<K>(ring[d], matched, r, I, p, rr_base, q_ok, q2, qmin, target, branch);
+        seq_load<K>(matched, I, r + D, n_req, recs, ring[d]);
+      }
+    }
+  }
+}
+
+// The batch in blocks of 64 requests, one per lane.  A cached follow-up puts its prefill on
+// prev whether it sticks or takes the last resort, so -- if every earlier request of the
+// block is decided that way -- request l's load on prev is exactly q2[prev] plus the costs
+// of the earlier requests with the same prev.  With that load, "prev meets its deadline"
+// (stick) is exact, and "min(2q) + cost_rest misses it" (last resort) is exact with any
+// lower bound of min(2q), which only grows; out-of-domain requests change nothing.  The
+// requests before the first one not settled this way are decided together, that one
+// alone with the sequential rule, and the next block starts after it.  After two blocks in
+// a row that settle nothing (e.g. first turns, which always need a scan), the next 64
+// requests go through the sequential rule with prefetching.
 template <int K, int D>
 __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict__ matched, int32_t n_req,
                                                        int32_t I, const int64_t *__restrict__ q, RouteParams p,
@@ -458,27 +524,100 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
                                                        int32_t *__restrict__ target, uint8_t *__restrict__ branch,
                                                        int64_t *__restrict__ q_out) {
   __shared__ i128 q2[SEQ_MAX_I];
+  __shared__ uint32_t n_on[SEQ_MAX_I];  // block requests per prev (0 between blocks)
   const int lane = threadIdx.x;
   bool q_ok = true;
   for (int32_t i = lane; i < I; i += 64) {
     const int64_t qi = q[i];
     if (qi < 0 || qi >= (int64_t(1) << 62)) q_ok = false;
     q2[i] = i128(2) * qi;
+    n_on[i] = 0;
   }
   q_ok = __ballot(!q_ok) == 0;
   __syncthreads();
-  i128 qmin = seq_qmin(q2, I);
-  SeqRow<K> ring[D];
-#pragma unroll
-  for (int d = 0; d < D; ++d) seq_load<K>(matched, I, d, n_req, recs, ring[d]);
-  for (int32_t r0 = 0; r0 < n_req; r0 += D) {
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int32_t r = r0 + d;
-      if (r < n_req) {
-        seq_decide<K>(ring[d], matched, r, I, p, rr_base, q_ok, q2, qmin, target, branch);
-        seq_load<K>(matched, I, r + D, n_req, recs, ring[d]);
+  i128 qmin = seq_qmin(q2, I);  // a lower bound of min(2q) from here on (loads only grow)
+  const bool slack_inf = p.slack_den == 0;
+  int32_t r0 = 0;
+  int streak = 0;
+  while (r0 < n_req) {
+    if (streak >= 2) {
+      const int32_t re = n_req - r0 < 64 ? n_req : r0 + 64;
+      seq_exact_block<K, D>(matched, n_req, I, p, rr_base, q_ok, recs, q2, qmin, target, branch, r0, re);
+      r0 = re;
+      streak = 0;
+      continue;
+    }
+    const int32_t nv = n_req - r0 < 64 ? n_req - r0 : 64;
+    const int32_t r = r0 + lane;
+    int32_t rv = r < n_req ? r : n_req - 1;
+    asm volatile("" : "+v"(rv));  // a vector load: see seq_load
+    const SeqRec rec = recs[rv];
+    const bool in = lane < nv;
+    const bool ok = q_ok && (rec.flags & 1);
+    const bool sticky = ok && (rec.flags & 2) && (rec.flags & 4);  // cached follow-up: its prefill goes to prev
+    const int32_t prev = rec.prev;
+    const bool mine = in && sticky;
+    if (mine) atomicAdd(&n_on[prev], 1u);
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    // requests sharing a prev within the block form a group (lanes in index order): each
+    // adds the costs of the group's earlier requests to its load on prev
+    uint64_t todo = __ballot(mine && n_on[prev] > 1);
+    __builtin_amdgcn_wave_barrier();
+    if (mine) n_on[prev] = 0;
+    i128 excl = 0;
+    uint64_t group = 0;  // lanes with my prev (0: nobody else has it)
+    while (todo) {
+      const int32_t p0 = __builtin_amdgcn_readlane(prev, __builtin_ctzll(todo));
+      const uint64_t m = __ballot(mine && prev == p0);
+      todo &= ~m;
+      i128 run = 0;
+      for (uint64_t mm = m; mm; mm &= mm - 1) {
+        const int l = __builtin_ctzll(mm);
+        if (lane == l) {
+          excl = run;
+          group = m;
+        }
+        run += readlane128(rec.cost_prev, l);
       }
+    }
+    const i128 q_pre = mine ? q2[prev] : i128(0);
+    const i128 q_prev = q_pre + excl;
+    bool settled = !ok;  // out of domain: settled, nothing queued
+    uint8_t br = SMETRIC_INVALID;
+    if (sticky) {
+      if (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound) {
+        settled = true;
+        br = SMETRIC_STICK;
+      } else if ((qmin + rec.cost_rest) * p.slack_den > rec.bound || rec.m0 * p.slack_den > rec.bound) {
+        settled = true;
+        br = SMETRIC_LAST_RESORT;
+      }
+    }
+    const uint64_t open = __ballot(in && !settled);
+    const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
+    // the first request not settled needs its row: requested now, used below
+    SeqRow<K> row;
+    if (f < nv) seq_load<K>(matched, I, r0 + f, n_req, recs, row);
+    if (lane < f) {
+      target[r] = ok ? prev : -1;
+      branch[r] = br;
+    }
+    // prev's new load, written by the last of the decided requests with that prev
+    const uint64_t decided = f >= 64 ? ~uint64_t(0) : (uint64_t(1) << f) - 1;
+    const uint64_t after_me = lane == 63 ? uint64_t(0) : ~((uint64_t(2) << lane) - 1);
+    const bool last = mine && lane < f && (group & after_me & decided) == 0;
+    __builtin_amdgcn_wave_barrier();
+    if (last) q2[prev] = q_prev + rec.cost_prev;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    // the minimum can only have moved if an instance at the minimum took load
+    if (__ballot(mine && lane < f && q_pre == qmin)) qmin = seq_qmin(q2, I);
+    r0 += f;
+    if (f < nv) {  // the first request not settled: the sequential rule
+      seq_decide<K>(row, matched, r0, I, p, rr_base, q_ok, q2, qmin, target, branch);
+      r0 += 1;
+      streak = f == 0 ? streak + 1 : 0;
     }
   }
   __syncthreads();
@@ -575,7 +714,7 @@ extern "C" int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t 
   SeqRec *recs = static_cast<SeqRec *>(workspace);
   if (n_req > 0)
     hipLaunchKernelGGL(route_seq_prep_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
-                       n_instances, prompt_len, hist_len, turn, rp, recs);
+                       n_instances, prompt_len, hist_len, turn, q, rp, recs);
   const int kk = (n_instances + 63) / 64;
 #define SEQ_LAUNCH(K, D)                                                                                       \
   hipLaunchKernelGGL((route_seq_kernel<K, D>), dim3(1), dim3(64), 0, stream, matched, n_req, n_instances,         \

@@ -151,6 +151,35 @@ def test_seq_random_parity(I):
         assert 4 in seen
 
 
+@pytest.mark.parametrize("I", [2, 4, 37])
+def test_seq_blocks_of_cached_follow_ups(I):
+    """Cached follow-ups only, on few instances: most requests of every 64-request block
+    share a prev, and the queues cross deadlines inside blocks, so the block-wise decisions
+    (loads accumulated over earlier requests with the same prev) meet the sequential rule's
+    sticks, last resorts and migrations; a sprinkle of first turns and out-of-domain rows."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(300 + I)
+    R = 5000
+    L = rng.integers(1024, 8192, R).astype(np.int32)
+    prev = rng.integers(0, I, R)
+    m = (rng.integers(0, 30, (R, I)) * (L // 16)[:, None] // 100).astype(np.int32)
+    m[np.arange(R), prev] = (L // 16) * rng.integers(60, 100, R) // 100
+    hist = (L * 6 // 10).astype(np.int32)  # c[prev] * 16 > hist / 2: cached
+    turn = np.ones(R, np.int32)
+    turn[rng.random(R) < 0.01] = 0
+    m[rng.random(R) < 0.005, 0] = 1 << 20  # out of domain (c > L / B)
+    q = rng.integers(0, 40, I).astype(np.int64) * W.Q_UNIT_NS
+    seen = set()
+    # the last two make per-request costs exceed 2^32 ns (words with bit 31 set cross lanes)
+    for over in ({}, dict(slack_num=1, slack_den=2), dict(slack_num=4, slack_den=1), dict(c_lin=20_000),
+                 dict(c_lin=4_000_000, slo_b=2**32), dict(c_lin=4_000_000, c_att=3_000, slo_b=2**32, slo_a=2**32)):
+        p = dict(W.DEFAULT_PARAMS, **over)
+        _, ob = _seq_both(S, m, L, hist, turn, q, p, 12345)
+        seen |= set(ob.tolist())
+    say(f"  I={I}: branches seen {sorted(seen)}")
+    assert {0, 2, 3, 255} <= seen
+
+
 def test_seq_extremes_invalid_and_limits():
     from paper_2607_08565_amd import smetric as S
     rng = np.random.default_rng(8)
