@@ -244,9 +244,10 @@ CALL_KERNELS = {
               "probe_kernel"],
     "match": ["match_kernel<1, true>"],
     "route": ["route_kernel<0>"],
-    "insert": ["fill_kernel", "insp_classify_kernel", "insp_size_kernel", "kt_clear_kernel", "insp_keyclaim_kernel",
-               "insp_size2_kernel", "dd_clear_kernel", "insp_dedupe_kernel", "insp_check_kernel", "insp_refresh_kernel",
-               "insp_place_kernel", "spill_kernel", "deferred_kernel"],
+    "insert": ["fill_kernel", "insp_valid_kernel", "insp_classify_kernel", "insp_size_kernel", "insp_bcount_kernel",
+               "insp_bscan_kernel", "insp_size2_kernel", "dd_clear_kernel", "insp_bscatter_kernel",
+               "insp_bdedupe_kernel", "insp_check_kernel", "insp_refresh_kernel", "insp_place_kernel", "spill_kernel",
+               "deferred_kernel"],
 }
 
 

@@ -154,7 +154,7 @@ inline uint64_t flat_segment(uint64_t n) { return (n + flat_span() - 1) / flat_s
 // Probe state shared by smetric_probe and the calls that consume it.
 struct ProbeHdr {
   int err;                          // first input error (EINVAL) found while partitioning
-  int pad0;
+  int bad_key;                      // nonzero if a key is one of the two reserved values
   unsigned long long n;             // number of blocks probed (0 when invalid)
   unsigned long long tot[NREG];     // blocks per region
 };
@@ -165,7 +165,7 @@ struct ProbeView {
   uint32_t *hist;       // [PART_WG][NREG] blocks of each region in each partition chunk
   uint64_t *base;       // [PART_WG][NREG] first region-order position of each (chunk, region)
   uint64_t *part_key;   // region order: key
-  uint64_t *part_br;    // region order: block index | request << 32
+  uint32_t *part_req;   // region order: request of the block
   uint64_t *desc_p;     // region order: holder descriptor
   uint64_t cap;         // blocks the buffer holds
 };
@@ -179,7 +179,7 @@ inline uint64_t probe_layout(int64_t n_blocks, ProbeView *v, void *base) {
   };
   const uint64_t o_hdr = take(sizeof(ProbeHdr)), o_req = take(4 * n), o_inv = take(4 * n),
                  o_hist = take(4ull * NREG * PART_WG), o_base = take(8ull * NREG * PART_WG), o_k = take(8 * n),
-                 o_br = take(8 * n), o_dp = take(8 * n);
+                 o_rq = take(4 * n), o_dp = take(8 * n);
   if (v) {
     char *b = static_cast<char *>(base);
     v->hdr = reinterpret_cast<ProbeHdr *>(b + o_hdr);
@@ -188,7 +188,7 @@ inline uint64_t probe_layout(int64_t n_blocks, ProbeView *v, void *base) {
     v->hist = reinterpret_cast<uint32_t *>(b + o_hist);
     v->base = reinterpret_cast<uint64_t *>(b + o_base);
     v->part_key = reinterpret_cast<uint64_t *>(b + o_k);
-    v->part_br = reinterpret_cast<uint64_t *>(b + o_br);
+    v->part_req = reinterpret_cast<uint32_t *>(b + o_rq);
     v->desc_p = reinterpret_cast<uint64_t *>(b + o_dp);
     v->cap = n;
   }

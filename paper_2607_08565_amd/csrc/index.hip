@@ -297,9 +297,12 @@ struct WsHdr {
   unsigned long long n_cand;   // pairs absent before the batch (region-ordered insert)
   unsigned long long n_dd;     // dedupe slots in use (a power of two)
   unsigned long long n_def;    // new pairs deferred until their key's conversion
-  unsigned long long n_dup;    // region-ordered insert: candidates whose key an earlier one claimed
-  unsigned long long n_dd2;    // region-ordered insert: pair-table slots in use (a power of two)
-  unsigned long long pad[23];
+  unsigned long long nsub;     // region-ordered insert: bins per region (a power of two)
+  unsigned long long n_dd2;    // region-ordered insert: fallback pair-table slots in use
+  unsigned long long n_over;   // region-ordered insert: candidates in bins too large for LDS
+  int req_bad;                 // region-ordered insert: some request's target or session is invalid
+  int inl;                     // region-ordered insert: refreshes done by the classify pass
+  unsigned long long pad[21];
 };
 static_assert(sizeof(WsHdr) == 256, "ws header size");
 
@@ -318,35 +321,50 @@ struct Cand {
   uint64_t w2;  // same encoding as DSlot::w2
 };
 
-// Key-only claim table of the region-ordered insert: the first candidate of a key claims
-// the slot, later ones count themselves in `extra`.
-struct KSlot {
-  uint64_t key;
-  unsigned long long extra;
-};
-
-// Distinct new pair of the region-ordered insert.  h >= 0: its key repeats among the
-// candidates and dd[h] holds the pair's final (lowest) request.
+// Distinct new pair of the region-ordered insert, in bin order (key KEY_EMPTY: a dropped
+// duplicate).  w2 as in DSlot, or NP_FALLBACK | h: the pair went through the fallback
+// pair table and dd[h].w2 holds its final (lowest) request.
 struct NewPair {
   uint64_t key;
   uint64_t w2;
-  int64_t h;
 };
+constexpr uint64_t NP_FALLBACK = uint64_t(1) << 63;
+__device__ __forceinline__ uint64_t np_w2(const NewPair &e, const DSlot *dd) {
+  return (e.w2 & NP_FALLBACK) ? dd[e.w2 & ~NP_FALLBACK].w2 : e.w2;
+}
+
+// Binning of the region-ordered insert's candidates: bins are NREG x nsub equal ranges of
+// home buckets, so every candidate of a key -- and of a (key, instance) pair -- lies in
+// one bin, and a bin is deduplicated in LDS by one workgroup.
+constexpr int KCH = 32;                     // chunks per region of the bin partition
+constexpr int SEG_PER_CH = FLAT_WG / KCH;   // classify segments per chunk
+constexpr int NSUB_MAX = 1024;              // bins per region, at most
+constexpr int NBIN_MAX = NREG * NSUB_MAX;
+constexpr int BIN_TARGET = 1536;            // nsub keeps the mean bin at or below this
+constexpr int DT = 4096;                    // slots of a bin's LDS pair table
+constexpr int BIN_CAP = 3072;               // larger bins use the fallback pair table
+static_assert(FLAT_WG % KCH == 0 && SEG_PER_CH <= 64, "chunk = whole classify segments");
+static_assert(BIN_CAP + WG_THREADS < DT, "an LDS pair table never fills");
 
 struct InsWs {
   WsHdr *hdr;
   uint64_t *pos;    // per block: slot + 1 of an entry to refresh, 0 = none
-  DSlot *dd;        // dedupe table
+  DSlot *dd;        // dedupe table (region-ordered insert: fallback pair table)
   uint64_t *list;   // dedupe slots of distinct new pairs
   uint64_t *trig;   // keys queued for conversion
   uint64_t *def;    // list positions of deferred new pairs
-  Cand *cand;       // region-ordered insert: absent pairs, one segment per workgroup
-  uint32_t *cand_h;    // region-ordered insert: key-table slot of each candidate
-  KSlot *kt;           // region-ordered insert: key claims
-  NewPair *np;         // region-ordered insert: distinct new pairs, one segment per workgroup
-  uint32_t *cand_cnt;  // entries in each workgroup's candidate segment
-  uint32_t *dup_cnt;   // repeated-key candidates seen by each workgroup
-  uint32_t *list_cnt;  // entries in each workgroup's new-pair segment
+  Cand *cand;       // region-ordered insert: absent pairs, one segment per workgroup,
+                    // cut into one part per region
+  uint32_t *cand_cnt;  // [FLAT_WG] candidates in each segment
+  uint32_t *ctot;   // [NREG][KCH] candidates in each chunk of the bin partition
+  uint32_t *soff;   // [FLAT_WG][NREG] offset of each (segment, region) part in its segment
+  uint32_t *rcnt;   // [FLAT_WG][NREG] candidates in each part
+  uint32_t *hist2;  // [NREG][KCH][NSUB_MAX] candidates of each bin in each chunk
+  uint32_t *base2;  // [NREG][KCH][NSUB_MAX] first bin-order position of each (chunk, bin)
+  uint32_t *bstart; // [NBIN_MAX + 1] first bin-order position of each bin
+  uint32_t *bdist;  // [NBIN_MAX] distinct new pairs of each bin
+  Cand *bcand;      // candidates in bin order
+  NewPair *np;      // bin order: distinct new pairs
   uint64_t n_dedupe;
   uint64_t list_cap;  // entries in list and trig
   uint64_t seg;       // segment length of the region-ordered insert
@@ -376,12 +394,16 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
   const uint64_t o_trig = take(8 * nl);
   const uint64_t o_def = take(8 * nl);
   const uint64_t o_cand = take(sizeof(Cand) * seg_n);
-  const uint64_t o_ch = take(4 * seg_n);
-  const uint64_t o_kt = take(sizeof(KSlot) * nd);
-  const uint64_t o_np = take(sizeof(NewPair) * seg_n);
-  const uint64_t o_cc = take(4 * FLAT_WG);
-  const uint64_t o_dc = take(4 * FLAT_WG);
-  const uint64_t o_lc = take(4 * FLAT_WG);
+  const uint64_t o_cc = take(4ull * FLAT_WG);
+  const uint64_t o_ct = take(4ull * NREG * KCH);
+  const uint64_t o_soff = take(4ull * FLAT_WG * NREG);
+  const uint64_t o_rcnt = take(4ull * FLAT_WG * NREG);
+  const uint64_t o_h2 = take(4ull * NREG * KCH * NSUB_MAX);
+  const uint64_t o_b2 = take(4ull * NREG * KCH * NSUB_MAX);
+  const uint64_t o_bs = take(4ull * (NBIN_MAX + 1));
+  const uint64_t o_bd = take(4ull * NBIN_MAX);
+  const uint64_t o_bc = take(sizeof(Cand) * n);
+  const uint64_t o_np = take(sizeof(NewPair) * n);
   if (ws) {
     char *b = static_cast<char *>(base);
     ws->hdr = reinterpret_cast<WsHdr *>(b + o_hdr);
@@ -391,12 +413,16 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
     ws->trig = reinterpret_cast<uint64_t *>(b + o_trig);
     ws->def = reinterpret_cast<uint64_t *>(b + o_def);
     ws->cand = reinterpret_cast<Cand *>(b + o_cand);
-    ws->cand_h = reinterpret_cast<uint32_t *>(b + o_ch);
-    ws->kt = reinterpret_cast<KSlot *>(b + o_kt);
-    ws->np = reinterpret_cast<NewPair *>(b + o_np);
-    ws->dup_cnt = reinterpret_cast<uint32_t *>(b + o_dc);
     ws->cand_cnt = reinterpret_cast<uint32_t *>(b + o_cc);
-    ws->list_cnt = reinterpret_cast<uint32_t *>(b + o_lc);
+    ws->ctot = reinterpret_cast<uint32_t *>(b + o_ct);
+    ws->soff = reinterpret_cast<uint32_t *>(b + o_soff);
+    ws->rcnt = reinterpret_cast<uint32_t *>(b + o_rcnt);
+    ws->hist2 = reinterpret_cast<uint32_t *>(b + o_h2);
+    ws->base2 = reinterpret_cast<uint32_t *>(b + o_b2);
+    ws->bstart = reinterpret_cast<uint32_t *>(b + o_bs);
+    ws->bdist = reinterpret_cast<uint32_t *>(b + o_bd);
+    ws->bcand = reinterpret_cast<Cand *>(b + o_bc);
+    ws->np = reinterpret_cast<NewPair *>(b + o_np);
     ws->n_dedupe = nd;
     ws->list_cap = nl;
     ws->seg = seg;
@@ -596,6 +622,19 @@ __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned l
 // ---------------------------------------------------------------------------------
 // Region-ordered insert, from the descriptors of smetric_probe
 // ---------------------------------------------------------------------------------
+// Pipeline (no sort, no global atomics on the way to the distinct new pairs):
+//   classify   per block in region order: refresh position, or candidate appended to the
+//              region's part of the workgroup's segment; when no error can abort the
+//              insert (checked beforehand: keys, requests, capacity for every block) the
+//              refresh is done here and its pass is skipped
+//   bins       the candidates partitioned into NREG x nsub bins of home buckets (count,
+//              scan, scatter, as the probe's region partition), so all candidates of a
+//              pair share a bin
+//   dedupe     one workgroup per bin: an LDS pair table keeps each (key, instance) once
+//              with its lowest request; bins above BIN_CAP use the global pair table
+//   check      all-or-nothing: EINVAL or EFULL leave the index unchanged
+//   refresh    epoch = max(old, epoch) at the classified positions (if not done above)
+//   place      distinct new pairs in bin (so region) order; spill and deferred as above
 // find_member with each bucket read whole (keys and values in one 128-byte request), so
 // a chain step is one round trip.
 __device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t inst) {
@@ -623,28 +662,58 @@ __device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t ins
 // classify: per probed block (region order), is (key, target) already an entry?  The
 // descriptor answers it for NONE and ONE; HOT needs the bitmap bit and the member slot
 // (inside the key's region), MANY a chain walk.  Existing -> refresh position; absent ->
-// candidate, appended to this workgroup's segment (LDS counter, no global atomics).
+// candidate, appended to the part of this workgroup's segment that holds its region
+// (LDS counters, no global atomics).  The part of region g has room for every position
+// of the workgroup in g: with F(x) = the workgroup's positions below x, it starts at
+// F(start of g).
 // All FLAT_WG workgroups advance through the region order together.  Each thread takes
 // CU positions per round (the same positions as a plain grid-stride loop, so segments
 // keep their bound), with every load of the round issued before any result is used.
+__device__ __forceinline__ uint32_t positions_below(uint64_t x, uint64_t span, uint32_t w) {
+  const uint64_t r = x % span, lo = uint64_t(w) * TB;
+  return uint32_t((x / span) * TB + (r <= lo ? 0 : (r - lo < TB ? r - lo : TB)));
+}
+
 __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeView pv, InsWs ws,
-                                                           const int32_t *instance, const uint32_t *session) {
-  __shared__ unsigned int lc;
-  if (threadIdx.x == 0) lc = 0;
+                                                           const int32_t *instance, const uint32_t *session,
+                                                           uint32_t epoch) {
+  __shared__ unsigned int lc[NREG];
+  __shared__ uint32_t part[NREG];
+  __shared__ unsigned long long rb[NREG + 1];  // region boundaries in position order
+  const int tid = threadIdx.x;
+  const uint64_t span = uint64_t(gridDim.x) * TB;
+  if (tid == 0) {
+    unsigned long long acc = 0;
+    for (int g = 0; g < NREG; ++g) {
+      rb[g] = acc;
+      acc += pv.hdr->tot[g];
+    }
+    rb[NREG] = acc;
+  }
+  __syncthreads();
+  if (tid < NREG) {
+    lc[tid] = 0;
+    part[tid] = positions_below(rb[tid], span, blockIdx.x);
+  }
   __syncthreads();
   const uint64_t n = pv.hdr->n;
   if (pv.hdr->err) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-      ws_error(ws.hdr, SMETRIC_EINVAL);
-      ws.cand_cnt[0] = 0;
+    if (blockIdx.x == 0 && tid == 0) ws_error(ws.hdr, SMETRIC_EINVAL);
+    if (tid < NREG) {
+      ws.rcnt[uint64_t(blockIdx.x) * NREG + tid] = 0;
+      ws.soff[uint64_t(blockIdx.x) * NREG + tid] = 0;
     }
-    if (threadIdx.x == 0) ws.cand_cnt[blockIdx.x] = 0;
+    if (tid == 0) ws.cand_cnt[blockIdx.x] = 0;
     return;
   }
+  // No error can abort this insert (valid keys and requests; even if every block were a new
+  // entry the index would not overflow): refreshes are done here, in place.
+  const bool inl = !pv.hdr->bad_key && !ws.hdr->req_bad && ix.hdr->n_entries + n <= ix.capacity;
+  if (blockIdx.x == 0 && tid == 0) ws.hdr->inl = inl;
   Cand *seg = ws.cand + uint64_t(blockIdx.x) * ws.seg;
   constexpr int CU = 4;
-  const uint64_t span = uint64_t(gridDim.x) * TB;
-  for (uint64_t i0 = uint64_t(blockIdx.x) * TB + threadIdx.x; i0 < n; i0 += CU * span) {
+  int gcur = 0;  // region of this thread's current position (positions only increase)
+  for (uint64_t i0 = uint64_t(blockIdx.x) * TB + tid; i0 < n; i0 += CU * span) {
     // positions past the end read the last position (in bounds) and are dropped below
     uint64_t key[CU], d[CU];
     uint32_t r[CU];
@@ -652,7 +721,7 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
     for (int u = 0; u < CU; ++u) {
       const uint64_t i = i0 + u * span < n ? i0 + u * span : n - 1;
       key[u] = pv.part_key[i];
-      r[u] = uint32_t(pv.part_br[i] >> 32);
+      r[u] = pv.part_req[i];
       d[u] = pv.desc_p[i];
     }
     int32_t t[CU];
@@ -669,38 +738,80 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
       const bool hot = desc_kind(d[u]) == D_HOT && t[u] >= 0 && t[u] < ix.n_inst;
       hw[u] = ix.pool[(hot ? desc_x(d[u]) : 0) * uint64_t(ix.words) + (hot ? uint32_t(t[u]) >> 6 : 0u)];
     }
+    int64_t slot[CU];
 #pragma unroll
     for (int u = 0; u < CU; ++u) {
+      slot[u] = -1;
       const uint64_t i = i0 + u * span;
-      if (i >= n) break;
-      uint64_t pos = 0;
+      if (i >= n) continue;
+      while (gcur < NREG - 1 && rb[gcur + 1] <= i) ++gcur;
       if (t[u] < 0 || t[u] >= ix.n_inst || sess[u] >= SESSION_LIMIT || key[u] == KEY_EMPTY || key[u] == KEY_TOMB) {
         ws_error(ws.hdr, SMETRIC_EINVAL);
       } else {
         const uint32_t kind = desc_kind(d[u]);
-        int64_t slot = -1;
         if (kind == D_ONE) {
-          if (desc_inst(d[u]) == uint32_t(t[u])) slot = int64_t(desc_x(d[u]));
+          if (desc_inst(d[u]) == uint32_t(t[u])) slot[u] = int64_t(desc_x(d[u]));
         } else if (kind == D_HOT) {
-          if ((hw[u] >> (t[u] & 63)) & 1) slot = find_member_line(ix, key[u], uint32_t(t[u])).slot;
+          if ((hw[u] >> (t[u] & 63)) & 1) slot[u] = find_member_line(ix, key[u], uint32_t(t[u])).slot;
         } else if (kind == D_MANY) {
-          slot = find_entry(ix, key[u], uint32_t(t[u])).slot;
+          slot[u] = find_entry(ix, key[u], uint32_t(t[u])).slot;
         }
-        if (slot >= 0) pos = uint64_t(slot) + 1;
-        else seg[atomicAdd(&lc, 1u)] = Cand{key[u], ((uint64_t(t[u]) + 1) << 32) | r[u]};
+        if (slot[u] < 0)
+          seg[part[gcur] + atomicAdd(&lc[gcur], 1u)] = Cand{key[u], ((uint64_t(t[u]) + 1) << 32) | r[u]};
       }
-      ws.pos[i] = pos;
+    }
+    if (inl) {
+      // epoch = max(old, epoch): every value requested before any is written back (a
+      // position without an entry reads slot 0's value, always present, and drops it)
+      uint64_t v[CU];
+#pragma unroll
+      for (int u = 0; u < CU; ++u) v[u] = *val_ptr(ix, slot[u] >= 0 ? slot[u] : 0);
+#pragma unroll
+      for (int u = 0; u < CU; ++u)
+        if (slot[u] >= 0 && val_epoch(v[u]) < epoch)
+          *val_ptr(ix, slot[u]) = (v[u] & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+    } else {
+#pragma unroll
+      for (int u = 0; u < CU; ++u)
+        if (i0 + u * span < n) ws.pos[i0 + u * span] = slot[u] >= 0 ? uint64_t(slot[u]) + 1 : 0;
     }
   }
   __syncthreads();
-  if (threadIdx.x == 0) ws.cand_cnt[blockIdx.x] = lc;
+  if (tid < NREG) {
+    ws.rcnt[uint64_t(blockIdx.x) * NREG + tid] = lc[tid];
+    ws.soff[uint64_t(blockIdx.x) * NREG + tid] = part[tid];
+  }
+  if (tid == 0) {
+    unsigned int all = 0;
+    for (int g = 0; g < NREG; ++g) all += lc[g];
+    ws.cand_cnt[blockIdx.x] = all;
+  }
 }
 
-// Sum of the FLAT_WG per-workgroup counts, by one workgroup of TB threads.
-__device__ unsigned long long sum_counts(const uint32_t *cnt) {
+// Flags a request whose target or session is out of range (the classify pass then takes
+// the path that checks every block before the index changes).
+__global__ __launch_bounds__(TB) void insp_valid_kernel(DevIndex ix, InsWs ws, const int32_t *instance,
+                                                        const uint32_t *session, int32_t n_req) {
+  bool bad = false;
+  for (int32_t r = blockIdx.x * TB + threadIdx.x; r < n_req; r += gridDim.x * TB)
+    bad |= instance[r] < 0 || instance[r] >= ix.n_inst || session[r] >= SESSION_LIMIT;
+  if (bad) atomicOr(&ws.hdr->req_bad, 1);
+}
+
+// Sum of n 32-bit counts, by one workgroup of TB threads (eight loads in flight per thread).
+__device__ unsigned long long sum_counts(const uint32_t *cnt, uint32_t n) {
   __shared__ unsigned long long part[TB / 64];
   unsigned long long c = 0;
-  for (int w = threadIdx.x; w < FLAT_WG; w += TB) c += cnt[w];
+  for (uint32_t w0 = 0; w0 < n; w0 += 8 * TB) {
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t w = w0 + u * TB + threadIdx.x;
+      v[u] = w < n ? cnt[w] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) c += v[u];
+  }
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = c;
@@ -708,27 +819,146 @@ __device__ unsigned long long sum_counts(const uint32_t *cnt) {
   unsigned long long all = 0;
 #pragma unroll
   for (int i = 0; i < TB / 64; ++i) all += part[i];
+  __syncthreads();
   return all;
 }
 
-// total candidates -> size of the key table: the least power of two >= 1.5 x candidates
+// total candidates -> bins per region: the least power of two that keeps the mean bin at
+// or below BIN_TARGET candidates (at most NSUB_MAX)
 __global__ __launch_bounds__(TB) void insp_size_kernel(InsWs ws) {
-  const unsigned long long c = sum_counts(ws.cand_cnt);
+  const unsigned long long c = sum_counts(ws.cand_cnt, FLAT_WG);
   if (threadIdx.x != 0) return;
   ws.hdr->n_cand = c;
-  uint64_t nd = 64;
-  while (nd < c + c / 2 && nd < ws.n_dedupe) nd <<= 1;
-  ws.hdr->n_dd = nd;
+  uint64_t nsub = 1;
+  while (nsub < NSUB_MAX && nsub * NREG * BIN_TARGET < c) nsub <<= 1;
+  ws.hdr->nsub = nsub;
 }
 
-// repeated-key candidates -> size of the pair table: a key seen m >= 2 times puts m <= 2 (m - 1)
-// candidates there, so 1.5 x 2 x repeats slots keep it at most 2/3 full
-__global__ __launch_bounds__(TB) void insp_size2_kernel(InsWs ws) {
-  const unsigned long long c = sum_counts(ws.dup_cnt);
-  if (threadIdx.x != 0) return;
-  ws.hdr->n_dup = c;
-  uint64_t nd = 64;
-  while (nd < 3 * c && nd < ws.n_dedupe) nd <<= 1;
+// Bin of a key among NREG * nsub equal ranges of home buckets; bin / nsub is its region.
+__device__ __forceinline__ uint32_t bin_of(uint64_t key, uint64_t n_buckets, uint32_t nsub) {
+  return uint32_t(home_bucket(key, n_buckets) * (uint64_t(NREG) * nsub) / n_buckets);
+}
+
+// The candidates of chunk (g, c): the region-g parts of classify segments
+// [c SEG_PER_CH, (c + 1) SEG_PER_CH), seen as one array through the parts' prefix sums.
+struct ChunkParts {
+  uint32_t pre[SEG_PER_CH + 1];  // prefix of the parts' counts
+  uint64_t at[SEG_PER_CH];       // start of each part in ws.cand
+};
+__device__ void chunk_parts(const InsWs &ws, int g, int c, ChunkParts &cp) {
+  if (threadIdx.x == 0) {
+    uint32_t acc = 0;
+    for (int p = 0; p < SEG_PER_CH; ++p) {
+      const uint64_t w = uint64_t(c) * SEG_PER_CH + p;
+      cp.pre[p] = acc;
+      cp.at[p] = w * ws.seg + ws.soff[w * NREG + g];
+      acc += ws.rcnt[w * NREG + g];
+    }
+    cp.pre[SEG_PER_CH] = acc;
+  }
+  __syncthreads();
+}
+__device__ __forceinline__ const Cand *chunk_item(const InsWs &ws, const ChunkParts &cp, uint32_t v) {
+  int lo = 0, hi = SEG_PER_CH;  // the part p with pre[p] <= v < pre[p + 1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (cp.pre[mid] <= v) lo = mid;
+    else hi = mid;
+  }
+  return ws.cand + cp.at[lo] + (v - cp.pre[lo]);
+}
+
+// Count pass of the bin partition: workgroup (g, c) histograms its chunk over region g's
+// bins (eight candidates per thread per round, loads first) and records the chunk's size.
+__global__ __launch_bounds__(TB) void insp_bcount_kernel(DevIndex ix, InsWs ws) {
+  __shared__ ChunkParts cp;
+  __shared__ uint32_t h[NSUB_MAX];
+  const int g = blockIdx.x / KCH, c = blockIdx.x % KCH;
+  const uint32_t nsub = uint32_t(ws.hdr->nsub);
+  for (int s = threadIdx.x; s < NSUB_MAX; s += TB) h[s] = 0;
+  chunk_parts(ws, g, c, cp);  // synchronises
+  const uint32_t m = cp.pre[SEG_PER_CH];
+  constexpr int UC = 8;
+  for (uint32_t v0 = 0; v0 < m; v0 += UC * TB) {
+    uint64_t k[UC];
+#pragma unroll
+    for (int u = 0; u < UC; ++u) {
+      const uint32_t v = v0 + u * TB + threadIdx.x;
+      k[u] = v < m ? chunk_item(ws, cp, v)->key : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < UC; ++u) {
+      if (v0 + u * TB + threadIdx.x < m) {
+        const uint32_t sub = bin_of(k[u], ix.n_buckets, nsub) - uint32_t(g) * nsub;
+        atomicAdd(&h[sub < nsub ? sub : nsub - 1], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  uint32_t *out = ws.hist2 + (uint64_t(g) * KCH + c) * NSUB_MAX;
+  for (uint32_t s = threadIdx.x; s < nsub; s += TB) out[s] = h[s];
+  if (threadIdx.x == 0) ws.ctot[g * KCH + c] = m;
+}
+
+// Scan pass: workgroup g gives every bin of region g its first position (regions in
+// order, bins in order inside a region) and every (chunk, bin) its running offset; bins
+// larger than BIN_CAP add their size to n_over.  One thread per bin, its KCH chunk
+// counts loaded at once.
+constexpr int SCAN_T = NSUB_MAX;
+static_assert(NREG * KCH <= SCAN_T, "one chunk total per thread for the region start");
+__global__ __launch_bounds__(SCAN_T) void insp_bscan_kernel(InsWs ws) {
+  __shared__ uint32_t wt[SCAN_T / 64];
+  __shared__ unsigned long long red[SCAN_T / 64];
+  const int g = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const uint32_t nsub = uint32_t(ws.hdr->nsub);
+  // first position of region g: the chunks of every region before it
+  unsigned long long before = t < g * KCH ? ws.ctot[t] : 0u;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) before += __shfl_xor(before, d, 64);
+  if (lane == 0) red[wave] = before;
+  const uint32_t *hg = ws.hist2 + uint64_t(g) * KCH * NSUB_MAX + t;
+  uint32_t hc[KCH];
+#pragma unroll
+  for (int c = 0; c < KCH; ++c) hc[c] = uint32_t(t) < nsub ? hg[uint64_t(c) * NSUB_MAX] : 0u;
+  uint32_t tot = 0;
+#pragma unroll
+  for (int c = 0; c < KCH; ++c) tot += hc[c];
+  uint32_t x = tot;  // inclusive scan of the bin totals over the workgroup
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wt[wave] = x;
+  __syncthreads();
+  unsigned long long start = 0;
+#pragma unroll
+  for (int i = 0; i < SCAN_T / 64; ++i) start += red[i];
+  uint32_t pre = x - tot;
+  for (int i = 0; i < wave; ++i) pre += wt[i];
+  if (uint32_t(t) < nsub) {
+    const uint32_t first = uint32_t(start) + pre;
+    ws.bstart[uint64_t(g) * nsub + t] = first;
+    uint32_t acc = first;
+    uint32_t *bg = ws.base2 + uint64_t(g) * KCH * NSUB_MAX + t;
+#pragma unroll
+    for (int c = 0; c < KCH; ++c) {
+      bg[uint64_t(c) * NSUB_MAX] = acc;
+      acc += hc[c];
+    }
+    if (tot > uint32_t(BIN_CAP)) atomicAdd(&ws.hdr->n_over, (unsigned long long)tot);
+    if (g == NREG - 1 && uint32_t(t) == nsub - 1) ws.bstart[uint64_t(NREG) * nsub] = acc;
+  }
+}
+
+// fallback pair-table size for the oversized bins: a power of two >= 2 x their candidates
+__global__ void insp_size2_kernel(InsWs ws) {
+  const unsigned long long c = ws.hdr->n_over;
+  uint64_t nd = 0;
+  if (c) {
+    nd = 64;
+    while (nd < 2 * c && nd < ws.n_dedupe) nd <<= 1;
+  }
   ws.hdr->n_dd2 = nd;
 }
 
@@ -738,84 +968,203 @@ __global__ void dd_clear_kernel(DSlot *dd, uint64_t n, const unsigned long long 
   for (uint64_t h = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; h < nd; h += stride) dd[h] = DSlot{0, 0};
 }
 
-__global__ void kt_clear_kernel(KSlot *kt, const unsigned long long *n_dev) {
-  const uint64_t nd = *n_dev;
-  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t h = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; h < nd; h += stride) kt[h] = KSlot{0, 0};
-}
-
-// Claim the candidate's key alone: one compare-and-swap for the first candidate of a key,
-// an increment of the slot's count for every later one.  Returns the slot.
-__device__ uint32_t claim_key(const InsWs &ws, uint64_t nd, uint64_t key, bool &repeat) {
-  uint64_t h = mix64(key ^ 0x5851F42D4C957F2Dull) & (nd - 1);
-  for (uint64_t step = 0; step < nd; ++step, h = (h + 1) & (nd - 1)) {
-    KSlot *k = ws.kt + h;
-    // a plain load first: occupied slots are passed without an atomic
-    uint64_t cur = __hip_atomic_load(&k->key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (cur == KEY_EMPTY) {
-      cur = atomicCAS(reinterpret_cast<unsigned long long *>(&k->key), KEY_EMPTY, key);
-      if (cur == KEY_EMPTY) {
-        repeat = false;
-        return uint32_t(h);
+// Scatter pass: workgroup (g, c) moves its chunk into bin order one tile at a time (LDS
+// ranks per bin, the tile regrouped by bin in LDS, each bin's part written as one run
+// after the previous tile's).
+constexpr int U2 = 8;
+constexpr int TILE2 = U2 * TB;
+static_assert(NSUB_MAX % TB == 0, "bins per thread in the scans");
+__global__ __launch_bounds__(TB) void insp_bscatter_kernel(DevIndex ix, InsWs ws) {
+  __shared__ ChunkParts cp;
+  __shared__ uint32_t cnt[NSUB_MAX], tstart[NSUB_MAX], run[NSUB_MAX], wt[TB / 64];
+  __shared__ Cand sc[TILE2];
+  __shared__ uint16_t ssub[TILE2];
+  const int g = blockIdx.x / KCH, c = blockIdx.x % KCH, t = threadIdx.x;
+  const uint32_t nsub = uint32_t(ws.hdr->nsub);
+  const uint32_t *b2 = ws.base2 + (uint64_t(g) * KCH + c) * NSUB_MAX;
+  for (uint32_t s = t; s < NSUB_MAX; s += TB) {
+    run[s] = s < nsub ? b2[s] : 0;
+    cnt[s] = 0;
+  }
+  chunk_parts(ws, g, c, cp);  // synchronises
+  const uint32_t m = cp.pre[SEG_PER_CH];
+  for (uint32_t t0 = 0; t0 < m; t0 += TILE2) {
+    Cand e[U2];
+    uint32_t sub[U2], rk[U2];
+#pragma unroll
+    for (int u = 0; u < U2; ++u) {
+      const uint32_t v = t0 + u * TB + t;
+      e[u] = v < m ? *chunk_item(ws, cp, v) : Cand{0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < U2; ++u) {
+      const uint32_t s = bin_of(e[u].key, ix.n_buckets, nsub) - uint32_t(g) * nsub;
+      sub[u] = s < nsub ? s : nsub - 1;
+      rk[u] = t0 + u * TB + t < m ? atomicAdd(&cnt[sub[u]], 1u) : 0;
+    }
+    __syncthreads();
+    // exclusive scan of the tile's bin counts
+    constexpr int Q = NSUB_MAX / TB;
+    uint32_t q[Q], sum = 0;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      q[j] = cnt[t * Q + j];
+      sum += q[j];
+    }
+    uint32_t x = sum;
+    const int lane = t & 63, wave = t >> 6;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (lane == 63) wt[wave] = x;
+    __syncthreads();
+    uint32_t pre = x - sum;
+    for (int i = 0; i < wave; ++i) pre += wt[i];
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      tstart[t * Q + j] = pre;
+      pre += q[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U2; ++u) {
+      if (t0 + u * TB + t < m) {
+        const uint32_t p = tstart[sub[u]] + rk[u];
+        sc[p] = e[u];
+        ssub[p] = uint16_t(sub[u]);
       }
     }
-    if (cur == key) {
-      atomicAdd(&k->extra, 1ull);
-      repeat = true;
-      return uint32_t(h);
+    __syncthreads();
+    const uint32_t in_tile = m - t0 < uint32_t(TILE2) ? m - t0 : uint32_t(TILE2);
+#pragma unroll
+    for (int u = 0; u < U2; ++u) {
+      const uint32_t p = u * TB + t;
+      if (p < in_tile) {
+        const uint32_t s = ssub[p];
+        ws.bcand[run[s] + (p - tstart[s])] = sc[p];
+      }
+    }
+    __syncthreads();
+    for (uint32_t s = t; s < nsub; s += TB) {
+      run[s] += cnt[s];
+      cnt[s] = 0;
+    }
+    __syncthreads();
+  }
+}
+
+// Enter candidate (key, mine) in a bin's LDS pair table (the pair table's rule: a slot's
+// key is claimed first, then its instance; the same pair keeps the lowest request).
+__device__ __forceinline__ void lds_pair(unsigned long long *tk, unsigned long long *tw, uint64_t key,
+                                         uint64_t mine) {
+  uint32_t h = uint32_t(mix64(key ^ ((mine >> 32) * 0xC2B2AE3D27D4EB4Full))) & (DT - 1);
+  for (int step = 0; step < DT; ++step, h = (h + 1) & (DT - 1)) {
+    unsigned long long k = tk[h];
+    if (k == KEY_EMPTY) k = atomicCAS(&tk[h], 0ull, (unsigned long long)key);
+    if (k != KEY_EMPTY && k != key) continue;
+    unsigned long long w = tw[h];
+    while (true) {
+      if (w == 0) {
+        const unsigned long long prev = atomicCAS(&tw[h], 0ull, (unsigned long long)mine);
+        if (prev == 0) return;
+        w = prev;
+        continue;
+      }
+      if ((w >> 32) == (mine >> 32)) {
+        if (mine < w) atomicMin(&tw[h], (unsigned long long)mine);
+        return;
+      }
+      break;  // another instance's pair: keep probing
     }
   }
-  ws_error(ws.hdr, SMETRIC_EINTERNAL);
-  repeat = false;
-  return 0;
 }
 
-// workgroup w claims the keys of its candidate segment
-__global__ __launch_bounds__(TB) void insp_keyclaim_kernel(InsWs ws) {
-  __shared__ unsigned int lc;
-  if (threadIdx.x == 0) lc = 0;
-  __syncthreads();
-  const uint64_t nd = ws.hdr->n_dd;
-  const uint32_t n = ws.cand_cnt[blockIdx.x];
-  const uint64_t base = uint64_t(blockIdx.x) * ws.seg;
-  uint32_t mine = 0;
-  for (uint32_t k = threadIdx.x; k < n; k += TB) {
-    bool repeat;
-    ws.cand_h[base + k] = claim_key(ws, nd, ws.cand[base + k].key, repeat);
-    mine += repeat;
-  }
-  if (mine) atomicAdd(&lc, mine);
-  __syncthreads();
-  if (threadIdx.x == 0) ws.dup_cnt[blockIdx.x] = lc;
-}
-
-// workgroup w turns its candidate segment into its new-pair segment: a candidate whose key
-// no other candidate has is a distinct new pair as it stands; the others go through the
-// (key, instance) pair table, where the lowest request index wins
-__global__ __launch_bounds__(TB) void insp_dedupe_kernel(InsWs ws) {
-  __shared__ unsigned int lc;
-  if (threadIdx.x == 0) lc = 0;
-  __syncthreads();
+// Dedupe pass: each bin of at most BIN_CAP candidates is deduplicated in an LDS pair
+// table and its distinct pairs written to the front of its range of np (the rest get
+// KEY_EMPTY); a larger bin sends its candidates through the fallback pair table in
+// place.  Workgroups take bins in order; a bin's candidates are loaded (all at once)
+// before its table is cleared.
+constexpr int DD_T = 512;
+constexpr int DD_U = BIN_CAP / DD_T;
+static_assert(BIN_CAP % DD_T == 0 && DT % DD_T == 0, "whole candidates and slots per thread");
+__global__ __launch_bounds__(DD_T) void insp_bdedupe_kernel(InsWs ws) {
+  __shared__ unsigned long long tk[DT], tw[DT];
+  __shared__ uint32_t wt[DD_T / 64];
+  __shared__ unsigned int nfb;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const uint32_t nbin = uint32_t(ws.hdr->nsub) * NREG;
   const uint64_t nd2 = ws.hdr->n_dd2;
-  const uint32_t n = ws.cand_cnt[blockIdx.x];
-  const uint64_t base = uint64_t(blockIdx.x) * ws.seg;
-  for (uint32_t k = threadIdx.x; k < n; k += TB) {
-    const Cand c = ws.cand[base + k];
-    const unsigned long long extra = ws.kt[ws.cand_h[base + k]].extra;
-    int64_t h = -1;
-    bool fresh = true;
-    if (extra != 0) {
-      h = dedupe_pair(ws, nd2, c.key, c.w2);
-      fresh = h >= 0;
+  for (uint32_t b = blockIdx.x; b < nbin; b += gridDim.x) {
+    const uint32_t lo = ws.bstart[b], hi = ws.bstart[b + 1], m = hi - lo;
+    if (m == 0) {
+      if (t == 0) ws.bdist[b] = 0;
+      continue;
     }
-    if (fresh) ws.np[base + atomicAdd(&lc, 1u)] = NewPair{c.key, c.w2, h};
+    if (m > uint32_t(BIN_CAP)) {
+      if (t == 0) nfb = 0;
+      __syncthreads();
+      uint32_t mine = 0;
+      for (uint32_t k = lo + t; k < hi; k += DD_T) {
+        const Cand e = ws.bcand[k];
+        const int64_t h = dedupe_pair(ws, nd2, e.key, e.w2);
+        ws.np[k] = h >= 0 ? NewPair{e.key, NP_FALLBACK | uint64_t(h)} : NewPair{KEY_EMPTY, 0};
+        mine += h >= 0;
+      }
+      if (mine) atomicAdd(&nfb, mine);
+      __syncthreads();
+      if (t == 0) ws.bdist[b] = nfb;
+      __syncthreads();
+      continue;
+    }
+    Cand e[DD_U];
+#pragma unroll
+    for (int u = 0; u < DD_U; ++u) {
+      const uint32_t k = lo + u * DD_T + t;
+      e[u] = k < hi ? ws.bcand[k] : Cand{KEY_EMPTY, 0};
+    }
+    for (int j = t; j < DT; j += DD_T) {
+      tk[j] = 0;
+      tw[j] = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < DD_U; ++u)
+      if (e[u].key != KEY_EMPTY) lds_pair(tk, tw, e[u].key, e[u].w2);
+    __syncthreads();
+    // compact the occupied slots: thread t owns slots [t Q, t Q + Q)
+    constexpr int Q = DT / DD_T;
+    uint32_t occ = 0;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) occ += tk[t * Q + j] != KEY_EMPTY;
+    uint32_t x = occ;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (lane == 63) wt[wave] = x;
+    __syncthreads();
+    uint32_t pre = x - occ, total = 0;
+#pragma unroll
+    for (int i = 0; i < DD_T / 64; ++i) {
+      pre += i < wave ? wt[i] : 0;
+      total += wt[i];
+    }
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      const unsigned long long k = tk[t * Q + j];
+      if (k != KEY_EMPTY) ws.np[lo + pre++] = NewPair{uint64_t(k), uint64_t(tw[t * Q + j])};
+    }
+    for (uint32_t k = lo + total + t; k < hi; k += DD_T) ws.np[k] = NewPair{KEY_EMPTY, 0};
+    if (t == 0) ws.bdist[b] = total;
+    __syncthreads();
   }
-  __syncthreads();
-  if (threadIdx.x == 0) ws.list_cnt[blockIdx.x] = lc;
 }
 
 __global__ __launch_bounds__(TB) void insp_check_kernel(DevIndex ix, InsWs ws) {
-  const unsigned long long c = sum_counts(ws.list_cnt);
+  const unsigned long long c = sum_counts(ws.bdist, uint32_t(ws.hdr->nsub) * NREG);
   if (threadIdx.x != 0) return;
   WsHdr *h = ws.hdr;
   h->n_new = c;
@@ -829,7 +1178,7 @@ __global__ __launch_bounds__(TB) void insp_check_kernel(DevIndex ix, InsWs ws) {
 }
 
 __global__ __launch_bounds__(TB) void insp_refresh_kernel(DevIndex ix, ProbeView pv, InsWs ws, uint32_t epoch) {
-  if (ws.hdr->abort) return;
+  if (ws.hdr->abort || ws.hdr->inl) return;
   const uint64_t n = pv.hdr->n;
   const uint64_t span = uint64_t(gridDim.x) * TB;
   for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += span) {
@@ -841,25 +1190,28 @@ __global__ __launch_bounds__(TB) void insp_refresh_kernel(DevIndex ix, ProbeView
   }
 }
 
-// workgroup w enters its new-pair segment (in region order, like every segment)
+// place: the distinct new pairs in bin order (so in region order), all FLAT_WG
+// workgroups advancing through it together
 __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
                                                         uint32_t epoch) {
   if (ws.hdr->abort) return;
-  const uint32_t n = ws.list_cnt[blockIdx.x];
-  const uint64_t base = uint64_t(blockIdx.x) * ws.seg;
-  for (uint32_t k0 = 0; k0 < n; k0 += TB) {  // whole workgroups iterate together
-    const uint32_t k = k0 + threadIdx.x;
+  const uint64_t n = ws.hdr->n_cand;
+  const uint64_t span = uint64_t(gridDim.x) * TB;
+  for (uint64_t p0 = uint64_t(blockIdx.x) * TB; p0 < n; p0 += span) {  // whole workgroups iterate together
+    const uint64_t p = p0 + threadIdx.x;
     int64_t tk = -1, df = -1;
-    if (k < n) {
-      const NewPair e = ws.np[base + k];
-      const uint64_t w2 = e.h >= 0 ? ws.dd[e.h].w2 : e.w2;  // a repeated pair's lowest request
-      bool trig;
-      const int pl = place_new(ix, e.key, dd_inst(w2), epoch, session[dd_req(w2)], trig, true);
-      if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
-      else if (pl == DEFERRED) df = int64_t(base + k);
-      else if (trig) tk = int64_t(base + k);
+    if (p < n) {
+      const NewPair e = ws.np[p];
+      if (e.key != KEY_EMPTY) {
+        const uint64_t w2 = np_w2(e, ws.dd);  // a fallback pair's lowest request
+        bool trig;
+        const int pl = place_new(ix, e.key, dd_inst(w2), epoch, session[dd_req(w2)], trig, true);
+        if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+        else if (pl == DEFERRED) df = int64_t(p);
+        else if (trig) tk = int64_t(p);
+      }
     }
-    append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by list position
+    append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by np position
     append_wave(&ws.hdr->n_def, ws.def, ws.list_cap, df);
   }
 }
@@ -1034,7 +1386,7 @@ __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsign
     int pl;
     if (np) {
       const NewPair e = np[t];
-      const uint64_t w2 = e.h >= 0 ? dd[e.h].w2 : e.w2;
+      const uint64_t w2 = np_w2(e, dd);
       pl = place_new(ix, e.key, dd_inst(w2), epoch, session[dd_req(w2)], trig, false);
     } else if (via) {
       const DSlot d = dd[via[t]];
@@ -1342,14 +1694,18 @@ extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe
   int rc;
   if ((rc = fill(ws.hdr, sizeof(WsHdr), 0, stream))) return rc;
   const dim3 flat(FLAT_WG), blk(TB);
-  hipLaunchKernelGGL(insp_classify_kernel, flat, blk, 0, stream, ix, pv, ws, instance, session);
+  const dim3 chunks(NREG * KCH);
+  hipLaunchKernelGGL(insp_valid_kernel, dim3(grid_for(uint64_t(n_req))), blk, 0, stream, ix, ws, instance, session,
+                     n_req);
+  hipLaunchKernelGGL(insp_classify_kernel, flat, blk, 0, stream, ix, pv, ws, instance, session, epoch);
   hipLaunchKernelGGL(insp_size_kernel, dim3(1), blk, 0, stream, ws);
-  hipLaunchKernelGGL(kt_clear_kernel, dim3(grid_for(ws.n_dedupe)), blk, 0, stream, ws.kt, &ws.hdr->n_dd);
-  hipLaunchKernelGGL(insp_keyclaim_kernel, flat, blk, 0, stream, ws);
-  hipLaunchKernelGGL(insp_size2_kernel, dim3(1), blk, 0, stream, ws);
+  hipLaunchKernelGGL(insp_bcount_kernel, chunks, blk, 0, stream, ix, ws);
+  hipLaunchKernelGGL(insp_bscan_kernel, dim3(NREG), dim3(SCAN_T), 0, stream, ws);
+  hipLaunchKernelGGL(insp_size2_kernel, dim3(1), dim3(1), 0, stream, ws);
   hipLaunchKernelGGL(dd_clear_kernel, dim3(grid_for(ws.n_dedupe)), blk, 0, stream, ws.dd, ws.n_dedupe,
                      &ws.hdr->n_dd2);
-  hipLaunchKernelGGL(insp_dedupe_kernel, flat, blk, 0, stream, ws);
+  hipLaunchKernelGGL(insp_bscatter_kernel, chunks, blk, 0, stream, ix, ws);
+  hipLaunchKernelGGL(insp_bdedupe_kernel, flat, dim3(DD_T), 0, stream, ws);
   hipLaunchKernelGGL(insp_check_kernel, dim3(1), blk, 0, stream, ix, ws);
   hipLaunchKernelGGL(insp_refresh_kernel, flat, blk, 0, stream, ix, pv, ws, epoch);
   hipLaunchKernelGGL(insp_place_kernel, flat, blk, 0, stream, ix, ws, session, epoch);

@@ -11,12 +11,13 @@
 // well inside that reach), with no global atomics:
 //   requests  one wavefront per request checks the tiling and records each block's request
 //   count     PART_WG workgroups, one contiguous chunk of blocks each: LDS histogram of
-//             regions -> one row of the [chunk][region] matrix, plus region totals
+//             regions -> one row of the [chunk][region] matrix, plus region totals; a
+//             key equal to a reserved value (the table's EMPTY or TOMB marker) is flagged
 //   scan      one workgroup per region: its first position, then running offsets over
 //             chunks -> first position of every (chunk, region) pair
 //   scatter   each chunk again, one tile at a time: regrouped by region in LDS, then
-//             (key, block | request << 32) written as one contiguous run per region at its
-//             region-order position, and the inverse index block -> position
+//             (key, request) written as one contiguous run per region at its region-order
+//             position, and the inverse index block -> position
 //   probe     a fixed grid of FLAT_WG workgroups walks the region-ordered keys; all
 //             workgroups advance through the regions together, so the live window slides
 //             through the table.  One 128-byte bucket read per chain step (keys and values
@@ -92,6 +93,7 @@ __global__ __launch_bounds__(TB) void part_count_kernel(DevIndex ix, ProbeView p
   __syncthreads();
   uint64_t lo, hi;
   chunk_of(n, lo, hi);
+  bool bad = false;
   for (uint64_t t0 = lo; t0 < hi; t0 += TILE) {
     uint64_t k[U];
 #pragma unroll
@@ -101,8 +103,12 @@ __global__ __launch_bounds__(TB) void part_count_kernel(DevIndex ix, ProbeView p
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (t0 + u * TB + threadIdx.x < hi) atomicAdd(&h[region_of(k[u], ix.n_buckets)], 1u);
+      if (t0 + u * TB + threadIdx.x < hi) {
+        atomicAdd(&h[region_of(k[u], ix.n_buckets)], 1u);
+        bad |= k[u] == KEY_EMPTY || k[u] == KEY_TOMB;
+      }
   }
+  if (bad) atomicOr(&pv.hdr->bad_key, 1);
   __syncthreads();
   for (int g = threadIdx.x; g < NREG; g += TB) {
     const unsigned int c = h[g];
@@ -148,7 +154,8 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
                                                           uint64_t n) {
   __shared__ unsigned long long run[NREG];
   __shared__ uint32_t cnt[NREG], tstart[NREG], wt[TB / 64];
-  __shared__ uint64_t skey[TILE_W], sbr[TILE_W];
+  __shared__ uint64_t skey[TILE_W];
+  __shared__ uint32_t sblk[TILE_W], sreq[TILE_W];
   __shared__ uint8_t sg[TILE_W];
   if (pv.hdr->err) return;
   const int t = threadIdx.x;
@@ -185,7 +192,8 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
       if (b < hi) {
         const uint32_t p = tstart[g[u]] + rk[u];
         skey[p] = k[u];
-        sbr[p] = b | (uint64_t(r[u]) << 32);
+        sblk[p] = uint32_t(b);
+        sreq[p] = r[u];
         sg[p] = g[u];
       }
     }
@@ -196,10 +204,9 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
       if (p < total) {
         const uint32_t gg = sg[p];
         const uint64_t pos = run[gg] + (p - tstart[gg]);
-        const uint64_t br = sbr[p];
         pv.part_key[pos] = skey[p];
-        pv.part_br[pos] = br;
-        pv.inv[uint32_t(br)] = uint32_t(pos);
+        pv.part_req[pos] = sreq[p];
+        pv.inv[sblk[p]] = uint32_t(pos);
       }
     }
     __syncthreads();
