@@ -268,6 +268,71 @@ def test_efull_and_einval_leave_index_unchanged():
     assert st == oracle.EFULL and pair.gix.stats()[1] == 0
 
 
+def _probed_insert_both(pair, d_keys, d_boff, nb, okeys, blk_off, inst, sess, epoch):
+    """The region-ordered insert (probe state -> insert) on the GPU, the oracle's insert on the CPU."""
+    n_req = len(blk_off) - 1
+    state = pair.gix.probe(d_keys, d_boff, nb)
+    pair.gix.insert_probed(state, n_req, nb, to_dev(np.asarray(inst, np.int32)), to_dev(np.asarray(sess, np.uint32)),
+                           epoch)
+    return pair.oix.insert(okeys, blk_off, inst, sess, epoch)
+
+
+def test_probed_insert_oversized_bins_and_duplicates():
+    """Thousands of candidates of the same few keys: their bins exceed the LDS pair table and
+    go through the fallback pair table; repeated (key, instance) pairs keep the lowest request."""
+    rng = np.random.default_rng(21)
+    I, R = 512, 4096
+    pair = Pair(400_000, I)
+    base = rng.integers(0, W.VOCAB, 16 * 40, dtype=np.int32)
+    prompts = [base[: 16 * int(rng.integers(20, 41))] for _ in range(R)]
+    off = np.zeros(R + 1, np.int64)
+    off[1:] = np.cumsum([len(x) for x in prompts])
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(np.concatenate(prompts), off)
+    say(f"oversized bins: {nb} candidates of 40 keys")
+    inst = rng.integers(0, I, R).astype(np.int32)
+    sess = rng.permutation(R).astype(np.uint32)  # lowest request != lowest session
+    assert _probed_insert_both(pair, d_keys, d_boff, nb, okeys, blk_off, inst, sess, 3) == 0
+    pair.compare_index("oversized bins")
+    # again with new instances and an older epoch: refreshes keep the newer epoch
+    inst2 = rng.integers(0, I, R).astype(np.int32)
+    assert _probed_insert_both(pair, d_keys, d_boff, nb, okeys, blk_off, inst2, sess[::-1].copy(), 2) == 0
+    pair.compare_index("oversized bins, second batch")
+
+
+def test_probed_insert_errors_and_two_pass_refresh():
+    """The region-ordered insert's all-or-nothing errors, and its refresh pass when an error
+    cannot be ruled out beforehand (the index near capacity, or an invalid request without blocks)."""
+    rng = np.random.default_rng(22)
+    pair = Pair(100, 3)
+    toks, off = _rand_prompts(rng, 4, 300, 700)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+    half = np.array([0, nb // 2])
+    assert _probed_insert_both(pair, d_keys, to_dev(half), nb // 2, okeys, half, [1], [1], 1) == 0
+    pair.compare_index("first")
+    assert _probed_insert_both(pair, d_keys, d_boff, nb, okeys, blk_off, [0, 1, 2, 0], [1, 2, 3, 4], 2) == oracle.EFULL
+    pair.compare_index("efull")
+    assert _probed_insert_both(pair, d_keys, d_boff, nb, okeys, blk_off, [0, 5, 1, 1], [1, 2, 3, 4], 3) == oracle.EINVAL
+    pair.compare_index("einval")
+    _, st = pair.gix.stats(reset_status=True)
+    assert st == oracle.EFULL and pair.gix.stats()[1] == 0
+    # entries + blocks > capacity, but the new pairs fit: refreshes in their own pass
+    near = Pair(100, 3)
+    near.hash_both(toks, off)
+    assert _probed_insert_both(near, d_keys, to_dev(half), nb // 2, okeys, half, [1], [1], 1) == 0
+    assert near.oix.size + nb // 2 > 100
+    assert _probed_insert_both(near, d_keys, to_dev(half), nb // 2, okeys, half, [1], [7], 4) == 0
+    near.compare_index("refresh pass near capacity")
+    # a request without blocks may name any target; the others' pairs are entered
+    big = Pair(10_000, 3)
+    off2 = np.concatenate([off[:2], off[1:2], off[2:] - 0])  # request 1 is empty
+    toks2 = toks
+    d_boff2, nb2, d_keys2, okeys2, blk_off2 = big.hash_both(toks2, off2)
+    assert _probed_insert_both(big, d_keys2, d_boff2, nb2, okeys2, blk_off2, [0, 9, 1, 2, 0], [1, 2, 3, 4, 5], 1) == 0
+    big.compare_index("empty request with an invalid target")
+    assert _probed_insert_both(big, d_keys2, d_boff2, nb2, okeys2, blk_off2, [2, 9, 1, 0, 0], [6, 7, 8, 9, 10], 2) == 0
+    big.compare_index("refresh pass after an invalid empty request")
+
+
 def test_match_bad_range_and_empty_requests():
     rng = np.random.default_rng(10)
     pair = Pair(10_000, 5)
