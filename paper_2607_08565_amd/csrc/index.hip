@@ -337,13 +337,20 @@ __device__ __forceinline__ uint64_t np_w2(const NewPair &e, const DSlot *dd) {
 // home buckets, so every candidate of a key -- and of a (key, instance) pair -- lies in
 // one bin, and a bin is deduplicated in LDS by one workgroup.
 constexpr int KCH = 32;                     // chunks per region of the bin partition
-constexpr int SEG_PER_CH = FLAT_WG / KCH;   // classify segments per chunk
+// The classify pass runs INS_WG workgroups (as many as the device holds at its register
+// use), each filling one candidate segment.
+constexpr int INS_WG = 1024;
+inline uint64_t ins_segment(uint64_t n) {
+  const uint64_t span = uint64_t(INS_WG) * WG_THREADS;
+  return (n + span - 1) / span * WG_THREADS;
+}
+constexpr int SEG_PER_CH = INS_WG / KCH;    // classify segments per chunk
 constexpr int NSUB_MAX = 1024;              // bins per region, at most
 constexpr int NBIN_MAX = NREG * NSUB_MAX;
 constexpr int BIN_TARGET = 1536;            // nsub keeps the mean bin at or below this
 constexpr int DT = 4096;                    // slots of a bin's LDS pair table
 constexpr int BIN_CAP = 3072;               // larger bins use the fallback pair table
-static_assert(FLAT_WG % KCH == 0 && SEG_PER_CH <= 64, "chunk = whole classify segments");
+static_assert(INS_WG % KCH == 0 && SEG_PER_CH <= 64, "chunk = whole classify segments");
 static_assert(BIN_CAP + WG_THREADS < DT, "an LDS pair table never fills");
 
 struct InsWs {
@@ -355,10 +362,10 @@ struct InsWs {
   uint64_t *def;    // list positions of deferred new pairs
   Cand *cand;       // region-ordered insert: absent pairs, one segment per workgroup,
                     // cut into one part per region
-  uint32_t *cand_cnt;  // [FLAT_WG] candidates in each segment
+  uint32_t *cand_cnt;  // [INS_WG] candidates in each segment
   uint32_t *ctot;   // [NREG][KCH] candidates in each chunk of the bin partition
-  uint32_t *soff;   // [FLAT_WG][NREG] offset of each (segment, region) part in its segment
-  uint32_t *rcnt;   // [FLAT_WG][NREG] candidates in each part
+  uint32_t *soff;   // [INS_WG][NREG] offset of each (segment, region) part in its segment
+  uint32_t *rcnt;   // [INS_WG][NREG] candidates in each part
   uint32_t *hist2;  // [NREG][KCH][NSUB_MAX] candidates of each bin in each chunk
   uint32_t *base2;  // [NREG][KCH][NSUB_MAX] first bin-order position of each (chunk, bin)
   uint32_t *bstart; // [NBIN_MAX + 1] first bin-order position of each bin
@@ -379,7 +386,7 @@ uint64_t dedupe_size(int64_t n_blocks) {
 uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
   const uint64_t n = uint64_t(n_blocks < 1 ? 1 : n_blocks);
   const uint64_t nd = dedupe_size(n_blocks);
-  const uint64_t seg = flat_segment(n), seg_n = seg * FLAT_WG;
+  const uint64_t seg = ins_segment(n), seg_n = seg * INS_WG;
   const uint64_t nl = seg_n > n ? seg_n : n;
   uint64_t off = 0;
   auto take = [&](uint64_t bytes) {
@@ -394,10 +401,10 @@ uint64_t insert_ws_layout(int64_t n_blocks, InsWs *ws, void *base) {
   const uint64_t o_trig = take(8 * nl);
   const uint64_t o_def = take(8 * nl);
   const uint64_t o_cand = take(sizeof(Cand) * seg_n);
-  const uint64_t o_cc = take(4ull * FLAT_WG);
+  const uint64_t o_cc = take(4ull * INS_WG);
   const uint64_t o_ct = take(4ull * NREG * KCH);
-  const uint64_t o_soff = take(4ull * FLAT_WG * NREG);
-  const uint64_t o_rcnt = take(4ull * FLAT_WG * NREG);
+  const uint64_t o_soff = take(4ull * INS_WG * NREG);
+  const uint64_t o_rcnt = take(4ull * INS_WG * NREG);
   const uint64_t o_h2 = take(4ull * NREG * KCH * NSUB_MAX);
   const uint64_t o_b2 = take(4ull * NREG * KCH * NSUB_MAX);
   const uint64_t o_bs = take(4ull * (NBIN_MAX + 1));
@@ -666,7 +673,7 @@ __device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t ins
 // (LDS counters, no global atomics).  The part of region g has room for every position
 // of the workgroup in g: with F(x) = the workgroup's positions below x, it starts at
 // F(start of g).
-// All FLAT_WG workgroups advance through the region order together.  Each thread takes
+// All INS_WG workgroups advance through the region order together.  Each thread takes
 // CU positions per round (the same positions as a plain grid-stride loop, so segments
 // keep their bound), with every load of the round issued before any result is used.
 __device__ __forceinline__ uint32_t positions_below(uint64_t x, uint64_t span, uint32_t w) {
@@ -826,7 +833,7 @@ __device__ unsigned long long sum_counts(const uint32_t *cnt, uint32_t n) {
 // total candidates -> bins per region: the least power of two that keeps the mean bin at
 // or below BIN_TARGET candidates (at most NSUB_MAX)
 __global__ __launch_bounds__(TB) void insp_size_kernel(InsWs ws) {
-  const unsigned long long c = sum_counts(ws.cand_cnt, FLAT_WG);
+  const unsigned long long c = sum_counts(ws.cand_cnt, INS_WG);
   if (threadIdx.x != 0) return;
   ws.hdr->n_cand = c;
   uint64_t nsub = 1;
@@ -1697,7 +1704,7 @@ extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe
   const dim3 chunks(NREG * KCH);
   hipLaunchKernelGGL(insp_valid_kernel, dim3(grid_for(uint64_t(n_req))), blk, 0, stream, ix, ws, instance, session,
                      n_req);
-  hipLaunchKernelGGL(insp_classify_kernel, flat, blk, 0, stream, ix, pv, ws, instance, session, epoch);
+  hipLaunchKernelGGL(insp_classify_kernel, dim3(INS_WG), blk, 0, stream, ix, pv, ws, instance, session, epoch);
   hipLaunchKernelGGL(insp_size_kernel, dim3(1), blk, 0, stream, ws);
   hipLaunchKernelGGL(insp_bcount_kernel, chunks, blk, 0, stream, ix, ws);
   hipLaunchKernelGGL(insp_bscan_kernel, dim3(NREG), dim3(SCAN_T), 0, stream, ws);
