@@ -46,6 +46,12 @@ def parse():
     ap.add_argument("--pipelined", action="store_true",
                     help="two streams: the next batch's hash and partition run beside the current batch's insert "
                          "(default: one batch at a time on one stream, so each kernel's duration is its own)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after the timed steps, copy 1 GiB on the device (the counter runs' scale)")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="print the per-kernel summary of a rocprofv3 --kernel-trace run of this script and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the traffic file from two rocprofv3 --pmc runs of this script and exit")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (rocprofv3 FETCH_SIZE/WRITE_SIZE), if present")
     return ap.parse_args()
@@ -239,7 +245,7 @@ class Setup:
 
 # kernels each timed call launches, in order (names as rocprofv3 reports them)
 CALL_KERNELS = {
-    "hash": ["hash16_kernel"],
+    "hash": ["hash16_kernel<8>"],
     "probe": ["zero_kernel", "req_of_kernel", "part_count_kernel", "part_scan_kernel", "part_scatter_kernel",
               "probe_kernel"],
     "match": ["match_kernel<1, true>"],
@@ -249,6 +255,95 @@ CALL_KERNELS = {
                "insp_bdedupe_kernel", "insp_check_kernel", "insp_refresh_kernel", "insp_place_kernel", "spill_kernel",
                "deferred_kernel"],
 }
+
+
+def _kname(full: str) -> str:
+    """Kernel name as rocprofv3 prints it, without namespaces, return type and arguments."""
+    n = full.replace("smk::(anonymous namespace)::", "")
+    if n.startswith("void "):
+        n = n[5:]
+    depth = 0
+    for i, ch in enumerate(n):  # cut at the argument list (the first '(' outside template brackets)
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return n[:i]
+    return n
+
+
+STEP_SEQ = [k for c in ("hash", "probe", "match", "route", "insert") for k in CALL_KERNELS[c]]
+CALL_OF = {k: c for c in CALL_KERNELS for k in CALL_KERNELS[c]}
+
+
+def timed_step_dispatches(rows, steps: int):
+    """rows: (dispatch_id, kernel name, payload) in any order.  Returns the dispatches of the
+    last `steps` occurrences of one whole step (its kernels in launch order), as a list of
+    lists of (name, payload); set-up, warm-up and later measurements are left out."""
+    rows = sorted(rows, key=lambda r: r[0])
+    names = [r[1] for r in rows]
+    L = len(STEP_SEQ)
+    starts = [i for i in range(len(rows) - L + 1) if names[i:i + L] == STEP_SEQ]
+    if len(starts) < steps:
+        raise SystemExit(f"found {len(starts)} whole steps in the trace, expected {steps}")
+    return [[(names[j], rows[j][2]) for j in range(i, i + L)] for i in starts[-steps:]]
+
+
+def summarize_trace(csv_path: str, steps: int):
+    """Markdown summary of a rocprofv3 --kernel-trace CSV: per-kernel durations over the
+    timed steps of one bench.py run."""
+    import csv
+    rows = [(int(r["Dispatch_Id"]), _kname(r["Kernel_Name"]),
+             (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3) for r in csv.DictReader(open(csv_path))]
+    st = timed_step_dispatches(rows, steps)
+    out = ["| call | kernel | mean µs | min µs | max µs |", "|---|---|---|---|---|"]
+    per_call = {}
+    for j, k in enumerate(STEP_SEQ):
+        d = [s[j][1] for s in st]
+        out.append(f"| {CALL_OF[k]} | {k} | {np.mean(d):.1f} | {min(d):.1f} | {max(d):.1f} |")
+        per_call[CALL_OF[k]] = per_call.get(CALL_OF[k], 0.0) + float(np.mean(d))
+    out += ["", "| call | sum of kernel means µs |", "|---|---|"]
+    out += [f"| {c} | {v:.1f} |" for c, v in per_call.items()]
+    return "\n".join(out)
+
+
+def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int):
+    """HBM traffic per timed call from two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE,
+    KiB per dispatch), each scaled by what the counter reads for the 1 GiB device copy that
+    --calibrate-copy issues after the timed steps (the largest copy kernel of each run)."""
+    import csv
+
+    def load(path, counter):
+        rows, copies = [], []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            n, v = _kname(r["Kernel_Name"]), float(r["Counter_Value"]) * 1024.0
+            rows.append((int(r["Dispatch_Id"]), n, v))
+            if "copyBuffer" in n:
+                copies.append((int(r["Dispatch_Id"]), v))
+        return rows, max(v for _, v in copies) if copies else 0.0  # the largest copy: the calibration
+
+    fr, fcopy = load(fetch_csv, "FETCH_SIZE")
+    wr, wcopy = load(write_csv, "WRITE_SIZE")
+    if fcopy <= 0 or wcopy <= 0:
+        raise SystemExit("no calibration copy in the counter runs (run bench.py with --calibrate-copy)")
+    kf, kw = copy_bytes / fcopy, copy_bytes / wcopy
+    fs, ws = timed_step_dispatches(fr, steps), timed_step_dispatches(wr, steps)
+    res = {"sources_sha256_16": kernel_sources_hash(), "fetch_scale": round(kf, 4), "write_scale": round(kw, 4),
+           "kernels": {}}
+    out = [f"Copy calibration: FETCH_SIZE x {kf:.3f}, WRITE_SIZE x {kw:.3f} = bytes of a {copy_bytes >> 20} MiB copy.",
+           "", "| call | kernel | fetched MB | written MB | traffic MB |", "|---|---|---|---|---|"]
+    for j, k in enumerate(STEP_SEQ):
+        f = float(np.mean([s[j][1] for s in fs])) * kf
+        w = float(np.mean([s[j][1] for s in ws])) * kw
+        res["kernels"][k] = round(f + w)
+        res[CALL_OF[k]] = res.get(CALL_OF[k], 0) + round(f + w)
+        out.append(f"| {CALL_OF[k]} | {k} | {f / 1e6:.1f} | {w / 1e6:.1f} | {(f + w) / 1e6:.1f} |")
+    out += ["", "| call | traffic MB per launch |", "|---|---|"]
+    out += [f"| {c} | {res[c] / 1e6:.1f} |" for c in ("hash", "probe", "match", "route", "insert")]
+    return res, "\n".join(out)
 
 
 def kernel_sources_hash() -> str:
@@ -497,8 +592,20 @@ def variants_parity(setup, inputs) -> dict:
     return res
 
 
+COPY_BYTES = 1 << 30
+
+
 def main():
     args = parse()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.steps))
+        return
+    if args.summarize_pmc:
+        res, md = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.steps, COPY_BYTES)
+        with open(args.traffic, "w") as f:
+            json.dump(res, f, indent=1)
+        print(md)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU: the matching/routing path is "
                                    "not sharded across GPUs in this build (pass --gpus 1)"}))
@@ -605,6 +712,13 @@ def main():
         "roofline": roof,
         "roofline_insert": insert,
     }
+    if args.calibrate_copy:  # a device copy of known size, for the HBM counters' scale
+        src = torch.ones(COPY_BYTES, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     variants, var_inputs = measure_variants(setup, last)
     out["variants"] = variants
     out["evict"] = measure_evict(setup)

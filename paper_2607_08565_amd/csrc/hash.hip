@@ -15,8 +15,8 @@
 //    permutes) yields the block digest.
 //  * other even B: one wavefront per request; lane l digests block l of the tile.
 //  Digests go through LDS so that lane l then owns block l of the tile; the chain is an
-//  inclusive scan of affine maps x -> M x + e_l across the wavefront (Kogge-Stone with
-//  the uniform multipliers M^1..M^32).  A tile's carry-in composes the affine maps of
+//  inclusive scan of affine maps x -> M x + e_l across the wavefront, done with DPP moves
+//  (row shifts, then the row broadcasts) and per-lane powers of M.  A tile's carry-in composes the affine maps of
 //  the tiles before it.  Because the chain is affine, this equals the sequential
 //  definition exactly.
 #include "common.h"
@@ -37,12 +37,6 @@ __device__ __forceinline__ uint64_t splitmix_out(uint64_t seed, uint64_t t) {
   return finalise(seed + (t + 1) * GOLDEN);
 }
 
-__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int d) {
-  int lo = __shfl_up(int(uint32_t(v)), d, 64);
-  int hi = __shfl_up(int(uint32_t(v >> 32)), d, 64);
-  return (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo);
-}
-
 template <int CTRL>
 __device__ __forceinline__ uint64_t dpp64(uint64_t v) {
   int lo = __builtin_amdgcn_mov_dpp(int(uint32_t(v)), CTRL, 0xF, 0xF, false);
@@ -61,7 +55,17 @@ struct ChainConsts {
   uint64_t s_init;
   uint64_t Mpow[6];  // M^1, M^2, M^4, ..., M^32
   uint64_t Mlane;    // M^(lane+1)
+  uint64_t Mrow;     // M^(lane % 16 + 1): joins a row to the last lane of the row before
+  uint64_t Mhalf;    // M^(lane - 31) for lanes 32..63: joins them to lane 31
 };
+
+__device__ __forceinline__ uint64_t mpow(const uint64_t Mpow[6], uint32_t e) {
+  uint64_t r = 1;
+#pragma unroll
+  for (int k = 0; k < 6; ++k)
+    if ((e >> k) & 1) r *= Mpow[k];
+  return r;
+}
 
 __device__ ChainConsts chain_consts(uint64_t seed, int B) {
   ChainConsts c;
@@ -72,16 +76,35 @@ __device__ ChainConsts chain_consts(uint64_t seed, int B) {
     c.Mpow[k] = p;
     p *= p;
   }
-  // M^(lane+1) by binary exponentiation
-  uint32_t e = (threadIdx.x & 63) + 1;
-  uint64_t r = 1, b = c.M;
-  while (e) {
-    if (e & 1) r *= b;
-    b *= b;
-    e >>= 1;
-  }
-  c.Mlane = r;
+  // per-lane powers by binary exponentiation (exponents 1..64)
+  const uint32_t lane = threadIdx.x & 63;
+  c.Mlane = lane == 63 ? c.Mpow[5] * c.Mpow[5] : mpow(c.Mpow, lane + 1);
+  c.Mrow = mpow(c.Mpow, (lane & 15) + 1);
+  c.Mhalf = mpow(c.Mpow, lane >= 32 ? lane - 31 : 1);
   return c;
+}
+
+// DPP move of a 64-bit value (both halves with the same control); lanes the control
+// gives no source, and rows outside ROW_MASK, read 0.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ uint64_t dpp_take64(uint64_t v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, int(uint32_t(v)), CTRL, ROW_MASK, 0xF, true);
+  const int hi = __builtin_amdgcn_update_dpp(0, int(uint32_t(v >> 32)), CTRL, ROW_MASK, 0xF, true);
+  return (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo);
+}
+
+// Inclusive scan of the affine maps x -> M x + v_l across the wavefront, in DPP only:
+// returns sum_{k <= l} M^(l-k) v_k.  Distances 1, 2, 4, 8 inside each row of 16 lanes
+// (row_shr), then rows 1 and 3 take the last lane of the row before (row_bcast:15), then
+// lanes 32..63 take lane 31 (row_bcast:31).
+__device__ __forceinline__ uint64_t affine_scan64(uint64_t v, const ChainConsts &cc) {
+  v += cc.Mpow[0] * dpp_take64<0x111>(v);  // row_shr:1
+  v += cc.Mpow[1] * dpp_take64<0x112>(v);  // row_shr:2
+  v += cc.Mpow[2] * dpp_take64<0x114>(v);  // row_shr:4
+  v += cc.Mpow[3] * dpp_take64<0x118>(v);  // row_shr:8
+  v += cc.Mrow * dpp_take64<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+  v += cc.Mhalf * dpp_take64<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+  return v;
 }
 
 // Given lane l's block digest for block j = j0 + l (valid when l < n_valid), finish the
@@ -91,13 +114,7 @@ __device__ __forceinline__ uint64_t finish_tile(uint64_t d, int64_t j0, int n_va
                                                 const ChainConsts &cc, uint64_t *out) {
   const int lane = threadIdx.x & 63;
   const int64_t j = j0 + lane;
-  uint64_t v = lane < n_valid ? finalise(d + uint64_t(j)) : 0;
-#pragma unroll
-  for (int k = 0; k < 6; ++k) {
-    const int dist = 1 << k;
-    uint64_t t = shfl_up64(v, dist);
-    if (lane >= dist) v += cc.Mpow[k] * t;
-  }
+  const uint64_t v = affine_scan64(lane < n_valid ? finalise(d + uint64_t(j)) : 0, cc);
   const uint64_t s = cc.Mlane * carry + v;  // s_j = M^(l+1) carry + sum_k M^(l-k) e_k
   if (lane < n_valid) out[lane] = remap(finalise(s));
   return uint64_t(__shfl(int64_t(s), 63, 64));
@@ -123,7 +140,7 @@ constexpr int WAVES = 1;  // wavefronts per workgroup of the generic kernel
 // advanced through the aggregates of the tiles before its own (x -> M^64 x + agg, as
 // every tile before the request's last is full).  Each wavefront loads its next tile's
 // tokens before working on the current one.
-constexpr int NW = 4;
+constexpr int HASH_NW = 8;  // wavefronts per request of the B = 16 kernel
 
 struct Tile16 {
   int4 v[4];
@@ -139,6 +156,7 @@ __device__ __forceinline__ void load_tile16(const int32_t *x, int64_t tile, int6
   }
 }
 
+template <int NW>
 __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restrict__ tokens,
                                                          int64_t n_tokens,
                                                          const int64_t *__restrict__ tok_off,
@@ -187,13 +205,7 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     // local inclusive scan of the tile's affine maps from state 0
-    uint64_t v = lane < n_valid ? finalise(dig[wave][lane] + uint64_t(j0 + lane)) : 0;
-#pragma unroll
-    for (int k = 0; k < 6; ++k) {
-      const int dist = 1 << k;
-      const uint64_t t = shfl_up64(v, dist);
-      if (lane >= dist) v += cc.Mpow[k] * t;
-    }
+    const uint64_t v = affine_scan64(lane < n_valid ? finalise(dig[wave][lane] + uint64_t(j0 + lane)) : 0, cc);
     if (lane == 63) agg[wave] = v;
     __syncthreads();
     uint64_t c = carry;
@@ -256,7 +268,7 @@ extern "C" int smetric_hash_blocks(const int32_t *tokens, int64_t n_tokens, cons
     return SMETRIC_EINVAL;
   const dim3 grid((n_req + WAVES - 1) / WAVES), block(64 * WAVES);
   if (block_size == 16)
-    hipLaunchKernelGGL(hash16_kernel, dim3(n_req), dim3(64 * NW), 0, stream, tokens, n_tokens, tok_off, blk_off,
+    hipLaunchKernelGGL(hash16_kernel<HASH_NW>, dim3(n_req), dim3(64 * HASH_NW), 0, stream, tokens, n_tokens, tok_off, blk_off,
                        n_req, n_blocks, seed, keys, status);
   else
     hipLaunchKernelGGL(hash_generic_kernel, grid, block, 0, stream, tokens, n_tokens, tok_off,
