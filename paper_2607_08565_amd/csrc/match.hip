@@ -155,6 +155,12 @@ __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
   return (uint64_t(hi) << 32) | lo;
 }
 
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int mask) {
+  const uint32_t lo = uint32_t(__shfl_xor(int(uint32_t(v)), mask, 64));
+  const uint32_t hi = uint32_t(__shfl_xor(int(uint32_t(v >> 32)), mask, 64));
+  return (uint64_t(hi) << 32) | lo;
+}
+
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
@@ -345,6 +351,19 @@ __global__ __launch_bounds__(64 * MW) void match_kernel(DevIndex ix, const uint6
           }
         }
         const int nblk = GQ * bpl < 64 - jj ? GQ * bpl : 64 - jj;
+        // the group's blocks at once: lane (sub, wl) ANDs its words over the loads, the lane
+        // groups then combine theirs, so every lane holds word wl of the intersection of the
+        // group's blocks in this chunk (one past the request's end reads as empty, so the
+        // survivors are written below); if every alive instance holds them all, nobody drops
+        // here and the block-by-block AND is skipped
+        uint64_t all = ~uint64_t(0);
+#pragma unroll
+        for (int q = 0; q < GQ; ++q) all &= jj + q * bpl + sub < 64 ? hq[q] : ~uint64_t(0);
+        for (int d = lpb; d < 64; d <<= 1) all &= shfl_xor64(all, d);
+        if (!__ballot((A[0] & ~all) != 0)) {
+          jj += nblk;
+          continue;
+        }
 #pragma unroll
         for (int q = 0; q < GQ; ++q) {
           for (int s2 = 0; s2 < bpl; ++s2) {
