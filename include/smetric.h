@@ -200,6 +200,21 @@ int smetric_probe_partition(const smetric_index *idx, const uint64_t *keys, cons
                             hipStream_t stream);
 int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes, int64_t n_blocks,
                          hipStream_t stream);
+
+/* smetric_hash_partition: smetric_hash_blocks (the block keys, Sec. 3.1 and App. A)
+ * followed by smetric_probe_partition on the keys it writes, in one call; for
+ * block_size = 16 the hash kernel takes the partition's region counts itself, so the keys
+ * are not read back for counting.  Arguments are those of the two calls (tokens, tok_off,
+ * blk_off, keys, status as in smetric_hash_blocks; idx, probe, probe_bytes as in
+ * smetric_probe_partition); afterwards `keys` holds the block keys and the probe state is
+ * ready for smetric_probe_lookup, exactly as after the two calls.  A request whose token
+ * range does not match its block range sets status EINVAL, as in smetric_hash_blocks,
+ * and (block_size 16) also marks the probe state invalid, so its consumers report EINVAL.
+ * Host errors: those of the two calls. */
+int smetric_hash_partition(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_off,
+                           const int64_t *blk_off, int32_t n_req, int64_t n_blocks, int32_t block_size,
+                           uint64_t seed, uint64_t *keys, int32_t *status, const smetric_index *idx,
+                           void *probe, uint64_t probe_bytes, hipStream_t stream);
 int smetric_match_probed(const smetric_index *idx, const void *probe, uint64_t probe_bytes,
                          const uint64_t *keys, const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
                          int32_t *matched, hipStream_t stream);

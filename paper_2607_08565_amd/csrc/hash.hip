@@ -156,7 +156,11 @@ __device__ __forceinline__ void load_tile16(const int32_t *x, int64_t tile, int6
   }
 }
 
-template <int NW>
+// COUNT: also the region partition's count pass -- every key adds one to its (partition
+// chunk, table region) cell of `hist` (chunks of clen blocks, as the partition cuts them);
+// a request's blocks meet at most two chunks unless it is longer than a chunk, so they are
+// counted in LDS and added with one atomic per nonzero cell (the rare rest directly).
+template <int NW, bool COUNT>
 __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restrict__ tokens,
                                                          int64_t n_tokens,
                                                          const int64_t *__restrict__ tok_off,
@@ -164,14 +168,20 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
                                                          int32_t n_req, int64_t n_blocks,
                                                          uint64_t seed,
                                                          uint64_t *__restrict__ keys,
-                                                         int32_t *status) {
+                                                         int32_t *status,
+                                                         uint32_t *__restrict__ hist, uint64_t n_buckets,
+                                                         uint64_t clen, int *probe_err) {
   __shared__ uint64_t dig[NW][64];
   __shared__ uint64_t agg[NW];
+  __shared__ unsigned int lh[COUNT ? 2 * NREG : 1];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x;
   int64_t t0, b0, nb;
   if (!request_ok(tok_off, blk_off, r, n_tokens, n_blocks, 16, t0, b0, nb)) {
     if (threadIdx.x == 0 && status) atomicCAS(status, 0, SMETRIC_EINVAL);
+    // counting: this request's blocks are neither written nor counted, so the partition
+    // must not run on the counts (it would place more blocks than it reserved)
+    if (COUNT && threadIdx.x == 0) atomicCAS(probe_err, 0, SMETRIC_EINVAL);
     return;  // the whole workgroup leaves before any barrier
   }
   const ChainConsts cc = chain_consts(seed, 16);
@@ -185,6 +195,8 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
   const int32_t *x = tokens + t0;
   const int64_t n_tiles = (nb + 63) / 64;
   uint64_t carry = cc.s_init;  // chain state before the step's first block
+  const uint64_t c_lo = COUNT ? uint64_t(b0) / clen : 0, B1 = (c_lo + 1) * clen, B2 = B1 + clen;
+  if (COUNT && threadIdx.x < 2 * NREG) lh[threadIdx.x] = 0;  // first used after the step's barrier
   Tile16 cur, nxt;
   load_tile16(x, wave, nb, q, lane, cur);
   for (int64_t step0 = 0; step0 < n_tiles; step0 += NW) {
@@ -210,13 +222,26 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
     __syncthreads();
     uint64_t c = carry;
     for (int w = 0; w < wave; ++w) c = M64 * c + agg[w];
-    if (lane < n_valid) keys[b0 + j0 + lane] = remap(finalise(cc.Mlane * c + v));
+    if (lane < n_valid) {
+      const uint64_t key = remap(finalise(cc.Mlane * c + v));
+      keys[b0 + j0 + lane] = key;
+      if (COUNT) {
+        const uint64_t b = uint64_t(b0 + j0 + lane);
+        const uint32_t g = region_of(key, n_buckets);
+        if (b < B2) atomicAdd(&lh[(b >= B1 ? NREG : 0) + g], 1u);
+        else atomicAdd(&hist[(b / clen) * NREG + g], 1u);
+      }
+    }
     uint64_t next = carry;
 #pragma unroll
     for (int w = 0; w < NW; ++w) next = M64 * next + agg[w];
     carry = next;  // used only when every tile of this step was full
     __syncthreads();
     cur = nxt;
+  }
+  if (COUNT && threadIdx.x < 2 * NREG) {  // the loop ended on a barrier: lh is complete
+    const unsigned int v = lh[threadIdx.x];
+    if (v) atomicAdd(&hist[(c_lo + threadIdx.x / NREG) * NREG + threadIdx.x % NREG], v);
   }
 }
 
@@ -268,12 +293,36 @@ extern "C" int smetric_hash_blocks(const int32_t *tokens, int64_t n_tokens, cons
     return SMETRIC_EINVAL;
   const dim3 grid((n_req + WAVES - 1) / WAVES), block(64 * WAVES);
   if (block_size == 16)
-    hipLaunchKernelGGL(hash16_kernel<HASH_NW>, dim3(n_req), dim3(64 * HASH_NW), 0, stream, tokens, n_tokens, tok_off, blk_off,
-                       n_req, n_blocks, seed, keys, status);
+    hipLaunchKernelGGL((hash16_kernel<HASH_NW, false>), dim3(n_req), dim3(64 * HASH_NW), 0, stream, tokens, n_tokens, tok_off, blk_off,
+                       n_req, n_blocks, seed, keys, status, static_cast<uint32_t *>(nullptr), uint64_t(0), uint64_t(1),
+                       static_cast<int *>(nullptr));
   else
     hipLaunchKernelGGL(hash_generic_kernel, grid, block, 0, stream, tokens, n_tokens, tok_off,
                        blk_off, n_req, n_blocks, int(block_size), seed, keys, status);
   return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_hash_partition(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_off,
+                                      const int64_t *blk_off, int32_t n_req, int64_t n_blocks, int32_t block_size,
+                                      uint64_t seed, uint64_t *keys, int32_t *status, const smetric_index *idx,
+                                      void *probe, uint64_t probe_bytes, hipStream_t stream) {
+  if (n_req < 0 || n_tokens < 0 || n_blocks < 0 || block_size < 2 || block_size > 256 || (block_size & 1))
+    return SMETRIC_EINVAL;
+  if (n_req > 0 && (!tok_off || (n_tokens > 0 && !tokens))) return SMETRIC_EINVAL;
+  if (int rc = probe_state_args(idx, keys, blk_off, n_req, n_blocks, probe, probe_bytes)) return rc;
+  ProbeView pv;
+  probe_layout(n_blocks, &pv, probe);
+  const DevIndex ix = dev_view(idx);  // geometry only
+  const bool counted = block_size == 16 && n_req > 0;
+  partition_head(pv, blk_off, n_req, n_blocks, counted, stream);
+  if (counted)
+    hipLaunchKernelGGL((hash16_kernel<HASH_NW, true>), dim3(n_req), dim3(64 * HASH_NW), 0, stream, tokens, n_tokens,
+                       tok_off, blk_off, n_req, n_blocks, seed, keys, status, pv.hist, ix.n_buckets,
+                       partition_chunk(uint64_t(n_blocks)), &pv.hdr->err);
+  else if (n_req > 0)
+    hipLaunchKernelGGL(hash_generic_kernel, dim3((n_req + WAVES - 1) / WAVES), dim3(64 * WAVES), 0, stream, tokens,
+                       n_tokens, tok_off, blk_off, n_req, n_blocks, int(block_size), seed, keys, status);
+  return partition_tail(ix, pv, keys, uint64_t(n_blocks), counted, stream);
 }
 
 extern "C" int smetric_block_offsets(const int64_t *tok_off, int32_t n_req, int32_t block_size,

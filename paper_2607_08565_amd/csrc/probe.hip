@@ -110,22 +110,20 @@ __global__ __launch_bounds__(TB) void part_count_kernel(DevIndex ix, ProbeView p
   }
   if (bad) atomicOr(&pv.hdr->bad_key, 1);
   __syncthreads();
-  for (int g = threadIdx.x; g < NREG; g += TB) {
-    const unsigned int c = h[g];
-    pv.hist[uint64_t(blockIdx.x) * NREG + g] = c;
-    if (c) atomicAdd(&pv.hdr->tot[g], (unsigned long long)c);
-  }
+  for (int g = threadIdx.x; g < NREG; g += TB) pv.hist[uint64_t(blockIdx.x) * NREG + g] = h[g];
 }
 
-// Workgroup g: first position of region g (sum of the totals before it), then the
-// running offsets of its chunks.
+// Workgroup g: first position of region g (the blocks of every region before it, summed
+// over all chunks), then the running offsets of its chunks, and its own total.
 static_assert(PART_WG == 4 * TB, "each thread of the scan covers 4 chunks");
 __global__ __launch_bounds__(TB) void part_scan_kernel(ProbeView pv) {
   __shared__ uint32_t wt[TB / 64];
   __shared__ unsigned long long red[TB / 64];
   const int g = blockIdx.x, t = threadIdx.x;
   unsigned long long v = 0;
-  for (int i = t; i < g; i += TB) v += pv.hdr->tot[i];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    for (int i = 0; i < g; ++i) v += pv.hist[uint64_t(4 * t + j) * NREG + i];
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
   if ((t & 63) == 0) red[t >> 6] = v;
@@ -143,6 +141,7 @@ __global__ __launch_bounds__(TB) void part_scan_kernel(ProbeView pv) {
     pv.base[uint64_t(4 * t + j) * NREG + g] = off + acc;
     acc += c[j];
   }
+  if (t == 0) pv.hdr->tot[g] = total;
   if (g == NREG - 1 && t == 0) pv.hdr->n = pv.hdr->err ? 0 : off + total;
 }
 
@@ -333,6 +332,32 @@ int probe_args(const smetric_index *idx, const uint64_t *keys, const int64_t *bl
 }
 }  // namespace
 
+namespace smk {
+int probe_state_args(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                     int64_t n_blocks, void *probe, uint64_t probe_bytes) {
+  return probe_args(idx, keys, blk_off, n_req, n_blocks, probe, probe_bytes);
+}
+
+void partition_head(ProbeView &pv, const int64_t *blk_off, int32_t n_req, int64_t n_blocks, bool clear_hist,
+                    hipStream_t stream) {
+  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hdr),
+                     uint64_t(sizeof(ProbeHdr) / 8));
+  if (clear_hist)
+    hipLaunchKernelGGL(zero_kernel, dim3(16), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hist),
+                       uint64_t(PART_WG) * NREG / 2);
+  if (n_req > 0)
+    hipLaunchKernelGGL(req_of_kernel, dim3(n_req), dim3(64), 0, stream, pv, blk_off, n_req, n_blocks);
+}
+
+int partition_tail(const DevIndex &ix, ProbeView &pv, const uint64_t *keys, uint64_t n, bool counted,
+                   hipStream_t stream) {
+  if (!counted) hipLaunchKernelGGL(part_count_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
+  hipLaunchKernelGGL(part_scan_kernel, dim3(NREG), dim3(TB), 0, stream, pv);
+  hipLaunchKernelGGL(part_scatter_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
+  return hip_rc(hipGetLastError());
+}
+}  // namespace smk
+
 extern "C" int smetric_probe_partition(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
                                        int32_t n_req, int64_t n_blocks, void *probe, uint64_t probe_bytes,
                                        hipStream_t stream) {
@@ -340,15 +365,8 @@ extern "C" int smetric_probe_partition(const smetric_index *idx, const uint64_t 
   ProbeView pv;
   probe_layout(n_blocks, &pv, probe);
   const DevIndex ix = dev_view(idx);  // geometry only: the table's contents are not read here
-  const uint64_t n = uint64_t(n_blocks);
-  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hdr),
-                     uint64_t(sizeof(ProbeHdr) / 8));
-  if (n_req > 0)
-    hipLaunchKernelGGL(req_of_kernel, dim3(n_req), dim3(64), 0, stream, pv, blk_off, n_req, n_blocks);
-  hipLaunchKernelGGL(part_count_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
-  hipLaunchKernelGGL(part_scan_kernel, dim3(NREG), dim3(TB), 0, stream, pv);
-  hipLaunchKernelGGL(part_scatter_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
-  return hip_rc(hipGetLastError());
+  partition_head(pv, blk_off, n_req, n_blocks, false, stream);
+  return partition_tail(ix, pv, keys, uint64_t(n_blocks), false, stream);
 }
 
 extern "C" int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes, int64_t n_blocks,

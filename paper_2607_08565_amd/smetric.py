@@ -78,6 +78,7 @@ def _load() -> C.CDLL:
         "smetric_probe": [PIX, P, P, I32, I64, P, U64, P],
         "smetric_probe_partition": [PIX, P, P, I32, I64, P, U64, P],
         "smetric_probe_lookup": [PIX, P, U64, I64, P],
+        "smetric_hash_partition": [P, I64, P, P, I32, I64, I32, U64, P, P, PIX, P, U64, P],
         "smetric_match_probed": [PIX, P, U64, P, P, I32, I64, P, P],
         "smetric_index_insert_probed": [PIX, P, U64, I32, I64, P, P, U32, P, U64, P],
     }
@@ -97,7 +98,7 @@ EXPORTED = (
     "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
     "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq", "smetric_sessions_ws_bytes",
     "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
-    "smetric_probe_partition", "smetric_probe_lookup",
+    "smetric_probe_partition", "smetric_probe_lookup", "smetric_hash_partition",
 )
 
 
@@ -381,6 +382,23 @@ class Index:
             self.ref, _dev(keys, torch.uint64, "keys"), _dev(blk_off, torch.int64, "blk_off"), R, n_blocks,
             C.c_void_p(state.data_ptr()), state.numel(), _stream()))
         return state
+
+    def hash_partition(self, tokens: torch.Tensor, tok_off: torch.Tensor, blk_off: torch.Tensor, n_blocks: int,
+                       block_size: int = BLOCK, seed: int = DEFAULT_SEED, keys: torch.Tensor | None = None,
+                       status: torch.Tensor | None = None, state: torch.Tensor | None = None):
+        """hash_blocks + probe_partition in one call; returns (keys, probe state)."""
+        R = tok_off.numel() - 1
+        if keys is None:
+            keys = torch.empty(max(n_blocks, 1), dtype=torch.uint64, device=tokens.device)
+        need = probe_ws_bytes(n_blocks)
+        if state is None or state.numel() < need:
+            state = torch.empty(need, dtype=torch.uint8, device=tokens.device)
+        _check("smetric_hash_partition", _lib.smetric_hash_partition(
+            _dev(tokens, torch.int32, "tokens"), tokens.numel(), _dev(tok_off, torch.int64, "tok_off"),
+            _dev(blk_off, torch.int64, "blk_off"), R, n_blocks, block_size, C.c_uint64(seed),
+            _dev(keys, torch.uint64, "keys"), _dev(status, torch.int32, "status") if status is not None else None,
+            self.ref, C.c_void_p(state.data_ptr()), state.numel(), _stream()))
+        return keys, state
 
     def probe_lookup(self, state: torch.Tensor, n_blocks: int):
         """Second half of probe(): reads the index."""

@@ -333,6 +333,66 @@ def test_probed_insert_errors_and_two_pass_refresh():
     big.compare_index("refresh pass after an invalid empty request")
 
 
+@pytest.mark.parametrize("B", [16, 8])
+def test_hash_partition_equals_the_separate_calls(B):
+    """smetric_hash_partition (the hash taking the partition's region counts itself for
+    B = 16) leaves the same keys and probe state as hash + partition: every block key,
+    matched row, decision and the index after the insert equal the oracle's."""
+    rng = np.random.default_rng(30 + B)
+    I = 64
+    pair = Pair(2_000_000, I, block=B)
+    pre = rng.integers(0, W.VOCAB, 64 * B * 3, dtype=np.int32)
+    prompts = [np.concatenate([pre[: int(rng.integers(0, len(pre)))],
+                               rng.integers(0, W.VOCAB, int(rng.integers(0, 70 * B)), dtype=np.int32)])
+               for _ in range(300)]
+    off = np.zeros(301, np.int64)
+    off[1:] = np.cumsum([len(x) for x in prompts])
+    toks = np.concatenate(prompts)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)  # warm the index with half of them
+    half = 150
+    hb = blk_off[: half + 1]
+    assert pair.insert_both(d_keys, to_dev(hb), int(hb[-1]), okeys, hb, rng.integers(0, I, half).astype(np.int32),
+                            np.arange(half), 1) == 0
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(off), d_boff, nb, block_size=B, seed=pair.seed,
+                                          status=status)
+    assert int(status.item()) == 0
+    assert np.array_equal(keys[:nb].cpu().numpy(), okeys), "keys"
+    pair.gix.probe_lookup(state, nb)
+    gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
+    om = pair.oix.match(okeys, blk_off)
+    assert np.array_equal(gm, om), "matched rows"
+    R = len(prompts)
+    inst = rng.integers(0, I, R).astype(np.int32)
+    pair.gix.insert_probed(state, R, nb, to_dev(inst), to_dev(np.arange(R, dtype=np.uint32) + 500), 2)
+    assert pair.oix.insert(okeys, blk_off, inst, np.arange(R) + 500, 2) == 0
+    pair.compare_index(f"hash_partition B={B}")
+
+
+def test_hash_partition_bad_token_range_invalidates_the_state():
+    """A request whose token range does not give its block count: the hash flags status,
+    the counting hash marks the probe state invalid, and the consumers report EINVAL
+    without touching anything out of bounds."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(33)
+    pair = Pair(10_000, 4)
+    toks = rng.integers(0, W.VOCAB, 16 * 40, dtype=np.int32)
+    tok_off = np.array([0, 16 * 10, 16 * 25, 16 * 40], np.int64)
+    blk_off = np.array([0, 10, 27, 40], np.int64)  # request 1 claims 17 blocks of a 15-block range
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    d_boff = to_dev(blk_off)
+    keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(tok_off), d_boff, 40, status=status)
+    assert int(status.item()) == S.EINVAL
+    pair.gix.probe_lookup(state, 40)
+    m = pair.gix.match_probed(state, keys, d_boff, 40).cpu().numpy()
+    assert not m.any()
+    _, st = pair.gix.stats(reset_status=True)
+    assert st == S.EINVAL
+    pair.gix.insert_probed(state, 3, 40, to_dev(np.array([0, 1, 2], np.int32)), to_dev(np.array([1, 2, 3], np.uint32)), 1)
+    n, st = pair.gix.stats()
+    assert n == 0 and st == S.EINVAL
+
+
 def test_match_bad_range_and_empty_requests():
     rng = np.random.default_rng(10)
     pair = Pair(10_000, 5)
