@@ -107,6 +107,7 @@ class SessionWorkload:
         self.streams = streams      # per-session token stream, length >= lens[-1, s]
         self.load = load            # "uniform100", "poisson50", "prev_counts"
         self.placement = placement  # optional int32[n_turns, n_sess]: open-loop placement of turn t
+        self.prefix_of = None       # optional int64[n_sess]: shared prefix of each session (-1: none)
 
     def batch(self, t: int, prev_targets: np.ndarray | None = None) -> Batch:
         L = self.lens[t]
@@ -158,7 +159,9 @@ def config0(n_sess: int = 64, n_turns: int = 4, n_inst: int = 8, l0: int = 1024,
     prefix_of[_rng(cfg, S_PREFIX).permutation(n_sess)[:n_pref]] = 0
     streams = _streams_with_prefix(cfg, n_sess, lens[-1], prefix_of, [prefix])
     placement = _rng(cfg, S_PLACE).integers(0, n_inst, size=(n_turns, n_sess)).astype(np.int32)
-    return SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "uniform100", placement)
+    wl = SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "uniform100", placement)
+    wl.prefix_of = prefix_of
+    return wl
 
 
 def config1(n_sess: int = 4096, n_turns: int = 10, n_inst: int = 64, l0: int = 4096,
@@ -178,7 +181,9 @@ def config1(n_sess: int = 4096, n_turns: int = 10, n_inst: int = 64, l0: int = 4
     prefixes = [uniform_tokens(rp, prefix_len) for _ in range(n_prefix)]
     prefix_of = zipf_choice(_rng(cfg, S_PREFIX), n_prefix, 1.1, n_sess)
     streams = _streams_with_prefix(cfg, n_sess, lens[-1], prefix_of, prefixes)
-    return SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "poisson50")
+    wl = SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "poisson50")
+    wl.prefix_of = prefix_of
+    return wl
 
 
 def config2(n_sess: int = 1024, n_turns: int = 30, n_inst: int = 256, l0: int = 16384,
@@ -198,7 +203,9 @@ def config2(n_sess: int = 1024, n_turns: int = 30, n_inst: int = 256, l0: int = 
     prefixes = [uniform_tokens(rp, prefix_len) for _ in range(n_prefix)]
     prefix_of = _rng(cfg, S_PREFIX).integers(0, n_prefix, size=n_sess)
     streams = _streams_with_prefix(cfg, n_sess, lens[-1], prefix_of, prefixes)
-    return SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "prev_counts")
+    wl = SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "prev_counts")
+    wl.prefix_of = prefix_of
+    return wl
 
 
 def config3(n_sess: int = 8192, n_turns: int = 8, n_inst: int = 128, prefix_len: int = 32768,
@@ -215,7 +222,22 @@ def config3(n_sess: int = 8192, n_turns: int = 8, n_inst: int = 128, prefix_len:
         lens[t] = lens[t - 1] + app
     prefix = uniform_tokens(_rng(cfg, S_PREFIXTOK), prefix_len)
     streams = _streams_with_prefix(cfg, n_sess, lens[-1], np.zeros(n_sess, np.int64), [prefix])
-    return SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "poisson50")
+    wl = SessionWorkload(cfg, n_inst, n_sess, n_turns, lens, streams, "poisson50")
+    wl.prefix_of = np.zeros(n_sess, np.int64)
+    return wl
+
+
+def open_loop_placement(wl: SessionWorkload) -> np.ndarray:
+    """int32[n_turns, n_sess]: a uniform-random instance for every turn of every session,
+    for running a closed-loop configuration open loop (turn t entered on its placement
+    before batch t + 1), which lets a request's exact index restriction be built without
+    replaying the routing of every earlier batch."""
+    return _rng(wl.cfg, S_PLACE, 1).integers(0, wl.n_inst, size=(wl.n_turns, wl.n_sess)).astype(np.int32)
+
+
+def prefix_blocks(wl_cfg: int) -> int:
+    """Length in blocks of the shared prefix every session of configurations 1-3 starts with."""
+    return {1: 2048, 2: 8192, 3: 32768}[wl_cfg] // BLOCK
 
 
 # ---------------------------------------------------------------------------------------
