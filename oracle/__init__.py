@@ -81,6 +81,8 @@ def _load():
     lib.orc_route_seq.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P, P]
     lib.orc_route_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
                                     P, P]
+    lib.orc_route_seq_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
+                                        P, P, P, P]
     _lib = lib
     return lib
 
@@ -262,6 +264,33 @@ def route_seq(matched, prompt_len, hist_len, turn, q, params: dict, rr_base: int
     if rc != OK:
         raise ValueError(f"orc_route_seq rc={rc}")
     return target[:R], branch[:R], q_out
+
+
+def route_seq_coloc(matched, prompt_len, hist_len, turn, q, slack, n_run, params: dict, rr_base: int = 0):
+    """The rule under PD colocation with requests taken one at a time: each decided by
+    route_coloc on the state the earlier ones left (their prefill queued on their target,
+    one more request there).  Returns (target int32[R], branch uint8[R], q_after int64[I]
+    in ns rounded down, n_after int64[I])."""
+    matched = _arr(matched, np.int32)
+    R, I = matched.shape
+    prompt_len = _arr(prompt_len, np.int32)
+    hist_len = _arr(hist_len, np.int32)
+    turn = _arr(turn, np.int32)
+    q = _arr(q, np.int64)
+    slack = _arr(slack, np.int64)
+    n_run = _arr(n_run, np.int32)
+    p = _Params(**params)
+    target = np.zeros(max(R, 1), np.int32)
+    branch = np.zeros(max(R, 1), np.uint8)
+    q_out = np.zeros(I, np.int64)
+    n_out = np.zeros(I, np.int64)
+    rc = _load().orc_route_seq_coloc(_ptr(matched) if matched.size else None, R, I,
+                                     _ptr(prompt_len) if R else None, _ptr(hist_len) if R else None,
+                                     _ptr(turn) if R else None, _ptr(q), _ptr(slack), _ptr(n_run), C.byref(p),
+                                     C.c_uint64(rr_base), _ptr(target), _ptr(branch), _ptr(q_out), _ptr(n_out))
+    if rc != OK:
+        raise ValueError(f"orc_route_seq_coloc rc={rc}")
+    return target[:R], branch[:R], q_out, n_out
 
 
 def sessions(keys, blk_off, user, turn):

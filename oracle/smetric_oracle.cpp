@@ -724,4 +724,110 @@ int orc_route_coloc(const int32_t *matched, int32_t n_req, int32_t I, const int3
   return ORC_OK;
 }
 
+
+// Route under PD colocation with requests taken one at a time (App. B pseudocode, whose
+// req = receive() handles one request; Sec. 4.2 (a) for what q means).  Request r is
+// decided exactly as orc_route_coloc decides it, on the instance state that the earlier
+// requests of the batch left: after each decision the request's prefill joins its target's
+// queue (q[t] += prefill_cost(req, c[t])) and the request is one more request at the target
+// (n_run[t] += 1).  The TPOT filter's decode slacks are the caller's: the new request has
+// no live decode yet (its decode length is unknown, App. B), so they do not change.
+// Out-of-domain requests (branch 255) change nothing.  q_out (ns, halved and rounded down
+// like orc_route_seq) and n_out receive the final state when non-null.
+int orc_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
+                        const int32_t *hist_len, const int32_t *turn, const int64_t *q, const int64_t *slack,
+                        const int32_t *n_run, const orc_params *p, uint64_t rr_base, int32_t *target,
+                        uint8_t *branch, int64_t *q_out, int64_t *n_out) {
+  typedef __int128 i128;
+  const int64_t LIM32 = int64_t(1) << 32;
+  if (n_req < 0 || I < 1 || I > 65536) return ORC_EINVAL;
+  if (p->c_lin < 0 || p->c_lin > LIM32 || p->c_att < 0 || p->c_att > LIM32 || p->slo_b < 0 ||
+      p->slo_b > LIM32 || p->slo_a < 0 || p->slo_a > LIM32 || p->slack_num < 0 ||
+      p->slack_den < 0 || p->hit_num < 0 || p->hit_den <= 0 || p->hit_num >= p->hit_den ||
+      p->block_size < 2 || p->block_size > 256 || (p->block_size & 1))
+    return ORC_EINVAL;
+  std::vector<i128> q2(I);         // 2 q, exact
+  std::vector<int64_t> n(I);
+  bool inst_ok = true;
+  for (int32_t i = 0; i < I; ++i) {
+    if (q[i] < 0 || q[i] >= (int64_t(1) << 62) || n_run[i] < 0) inst_ok = false;
+    q2[i] = i128(2) * q[i];
+    n[i] = n_run[i];
+  }
+  const int64_t B = p->block_size;
+  for (int32_t r = 0; r < n_req; ++r) {
+    // the batch rule on one request, with the current state (loads kept doubled, so that
+    // the half-token costs of Eq. (1) stay exact; the decision compares 2q + cost2)
+    const int32_t *c = matched + int64_t(r) * I;
+    const int64_t L = prompt_len[r];
+    bool ok = inst_ok && L >= 0 && L <= (int64_t(1) << 24) && hist_len[r] >= 0 && turn[r] >= 0;
+    for (int32_t i = 0; ok && i < I; ++i) ok = c[i] >= 0 && c[i] <= L / B;
+    if (!ok) {
+      target[r] = -1;
+      branch[r] = 255;
+      continue;
+    }
+    auto cost2 = [&](int32_t i) -> i128 {
+      const i128 m = L - B * c[i];
+      return i128(2) * p->c_lin * m + i128(p->c_att) * m * (i128(2) * L - m);
+    };
+    const int64_t NO_DECODE = int64_t(1) << 62;
+    std::vector<bool> in_cand(I);
+    bool any = false;
+    for (int32_t i = 0; i < I; ++i) {
+      in_cand[i] = slack[i] >= NO_DECODE || cost2(i) <= i128(2) * slack[i];
+      any = any || in_cand[i];
+    }
+    if (!any)
+      for (int32_t i = 0; i < I; ++i) in_cand[i] = true;
+    auto est2 = [&](int32_t i) -> i128 { return q2[i] + cost2(i); };
+    const i128 bound2 = i128(2) * (i128(p->slo_b) + i128(p->slo_a) * L);
+    auto meets_ttft = [&](int32_t i) -> bool {
+      if (p->slack_den == 0) return true;
+      return est2(i) * p->slack_den <= i128(p->slack_num) * bound2;
+    };
+    int32_t prev = 0;
+    for (int32_t i = 1; i < I; ++i)
+      if (c[i] > c[prev]) prev = i;
+    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    int32_t best = -1;
+    for (int32_t k = 0; k < I; ++k) {
+      const int32_t i = (start + k) % I;
+      if (!in_cand[i]) continue;
+      if (best < 0 || est2(i) * n[i] < est2(best) * n[best]) best = i;  // earlier rotation wins ties
+    }
+    const bool cached = i128(B) * c[prev] * p->hit_den > i128(p->hit_num) * hist_len[r];
+    int32_t t;
+    uint8_t br;
+    if (turn[r] == 0) {
+      t = best;
+      br = 0;
+    } else if (!cached) {
+      t = best;
+      br = 1;
+    } else if (!meets_ttft(prev)) {
+      t = best;
+      br = 4;
+    } else if (!in_cand[prev]) {
+      t = best;
+      br = 5;
+    } else {
+      t = prev;
+      br = 2;
+    }
+    target[r] = t;
+    branch[r] = br;
+    q2[t] += cost2(t);  // the request's prefill joins its target's queue
+    n[t] += 1;          // and it is one more request at the target
+  }
+  if (q_out)
+    for (int32_t i = 0; i < I; ++i) {
+      const i128 v = q2[i] / 2;
+      q_out[i] = v > i128(INT64_MAX) ? INT64_MAX : int64_t(v);
+    }
+  if (n_out)
+    for (int32_t i = 0; i < I; ++i) n_out[i] = n[i];
+  return ORC_OK;
+}
+
 }  // extern "C"
