@@ -81,6 +81,7 @@ def _load():
     lib.orc_route_seq.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, C.POINTER(_Params), C.c_uint64, P, P, P]
     lib.orc_route_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
                                     P, P]
+    lib.orc_test_prod_less.argtypes = [C.c_int64, C.c_uint64, C.c_uint64, C.c_int64, C.c_uint64, C.c_uint64]
     lib.orc_route_seq_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
                                         P, P, P, P]
     _lib = lib
@@ -291,6 +292,12 @@ def route_seq_coloc(matched, prompt_len, hist_len, turn, q, slack, n_run, params
     if rc != OK:
         raise ValueError(f"orc_route_seq_coloc rc={rc}")
     return target[:R], branch[:R], q_out, n_out
+
+
+def test_prod_less(a: int, x: int, b: int, y: int) -> bool:
+    """The oracle's exact a * x < b * y (0 <= a, b < 2^127; 0 <= x, y < 2^64)."""
+    m = (1 << 64) - 1
+    return bool(_load().orc_test_prod_less(a >> 64, a & m, x, b >> 64, b & m, y))
 
 
 def sessions(keys, blk_off, user, turn):

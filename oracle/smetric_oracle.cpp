@@ -734,6 +734,28 @@ int orc_route_coloc(const int32_t *matched, int32_t n_req, int32_t I, const int3
 // no live decode yet (its decode length is unknown, App. B), so they do not change.
 // Out-of-domain requests (branch 255) change nothing.  q_out (ns, halved and rounded down
 // like orc_route_seq) and n_out receive the final state when non-null.
+// a * x < b * y, exactly, for 0 <= a, b < 2^127 and x, y < 2^64: the products (< 2^191) are
+// formed as (high 128 bits, low 64 bits).
+static bool prod_less(__int128 a, uint64_t x, __int128 b, uint64_t y) {
+  typedef unsigned __int128 u128;
+  auto mul = [](u128 v, uint64_t m, u128 &hi, uint64_t &lo) {
+    const u128 p_lo = (v & ~uint64_t(0)) * u128(m), p_hi = (v >> 64) * u128(m);
+    lo = uint64_t(p_lo);
+    hi = p_hi + (p_lo >> 64);
+  };
+  u128 ah, bh;
+  uint64_t al, bl;
+  mul(u128(a), x, ah, al);
+  mul(u128(b), y, bh, bl);
+  return ah < bh || (ah == bh && al < bl);
+}
+
+// Test hook for the comparison above: a and b as (high, low) 64-bit words.
+int orc_test_prod_less(int64_t a_hi, uint64_t a_lo, uint64_t x, int64_t b_hi, uint64_t b_lo, uint64_t y) {
+  const __int128 a = (__int128(a_hi) << 64) | a_lo, b = (__int128(b_hi) << 64) | b_lo;
+  return prod_less(a, x, b, y) ? 1 : 0;
+}
+
 int orc_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
                         const int32_t *hist_len, const int32_t *turn, const int64_t *q, const int64_t *slack,
                         const int32_t *n_run, const orc_params *p, uint64_t rr_base, int32_t *target,
@@ -790,11 +812,13 @@ int orc_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t I, const 
     for (int32_t i = 1; i < I; ++i)
       if (c[i] > c[prev]) prev = i;
     const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    // the loads and counts grow with every request, so the LMetric product is compared in
+    // 192 bits (est2 < 2^113, n < 2^33 over any batch)
     int32_t best = -1;
     for (int32_t k = 0; k < I; ++k) {
       const int32_t i = (start + k) % I;
       if (!in_cand[i]) continue;
-      if (best < 0 || est2(i) * n[i] < est2(best) * n[best]) best = i;  // earlier rotation wins ties
+      if (best < 0 || prod_less(est2(i), uint64_t(n[i]), est2(best), uint64_t(n[best]))) best = i;  // earlier rotation wins ties
     }
     const bool cached = i128(B) * c[prev] * p->hit_den > i128(p->hit_num) * hist_len[r];
     int32_t t;

@@ -116,3 +116,18 @@ def test_out_of_domain_requests_change_nothing():
         qs[t[r]] += cost2(int(L[r]), int(m[r, t[r]])) // 2
         ns[t[r]] += 1
     assert q_after.tolist() == qs and n_after.tolist() == ns
+
+
+def test_score_comparison_is_exact_past_128_bits():
+    """The LMetric product of a running state can pass 2^127 (loads and counts both grow);
+    the oracle compares it in 192 bits: checked against Python integers."""
+    rng = np.random.default_rng(5)
+    for _ in range(2000):
+        a, b = (int(v) for v in rng.integers(0, 2**63, 2, dtype=np.uint64))
+        a = (a << 64) | int(rng.integers(0, 2**63, dtype=np.uint64))
+        b = (b << 64) | int(rng.integers(0, 2**63, dtype=np.uint64))
+        x, y = (int(v) for v in rng.integers(0, 2**63, 2, dtype=np.uint64))
+        if rng.random() < 0.3:
+            b, y = a, x + int(rng.integers(-1, 2))  # near ties
+            y = max(y, 0)
+        assert oracle.test_prod_less(a, x, b, y) == (a * x < b * y)
