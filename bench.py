@@ -513,6 +513,25 @@ def measure_variants(setup, b: int, reps: int = 20):
                         "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist(),
                         "targets_differing_from_batch_snapshot": int((st != snap_t).sum())}
     inputs["route_seq"] = (st, br.cpu().numpy(), q_out.cpu().numpy(), b)
+    # the colocated rule, one request at a time: the queue and the request counts update
+    n_out = torch.empty(I, dtype=torch.int64, device="cuda")
+    call = lambda: S.route_seq_coloc(setup.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], d_slack, d_run,
+                                     W.DEFAULT_PARAMS, tb.batch.rr_base, target=tgt, branch=br, q_out=q_out,
+                                     n_out=n_out, workspace=ws)
+    call()
+    e0.record()
+    for _ in range(seq_reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / seq_reps
+    sc = tgt.cpu().numpy()
+    out["route_seq_coloc"] = {"rule": "PD colocation (App. B), each request sees the queue and request counts "
+                                      "updated by the earlier ones",
+                              "ms": round(ms, 4), "requests_per_s": round(R / (ms / 1e3), 1),
+                              "branches": np.bincount(br.cpu().numpy(), minlength=6).tolist(),
+                              "targets_differing_from_batch_snapshot": int((sc != inputs["route_coloc"][2]).sum())}
+    inputs["route_seq_coloc"] = (sc, br.cpu().numpy(), q_out.cpu().numpy(), n_out.cpu().numpy(), b)
     # the Sec. 5.4 ablation's load-aware filter, load = queued prefill + 100 ms per running request
     load = d["q"] + d_run.to(torch.int64) * 100_000_000
     call = lambda: S.route_loadaware(setup.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], load, (1, 2),
@@ -587,6 +606,13 @@ def variants_parity(setup, inputs) -> dict:
                                   setup.W.DEFAULT_PARAMS, bt.rr_base)
     res["route_seq"] = {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb)
                                                                     and np.array_equal(oq, gq))}
+    gt, gb, gq, gn, b = inputs["route_seq_coloc"]
+    bt = setup.host[b].batch
+    slack, n_run = inputs["route_coloc"][0], inputs["route_coloc"][1]
+    ot, ob, oq, on = oracle.route_seq_coloc(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, bt.turn, bt.q,
+                                            slack, n_run, setup.W.DEFAULT_PARAMS, bt.rr_base)
+    res["route_seq_coloc"] = {"requests": int(len(ot)), "bit_exact": bool(
+        np.array_equal(ot, gt) and np.array_equal(ob, gb) and np.array_equal(oq, gq) and np.array_equal(on, gn))}
     load, gt, gb, b = inputs["route_loadaware"]
     bt = setup.host[b].batch
     ot, ob = oracle.route_loadaware(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, bt.turn, bt.q, load,

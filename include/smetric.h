@@ -14,6 +14,7 @@
  *   smetric_route         the stick / balance / migrate decision          (Sec. 4.2, Eq. (1))
  *   smetric_route_seq     the same decision, requests routed one at a time (Sec. 4.2 (a))
  *   smetric_route_coloc   the same decision under PD colocation           (App. B)
+ *   smetric_route_seq_coloc  colocation, requests routed one at a time    (App. B, Sec. 4.2 (a))
  *   smetric_sessions      session reconstruction from block hashes        (App. A)
  *   smetric_route_loadaware  the Sec. 5.4 ablation's load-aware filter
  *   smetric_imbalance     per-window max / mean load                      (Sec. 4.1)
@@ -346,7 +347,9 @@ int smetric_sessions(const uint64_t *keys, const int64_t *blk_off, int32_t n_req
  *   workspace  >= smetric_route_seq_ws_bytes(n_req) bytes (80 per request), 256-B aligned
  * Other arguments, domains, branches and errors as smetric_route, and n_instances must be
  * <= 4096 (EINVAL otherwise); EWORKSPACE for a short workspace.  Out-of-domain requests
- * (branch 255) add no load.
+ * (branch 255) add no load.  The running loads must stay representable: EINVAL when
+ * (2^63 + (n_req + 1) (2 C_LIN 2^24 + C_ATT 2^48)) max(slack_den, 1) >= 2^126 (the
+ * largest load the batch could reach, times SLACK's denominator in the deadline check).
  * --------------------------------------------------------------------------------- */
 int smetric_route_seq_ws_bytes(int32_t n_req, uint64_t *ws_bytes /* host */);
 int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t n_instances,
@@ -379,6 +382,30 @@ int smetric_route_coloc(const int32_t *matched, int32_t n_req, int32_t n_instanc
                         const int64_t *q, const int64_t *tpot_slack, const int32_t *n_running,
                         const smetric_params *params /* host */, uint64_t rr_base, int32_t *target,
                         uint8_t *branch, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * Route under PD colocation with requests taken one at a time (App. B, whose router
+ * receives one request at a time): request r is decided by smetric_route_coloc's rule on
+ * the state the earlier requests of the batch left -- each routed request's prefill
+ * joins its target's queue and it is one more request there:
+ *   q_r[i] = q[i] + sum over r' < r routed to i of prefill_cost(r', c[r'][i]),
+ *   n_r[i] = n_running[i] + number of r' < r routed to i.
+ * The decode slacks stay as given: the request's own decode is not live yet (its length
+ * is unknown, App. B).  The LMetric scores est2 x n are compared exactly in 192 bits.
+ *   q_out      int64[n_instances] (out, optional: NULL) final loads in ns, rounded down
+ *   n_out      int64[n_instances] (out, optional: NULL) final request counts
+ *   workspace  >= smetric_route_seq_ws_bytes(n_req) bytes, 256-B aligned
+ * Other arguments, domains, branches and errors as smetric_route_coloc; n_instances must
+ * be <= 4096 and the batch's loads representable as for smetric_route_seq (EINVAL
+ * otherwise); EWORKSPACE for a short workspace.  Out-of-domain requests (branch 255)
+ * change nothing.
+ * --------------------------------------------------------------------------------- */
+int smetric_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                            const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                            const int64_t *q, const int64_t *tpot_slack, const int32_t *n_running,
+                            const smetric_params *params /* host */, uint64_t rr_base, int32_t *target,
+                            uint8_t *branch, int64_t *q_out, int64_t *n_out, void *workspace,
+                            uint64_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------
  * Post-route insert: every full block of request r goes on instance[r] (the routed

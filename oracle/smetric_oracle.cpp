@@ -554,6 +554,17 @@ int orc_sessions(const uint64_t *keys, const int64_t *blk_off, int32_t n_req, in
 // instance.  The decision for each request is orc_route's with that q; loads are kept
 // doubled (2q, exact with Eq. (1)'s n/2 term) in 128 bits.  Out-of-domain requests add no
 // load.  q_out (optional) gets the final loads in ns, rounded down.
+// Requests routed one at a time: the running loads grow with the batch, and the deadline
+// check multiplies them by SLACK's denominator.  A batch is in domain only when the largest
+// load it can reach -- 2 q < 2^63 plus (n_req + 1) times the largest doubled cost of a
+// request in domain, 2 C_LIN 2^24 + C_ATT 2^48 -- times the denominator stays below 2^126.
+static bool seq_loads_fit(const orc_params *p, int32_t n_req) {
+  typedef __int128 i128;
+  const i128 cmax = i128(2) * p->c_lin * (int64_t(1) << 24) + i128(p->c_att) * (i128(1) << 48);
+  const i128 worst = (i128(1) << 63) + i128(int64_t(n_req) + 1) * cmax;
+  return worst < (i128(1) << 126) / i128(p->slack_den > 0 ? p->slack_den : 1);
+}
+
 int orc_route_seq(const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
                   const int32_t *hist_len, const int32_t *turn, const int64_t *q, const orc_params *p,
                   uint64_t rr_base, int32_t *target, uint8_t *branch, int64_t *q_out) {
@@ -565,6 +576,7 @@ int orc_route_seq(const int32_t *matched, int32_t n_req, int32_t I, const int32_
       p->slack_den < 0 || p->hit_num < 0 || p->hit_den <= 0 || p->hit_num >= p->hit_den ||
       p->block_size < 2 || p->block_size > 256 || (p->block_size & 1))
     return ORC_EINVAL;
+  if (!seq_loads_fit(p, n_req)) return ORC_EINVAL;
   const int64_t B = p->block_size;
   bool q_ok = true;
   std::vector<i128> q2(I);
@@ -768,6 +780,7 @@ int orc_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t I, const 
       p->slack_den < 0 || p->hit_num < 0 || p->hit_den <= 0 || p->hit_num >= p->hit_den ||
       p->block_size < 2 || p->block_size > 256 || (p->block_size & 1))
     return ORC_EINVAL;
+  if (!seq_loads_fit(p, n_req)) return ORC_EINVAL;
   std::vector<i128> q2(I);         // 2 q, exact
   std::vector<int64_t> n(I);
   bool inst_ok = true;

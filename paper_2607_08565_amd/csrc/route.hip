@@ -27,9 +27,14 @@ struct RouteParams {
   int32_t slack_num, slack_den, hit_num, hit_den, B;
 };
 
+// 2 q + 2 x Eq. (1): for requests in domain n = L - B c and L are at most 2^24, so
+// 2 C_LIN n < 2^58 and n (2L - n) < 2^49 fit 64 bits, and the only wide product is
+// C_ATT x n (2L - n) (64 x 64 -> 128 bits).
 __device__ __forceinline__ i128 est2(const RouteParams &p, int64_t L, int32_t c, int64_t q) {
-  const i128 n = L - int64_t(p.B) * c;
-  return i128(2) * q + i128(2) * p.c_lin * n + i128(p.c_att) * n * (i128(2) * L - n);
+  const uint64_t n = uint64_t(L - int64_t(p.B) * c);
+  const uint64_t w = n * (uint64_t(2 * L) - n);
+  typedef unsigned __int128 u128_;
+  return i128(2) * q + i128(uint64_t(2 * p.c_lin) * n) + i128(u128_(uint64_t(p.c_att)) * w);
 }
 
 __device__ __forceinline__ i128 shfl_xor128(i128 v, int m) {
@@ -629,6 +634,364 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
     }
 }
 
+// ---------------------------------------------------------------------------------
+// Online load update under PD colocation (App. B, whose req = receive() takes one request
+// at a time).  The running state is the queued prefill 2q[i] and the request count n[i];
+// each request is decided by the batch colocation rule on the state the earlier requests
+// left, then its prefill joins the target's queue and it is one more request there.  The
+// decode slacks are the caller's (the request's own decode is not live yet).
+//   prep  one wavefront per request: domain, prev = argmax c, session_cached, follow-up,
+//         whether prev is a candidate (passes the TPOT filter, or no instance does), the
+//         cost on prev and the deadline -- none of it depends on the running state.
+//   seq   ONE wavefront; 2q, n and the slacks in LDS.  A cached follow-up whose prev is a
+//         candidate sticks iff prev meets its deadline, which needs only prev's load: 64
+//         requests are settled per step as in route_seq_kernel (the step's earlier
+//         requests with the same prev add their costs); the first request not settled is
+//         decided alone by a scan of its row for the LMetric minimum over the candidates.
+//         The scores est2 x n are compared in 192 bits: over a batch both factors grow.
+// ---------------------------------------------------------------------------------
+constexpr int SEQC_MAX_I = 4096;  // LDS: 2q (64 KB), n and slack (32 KB each), step counters
+
+struct SeqCRec {
+  int32_t prev;
+  int32_t flags;  // bit 0: in domain (apart from the instance state), 1: session cached,
+                  // 2: follow-up, 3: prev is a candidate
+  int32_t L;
+  int32_t pad;
+  i128 cost_prev;  // 2 x prefill_cost(req, c[prev])
+  i128 bound;      // SLACK_num x 2 (b + a L)
+};
+static_assert(sizeof(SeqCRec) <= sizeof(SeqRec), "the workspace of smetric_route_seq fits both rules");
+
+__device__ __forceinline__ bool tpot_pass(int64_t slack, i128 cost2) {
+  return slack >= NO_DECODE || cost2 <= i128(2) * slack;
+}
+
+__global__ __launch_bounds__(64 * RW) void route_seqc_prep_kernel(const int32_t *__restrict__ matched, int32_t n_req,
+                                                                  int32_t I, const int32_t *__restrict__ prompt_len,
+                                                                  const int32_t *__restrict__ hist_len,
+                                                                  const int32_t *__restrict__ turn,
+                                                                  const int64_t *__restrict__ slack, RouteParams p,
+                                                                  SeqCRec *__restrict__ rec) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * RW + wave;
+  if (r >= n_req) return;
+  const int32_t *c = matched + int64_t(r) * I;
+  const int64_t L = prompt_len[r];
+  const int32_t hist = hist_len[r], tr = turn[r];
+  bool ok = L >= 0 && L <= (int64_t(1) << 24) && hist >= 0 && tr >= 0;
+  const int64_t max_c = ok ? L / p.B : -1;
+  int32_t bc = -1, bi = 0x7FFFFFFF;
+  bool any_pass = false;
+  for (int32_t i = lane; i < I; i += 64) {
+    const int32_t ci = c[i];
+    if (ci < 0 || ci > max_c) ok = false;
+    if (ci > bc) {
+      bc = ci;
+      bi = i;
+    }
+    if (ok && tpot_pass(slack[i], est2(p, L, ci, 0))) any_pass = true;
+  }
+  ok = __ballot(!ok) == 0;
+  any_pass = __ballot(any_pass) != 0;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const int32_t oc = __shfl_xor(bc, m, 64), oi = __shfl_xor(bi, m, 64);
+    if (oc > bc || (oc == bc && oi < bi)) {
+      bc = oc;
+      bi = oi;
+    }
+  }
+  if (lane != 0) return;
+  SeqCRec out;
+  const i128 cost_prev = ok ? est2(p, L, bc, 0) : i128(0);
+  const bool cached = ok && i128(p.B) * bc * p.hit_den > i128(p.hit_num) * hist;
+  const bool prev_cand = ok && (!any_pass || tpot_pass(slack[bi], cost_prev));
+  out.prev = ok ? bi : 0;
+  out.flags = int32_t(ok) | (int32_t(cached) << 1) | (int32_t(tr != 0) << 2) | (int32_t(prev_cand) << 3);
+  out.L = ok ? int32_t(L) : 0;
+  out.pad = 0;
+  out.cost_prev = cost_prev;
+  out.bound = i128(p.slack_num) * (i128(2) * (i128(p.slo_b) + i128(p.slo_a) * (ok ? L : 0)));
+  rec[r] = out;
+}
+
+// a * x for 0 <= a < 2^127, x < 2^64, as (high 128 bits, low 64 bits)
+typedef unsigned __int128 u128;
+struct P192 {
+  u128 hi;
+  uint64_t lo;
+};
+__device__ __forceinline__ P192 mul192(i128 a, uint64_t x) {
+  const u128 ua = u128(a);
+  const u128 p_lo = u128(uint64_t(ua)) * u128(x);
+  const uint64_t a_hi = uint64_t(ua >> 64);
+  if (a_hi == 0) return P192{p_lo >> 64, uint64_t(p_lo)};  // the usual case: a load below 2^64
+  return P192{u128(a_hi) * u128(x) + (p_lo >> 64), uint64_t(p_lo)};
+}
+__device__ __forceinline__ bool less192(const P192 &a, const P192 &b) {
+  return a.hi < b.hi || (a.hi == b.hi && a.lo < b.lo);
+}
+// (score, rotation distance) minimum with 192-bit scores; d = INT_MAX marks "none yet"
+struct MinPD {
+  P192 s;
+  int32_t d;
+};
+__device__ __forceinline__ void min_pd(MinPD &a, const P192 &s, int32_t d) {
+  if (d != 0x7FFFFFFF && (a.d == 0x7FFFFFFF || less192(s, a.s) || (!less192(a.s, s) && d < a.d))) {
+    a.s = s;
+    a.d = d;
+  }
+}
+__device__ __forceinline__ void min_pd_xor(MinPD &a, int m) {
+  P192 o;
+  o.hi = u128(shfl_xor128(i128(a.s.hi), m));
+  o.lo = (uint64_t(uint32_t(__shfl_xor(int(a.s.lo >> 32), m, 64))) << 32) |
+         uint32_t(__shfl_xor(int(uint32_t(a.s.lo)), m, 64));
+  min_pd(a, o, __shfl_xor(a.d, m, 64));
+}
+
+template <int K>
+struct SeqCRow {
+  int32_t v[K];  // c[r][lane + 64 k] (K = 0: read on demand)
+  SeqCRec rec;
+};
+
+template <int K>
+__device__ __forceinline__ void seqc_load(const int32_t *__restrict__ matched, int32_t I, int32_t r, int32_t n_req,
+                                          const SeqCRec *__restrict__ recs, SeqCRow<K> &row) {
+  const int lane = threadIdx.x;  // clamped, unconditional loads: see seq_load
+  const int32_t rr = r < n_req ? r : n_req - 1;
+  const int32_t *c = matched + int64_t(rr) * I;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int i = lane + 64 * k;
+    row.v[k] = c[i < I ? i : I - 1];
+  }
+  int32_t rv = rr;
+  asm volatile("" : "+v"(rv));  // a vector load on purpose: see seq_load
+  row.rec = recs[rv];
+}
+
+// Decide request r alone (wavefront-uniform branches, identical stores from every lane).
+template <int K>
+__device__ __forceinline__ void seqc_decide(const SeqCRow<K> &row, const int32_t *__restrict__ matched, int32_t r,
+                                            int32_t I, const RouteParams &p, uint64_t rr_base, bool st_ok, i128 *q2,
+                                            int64_t *nr, const int64_t *sl, int32_t *__restrict__ target,
+                                            uint8_t *__restrict__ branch) {
+  const int lane = threadIdx.x;
+  const int32_t flags = uni(row.rec.flags);
+  if (!st_ok || !(flags & 1)) {
+    target[r] = -1;
+    branch[r] = SMETRIC_INVALID;
+    return;
+  }
+  const int32_t prev = uni(row.rec.prev);
+  const bool cached = flags & 2, follow_up = flags & 4, prev_cand = flags & 8;
+  const bool slack_inf = p.slack_den == 0;
+  const i128 cost_prev = row.rec.cost_prev, bound = row.rec.bound;
+  const bool meets_prev = slack_inf || (q2[prev] + cost_prev) * p.slack_den <= bound;
+  int32_t t;
+  uint8_t br;
+  i128 cost_t;
+  if (follow_up && cached && meets_prev && prev_cand) {
+    t = prev;
+    br = SMETRIC_STICK;
+    cost_t = cost_prev;
+  } else {
+    const int64_t L = uni(row.rec.L);
+    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    const int32_t *c = matched + int64_t(r) * I;
+    MinPD pass{{0, 0}, 0x7FFFFFFF}, all{{0, 0}, 0x7FFFFFFF};
+    if (K > 0) {
+#pragma unroll
+      for (int k = 0; k < (K > 0 ? K : 1); ++k) {
+        const int32_t i = lane + 64 * k;
+        const int32_t ii = i < I ? i : I - 1;
+        const i128 cst = est2(p, L, row.v[k], 0);
+        const P192 sc = mul192(q2[ii] + cst, uint64_t(nr[ii]));
+        const int32_t d = i < I ? (i >= start ? i - start : i - start + I) : 0x7FFFFFFF;
+        min_pd(all, sc, d);
+        if (tpot_pass(sl[ii], cst)) min_pd(pass, sc, d);
+      }
+    } else {
+      for (int32_t i = lane; i < I; i += 64) {
+        const i128 cst = est2(p, L, c[i], 0);
+        const P192 sc = mul192(q2[i] + cst, uint64_t(nr[i]));
+        const int32_t d = i >= start ? i - start : i - start + I;
+        min_pd(all, sc, d);
+        if (tpot_pass(sl[i], cst)) min_pd(pass, sc, d);
+      }
+    }
+    // only the minimum the rule uses is reduced: over the candidates if any instance
+    // passes the TPOT filter, else over all
+    const bool any = __ballot(pass.d != 0x7FFFFFFF) != 0;
+    MinPD best = any ? pass : all;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) min_pd_xor(best, m);
+    t = (start + uni(best.d)) % I;
+    br = !follow_up ? SMETRIC_FIRST_TURN
+                    : (!cached ? SMETRIC_EVICTED : (!meets_prev ? SMETRIC_MIGRATE : SMETRIC_MIGRATE_TPOT));
+    int32_t ct;
+    if (K > 0) {
+      int32_t v = 0;
+#pragma unroll
+      for (int k = 0; k < (K > 0 ? K : 1); ++k)
+        if (k == t / 64) v = row.v[k];
+      ct = uni(__shfl(v, t % 64, 64));
+    } else {
+      ct = uni(c[t]);
+    }
+    cost_t = t == prev ? cost_prev : est2(p, L, ct, 0);
+  }
+  // one wavefront does every LDS access, in program order (see seq_decide)
+  const i128 old = q2[t];
+  const int64_t nold = nr[t];
+  target[r] = t;
+  branch[r] = br;
+  q2[t] = old + cost_t;  // the request's prefill joins its target's queue
+  nr[t] = nold + 1;      // and it is one more request there
+}
+
+template <int K, int D>
+__device__ __forceinline__ void seqc_exact_block(const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
+                                                 const RouteParams &p, uint64_t rr_base, bool st_ok,
+                                                 const SeqCRec *__restrict__ recs, i128 *q2, int64_t *nr,
+                                                 const int64_t *sl, int32_t *__restrict__ target,
+                                                 uint8_t *__restrict__ branch, int32_t rs, int32_t re) {
+  SeqCRow<K> ring[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) seqc_load<K>(matched, I, rs + d, n_req, recs, ring[d]);
+  for (int32_t r0 = rs; r0 < re; r0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int32_t r = r0 + d;
+      if (r < re) {
+        seqc_decide<K>(ring[d], matched, r, I, p, rr_base, st_ok, q2, nr, sl, target, branch);
+        seqc_load<K>(matched, I, r + D, n_req, recs, ring[d]);
+      }
+    }
+  }
+}
+
+// The batch in steps of 64 requests, one per lane, as route_seq_kernel: a cached follow-up
+// whose prev is a candidate sticks iff prev meets its deadline on its exact load (prev's
+// load plus the costs of the step's earlier requests with that prev, all of which stuck if
+// the step got that far); the requests before the first one not settled are decided
+// together -- each group's last one writing prev's load and count -- that one alone, and
+// the next step starts after it.  Two steps in a row that settle nothing: the next 64
+// go through the sequential rule with prefetching.
+template <int K, int D>
+__global__ __launch_bounds__(64) void route_seqc_kernel(const int32_t *__restrict__ matched, int32_t n_req,
+                                                        int32_t I, const int64_t *__restrict__ q,
+                                                        const int64_t *__restrict__ slack,
+                                                        const int32_t *__restrict__ n_run, RouteParams p,
+                                                        uint64_t rr_base, const SeqCRec *__restrict__ recs,
+                                                        int32_t *__restrict__ target, uint8_t *__restrict__ branch,
+                                                        int64_t *__restrict__ q_out, int64_t *__restrict__ n_out) {
+  __shared__ i128 q2[SEQC_MAX_I];
+  __shared__ int64_t nr[SEQC_MAX_I];
+  __shared__ int64_t sl[SEQC_MAX_I];
+  __shared__ uint32_t n_on[SEQC_MAX_I];  // step requests per prev (0 between steps)
+  const int lane = threadIdx.x;
+  bool st_ok = true;
+  for (int32_t i = lane; i < I; i += 64) {
+    const int64_t qi = q[i];
+    const int32_t ni = n_run[i];
+    if (qi < 0 || qi >= (int64_t(1) << 62) || ni < 0) st_ok = false;
+    q2[i] = i128(2) * qi;
+    nr[i] = ni;
+    sl[i] = slack[i];
+    n_on[i] = 0;
+  }
+  st_ok = __ballot(!st_ok) == 0;
+  __syncthreads();
+  const bool slack_inf = p.slack_den == 0;
+  int32_t r0 = 0;
+  int streak = 0;
+  while (r0 < n_req) {
+    if (streak >= 2) {
+      const int32_t re = n_req - r0 < 64 ? n_req : r0 + 64;
+      seqc_exact_block<K, D>(matched, n_req, I, p, rr_base, st_ok, recs, q2, nr, sl, target, branch, r0, re);
+      r0 = re;
+      streak = 0;
+      continue;
+    }
+    const int32_t nv = n_req - r0 < 64 ? n_req - r0 : 64;
+    const int32_t r = r0 + lane;
+    int32_t rv = r < n_req ? r : n_req - 1;
+    asm volatile("" : "+v"(rv));  // a vector load: see seq_load
+    const SeqCRec rec = recs[rv];
+    const bool in = lane < nv;
+    const bool ok = st_ok && (rec.flags & 1);
+    const bool sticky = ok && (rec.flags & 2) && (rec.flags & 4) && (rec.flags & 8);
+    const int32_t prev = rec.prev;
+    const bool mine = in && sticky;
+    if (mine) atomicAdd(&n_on[prev], 1u);
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    uint64_t todo = __ballot(mine && n_on[prev] > 1);
+    __builtin_amdgcn_wave_barrier();
+    if (mine) n_on[prev] = 0;
+    i128 excl = 0;
+    uint64_t group = 0;  // lanes with my prev (0: nobody else has it)
+    while (todo) {
+      const int32_t p0 = __builtin_amdgcn_readlane(prev, __builtin_ctzll(todo));
+      const uint64_t m = __ballot(mine && prev == p0);
+      todo &= ~m;
+      i128 run = 0;
+      for (uint64_t mm = m; mm; mm &= mm - 1) {
+        const int l = __builtin_ctzll(mm);
+        if (lane == l) {
+          excl = run;
+          group = m;
+        }
+        run += readlane128(rec.cost_prev, l);
+      }
+    }
+    const i128 q_prev = (mine ? q2[prev] : i128(0)) + excl;
+    bool settled = !ok;  // out of domain: settled, nothing queued
+    uint8_t br = SMETRIC_INVALID;
+    if (sticky && (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound)) {
+      settled = true;
+      br = SMETRIC_STICK;
+    }
+    const uint64_t open = __ballot(in && !settled);
+    const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
+    SeqCRow<K> row;
+    if (f < nv) seqc_load<K>(matched, I, r0 + f, n_req, recs, row);
+    if (lane < f) {
+      target[r] = ok ? prev : -1;
+      branch[r] = br;
+    }
+    const uint64_t decided = f >= 64 ? ~uint64_t(0) : (uint64_t(1) << f) - 1;
+    const uint64_t after_me = lane == 63 ? uint64_t(0) : ~((uint64_t(2) << lane) - 1);
+    const bool last = mine && lane < f && (group & after_me & decided) == 0;
+    const int64_t added = group ? __popcll(group & decided) : 1;  // the group's requests decided here
+    __builtin_amdgcn_wave_barrier();
+    if (last) {
+      q2[prev] = q_prev + rec.cost_prev;
+      nr[prev] = nr[prev] + added;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    r0 += f;
+    if (f < nv) {  // the first request not settled: the sequential rule
+      seqc_decide<K>(row, matched, r0, I, p, rr_base, st_ok, q2, nr, sl, target, branch);
+      r0 += 1;
+      streak = f == 0 ? streak + 1 : 0;
+    }
+  }
+  __syncthreads();
+  for (int32_t i = lane; i < I; i += 64) {
+    if (q_out) {
+      const i128 v = q2[i] >> 1;
+      q_out[i] = v > i128(INT64_MAX) ? INT64_MAX : int64_t(v);
+    }
+    if (n_out) n_out[i] = nr[i];
+  }
+}
+
 int route_params(const smetric_params *params, int32_t n_req, int32_t n_instances, RouteParams &rp) {
   if (!params || n_req < 0 || n_instances < 1 || n_instances > 65536) return SMETRIC_EINVAL;
   const smetric_params &P = *params;
@@ -641,6 +1004,16 @@ int route_params(const smetric_params *params, int32_t n_req, int32_t n_instance
   rp = RouteParams{P.c_lin, P.c_att, P.slo_b, P.slo_a, P.slack_num, P.slack_den, P.hit_num, P.hit_den,
                    P.block_size};
   return SMETRIC_OK;
+}
+
+// Requests routed one at a time: every running load stays below 2 q + (n_req + 1) x the
+// largest doubled cost a request in domain can add (L <= 2^24, so n (2L - n) <= 2^48), and
+// the deadline check multiplies it by SLACK's denominator.  The batch is accepted only when
+// that product stays below 2^126, so no comparison of the online rules can overflow.
+bool seq_loads_fit(const RouteParams &p, int32_t n_req) {
+  const i128 cmax = i128(2) * p.c_lin * (int64_t(1) << 24) + i128(p.c_att) * (i128(1) << 48);
+  const i128 worst = (i128(1) << 63) + i128(int64_t(n_req) + 1) * cmax;
+  return worst < (i128(1) << 126) / i128(p.slack_den > 0 ? p.slack_den : 1);
 }
 
 }  // namespace
@@ -693,6 +1066,40 @@ extern "C" int smetric_route_coloc(const int32_t *matched, int32_t n_req, int32_
   return hip_rc(hipGetLastError());
 }
 
+extern "C" int smetric_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                                       const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                                       const int64_t *q, const int64_t *tpot_slack, const int32_t *n_running,
+                                       const smetric_params *params, uint64_t rr_base, int32_t *target,
+                                       uint8_t *branch, int64_t *q_out, int64_t *n_out, void *workspace,
+                                       uint64_t ws_bytes, hipStream_t stream) {
+  RouteParams rp;
+  if (int rc = route_params(params, n_req, n_instances, rp)) return rc;
+  if (n_instances > SEQC_MAX_I || !seq_loads_fit(rp, n_req)) return SMETRIC_EINVAL;
+  if (!q || !tpot_slack || !n_running) return SMETRIC_EINVAL;
+  if (n_req > 0 && (!matched || !prompt_len || !hist_len || !turn || !target || !branch)) return SMETRIC_EINVAL;
+  uint64_t need = 0;
+  smetric_route_seq_ws_bytes(n_req, &need);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) || ws_bytes < need) return SMETRIC_EWORKSPACE;
+  SeqCRec *recs = static_cast<SeqCRec *>(workspace);
+  if (n_req > 0)
+    hipLaunchKernelGGL(route_seqc_prep_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched,
+                       n_req, n_instances, prompt_len, hist_len, turn, tpot_slack, rp, recs);
+  const int kk = (n_instances + 63) / 64;
+#define SEQC_LAUNCH(K, D)                                                                                        \
+  hipLaunchKernelGGL((route_seqc_kernel<K, D>), dim3(1), dim3(64), 0, stream, matched, n_req, n_instances, q,      \
+                     tpot_slack, n_running, rp, rr_base, recs, target, branch, q_out, n_out)
+  // prefetch depth D: D * (K + 3) vector loads in flight (K row words and a 48-byte record
+  // per request) stay within the 63 the wait counter tracks
+  if (kk <= 1) SEQC_LAUNCH(1, 8);
+  else if (kk <= 2) SEQC_LAUNCH(2, 8);
+  else if (kk <= 4) SEQC_LAUNCH(4, 7);
+  else if (kk <= 8) SEQC_LAUNCH(8, 5);
+  else if (kk <= 16) SEQC_LAUNCH(16, 3);
+  else SEQC_LAUNCH(0, 8);
+#undef SEQC_LAUNCH
+  return hip_rc(hipGetLastError());
+}
+
 extern "C" int smetric_route_seq_ws_bytes(int32_t n_req, uint64_t *ws_bytes) {
   if (n_req < 0 || !ws_bytes) return SMETRIC_EINVAL;
   *ws_bytes = (uint64_t(n_req < 1 ? 1 : n_req) * sizeof(SeqRec) + 255) / 256 * 256;
@@ -706,7 +1113,7 @@ extern "C" int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t 
                                  uint64_t ws_bytes, hipStream_t stream) {
   RouteParams rp;
   if (int rc = route_params(params, n_req, n_instances, rp)) return rc;
-  if (n_instances > SEQ_MAX_I) return SMETRIC_EINVAL;
+  if (n_instances > SEQ_MAX_I || !seq_loads_fit(rp, n_req)) return SMETRIC_EINVAL;
   if (!q) return SMETRIC_EINVAL;
   if (n_req > 0 && (!matched || !prompt_len || !hist_len || !turn || !target || !branch)) return SMETRIC_EINVAL;
   uint64_t need = 0;

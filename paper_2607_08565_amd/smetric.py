@@ -69,6 +69,7 @@ def _load() -> C.CDLL:
         "smetric_sessions_ws_bytes": [I32, P],
         "smetric_sessions": [P, P, I32, I64, P, P, P, P, P, P, U64, P],
         "smetric_route_seq": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P, U64, P],
+        "smetric_route_seq_coloc": [P, I32, I32, P, P, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P, P, U64, P],
         "smetric_index_insert_ws_bytes": [I64, P],
         "smetric_index_insert": [PIX, P, P, I32, I64, P, P, U32, P, U64, P],
         "smetric_index_evict_ws_bytes": [PIX, P],
@@ -98,7 +99,7 @@ EXPORTED = (
     "smetric_probe_ws_bytes", "smetric_probe", "smetric_match_probed", "smetric_index_insert_probed",
     "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq", "smetric_sessions_ws_bytes",
     "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
-    "smetric_probe_partition", "smetric_probe_lookup", "smetric_hash_partition",
+    "smetric_probe_partition", "smetric_probe_lookup", "smetric_hash_partition", "smetric_route_seq_coloc",
 )
 
 
@@ -190,6 +191,33 @@ def route_seq(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.T
         C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
         _dev(q_out, torch.int64, "q_out"), _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
     return target[:R], branch[:R], q_out
+
+def route_seq_coloc(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
+                    q: torch.Tensor, tpot_slack: torch.Tensor, n_running: torch.Tensor, params: dict,
+                    rr_base: int = 0, target: torch.Tensor | None = None, branch: torch.Tensor | None = None,
+                    q_out: torch.Tensor | None = None, n_out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None):
+    """smetric_route_seq_coloc: the colocation rule with requests routed one at a time.
+    Returns (target, branch, q_out, n_out)."""
+    R, I = matched.shape
+    dev = matched.device
+    target = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if target is None else target
+    branch = torch.empty(max(R, 1), dtype=torch.uint8, device=dev) if branch is None else branch
+    q_out = torch.empty(I, dtype=torch.int64, device=dev) if q_out is None else q_out
+    n_out = torch.empty(I, dtype=torch.int64, device=dev) if n_out is None else n_out
+    need = route_seq_ws_bytes(R)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    p = _Params(**params)
+    _check("smetric_route_seq_coloc", _lib.smetric_route_seq_coloc(
+        _dev(matched, torch.int32, "matched"), R, I, _dev(prompt_len, torch.int32, "prompt_len"),
+        _dev(hist_len, torch.int32, "hist_len"), _dev(turn, torch.int32, "turn"), _dev(q, torch.int64, "q"),
+        _dev(tpot_slack, torch.int64, "tpot_slack"), _dev(n_running, torch.int32, "n_running"), C.byref(p),
+        C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
+        _dev(q_out, torch.int64, "q_out"), _dev(n_out, torch.int64, "n_out"),
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
+    return target[:R], branch[:R], q_out, n_out
+
 
 def route_loadaware(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
                     q: torch.Tensor, load: torch.Tensor, margin: tuple[int, int], params: dict, rr_base: int = 0,

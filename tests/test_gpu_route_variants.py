@@ -233,6 +233,132 @@ def test_seq_on_matched_rows_of_a_session_workload():
 
 
 # ---------------------------------------------------------------------------------
+# Colocation rule, requests routed one at a time (App. B)
+# ---------------------------------------------------------------------------------
+def _seqc_both(S, m, L, hist, turn, q, slack, n_run, p, rr):
+    gt, gb, gq, gn = S.route_seq_coloc(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), to_dev(slack),
+                                       to_dev(n_run), p, rr)
+    ot, ob, oq, on = oracle.route_seq_coloc(m, L, hist, turn, q, slack, n_run, p, rr)
+    gt, gb, gq, gn = gt.cpu().numpy(), gb.cpu().numpy(), gq.cpu().numpy(), gn.cpu().numpy()
+    bad = np.nonzero((gt != ot) | (gb != ob))[0]
+    assert len(bad) == 0, f"{len(bad)} decisions differ, first {bad[:5]}: gpu {gt[bad[:3]]}/{gb[bad[:3]]} oracle {ot[bad[:3]]}/{ob[bad[:3]]}"
+    assert np.array_equal(gq, oq), "final loads differ"
+    assert np.array_equal(gn, on), "final request counts differ"
+    return ot, ob
+
+
+@pytest.mark.parametrize("I", [1, 3, 64, 65, 1000, 1024, 1025, 4096])
+def test_seqc_random_parity(I):
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(400 + I)
+    R = 3000 if I <= 1025 else 800
+    m, L, hist, turn, q, slack, n_run = _coloc_inputs(rng, R, I)
+    seen = set()
+    for over in ({}, dict(slack_num=0, slack_den=1), dict(slack_num=1, slack_den=0), dict(c_att=0, c_lin=1),
+                 dict(slack_num=3, slack_den=2, hit_num=0, hit_den=5)):
+        p = dict(W.DEFAULT_PARAMS, **over)
+        for rr in (0, 987654321):
+            _, ob = _seqc_both(S, m, L, hist, turn, q, slack, n_run, p, rr)
+            seen |= set(ob.tolist())
+    _seqc_both(S, m, L, hist, turn, q, np.full(I, -1, np.int64), n_run, W.DEFAULT_PARAMS, 5)  # nobody passes
+    _seqc_both(S, m, L, hist, turn, q, slack, np.zeros(I, np.int32), W.DEFAULT_PARAMS, 5)  # an idle fleet
+    say(f"  I={I}: branches seen {sorted(seen)}")
+    assert {0, 1, 2, 4} <= seen
+    if I >= 64:
+        assert 5 in seen
+
+
+@pytest.mark.parametrize("I", [2, 4, 37])
+def test_seqc_blocks_of_cached_follow_ups(I):
+    """Cached follow-ups whose prev is a candidate, on few instances: most requests of
+    every 64-request step share a prev and the queues cross deadlines inside steps, so the
+    step-wise sticks meet the sequential rule's migrations; some prevs fail the TPOT filter,
+    a sprinkle of first turns and out-of-domain rows."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(500 + I)
+    R = 5000
+    L = rng.integers(1024, 8192, R).astype(np.int32)
+    prev = rng.integers(0, I, R)
+    m = (rng.integers(0, 30, (R, I)) * (L // 16)[:, None] // 100).astype(np.int32)
+    m[np.arange(R), prev] = (L // 16) * rng.integers(60, 100, R) // 100
+    hist = (L * 6 // 10).astype(np.int32)
+    turn = np.ones(R, np.int32)
+    turn[rng.random(R) < 0.01] = 0
+    m[rng.random(R) < 0.005, 0] = 1 << 20  # out of domain (c > L / B)
+    q = rng.integers(0, 40, I).astype(np.int64) * W.Q_UNIT_NS
+    slack = np.full(I, oracle.NO_DECODE, np.int64)
+    slack[0] = 10**8  # instance 0 fails the filter for the longer stalls
+    n_run = rng.integers(0, 20, I).astype(np.int32)
+    seen = set()
+    for over in ({}, dict(slack_num=1, slack_den=2), dict(slack_num=4, slack_den=1), dict(c_lin=20_000),
+                 dict(c_lin=4_000_000, slo_b=2**32), dict(c_lin=4_000_000, c_att=3_000, slo_b=2**32, slo_a=2**32)):
+        p = dict(W.DEFAULT_PARAMS, **over)
+        _, ob = _seqc_both(S, m, L, hist, turn, q, slack, n_run, p, 12345)
+        seen |= set(ob.tolist())
+    say(f"  I={I}: branches seen {sorted(seen)}")
+    assert {0, 2, 4, 255} <= seen
+
+
+def test_seqc_scores_past_128_bits_and_limits():
+    """140,000 maximal prefills on two instances with nearly 2^31 requests each: the LMetric
+    products pass 2^127, where only the exact comparison keeps both sides equal; then the
+    state-domain, size and overflow limits and the empty batch."""
+    from paper_2607_08565_amd import smetric as S
+    R, I = 140_000, 2
+    big = dict(W.DEFAULT_PARAMS, c_lin=1 << 32, c_att=1 << 32, block_size=256)
+    m = np.zeros((R, I), np.int32)
+    L = np.full(R, 1 << 24, np.int32)
+    z = np.zeros(R, np.int32)
+    q = np.zeros(I, np.int64)
+    slack = np.full(I, oracle.NO_DECODE, np.int64)
+    n_run = np.array([2**31 - 1, 2**31 - 3], np.int32)
+    ot, _ = _seqc_both(S, m, L, z, z, q, slack, n_run, big, 0)
+    cost2 = 2 * (1 << 32) * (1 << 24) + (1 << 32) * (1 << 48)
+    assert int(np.bincount(ot, minlength=2).max()) * cost2 * 2**31 > 2**127  # past 128 bits
+    n_bad = n_run.copy()
+    n_bad[1] = -1
+    _, ob = _seqc_both(S, m[:100], L[:100], z[:100], z[:100], q, slack, n_bad, big, 0)
+    assert set(ob.tolist()) == {255}
+    with pytest.raises(S.SmetricError):  # more instances than the LDS holds
+        S.route_seq_coloc(to_dev(np.zeros((2, 4097), np.int32)), to_dev(np.zeros(2, np.int32)),
+                          to_dev(np.zeros(2, np.int32)), to_dev(np.zeros(2, np.int32)),
+                          to_dev(np.zeros(4097, np.int64)), to_dev(np.zeros(4097, np.int64)),
+                          to_dev(np.zeros(4097, np.int32)), W.DEFAULT_PARAMS)
+    with pytest.raises(S.SmetricError):  # loads that could overflow the deadline check
+        huge = dict(big, slack_num=1, slack_den=2**31 - 1)
+        S.route_seq_coloc(to_dev(m), to_dev(L), to_dev(z), to_dev(z), to_dev(q), to_dev(slack), to_dev(n_run), huge)
+    gt, gb, gq, gn = S.route_seq_coloc(to_dev(np.zeros((0, 5), np.int32)), to_dev(np.zeros(0, np.int32)),
+                                       to_dev(np.zeros(0, np.int32)), to_dev(np.zeros(0, np.int32)),
+                                       to_dev(np.arange(5, dtype=np.int64)), to_dev(np.zeros(5, np.int64)),
+                                       to_dev(np.arange(5, dtype=np.int32)), W.DEFAULT_PARAMS)
+    assert gq.cpu().numpy().tolist() == list(range(5)) and gn.cpu().numpy().tolist() == list(range(5))
+
+
+def test_seqc_on_matched_rows_of_a_session_workload():
+    """The colocated rule one request at a time on the real c rows of a scaled mid-fleet
+    workload (closed loop), against the batch-snapshot rule for reference."""
+    from paper_2607_08565_amd import smetric as S
+    wl = W.config1(n_sess=256, n_turns=3)
+    pair = Pair(4_000_000, wl.n_inst)
+    rng = np.random.default_rng(13)
+    prev = None
+    for t in range(3):
+        b = wl.batch(t, prev)
+        d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(b.tokens, b.tok_off)
+        om = pair.oix.match(okeys, blk_off)
+        assert np.array_equal(pair.gix.match(d_keys, d_boff, nb).cpu().numpy(), om)
+        slack = rng.integers(0, 2 * 10**9, wl.n_inst).astype(np.int64)
+        slack[rng.random(wl.n_inst) < 0.3] = oracle.NO_DECODE
+        n_run = rng.integers(0, 30, wl.n_inst).astype(np.int32)
+        ot, ob = _seqc_both(S, om, b.prompt_len, b.hist_len, b.turn, b.q, slack, n_run, W.DEFAULT_PARAMS, b.rr_base)
+        bt, _ = oracle.route_coloc(om, b.prompt_len, b.hist_len, b.turn, b.q, slack, n_run, W.DEFAULT_PARAMS, b.rr_base)
+        say(f"  batch {t}: branches {np.bincount(ob, minlength=6).tolist()}, "
+            f"{int((bt != ot).sum())} of {len(ot)} targets differ from the batch-snapshot rule")
+        pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, ot, b.session, b.epoch)
+        prev = ot
+
+
+# ---------------------------------------------------------------------------------
 # Sec. 5.4 ablation: load-aware filter; Sec. 4.1 load-imbalance metric
 # ---------------------------------------------------------------------------------
 @pytest.mark.parametrize("I", [1, 3, 64, 65, 1000, 5000])

@@ -131,3 +131,32 @@ def test_score_comparison_is_exact_past_128_bits():
             b, y = a, x + int(rng.integers(-1, 2))  # near ties
             y = max(y, 0)
         assert oracle.test_prod_less(a, x, b, y) == (a * x < b * y)
+
+
+def test_batches_whose_loads_could_overflow_are_refused():
+    """Both one-at-a-time rules accept a batch only if its largest reachable load, times
+    SLACK's denominator, stays below 2^126 (checked here with Python integers at the edge)."""
+    import pytest
+    big = dict(P, c_lin=2**32, c_att=2**32, slack_num=1, slack_den=2**31 - 1)
+    cmax = 2 * 2**32 * 2**24 + 2**32 * 2**48  # the largest doubled cost of a request in domain
+
+    def fits(R):
+        return (2**63 + (R + 1) * cmax) * (2**31 - 1) < 2**126
+
+    R_ok = (2**126 // (2**31 - 1) - 2**63) // cmax - 1
+    while not fits(R_ok):
+        R_ok -= 1
+    while fits(R_ok + 1):
+        R_ok += 1
+    for R, ok in ((R_ok, True), (R_ok + 1, False)):
+        m = np.zeros((R, 1), np.int32)
+        z = np.zeros(R, np.int32)
+        args = (m, z, z, z, np.zeros(1, np.int64))
+        if ok:
+            oracle.route_seq(*args, big, 0)
+            oracle.route_seq_coloc(*args, np.full(1, NO_DECODE, np.int64), np.zeros(1, np.int32), big, 0)
+        else:
+            with pytest.raises(ValueError):
+                oracle.route_seq(*args, big, 0)
+            with pytest.raises(ValueError):
+                oracle.route_seq_coloc(*args, np.full(1, NO_DECODE, np.int64), np.zeros(1, np.int32), big, 0)
