@@ -269,7 +269,7 @@ struct SeqRec {
   int32_t prev;    // argmax c, lowest id
   int32_t flags;   // bit 0: in domain (apart from q), bit 1: session cached, bit 2: follow-up
   int32_t L;       // prompt length
-  int32_t pad;
+  int32_t start;   // (rr_base + r) mod I: where the rotation of rr_argmin starts
   i128 cost_prev;  // 2 x prefill_cost(req, c[prev]), Eq. (1)
   i128 cost_rest;  // 2 x prefill_cost at the largest hit of any other instance: a lower
                    // bound of every other instance's cost (Eq. (1) falls as the hit grows)
@@ -284,7 +284,7 @@ __global__ __launch_bounds__(64 * RW) void route_seq_prep_kernel(const int32_t *
                                                                  const int32_t *__restrict__ hist_len,
                                                                  const int32_t *__restrict__ turn,
                                                                  const int64_t *__restrict__ q, RouteParams p,
-                                                                 SeqRec *__restrict__ rec) {
+                                                                 uint64_t rr_base, SeqRec *__restrict__ rec) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * RW + wave;
   if (r >= n_req) return;
@@ -341,7 +341,7 @@ __global__ __launch_bounds__(64 * RW) void route_seq_prep_kernel(const int32_t *
   out.prev = ok ? bi : 0;
   out.flags = int32_t(ok) | (int32_t(cached) << 1) | (int32_t(tr != 0) << 2);
   out.L = ok ? int32_t(L) : 0;
-  out.pad = 0;
+  out.start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
   out.cost_prev = ok ? est2(p, L, bc, 0) : i128(0);
   // one instance: nothing else to bound, any value will do
   out.cost_rest = ok ? est2(p, L, c2 < 0 ? bc : c2, 0) : i128(0);
@@ -407,7 +407,7 @@ __device__ __forceinline__ i128 readlane128(i128 v, int l) {
 // regions: the compiler can then wait for exactly the prefetched loads it uses.
 template <int K>
 __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *__restrict__ matched, int32_t r,
-                                           int32_t I, const RouteParams &p, uint64_t rr_base, bool q_ok, i128 *q2,
+                                           int32_t I, const RouteParams &p, bool q_ok, i128 *q2,
                                            i128 &qmin, int32_t *__restrict__ target, uint8_t *__restrict__ branch) {
   const int lane = threadIdx.x;
   const int32_t flags = uni(row.rec.flags);
@@ -438,7 +438,7 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
   } else {
     const int64_t L = uni(row.rec.L);
     const int32_t tr = follow_up ? 1 : 0;
-    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    const int32_t start = uni(row.rec.start);
     const int32_t *c = matched + int64_t(r) * I;
     MinSD best{0, 0x7FFFFFFF};
     if (K > 0) {
@@ -455,7 +455,8 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
     }
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) min_sd(best, shfl_xor128(best.s, m), __shfl_xor(best.d, m, 64));
-    const int32_t bal = (start + uni(best.d)) % I;
+    const int32_t bal0 = start + uni(best.d);  // start, d < I
+    const int32_t bal = bal0 >= I ? bal0 - I : bal0;
     if (tr == 0) {
       t = bal;
       br = SMETRIC_FIRST_TURN;
@@ -494,7 +495,7 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
 // Requests [rs, re) one at a time, rows and records prefetched D requests ahead.
 template <int K, int D>
 __device__ __forceinline__ void seq_exact_block(const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
-                                                const RouteParams &p, uint64_t rr_base, bool q_ok,
+                                                const RouteParams &p, bool q_ok,
                                                 const SeqRec *__restrict__ recs, i128 *q2, i128 &qmin,
                                                 int32_t *__restrict__ target, uint8_t *__restrict__ branch,
                                                 int32_t rs, int32_t re) {
@@ -506,7 +507,7 @@ __device__ __forceinline__ void seq_exact_block(const int32_t *__restrict__ matc
     for (int d = 0; d < D; ++d) {
       const int32_t r = r0 + d;
       if (r < re) {
-        seq_decide<K>(ring[d], matched, r, I, p, rr_base, q_ok, q2, qmin, target, branch);
+        seq_decide<K>(ring[d], matched, r, I, p, q_ok, q2, qmin, target, branch);
         seq_load<K>(matched, I, r + D, n_req, recs, ring[d]);
       }
     }
@@ -526,7 +527,7 @@ __device__ __forceinline__ void seq_exact_block(const int32_t *__restrict__ matc
 template <int K, int D>
 __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict__ matched, int32_t n_req,
                                                        int32_t I, const int64_t *__restrict__ q, RouteParams p,
-                                                       uint64_t rr_base, const SeqRec *__restrict__ recs,
+                                                       const SeqRec *__restrict__ recs,
                                                        int32_t *__restrict__ target, uint8_t *__restrict__ branch,
                                                        int64_t *__restrict__ q_out) {
   __shared__ i128 q2[SEQ_MAX_I];
@@ -548,7 +549,7 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
   while (r0 < n_req) {
     if (streak >= 2) {
       const int32_t re = n_req - r0 < 64 ? n_req : r0 + 64;
-      seq_exact_block<K, D>(matched, n_req, I, p, rr_base, q_ok, recs, q2, qmin, target, branch, r0, re);
+      seq_exact_block<K, D>(matched, n_req, I, p, q_ok, recs, q2, qmin, target, branch, r0, re);
       r0 = re;
       streak = 0;
       continue;
@@ -621,7 +622,7 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
     if (__ballot(mine && lane < f && q_pre == qmin)) qmin = seq_qmin(q2, I);
     r0 += f;
     if (f < nv) {  // the first request not settled: the sequential rule
-      seq_decide<K>(row, matched, r0, I, p, rr_base, q_ok, q2, qmin, target, branch);
+      seq_decide<K>(row, matched, r0, I, p, q_ok, q2, qmin, target, branch);
       r0 += 1;
       streak = f == 0 ? streak + 1 : 0;
     }
@@ -643,21 +644,22 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
 //   prep  one wavefront per request: domain, prev = argmax c, session_cached, follow-up,
 //         whether prev is a candidate (passes the TPOT filter, or no instance does), the
 //         cost on prev and the deadline -- none of it depends on the running state.
-//   seq   ONE wavefront; 2q, n and the slacks in LDS.  A cached follow-up whose prev is a
-//         candidate sticks iff prev meets its deadline, which needs only prev's load: 64
-//         requests are settled per step as in route_seq_kernel (the step's earlier
-//         requests with the same prev add their costs); the first request not settled is
-//         decided alone by a scan of its row for the LMetric minimum over the candidates.
+//   seq   ONE workgroup; 2q and n in LDS, the slacks in the registers of the instances'
+//         threads.  A cached follow-up whose prev is a candidate sticks iff prev meets its
+//         deadline, which needs only prev's load: wavefront 0 settles 64 requests per step
+//         as in route_seq_kernel (the step's earlier requests with the same prev add their
+//         costs); the first request not settled is decided by the whole workgroup, each
+//         thread scoring its instances, then a wavefront and a cross-wavefront minimum.
 //         The scores est2 x n are compared in 192 bits: over a batch both factors grow.
 // ---------------------------------------------------------------------------------
-constexpr int SEQC_MAX_I = 4096;  // LDS: 2q (64 KB), n and slack (32 KB each), step counters
+constexpr int SEQC_MAX_I = 4096;  // LDS: 2q (64 KB), n and the step counters (16 KB each)
 
 struct SeqCRec {
   int32_t prev;
   int32_t flags;  // bit 0: in domain (apart from the instance state), 1: session cached,
-                  // 2: follow-up, 3: prev is a candidate
+                  // 2: follow-up, 3: prev is a candidate, 4: some instance passes the TPOT filter
   int32_t L;
-  int32_t pad;
+  int32_t start;  // (rr_base + r) mod I
   i128 cost_prev;  // 2 x prefill_cost(req, c[prev])
   i128 bound;      // SLACK_num x 2 (b + a L)
 };
@@ -672,7 +674,7 @@ __global__ __launch_bounds__(64 * RW) void route_seqc_prep_kernel(const int32_t 
                                                                   const int32_t *__restrict__ hist_len,
                                                                   const int32_t *__restrict__ turn,
                                                                   const int64_t *__restrict__ slack, RouteParams p,
-                                                                  SeqCRec *__restrict__ rec) {
+                                                                  uint64_t rr_base, SeqCRec *__restrict__ rec) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * RW + wave;
   if (r >= n_req) return;
@@ -708,26 +710,29 @@ __global__ __launch_bounds__(64 * RW) void route_seqc_prep_kernel(const int32_t 
   const bool cached = ok && i128(p.B) * bc * p.hit_den > i128(p.hit_num) * hist;
   const bool prev_cand = ok && (!any_pass || tpot_pass(slack[bi], cost_prev));
   out.prev = ok ? bi : 0;
-  out.flags = int32_t(ok) | (int32_t(cached) << 1) | (int32_t(tr != 0) << 2) | (int32_t(prev_cand) << 3);
+  out.flags = int32_t(ok) | (int32_t(cached) << 1) | (int32_t(tr != 0) << 2) | (int32_t(prev_cand) << 3) |
+              (int32_t(any_pass) << 4);
   out.L = ok ? int32_t(L) : 0;
-  out.pad = 0;
+  out.start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
   out.cost_prev = cost_prev;
   out.bound = i128(p.slack_num) * (i128(2) * (i128(p.slo_b) + i128(p.slo_a) * (ok ? L : 0)));
   rec[r] = out;
 }
 
-// a * x for 0 <= a < 2^127, x < 2^64, as (high 128 bits, low 64 bits)
+// a * x for 0 <= a < 2^127, x < 2^32, as (high 128 bits, low 64 bits)
 typedef unsigned __int128 u128;
 struct P192 {
   u128 hi;
   uint64_t lo;
 };
-__device__ __forceinline__ P192 mul192(i128 a, uint64_t x) {
+__device__ __forceinline__ P192 mul192(i128 a, uint32_t x) {
   const u128 ua = u128(a);
-  const u128 p_lo = u128(uint64_t(ua)) * u128(x);
+  const uint64_t p0 = uint64_t(uint32_t(ua)) * x;                           // < 2^64
+  const uint64_t p1 = uint64_t(uint32_t(uint64_t(ua) >> 32)) * x + (p0 >> 32);  // < 2^64
+  const uint64_t lo = (p1 << 32) | uint32_t(p0);
   const uint64_t a_hi = uint64_t(ua >> 64);
-  if (a_hi == 0) return P192{p_lo >> 64, uint64_t(p_lo)};  // the usual case: a load below 2^64
-  return P192{u128(a_hi) * u128(x) + (p_lo >> 64), uint64_t(p_lo)};
+  if (a_hi == 0) return P192{u128(p1 >> 32), lo};  // the usual case: a load below 2^64
+  return P192{u128(a_hi) * x + (p1 >> 32), lo};
 }
 __device__ __forceinline__ bool less192(const P192 &a, const P192 &b) {
   return a.hi < b.hi || (a.hi == b.hi && a.lo < b.lo);
@@ -751,21 +756,81 @@ __device__ __forceinline__ void min_pd_xor(MinPD &a, int m) {
   min_pd(a, o, __shfl_xor(a.d, m, 64));
 }
 
-template <int K>
+// DPP move of a 64-bit value from lane l - s of the same row (row_shr:s) or from the last lane
+// of an earlier row (row_bcast); lanes without a source, or outside the row mask, keep v.
+template <int CTRL, int RM>
+__device__ __forceinline__ uint64_t dpp_or_own64(uint64_t v) {
+  const int lo = __builtin_amdgcn_update_dpp(int(uint32_t(v)), int(uint32_t(v)), CTRL, RM, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(int(uint32_t(v >> 32)), int(uint32_t(v >> 32)), CTRL, RM, 0xF, false);
+  return (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo);
+}
+template <int CTRL, int RM>
+__device__ __forceinline__ void dpp_min_key(uint64_t &k1, uint64_t &k0) {
+  const uint64_t o1 = dpp_or_own64<CTRL, RM>(k1), o0 = dpp_or_own64<CTRL, RM>(k0);
+  if (o1 < k1 || (o1 == k1 && o0 < k0)) {
+    k1 = o1;
+    k0 = o0;
+  }
+}
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+  return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), l))) << 32) |
+         uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
+}
+
+// Minimum of (score, d) over lanes 0..N-1 (N = 64: the wavefront; N <= 16: within row 0);
+// every lane gets it.  While every score is below 2^96 the pair is compared as two 64-bit
+// words (score bits 32..95; score bits 0..31 and d) and reduced with DPP moves toward lane
+// N - 1 (row_shr 1, 2, 4, 8, then row_bcast 15 and 31); otherwise with 192-bit shuffles.
+template <int N>
+__device__ __forceinline__ MinPD wave_min_pd(MinPD a) {
+  const bool none = a.d == 0x7FFFFFFF;
+  if (__ballot(!none && (a.s.hi >> 32) != 0) == 0) {
+    uint64_t k1 = ~uint64_t(0), k0 = ~uint64_t(0);  // d < 2^31 - 1: no entry has k0 = ~0
+    if (!none) {
+      k1 = (uint64_t(a.s.hi) << 32) | (a.s.lo >> 32);
+      k0 = (a.s.lo << 32) | uint32_t(a.d);
+    }
+    if (N > 1) dpp_min_key<0x111, 0xF>(k1, k0);
+    if (N > 2) dpp_min_key<0x112, 0xF>(k1, k0);
+    if (N > 4) dpp_min_key<0x114, 0xF>(k1, k0);
+    if (N > 8) dpp_min_key<0x118, 0xF>(k1, k0);
+    if (N > 16) {
+      dpp_min_key<0x142, 0xA>(k1, k0);  // row_bcast:15 into rows 1 and 3
+      dpp_min_key<0x143, 0xC>(k1, k0);  // row_bcast:31 into rows 2 and 3
+    }
+    k1 = readlane64(k1, N - 1);
+    k0 = readlane64(k0, N - 1);
+    if (k0 == ~uint64_t(0)) return MinPD{{0, 0}, 0x7FFFFFFF};
+    return MinPD{{u128(k1 >> 32), (k1 << 32) | (k0 >> 32)}, int32_t(uint32_t(k0))};
+  }
+  for (int m = N > 32 ? 32 : N / 2; m >= 1; m >>= 1) min_pd_xor(a, m);  // lanes 0..N-1 hold the minimum
+  MinPD r;
+  r.s.hi = u128(readlane128(i128(a.s.hi), 0));
+  r.s.lo = readlane64(a.s.lo, 0);
+  r.d = __builtin_amdgcn_readlane(a.d, 0);
+  return r;
+}
+
+// The sequential kernel runs as one workgroup of NW wavefronts.  Instance i belongs to
+// thread i mod (64 NW): that thread holds the instance's decode slack and its matched-prefix
+// values of the prefetched requests in registers, scores it, and is the one that adds a
+// request's prefill to the instance's queue (so a queue is written by one thread only, and
+// read by others only across a barrier).
+template <int KT>
 struct SeqCRow {
-  int32_t v[K];  // c[r][lane + 64 k] (K = 0: read on demand)
+  int32_t v[KT];  // c[r][tid + 64 NW k]
   SeqCRec rec;
 };
 
-template <int K>
+template <int NW, int KT>
 __device__ __forceinline__ void seqc_load(const int32_t *__restrict__ matched, int32_t I, int32_t r, int32_t n_req,
-                                          const SeqCRec *__restrict__ recs, SeqCRow<K> &row) {
-  const int lane = threadIdx.x;  // clamped, unconditional loads: see seq_load
+                                          const SeqCRec *__restrict__ recs, SeqCRow<KT> &row) {
+  const int tid = threadIdx.x;  // clamped, unconditional loads: see seq_load
   const int32_t rr = r < n_req ? r : n_req - 1;
   const int32_t *c = matched + int64_t(rr) * I;
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int i = lane + 64 * k;
+  for (int k = 0; k < KT; ++k) {
+    const int i = tid + 64 * NW * k;
     row.v[k] = c[i < I ? i : I - 1];
   }
   int32_t rv = rr;
@@ -773,222 +838,222 @@ __device__ __forceinline__ void seqc_load(const int32_t *__restrict__ matched, i
   row.rec = recs[rv];
 }
 
-// Decide request r alone (wavefront-uniform branches, identical stores from every lane).
-template <int K>
-__device__ __forceinline__ void seqc_decide(const SeqCRow<K> &row, const int32_t *__restrict__ matched, int32_t r,
-                                            int32_t I, const RouteParams &p, uint64_t rr_base, bool st_ok, i128 *q2,
-                                            int64_t *nr, const int64_t *sl, int32_t *__restrict__ target,
+// Decide request r (every thread of the workgroup calls this with the same r and record;
+// the branches are uniform).  On return the target's queue and count include the request.
+template <int NW, int KT>
+__device__ __forceinline__ void seqc_decide(const SeqCRow<KT> &row, int32_t r, int32_t I, const RouteParams &p,
+                                            bool st_ok, i128 *q2, uint32_t *nr,
+                                            const int64_t (&sl)[KT], MinPD *part, int32_t *__restrict__ target,
                                             uint8_t *__restrict__ branch) {
-  const int lane = threadIdx.x;
+  constexpr int NT = 64 * NW;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int32_t flags = uni(row.rec.flags);
   if (!st_ok || !(flags & 1)) {
-    target[r] = -1;
-    branch[r] = SMETRIC_INVALID;
-    return;
+    if (tid == 0) {
+      target[r] = -1;
+      branch[r] = SMETRIC_INVALID;
+    }
+    return;  // nothing queued: no barrier needed
   }
   const int32_t prev = uni(row.rec.prev);
-  const bool cached = flags & 2, follow_up = flags & 4, prev_cand = flags & 8;
+  const int64_t L = uni(row.rec.L);
+  const bool cached = flags & 2, follow_up = flags & 4, prev_cand = flags & 8, any_pass = flags & 16;
   const bool slack_inf = p.slack_den == 0;
-  const i128 cost_prev = row.rec.cost_prev, bound = row.rec.bound;
-  const bool meets_prev = slack_inf || (q2[prev] + cost_prev) * p.slack_den <= bound;
+  const bool meets_prev = slack_inf || (q2[prev] + row.rec.cost_prev) * p.slack_den <= row.rec.bound;
   int32_t t;
   uint8_t br;
-  i128 cost_t;
   if (follow_up && cached && meets_prev && prev_cand) {
     t = prev;
     br = SMETRIC_STICK;
-    cost_t = cost_prev;
+    __syncthreads();  // every thread has read prev's queue before its owner adds to it
   } else {
-    const int64_t L = uni(row.rec.L);
-    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
-    const int32_t *c = matched + int64_t(r) * I;
-    MinPD pass{{0, 0}, 0x7FFFFFFF}, all{{0, 0}, 0x7FFFFFFF};
-    if (K > 0) {
+    // LMetric minimum over the candidates: the instances that pass the TPOT filter if any
+    // does (fixed per request: the slacks do not change), else all of them
+    const int32_t start = uni(row.rec.start);
+    MinPD best{{0, 0}, 0x7FFFFFFF};
 #pragma unroll
-      for (int k = 0; k < (K > 0 ? K : 1); ++k) {
-        const int32_t i = lane + 64 * k;
-        const int32_t ii = i < I ? i : I - 1;
+    for (int k = 0; k < KT; ++k) {
+      const int32_t i = tid + NT * k;
+      if (i < I) {
         const i128 cst = est2(p, L, row.v[k], 0);
-        const P192 sc = mul192(q2[ii] + cst, uint64_t(nr[ii]));
-        const int32_t d = i < I ? (i >= start ? i - start : i - start + I) : 0x7FFFFFFF;
-        min_pd(all, sc, d);
-        if (tpot_pass(sl[ii], cst)) min_pd(pass, sc, d);
-      }
-    } else {
-      for (int32_t i = lane; i < I; i += 64) {
-        const i128 cst = est2(p, L, c[i], 0);
-        const P192 sc = mul192(q2[i] + cst, uint64_t(nr[i]));
-        const int32_t d = i >= start ? i - start : i - start + I;
-        min_pd(all, sc, d);
-        if (tpot_pass(sl[i], cst)) min_pd(pass, sc, d);
+        if (!any_pass || tpot_pass(sl[k], cst))
+          min_pd(best, mul192(q2[i] + cst, nr[i]), i >= start ? i - start : i - start + I);
       }
     }
-    // only the minimum the rule uses is reduced: over the candidates if any instance
-    // passes the TPOT filter, else over all
-    const bool any = __ballot(pass.d != 0x7FFFFFFF) != 0;
-    MinPD best = any ? pass : all;
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) min_pd_xor(best, m);
-    t = (start + uni(best.d)) % I;
+    best = wave_min_pd<64>(best);
+    if (lane == 0) part[tid >> 6] = best;
+    __syncthreads();  // the partial minima are written and every queue read
+    best = lane < NW ? part[lane] : MinPD{{0, 0}, 0x7FFFFFFF};
+    best = wave_min_pd<NW>(best);
+    t = start + uni(best.d);  // start, d < I
+    t = t >= I ? t - I : t;
     br = !follow_up ? SMETRIC_FIRST_TURN
                     : (!cached ? SMETRIC_EVICTED : (!meets_prev ? SMETRIC_MIGRATE : SMETRIC_MIGRATE_TPOT));
-    int32_t ct;
-    if (K > 0) {
-      int32_t v = 0;
-#pragma unroll
-      for (int k = 0; k < (K > 0 ? K : 1); ++k)
-        if (k == t / 64) v = row.v[k];
-      ct = uni(__shfl(v, t % 64, 64));
-    } else {
-      ct = uni(c[t]);
-    }
-    cost_t = t == prev ? cost_prev : est2(p, L, ct, 0);
   }
-  // one wavefront does every LDS access, in program order (see seq_decide)
-  const i128 old = q2[t];
-  const int64_t nold = nr[t];
-  target[r] = t;
-  branch[r] = br;
-  q2[t] = old + cost_t;  // the request's prefill joins its target's queue
-  nr[t] = nold + 1;      // and it is one more request there
+  if (tid == t % NT) {  // the target's owner: its prefill joins the queue, one more request there
+    const int kt = t / NT;
+    int32_t ct = 0;
+#pragma unroll
+    for (int k = 0; k < KT; ++k)
+      if (k == kt) ct = row.v[k];
+    q2[t] += t == prev ? row.rec.cost_prev : est2(p, L, ct, 0);
+    nr[t] += 1;
+    target[r] = t;
+    branch[r] = br;
+  }
+  __syncthreads();  // the queue, the count and the partial minima are settled for the next request
 }
 
-template <int K, int D>
+template <int NW, int KT, int D>
 __device__ __forceinline__ void seqc_exact_block(const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
-                                                 const RouteParams &p, uint64_t rr_base, bool st_ok,
-                                                 const SeqCRec *__restrict__ recs, i128 *q2, int64_t *nr,
-                                                 const int64_t *sl, int32_t *__restrict__ target,
-                                                 uint8_t *__restrict__ branch, int32_t rs, int32_t re) {
-  SeqCRow<K> ring[D];
+                                                 const RouteParams &p, bool st_ok,
+                                                 const SeqCRec *__restrict__ recs, i128 *q2, uint32_t *nr,
+                                                 const int64_t (&sl)[KT], MinPD *part,
+                                                 int32_t *__restrict__ target, uint8_t *__restrict__ branch,
+                                                 int32_t rs, int32_t re) {
+  SeqCRow<KT> ring[D];
 #pragma unroll
-  for (int d = 0; d < D; ++d) seqc_load<K>(matched, I, rs + d, n_req, recs, ring[d]);
+  for (int d = 0; d < D; ++d) seqc_load<NW, KT>(matched, I, rs + d, n_req, recs, ring[d]);
   for (int32_t r0 = rs; r0 < re; r0 += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int32_t r = r0 + d;
       if (r < re) {
-        seqc_decide<K>(ring[d], matched, r, I, p, rr_base, st_ok, q2, nr, sl, target, branch);
-        seqc_load<K>(matched, I, r + D, n_req, recs, ring[d]);
+        seqc_decide<NW, KT>(ring[d], r, I, p, st_ok, q2, nr, sl, part, target, branch);
+        seqc_load<NW, KT>(matched, I, r + D, n_req, recs, ring[d]);
       }
     }
   }
 }
 
-// The batch in steps of 64 requests, one per lane, as route_seq_kernel: a cached follow-up
-// whose prev is a candidate sticks iff prev meets its deadline on its exact load (prev's
-// load plus the costs of the step's earlier requests with that prev, all of which stuck if
-// the step got that far); the requests before the first one not settled are decided
-// together -- each group's last one writing prev's load and count -- that one alone, and
-// the next step starts after it.  Two steps in a row that settle nothing: the next 64
-// go through the sequential rule with prefetching.
-template <int K, int D>
-__global__ __launch_bounds__(64) void route_seqc_kernel(const int32_t *__restrict__ matched, int32_t n_req,
-                                                        int32_t I, const int64_t *__restrict__ q,
-                                                        const int64_t *__restrict__ slack,
-                                                        const int32_t *__restrict__ n_run, RouteParams p,
-                                                        uint64_t rr_base, const SeqCRec *__restrict__ recs,
-                                                        int32_t *__restrict__ target, uint8_t *__restrict__ branch,
-                                                        int64_t *__restrict__ q_out, int64_t *__restrict__ n_out) {
+// The batch in steps of 64 requests, one per lane of wavefront 0, as route_seq_kernel: a
+// cached follow-up whose prev is a candidate sticks iff prev meets its deadline on its exact
+// load (prev's load plus the costs of the step's earlier requests with that prev, all of
+// which stuck if the step got that far); the requests before the first one not settled are
+// decided together -- each group's last one writing prev's load and count -- and that one
+// by the whole workgroup, and the next step starts after it.  Two steps in a row that
+// settle nothing: the next 64 requests are decided one by one with prefetching.
+template <int NW, int KT, int D>
+__global__ __launch_bounds__(64 * NW) void route_seqc_kernel(const int32_t *__restrict__ matched, int32_t n_req,
+                                                             int32_t I, const int64_t *__restrict__ q,
+                                                             const int64_t *__restrict__ slack,
+                                                             const int32_t *__restrict__ n_run, RouteParams p,
+                                                             const SeqCRec *__restrict__ recs,
+                                                             int32_t *__restrict__ target,
+                                                             uint8_t *__restrict__ branch, int64_t *__restrict__ q_out,
+                                                             int64_t *__restrict__ n_out) {
+  constexpr int NT = 64 * NW;
   __shared__ i128 q2[SEQC_MAX_I];
-  __shared__ int64_t nr[SEQC_MAX_I];
-  __shared__ int64_t sl[SEQC_MAX_I];
+  __shared__ uint32_t nr[SEQC_MAX_I];    // n_running + requests added: below 2^31 + 2^31
   __shared__ uint32_t n_on[SEQC_MAX_I];  // step requests per prev (0 between steps)
-  const int lane = threadIdx.x;
-  bool st_ok = true;
-  for (int32_t i = lane; i < I; i += 64) {
-    const int64_t qi = q[i];
-    const int32_t ni = n_run[i];
-    if (qi < 0 || qi >= (int64_t(1) << 62) || ni < 0) st_ok = false;
-    q2[i] = i128(2) * qi;
-    nr[i] = ni;
-    sl[i] = slack[i];
-    n_on[i] = 0;
+  __shared__ MinPD part[NW];
+  __shared__ int32_t step_f;
+  const int tid = threadIdx.x, lane = tid & 63;
+  int64_t sl[KT];
+  int ok_st = 1;
+#pragma unroll
+  for (int k = 0; k < KT; ++k) {
+    const int32_t i = tid + NT * k;
+    sl[k] = 0;
+    if (i < I) {
+      const int64_t qi = q[i];
+      const int32_t ni = n_run[i];
+      if (qi < 0 || qi >= (int64_t(1) << 62) || ni < 0) ok_st = 0;
+      q2[i] = i128(2) * qi;
+      nr[i] = uint32_t(ni);
+      n_on[i] = 0;
+      sl[k] = slack[i];
+    }
   }
-  st_ok = __ballot(!st_ok) == 0;
-  __syncthreads();
+  const bool st_ok = __syncthreads_and(ok_st) != 0;
   const bool slack_inf = p.slack_den == 0;
   int32_t r0 = 0;
   int streak = 0;
   while (r0 < n_req) {
     if (streak >= 2) {
       const int32_t re = n_req - r0 < 64 ? n_req : r0 + 64;
-      seqc_exact_block<K, D>(matched, n_req, I, p, rr_base, st_ok, recs, q2, nr, sl, target, branch, r0, re);
+      seqc_exact_block<NW, KT, D>(matched, n_req, I, p, st_ok, recs, q2, nr, sl, part, target, branch, r0,
+                                  re);
       r0 = re;
       streak = 0;
       continue;
     }
     const int32_t nv = n_req - r0 < 64 ? n_req - r0 : 64;
-    const int32_t r = r0 + lane;
-    int32_t rv = r < n_req ? r : n_req - 1;
-    asm volatile("" : "+v"(rv));  // a vector load: see seq_load
-    const SeqCRec rec = recs[rv];
-    const bool in = lane < nv;
-    const bool ok = st_ok && (rec.flags & 1);
-    const bool sticky = ok && (rec.flags & 2) && (rec.flags & 4) && (rec.flags & 8);
-    const int32_t prev = rec.prev;
-    const bool mine = in && sticky;
-    if (mine) atomicAdd(&n_on[prev], 1u);
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    uint64_t todo = __ballot(mine && n_on[prev] > 1);
-    __builtin_amdgcn_wave_barrier();
-    if (mine) n_on[prev] = 0;
-    i128 excl = 0;
-    uint64_t group = 0;  // lanes with my prev (0: nobody else has it)
-    while (todo) {
-      const int32_t p0 = __builtin_amdgcn_readlane(prev, __builtin_ctzll(todo));
-      const uint64_t m = __ballot(mine && prev == p0);
-      todo &= ~m;
-      i128 run = 0;
-      for (uint64_t mm = m; mm; mm &= mm - 1) {
-        const int l = __builtin_ctzll(mm);
-        if (lane == l) {
-          excl = run;
-          group = m;
+    if (tid < 64) {  // wavefront 0 settles the step's sticky requests
+      const int32_t r = r0 + lane;
+      int32_t rv = r < n_req ? r : n_req - 1;
+      asm volatile("" : "+v"(rv));  // a vector load: see seq_load
+      const SeqCRec rec = recs[rv];
+      const bool in = lane < nv;
+      const bool ok = st_ok && (rec.flags & 1);
+      const bool sticky = ok && (rec.flags & 2) && (rec.flags & 4) && (rec.flags & 8);
+      const int32_t prev = rec.prev;
+      const bool mine = in && sticky;
+      if (mine) atomicAdd(&n_on[prev], 1u);
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      uint64_t todo = __ballot(mine && n_on[prev] > 1);
+      __builtin_amdgcn_wave_barrier();
+      if (mine) n_on[prev] = 0;
+      i128 excl = 0;
+      uint64_t group = 0;  // lanes with my prev (0: nobody else has it)
+      while (todo) {
+        const int32_t p0 = __builtin_amdgcn_readlane(prev, __builtin_ctzll(todo));
+        const uint64_t m = __ballot(mine && prev == p0);
+        todo &= ~m;
+        i128 run = 0;
+        for (uint64_t mm = m; mm; mm &= mm - 1) {
+          const int l = __builtin_ctzll(mm);
+          if (lane == l) {
+            excl = run;
+            group = m;
+          }
+          run += readlane128(rec.cost_prev, l);
         }
-        run += readlane128(rec.cost_prev, l);
       }
+      const i128 q_prev = (mine ? q2[prev] : i128(0)) + excl;
+      bool settled = !ok;  // out of domain: settled, nothing queued
+      uint8_t br = SMETRIC_INVALID;
+      if (sticky && (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound)) {
+        settled = true;
+        br = SMETRIC_STICK;
+      }
+      const uint64_t open = __ballot(in && !settled);
+      const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
+      if (lane < f) {
+        target[r] = ok ? prev : -1;
+        branch[r] = br;
+      }
+      const uint64_t decided = f >= 64 ? ~uint64_t(0) : (uint64_t(1) << f) - 1;
+      const uint64_t after_me = lane == 63 ? uint64_t(0) : ~((uint64_t(2) << lane) - 1);
+      const bool last = mine && lane < f && (group & after_me & decided) == 0;
+      const uint32_t added = group ? __popcll(group & decided) : 1;  // the group's requests decided here
+      __builtin_amdgcn_wave_barrier();
+      if (last) {
+        q2[prev] = q_prev + rec.cost_prev;
+        nr[prev] = nr[prev] + added;
+      }
+      if (lane == 0) step_f = f;
     }
-    const i128 q_prev = (mine ? q2[prev] : i128(0)) + excl;
-    bool settled = !ok;  // out of domain: settled, nothing queued
-    uint8_t br = SMETRIC_INVALID;
-    if (sticky && (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound)) {
-      settled = true;
-      br = SMETRIC_STICK;
-    }
-    const uint64_t open = __ballot(in && !settled);
-    const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
-    SeqCRow<K> row;
-    if (f < nv) seqc_load<K>(matched, I, r0 + f, n_req, recs, row);
-    if (lane < f) {
-      target[r] = ok ? prev : -1;
-      branch[r] = br;
-    }
-    const uint64_t decided = f >= 64 ? ~uint64_t(0) : (uint64_t(1) << f) - 1;
-    const uint64_t after_me = lane == 63 ? uint64_t(0) : ~((uint64_t(2) << lane) - 1);
-    const bool last = mine && lane < f && (group & after_me & decided) == 0;
-    const int64_t added = group ? __popcll(group & decided) : 1;  // the group's requests decided here
-    __builtin_amdgcn_wave_barrier();
-    if (last) {
-      q2[prev] = q_prev + rec.cost_prev;
-      nr[prev] = nr[prev] + added;
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __syncthreads();  // the step's queues and f are settled for every wavefront
+    const int32_t f = step_f;
     r0 += f;
     if (f < nv) {  // the first request not settled: the sequential rule
-      seqc_decide<K>(row, matched, r0, I, p, rr_base, st_ok, q2, nr, sl, target, branch);
+      SeqCRow<KT> row;
+      seqc_load<NW, KT>(matched, I, r0, n_req, recs, row);
+      seqc_decide<NW, KT>(row, r0, I, p, st_ok, q2, nr, sl, part, target, branch);
       r0 += 1;
       streak = f == 0 ? streak + 1 : 0;
     }
+    __syncthreads();  // step_f is read by every wavefront before wavefront 0 writes the next
   }
   __syncthreads();
-  for (int32_t i = lane; i < I; i += 64) {
+  for (int32_t i = tid; i < I; i += NT) {
     if (q_out) {
       const i128 v = q2[i] >> 1;
       q_out[i] = v > i128(INT64_MAX) ? INT64_MAX : int64_t(v);
     }
-    if (n_out) n_out[i] = nr[i];
+    if (n_out) n_out[i] = st_ok ? int64_t(nr[i]) : int64_t(n_run[i]);  // an invalid state is echoed as given
   }
 }
 
@@ -1083,19 +1148,16 @@ extern "C" int smetric_route_seq_coloc(const int32_t *matched, int32_t n_req, in
   SeqCRec *recs = static_cast<SeqCRec *>(workspace);
   if (n_req > 0)
     hipLaunchKernelGGL(route_seqc_prep_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched,
-                       n_req, n_instances, prompt_len, hist_len, turn, tpot_slack, rp, recs);
-  const int kk = (n_instances + 63) / 64;
-#define SEQC_LAUNCH(K, D)                                                                                        \
-  hipLaunchKernelGGL((route_seqc_kernel<K, D>), dim3(1), dim3(64), 0, stream, matched, n_req, n_instances, q,      \
-                     tpot_slack, n_running, rp, rr_base, recs, target, branch, q_out, n_out)
-  // prefetch depth D: D * (K + 3) vector loads in flight (K row words and a 48-byte record
-  // per request) stay within the 63 the wait counter tracks
-  if (kk <= 1) SEQC_LAUNCH(1, 8);
-  else if (kk <= 2) SEQC_LAUNCH(2, 8);
-  else if (kk <= 4) SEQC_LAUNCH(4, 7);
-  else if (kk <= 8) SEQC_LAUNCH(8, 5);
-  else if (kk <= 16) SEQC_LAUNCH(16, 3);
-  else SEQC_LAUNCH(0, 8);
+                       n_req, n_instances, prompt_len, hist_len, turn, tpot_slack, rp, rr_base, recs);
+#define SEQC_LAUNCH(NW, KT, D)                                                                                   \
+  hipLaunchKernelGGL((route_seqc_kernel<NW, KT, D>), dim3(1), dim3(64 * NW), 0, stream, matched, n_req,          \
+                     n_instances, q, tpot_slack, n_running, rp, recs, target, branch, q_out, n_out)
+  // one workgroup; instances per thread KT <= 4 (SEQC_MAX_I = 4 x 1024).  Prefetch depth D:
+  // D * (KT + 3) vector loads in flight (KT row words and a 48-byte record per request)
+  if (n_instances <= 256) SEQC_LAUNCH(4, 1, 4);
+  else if (n_instances <= 1024) SEQC_LAUNCH(8, 2, 4);
+  else if (n_instances <= 2048) SEQC_LAUNCH(16, 2, 4);
+  else SEQC_LAUNCH(16, 4, 2);
 #undef SEQC_LAUNCH
   return hip_rc(hipGetLastError());
 }
@@ -1122,11 +1184,11 @@ extern "C" int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t 
   SeqRec *recs = static_cast<SeqRec *>(workspace);
   if (n_req > 0)
     hipLaunchKernelGGL(route_seq_prep_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
-                       n_instances, prompt_len, hist_len, turn, q, rp, recs);
+                       n_instances, prompt_len, hist_len, turn, q, rp, rr_base, recs);
   const int kk = (n_instances + 63) / 64;
 #define SEQ_LAUNCH(K, D)                                                                                       \
   hipLaunchKernelGGL((route_seq_kernel<K, D>), dim3(1), dim3(64), 0, stream, matched, n_req, n_instances,         \
-                     q, rp, rr_base, recs, target, branch, q_out)
+                     q, rp, recs, target, branch, q_out)
   // prefetch depth D: D * (K + 4) vector loads in flight (K row words and a 64-byte
   // record per request) stay within the 63 the wait counter tracks
   if (kk <= 1) SEQ_LAUNCH(1, 8);
