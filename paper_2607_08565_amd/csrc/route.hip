@@ -911,18 +911,15 @@ __device__ __forceinline__ void seqc_exact_block(const int32_t *__restrict__ mat
                                                  const int64_t (&sl)[KT], MinPD *part,
                                                  int32_t *__restrict__ target, uint8_t *__restrict__ branch,
                                                  int32_t rs, int32_t re) {
+  // the ring shifts by one register copy per request, so the decision is inlined once
   SeqCRow<KT> ring[D];
 #pragma unroll
   for (int d = 0; d < D; ++d) seqc_load<NW, KT>(matched, I, rs + d, n_req, recs, ring[d]);
-  for (int32_t r0 = rs; r0 < re; r0 += D) {
+  for (int32_t r = rs; r < re; ++r) {
+    seqc_decide<NW, KT>(ring[0], r, I, p, st_ok, q2, nr, sl, part, target, branch);
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int32_t r = r0 + d;
-      if (r < re) {
-        seqc_decide<NW, KT>(ring[d], r, I, p, st_ok, q2, nr, sl, part, target, branch);
-        seqc_load<NW, KT>(matched, I, r + D, n_req, recs, ring[d]);
-      }
-    }
+    for (int d = 0; d + 1 < D; ++d) ring[d] = ring[d + 1];
+    seqc_load<NW, KT>(matched, I, r + D, n_req, recs, ring[D - 1]);
   }
 }
 
