@@ -515,6 +515,7 @@ def measure_variants(setup, b: int, reps: int = 20):
     inputs["route_seq"] = (st, br.cpu().numpy(), q_out.cpu().numpy(), b)
     # the colocated rule, one request at a time: the queue and the request counts update
     n_out = torch.empty(I, dtype=torch.int64, device="cuda")
+    ws = torch.empty(S.route_seq_coloc_ws_bytes(R, I), dtype=torch.uint8, device="cuda")
     call = lambda: S.route_seq_coloc(setup.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], d_slack, d_run,
                                      W.DEFAULT_PARAMS, tb.batch.rr_base, target=tgt, branch=br, q_out=q_out,
                                      n_out=n_out, workspace=ws)

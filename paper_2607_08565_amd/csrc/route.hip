@@ -644,12 +644,13 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
 //   prep  one wavefront per request: domain, prev = argmax c, session_cached, follow-up,
 //         whether prev is a candidate (passes the TPOT filter, or no instance does), the
 //         cost on prev and the deadline -- none of it depends on the running state.
-//   seq   ONE workgroup; 2q and n in LDS, the slacks in the registers of the instances'
-//         threads.  A cached follow-up whose prev is a candidate sticks iff prev meets its
-//         deadline, which needs only prev's load: wavefront 0 settles 64 requests per step
-//         as in route_seq_kernel (the step's earlier requests with the same prev add their
-//         costs); the first request not settled is decided by the whole workgroup, each
-//         thread scoring its instances, then a wavefront and a cross-wavefront minimum.
+//   rank  per request, its best candidates on a state shortly before its decision (see
+//         the speculative blocks below), many workgroups at once.
+//   seq   ONE wavefront with 2q and n in LDS.  A cached follow-up whose prev is a
+//         candidate sticks iff prev meets its deadline, which needs only prev's load: 64
+//         requests are settled per step as in route_seq_kernel (the step's earlier
+//         requests with the same prev add their costs); the first request not settled is
+//         decided by rescoring its listed candidates on the current state.
 //         The scores est2 x n are compared in 192 bits: over a batch both factors grow.
 // ---------------------------------------------------------------------------------
 constexpr int SEQC_MAX_I = 4096;  // LDS: 2q (64 KB), n and the step counters (16 KB each)
@@ -663,7 +664,6 @@ struct SeqCRec {
   i128 cost_prev;  // 2 x prefill_cost(req, c[prev])
   i128 bound;      // SLACK_num x 2 (b + a L)
 };
-static_assert(sizeof(SeqCRec) <= sizeof(SeqRec), "the workspace of smetric_route_seq fits both rules");
 
 __device__ __forceinline__ bool tpot_pass(int64_t slack, i128 cost2) {
   return slack >= NO_DECODE || cost2 <= i128(2) * slack;
@@ -777,6 +777,22 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
          uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
 }
 
+// Lexicographic minimum of (k1, k0) over lanes 0..N-1 (N = 64: the wavefront; N <= 16:
+// within row 0) by DPP moves toward lane N - 1; every lane gets it.
+template <int N>
+__device__ __forceinline__ void wave_min_key(uint64_t &k1, uint64_t &k0) {
+  if (N > 1) dpp_min_key<0x111, 0xF>(k1, k0);
+  if (N > 2) dpp_min_key<0x112, 0xF>(k1, k0);
+  if (N > 4) dpp_min_key<0x114, 0xF>(k1, k0);
+  if (N > 8) dpp_min_key<0x118, 0xF>(k1, k0);
+  if (N > 16) {
+    dpp_min_key<0x142, 0xA>(k1, k0);  // row_bcast:15 into rows 1 and 3
+    dpp_min_key<0x143, 0xC>(k1, k0);  // row_bcast:31 into rows 2 and 3
+  }
+  k1 = readlane64(k1, N - 1);
+  k0 = readlane64(k0, N - 1);
+}
+
 // Minimum of (score, d) over lanes 0..N-1 (N = 64: the wavefront; N <= 16: within row 0);
 // every lane gets it.  While every score is below 2^96 the pair is compared as two 64-bit
 // words (score bits 32..95; score bits 0..31 and d) and reduced with DPP moves toward lane
@@ -790,16 +806,7 @@ __device__ __forceinline__ MinPD wave_min_pd(MinPD a) {
       k1 = (uint64_t(a.s.hi) << 32) | (a.s.lo >> 32);
       k0 = (a.s.lo << 32) | uint32_t(a.d);
     }
-    if (N > 1) dpp_min_key<0x111, 0xF>(k1, k0);
-    if (N > 2) dpp_min_key<0x112, 0xF>(k1, k0);
-    if (N > 4) dpp_min_key<0x114, 0xF>(k1, k0);
-    if (N > 8) dpp_min_key<0x118, 0xF>(k1, k0);
-    if (N > 16) {
-      dpp_min_key<0x142, 0xA>(k1, k0);  // row_bcast:15 into rows 1 and 3
-      dpp_min_key<0x143, 0xC>(k1, k0);  // row_bcast:31 into rows 2 and 3
-    }
-    k1 = readlane64(k1, N - 1);
-    k0 = readlane64(k0, N - 1);
+    wave_min_key<N>(k1, k0);
     if (k0 == ~uint64_t(0)) return MinPD{{0, 0}, 0x7FFFFFFF};
     return MinPD{{u128(k1 >> 32), (k1 << 32) | (k0 >> 32)}, int32_t(uint32_t(k0))};
   }
@@ -811,247 +818,403 @@ __device__ __forceinline__ MinPD wave_min_pd(MinPD a) {
   return r;
 }
 
-// The sequential kernel runs as one workgroup of NW wavefronts.  Instance i belongs to
-// thread i mod (64 NW): that thread holds the instance's decode slack and its matched-prefix
-// values of the prefetched requests in registers, scores it, and is the one that adds a
-// request's prefill to the instance's queue (so a queue is written by one thread only, and
-// read by others only across a barrier).
-template <int KT>
-struct SeqCRow {
-  int32_t v[KT];  // c[r][tid + 64 NW k]
-  SeqCRec rec;
-};
+// ---------------------------------------------------------------------------------
+// Speculative blocks.  A decision adds to one instance's queue and count, so it raises
+// that instance's score and no other.  Requests are taken in blocks of SQW.  Launch L runs
+// two kinds of workgroup on the state X_L it starts from (the queues and counts after
+// blocks 0 .. L-2): ranking workgroups list, for every request of block L, its SQK best
+// candidates on X_L; the deciding workgroup decides block L-1 starting from X_L and writes
+// X_{L+1}.  When a request of block L is decided (launch L+1), the instances whose scores
+// have changed since X_L are those updated by block L-1 and by the earlier requests of
+// block L: at most 2 SQW - 1 < SQK.  So some listed candidate e* still has its X_L score,
+// and every unlisted candidate x scores at least its X_L score, which is above e*'s (the
+// keys (score, rotation distance) are distinct): the minimum over all candidates is the
+// minimum over the list, rescored on the current state.  Nothing is approximated.
+// ---------------------------------------------------------------------------------
+constexpr int SQW = 64;       // requests per block
+constexpr int SQK = 2 * SQW;  // listed candidates per request
+constexpr int SQT = 1024;     // threads per workgroup of the block kernel
+constexpr int SQ_NP = SEQC_MAX_I;
+static_assert(SQ_NP <= 4096, "rotation distances are packed in 12 bits");
 
-template <int NW, int KT>
-__device__ __forceinline__ void seqc_load(const int32_t *__restrict__ matched, int32_t I, int32_t r, int32_t n_req,
-                                          const SeqCRec *__restrict__ recs, SeqCRow<KT> &row) {
-  const int tid = threadIdx.x;  // clamped, unconditional loads: see seq_load
-  const int32_t rr = r < n_req ? r : n_req - 1;
-  const int32_t *c = matched + int64_t(rr) * I;
-#pragma unroll
-  for (int k = 0; k < KT; ++k) {
-    const int i = tid + 64 * NW * k;
-    row.v[k] = c[i < I ? i : I - 1];
+struct SeqCWs {
+  SeqCRec *recs;     // [n_req]
+  uint32_t *l_inst;  // [2][SQW][SQK] listed instances, by block parity, request in block, rank
+  i128 *l_cst;       // [2][SQW][SQK] their doubled prefill costs for the request
+  uint32_t *l_cnt;   // [2][SQW] entries listed
+  i128 *q2;          // [2][I] doubled queues; X_L is [L & 1]
+  uint32_t *nr;      // [2][I] request counts
+  int32_t *st;       // 1 iff the instance state given is in domain
+};
+inline uint64_t seqc_layout(int32_t n_req, int32_t I, SeqCWs *w, void *base) {
+  uint64_t off = 0;
+  auto take = [&](uint64_t bytes) {
+    const uint64_t o = off;
+    off = (off + bytes + 255) / 256 * 256;
+    return o;
+  };
+  const uint64_t R = uint64_t(n_req < 1 ? 1 : n_req), NI = uint64_t(I < 1 ? 1 : I);
+  const uint64_t o_rec = take(R * sizeof(SeqCRec)), o_li = take(4ull * 2 * SQW * SQK),
+                 o_lc = take(16ull * 2 * SQW * SQK), o_ln = take(4ull * 2 * SQW), o_q = take(16 * 2 * NI),
+                 o_n = take(4 * 2 * NI), o_st = take(4);
+  if (w) {
+    char *b = static_cast<char *>(base);
+    w->recs = reinterpret_cast<SeqCRec *>(b + o_rec);
+    w->l_inst = reinterpret_cast<uint32_t *>(b + o_li);
+    w->l_cst = reinterpret_cast<i128 *>(b + o_lc);
+    w->l_cnt = reinterpret_cast<uint32_t *>(b + o_ln);
+    w->q2 = reinterpret_cast<i128 *>(b + o_q);
+    w->nr = reinterpret_cast<uint32_t *>(b + o_n);
+    w->st = reinterpret_cast<int32_t *>(b + o_st);
   }
-  int32_t rv = rr;
-  asm volatile("" : "+v"(rv));  // a vector load on purpose: see seq_load
-  row.rec = recs[rv];
+  return off;
 }
 
-// Decide request r (every thread of the workgroup calls this with the same r and record;
-// the branches are uniform).  On return the target's queue and count include the request.
-template <int NW, int KT>
-__device__ __forceinline__ void seqc_decide(const SeqCRow<KT> &row, int32_t r, int32_t I, const RouteParams &p,
-                                            bool st_ok, i128 *q2, uint32_t *nr,
-                                            const int64_t (&sl)[KT], MinPD *part, int32_t *__restrict__ target,
-                                            uint8_t *__restrict__ branch) {
-  constexpr int NT = 64 * NW;
-  const int tid = threadIdx.x, lane = tid & 63;
+// X_0: the doubled queues and the counts given, and whether they are in domain.
+__global__ __launch_bounds__(SQT) void route_seqc_init_kernel(int32_t I, const int64_t *__restrict__ q,
+                                                              const int32_t *__restrict__ n_run, SeqCWs w) {
+  int ok = 1;
+  for (int32_t i = threadIdx.x; i < I; i += SQT) {
+    const int64_t qi = q[i];
+    const int32_t ni = n_run[i];
+    if (qi < 0 || qi >= (int64_t(1) << 62) || ni < 0) ok = 0;
+    w.q2[i] = i128(2) * qi;
+    w.nr[i] = uint32_t(ni);
+  }
+  ok = __syncthreads_and(ok);
+  if (threadIdx.x == 0) *w.st = ok;
+}
+
+// Ranking: request j of block L, on X_L.  Every candidate's key (score x 2^12 + rotation
+// distance; the score is below 2^160, so the key fits three words) goes into LDS, the
+// keys are sorted (bitonic, ascending; non-candidates and padding are all ones), and the
+// first SQK candidates are listed with their costs.
+__device__ __forceinline__ void seqc_rank(int32_t L, const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
+                                          const int64_t *__restrict__ slack, const RouteParams &p, const SeqCWs &w,
+                                          uint64_t *smem) {
+  const int tid = threadIdx.x;
+  const int32_t j = int32_t(blockIdx.x) - 1;
+  const int32_t r = L * SQW + j;
+  if (r >= n_req) return;  // whole workgroup
+  const uint64_t le = uint64_t((L & 1) * SQW + j);
+  const SeqCRec rec = w.recs[r];
+  if (!*w.st || !(rec.flags & 1)) {  // out of domain: decided without a list
+    if (tid == 0) w.l_cnt[le] = 0;
+    return;
+  }
+  const int64_t Lr = rec.L;
+  const int32_t start = rec.start;
+  const bool any_pass = rec.flags & 16;
+  const i128 *q2 = w.q2 + uint64_t(L & 1) * I;
+  const uint32_t *nr = w.nr + uint64_t(L & 1) * I;
+  const int32_t *c = matched + int64_t(r) * I;
+  int NP = 2;
+  while (NP < I) NP <<= 1;
+  uint64_t *k2 = smem, *k1 = smem + SQ_NP, *k0 = smem + 2 * SQ_NP;
+  for (int32_t i = tid; i < NP; i += SQT) {
+    uint64_t a2 = ~uint64_t(0), a1 = ~uint64_t(0), a0 = ~uint64_t(0);
+    if (i < I) {
+      const i128 cst = est2(p, Lr, c[i], 0);
+      if (!any_pass || tpot_pass(slack[i], cst)) {
+        const P192 s = mul192(q2[i] + cst, nr[i]);
+        const uint64_t d = uint64_t(i >= start ? i - start : i - start + I);
+        const uint64_t h0 = uint64_t(s.hi), h1 = uint64_t(s.hi >> 64);
+        a0 = (s.lo << 12) | d;
+        a1 = (s.lo >> 52) | (h0 << 12);
+        a2 = (h0 >> 52) | (h1 << 12);  // below 2^44: no candidate's key is all ones
+      }
+    }
+    k2[i] = a2;
+    k1[i] = a1;
+    k0[i] = a0;
+  }
+  __syncthreads();
+  for (int size = 2; size <= NP; size <<= 1)
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int u = tid; u < NP / 2; u += SQT) {
+        const int a = ((u & ~(stride - 1)) << 1) | (u & (stride - 1)), b = a + stride;
+        const uint64_t a2 = k2[a], a1 = k1[a], a0 = k0[a], b2 = k2[b], b1 = k1[b], b0 = k0[b];
+        const bool b_less = b2 < a2 || (b2 == a2 && (b1 < a1 || (b1 == a1 && b0 < a0)));
+        if (b_less == ((a & size) == 0)) {
+          k2[a] = b2;
+          k1[a] = b1;
+          k0[a] = b0;
+          k2[b] = a2;
+          k1[b] = a1;
+          k0[b] = a0;
+        }
+      }
+      __syncthreads();
+    }
+  bool listed = false;
+  if (tid < SQK && tid < NP && !(k2[tid] == ~uint64_t(0) && k1[tid] == ~uint64_t(0) && k0[tid] == ~uint64_t(0))) {
+    listed = true;
+    int32_t inst = start + int32_t(k0[tid] & 4095);
+    inst = inst >= I ? inst - I : inst;
+    w.l_inst[le * SQK + tid] = uint32_t(inst);
+    w.l_cst[le * SQK + tid] = est2(p, Lr, c[inst], 0);
+  }
+  const int cnt = __syncthreads_count(listed);  // the listed entries are the first cnt
+  if (tid == 0) w.l_cnt[le] = uint32_t(cnt);
+}
+
+// A request to decide with its record and list (entries lane and lane + 64).
+struct SeqLRow {
+  SeqCRec rec;
+  uint32_t cnt;
+  uint32_t inst[2];
+  i128 cst[2];
+};
+__device__ __forceinline__ void seqc_lrow_load(int32_t r, int32_t re, const SeqCWs &w, SeqLRow &row) {
+  const int lane = threadIdx.x & 63;
+  int32_t rr = r < re ? r : re - 1;  // clamped, unconditional loads: see seq_load
+  asm volatile("" : "+v"(rr));       // vector loads on purpose: see seq_load
+  row.rec = w.recs[rr];
+  const uint64_t le = uint64_t(((rr / SQW) & 1) * SQW + rr % SQW);
+  row.cnt = w.l_cnt[le];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    row.inst[h] = w.l_inst[le * SQK + lane + 64 * h];
+    row.cst[h] = w.l_cst[le * SQK + lane + 64 * h];
+  }
+}
+
+// Decide request r alone on the current state (wavefront 0; uniform branches).
+__device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, int32_t I, const RouteParams &p,
+                                                 bool st_ok, i128 *q2, uint32_t *nr, int32_t *__restrict__ target,
+                                                 uint8_t *__restrict__ branch) {
+  const int lane = threadIdx.x & 63;
   const int32_t flags = uni(row.rec.flags);
   if (!st_ok || !(flags & 1)) {
-    if (tid == 0) {
+    if (lane == 0) {
       target[r] = -1;
       branch[r] = SMETRIC_INVALID;
     }
-    return;  // nothing queued: no barrier needed
+    return;
   }
   const int32_t prev = uni(row.rec.prev);
-  const int64_t L = uni(row.rec.L);
-  const bool cached = flags & 2, follow_up = flags & 4, prev_cand = flags & 8, any_pass = flags & 16;
+  const bool cached = flags & 2, follow_up = flags & 4, prev_cand = flags & 8;
   const bool slack_inf = p.slack_den == 0;
   const bool meets_prev = slack_inf || (q2[prev] + row.rec.cost_prev) * p.slack_den <= row.rec.bound;
   int32_t t;
   uint8_t br;
+  bool mine;     // this lane adds the request to t's queue and count
+  i128 cost = 0;
   if (follow_up && cached && meets_prev && prev_cand) {
     t = prev;
     br = SMETRIC_STICK;
-    __syncthreads();  // every thread has read prev's queue before its owner adds to it
+    mine = lane == 0;
+    cost = row.rec.cost_prev;
   } else {
-    // LMetric minimum over the candidates: the instances that pass the TPOT filter if any
-    // does (fixed per request: the slacks do not change), else all of them
     const int32_t start = uni(row.rec.start);
-    MinPD best{{0, 0}, 0x7FFFFFFF};
+    const int32_t cnt = uni(int32_t(row.cnt));
+    i128 a[2];
+    uint32_t n[2], d[2];
+    bool v[2], wide = false;
 #pragma unroll
-    for (int k = 0; k < KT; ++k) {
-      const int32_t i = tid + NT * k;
-      if (i < I) {
-        const i128 cst = est2(p, L, row.v[k], 0);
-        if (!any_pass || tpot_pass(sl[k], cst))
-          min_pd(best, mul192(q2[i] + cst, nr[i]), i >= start ? i - start : i - start + I);
-      }
+    for (int h = 0; h < 2; ++h) {
+      v[h] = lane + 64 * h < cnt;
+      const int32_t i = v[h] ? int32_t(row.inst[h]) : 0;
+      a[h] = q2[i] + row.cst[h];
+      n[h] = nr[i];
+      d[h] = uint32_t(i >= start ? i - start : i - start + I);
+      wide |= v[h] && (a[h] >> 64) != 0;
     }
-    best = wave_min_pd<64>(best);
-    if (lane == 0) part[tid >> 6] = best;
-    __syncthreads();  // the partial minima are written and every queue read
-    best = lane < NW ? part[lane] : MinPD{{0, 0}, 0x7FFFFFFF};
-    best = wave_min_pd<NW>(best);
-    t = start + uni(best.d);  // start, d < I
+    int32_t dmin;
+    if (__ballot(wide) == 0) {  // every listed queue below 2^64: scores below 2^96, two words
+      uint64_t k1 = ~uint64_t(0), k0 = ~uint64_t(0);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (v[h]) {
+          const uint64_t lo = uint64_t(a[h]);
+          const uint64_t p0 = uint64_t(uint32_t(lo)) * n[h];
+          const uint64_t p1 = (lo >> 32) * n[h] + (p0 >> 32);  // score = p1 2^32 + low word of p0
+          const uint64_t c0 = (p0 << 32) | d[h];
+          if (p1 < k1 || (p1 == k1 && c0 < k0)) {
+            k1 = p1;
+            k0 = c0;
+          }
+        }
+      wave_min_key<64>(k1, k0);
+      dmin = int32_t(uint32_t(k0));
+    } else {
+      MinPD best{{0, 0}, 0x7FFFFFFF};
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (v[h]) min_pd(best, mul192(a[h], n[h]), int32_t(d[h]));
+      best = wave_min_pd<64>(best);
+      dmin = best.d;
+    }
+    t = start + uni(dmin);  // start, d < I
     t = t >= I ? t - I : t;
     br = !follow_up ? SMETRIC_FIRST_TURN
                     : (!cached ? SMETRIC_EVICTED : (!meets_prev ? SMETRIC_MIGRATE : SMETRIC_MIGRATE_TPOT));
-  }
-  if (tid == t % NT) {  // the target's owner: its prefill joins the queue, one more request there
-    const int kt = t / NT;
-    int32_t ct = 0;
+    mine = false;
 #pragma unroll
-    for (int k = 0; k < KT; ++k)
-      if (k == kt) ct = row.v[k];
-    q2[t] += t == prev ? row.rec.cost_prev : est2(p, L, ct, 0);
+    for (int h = 0; h < 2; ++h)
+      if (lane + 64 * h < cnt && int32_t(row.inst[h]) == t) {
+        mine = true;
+        cost = row.cst[h];
+      }
+  }
+  __builtin_amdgcn_wave_barrier();
+  if (mine) {  // one lane: the listed instances are distinct
+    q2[t] += cost;
     nr[t] += 1;
     target[r] = t;
     branch[r] = br;
   }
-  __syncthreads();  // the queue, the count and the partial minima are settled for the next request
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
 }
 
-template <int NW, int KT, int D>
-__device__ __forceinline__ void seqc_exact_block(const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
-                                                 const RouteParams &p, bool st_ok,
-                                                 const SeqCRec *__restrict__ recs, i128 *q2, uint32_t *nr,
-                                                 const int64_t (&sl)[KT], MinPD *part,
-                                                 int32_t *__restrict__ target, uint8_t *__restrict__ branch,
-                                                 int32_t rs, int32_t re) {
-  // the ring shifts by one register copy per request, so the decision is inlined once
-  SeqCRow<KT> ring[D];
-#pragma unroll
-  for (int d = 0; d < D; ++d) seqc_load<NW, KT>(matched, I, rs + d, n_req, recs, ring[d]);
-  for (int32_t r = rs; r < re; ++r) {
-    seqc_decide<NW, KT>(ring[0], r, I, p, st_ok, q2, nr, sl, part, target, branch);
-#pragma unroll
-    for (int d = 0; d + 1 < D; ++d) ring[d] = ring[d + 1];
-    seqc_load<NW, KT>(matched, I, r + D, n_req, recs, ring[D - 1]);
-  }
-}
-
-// The batch in steps of 64 requests, one per lane of wavefront 0, as route_seq_kernel: a
-// cached follow-up whose prev is a candidate sticks iff prev meets its deadline on its exact
-// load (prev's load plus the costs of the step's earlier requests with that prev, all of
-// which stuck if the step got that far); the requests before the first one not settled are
-// decided together -- each group's last one writing prev's load and count -- and that one
-// by the whole workgroup, and the next step starts after it.  Two steps in a row that
-// settle nothing: the next 64 requests are decided one by one with prefetching.
-template <int NW, int KT, int D>
-__global__ __launch_bounds__(64 * NW) void route_seqc_kernel(const int32_t *__restrict__ matched, int32_t n_req,
-                                                             int32_t I, const int64_t *__restrict__ q,
-                                                             const int64_t *__restrict__ slack,
-                                                             const int32_t *__restrict__ n_run, RouteParams p,
-                                                             const SeqCRec *__restrict__ recs,
-                                                             int32_t *__restrict__ target,
-                                                             uint8_t *__restrict__ branch, int64_t *__restrict__ q_out,
-                                                             int64_t *__restrict__ n_out) {
-  constexpr int NT = 64 * NW;
-  __shared__ i128 q2[SEQC_MAX_I];
-  __shared__ uint32_t nr[SEQC_MAX_I];    // n_running + requests added: below 2^31 + 2^31
-  __shared__ uint32_t n_on[SEQC_MAX_I];  // step requests per prev (0 between steps)
-  __shared__ MinPD part[NW];
-  __shared__ int32_t step_f;
-  const int tid = threadIdx.x, lane = tid & 63;
-  int64_t sl[KT];
-  int ok_st = 1;
-#pragma unroll
-  for (int k = 0; k < KT; ++k) {
-    const int32_t i = tid + NT * k;
-    sl[k] = 0;
-    if (i < I) {
-      const int64_t qi = q[i];
-      const int32_t ni = n_run[i];
-      if (qi < 0 || qi >= (int64_t(1) << 62) || ni < 0) ok_st = 0;
-      q2[i] = i128(2) * qi;
-      nr[i] = uint32_t(ni);
-      n_on[i] = 0;
-      sl[k] = slack[i];
-    }
-  }
-  const bool st_ok = __syncthreads_and(ok_st) != 0;
+// Deciding: block L-1 in steps of up to 64 requests, one per lane, as route_seq_kernel (a
+// cached follow-up whose prev is a candidate sticks iff prev meets its deadline on its
+// exact load: prev's queue plus the costs of the step's earlier requests with that prev);
+// the first request not settled is decided by its list, and the next step starts after it.
+// After two steps that settle nothing, the next 64 requests go one by one with their
+// records and lists loaded D requests ahead.
+template <int D>
+__device__ __forceinline__ void seqc_decide_block(int32_t bs, int32_t be, int32_t I, const RouteParams &p,
+                                                  const SeqCWs &w, i128 *q2, uint32_t *nr, uint32_t *n_on,
+                                                  int32_t *__restrict__ target, uint8_t *__restrict__ branch) {
+  const int lane = threadIdx.x & 63;
+  const bool st_ok = *w.st != 0;
   const bool slack_inf = p.slack_den == 0;
-  int32_t r0 = 0;
+  int32_t r0 = bs;
   int streak = 0;
-  while (r0 < n_req) {
+  while (r0 < be) {
     if (streak >= 2) {
-      const int32_t re = n_req - r0 < 64 ? n_req : r0 + 64;
-      seqc_exact_block<NW, KT, D>(matched, n_req, I, p, st_ok, recs, q2, nr, sl, part, target, branch, r0,
-                                  re);
+      const int32_t re = be - r0 < 64 ? be : r0 + 64;
+      // ring slots are used in place (no register copies, which would have to wait for the
+      // newest loads) and refilled unconditionally (clamped): a load under a branch is
+      // waited for at the join
+      SeqLRow ring[D];
+#pragma unroll
+      for (int d = 0; d < D; ++d) seqc_lrow_load(r0 + d, be, w, ring[d]);
+      for (int32_t r = r0; r < re; r += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+          if (r + d < re) seqc_list_decide(ring[d], r + d, I, p, st_ok, q2, nr, target, branch);
+          seqc_lrow_load(r + d + D, be, w, ring[d]);
+        }
+      }
       r0 = re;
       streak = 0;
       continue;
     }
-    const int32_t nv = n_req - r0 < 64 ? n_req - r0 : 64;
-    if (tid < 64) {  // wavefront 0 settles the step's sticky requests
-      const int32_t r = r0 + lane;
-      int32_t rv = r < n_req ? r : n_req - 1;
-      asm volatile("" : "+v"(rv));  // a vector load: see seq_load
-      const SeqCRec rec = recs[rv];
-      const bool in = lane < nv;
-      const bool ok = st_ok && (rec.flags & 1);
-      const bool sticky = ok && (rec.flags & 2) && (rec.flags & 4) && (rec.flags & 8);
-      const int32_t prev = rec.prev;
-      const bool mine = in && sticky;
-      if (mine) atomicAdd(&n_on[prev], 1u);
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      uint64_t todo = __ballot(mine && n_on[prev] > 1);
-      __builtin_amdgcn_wave_barrier();
-      if (mine) n_on[prev] = 0;
-      i128 excl = 0;
-      uint64_t group = 0;  // lanes with my prev (0: nobody else has it)
-      while (todo) {
-        const int32_t p0 = __builtin_amdgcn_readlane(prev, __builtin_ctzll(todo));
-        const uint64_t m = __ballot(mine && prev == p0);
-        todo &= ~m;
-        i128 run = 0;
-        for (uint64_t mm = m; mm; mm &= mm - 1) {
-          const int l = __builtin_ctzll(mm);
-          if (lane == l) {
-            excl = run;
-            group = m;
-          }
-          run += readlane128(rec.cost_prev, l);
+    const int32_t nv = be - r0 < 64 ? be - r0 : 64;
+    const int32_t r = r0 + lane;
+    int32_t rv = r < be ? r : be - 1;
+    asm volatile("" : "+v"(rv));  // a vector load: see seq_load
+    const SeqCRec rec = w.recs[rv];
+    const bool in = lane < nv;
+    const bool ok = st_ok && (rec.flags & 1);
+    const bool sticky = ok && (rec.flags & 2) && (rec.flags & 4) && (rec.flags & 8);
+    const int32_t prev = rec.prev;
+    const bool mine = in && sticky;
+    if (mine) atomicAdd(&n_on[prev], 1u);
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    uint64_t todo = __ballot(mine && n_on[prev] > 1);
+    __builtin_amdgcn_wave_barrier();
+    if (mine) n_on[prev] = 0;
+    i128 excl = 0;
+    uint64_t group = 0;  // lanes with my prev (0: nobody else has it)
+    while (todo) {
+      const int32_t p0 = __builtin_amdgcn_readlane(prev, __builtin_ctzll(todo));
+      const uint64_t m = __ballot(mine && prev == p0);
+      todo &= ~m;
+      i128 run = 0;
+      for (uint64_t mm = m; mm; mm &= mm - 1) {
+        const int l = __builtin_ctzll(mm);
+        if (lane == l) {
+          excl = run;
+          group = m;
         }
+        run += readlane128(rec.cost_prev, l);
       }
-      const i128 q_prev = (mine ? q2[prev] : i128(0)) + excl;
-      bool settled = !ok;  // out of domain: settled, nothing queued
-      uint8_t br = SMETRIC_INVALID;
-      if (sticky && (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound)) {
-        settled = true;
-        br = SMETRIC_STICK;
-      }
-      const uint64_t open = __ballot(in && !settled);
-      const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
-      if (lane < f) {
-        target[r] = ok ? prev : -1;
-        branch[r] = br;
-      }
-      const uint64_t decided = f >= 64 ? ~uint64_t(0) : (uint64_t(1) << f) - 1;
-      const uint64_t after_me = lane == 63 ? uint64_t(0) : ~((uint64_t(2) << lane) - 1);
-      const bool last = mine && lane < f && (group & after_me & decided) == 0;
-      const uint32_t added = group ? __popcll(group & decided) : 1;  // the group's requests decided here
-      __builtin_amdgcn_wave_barrier();
-      if (last) {
-        q2[prev] = q_prev + rec.cost_prev;
-        nr[prev] = nr[prev] + added;
-      }
-      if (lane == 0) step_f = f;
     }
-    __syncthreads();  // the step's queues and f are settled for every wavefront
-    const int32_t f = step_f;
+    const i128 q_prev = (mine ? q2[prev] : i128(0)) + excl;
+    bool settled = !ok;  // out of domain: settled, nothing queued
+    uint8_t br = SMETRIC_INVALID;
+    if (sticky && (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound)) {
+      settled = true;
+      br = SMETRIC_STICK;
+    }
+    const uint64_t open = __ballot(in && !settled);
+    const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
+    SeqLRow row;
+    if (f < nv) seqc_lrow_load(r0 + f, be, w, row);
+    if (lane < f) {
+      target[r] = ok ? prev : -1;
+      branch[r] = br;
+    }
+    const uint64_t decided = f >= 64 ? ~uint64_t(0) : (uint64_t(1) << f) - 1;
+    const uint64_t after_me = lane == 63 ? uint64_t(0) : ~((uint64_t(2) << lane) - 1);
+    const bool last = mine && lane < f && (group & after_me & decided) == 0;
+    const uint32_t added = group ? __popcll(group & decided) : 1;  // the group's requests decided here
+    __builtin_amdgcn_wave_barrier();
+    if (last) {
+      q2[prev] = q_prev + rec.cost_prev;
+      nr[prev] = nr[prev] + added;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     r0 += f;
-    if (f < nv) {  // the first request not settled: the sequential rule
-      SeqCRow<KT> row;
-      seqc_load<NW, KT>(matched, I, r0, n_req, recs, row);
-      seqc_decide<NW, KT>(row, r0, I, p, st_ok, q2, nr, sl, part, target, branch);
+    if (f < nv) {  // the first request not settled: decided by its list
+      seqc_list_decide(row, r0, I, p, st_ok, q2, nr, target, branch);
       r0 += 1;
       streak = f == 0 ? streak + 1 : 0;
     }
-    __syncthreads();  // step_f is read by every wavefront before wavefront 0 writes the next
+  }
+}
+
+// Launch L: workgroup 0 decides block L-1 (L >= 1) and writes X_{L+1}; workgroups 1 ..
+// rank the requests of block L (L < number of blocks).
+__global__ __launch_bounds__(SQT) void route_seqc_block_kernel(int32_t L, const int32_t *__restrict__ matched,
+                                                               int32_t n_req, int32_t I,
+                                                               const int64_t *__restrict__ slack, RouteParams p,
+                                                               SeqCWs w, int32_t *__restrict__ target,
+                                                               uint8_t *__restrict__ branch) {
+  // ranking: three key words per instance; deciding: queues (16 B), counts and step counters
+  __shared__ uint64_t smem[3 * SQ_NP];
+  if (blockIdx.x > 0) {
+    seqc_rank(L, matched, n_req, I, slack, p, w, smem);
+    return;
+  }
+  i128 *q2 = reinterpret_cast<i128 *>(smem);
+  uint32_t *nr = reinterpret_cast<uint32_t *>(smem + 2 * SQ_NP);
+  uint32_t *n_on = nr + SQ_NP;
+  const uint64_t sx = uint64_t(L & 1) * I, sy = uint64_t((L + 1) & 1) * I;
+  for (int32_t i = threadIdx.x; i < I; i += SQT) {
+    q2[i] = w.q2[sx + i];
+    nr[i] = w.nr[sx + i];
+    n_on[i] = 0;
   }
   __syncthreads();
-  for (int32_t i = tid; i < I; i += NT) {
-    if (q_out) {
-      const i128 v = q2[i] >> 1;
-      q_out[i] = v > i128(INT64_MAX) ? INT64_MAX : int64_t(v);
-    }
-    if (n_out) n_out[i] = st_ok ? int64_t(nr[i]) : int64_t(n_run[i]);  // an invalid state is echoed as given
+  if (L >= 1 && threadIdx.x < 64) {
+    const int32_t bs = (L - 1) * SQW, be = n_req - bs < SQW ? n_req : bs + SQW;
+    seqc_decide_block<3>(bs, be, I, p, w, q2, nr, n_on, target, branch);
   }
+  __syncthreads();
+  for (int32_t i = threadIdx.x; i < I; i += SQT) {
+    w.q2[sy + i] = q2[i];
+    w.nr[sy + i] = nr[i];
+  }
+}
+
+__global__ void route_seqc_final_kernel(int32_t I, int32_t slot, SeqCWs w, const int64_t *__restrict__ q,
+                                        const int32_t *__restrict__ n_run, int64_t *__restrict__ q_out,
+                                        int64_t *__restrict__ n_out) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= I) return;
+  const bool ok = *w.st != 0;  // an invalid state is echoed as given
+  if (q_out) {
+    const i128 v = w.q2[uint64_t(slot) * I + i] >> 1;
+    q_out[i] = !ok ? q[i] : (v > i128(INT64_MAX) ? INT64_MAX : int64_t(v));
+  }
+  if (n_out) n_out[i] = ok ? int64_t(w.nr[uint64_t(slot) * I + i]) : int64_t(n_run[i]);
 }
 
 int route_params(const smetric_params *params, int32_t n_req, int32_t n_instances, RouteParams &rp) {
@@ -1139,24 +1302,30 @@ extern "C" int smetric_route_seq_coloc(const int32_t *matched, int32_t n_req, in
   if (n_instances > SEQC_MAX_I || !seq_loads_fit(rp, n_req)) return SMETRIC_EINVAL;
   if (!q || !tpot_slack || !n_running) return SMETRIC_EINVAL;
   if (n_req > 0 && (!matched || !prompt_len || !hist_len || !turn || !target || !branch)) return SMETRIC_EINVAL;
-  uint64_t need = 0;
-  smetric_route_seq_ws_bytes(n_req, &need);
+  const uint64_t need = seqc_layout(n_req, n_instances, nullptr, nullptr);
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) || ws_bytes < need) return SMETRIC_EWORKSPACE;
-  SeqCRec *recs = static_cast<SeqCRec *>(workspace);
+  SeqCWs w;
+  seqc_layout(n_req, n_instances, &w, workspace);
   if (n_req > 0)
     hipLaunchKernelGGL(route_seqc_prep_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched,
-                       n_req, n_instances, prompt_len, hist_len, turn, tpot_slack, rp, rr_base, recs);
-#define SEQC_LAUNCH(NW, KT, D)                                                                                   \
-  hipLaunchKernelGGL((route_seqc_kernel<NW, KT, D>), dim3(1), dim3(64 * NW), 0, stream, matched, n_req,          \
-                     n_instances, q, tpot_slack, n_running, rp, recs, target, branch, q_out, n_out)
-  // one workgroup; instances per thread KT <= 4 (SEQC_MAX_I = 4 x 1024).  Prefetch depth D:
-  // D * (KT + 3) vector loads in flight (KT row words and a 48-byte record per request)
-  if (n_instances <= 256) SEQC_LAUNCH(4, 1, 4);
-  else if (n_instances <= 1024) SEQC_LAUNCH(8, 2, 4);
-  else if (n_instances <= 2048) SEQC_LAUNCH(16, 2, 4);
-  else SEQC_LAUNCH(16, 4, 2);
-#undef SEQC_LAUNCH
+                       n_req, n_instances, prompt_len, hist_len, turn, tpot_slack, rp, rr_base, w.recs);
+  hipLaunchKernelGGL(route_seqc_init_kernel, dim3(1), dim3(SQT), 0, stream, n_instances, q, n_running, w);
+  const int32_t n_blk = (n_req + SQW - 1) / SQW;
+  for (int32_t L = 0; L <= n_blk; ++L) {
+    const int32_t rank = L < n_blk ? (n_req - L * SQW < SQW ? n_req - L * SQW : SQW) : 0;
+    hipLaunchKernelGGL(route_seqc_block_kernel, dim3(1 + rank), dim3(SQT), 0, stream, L, matched, n_req,
+                       n_instances, tpot_slack, rp, w, target, branch);
+  }
+  if (q_out || n_out)
+    hipLaunchKernelGGL(route_seqc_final_kernel, dim3((n_instances + 255) / 256), dim3(256), 0, stream, n_instances,
+                       (n_blk + 1) & 1, w, q, n_running, q_out, n_out);
   return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_route_seq_coloc_ws_bytes(int32_t n_req, int32_t n_instances, uint64_t *ws_bytes) {
+  if (n_req < 0 || n_instances < 1 || n_instances > SEQC_MAX_I || !ws_bytes) return SMETRIC_EINVAL;
+  *ws_bytes = seqc_layout(n_req, n_instances, nullptr, nullptr);
+  return SMETRIC_OK;
 }
 
 extern "C" int smetric_route_seq_ws_bytes(int32_t n_req, uint64_t *ws_bytes) {

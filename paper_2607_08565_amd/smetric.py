@@ -63,6 +63,7 @@ def _load() -> C.CDLL:
         "smetric_route": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_route_coloc": [P, I32, I32, P, P, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
         "smetric_route_seq_ws_bytes": [I32, P],
+        "smetric_route_seq_coloc_ws_bytes": [I32, I32, P],
         "smetric_route_loadaware": [P, I32, I32, P, P, P, P, P, I32, I32, C.POINTER(_Params), U64, P, P, P],
         "smetric_imbalance_ws_bytes": [I32, I32, P],
         "smetric_imbalance": [P, P, P, I64, I32, I64, I32, P, P, P, P, U64, P],
@@ -100,6 +101,7 @@ EXPORTED = (
     "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq", "smetric_sessions_ws_bytes",
     "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
     "smetric_probe_partition", "smetric_probe_lookup", "smetric_hash_partition", "smetric_route_seq_coloc",
+    "smetric_route_seq_coloc_ws_bytes",
 )
 
 
@@ -170,6 +172,12 @@ def route_seq_ws_bytes(n_req: int) -> int:
     return b.value
 
 
+def route_seq_coloc_ws_bytes(n_req: int, n_instances: int) -> int:
+    b = C.c_uint64(0)
+    _check("smetric_route_seq_coloc_ws_bytes", _lib.smetric_route_seq_coloc_ws_bytes(n_req, n_instances, C.byref(b)))
+    return b.value
+
+
 def route_seq(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
               q: torch.Tensor, params: dict, rr_base: int = 0, target: torch.Tensor | None = None,
               branch: torch.Tensor | None = None, q_out: torch.Tensor | None = None,
@@ -205,7 +213,7 @@ def route_seq_coloc(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: t
     branch = torch.empty(max(R, 1), dtype=torch.uint8, device=dev) if branch is None else branch
     q_out = torch.empty(I, dtype=torch.int64, device=dev) if q_out is None else q_out
     n_out = torch.empty(I, dtype=torch.int64, device=dev) if n_out is None else n_out
-    need = route_seq_ws_bytes(R)
+    need = route_seq_coloc_ws_bytes(R, I) if 1 <= I <= 4096 else 256  # else the call reports EINVAL
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     p = _Params(**params)

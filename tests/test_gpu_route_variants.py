@@ -299,6 +299,26 @@ def test_seqc_blocks_of_cached_follow_ups(I):
     assert {0, 2, 4, 255} <= seen
 
 
+@pytest.mark.parametrize("I", [129, 300, 1000])
+def test_seqc_identical_requests_exhaust_candidate_lists(I):
+    """Identical requests rank the instances alike, so the earlier requests of a block and of
+    the block before take the best listed candidates of the later ones: the regime where
+    the minimum over a request's list (its 128 best on the state before the previous block,
+    rescored) must still equal the minimum over all instances."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(900 + I)
+    R = 4000
+    m = np.zeros((R, I), np.int32)
+    L = np.full(R, 8192, np.int32)
+    z = np.zeros(R, np.int32)
+    for q, n_run in ((np.zeros(I, np.int64), np.zeros(I, np.int32)),
+                     (rng.integers(0, 10**9, I).astype(np.int64), rng.integers(0, 5, I).astype(np.int32))):
+        slack = np.full(I, oracle.NO_DECODE, np.int64)
+        ot, ob = _seqc_both(S, m, L, z, z, q, slack, n_run, W.DEFAULT_PARAMS, 11)
+        assert set(ob.tolist()) == {0}
+        assert len(np.unique(ot[:I])) > I // 2  # the first ones spread over the fleet
+
+
 def test_seqc_scores_past_128_bits_and_limits():
     """140,000 maximal prefills on two instances with nearly 2^31 requests each: the LMetric
     products pass 2^127, where only the exact comparison keeps both sides equal; then the
