@@ -395,12 +395,12 @@ int smetric_route_coloc(const int32_t *matched, int32_t n_req, int32_t n_instanc
  *   q_out      int64[n_instances] (out, optional: NULL) final loads in ns, rounded down
  *   n_out      int64[n_instances] (out, optional: NULL) final request counts
  *   workspace  >= smetric_route_seq_coloc_ws_bytes(n_req, n_instances) bytes, 256-B
- *              aligned (48 B per request, ~330 KB of candidate lists, 40 B per instance)
+ *              aligned (48 B per request, ~82 KB of candidate lists, 40 B per instance)
  * Other arguments, domains, branches and errors as smetric_route_coloc; n_instances must
  * be <= 4096 and the batch's loads representable as for smetric_route_seq (EINVAL
  * otherwise); EWORKSPACE for a short workspace.  Out-of-domain requests (branch 255)
- * change nothing.  The call enqueues about n_req / 64 + 4 kernel launches: requests are
- * decided in blocks of 64, each from a list of its 128 best candidates ranked on the state
+ * change nothing.  The call enqueues about n_req / 32 + 4 kernel launches: requests are
+ * decided in blocks of 32, each from a list of its 64 best candidates ranked on the state
  * before the previous block, which provably contains the exact minimum.
  * --------------------------------------------------------------------------------- */
 int smetric_route_seq_coloc_ws_bytes(int32_t n_req, int32_t n_instances, uint64_t *ws_bytes /* host */);

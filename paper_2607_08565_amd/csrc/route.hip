@@ -831,8 +831,9 @@ __device__ __forceinline__ MinPD wave_min_pd(MinPD a) {
 // keys (score, rotation distance) are distinct): the minimum over all candidates is the
 // minimum over the list, rescored on the current state.  Nothing is approximated.
 // ---------------------------------------------------------------------------------
-constexpr int SQW = 64;       // requests per block
+constexpr int SQW = 32;       // requests per block
 constexpr int SQK = 2 * SQW;  // listed candidates per request
+constexpr int SQE = SQK / 64;  // listed candidates per lane when a request is decided
 constexpr int SQT = 1024;     // threads per workgroup of the block kernel
 constexpr int SQ_NP = SEQC_MAX_I;
 static_assert(SQ_NP <= 4096, "rotation distances are packed in 12 bits");
@@ -958,12 +959,12 @@ __device__ __forceinline__ void seqc_rank(int32_t L, const int32_t *__restrict__
   if (tid == 0) w.l_cnt[le] = uint32_t(cnt);
 }
 
-// A request to decide with its record and list (entries lane and lane + 64).
+// A request to decide with its record and list (entries lane + 64 h, h < SQE).
 struct SeqLRow {
   SeqCRec rec;
   uint32_t cnt;
-  uint32_t inst[2];
-  i128 cst[2];
+  uint32_t inst[SQE];
+  i128 cst[SQE];
 };
 __device__ __forceinline__ void seqc_lrow_load(int32_t r, int32_t re, const SeqCWs &w, SeqLRow &row) {
   const int lane = threadIdx.x & 63;
@@ -973,7 +974,7 @@ __device__ __forceinline__ void seqc_lrow_load(int32_t r, int32_t re, const SeqC
   const uint64_t le = uint64_t(((rr / SQW) & 1) * SQW + rr % SQW);
   row.cnt = w.l_cnt[le];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < SQE; ++h) {
     row.inst[h] = w.l_inst[le * SQK + lane + 64 * h];
     row.cst[h] = w.l_cst[le * SQK + lane + 64 * h];
   }
@@ -995,7 +996,23 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
   const int32_t prev = uni(row.rec.prev);
   const bool cached = flags & 2, follow_up = flags & 4, prev_cand = flags & 8;
   const bool slack_inf = p.slack_den == 0;
-  const bool meets_prev = slack_inf || (q2[prev] + row.rec.cost_prev) * p.slack_den <= row.rec.bound;
+  // the listed instances' queues and counts are read with prev's queue, before the branch
+  const int32_t start = uni(row.rec.start);
+  const int32_t cnt = uni(int32_t(row.cnt));
+  const i128 q_prev = q2[prev];
+  i128 a[SQE];
+  uint32_t n[SQE], d[SQE];
+  bool v[SQE], wide = false;
+#pragma unroll
+  for (int h = 0; h < SQE; ++h) {
+    v[h] = lane + 64 * h < cnt;
+    const int32_t i = v[h] ? int32_t(row.inst[h]) : 0;
+    a[h] = q2[i] + row.cst[h];
+    n[h] = nr[i];
+    d[h] = uint32_t(i >= start ? i - start : i - start + I);
+    wide |= v[h] && (a[h] >> 64) != 0;
+  }
+  const bool meets_prev = slack_inf || (q_prev + row.rec.cost_prev) * p.slack_den <= row.rec.bound;
   int32_t t;
   uint8_t br;
   bool mine;     // this lane adds the request to t's queue and count
@@ -1006,25 +1023,11 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     mine = lane == 0;
     cost = row.rec.cost_prev;
   } else {
-    const int32_t start = uni(row.rec.start);
-    const int32_t cnt = uni(int32_t(row.cnt));
-    i128 a[2];
-    uint32_t n[2], d[2];
-    bool v[2], wide = false;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      v[h] = lane + 64 * h < cnt;
-      const int32_t i = v[h] ? int32_t(row.inst[h]) : 0;
-      a[h] = q2[i] + row.cst[h];
-      n[h] = nr[i];
-      d[h] = uint32_t(i >= start ? i - start : i - start + I);
-      wide |= v[h] && (a[h] >> 64) != 0;
-    }
     int32_t dmin;
     if (__ballot(wide) == 0) {  // every listed queue below 2^64: scores below 2^96, two words
       uint64_t k1 = ~uint64_t(0), k0 = ~uint64_t(0);
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < SQE; ++h)
         if (v[h]) {
           const uint64_t lo = uint64_t(a[h]);
           const uint64_t p0 = uint64_t(uint32_t(lo)) * n[h];
@@ -1040,7 +1043,7 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     } else {
       MinPD best{{0, 0}, 0x7FFFFFFF};
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < SQE; ++h)
         if (v[h]) min_pd(best, mul192(a[h], n[h]), int32_t(d[h]));
       best = wave_min_pd<64>(best);
       dmin = best.d;
@@ -1051,7 +1054,7 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
                     : (!cached ? SMETRIC_EVICTED : (!meets_prev ? SMETRIC_MIGRATE : SMETRIC_MIGRATE_TPOT));
     mine = false;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < SQE; ++h)
       if (lane + 64 * h < cnt && int32_t(row.inst[h]) == t) {
         mine = true;
         cost = row.cst[h];

@@ -303,8 +303,8 @@ def test_seqc_blocks_of_cached_follow_ups(I):
 def test_seqc_identical_requests_exhaust_candidate_lists(I):
     """Identical requests rank the instances alike, so the earlier requests of a block and of
     the block before take the best listed candidates of the later ones: the regime where
-    the minimum over a request's list (its 128 best on the state before the previous block,
-    rescored) must still equal the minimum over all instances."""
+    the minimum over a request's list (its best candidates on the state before the previous
+    block, rescored) must still equal the minimum over all instances."""
     from paper_2607_08565_amd import smetric as S
     rng = np.random.default_rng(900 + I)
     R = 4000
