@@ -299,7 +299,7 @@ def test_seqc_blocks_of_cached_follow_ups(I):
     assert {0, 2, 4, 255} <= seen
 
 
-@pytest.mark.parametrize("I", [129, 300, 1000])
+@pytest.mark.parametrize("I", [129, 300, 1000, 2049])
 def test_seqc_identical_requests_exhaust_candidate_lists(I):
     """Identical requests rank the instances alike, so the earlier requests of a block and of
     the block before take the best listed candidates of the later ones: the regime where
