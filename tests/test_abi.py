@@ -45,3 +45,11 @@ def test_host_side_errors_without_gpu():
     blk, nb = S.block_offsets([0, 15, 31, 100, 100], 16)
     assert blk.tolist() == [0, 0, 1, 5, 5] and nb == 5
     assert S.insert_ws_bytes(1000) > 16 * 1000
+    # the online colocation route's workspace: records per request, two blocks of candidate
+    # lists, two copies of the instance state; at most 4,096 instances
+    small, big = S.route_seq_coloc_ws_bytes(1, 8), S.route_seq_coloc_ws_bytes(16384, 1024)
+    assert big >= 16384 * 48 + 2 * 1024 * 20 > small > 0 and small % 256 == 0 and big % 256 == 0
+    assert S.route_seq_coloc_ws_bytes(0, 4096) > 2 * 4096 * 20
+    for bad in ((-1, 8), (10, 0), (10, 4097)):
+        with pytest.raises(S.SmetricError):
+            S.route_seq_coloc_ws_bytes(*bad)
