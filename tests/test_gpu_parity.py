@@ -393,6 +393,28 @@ def test_hash_partition_bad_token_range_invalidates_the_state():
     assert n == 0 and st == S.EINVAL
 
 
+def test_hash_partition_with_no_full_block():
+    """Every prompt shorter than one block: no keys, an empty probe state, all-zero matched
+    rows, nothing inserted and no error, on the fused call's counting path."""
+    rng = np.random.default_rng(34)
+    pair = Pair(10_000, 6)
+    lens = np.array([0, 1, 15, 7, 0, 15], np.int64)
+    tok_off = np.zeros(len(lens) + 1, np.int64)
+    tok_off[1:] = np.cumsum(lens)
+    toks = rng.integers(0, W.VOCAB, int(tok_off[-1]), dtype=np.int32)
+    blk_off = np.zeros(len(lens) + 1, np.int64)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    d_boff = to_dev(blk_off)
+    keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(tok_off), d_boff, 0, status=status)
+    assert int(status.item()) == 0
+    pair.gix.probe_lookup(state, 0)
+    m = pair.gix.match_probed(state, keys, d_boff, 0).cpu().numpy()
+    assert m.shape == (len(lens), 6) and not m.any()
+    R = len(lens)
+    pair.gix.insert_probed(state, R, 0, to_dev(np.zeros(R, np.int32)), to_dev(np.arange(R, dtype=np.uint32)), 1)
+    assert pair.gix.stats() == (0, 0)
+
+
 def test_match_bad_range_and_empty_requests():
     rng = np.random.default_rng(10)
     pair = Pair(10_000, 5)
