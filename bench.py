@@ -443,7 +443,18 @@ def cpu_baseline(setup, budget_s: float, gpu_out):
               and np.array_equal(g_b[:n], br))
     return dict(value=n / dt, unit="requests/s", cores=1, kind="oracle",
                 sample=f"first {n} requests of batch 0 (of {setup.args.n_req}), hash+match+route+insert, "
-                       f"index restricted to their keys, single thread, {dt:.1f} s"), parity, n
+                       f"index restricted to their keys, single thread, {dt:.1f} s",
+                cpu=host_cpu_model(), host_threads=os.cpu_count()), parity, n
+
+
+def host_cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def measure_evict(setup):
