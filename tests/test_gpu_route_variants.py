@@ -268,7 +268,7 @@ def test_seqc_random_parity(I):
         assert 5 in seen
 
 
-@pytest.mark.parametrize("I", [2, 4, 37])
+@pytest.mark.parametrize("I", [2, 4, 37, 150])
 def test_seqc_blocks_of_cached_follow_ups(I):
     """Cached follow-ups whose prev is a candidate, on few instances: most requests of
     every 64-request step share a prev and the queues cross deadlines inside steps, so the
