@@ -1226,16 +1226,20 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
 // ---------------------------------------------------------------------------------
 // Evict / dump
 // ---------------------------------------------------------------------------------
-// All live entries (plain and member slots; headers are not entries), in no particular
-// order.  Each thread takes GB consecutive buckets per round; a workgroup reserves its
-// round's output with one atomic (one per entry made a single counter the bottleneck).
+// All live entries (plain and member slots; headers are not entries), in table order.
+// Each thread takes GB consecutive buckets per round; a workgroup reserves its round's
+// output with one atomic (one per entry made a single counter the bottleneck).  Optional
+// outputs: each entry's slot (bit 63 set for a member slot) and the number of tombstones,
+// added once per wavefront at the end.
 constexpr int GB = 2;
-__global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals,
-                                                    unsigned long long *count, uint64_t cap) {
+__global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals, uint64_t *pos,
+                                                    unsigned long long *count, unsigned long long *n_tomb,
+                                                    uint64_t cap) {
   __shared__ uint32_t wt[TB / 64];
   __shared__ unsigned long long wg_base;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t per_round = uint64_t(TB) * GB;
+  uint32_t tombs = 0, d0_or = 0, d0_and = ~0u;  // the entries' first selection digit (epoch >> 11)
   for (uint64_t b0 = uint64_t(blockIdx.x) * per_round; b0 < ix.n_buckets; b0 += uint64_t(gridDim.x) * per_round) {
     uint32_t live = 0;  // bit s + SLOTS * g: slot s of bucket g is an entry
     uint64_t k[GB][SLOTS], v[GB][SLOTS];
@@ -1252,9 +1256,14 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
         v[g][2 * i + 1] = vv.y;
       }
 #pragma unroll
-      for (int s = 0; s < SLOTS; ++s)
-        if (b < ix.n_buckets && k[g][s] != KEY_EMPTY && k[g][s] != KEY_TOMB && val_kind(v[g][s]) != HEADER)
+      for (int s = 0; s < SLOTS; ++s) {
+        if (b < ix.n_buckets && k[g][s] != KEY_EMPTY && k[g][s] != KEY_TOMB && val_kind(v[g][s]) != HEADER) {
           live |= 1u << (g * SLOTS + s);
+          d0_or |= val_epoch(v[g][s]) >> 11;
+          d0_and &= val_epoch(v[g][s]) >> 11;
+        }
+        tombs += b < ix.n_buckets && k[g][s] == KEY_TOMB;
+      }
     }
     // exclusive prefix of the live counts over the workgroup
     const uint32_t c = __popc(live);
@@ -1283,11 +1292,42 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
           if (at < cap) {
             keys[at] = k[g][s];
             vals[at] = val_plain(v[g][s]);
+            if (pos)
+              pos[at] = ((b0 + uint64_t(threadIdx.x) * GB + g) * SLOTS + s) |
+                        (uint64_t(val_kind(v[g][s]) == MEMBER) << 63);
           }
           ++at;
         }
     __syncthreads();  // wt and wg_base are reused by the next round
   }
+  if (n_tomb) {  // n_tomb[1], n_tomb[2]: OR and AND of the first selection digit
+    uint32_t t = tombs, o = d0_or, a = d0_and;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+      t += __shfl_xor(t, d, 64);
+      o |= __shfl_xor(o, d, 64);
+      a &= __shfl_xor(a, d, 64);
+    }
+    if (lane == 0) {
+      if (t) atomicAdd(n_tomb, (unsigned long long)t);
+      atomicOr(n_tomb + 1, (unsigned long long)o);
+      atomicAnd(n_tomb + 2, (unsigned long long)a);
+    }
+  }
+}
+
+// The header slot of a key with a bitmap record (-1: none); it lies in the key's chain.
+__device__ int64_t find_header(const DevIndex &ix, uint64_t key) {
+  uint64_t b = home_bucket(key, ix.n_buckets);
+  for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
+    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+    for (int s = 0; s < SLOTS; ++s) {
+      const uint64_t k = bk[s];
+      if (k == KEY_EMPTY) return -1;
+      if (k == key && val_kind(bk[SLOTS + s]) == HEADER) return int64_t(b * SLOTS + s);
+    }
+  }
+  return -1;
 }
 
 // Eviction as a selection: the m-th smallest entry under (epoch, key, instance) is found
@@ -1406,20 +1446,58 @@ __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsign
   }
 }
 
-__global__ void set_counts_kernel(IndexHdr *h, unsigned long long n_entries) {
+__global__ void set_counts_kernel(IndexHdr *h, unsigned long long n_entries, int reset_records) {
   h->n_entries = n_entries;
-  h->rec_used = 0;
+  if (reset_records) h->rec_used = 0;
 }
 
+// Eviction in place: the gathered entries at or below the cut become tombstones (a member
+// also leaves its key's bitmap); every other entry keeps its slot.  Tombstones are never
+// reclaimed by inserts, so the caller rebuilds the table instead once they would pass an
+// eighth of the slots.
+__global__ __launch_bounds__(TB) void evict_tomb_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
+                                                        const uint64_t *__restrict__ vals,
+                                                        const uint64_t *__restrict__ pos, uint64_t n, SelPrefix cut) {
+  const uint64_t stride = uint64_t(gridDim.x) * TB;
+  for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += stride) {
+    const uint64_t k = keys[i], v = vals[i];
+    if (sel_cmp(k, v, cut) > 0) continue;  // survives
+    const uint64_t ps = pos[i], slot = ps & ~(uint64_t(1) << 63);
+    ix.slots[(slot / SLOTS) * BUCKET_WORDS + slot % SLOTS] = KEY_TOMB;
+    if (ps >> 63) {
+      const int64_t h = find_header(ix, k);
+      if (h < 0) {
+        set_status(ix.hdr, SMETRIC_EINTERNAL);
+        continue;
+      }
+      const uint64_t rec = val_rec(*val_ptr(ix, h));
+      const uint32_t inst = val_inst(v);
+      atomicAnd(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
+                ~(1ull << (inst & 63)));
+    }
+  }
+}
+
+// One selection pass: the histogram of the next digit over the entries on the prefix.
+// With ck non-null those entries are also copied to (ck, cv) (in no particular order; the
+// caller does so only when few are left), so the later passes read them alone.
 __global__ __launch_bounds__(TB) void sel_hist_kernel(const uint64_t *keys, const uint64_t *vals, uint64_t n,
-                                                      SelPrefix p, unsigned long long *hist) {
+                                                      SelPrefix p, unsigned long long *hist, uint64_t *ck,
+                                                      uint64_t *cv, unsigned long long *n_c) {
   __shared__ uint32_t h[SEL_BINS];
   for (int b = threadIdx.x; b < SEL_BINS; b += TB) h[b] = 0;
   __syncthreads();
   const uint64_t stride = uint64_t(gridDim.x) * TB;
   for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += stride) {
     const uint64_t k = keys[i], v = vals[i];
-    if (sel_cmp(k, v, p) == 0) atomicAdd(&h[sel_digit(k, v, p.level)], 1u);
+    if (sel_cmp(k, v, p) == 0) {
+      atomicAdd(&h[sel_digit(k, v, p.level)], 1u);
+      if (ck) {
+        const unsigned long long at = atomicAdd(n_c, 1ull);
+        ck[at] = k;
+        cv[at] = v;
+      }
+    }
   }
   __syncthreads();
   for (int b = threadIdx.x; b < SEL_BINS; b += TB)
@@ -1485,7 +1563,8 @@ int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, uint6
   int rc = fill(ws.count, 256, 0, s);
   if (rc) return rc;
   const uint64_t n_slots = ix.n_buckets * SLOTS;
-  hipLaunchKernelGGL(gather_kernel, dim3(grid_for(n_slots)), dim3(TB), 0, s, ix, ws.ka, ws.va, ws.count, n);
+  hipLaunchKernelGGL(gather_kernel, dim3(grid_for(n_slots)), dim3(TB), 0, s, ix, ws.ka, ws.va, nullptr, ws.count,
+                     nullptr, n);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   unsigned long long got = 0;
   if (hipMemcpyAsync(&got, ws.count, 8, hipMemcpyDeviceToHost, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
@@ -1603,28 +1682,51 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   const uint64_t n = h.n_entries;
   const uint64_t m = uint64_t((static_cast<unsigned __int128>(n) * frac_num + frac_den - 1) / frac_den);
   if (m == 0) return SMETRIC_OK;
-  // all entries, unordered
-  if ((rc = fill(ws.count, 256, 0, stream))) return rc;
+  // all entries, in table order
+  if ((rc = fill(ws.count, 256, 0, stream)) || (rc = fill(ws.count + 5, 8, ~uint64_t(0), stream))) return rc;
   const DevIndex ix = dev_view(idx);
+  uint64_t *pos = ws.kb;  // free until a dump: each entry's slot
   hipLaunchKernelGGL(gather_kernel, dim3(grid_for(ix.n_buckets * SLOTS)), dim3(TB), 0, stream, ix, ws.ka, ws.va,
-                     ws.count, n);
-  unsigned long long got = 0;
-  if (hipMemcpyAsync(&got, ws.count, 8, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+                     pos, ws.count, ws.count + 3, n);
+  unsigned long long cnt[6] = {0, 0, 0, 0, 0, 0};
+  if (hipMemcpyAsync(cnt, ws.count, sizeof(cnt), hipMemcpyDeviceToHost, stream) != hipSuccess ||
       hipStreamSynchronize(stream) != hipSuccess)
     return SMETRIC_EHIP;
-  if (got != n) return SMETRIC_EINTERNAL;
+  if (cnt[0] != n) return SMETRIC_EINTERNAL;
+  const uint64_t n_tomb = cnt[3];
   // select the m-th smallest, one digit per pass; stop once its whole bin is evicted
   SelPrefix p{};
-  uint64_t rem = m;  // rank of the m-th smallest among the entries on the prefix (1-based)
+  uint64_t rem = m;          // rank of the m-th smallest among the entries on the prefix (1-based)
+  uint64_t on_prefix = n;    // entries on the prefix
+  int l0 = 0;
+  if (cnt[4] == cnt[5]) {  // every entry has the same first digit (the epochs' top bits): no pass
+    p.digit[0] = uint32_t(cnt[4]);
+    p.level = l0 = 1;
+  }
+  const uint64_t *sk = ws.ka, *sv = ws.va;  // the entries the passes read
+  uint64_t sn = n;
   unsigned long long hh[SEL_BINS];
-  for (int l = 0; l < SEL_LEVELS; ++l) {
+  for (int l = l0; l < SEL_LEVELS && rem < on_prefix; ++l) {
     p.level = l;
+    // once few entries are left on the prefix, this pass copies them out and the later
+    // passes read those alone
+    const bool compact = sk == ws.ka && on_prefix <= (uint64_t(1) << 20);
     if ((rc = fill(ws.hist, 8 * SEL_BINS, 0, stream))) return rc;
-    hipLaunchKernelGGL(sel_hist_kernel, dim3(grid_for(n) < 1024 ? grid_for(n) : 1024), dim3(TB), 0, stream, ws.ka,
-                       ws.va, n, p, ws.hist);
+    if (compact && (rc = fill(ws.count + 6, 8, 0, stream))) return rc;
+    const int grid = grid_for(sn) < 1024 ? grid_for(sn) : 1024;
+    hipLaunchKernelGGL(sel_hist_kernel, dim3(grid), dim3(TB), 0, stream, sk, sv, sn, p, ws.hist,
+                       compact ? ws.ea : nullptr, compact ? ws.ia : nullptr, ws.count + 6);
+    unsigned long long n_c = 0;
     if (hipMemcpyAsync(hh, ws.hist, 8 * SEL_BINS, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        (compact && hipMemcpyAsync(&n_c, ws.count + 6, 8, hipMemcpyDeviceToHost, stream) != hipSuccess) ||
         hipStreamSynchronize(stream) != hipSuccess)
       return SMETRIC_EHIP;
+    if (compact) {
+      if (n_c != on_prefix) return SMETRIC_EINTERNAL;
+      sk = ws.ea;
+      sv = ws.ia;
+      sn = n_c;
+    }
     uint64_t below = 0;
     int b = 0;
     while (b < SEL_BINS && below + hh[b] < rem) below += hh[b++];
@@ -1632,14 +1734,22 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
     p.digit[l] = uint32_t(b);
     p.level = l + 1;
     rem -= below;
-    if (rem == hh[b]) break;  // the whole bin goes: the prefix itself is the cut
-    if (l + 1 == SEL_LEVELS) return SMETRIC_EINTERNAL;  // the full tuple is unique
+    on_prefix = hh[b];  // rem == on_prefix: the whole bin goes, the prefix itself is the cut
+    if (rem < on_prefix && l + 1 == SEL_LEVELS) return SMETRIC_EINTERNAL;  // the full tuple is unique
   }
-  // rebuild from the survivors: the entries above the cut, exactly n - m of them
+  // few tombstones: evict in place, the survivors keep their slots
+  if ((n_tomb + m) * 8 <= ix.n_buckets * SLOTS) {
+    hipLaunchKernelGGL(evict_tomb_kernel, dim3(grid_for(n)), dim3(TB), 0, stream, ix, ws.ka, ws.va, pos, n, p);
+    hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m), 0);
+    if ((rc = hip_rc(hipGetLastError()))) return rc;
+    return hip_rc(hipStreamSynchronize(stream));
+  }
+  // else rebuild from the survivors (the entries above the cut, exactly n - m of them),
+  // which also clears every tombstone
   uint64_t *keys = ws.ka, *vals = ws.va;
   if ((rc = fill(ix.slots, ix.n_buckets * BUCKET_WORDS * 8, 0, stream))) return rc;
   if ((rc = fill(ix.pool, ix.n_records * uint64_t(ix.words) * 8, 0, stream))) return rc;
-  hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m));
+  hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m), 1);
   uint64_t *trig = ws.ea;  // free buffers: the conversion queue and the deferred pairs
   unsigned long long *n_trig = ws.count + 1;
   uint64_t *def = ws.ia;

@@ -85,11 +85,14 @@ def test_config2_scaled_prev_counts(probed):
 
 
 @pytest.mark.parametrize("probed", [False, True])
-def test_config3_scaled_with_eviction(probed):
+@pytest.mark.parametrize("frac", [(1, 20), (1, 3)])
+def test_config3_scaled_with_eviction(probed, frac):
     """One shared prefix held by every instance (bitmap records, WIDE alive sets of 128),
-    divergent tails, 5 % LRU eviction after every batch (orphaned descendants)."""
+    divergent tails, LRU eviction after every batch (orphaned descendants).  5 % per batch
+    evicts in place (tombstones, members leaving their bitmaps); a third per batch passes
+    the tombstone limit and rebuilds the table."""
     wl = W.config3(n_sess=160, n_turns=5, prefix_len=4096, tail=(256, 3000), app=512)
-    run_sessions(wl, 5, capacity=400_000, evict=(1, 20), probed=probed)
+    run_sessions(wl, 5, capacity=400_000, evict=frac, probed=probed)
 
 
 def test_partition_overlaps_previous_insert():
