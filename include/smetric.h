@@ -438,7 +438,9 @@ int smetric_index_insert(smetric_index *idx, const uint64_t *keys, const int64_t
 /* ---------------------------------------------------------------------------------
  * LRU eviction of a fraction frac_num/frac_den of the entries (the paper's local tier
  * evicts; its policy is not specified): removes exactly ceil(N * num / den) entries, the
- * smallest under the total order (epoch, key, instance), then rebuilds the table.
+ * smallest under the total order (epoch, key, instance).  The removed slots become
+ * tombstones while tombstones stay below an eighth of the table's slots; past that the
+ * table is rebuilt from the survivors, which clears every tombstone.
  * Synchronizes.  EINVAL if frac_den == 0 or frac_num > frac_den.
  * Dump: all entries sorted by (key, instance) into keys_out / vals_out (device,
  * `cap` each), vals = instance << 48 | epoch << 24 | session; *n_out (host) = entry
