@@ -1230,16 +1230,27 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
 // Each thread takes GB consecutive buckets per round; a workgroup reserves its round's
 // output with one atomic (one per entry made a single counter the bottleneck).  Optional
 // outputs: each entry's slot (bit 63 set for a member slot) and the number of tombstones,
-// added once per wavefront at the end.
+// added once per wavefront at the end; with hist1, the eviction's second selection digit
+// (the epoch's low 11 bits) is counted over the entries whose first digit is 0, in LDS,
+// each thread folding runs of its last EC distinct epochs in registers first.
 constexpr int GB = 2;
+constexpr int EC = 4;
 __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals, uint64_t *pos,
                                                     unsigned long long *count, unsigned long long *n_tomb,
-                                                    uint64_t cap) {
+                                                    unsigned long long *hist1, uint64_t cap) {
   __shared__ uint32_t wt[TB / 64];
   __shared__ unsigned long long wg_base;
+  __shared__ uint32_t h1[2048];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t per_round = uint64_t(TB) * GB;
   uint32_t tombs = 0, d0_or = 0, d0_and = ~0u;  // the entries' first selection digit (epoch >> 11)
+  uint32_t ce[EC], cn[EC];                       // cached epochs (low bits) and their counts
+#pragma unroll
+  for (int j = 0; j < EC; ++j) cn[j] = ce[j] = 0;
+  if (hist1) {
+    for (int b = threadIdx.x; b < 2048; b += TB) h1[b] = 0;
+    __syncthreads();
+  }
   for (uint64_t b0 = uint64_t(blockIdx.x) * per_round; b0 < ix.n_buckets; b0 += uint64_t(gridDim.x) * per_round) {
     uint32_t live = 0;  // bit s + SLOTS * g: slot s of bucket g is an entry
     uint64_t k[GB][SLOTS], v[GB][SLOTS];
@@ -1259,8 +1270,20 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
       for (int s = 0; s < SLOTS; ++s) {
         if (b < ix.n_buckets && k[g][s] != KEY_EMPTY && k[g][s] != KEY_TOMB && val_kind(v[g][s]) != HEADER) {
           live |= 1u << (g * SLOTS + s);
-          d0_or |= val_epoch(v[g][s]) >> 11;
-          d0_and &= val_epoch(v[g][s]) >> 11;
+          const uint32_t ep = val_epoch(v[g][s]);
+          d0_or |= ep >> 11;
+          d0_and &= ep >> 11;
+          if (hist1 && (ep >> 11) == 0) {
+            bool hit = false;
+#pragma unroll
+            for (int j = 0; j < EC; ++j)
+              if (!hit && (cn[j] == 0 || ce[j] == ep)) {
+                ce[j] = ep;
+                ++cn[j];
+                hit = true;
+              }
+            if (!hit) atomicAdd(&h1[ep], 1u);
+          }
         }
         tombs += b < ix.n_buckets && k[g][s] == KEY_TOMB;
       }
@@ -1299,6 +1322,14 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
           ++at;
         }
     __syncthreads();  // wt and wg_base are reused by the next round
+  }
+  if (hist1) {
+#pragma unroll
+    for (int j = 0; j < EC; ++j)
+      if (cn[j]) atomicAdd(&h1[ce[j]], cn[j]);
+    __syncthreads();
+    for (int b = threadIdx.x; b < 2048; b += TB)
+      if (h1[b]) atomicAdd(&hist1[b], (unsigned long long)h1[b]);
   }
   if (n_tomb) {  // n_tomb[1], n_tomb[2]: OR and AND of the first selection digit
     uint32_t t = tombs, o = d0_or, a = d0_and;
@@ -1564,7 +1595,7 @@ int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, uint6
   if (rc) return rc;
   const uint64_t n_slots = ix.n_buckets * SLOTS;
   hipLaunchKernelGGL(gather_kernel, dim3(grid_for(n_slots)), dim3(TB), 0, s, ix, ws.ka, ws.va, nullptr, ws.count,
-                     nullptr, n);
+                     nullptr, nullptr, n);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   unsigned long long got = 0;
   if (hipMemcpyAsync(&got, ws.count, 8, hipMemcpyDeviceToHost, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
@@ -1683,13 +1714,17 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   const uint64_t m = uint64_t((static_cast<unsigned __int128>(n) * frac_num + frac_den - 1) / frac_den);
   if (m == 0) return SMETRIC_OK;
   // all entries, in table order
-  if ((rc = fill(ws.count, 256, 0, stream)) || (rc = fill(ws.count + 5, 8, ~uint64_t(0), stream))) return rc;
+  if ((rc = fill(ws.count, 256, 0, stream)) || (rc = fill(ws.count + 5, 8, ~uint64_t(0), stream)) ||
+      (rc = fill(ws.hist, 8 * 2048, 0, stream)))
+    return rc;
   const DevIndex ix = dev_view(idx);
   uint64_t *pos = ws.kb;  // free until a dump: each entry's slot
   hipLaunchKernelGGL(gather_kernel, dim3(grid_for(ix.n_buckets * SLOTS)), dim3(TB), 0, stream, ix, ws.ka, ws.va,
-                     pos, ws.count, ws.count + 3, n);
+                     pos, ws.count, ws.count + 3, ws.hist, n);
   unsigned long long cnt[6] = {0, 0, 0, 0, 0, 0};
+  unsigned long long hh[SEL_BINS];
   if (hipMemcpyAsync(cnt, ws.count, sizeof(cnt), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+      hipMemcpyAsync(hh, ws.hist, 8 * 2048, hipMemcpyDeviceToHost, stream) != hipSuccess ||
       hipStreamSynchronize(stream) != hipSuccess)
     return SMETRIC_EHIP;
   if (cnt[0] != n) return SMETRIC_EINTERNAL;
@@ -1702,10 +1737,19 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   if (cnt[4] == cnt[5]) {  // every entry has the same first digit (the epochs' top bits): no pass
     p.digit[0] = uint32_t(cnt[4]);
     p.level = l0 = 1;
+    if (cnt[4] == 0 && rem < on_prefix) {  // and the gather counted the second digit: no pass either
+      uint64_t below = 0;
+      int b = 0;
+      while (b < 2048 && below + hh[b] < rem) below += hh[b++];
+      if (b == 2048) return SMETRIC_EINTERNAL;
+      p.digit[1] = uint32_t(b);
+      p.level = l0 = 2;
+      rem -= below;
+      on_prefix = hh[b];
+    }
   }
   const uint64_t *sk = ws.ka, *sv = ws.va;  // the entries the passes read
   uint64_t sn = n;
-  unsigned long long hh[SEL_BINS];
   for (int l = l0; l < SEL_LEVELS && rem < on_prefix; ++l) {
     p.level = l;
     // once few entries are left on the prefix, this pass copies them out and the later
