@@ -54,6 +54,7 @@ struct DevIndex {
   int32_t n_inst;
   int32_t words;      // bitmap words per record
   int32_t threshold;  // spill threshold T
+  uint64_t nb_inv;    // floor(2^64 / n_buckets) (any value when n_buckets = 1): see scaled_floor
 };
 
 inline DevIndex dev_view(const smetric_index *ix) {
@@ -67,6 +68,7 @@ inline DevIndex dev_view(const smetric_index *ix) {
   d.n_inst = ix->n_instances;
   d.words = ix->bitmap_words;
   d.threshold = ix->spill_threshold;
+  d.nb_inv = d.n_buckets > 1 ? uint64_t((static_cast<unsigned __int128>(1) << 64) / d.n_buckets) : ~uint64_t(0);
   return d;
 }
 
@@ -82,21 +84,30 @@ __host__ __device__ inline uint64_t mix64(uint64_t k) {
 __device__ inline uint64_t home_bucket(uint64_t key, uint64_t n_buckets) {
   return __umul64hi(mix64(key), n_buckets);
 }
+// floor(h mult / n) for h < n, h mult < 2^64, without a 64-bit division: with inv =
+// floor(2^64 / n), q = floor(h mult inv / 2^64) is at most 2 below the quotient.
+__device__ __forceinline__ uint64_t scaled_floor(uint64_t h, uint64_t mult, uint64_t n, uint64_t inv) {
+  const uint64_t x = h * mult;
+  uint64_t q = __umul64hi(x, inv);
+  q += (q + 1) * n <= x;
+  q += (q + 1) * n <= x;
+  return q;
+}
 // Table regions: the bucket range split into NREG equal parts.  Probes, refreshes and
 // claims are issued region by region so the pages live at any moment stay within the
 // translation caches' reach (~2 GiB); few regions keep the partition's runs long.
 constexpr int NREG = 16;
-__device__ __forceinline__ uint32_t region_of(uint64_t key, uint64_t n_buckets) {
-  return uint32_t(home_bucket(key, n_buckets) * NREG / n_buckets);
+__device__ __forceinline__ uint32_t region_of(uint64_t key, uint64_t n_buckets, uint64_t nb_inv) {
+  return uint32_t(scaled_floor(home_bucket(key, n_buckets), NREG, n_buckets, nb_inv));
 }
 
 // Bucket chain for a member entry (key, inst) of a key that uses a bitmap record: a
 // pseudo-random bucket inside the region of the key's home bucket, so member lookups
 // issued in region order stay inside the same window of the table.
-__device__ inline uint64_t member_bucket(uint64_t key, uint32_t inst, uint64_t n_buckets) {
+__device__ inline uint64_t member_bucket(uint64_t key, uint32_t inst, uint64_t n_buckets, uint64_t nb_inv) {
   const uint64_t h = mix64(key ^ ((uint64_t(inst) + 1) * 0x9E3779B97F4A7C15ull));
   if (n_buckets < uint64_t(4 * NREG)) return __umul64hi(h, n_buckets);
-  const uint64_t g = region_of(key, n_buckets);
+  const uint64_t g = region_of(key, n_buckets, nb_inv);
   const uint64_t lo = g * n_buckets / NREG, hi = (g + 1) * n_buckets / NREG;
   return lo + __umul64hi(h, hi - lo);
 }

@@ -6,8 +6,8 @@
 // s_j = M s_{j-1} + e_j and a finalised key.
 //
 // Mapping to gfx950: requests are cut into tiles of 64 blocks.
-//  * B = 16 (the fast path): one workgroup of four wavefronts per request, wavefront w
-//    taking tiles w, w + 4, ... and loading its next tile while it hashes the current one,
+//  * B = 16 (the fast path): one workgroup of eight wavefronts per request, wavefront w
+//    taking tiles w, w + 8, ... and loading its next tile while it hashes the current one,
 //    so long prompts do not serialise on one wavefront.  Tokens are read as 16-byte
 //    vectors, lane l of load u taking tokens [256u + 4l, 256u + 4l + 4) of the tile, so
 //    every load instruction covers 1 KB of contiguous HBM.  Four lanes share a block;
@@ -170,7 +170,7 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
                                                          uint64_t *__restrict__ keys,
                                                          int32_t *status,
                                                          uint32_t *__restrict__ hist, uint64_t n_buckets,
-                                                         uint64_t clen, int *probe_err) {
+                                                         uint64_t nb_inv, uint64_t clen, int *probe_err) {
   __shared__ uint64_t dig[NW][64];
   __shared__ uint64_t agg[NW];
   __shared__ unsigned int lh[COUNT ? 2 * NREG : 1];
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
       keys[b0 + j0 + lane] = key;
       if (COUNT) {
         const uint64_t b = uint64_t(b0 + j0 + lane);
-        const uint32_t g = region_of(key, n_buckets);
+        const uint32_t g = region_of(key, n_buckets, nb_inv);
         if (b < B2) atomicAdd(&lh[(b >= B1 ? NREG : 0) + g], 1u);
         else atomicAdd(&hist[(b / clen) * NREG + g], 1u);
       }
@@ -294,8 +294,8 @@ extern "C" int smetric_hash_blocks(const int32_t *tokens, int64_t n_tokens, cons
   const dim3 grid((n_req + WAVES - 1) / WAVES), block(64 * WAVES);
   if (block_size == 16)
     hipLaunchKernelGGL((hash16_kernel<HASH_NW, false>), dim3(n_req), dim3(64 * HASH_NW), 0, stream, tokens, n_tokens, tok_off, blk_off,
-                       n_req, n_blocks, seed, keys, status, static_cast<uint32_t *>(nullptr), uint64_t(0), uint64_t(1),
-                       static_cast<int *>(nullptr));
+                       n_req, n_blocks, seed, keys, status, static_cast<uint32_t *>(nullptr), uint64_t(0), uint64_t(0),
+                       uint64_t(1), static_cast<int *>(nullptr));
   else
     hipLaunchKernelGGL(hash_generic_kernel, grid, block, 0, stream, tokens, n_tokens, tok_off,
                        blk_off, n_req, n_blocks, int(block_size), seed, keys, status);
@@ -317,7 +317,7 @@ extern "C" int smetric_hash_partition(const int32_t *tokens, int64_t n_tokens, c
   partition_head(pv, blk_off, n_req, n_blocks, counted, stream);
   if (counted)
     hipLaunchKernelGGL((hash16_kernel<HASH_NW, true>), dim3(n_req), dim3(64 * HASH_NW), 0, stream, tokens, n_tokens,
-                       tok_off, blk_off, n_req, n_blocks, seed, keys, status, pv.hist, ix.n_buckets,
+                       tok_off, blk_off, n_req, n_blocks, seed, keys, status, pv.hist, ix.n_buckets, ix.nb_inv,
                        partition_chunk(uint64_t(n_blocks)), &pv.hdr->err);
   else if (n_req > 0)
     hipLaunchKernelGGL(hash_generic_kernel, dim3((n_req + WAVES - 1) / WAVES), dim3(64 * WAVES), 0, stream, tokens,

@@ -115,7 +115,7 @@ struct Found {
 
 // Find the entry (key, inst), looking through a bitmap record when the key has one.
 __device__ Found find_member(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  uint64_t m = member_bucket(key, inst, ix.n_buckets);
+  uint64_t m = member_bucket(key, inst, ix.n_buckets, ix.nb_inv);
   for (uint64_t step = 0; step < ix.n_buckets; ++step, m = next_bucket(m, ix.n_buckets)) {
     const uint64_t *mk = ix.slots + m * BUCKET_WORDS;
     const BucketScan sc = scan_bucket(mk, key);
@@ -236,7 +236,7 @@ __device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32
     const uint64_t rec = val_rec(*val_ptr(ix, c.header));
     atomicOr(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
              1ull << (inst & 63));
-    const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, false);
+    const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, false);
     if (m.slot < 0) return FAILED;
     *val_ptr(ix, m.slot) = make_val(inst, MEMBER, epoch, sess);
     return PLACED;
@@ -269,7 +269,7 @@ __device__ bool spill_key(const DevIndex &ix, uint64_t key) {
       if (val_kind(v) != PLAIN) continue;
       const uint32_t inst = val_inst(v);
       bm[inst >> 6] |= 1ull << (inst & 63);
-      const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets), key, false);
+      const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, false);
       if (m.slot < 0) return false;
       *val_ptr(ix, m.slot) = make_val(inst, MEMBER, val_epoch(v), uint32_t(v & 0xFFFFFF));
       if (first < 0) {
@@ -645,7 +645,7 @@ __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned l
 // find_member with each bucket read whole (keys and values in one 128-byte request), so
 // a chain step is one round trip.
 __device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  uint64_t m = member_bucket(key, inst, ix.n_buckets);
+  uint64_t m = member_bucket(key, inst, ix.n_buckets, ix.nb_inv);
   for (uint64_t step = 0; step < ix.n_buckets; ++step, m = next_bucket(m, ix.n_buckets)) {
     const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + m * BUCKET_WORDS);
     ulonglong2 kk[SLOTS / 2], vv[SLOTS / 2];
@@ -842,8 +842,8 @@ __global__ __launch_bounds__(TB) void insp_size_kernel(InsWs ws) {
 }
 
 // Bin of a key among NREG * nsub equal ranges of home buckets; bin / nsub is its region.
-__device__ __forceinline__ uint32_t bin_of(uint64_t key, uint64_t n_buckets, uint32_t nsub) {
-  return uint32_t(home_bucket(key, n_buckets) * (uint64_t(NREG) * nsub) / n_buckets);
+__device__ __forceinline__ uint32_t bin_of(uint64_t key, uint64_t n_buckets, uint64_t nb_inv, uint32_t nsub) {
+  return uint32_t(scaled_floor(home_bucket(key, n_buckets), uint64_t(NREG) * nsub, n_buckets, nb_inv));
 }
 
 // The candidates of chunk (g, c): the region-g parts of classify segments
@@ -896,7 +896,7 @@ __global__ __launch_bounds__(TB) void insp_bcount_kernel(DevIndex ix, InsWs ws) 
 #pragma unroll
     for (int u = 0; u < UC; ++u) {
       if (v0 + u * TB + threadIdx.x < m) {
-        const uint32_t sub = bin_of(k[u], ix.n_buckets, nsub) - uint32_t(g) * nsub;
+        const uint32_t sub = bin_of(k[u], ix.n_buckets, ix.nb_inv, nsub) - uint32_t(g) * nsub;
         atomicAdd(&h[sub < nsub ? sub : nsub - 1], 1u);
       }
     }
@@ -1005,7 +1005,7 @@ __global__ __launch_bounds__(TB) void insp_bscatter_kernel(DevIndex ix, InsWs ws
     }
 #pragma unroll
     for (int u = 0; u < U2; ++u) {
-      const uint32_t s = bin_of(e[u].key, ix.n_buckets, nsub) - uint32_t(g) * nsub;
+      const uint32_t s = bin_of(e[u].key, ix.n_buckets, ix.nb_inv, nsub) - uint32_t(g) * nsub;
       sub[u] = s < nsub ? s : nsub - 1;
       rk[u] = t0 + u * TB + t < m ? atomicAdd(&cnt[sub[u]], 1u) : 0;
     }

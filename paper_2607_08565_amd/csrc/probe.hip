@@ -104,7 +104,7 @@ __global__ __launch_bounds__(TB) void part_count_kernel(DevIndex ix, ProbeView p
 #pragma unroll
     for (int u = 0; u < U; ++u)
       if (t0 + u * TB + threadIdx.x < hi) {
-        atomicAdd(&h[region_of(k[u], ix.n_buckets)], 1u);
+        atomicAdd(&h[region_of(k[u], ix.n_buckets, ix.nb_inv)], 1u);
         bad |= k[u] == KEY_EMPTY || k[u] == KEY_TOMB;
       }
   }
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
     }
 #pragma unroll
     for (int u = 0; u < UW; ++u) {
-      g[u] = uint8_t(region_of(k[u], ix.n_buckets));
+      g[u] = uint8_t(region_of(k[u], ix.n_buckets, ix.nb_inv));
       rk[u] = t0 + u * TB + t < hi ? atomicAdd(&cnt[g[u]], 1u) : 0;
     }
     __syncthreads();
