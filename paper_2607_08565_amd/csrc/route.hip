@@ -19,6 +19,7 @@ namespace smk {
 namespace {
 
 constexpr int RW = 4;  // waves per workgroup
+constexpr int RU = 4;  // instances per lane whose loads a route kernel issues together
 typedef __int128 i128;
 constexpr int64_t NO_DECODE = int64_t(1) << 62;  // decode slack meaning "no live decode"
 
@@ -75,24 +76,39 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
   i128 best_e = 0;
   int32_t best_d = 0x7FFFFFFF;                // argmin (est2, rotation distance)
   i128 load_sum = 0;                          // RULE 1
-  for (int32_t i = lane; i < I; i += 64) {
-    const int32_t ci = c[i];
-    const int64_t qi = q[i];
-    if (ci < 0 || ci > max_c || qi < 0 || qi >= (int64_t(1) << 62)) ok = false;
-    if (RULE == 1) {
-      const int64_t li = load[i];
-      if (li < 0 || li >= (int64_t(1) << 62)) ok = false;
-      load_sum += li;
+  // RU instances per lane at a time, their loads issued first (clamped, so branch-free)
+  for (int32_t i0 = lane; i0 < I; i0 += 64 * RU) {
+    int32_t cv[RU];
+    int64_t qv[RU], lv[RU];
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int32_t ii = i0 + 64 * u < I ? i0 + 64 * u : I - 1;
+      cv[u] = c[ii];
+      qv[u] = q[ii];
+      lv[u] = RULE == 1 ? load[ii] : 0;
     }
-    if (ci > best_c) {
-      best_c = ci;
-      best_ci = i;
-    }
-    const i128 e = est2(p, L, ci, qi);
-    const int32_t d = i >= start ? i - start : i - start + I;
-    if (best_d == 0x7FFFFFFF || e < best_e || (e == best_e && d < best_d)) {
-      best_e = e;
-      best_d = d;
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int32_t i = i0 + 64 * u;
+      if (i >= I) break;
+      const int32_t ci = cv[u];
+      const int64_t qi = qv[u];
+      if (ci < 0 || ci > max_c || qi < 0 || qi >= (int64_t(1) << 62)) ok = false;
+      if (RULE == 1) {
+        const int64_t li = lv[u];
+        if (li < 0 || li >= (int64_t(1) << 62)) ok = false;
+        load_sum += li;
+      }
+      if (ci > best_c) {
+        best_c = ci;
+        best_ci = i;
+      }
+      const i128 e = est2(p, L, ci, qi);
+      const int32_t d = i >= start ? i - start : i - start + I;
+      if (best_d == 0x7FFFFFFF || e < best_e || (e == best_e && d < best_d)) {
+        best_e = e;
+        best_d = d;
+      }
     }
   }
   ok = __ballot(!ok) == 0;
@@ -187,20 +203,34 @@ __global__ __launch_bounds__(64 * RW) void route_coloc_kernel(
 
   int32_t best_c = -1, best_ci = 0x7FFFFFFF;
   MinSD pass{0, 0x7FFFFFFF}, all{0, 0x7FFFFFFF};
-  for (int32_t i = lane; i < I; i += 64) {
-    const int32_t ci = c[i];
-    const int64_t qi = q[i];
-    const int32_t ni = n_run[i];
-    if (ci < 0 || ci > max_c || qi < 0 || qi >= (int64_t(1) << 62) || ni < 0) ok = false;
-    if (ci > best_c) {
-      best_c = ci;
-      best_ci = i;
+  for (int32_t i0 = lane; i0 < I; i0 += 64 * RU) {  // loads first, as in route_kernel
+    int32_t cv[RU], nv[RU];
+    int64_t qv[RU], sv[RU];
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int32_t ii = i0 + 64 * u < I ? i0 + 64 * u : I - 1;
+      cv[u] = c[ii];
+      qv[u] = q[ii];
+      nv[u] = n_run[ii];
+      sv[u] = slack[ii];
     }
-    const i128 cost = est2(p, L, ci, 0);
-    const i128 sc = (cost + i128(2) * qi) * ni;
-    const int32_t d = i >= start ? i - start : i - start + I;
-    min_sd(all, sc, d);
-    if (slack[i] >= NO_DECODE || cost <= i128(2) * slack[i]) min_sd(pass, sc, d);
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const int32_t i = i0 + 64 * u;
+      if (i >= I) break;
+      const int32_t ci = cv[u], ni = nv[u];
+      const int64_t qi = qv[u];
+      if (ci < 0 || ci > max_c || qi < 0 || qi >= (int64_t(1) << 62) || ni < 0) ok = false;
+      if (ci > best_c) {
+        best_c = ci;
+        best_ci = i;
+      }
+      const i128 cost = est2(p, L, ci, 0);
+      const i128 sc = (cost + i128(2) * qi) * ni;
+      const int32_t d = i >= start ? i - start : i - start + I;
+      min_sd(all, sc, d);
+      if (sv[u] >= NO_DECODE || cost <= i128(2) * sv[u]) min_sd(pass, sc, d);
+    }
   }
   ok = __ballot(!ok) == 0;
 #pragma unroll
