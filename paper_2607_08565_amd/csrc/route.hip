@@ -807,6 +807,18 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
          uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
 }
 
+// Minimum of a 64-bit key over the wavefront by DPP moves toward lane 63; every lane gets it.
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
+  uint64_t o;
+  o = dpp_or_own64<0x111, 0xF>(k), k = o < k ? o : k;
+  o = dpp_or_own64<0x112, 0xF>(k), k = o < k ? o : k;
+  o = dpp_or_own64<0x114, 0xF>(k), k = o < k ? o : k;
+  o = dpp_or_own64<0x118, 0xF>(k), k = o < k ? o : k;
+  o = dpp_or_own64<0x142, 0xA>(k), k = o < k ? o : k;  // row_bcast:15 into rows 1 and 3
+  o = dpp_or_own64<0x143, 0xC>(k), k = o < k ? o : k;  // row_bcast:31 into rows 2 and 3
+  return readlane64(k, 63);
+}
+
 // Lexicographic minimum of (k1, k0) over lanes 0..N-1 (N = 64: the wavefront; N <= 16:
 // within row 0) by DPP moves toward lane N - 1; every lane gets it.
 template <int N>
@@ -1056,6 +1068,7 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     int32_t dmin;
     if (__ballot(wide) == 0) {  // every listed queue below 2^64: scores below 2^96, two words
       uint64_t k1 = ~uint64_t(0), k0 = ~uint64_t(0);
+      bool big = false;
 #pragma unroll
       for (int h = 0; h < SQE; ++h)
         if (v[h]) {
@@ -1063,13 +1076,19 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
           const uint64_t p0 = uint64_t(uint32_t(lo)) * n[h];
           const uint64_t p1 = (lo >> 32) * n[h] + (p0 >> 32);  // score = p1 2^32 + low word of p0
           const uint64_t c0 = (p0 << 32) | d[h];
+          big |= p1 >= (uint64_t(1) << 20);
           if (p1 < k1 || (p1 == k1 && c0 < k0)) {
             k1 = p1;
             k0 = c0;
           }
         }
-      wave_min_key<64>(k1, k0);
-      dmin = int32_t(uint32_t(k0));
+      if (__ballot(big) == 0) {  // and below 2^52: (score, d) in one word, score 2^12 + d
+        const uint64_t k = k1 == ~uint64_t(0) ? ~uint64_t(0) : (k1 << 44) | ((k0 >> 32) << 12) | (k0 & 4095u);
+        dmin = int32_t(uint32_t(wave_min_u64(k)) & 4095u);
+      } else {
+        wave_min_key<64>(k1, k0);
+        dmin = int32_t(uint32_t(k0));
+      }
     } else {
       MinPD best{{0, 0}, 0x7FFFFFFF};
 #pragma unroll
