@@ -1237,7 +1237,7 @@ constexpr int GB = 2;
 constexpr int EC = 4;
 __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys, uint64_t *vals, uint64_t *pos,
                                                     unsigned long long *count, unsigned long long *n_tomb,
-                                                    unsigned long long *hist1, uint64_t cap) {
+                                                    unsigned long long *hist1, uint64_t *toff, uint64_t cap) {
   __shared__ uint32_t wt[TB / 64];
   __shared__ unsigned long long wg_base;
   __shared__ uint32_t h1[2048];
@@ -1304,7 +1304,10 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
       before += w < wave ? wt[w] : 0;
       total += wt[w];
     }
-    if (threadIdx.x == 0) wg_base = total ? atomicAdd(count, (unsigned long long)total) : 0;
+    if (threadIdx.x == 0) {
+      wg_base = total ? atomicAdd(count, (unsigned long long)total) : 0;
+      if (toff) toff[b0 / per_round] = (uint64_t(wg_base) << 16) | total;  // rounds land anywhere
+    }
     __syncthreads();
     unsigned long long at = wg_base + before + x - c;
 #pragma unroll
@@ -1404,15 +1407,25 @@ __device__ __forceinline__ int sel_cmp(uint64_t key, uint64_t v, const SelPrefix
 // race for a bucket, and a lane's writes land in the same few buckets.
 constexpr int RS = 16;
 __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const uint64_t *vals, uint64_t n,
-                                     SelPrefix cut, uint64_t *trig, unsigned long long *n_trig, uint64_t *def,
-                                     unsigned long long *n_def, uint64_t cap) {
+                                     SelPrefix cut, const uint64_t *pos, uint64_t *trig, unsigned long long *n_trig,
+                                     uint64_t *def, unsigned long long *n_def, uint64_t cap) {
   const int lane = threadIdx.x & 63;
   const uint64_t wave = (uint64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
   const uint64_t n_waves = (uint64_t(gridDim.x) * blockDim.x) >> 6;
   for (uint64_t t0 = wave * 64 * RS; t0 < n; t0 += n_waves * 64 * RS) {  // whole wavefronts iterate together
     const uint64_t base = t0 + uint64_t(lane) * RS;
-    uint64_t k[RS], v[RS];
-    if (base + RS <= n) {
+    uint32_t want = base < n ? (base + RS <= n ? 0xFFFFu : (1u << (n - base)) - 1u) : 0u;
+    if (pos) {  // only the entries the tile pass left to claims
+      uint32_t w = 0;
+#pragma unroll
+      for (int j = 0; j < RS; ++j) w |= uint32_t(base + j < n && ((pos[base + j] >> 62) & 1)) << j;
+      want &= w;
+    }
+    uint64_t k[RS], v[RS];  // (no early exit: the appends below are wavefront-wide)
+    if (!want) {
+#pragma unroll
+      for (int j = 0; j < RS; ++j) k[j] = v[j] = 0;
+    } else if (base + RS <= n) {
       const ulonglong2 *pk = reinterpret_cast<const ulonglong2 *>(keys + base);
       const ulonglong2 *pv = reinterpret_cast<const ulonglong2 *>(vals + base);
 #pragma unroll
@@ -1433,7 +1446,7 @@ __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const ui
     uint32_t tmask = 0, dmask = 0;  // entries of the stretch that trigger a conversion / are deferred
 #pragma unroll
     for (int j = 0; j < RS; ++j) {
-      if (base + j < n && sel_cmp(k[j], v[j], cut) > 0) {
+      if (((want >> j) & 1) && sel_cmp(k[j], v[j], cut) > 0) {
         bool t;
         const int pl = place_new(ix, k[j], val_inst(v[j]), val_epoch(v[j]), uint32_t(v[j] & 0xFFFFFF), t, true);
         if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
@@ -1446,6 +1459,83 @@ __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const ui
     append_wave_mask(n_trig, trig, cap, tmask, base);
     append_wave_mask(n_def, def, cap, dmask, base);
   }
+}
+
+// Rebuild, first pass, without atomics: workgroup k writes the whole of the cleared
+// table's tile k (the gather's round of TB x GB buckets), assembled in LDS.  Thread t owns
+// buckets 2t, 2t + 1 of the tile and takes the survivors whose old slot lay there (the
+// gather wrote each tile's entries in slot order): a plain entry whose home bucket is one
+// of the two goes to the first free slot from its home bucket on, so every slot between
+// its home and its slot is occupied, as linear probing requires.  Everything else --
+// members, entries whose home is elsewhere, a pair of full buckets -- is marked (bit 62 of
+// its slot word) for the claim pass, which enters it from its home bucket in the written
+// table as before.
+static_assert(GB == 2, "two buckets per thread");
+__global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
+                                                          const uint64_t *__restrict__ vals, uint64_t *__restrict__ pos,
+                                                          const uint64_t *__restrict__ toff, SelPrefix cut) {
+  constexpr int RT = TB * GB;
+  __shared__ uint64_t tb[RT * BUCKET_WORDS];  // the tile: keys, then values, per bucket
+  __shared__ uint16_t sp[RT * SLOTS];         // each entry's old slot in the tile (bit 15: a member)
+  const int t = threadIdx.x;
+  const uint64_t b_lo = uint64_t(blockIdx.x) * RT;
+  const uint64_t seg = toff[blockIdx.x] >> 16;
+  const uint32_t cnt = uint32_t(toff[blockIdx.x] & 0xFFFF);  // <= RT * SLOTS
+  for (int i = t; i < RT * BUCKET_WORDS; i += TB) tb[i] = 0;  // KEY_EMPTY
+  for (uint32_t i = t; i < cnt; i += TB) {
+    const uint64_t ps = pos[seg + i];
+    sp[i] = uint16_t(((ps & ((uint64_t(1) << 62) - 1)) - b_lo * SLOTS) | ((ps >> 63) << 15));
+  }
+  __syncthreads();
+  auto lower = [&](uint32_t slot) {  // first entry whose old slot in the tile is >= slot
+    uint32_t lo = 0, hi = cnt;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if ((sp[mid] & 0x7FFFu) < slot) lo = mid + 1;
+      else hi = mid;
+    }
+    return lo;
+  };
+  const uint32_t j_lo = lower(2 * SLOTS * t), n_mine = lower(2 * SLOTS * (t + 1)) - j_lo;  // <= 16
+  // the thread's entries, all loads first (clamped into its range)
+  constexpr int ME = 2 * SLOTS;
+  uint64_t k[ME], v[ME];
+#pragma unroll
+  for (int u = 0; u < ME; ++u) {  // unconditional loads, every index inside the tile's entries
+    const uint32_t j = j_lo + uint32_t(u) < cnt ? j_lo + uint32_t(u) : (cnt ? cnt - 1 : 0);
+    k[u] = keys[seg + j];
+    v[u] = vals[seg + j];
+  }
+  const uint64_t mine = b_lo + 2 * uint64_t(t);  // first of this thread's buckets
+  uint32_t used = 0;  // occupancy of the 16 slots of the thread's two buckets
+#pragma unroll
+  for (int u = 0; u < ME; ++u) {
+    if (uint32_t(u) >= n_mine) break;
+    if (sel_cmp(k[u], v[u], cut) <= 0) continue;  // evicted
+    const uint32_t e = sp[j_lo + u];
+    bool placed = false;
+    if (!(e >> 15)) {
+      const uint64_t h = home_bucket(k[u], ix.n_buckets);
+      if (h >= mine && h < mine + 2) {
+        const uint32_t free = ~used & (0xFFFFu << (uint32_t(h - mine) * SLOTS)) & 0xFFFFu;
+        if (free) {
+          const int s = __builtin_ctz(free);
+          used |= 1u << s;
+          const int bk = 2 * t + s / SLOTS;
+          tb[bk * BUCKET_WORDS + s % SLOTS] = k[u];
+          tb[bk * BUCKET_WORDS + SLOTS + s % SLOTS] = v[u];  // a plain value (kind bits 0)
+          placed = true;
+        }
+      }
+    }
+    if (!placed)  // for the claim pass
+      pos[seg + j_lo + u] = (b_lo * SLOTS + (e & 0x7FFFu)) | (uint64_t(e >> 15) << 63) | (uint64_t(1) << 62);
+  }
+  __syncthreads();
+  const uint64_t nb = ix.n_buckets - b_lo < uint64_t(RT) ? ix.n_buckets - b_lo : uint64_t(RT);
+  ulonglong2 *dst = reinterpret_cast<ulonglong2 *>(ix.slots + b_lo * BUCKET_WORDS);
+  const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(tb);
+  for (uint64_t w = t; w < nb * (BUCKET_WORDS / 2); w += TB) dst[w] = src[w];
 }
 
 // Enter the deferred pairs once their keys are converted (or, with the pool exhausted,
@@ -1539,6 +1629,7 @@ struct EvictWs {
   unsigned long long *hist;   // SEL_BINS counts of the eviction's selection passes
   uint64_t *ka, *va, *kb, *vb;  // entries and their sort ping-pong buffers
   uint64_t *ea, *ia;            // eviction's rebuild: conversion queue and deferred pairs
+  uint64_t *toff;               // eviction: per gather tile, output offset << 16 | entry count
   void *temp;
   size_t temp_bytes;
 };
@@ -1560,7 +1651,8 @@ uint64_t evict_ws_layout(uint64_t cap, EvictWs *ws, void *base) {
     return o;
   };
   const uint64_t o_cnt = take(256), o_hist = take(8 * SEL_BINS), o_ka = take(8 * n), o_va = take(8 * n), o_kb = take(8 * n),
-                 o_vb = take(8 * n), o_ea = take(8 * n), o_ia = take(8 * n), o_tmp = take(tb);
+                 o_vb = take(8 * n), o_ea = take(8 * n), o_ia = take(8 * n), o_toff = take(8 * (n / 512 + 64)),
+                 o_tmp = take(tb);
   if (ws) {
     char *b = static_cast<char *>(base);
     ws->count = reinterpret_cast<unsigned long long *>(b + o_cnt);
@@ -1571,6 +1663,7 @@ uint64_t evict_ws_layout(uint64_t cap, EvictWs *ws, void *base) {
     ws->vb = reinterpret_cast<uint64_t *>(b + o_vb);
     ws->ea = reinterpret_cast<uint64_t *>(b + o_ea);
     ws->ia = reinterpret_cast<uint64_t *>(b + o_ia);
+    ws->toff = reinterpret_cast<uint64_t *>(b + o_toff);
     ws->temp = b + o_tmp;
     ws->temp_bytes = tb;
   }
@@ -1595,7 +1688,7 @@ int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, uint6
   if (rc) return rc;
   const uint64_t n_slots = ix.n_buckets * SLOTS;
   hipLaunchKernelGGL(gather_kernel, dim3(grid_for(n_slots)), dim3(TB), 0, s, ix, ws.ka, ws.va, nullptr, ws.count,
-                     nullptr, nullptr, n);
+                     nullptr, nullptr, nullptr, n);
   if ((rc = hip_rc(hipGetLastError()))) return rc;
   unsigned long long got = 0;
   if (hipMemcpyAsync(&got, ws.count, 8, hipMemcpyDeviceToHost, s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
@@ -1720,7 +1813,7 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   const DevIndex ix = dev_view(idx);
   uint64_t *pos = ws.kb;  // free until a dump: each entry's slot
   hipLaunchKernelGGL(gather_kernel, dim3(grid_for(ix.n_buckets * SLOTS)), dim3(TB), 0, stream, ix, ws.ka, ws.va,
-                     pos, ws.count, ws.count + 3, ws.hist, n);
+                     pos, ws.count, ws.count + 3, ws.hist, ws.toff, n);
   unsigned long long cnt[6] = {0, 0, 0, 0, 0, 0};
   unsigned long long hh[SEL_BINS];
   if (hipMemcpyAsync(cnt, ws.count, sizeof(cnt), hipMemcpyDeviceToHost, stream) != hipSuccess ||
@@ -1791,15 +1884,17 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   // else rebuild from the survivors (the entries above the cut, exactly n - m of them),
   // which also clears every tombstone
   uint64_t *keys = ws.ka, *vals = ws.va;
-  if ((rc = fill(ix.slots, ix.n_buckets * BUCKET_WORDS * 8, 0, stream))) return rc;
   if ((rc = fill(ix.pool, ix.n_records * uint64_t(ix.words) * 8, 0, stream))) return rc;
   hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m), 1);
+  // tile pass (writes every bucket: no clear needed), then the claims for what it left
+  const uint64_t n_tiles = (ix.n_buckets + TB * GB - 1) / (TB * GB);
+  hipLaunchKernelGGL(rebuild_tile_kernel, dim3(n_tiles), dim3(TB), 0, stream, ix, keys, vals, pos, ws.toff, p);
   uint64_t *trig = ws.ea;  // free buffers: the conversion queue and the deferred pairs
   unsigned long long *n_trig = ws.count + 1;
   uint64_t *def = ws.ia;
   unsigned long long *n_def = ws.count + 2;
-  hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n / RS)), dim3(TB), 0, stream, ix, keys, vals, n, p, trig,
-                     n_trig, def, n_def, idx->capacity);
+  hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n / RS)), dim3(TB), 0, stream, ix, keys, vals, n, p, pos,
+                     trig, n_trig, def, n_def, idx->capacity);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr, nullptr,
                      nullptr);
   // every member of a key with a bitmap record is deferred here (millions): the full grid
