@@ -95,6 +95,14 @@ def test_config3_scaled_with_eviction(probed, frac):
     run_sessions(wl, 5, capacity=400_000, evict=frac, probed=probed)
 
 
+def test_config3_tombstones_accumulate_then_rebuild():
+    """An eighth evicted after each of ten batches: the first evictions leave tombstones in
+    place (inserts, matches and later evictions run over them), then the tombstones pass
+    the limit and the table is rebuilt; the dump equals the oracle's after every step."""
+    wl = W.config3(n_sess=160, n_turns=10, prefix_len=4096, tail=(256, 3000), app=512)
+    run_sessions(wl, 10, capacity=400_000, evict=(1, 8), probed=True)
+
+
 def test_partition_overlaps_previous_insert():
     """Two streams: batch t+1's hash and partition run while batch t's insert is still
     queued on the other stream (the partition reads the index geometry only); lookup waits
