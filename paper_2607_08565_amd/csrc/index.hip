@@ -1226,7 +1226,8 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
 // ---------------------------------------------------------------------------------
 // Evict / dump
 // ---------------------------------------------------------------------------------
-// All live entries (plain and member slots; headers are not entries), in table order.
+// All live entries (plain and member slots; headers are not entries): each round's tile of
+// TB x GB buckets in slot order, the tiles wherever their round's reservation fell.
 // Each thread takes GB consecutive buckets per round; a workgroup reserves its round's
 // output with one atomic (one per entry made a single counter the bottleneck).  Optional
 // outputs: each entry's slot (bit 63 set for a member slot) and the number of tombstones,
@@ -1399,9 +1400,10 @@ __device__ __forceinline__ int sel_cmp(uint64_t key, uint64_t v, const SelPrefix
   }
   return 0;
 }
-// Rebuild: enter the entries of (keys, vals)[0, n) that lie above the cut (the
-// eviction's selection prefix) into a cleared table.  The entries arrive in table order,
-// where neighbours share buckets, so lane l of a wavefront takes a stretch of RS
+// Rebuild, claim pass: enter the entries of (keys, vals)[0, n) that lie above the cut
+// (the eviction's selection prefix) and that the tile pass left (bit 62 of their slot
+// word), by claims from their home buckets.  The entries arrive tile by tile in slot
+// order, where neighbours share buckets, so lane l of a wavefront takes a stretch of RS
 // consecutive entries (one 128-byte line of keys and one of values, loaded at once) and
 // places them one after another: the lanes of one step are RS entries apart and rarely
 // race for a bucket, and a lane's writes land in the same few buckets.
@@ -1806,7 +1808,7 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   const uint64_t n = h.n_entries;
   const uint64_t m = uint64_t((static_cast<unsigned __int128>(n) * frac_num + frac_den - 1) / frac_den);
   if (m == 0) return SMETRIC_OK;
-  // all entries, in table order
+  // all entries, tile by tile in slot order
   if ((rc = fill(ws.count, 256, 0, stream)) || (rc = fill(ws.count + 5, 8, ~uint64_t(0), stream)) ||
       (rc = fill(ws.hist, 8 * 2048, 0, stream)))
     return rc;
