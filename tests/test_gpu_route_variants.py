@@ -268,6 +268,17 @@ def test_seqc_random_parity(I):
         assert 5 in seen
 
 
+@pytest.mark.parametrize("R", [1, 2, 31, 32, 33, 63, 64, 65, 97])
+def test_seqc_batch_sizes_around_block_edges(R):
+    """Batches of 1 to 97 requests: the last block partial or full, one to four blocks, on
+    a fleet larger than a candidate list and on one smaller."""
+    from paper_2607_08565_amd import smetric as S
+    for I in (7, 200):
+        rng = np.random.default_rng(1000 * R + I)
+        m, L, hist, turn, q, slack, n_run = _coloc_inputs(rng, R, I)
+        _seqc_both(S, m, L, hist, turn, q, slack, n_run, W.DEFAULT_PARAMS, 17 * R)
+
+
 @pytest.mark.parametrize("I", [2, 4, 37, 150])
 def test_seqc_blocks_of_cached_follow_ups(I):
     """Cached follow-ups whose prev is a candidate, on few instances: most requests of
