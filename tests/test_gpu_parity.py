@@ -439,6 +439,30 @@ def test_match_bad_range_and_empty_requests():
     assert pair.gix.stats()[1] == oracle.EINVAL == pair.oix.status
 
 
+def test_evict_everything_then_refill():
+    """Evicting all entries leaves only tombstones (in place), the next batch is matched
+    against an empty index and inserted over them, nothing-to-evict is a no-op, and a
+    second full eviction rebuilds; the dump equals the oracle's after every step."""
+    rng = np.random.default_rng(77)
+    pair = Pair(2_000, 6)  # small: the third full eviction passes the tombstone limit
+    for step in range(3):
+        toks, off = _rand_prompts(rng, 12, 200, 900)
+        d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+        gm = pair.gix.match(d_keys, d_boff, nb).cpu().numpy()
+        assert np.array_equal(gm, pair.oix.match(okeys, blk_off)), f"step {step}: matched rows"
+        inst = rng.integers(0, 6, 12).astype(np.int32)
+        assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, inst, np.arange(12) + 100 * step, step + 1) == 0
+        pair.compare_index(f"step {step} insert")
+        pair.gix.evict(0, 5)
+        assert pair.oix.evict(0, 5) == 0
+        pair.compare_index(f"step {step} evict nothing")
+        if step != 1:
+            pair.gix.evict(1, 1)
+            assert pair.oix.evict(1, 1) == 0
+            pair.compare_index(f"step {step} evict everything")
+            assert pair.gix.stats()[0] == 0
+
+
 def test_empty_batch_and_single_instance():
     from paper_2607_08565_amd import smetric as S
     pair = Pair(1000, 1)
