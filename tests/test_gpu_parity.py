@@ -527,3 +527,60 @@ def test_probed_path_rejects_untiled_requests():
     assert st == oracle.EINVAL
     after = pair.gix.dump()
     assert all(np.array_equal(a, b) for a, b in zip(before, after))
+
+
+@pytest.mark.parametrize("B", [16, 8])
+def test_reserved_marker_keys(B):
+    """Prompts built so that a block's unremapped key is the table's EMPTY (0) or TOMB
+    (2^64-1) marker, at block 0, at a 64-block tile edge, mid-prompt and as the last
+    block: smetric_hash_blocks and smetric_hash_partition both emit the remapped keys
+    (1, 2^64-2) bit for bit with the oracle, and the index stores, matches and refreshes
+    those keys like any other (the markers themselves are never written as keys)."""
+    from tests.reserved_keys import KEY_EMPTY, KEY_TOMB, prompt_with_reserved
+    seed = W.DEFAULT_SEED
+    rng = np.random.default_rng(40 + B)
+    prompts = [prompt_with_reserved(1, {0: KEY_EMPTY}, seed, B, rng=rng),
+               prompt_with_reserved(1, {0: KEY_TOMB}, seed, B, tail=B - 1, rng=rng),
+               prompt_with_reserved(130, {0: KEY_TOMB, 63: KEY_EMPTY, 64: KEY_TOMB, 100: KEY_TOMB, 129: KEY_EMPTY},
+                                    seed, B, tail=3, rng=rng),
+               prompt_with_reserved(70, {69: KEY_TOMB}, seed, B, rng=rng),
+               rng.integers(0, W.VOCAB, 40 * B + 9, dtype=np.int32)]
+    off = np.zeros(len(prompts) + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    toks = np.concatenate(prompts)
+    I = 4
+    pair = Pair(100_000, I, seed=seed, block=B)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+    where = {0: [1], 1: [2**64 - 2], 2: [2**64 - 2, 1, 2**64 - 2, 2**64 - 2, 1], 3: [2**64 - 2]}
+    pos = {0: [0], 1: [0], 2: [0, 63, 64, 100, 129], 3: [69]}
+    for r, ks in where.items():
+        got = [int(okeys[blk_off[r] + j]) for j in pos[r]]
+        assert got == ks, f"prompt {r}: oracle keys {[hex(k) for k in got]}"
+    assert not np.any(okeys == 0) and not np.any(okeys == np.uint64(2**64 - 1))
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(off), d_boff, nb, block_size=B, seed=seed,
+                                          status=status)
+    assert int(status.item()) == 0
+    assert np.array_equal(keys[:nb].cpu().numpy(), okeys), "fused hash + partition keys"
+    # enter every prompt on its own instance through the probed path, then route the same
+    # prompts again: each sees its whole block sequence on that instance
+    pair.gix.probe_lookup(state, nb)
+    gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
+    om = pair.oix.match(okeys, blk_off)
+    assert np.array_equal(gm, om) and not gm.any()
+    R = len(prompts)
+    inst = (np.arange(R) % I).astype(np.int32)
+    pair.gix.insert_probed(state, R, nb, to_dev(inst), to_dev(np.arange(R, dtype=np.uint32) + 1), 1)
+    assert pair.oix.insert(okeys, blk_off, inst, np.arange(R) + 1, 1) == 0
+    pair.compare_index(f"reserved keys B={B}")
+    gk, _ = pair.gix.dump()
+    assert {1, 2**64 - 2} <= set(int(k) for k in gk)
+    nbr = np.diff(blk_off)
+    for probed in (False, True):
+        b = W.Batch(tokens=toks, tok_off=off, prompt_len=np.diff(off).astype(np.int32),
+                    hist_len=np.diff(off).astype(np.int32), turn=np.ones(R, np.int32),
+                    session=np.arange(R, dtype=np.uint32) + 1, q=np.zeros(I, np.int64), rr_base=0, epoch=2 + probed)
+        pair.step(b, what=f"reserved keys again probed={probed}", probed=probed)
+        m = pair.oix.match(okeys, blk_off)
+        for r in range(R):
+            assert m[r][inst[r]] == nbr[r], (r, m[r].tolist())

@@ -181,3 +181,52 @@ def test_keys_never_reserved_and_no_collisions():
 def test_bad_block_size_rejected():
     with pytest.raises(ValueError):
         oracle.hash_blocks(np.zeros(10, np.int32), [0, 10], 15, 0)
+
+
+# --- the reserved-marker remap (last step of the chained block key) ------------------
+# Keys 0 and 2^64-1 are the device table's EMPTY and TOMB markers; the definition sends
+# them to 1 and 2^64-2.  The prompts below are built (tests/reserved_keys.py) so that
+# their unremapped key is exactly a marker.
+
+from tests.reserved_keys import KEY_EMPTY, KEY_TOMB, prompt_with_reserved  # noqa: E402
+
+
+@pytest.mark.parametrize("B", [16, 8, 64])
+def test_remap_sends_markers_to_their_neighbours(B):
+    seed = 0x5EED
+    for marker, want in ((KEY_EMPTY, 1), (KEY_TOMB, MASK - 1)):
+        t = prompt_with_reserved(1, {0: marker}, seed, B)
+        _, keys = oracle.hash_blocks(t, [0, len(t)], B, seed)
+        assert [int(k) for k in keys] == [want], (B, hex(marker))
+
+
+def test_remap_does_not_feed_back_into_the_chain():
+    """The chain continues from the true state s_j (0, or F^-1(2^64-1)), not from the
+    remapped key: block j+1's state equals its innovation plus M s_j, and the innovation
+    is recovered from the same block at the same position after an ordinary history."""
+    B, seed = 16, 31
+    _, M, _ = oracle.hash_consts(seed, B)
+    rng = np.random.default_rng(8)
+    nxt = rng.integers(0, 151936, B, dtype=np.int32)
+    other = rng.integers(0, 151936, B, dtype=np.int32)
+    ko = _keys(np.concatenate([other, nxt]), B, seed)
+    innov = (inv_finaliser(ko[1]) - M * inv_finaliser(ko[0])) & MASK
+    for marker in (KEY_EMPTY, KEY_TOMB):
+        t = np.concatenate([prompt_with_reserved(1, {0: marker}, seed, B), nxt])
+        k = _keys(t, B, seed)
+        s0 = inv_finaliser(marker)
+        assert k[0] in (1, MASK - 1)
+        assert inv_finaliser(k[1]) == (M * s0 + innov) & MASK
+
+
+def test_remap_in_the_middle_of_a_prompt():
+    """A marker key at block 5 of 9 and at the last block: only those keys move, and the
+    keys after block 5 are those of the unremapped chain (the same prompt's prefix
+    property holds through it)."""
+    B, seed = 16, 77
+    t = prompt_with_reserved(9, {5: KEY_TOMB, 8: KEY_EMPTY}, seed, B, tail=11)
+    k = _keys(t, B, seed)
+    assert k[5] == MASK - 1 and k[8] == 1
+    assert all(v not in (0, MASK, 1, MASK - 1) for i, v in enumerate(k) if i not in (5, 8))
+    for L in (5 * B, 6 * B, 6 * B + 3, 9 * B):
+        assert _keys(t[:L], B, seed) == k[: L // B]
