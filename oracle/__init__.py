@@ -20,6 +20,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "smetric_oracle.cpp")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# a separately built copy (e.g. the sanitizer build the tests make) may be named here
+_LIB_OVERRIDE = os.environ.get("SMETRIC_ORACLE_LIB")
 
 OK, EINVAL, EFULL = 0, -1, -2
 BRANCH_NAMES = {0: "first-turn", 1: "evicted", 2: "stick", 3: "last-resort", 4: "migrate", 255: "invalid"}
@@ -54,9 +56,12 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        build()
-    lib = C.CDLL(_LIB)
+    if _LIB_OVERRIDE:
+        lib = C.CDLL(_LIB_OVERRIDE)
+    else:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        lib = C.CDLL(_LIB)
     P = C.c_void_p
     lib.orc_hash_blocks.argtypes = [P, P, C.c_int32, C.c_int32, C.c_uint64, P, P]
     lib.orc_hash_consts.argtypes = [C.c_uint64, C.c_int32, P, P, P]
