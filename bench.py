@@ -2,11 +2,24 @@
 
 Workload (the throughput configuration): 1,024 instances, 16,384 requests per batch,
 prompt lengths lognormal(median 24,576, sigma 0.6) clipped to [1,024, 131,072], 70 % of
-each prompt's blocks being its session's prior turn (placed on a home instance before
-the run), 64 shared 4,096-token prefixes chosen Zipf(1.2), loads Poisson(50) x 20 ms,
-and an index padded with never-matching filler entries to ~200M entries.  Every timed
-step routes a batch of distinct sessions, so all steps have the same statistics; the
-tokens of every batch are resident in HBM before timing starts.
+each prompt's blocks being its session's prior turn, 64 shared 4,096-token prefixes
+chosen Zipf(1.2), loads Poisson(50) x 20 ms.
+
+The start index is fixed and does not depend on --steps: the prior turns of a fixed set
+of distinct batches (each on a uniform-random home instance), padded with never-matching
+filler entries to exactly --index-entries (200M) entries, in a table of --slots (2^28)
+slots, i.e. ~0.75 occupied, with capacity for one more batch of pairs.  Every step -- warm-
+up and timed -- starts from that index: a device snapshot of it is restored, untimed,
+before each step, so every timed step routes a batch of distinct, pre-inserted sessions
+against the same index.  Each timed step is bracketed by device synchronisations; the
+inputs of every batch are resident in HBM before timing starts.
+
+After the timed steps the last timed batch is checked at full size: the post-route
+insert leaves every request's whole block sequence on its target (the append-only
+property: matched[r][target[r]] = its block count, found by matching the batch again),
+and the entry count grows by exactly the distinct (key, target) pairs the targets did not
+hold; with the CPU baseline, a sample of its requests is compared bit for bit with the
+oracle.
 
 Prints one JSON line (see the fields at the end of main()).
 """
@@ -38,27 +51,29 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--n-req", type=int, default=16384)
     ap.add_argument("--n-inst", type=int, default=1024)
-    ap.add_argument("--index-entries", type=int, default=200_000_000, help="entries at the start of timing")
+    ap.add_argument("--index-entries", type=int, default=200_000_000,
+                    help="entries in the index at the start of every step")
+    ap.add_argument("--slots", type=int, default=1 << 28, help="slots of the index table")
+    ap.add_argument("--distinct-batches", type=int, default=8,
+                    help="distinct batches whose prior turns are in the start index; steps cycle over them")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle time budget for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--direct", action="store_true",
                     help="match and insert probe the index themselves instead of sharing one region-ordered probe")
-    ap.add_argument("--pipelined", action="store_true",
-                    help="two streams: the next batch's hash and partition run beside the current batch's insert "
-                         "(default: one batch at a time on one stream, so each kernel's duration is its own)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the timed steps, copy 1 GiB on the device (the counter runs' scale)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print the per-kernel summary of a rocprofv3 --kernel-trace run of this script and exit")
-    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="write the traffic file from two rocprofv3 --pmc runs of this script and exit")
+    ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_JSON"),
+                    help="write the traffic file from two rocprofv3 --pmc runs of this script (and the JSON "
+                         "line of one of them, which names the workload) and exit")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (rocprofv3 FETCH_SIZE/WRITE_SIZE), if present")
     return ap.parse_args()
 
 
 class Setup:
-    """Resident inputs, the pre-populated index and reusable output buffers."""
+    """Resident inputs, the fixed start index, its snapshot and reusable output buffers."""
 
     def __init__(self, args):
         import torch
@@ -68,11 +83,11 @@ class Setup:
 
         self.S, self.W, self.torch = S, W, torch
         self.args = args
-        self.n_batches = args.warmup + args.steps
+        self.n_distinct = args.distinct_batches
         self.tw = W.ThroughputWorkload(n_req=args.n_req, n_inst=args.n_inst)
         t0 = time.time()
-        self.host = [self.tw.batch(b) for b in range(self.n_batches)]
-        log(f"[setup] generated {self.n_batches} batches in {time.time() - t0:.1f}s")
+        self.host = [self.tw.batch(b) for b in range(self.n_distinct)]
+        log(f"[setup] generated {self.n_distinct} distinct batches in {time.time() - t0:.1f}s")
         self.dev = []
         for tb in self.host:
             b = tb.batch
@@ -93,24 +108,36 @@ class Setup:
         self.ws = torch.empty(S.insert_ws_bytes(max(max_blocks, self.filler_chunk)), dtype=torch.uint8, device="cuda")
         self.probe_state = torch.empty(S.probe_ws_bytes(max_blocks), dtype=torch.uint8, device="cuda")
         self.state2 = [self.probe_state, torch.empty(S.probe_ws_bytes(max_blocks), dtype=torch.uint8, device="cuda")]
-        # default-priority streams: front = hash + partition, back = lookup .. insert
+        # default-priority streams for the overlapped path measurement
         self.sA, self.sB = torch.cuda.Stream(), torch.cuda.Stream()
-        # index: the prior turns of every batch's sessions, then filler
-        growth = 30_000_000 * self.n_batches
-        self.capacity = args.index_entries + growth
-        self.index = S.Index(self.capacity, args.n_inst)
+        # the start index: capacity for the start entries plus one batch of pairs, so the
+        # insert's capacity pre-check always passes
+        self.capacity = args.index_entries + max_blocks
+        self.index = S.Index(self.capacity, args.n_inst, n_slots=args.slots)
         t0 = time.time()
-        for b, (tb, d) in enumerate(zip(self.host, self.dev)):
+        for tb, d in zip(self.host, self.dev):
             self._prepopulate(tb, d)
         n, st = self.index.stats()
         assert st == 0, f"index status {st} after prior turns"
         self.prior_entries = n
-        self._filler(max(args.index_entries - n, 0))
+        if n > args.index_entries:
+            raise SystemExit(f"{self.n_distinct} batches' prior turns give {n} entries, more than --index-entries")
+        self._filler(args.index_entries - n)
         n, st = self.index.stats()
-        assert st == 0, f"index status {st} after filler"
+        assert st == 0 and n == args.index_entries, f"index status {st}, {n} entries after filler"
         self.start_entries = n
-        log(f"[setup] index: {self.prior_entries} prior-turn entries + filler = {n} entries "
-            f"({self.index.mem.numel() / 2**30:.2f} GiB, capacity {self.capacity}) in {time.time() - t0:.1f}s")
+        self.snap = self.index.snapshot()
+        torch.cuda.synchronize()
+        log(f"[setup] index: {self.prior_entries} prior-turn entries + filler = {n} entries in {self.index.n_slots} "
+            f"slots (occupancy {n / self.index.n_slots:.3f}, {self.index.mem.numel() / 2**30:.2f} GiB, "
+            f"capacity {self.capacity}) in {time.time() - t0:.1f}s")
+
+    def batch_of(self, i: int) -> int:
+        """The batch that step i (warm-up steps first, then timed ones) routes."""
+        return i % self.n_distinct
+
+    def restore(self):
+        self.index.restore(self.snap)
 
     def _prepopulate(self, tb, d):
         torch, S = self.torch, self.S
@@ -132,8 +159,6 @@ class Setup:
         done, c = 0, 0
         while done < n:
             m = min(chunk, n - done)
-            m -= m % per if m >= per else 0
-            m = max(m, 1)
             keys, inst, sess = self.tw.filler(m, chunk=c)
             R = (m + per - 1) // per
             off = np.minimum(np.arange(R + 1, dtype=np.int64) * per, m)
@@ -144,76 +169,8 @@ class Setup:
             c += 1
 
     CALLS = ("hash", "probe", "match", "route", "insert")
-    PCALLS = ("hash", "lookup", "match", "route", "insert")
     # names in the JSON line: what each timed call is (region-ordered path)
     SHOW = {"hash": "hash_partition", "probe": "lookup", "match": "match", "route": "route", "insert": "insert"}
-
-    def front(self, b: int, ev=None):
-        """Batch b's hash and partition (one call): they read no index contents."""
-        d, p = self.dev[b], b % 2
-        rec = (lambda k, i: ev[k][i].record()) if ev is not None else (lambda k, i: None)
-        nb = d["n_blocks"]
-        rec("hash", 0)
-        self.index.hash_partition(d["tokens"], d["tok_off"], d["blk_off"], nb, keys=self.keys2[p],
-                                  state=self.state2[p])
-        rec("hash", 1)
-
-    def back(self, b: int, ev=None, before_insert=None):
-        """Batch b's lookup, match, route and insert."""
-        S, d, tb, p = self.S, self.dev[b], self.host[b], b % 2
-        rec = (lambda k, i: ev[k][i].record()) if ev is not None else (lambda k, i: None)
-        nb = d["n_blocks"]
-        rec("lookup", 0)
-        self.index.probe_lookup(self.state2[p], nb)
-        rec("lookup", 1)
-        rec("match", 0)
-        self.index.match_probed(self.state2[p], self.keys2[p], d["blk_off"], nb, matched=self.matched)
-        rec("match", 1)
-        rec("route", 0)
-        S.route(self.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], self.W.DEFAULT_PARAMS,
-                tb.batch.rr_base, target=self.target, branch=self.branch)
-        rec("route", 1)
-        if before_insert is not None:
-            before_insert()
-        rec("insert", 0)
-        self.index.insert_probed(self.state2[p], self.args.n_req, nb, self.target, d["session"], tb.batch.epoch,
-                                 workspace=self.ws)
-        rec("insert", 1)
-
-    def run_pipelined(self, b0: int, n: int, evs=None, after_back=None):
-        """Batches b0 .. b0+n-1 on two streams: batch b+1's front (hash, partition) starts
-        when batch b's insert does and runs beside it; back(b+1) waits for front(b+1) and,
-        on its own stream, for insert(b).  front(b+1) reuses the keys and probe-state
-        buffers of batch b-1, whose back has finished before insert(b) starts."""
-        torch = self.torch
-        done_front, at_insert = {}, {}
-
-        def do_front(b):
-            with torch.cuda.stream(self.sA):
-                if b - 1 in at_insert:
-                    self.sA.wait_event(at_insert[b - 1])
-                self.front(b, evs[b - b0] if evs else None)
-                e = torch.cuda.Event()
-                e.record(self.sA)
-                done_front[b] = e
-
-        def do_back(b):
-            def mark():
-                e = torch.cuda.Event()
-                e.record(self.sB)
-                at_insert[b] = e
-
-            with torch.cuda.stream(self.sB):
-                self.sB.wait_event(done_front[b])
-                self.back(b, evs[b - b0] if evs else None, before_insert=mark)
-
-        do_front(b0)
-        for k in range(n):
-            do_back(b0 + k)
-            if after_back is not None:
-                after_back(b0 + k)
-            if k + 1 < n:
-                do_front(b0 + k + 1)
 
     def step(self, b: int, ev=None):
         """The timed unit: every call of the path on the current stream."""
@@ -245,6 +202,45 @@ class Setup:
             self.index.insert_probed(self.probe_state, self.args.n_req, nb, self.target, d["session"],
                                      tb.batch.epoch, workspace=self.ws)
         rec(5)
+
+    def path_only(self, b: int, p: int, matched):
+        """Hash + partition, lookup and match of batch b into buffer set p (no route, no
+        insert: the index is not changed)."""
+        d, nb = self.dev[b], self.dev[b]["n_blocks"]
+        self.index.hash_partition(d["tokens"], d["tok_off"], d["blk_off"], nb, keys=self.keys2[p],
+                                  state=self.state2[p])
+        self.index.probe_lookup(self.state2[p], nb)
+        self.index.match_probed(self.state2[p], self.keys2[p], d["blk_off"], nb, matched=matched)
+
+    def path_overlapped(self, batches, matched2):
+        """The hash + probe path over consecutive batches on two default-priority streams:
+        batch k+1's hash and partition (stream A; it reads no index contents) run beside
+        batch k's lookup and match (stream B).  Buffer sets alternate, and a set is reused
+        only after the match that read it has finished.  Returns the wall time."""
+        torch = self.torch
+        hashed, matched_done = {}, {}
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k, b in enumerate(batches):
+            p = k % 2
+            with torch.cuda.stream(self.sA):
+                if k - 2 in matched_done:
+                    self.sA.wait_event(matched_done[k - 2])
+                d, nb = self.dev[b], self.dev[b]["n_blocks"]
+                self.index.hash_partition(d["tokens"], d["tok_off"], d["blk_off"], nb, keys=self.keys2[p],
+                                          state=self.state2[p])
+                e = torch.cuda.Event()
+                e.record(self.sA)
+                hashed[k] = e
+            with torch.cuda.stream(self.sB):
+                self.sB.wait_event(hashed[k])
+                self.index.probe_lookup(self.state2[p], nb)
+                self.index.match_probed(self.state2[p], self.keys2[p], d["blk_off"], nb, matched=matched2[p])
+                e = torch.cuda.Event()
+                e.record(self.sB)
+                matched_done[k] = e
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
 
 
 # kernels each timed call launches, in order (names as rocprofv3 reports them)
@@ -315,10 +311,18 @@ def summarize_trace(csv_path: str, steps: int):
     return "\n".join(out)
 
 
-def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int):
+def workload_key(cfg: dict) -> dict:
+    """What the counters depend on besides the kernel sources: the bench workload."""
+    return {k: cfg[k] for k in ("n_instances", "requests_per_batch", "index_entries_start", "index_slots",
+                                "index_capacity", "distinct_batches")}
+
+
+def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int, bench_json: str):
     """HBM traffic per timed call from two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE,
     KiB per dispatch), each scaled by what the counter reads for the 1 GiB device copy that
-    --calibrate-copy issues after the timed steps (the largest copy kernel of each run)."""
+    --calibrate-copy issues after the timed steps (the largest copy kernel of each run).
+    The result is keyed to the kernel sources and to the workload named by the JSON line of
+    one of the runs."""
     import csv
 
     def load(path, counter):
@@ -338,8 +342,10 @@ def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int):
         raise SystemExit("no calibration copy in the counter runs (run bench.py with --calibrate-copy)")
     kf, kw = copy_bytes / fcopy, copy_bytes / wcopy
     fs, ws = timed_step_dispatches(fr, steps), timed_step_dispatches(wr, steps)
-    res = {"sources_sha256_16": kernel_sources_hash(), "fetch_scale": round(kf, 4), "write_scale": round(kw, 4),
-           "kernels": {}}
+    line = [x for x in open(bench_json).read().splitlines() if x.startswith("{")][-1]
+    cfg = json.loads(line)["config"]
+    res = {"sources_sha256_16": kernel_sources_hash(), "workload": workload_key(cfg), "steps": steps,
+           "fetch_scale": round(kf, 4), "write_scale": round(kw, 4), "kernels": {}}
     out = [f"Copy calibration: FETCH_SIZE x {kf:.3f}, WRITE_SIZE x {kw:.3f} = bytes of a {copy_bytes >> 20} MiB copy.",
            "", "| call | kernel | fetched MB | written MB | traffic MB |", "|---|---|---|---|---|"]
     for j, k in enumerate(STEP_SEQ):
@@ -365,8 +371,12 @@ def kernel_sources_hash() -> str:
 def algorithmic_bytes(setup, b, matched, I):
     """Bytes the method itself must move for batch b (see the design notes):
     hash: 4 B per token read + 8 B per block key written;
-    match: per probed block 8 B key + one 64 B bucket burst, I/8 B of holder bitmap per
-    probed block of a widely shared prefix, 4 B per (request, instance) written."""
+    probe: 8 B key + one 64 B bucket burst per probed block (the lookup probes every block;
+    only the blocks up to and including each request's first block nobody holds are
+    necessary for the match);
+    match: the same 72 B per necessary block, I/8 B of holder bitmap per distinct block of a
+    widely shared prefix probed in the batch (each bitmap is charged once), 4 B per
+    (request, instance) written."""
     tb = setup.host[b]
     bt = tb.batch
     n_tok = int(bt.tok_off[-1])
@@ -374,40 +384,42 @@ def algorithmic_bytes(setup, b, matched, I):
     nb = np.diff(setup.dev[b]["blk_off_h"])
     cmax = matched.max(axis=1)
     probes = np.minimum(cmax + 1, nb)  # blocks up to and including the first block nobody holds
-    hot = np.minimum(probes, np.minimum(256, nb))  # blocks of the shared 4,096-token prefix
+    pre_blocks = len(setup.tw.prefixes[0]) // setup.W.BLOCK
+    hot = np.minimum(probes, np.minimum(pre_blocks, nb))  # probed blocks of the request's shared prefix
+    hot_distinct = int(sum(int(hot[tb.prefix_of == p].max(initial=0)) for p in range(len(setup.tw.prefixes))))
     R = len(nb)
+    H = hot_distinct * (I // 8)
     hash_b = 4 * n_tok + 8 * n_blk
-    match_b = int(probes.sum()) * (8 + 64) + int(hot.sum()) * (I // 8) + 4 * R * I
-    # the shared probe answers every block once (the insert needs all of them):
-    # 8 B key + one 64 B bucket burst in, an 8 B descriptor out
-    probe_b = n_blk * (8 + 64 + 8)
-    # the match that follows it reads one 8 B descriptor per necessary block
-    scan_b = int(probes.sum()) * 8 + int(hot.sum()) * (I // 8) + 4 * R * I
+    match_b = int(probes.sum()) * (8 + 64) + H + 4 * R * I
+    probe_b = n_blk * (8 + 64)
+    scan_b = int(probes.sum()) * 8 + H + 4 * R * I  # the match from descriptors: one per necessary block
     return dict(tokens=n_tok, blocks=n_blk, probes=int(probes.sum()), hot_probes=int(hot.sum()),
-                hash=hash_b, match=match_b, probe=probe_b, match_scan=scan_b, route=4 * R * I + 8 * I + 12 * R + 5 * R)
+                hot_distinct=hot_distinct, H=H, descriptor=8 * n_blk, hash=hash_b, match=match_b, probe=probe_b,
+                match_scan=scan_b, route=4 * R * I + 8 * I + 12 * R + 5 * R)
 
 
-def cpu_baseline(setup, budget_s: float, gpu_out):
-    """The oracle, as it stands, on a bounded sample of batch 0: the first n requests,
-    against the exact restriction of the index to their keys (their own prior turns and
-    every prior turn's copy of the shared prefixes they use; filler never matches).
-    Also checks the GPU's batch-0 outputs for those requests bit for bit."""
+def cpu_baseline(setup, b: int, budget_s: float, gpu_out):
+    """The oracle, as it stands, on a bounded sample of batch b: its first n requests,
+    against the exact restriction of the start index to their keys (their own prior turns
+    and every prior turn's copy of the shared prefixes they use; filler never matches),
+    timed on one core.  Also checks the GPU's outputs of that batch for those requests bit
+    for bit."""
     import oracle
 
     W = setup.W
     tw, hosts = setup.tw, setup.host
-    tb0 = hosts[0]
-    b0 = tb0.batch
+    tbs = hosts[b]
+    bs = tbs.batch
     params = W.DEFAULT_PARAMS
     prefix_len = len(tw.prefixes[0])
 
     def run(n):
         R = n
-        toks = b0.tokens[: b0.tok_off[R]]
-        tok_off = b0.tok_off[: R + 1]
+        toks = bs.tokens[: bs.tok_off[R]]
+        tok_off = bs.tok_off[: R + 1]
         ix = oracle.Index(1 << 40, tw.n_inst)
         # shared prefixes used by the sample, held by every session placed with them
-        used = set(tb0.prefix_of[:R].tolist())
+        used = set(tbs.prefix_of[:R].tolist())
         for p in sorted(used):
             pre = tw.prefixes[p]
             pb, pk = oracle.hash_blocks(pre, [0, len(pre)], W.BLOCK, W.DEFAULT_SEED)
@@ -420,30 +432,36 @@ def cpu_baseline(setup, budget_s: float, gpu_out):
                         ix.insert(pk[:m], [0, m], [tb.home[s]], [tb.batch.session[s]], 0)
         # the sample's own prior turns
         blk_off, keys = oracle.hash_blocks(toks, tok_off, W.BLOCK, W.DEFAULT_SEED)
-        prior = (tb0.prior_len[:R] // W.BLOCK).astype(np.int64)
+        prior = (tbs.prior_len[:R] // W.BLOCK).astype(np.int64)
         pos = np.concatenate([np.arange(blk_off[r], blk_off[r] + prior[r]) for r in range(R)])
         poff = np.zeros(R + 1, np.int64)
         poff[1:] = np.cumsum(prior)
-        ix.insert(keys[pos], poff, tb0.home[:R], b0.session[:R], 0)
+        ix.insert(keys[pos], poff, tbs.home[:R], bs.session[:R], 0)
         # timed: hash + match + route + insert, exactly the GPU step's work for n requests
         t0 = time.perf_counter()
         blk_off, keys = oracle.hash_blocks(toks, tok_off, W.BLOCK, W.DEFAULT_SEED)
         m = ix.match(keys, blk_off)
-        tgt, br = oracle.route(m, b0.prompt_len[:R], b0.hist_len[:R], b0.turn[:R], b0.q, params, b0.rr_base)
-        ix.insert(keys, blk_off, tgt, b0.session[:R], b0.epoch)
+        tgt, br = oracle.route(m, bs.prompt_len[:R], bs.hist_len[:R], bs.turn[:R], bs.q, params, bs.rr_base)
+        ix.insert(keys, blk_off, tgt, bs.session[:R], bs.epoch)
         dt = time.perf_counter() - t0
         return dt, keys, m, tgt, br
 
-    dt, *_ = run(8)
-    n = int(max(8, min(setup.args.n_req, 8 * budget_s / max(dt, 1e-6))))
-    dt, keys, m, tgt, br = run(n)
+    cpus = os.sched_getaffinity(0)
+    core = min(cpus)
+    os.sched_setaffinity(0, {core})  # the oracle is single-threaded: one core, as taskset -c would
+    try:
+        dt, *_ = run(8)
+        n = int(max(8, min(setup.args.n_req, 8 * budget_s / max(dt, 1e-6))))
+        dt, keys, m, tgt, br = run(n)
+    finally:
+        os.sched_setaffinity(0, cpus)
     g_keys, g_m, g_t, g_b = gpu_out
     nk = len(keys)
     parity = (np.array_equal(g_keys[:nk], keys) and np.array_equal(g_m[:n], m) and np.array_equal(g_t[:n], tgt)
               and np.array_equal(g_b[:n], br))
     return dict(value=n / dt, unit="requests/s", cores=1, kind="oracle",
-                sample=f"first {n} requests of batch 0 (of {setup.args.n_req}), hash+match+route+insert, "
-                       f"index restricted to their keys, single thread, {dt:.1f} s",
+                sample=f"first {n} requests (of {setup.args.n_req}) of the last timed batch, hash+match+route+insert, "
+                       f"start index restricted to their keys, single thread pinned to core {core}, {dt:.1f} s",
                 cpu=host_cpu_model(), host_threads=os.cpu_count()), parity, n
 
 
@@ -458,11 +476,11 @@ def host_cpu_model() -> str:
 
 
 def measure_evict(setup):
-    """LRU eviction of the whole bench index after the timed batches, wall-clock with
-    device syncs (the call ends in a stream sync of its own), exact count checked at full
-    size (ceil(N f) entries go, status stays 0): first 5 % (the divergent-prefix
-    configuration's rate), which leaves tombstones in place, then a third, which passes the
-    tombstone limit and rebuilds the table (what every few 5 % evictions cost)."""
+    """LRU eviction of the whole start index (restored first), wall-clock with device syncs
+    (the call ends in a stream sync of its own), exact count checked at full size (ceil(N f)
+    entries go, status stays 0): first 5 % (the divergent-prefix configuration's rate),
+    which leaves tombstones in place, then a third, which passes the tombstone limit and
+    rebuilds the table (what every few 5 % evictions cost)."""
     import torch
 
     out = {}
@@ -644,13 +662,46 @@ def variants_parity(setup, inputs) -> dict:
 COPY_BYTES = 1 << 30
 
 
+def insert_checks(setup, b: int, keys_h, matched_h, target_h, n_after: int) -> dict:
+    """Full-size checks of batch b's post-route insert into the start index (untimed).
+    (i) Append-only (Sec. 2; the target caches the prompt it prefills, Sec. 4.2): matching
+        the batch again gives matched[r][target[r]] = its block count for every request.
+    (ii) The entry count grows by exactly the distinct pairs (key_j, target_r) with
+        j >= matched[r][target_r]: the start index is prefix-closed on every instance (whole
+        prior turns; filler keys match nothing), so the target holds none of those blocks
+        and all the others; nothing is evicted."""
+    torch = setup.torch
+    d = setup.dev[b]
+    off = d["blk_off_h"]
+    nb = np.diff(off)
+    R = len(nb)
+    c_t = matched_h[np.arange(R), target_h].astype(np.int64)
+    starts, cnt = off[:-1] + c_t, nb - c_t
+    base = np.concatenate([[0], np.cumsum(cnt)[:-1]])
+    pos = np.repeat(starts - base, cnt) + np.arange(int(cnt.sum()))
+    k = keys_h[pos]
+    t = np.repeat(target_h.astype(np.uint64), cnt)
+    order = np.lexsort((t, k))
+    ks, ts = k[order], t[order]
+    expect = int(len(ks) > 0) + int(np.count_nonzero((ks[1:] != ks[:-1]) | (ts[1:] != ts[:-1])))
+    got = n_after - setup.start_entries
+    m2 = torch.empty_like(setup.matched)
+    setup.path_only(b, 1, m2)
+    m2 = m2.cpu().numpy()
+    whole = m2[np.arange(R), target_h] == nb
+    return {"append_only_all_requests": bool(whole.all()), "requests": int(R),
+            "requests_failing": int((~whole).sum()),
+            "new_entries": {"got": int(got), "expected_distinct_new_pairs": expect, "equal": bool(got == expect)}}
+
+
 def main():
     args = parse()
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.steps))
         return
     if args.summarize_pmc:
-        res, md = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.steps, COPY_BYTES)
+        res, md = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.steps, COPY_BYTES,
+                                args.summarize_pmc[2])
         with open(args.traffic, "w") as f:
             json.dump(res, f, indent=1)
         print(md)
@@ -664,54 +715,33 @@ def main():
     torch.cuda.set_device(0)
     setup = Setup(args)
     S = setup.S
-    pipelined = args.pipelined and not args.direct
-    # warmup (untimed); batch 0's outputs are kept for the sampled oracle check
-    gpu_out = None
-
-    def capture(b):
-        nonlocal gpu_out
-        if b == 0:
-            torch.cuda.synchronize()
-            nb0 = setup.dev[0]["n_blocks"]
-            gpu_out = (setup.keys2[0][:nb0].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
-                       setup.branch.cpu().numpy())
-
-    if pipelined:
-        setup.run_pipelined(0, args.warmup, after_back=capture)
-    else:
-        for b in range(args.warmup):
-            setup.step(b)
-            capture(b)
+    # warm-up (untimed), each step from the start index
+    for i in range(args.warmup):
+        setup.restore()
+        setup.step(setup.batch_of(i))
     torch.cuda.synchronize()
-    n_before, _ = setup.index.stats()
-    if pipelined:
-        evs = [{c: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                for c in Setup.PCALLS} for _ in range(args.steps)]
-    else:
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    if pipelined:
-        setup.run_pipelined(args.warmup, args.steps, evs)
-    else:
-        for k in range(args.steps):
-            setup.step(args.warmup + k, evs[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    if pipelined:
-        per = {c: float(np.mean([evs[k][c][0].elapsed_time(evs[k][c][1]) for k in range(args.steps)]))
-               for c in Setup.PCALLS}
-        per["probe"] = per["lookup"]
-    else:
-        per = {n: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
-               for i, n in enumerate(Setup.CALLS)}
-    n, st = setup.index.stats()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    wall = 0.0
+    for k in range(args.steps):
+        setup.restore()  # untimed: every step starts from the same index
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        setup.step(setup.batch_of(args.warmup + k), evs[k])
+        torch.cuda.synchronize()
+        wall += time.perf_counter() - t0
+    per = {n: float(np.mean([evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(args.steps)]))
+           for i, n in enumerate(Setup.CALLS)}
+    n_after, st = setup.index.stats()
     assert st == 0, f"index status {st}"
-    # algorithmic bytes for the last timed batch (match outputs still in the buffer)
-    last = args.warmup + args.steps - 1
-    alg = algorithmic_bytes(setup, last, setup.matched.cpu().numpy(), args.n_inst)
+    # the last timed batch, checked at full size (untimed)
+    last = setup.batch_of(args.warmup + args.steps - 1)
+    nb_last = setup.dev[last]["n_blocks"]
+    gpu_out = (setup.keys[:nb_last].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
+               setup.branch.cpu().numpy())
+    checks = insert_checks(setup, last, gpu_out[0], gpu_out[1], gpu_out[2], n_after)
+    alg = algorithmic_bytes(setup, last, gpu_out[1], args.n_inst)
     R = args.n_req
-    tokens = float(np.mean([setup.host[args.warmup + k].batch.n_tokens for k in range(args.steps)]))
+    tokens = float(np.mean([setup.host[setup.batch_of(args.warmup + k)].batch.n_tokens for k in range(args.steps)]))
     ms_step = wall * 1e3 / args.steps
     probe_match_ms = per["probe"] + per["match"]
     gbs = {"hash": alg["hash"] / per["hash"] / 1e6}
@@ -721,10 +751,20 @@ def main():
         gbs["probe"] = alg["probe"] / per["probe"] / 1e6
         gbs["match"] = alg["match_scan"] / per["match"] / 1e6
     dominant = max(("hash", "probe", "match", "route"), key=lambda k: per[k])
+    cfg = {"workload": f"throughput: {args.n_inst} instances, {R} requests/batch, lognormal(24576, 0.6) prompts in "
+                       f"[1024, 131072], 70% prior-turn blocks, 64 Zipf(1.2) 4096-token prefixes; start index "
+                       f"{setup.start_entries} entries in {setup.index.n_slots} slots (restored before every step)",
+           "n_instances": args.n_inst, "requests_per_batch": R, "block_size": 16,
+           "index_entries_start": setup.start_entries, "index_prior_turn_entries": setup.prior_entries,
+           "index_slots": setup.index.n_slots,
+           "occupancy_start": round(setup.start_entries / setup.index.n_slots, 4),
+           "index_entries_after_step": n_after, "index_capacity": setup.capacity,
+           "distinct_batches": setup.n_distinct, "tokens_per_batch": int(tokens)}
     tr = {}
     if os.path.exists(args.traffic) and not args.direct:
         t = json.load(open(args.traffic))
-        if t.get("sources_sha256_16") == kernel_sources_hash():  # counters of the current kernels only
+        # counters of the current kernels on this workload only
+        if t.get("sources_sha256_16") == kernel_sources_hash() and t.get("workload") == workload_key(cfg):
             tr = t
     launches = (lambda c: None if args.direct else CALL_KERNELS[c])
     show = (lambda c: c) if args.direct else (lambda c: Setup.SHOW[c])
@@ -732,36 +772,56 @@ def main():
             "achieved": round(gbs.get(dominant, 0.0), 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs.get(dominant, 0.0) / HBM_PEAK_GBS, 4),
             "traffic": round(tr[dominant]) if dominant in tr else None}
+    if dominant == "probe" and not args.direct:
+        roof["per_launch"] = {"blocks_probed": alg["blocks"], "bytes_per_probe": 72,
+                              "necessary_probes": alg["probes"],
+                              "necessary_fraction": round(alg["probes"] / max(alg["blocks"], 1), 4),
+                              "descriptor_bytes_written": alg["descriptor"]}
     # the post-route insert: one bucket burst per pair, 16 B per new entry, 8 B per refresh
-    new_pairs = (n - n_before) / args.steps
+    new_pairs = n_after - setup.start_entries
     n_blk = alg["blocks"]
     ins_b = 64 * n_blk + 16 * new_pairs + 8 * (n_blk - new_pairs)
     ins_gbs = ins_b / per["insert"] / 1e6
     insert = {"kernel": "insert", "launches": launches("insert"), "new_pairs": int(new_pairs),
               "achieved": round(ins_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
               "frac": round(ins_gbs / HBM_PEAK_GBS, 4), "traffic": round(tr["insert"]) if "insert" in tr else None}
-    path_gbs = (alg["hash"] + alg["match"]) / (per["hash"] + probe_match_ms) / 1e6
+    path_bytes = alg["hash"] + alg["match"]
+    path_ms = per["hash"] + probe_match_ms
+    path_gbs = path_bytes / path_ms / 1e6
+    path_gbs_noh = (path_bytes - alg["H"]) / path_ms / 1e6
     out = {
         "metric": METRIC, "value": round(R / (ms_step / 1e3), 1), "unit": "requests/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u64", "data": "synthetic",
-        "config": {"workload": f"throughput: {args.n_inst} instances, {R} requests/batch, lognormal(24576, 0.6) "
-                               f"prompts in [1024, 131072], 70% prior-turn blocks, 64 Zipf(1.2) 4096-token prefixes, "
-                               f"{setup.start_entries} index entries at start",
-                   "n_instances": args.n_inst, "requests_per_batch": R, "block_size": 16,
-                   "index_entries_start": setup.start_entries, "index_entries_end": n,
-                   "index_capacity": setup.capacity, "tokens_per_batch": int(tokens)},
-        "path": ("direct" if args.direct else "hash + region partition in one call, then the region-ordered lookup") + (
-            "; next batch's hash + partition overlap this batch's insert (2 streams)" if pipelined else
-            "; one batch at a time"),
+        "config": cfg,
+        "path": ("direct" if args.direct else "hash + region partition in one call, then the region-ordered lookup")
+                + "; one batch at a time, the index restored (untimed) before every step",
         "prompt_tokens_matched_per_s": round(tokens / ((per["hash"] + probe_match_ms) / 1e3), 1),
         "kernel_ms": {show(k): round(per[k], 4) for k in Setup.CALLS if not (args.direct and k == "probe")},
         "algorithmic_GBs": {show(k): round(v, 1) for k, v in gbs.items()},
         "hash_probe_path": {"GBs": round(path_gbs, 1), "frac_of_peak": round(path_gbs / HBM_PEAK_GBS, 4),
-                            "bytes": alg["hash"] + alg["match"], "probes": alg["probes"]},
+                            "frac_of_peak_without_shared_prefix_bitmaps": round(path_gbs_noh / HBM_PEAK_GBS, 4),
+                            "bytes": path_bytes, "shared_prefix_bitmap_bytes": alg["H"],
+                            "necessary_probes": alg["probes"], "blocks": alg["blocks"]},
         "roofline": roof,
         "roofline_insert": insert,
+        "branches": {"counts": np.bincount(gpu_out[3], minlength=5).tolist(),
+                     "names": ["first-turn", "evicted", "stick", "last-resort", "migrate"]},
+        "insert_checks": checks,
     }
+    if not args.direct:  # batch k+1's hash beside batch k's lookup and match (no route, no insert)
+        setup.restore()
+        m2 = [torch.empty_like(setup.matched), torch.empty_like(setup.matched)]
+        batches = [setup.batch_of(args.warmup + k) for k in range(args.steps)]
+        setup.path_overlapped(batches[:2], m2)  # warm
+        dt = setup.path_overlapped(batches, m2)
+        ms = dt * 1e3 / len(batches)
+        out["hash_probe_path_overlapped"] = {
+            "ms_per_batch": round(ms, 4), "GBs": round(path_bytes / ms / 1e6, 1),
+            "frac_of_peak": round(path_bytes / ms / 1e6 / HBM_PEAK_GBS, 4),
+            "how": "two streams: the next batch's hash + partition beside this batch's lookup + match; "
+                   "wall time over the timed batches"}
+        del m2
     if args.calibrate_copy:  # a device copy of known size, for the HBM counters' scale
         src = torch.ones(COPY_BYTES, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -771,11 +831,12 @@ def main():
         del src, dst
     variants, var_inputs = measure_variants(setup, last)
     out["variants"] = variants
+    setup.restore()
     out["evict"] = measure_evict(setup)
     if not args.no_cpu_baseline:
-        cb, parity, n_s = cpu_baseline(setup, args.cpu_seconds, gpu_out)
+        cb, parity, n_s = cpu_baseline(setup, last, args.cpu_seconds, gpu_out)
         out["cpu_baseline"] = cb
-        out["sampled_parity"] = {"requests": n_s, "bit_exact": bool(parity)}
+        out["sampled_parity"] = {"batch": "last timed", "requests": n_s, "bit_exact": bool(parity)}
         out["sampled_parity"]["variants"] = variants_parity(setup, var_inputs)
     print(json.dumps(out), flush=True)
 

@@ -127,20 +127,29 @@ typedef struct smetric_index {
   void *hdr;               /* device counters: entry count, status, pool use        */
 } smetric_index;
 
-/* Device bytes needed for an index of `capacity` entries over `n_instances` instances.
- * EINVAL if capacity == 0 or n_instances is not in [1, 65536]. */
-int smetric_index_bytes(uint64_t capacity, int32_t n_instances, uint64_t *bytes /* host */);
+/* Device bytes needed for an index of `capacity` live entries over `n_instances`
+ * instances.  n_slots = 0 sizes the table so that it is at most 3/4 full at capacity
+ * (headers and tombstones of keys with holder bitmaps included); otherwise the table has
+ * n_slots slots (rounded up to whole 8-slot buckets), which must leave at least 1/16 of
+ * them free at capacity.  A fuller table probes longer chains; in-place eviction then
+ * allows fewer tombstones (half the slots free at capacity, at most an eighth of all
+ * slots) before it rebuilds the table instead.
+ * EINVAL if capacity == 0 or > 2^40, n_instances is not in [1, 65536], or n_slots is
+ * nonzero and too small (or > 2^41). */
+int smetric_index_bytes(uint64_t capacity, int32_t n_instances, uint64_t n_slots, uint64_t *bytes /* host */);
 
-/* Lays the index out in `mem` (>= smetric_index_bytes) and clears it on `stream`.
- * `idx` (host) is filled in.  EINVAL on bad sizes, EHIP if the clear cannot launch. */
+/* Lays the index out in `mem` (>= smetric_index_bytes, 256-byte aligned) and clears it on
+ * `stream`.  `idx` (host) is filled in.  EINVAL on bad sizes, EHIP if the clear cannot
+ * launch. */
 int smetric_index_init(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
-                       int32_t n_instances, hipStream_t stream);
+                       int32_t n_instances, uint64_t n_slots, hipStream_t stream);
 
-/* Like init but leaves the buffer's contents alone: re-attaches an index whose bytes
- * were copied from another buffer laid out with the same capacity and n_instances
- * (a snapshot / restore of the whole index is a plain copy of mem_bytes). */
+/* Like init but leaves the buffer's contents alone: attaches `idx` to an index whose
+ * bytes were copied from another buffer laid out with the same capacity, n_instances and
+ * n_slots (a snapshot / restore of the whole index is a plain device copy of the bytes
+ * smetric_index_bytes reports).  No GPU work; EINVAL as for init. */
 int smetric_index_attach(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
-                         int32_t n_instances);
+                         int32_t n_instances, uint64_t n_slots);
 
 /* Entry count and sticky status (0 or the first device-detected error).  Synchronizes.
  * Pass reset_status != 0 to clear the status afterwards. */

@@ -340,4 +340,4 @@ extern "C" int smetric_block_offsets(const int64_t *tok_off, int32_t n_req, int3
   return SMETRIC_OK;
 }
 
-extern "C" int smetric_version(void) { return (0 << 16) | 1; }
+extern "C" int smetric_version(void) { return (0 << 16) | 2; }

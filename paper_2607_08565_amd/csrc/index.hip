@@ -66,8 +66,12 @@ struct Layout {
   uint64_t n_records, n_buckets, slots_off, pool_off, bytes;
 };
 
-bool layout_for(uint64_t capacity, int32_t n_inst, Layout &L) {
+// n_slots = 0: the table holds capacity entries (plus converted keys' headers and
+// tombstones) at <= 3/4 occupancy.  Otherwise the caller fixes the slot count (rounded up
+// to whole buckets), which must leave at least 1/16 of the slots free at capacity.
+bool layout_for(uint64_t capacity, int32_t n_inst, uint64_t n_slots, Layout &L) {
   if (capacity == 0 || capacity > (uint64_t(1) << 40) || n_inst < 1 || n_inst > 65536) return false;
+  if (n_slots > (uint64_t(1) << 41)) return false;
   L.words = bitmap_words_for(n_inst);
   L.threshold = threshold_for(n_inst);
   uint64_t rec = capacity / 256;
@@ -77,16 +81,21 @@ bool layout_for(uint64_t capacity, int32_t n_inst, Layout &L) {
   L.n_records = rec;
   // slots: live entries plus headers/tombstones of converted keys, at <= 3/4 occupancy
   const uint64_t slots = capacity + uint64_t(L.threshold) * rec;
-  L.n_buckets = (slots * 4 / 3 + SLOTS - 1) / SLOTS + 1;
+  if (n_slots == 0) {
+    L.n_buckets = (slots * 4 / 3 + SLOTS - 1) / SLOTS + 1;
+  } else {
+    L.n_buckets = (n_slots + SLOTS - 1) / SLOTS;
+    if (slots * 16 > L.n_buckets * SLOTS * 15) return false;
+  }
   L.slots_off = sizeof(IndexHdr);
   L.pool_off = L.slots_off + L.n_buckets * BUCKET_WORDS * 8;
   L.bytes = round_up(L.pool_off + L.n_records * uint64_t(L.words) * 8, 256);
   return true;
 }
 
-int attach(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity, int32_t n_inst) {
+int attach(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity, int32_t n_inst, uint64_t n_slots) {
   Layout L;
-  if (!idx || !mem || !layout_for(capacity, n_inst, L) || mem_bytes < L.bytes ||
+  if (!idx || !mem || !layout_for(capacity, n_inst, n_slots, L) || mem_bytes < L.bytes ||
       (reinterpret_cast<uintptr_t>(mem) & 255))
     return SMETRIC_EINVAL;
   char *base = static_cast<char *>(mem);
@@ -1715,24 +1724,24 @@ int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, uint6
 
 using namespace smk;
 
-extern "C" int smetric_index_bytes(uint64_t capacity, int32_t n_instances, uint64_t *bytes) {
+extern "C" int smetric_index_bytes(uint64_t capacity, int32_t n_instances, uint64_t n_slots, uint64_t *bytes) {
   Layout L;
-  if (!bytes || !layout_for(capacity, n_instances, L)) return SMETRIC_EINVAL;
+  if (!bytes || !layout_for(capacity, n_instances, n_slots, L)) return SMETRIC_EINVAL;
   *bytes = L.bytes;
   return SMETRIC_OK;
 }
 
 extern "C" int smetric_index_attach(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
-                                    int32_t n_instances) {
-  return attach(idx, mem, mem_bytes, capacity, n_instances);
+                                    int32_t n_instances, uint64_t n_slots) {
+  return attach(idx, mem, mem_bytes, capacity, n_instances, n_slots);
 }
 
 extern "C" int smetric_index_init(smetric_index *idx, void *mem, uint64_t mem_bytes, uint64_t capacity,
-                                  int32_t n_instances, hipStream_t stream) {
-  int rc = attach(idx, mem, mem_bytes, capacity, n_instances);
+                                  int32_t n_instances, uint64_t n_slots, hipStream_t stream) {
+  int rc = attach(idx, mem, mem_bytes, capacity, n_instances, n_slots);
   if (rc) return rc;
   Layout L;
-  layout_for(capacity, n_instances, L);
+  layout_for(capacity, n_instances, n_slots, L);
   return fill(mem, L.bytes, 0, stream);
 }
 
@@ -1876,8 +1885,15 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
     on_prefix = hh[b];  // rem == on_prefix: the whole bin goes, the prefix itself is the cut
     if (rem < on_prefix && l + 1 == SEL_LEVELS) return SMETRIC_EINTERNAL;  // the full tuple is unique
   }
-  // few tombstones: evict in place, the survivors keep their slots
-  if ((n_tomb + m) * 8 <= ix.n_buckets * SLOTS) {
+  // few tombstones: evict in place, the survivors keep their slots.  Tombstones may take
+  // an eighth of the slots, and at most half of what stays free with the live entries at
+  // capacity (the same eighth under the default 3/4 sizing), so every chain keeps
+  // reaching an EMPTY slot
+  const uint64_t n_slots = ix.n_buckets * SLOTS;
+  const uint64_t reserved = idx->capacity + uint64_t(ix.threshold) * ix.n_records;
+  const uint64_t tomb_cap_free = n_slots > reserved ? (n_slots - reserved) / 2 : 0;
+  const uint64_t tomb_cap = tomb_cap_free < n_slots / 8 ? tomb_cap_free : n_slots / 8;
+  if (n_tomb + m <= tomb_cap) {
     hipLaunchKernelGGL(evict_tomb_kernel, dim3(grid_for(n)), dim3(TB), 0, stream, ix, ws.ka, ws.va, pos, n, p);
     hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m), 0);
     if ((rc = hip_rc(hipGetLastError()))) return rc;

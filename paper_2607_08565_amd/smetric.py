@@ -55,9 +55,9 @@ def _load() -> C.CDLL:
         "smetric_version": [],
         "smetric_block_offsets": [P, I32, I32, P, P],
         "smetric_hash_blocks": [P, I64, P, P, I32, I64, I32, U64, P, P, P],
-        "smetric_index_bytes": [U64, I32, P],
-        "smetric_index_init": [PIX, P, U64, U64, I32, P],
-        "smetric_index_attach": [PIX, P, U64, U64, I32],
+        "smetric_index_bytes": [U64, I32, U64, P],
+        "smetric_index_init": [PIX, P, U64, U64, I32, U64, P],
+        "smetric_index_attach": [PIX, P, U64, U64, I32, U64],
         "smetric_index_stats": [PIX, P, P, I32, P],
         "smetric_match": [PIX, P, P, I32, I64, P, P],
         "smetric_route": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P],
@@ -319,23 +319,42 @@ def probe_ws_bytes(n_blocks: int) -> int:
     return int(b.value)
 
 
-def index_bytes(capacity: int, n_instances: int) -> int:
+def index_bytes(capacity: int, n_instances: int, n_slots: int = 0) -> int:
     b = C.c_uint64()
-    _check("smetric_index_bytes", _lib.smetric_index_bytes(C.c_uint64(capacity), n_instances, C.byref(b)))
+    _check("smetric_index_bytes", _lib.smetric_index_bytes(C.c_uint64(capacity), n_instances, C.c_uint64(n_slots),
+                                                           C.byref(b)))
     return int(b.value)
 
 
 class Index:
-    """Global block index in one device buffer (torch-allocated)."""
+    """Global block index in one device buffer (torch-allocated).  n_slots = 0: the
+    library's default sizing (at most 3/4 full at capacity); else the table's slot count."""
 
-    def __init__(self, capacity: int, n_instances: int, device="cuda", mem: torch.Tensor | None = None):
-        self.capacity, self.n_instances = capacity, n_instances
-        nbytes = index_bytes(capacity, n_instances)
+    def __init__(self, capacity: int, n_instances: int, device="cuda", mem: torch.Tensor | None = None,
+                 n_slots: int = 0, _attach: bool = False):
+        self.capacity, self.n_instances, self.n_slots_arg = capacity, n_instances, n_slots
+        nbytes = index_bytes(capacity, n_instances, n_slots)
         self.mem = torch.empty(nbytes, dtype=torch.uint8, device=device) if mem is None else mem
         self.c = _Index()
-        _check("smetric_index_init", _lib.smetric_index_init(
-            C.byref(self.c), C.c_void_p(self.mem.data_ptr()), nbytes, C.c_uint64(capacity), n_instances, _stream()))
+        if _attach:
+            _check("smetric_index_attach", _lib.smetric_index_attach(
+                C.byref(self.c), C.c_void_p(self.mem.data_ptr()), self.mem.numel(), C.c_uint64(capacity),
+                n_instances, C.c_uint64(n_slots)))
+        else:
+            _check("smetric_index_init", _lib.smetric_index_init(
+                C.byref(self.c), C.c_void_p(self.mem.data_ptr()), self.mem.numel(), C.c_uint64(capacity),
+                n_instances, C.c_uint64(n_slots), _stream()))
         self._ws = None
+
+    @classmethod
+    def attach(cls, mem: torch.Tensor, capacity: int, n_instances: int, n_slots: int = 0) -> "Index":
+        """An index over `mem`, whose bytes are a copy of an index laid out with the same
+        capacity, n_instances and n_slots (smetric_index_attach: nothing is cleared)."""
+        return cls(capacity, n_instances, device=mem.device, mem=mem, n_slots=n_slots, _attach=True)
+
+    @property
+    def n_slots(self) -> int:
+        return int(self.c.n_buckets) * 8
 
     @property
     def ref(self):
@@ -461,8 +480,12 @@ class Index:
             _dev(instance, torch.int32, "instance"), sess, C.c_uint32(epoch), C.c_void_p(ws.data_ptr()), ws.numel(),
             _stream()))
 
-    def snapshot(self) -> torch.Tensor:
-        return self.mem.clone()
+    def snapshot(self, out: torch.Tensor | None = None) -> torch.Tensor:
+        """A device copy of the whole index (attach it, or restore from it)."""
+        if out is None:
+            return self.mem.clone()
+        out.copy_(self.mem)
+        return out
 
     def restore(self, snap: torch.Tensor):
         self.mem.copy_(snap)

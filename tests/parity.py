@@ -28,11 +28,12 @@ def to_dev(a, dtype=None):
 class Pair:
     """The GPU path and the oracle holding the same index state."""
 
-    def __init__(self, capacity: int, n_inst: int, seed: int = W.DEFAULT_SEED, block: int = W.BLOCK):
+    def __init__(self, capacity: int, n_inst: int, seed: int = W.DEFAULT_SEED, block: int = W.BLOCK,
+                 n_slots: int = 0):
         from paper_2607_08565_amd import smetric as S
         self.S = S
         self.I, self.seed, self.B = n_inst, seed, block
-        self.gix = S.Index(capacity, n_inst)
+        self.gix = S.Index(capacity, n_inst, n_slots=n_slots)
         self.oix = oracle.Index(capacity, n_inst)
 
     def hash_both(self, tokens, tok_off):
@@ -100,10 +101,10 @@ class Pair:
 
 
 def run_sessions(wl: W.SessionWorkload, n_batches: int, capacity: int, evict: tuple[int, int] | None = None,
-                 probed: bool = False):
+                 probed: bool = False, n_slots: int = 0):
     """Batch t = turn t of every session.  Open-loop workloads (with a placement) first
     enter turn t-1 on its placed instance; closed-loop ones rely on the post-route insert."""
-    pair = Pair(capacity, wl.n_inst)
+    pair = Pair(capacity, wl.n_inst, n_slots=n_slots)
     prev_targets = None
     branches = []
     for t in range(n_batches):
@@ -121,3 +122,46 @@ def run_sessions(wl: W.SessionWorkload, n_batches: int, capacity: int, evict: tu
             assert pair.oix.evict(*evict) == 0
             pair.compare_index(f"batch {t} after evict")
     return pair, np.concatenate(branches)
+
+
+def distinct_new_pairs(keys_h, blk_off_h, matched_h, target_h) -> int:
+    """Distinct pairs (key_j of request r, target_r) with j >= matched[r][target_r]: the
+    entries an insert at the targets adds to an index that is prefix-closed on every
+    instance (each instance holds whole prompt prefixes), where the target holds exactly
+    the request's first matched[r][target_r] blocks."""
+    nb = np.diff(blk_off_h)
+    R = len(nb)
+    c_t = matched_h[np.arange(R), target_h].astype(np.int64)
+    starts, cnt = blk_off_h[:-1] + c_t, nb - c_t
+    base = np.concatenate([[0], np.cumsum(cnt)[:-1]]).astype(np.int64)
+    pos = np.repeat(starts - base, cnt) + np.arange(int(cnt.sum()))
+    k = keys_h[pos]
+    t = np.repeat(np.asarray(target_h, np.uint64), cnt)
+    o = np.lexsort((t, k))
+    ks, ts = k[o], t[o]
+    return int(len(ks) > 0) + int(np.count_nonzero((ks[1:] != ks[:-1]) | (ts[1:] != ts[:-1])))
+
+
+def check_probed_insert_full(gix, batch: W.Batch, blk_off_h, nb: int, keys, state, matched_h, target_h):
+    """A full-size check of the product path's post-route insert (smetric_index_insert_probed)
+    that needs no full oracle, on an index that is prefix-closed on every instance and not
+    evicted: (i) the entry count grows by exactly the distinct new (key, target) pairs, and
+    (ii) matching the same batch again gives matched[r][target[r]] = its block count for every
+    request (Sec. 2: prompts are append-only; Sec. 4.2: the target caches what it prefills)."""
+    R = batch.n_req
+    n0, st = gix.stats()
+    assert st == 0
+    expect = distinct_new_pairs(keys[:nb].cpu().numpy(), blk_off_h, matched_h, target_h)
+    gix.insert_probed(state, R, nb, to_dev(np.asarray(target_h, np.int32)),
+                      to_dev(np.asarray(batch.session, np.uint32)), batch.epoch)
+    n1, st = gix.stats()
+    assert st == 0, f"insert status {st}"
+    assert n1 - n0 == expect, f"insert added {n1 - n0} entries, expected {expect} distinct new pairs"
+    d_boff = to_dev(blk_off_h)
+    keys2, state2 = gix.hash_partition(to_dev(batch.tokens), to_dev(batch.tok_off), d_boff, nb)
+    gix.probe_lookup(state2, nb)
+    m2 = gix.match_probed(state2, keys2, d_boff, nb).cpu().numpy()
+    whole = m2[np.arange(R), np.asarray(target_h, np.int64)] == np.diff(blk_off_h)
+    assert whole.all(), f"{int((~whole).sum())} requests do not see their whole prompt on their target"
+    say(f"  insert checked at full size: +{n1 - n0} entries ({n1} total), every request whole on its target")
+    return n1 - n0

@@ -40,6 +40,17 @@ def test_host_side_errors_without_gpu():
         S.index_bytes(0, 8)
     with pytest.raises(S.SmetricError):
         S.index_bytes(100, 65537)
+    # an explicit slot count: whole 8-slot buckets, at least 1/16 free at capacity
+    # (capacity 1,000,000 over 1,024 instances keeps 3,906 bitmap records of T = 8 slots)
+    reserved = 1_000_000 + 8 * 3906
+    assert S.index_bytes(1_000_000, 1024, 2**21) > 16 * 2**21
+    assert S.index_bytes(1_000_000, 1024, 1_120_000) < S.index_bytes(1_000_000, 1024)  # fuller than the default
+    lo = -(-reserved * 16 // 15)
+    S.index_bytes(1_000_000, 1024, lo + 8)
+    with pytest.raises(S.SmetricError):
+        S.index_bytes(1_000_000, 1024, lo - 16)
+    with pytest.raises(S.SmetricError):
+        S.index_bytes(100, 8, 2**41 + 1)
     with pytest.raises(S.SmetricError):
         S.block_offsets([0, 10], 15)
     blk, nb = S.block_offsets([0, 15, 31, 100, 100], 16)

@@ -10,8 +10,13 @@ prompt) on their placements, plus its shared system prefix on every instance tha
 received a turn starting with that prefix; no other entry carries one of its keys (other
 sessions' private blocks are chained from different tokens).  Configuration 4 is checked
 the same way by bench.py at full size, configuration 0 in full in test_gpu_parity.
-Configuration 3 also runs one 5 % eviction of its full index, checked by what eviction
-must satisfy at any size: exactly ceil(N/20) entries leave, and every one that leaves
+After the check the last batch is entered at its targets through the product path's
+insert (smetric_index_insert_probed) and checked at full size by what that insert must
+satisfy on an index that is prefix-closed on every instance: the entry count grows by
+exactly the distinct new (key, target) pairs, and every request then sees its whole
+prompt on its target (append-only prompts, Sec. 2; the target caches what it prefills,
+Sec. 4.2).  Configuration 3 then runs one 5 % eviction of its full index, checked by
+what eviction must satisfy at any size: exactly ceil(N/20) entries leave, and every one that leaves
 precedes every one that stays under (epoch, key, instance)."""
 import numpy as np
 import pytest
@@ -19,7 +24,7 @@ import torch
 
 import oracle
 from paper_2607_08565_amd import workload as W
-from tests.parity import say, to_dev
+from tests.parity import check_probed_insert_full, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -62,8 +67,14 @@ def _open_loop_last_batch(wl, capacity, n_sample, seed):
                      b.rr_base)
     say(f"  last batch: {b.n_req} requests, {nb} blocks, {b.n_tokens} tokens")
     sample = np.sort(np.random.default_rng(seed).choice(wl.n_sess, n_sample, replace=False))
-    return dict(gix=gix, place=place, batch=b, blk_off=blk_off, keys=keys, gm=gm.cpu().numpy(),
-                gt=gt.cpu().numpy(), gb=gb.cpu().numpy(), sample=sample)
+    return dict(gix=gix, place=place, batch=b, blk_off=blk_off, keys=keys, state=state, nb=nb,
+                gm=gm.cpu().numpy(), gt=gt.cpu().numpy(), gb=gb.cpu().numpy(), sample=sample)
+
+
+def _check_insert(run):
+    """The product path's insert of the last batch at its targets, checked at full size."""
+    check_probed_insert_full(run["gix"], run["batch"], run["blk_off"], run["nb"], run["keys"], run["state"],
+                             run["gm"], run["gt"])
 
 
 def _check_sample(wl, run, capacity):
@@ -107,6 +118,7 @@ def test_config1_full_size_sampled():
     wl = W.config1()
     run = _open_loop_last_batch(wl, 45_000_000, 24, 101)
     br = _check_sample(wl, run, 45_000_000)
+    _check_insert(run)
     say("  sampled branches", br.tolist(), "all branches", np.bincount(run["gb"], minlength=5).tolist())
 
 
@@ -115,6 +127,7 @@ def test_config2_full_size_sampled():
     wl = W.config2()
     run = _open_loop_last_batch(wl, 160_000_000, 12, 102)
     br = _check_sample(wl, run, 160_000_000)
+    _check_insert(run)
     say("  sampled branches", br.tolist(), "all branches", np.bincount(run["gb"], minlength=5).tolist())
 
 
@@ -125,6 +138,7 @@ def test_config3_full_size_sampled_and_eviction():
     cap = 72_000_000  # a 0.7 load factor of ~50M entries
     run = _open_loop_last_batch(wl, cap, 16, 103)
     _check_sample(wl, run, cap)
+    _check_insert(run)
     gix = run["gix"]
     k0, v0 = gix.dump()
     gix.evict(1, 20)

@@ -580,7 +580,8 @@ def test_reserved_marker_keys(B):
         b = W.Batch(tokens=toks, tok_off=off, prompt_len=np.diff(off).astype(np.int32),
                     hist_len=np.diff(off).astype(np.int32), turn=np.ones(R, np.int32),
                     session=np.arange(R, dtype=np.uint32) + 1, q=np.zeros(I, np.int64), rr_base=0, epoch=2 + probed)
-        pair.step(b, what=f"reserved keys again probed={probed}", probed=probed)
+        pair.step(b, params=dict(W.DEFAULT_PARAMS, block_size=B), what=f"reserved keys again probed={probed}",
+                  probed=probed)
         m = pair.oix.match(okeys, blk_off)
         for r in range(R):
             assert m[r][inst[r]] == nbr[r], (r, m[r].tolist())
