@@ -367,6 +367,22 @@ int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t n_instances
                       int32_t *target, uint8_t *branch, int64_t *q_out, void *workspace,
                       uint64_t ws_bytes, hipStream_t stream);
 
+/* smetric_route_seq without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, outputs and errors as smetric_route_seq, with the per-request
+ * records kept in a scratch array inside the library -- one per GPU, 80 bytes for each of
+ * smetric_route_seq_noalloc_max_req() = 65,536 requests (5 MiB), held until the process
+ * ends.  Its device address is looked up on the first call on each device.  Allocates
+ * nothing; returns SMETRIC_EWORKSPACE when n_req exceeds the maximum (use smetric_route_seq
+ * with a workspace then), SMETRIC_EHIP if the scratch cannot be found.  Every call on a
+ * GPU uses that GPU's one array: calls that overlap on one GPU (on different streams, or
+ * from different threads) race, and must be ordered by the caller. */
+int smetric_route_seq_noalloc_max_req(void);
+int smetric_route_seq_noalloc(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                              const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                              const int64_t *q, const smetric_params *params /* host */, uint64_t rr_base,
+                              int32_t *target, uint8_t *branch, int64_t *q_out, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------------
  * Route under PD colocation (App. B pseudocode): smetric_route's rule with three changes.
  *   * TPOT filter: a colocated instance also decodes, and the new request's prefill

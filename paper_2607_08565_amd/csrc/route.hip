@@ -13,6 +13,8 @@
 // Mapping to gfx950: one wavefront per request; lane l scans instances l, l+64, ...,
 // keeping (max c, lowest id) and (min est2, rotation distance); two butterfly
 // reductions across the wavefront finish the argmax and the argmin; lane 0 decides.
+#include <mutex>
+
 #include "common.h"
 
 namespace smk {
@@ -1386,20 +1388,15 @@ extern "C" int smetric_route_seq_ws_bytes(int32_t n_req, uint64_t *ws_bytes) {
   return SMETRIC_OK;
 }
 
-extern "C" int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t n_instances,
-                                 const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
-                                 const int64_t *q, const smetric_params *params, uint64_t rr_base,
-                                 int32_t *target, uint8_t *branch, int64_t *q_out, void *workspace,
-                                 uint64_t ws_bytes, hipStream_t stream) {
-  RouteParams rp;
-  if (int rc = route_params(params, n_req, n_instances, rp)) return rc;
-  if (n_instances > SEQ_MAX_I || !seq_loads_fit(rp, n_req)) return SMETRIC_EINVAL;
-  if (!q) return SMETRIC_EINVAL;
-  if (n_req > 0 && (!matched || !prompt_len || !hist_len || !turn || !target || !branch)) return SMETRIC_EINVAL;
-  uint64_t need = 0;
-  smetric_route_seq_ws_bytes(n_req, &need);
-  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) || ws_bytes < need) return SMETRIC_EWORKSPACE;
-  SeqRec *recs = static_cast<SeqRec *>(workspace);
+namespace smk {
+namespace {
+
+// The online route after its host checks: the pre-pass writes every request's record
+// into recs (nothing there needs clearing), then one wavefront walks the batch.
+int route_seq_launch(const int32_t *matched, int32_t n_req, int32_t n_instances, const int32_t *prompt_len,
+                     const int32_t *hist_len, const int32_t *turn, const int64_t *q, const RouteParams &rp,
+                     uint64_t rr_base, int32_t *target, uint8_t *branch, int64_t *q_out, SeqRec *recs,
+                     hipStream_t stream) {
   if (n_req > 0)
     hipLaunchKernelGGL(route_seq_prep_kernel, dim3((n_req + RW - 1) / RW), dim3(64 * RW), 0, stream, matched, n_req,
                        n_instances, prompt_len, hist_len, turn, q, rp, rr_base, recs);
@@ -1417,4 +1414,74 @@ extern "C" int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t 
   else SEQ_LAUNCH(0, 8);
 #undef SEQ_LAUNCH
   return hip_rc(hipGetLastError());
+}
+
+int route_seq_checks(const int32_t *matched, int32_t n_req, int32_t n_instances, const int32_t *prompt_len,
+                     const int32_t *hist_len, const int32_t *turn, const int64_t *q, const smetric_params *params,
+                     int32_t *target, uint8_t *branch, RouteParams &rp) {
+  if (int rc = route_params(params, n_req, n_instances, rp)) return rc;
+  if (n_instances > SEQ_MAX_I || !seq_loads_fit(rp, n_req)) return SMETRIC_EINVAL;
+  if (!q) return SMETRIC_EINVAL;
+  if (n_req > 0 && (!matched || !prompt_len || !hist_len || !turn || !target || !branch)) return SMETRIC_EINVAL;
+  return SMETRIC_OK;
+}
+
+// Scratch of the allocation-free online route: one record per request, in a file-scope
+// device array that every GPU the library runs on holds until the process ends.  Host
+// code never passes the array's name to a kernel (on the host it is a stand-in, not a
+// device address): each device's address is looked up once, with that device current,
+// and kept.
+constexpr int32_t SEQ_NOALLOC_MAX_REQ = 65536;
+constexpr int SEQ_NOALLOC_MAX_DEVICES = 64;
+static __device__ __align__(256) SeqRec seq_scratch[SEQ_NOALLOC_MAX_REQ];
+std::mutex seq_scratch_mu;
+SeqRec *seq_scratch_dev[SEQ_NOALLOC_MAX_DEVICES] = {};
+
+int seq_scratch_ptr(SeqRec **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SEQ_NOALLOC_MAX_DEVICES) return SMETRIC_EHIP;
+  std::lock_guard<std::mutex> lock(seq_scratch_mu);
+  if (!seq_scratch_dev[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(seq_scratch)) != hipSuccess || !p) return SMETRIC_EHIP;
+    seq_scratch_dev[dev] = static_cast<SeqRec *>(p);
+  }
+  *out = seq_scratch_dev[dev];
+  return SMETRIC_OK;
+}
+
+}  // namespace
+}  // namespace smk
+
+extern "C" int smetric_route_seq(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                                 const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                                 const int64_t *q, const smetric_params *params, uint64_t rr_base,
+                                 int32_t *target, uint8_t *branch, int64_t *q_out, void *workspace,
+                                 uint64_t ws_bytes, hipStream_t stream) {
+  RouteParams rp;
+  if (int rc = route_seq_checks(matched, n_req, n_instances, prompt_len, hist_len, turn, q, params, target, branch,
+                                rp))
+    return rc;
+  uint64_t need = 0;
+  smetric_route_seq_ws_bytes(n_req, &need);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) || ws_bytes < need) return SMETRIC_EWORKSPACE;
+  return route_seq_launch(matched, n_req, n_instances, prompt_len, hist_len, turn, q, rp, rr_base, target, branch,
+                          q_out, static_cast<SeqRec *>(workspace), stream);
+}
+
+extern "C" int smetric_route_seq_noalloc_max_req(void) { return SEQ_NOALLOC_MAX_REQ; }
+
+extern "C" int smetric_route_seq_noalloc(const int32_t *matched, int32_t n_req, int32_t n_instances,
+                                         const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
+                                         const int64_t *q, const smetric_params *params, uint64_t rr_base,
+                                         int32_t *target, uint8_t *branch, int64_t *q_out, hipStream_t stream) {
+  RouteParams rp;
+  if (int rc = route_seq_checks(matched, n_req, n_instances, prompt_len, hist_len, turn, q, params, target, branch,
+                                rp))
+    return rc;
+  if (n_req > SEQ_NOALLOC_MAX_REQ) return SMETRIC_EWORKSPACE;
+  SeqRec *recs = nullptr;
+  if (int rc = seq_scratch_ptr(&recs)) return rc;
+  return route_seq_launch(matched, n_req, n_instances, prompt_len, hist_len, turn, q, rp, rr_base, target, branch,
+                          q_out, recs, stream);
 }

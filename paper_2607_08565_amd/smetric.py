@@ -70,6 +70,8 @@ def _load() -> C.CDLL:
         "smetric_sessions_ws_bytes": [I32, P],
         "smetric_sessions": [P, P, I32, I64, P, P, P, P, P, P, U64, P],
         "smetric_route_seq": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P, U64, P],
+        "smetric_route_seq_noalloc_max_req": [],
+        "smetric_route_seq_noalloc": [P, I32, I32, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P],
         "smetric_route_seq_coloc": [P, I32, I32, P, P, P, P, P, P, C.POINTER(_Params), U64, P, P, P, P, P, U64, P],
         "smetric_index_insert_ws_bytes": [I64, P],
         "smetric_index_insert": [PIX, P, P, I32, I64, P, P, U32, P, U64, P],
@@ -101,7 +103,7 @@ EXPORTED = (
     "smetric_route_coloc", "smetric_route_seq_ws_bytes", "smetric_route_seq", "smetric_sessions_ws_bytes",
     "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
     "smetric_probe_partition", "smetric_probe_lookup", "smetric_hash_partition", "smetric_route_seq_coloc",
-    "smetric_route_seq_coloc_ws_bytes",
+    "smetric_route_seq_coloc_ws_bytes", "smetric_route_seq_noalloc", "smetric_route_seq_noalloc_max_req",
 )
 
 
@@ -199,6 +201,28 @@ def route_seq(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.T
         C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
         _dev(q_out, torch.int64, "q_out"), _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream()))
     return target[:R], branch[:R], q_out
+
+def route_seq_noalloc(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
+                      q: torch.Tensor, params: dict, rr_base: int, target: torch.Tensor, branch: torch.Tensor,
+                      q_out: torch.Tensor | None = None):
+    """smetric_route_seq_noalloc: smetric_route_seq with the library's own scratch (no
+    workspace; at most route_seq_noalloc_max_req() requests).  The caller supplies the
+    outputs, so the call allocates nothing.  Returns (target, branch, q_out)."""
+    R, I = matched.shape
+    if R > route_seq_noalloc_max_req():
+        raise SmetricError("smetric_route_seq_noalloc", EWORKSPACE)
+    p = _Params(**params)
+    _check("smetric_route_seq_noalloc", _lib.smetric_route_seq_noalloc(
+        _dev(matched, torch.int32, "matched"), R, I, _dev(prompt_len, torch.int32, "prompt_len"),
+        _dev(hist_len, torch.int32, "hist_len"), _dev(turn, torch.int32, "turn"), _dev(q, torch.int64, "q"),
+        C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
+        None if q_out is None else _dev(q_out, torch.int64, "q_out"), _stream()))
+    return target[:R], branch[:R], q_out
+
+
+def route_seq_noalloc_max_req() -> int:
+    return int(_lib.smetric_route_seq_noalloc_max_req())
+
 
 def route_seq_coloc(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch.Tensor, turn: torch.Tensor,
                     q: torch.Tensor, tpot_slack: torch.Tensor, n_running: torch.Tensor, params: dict,
