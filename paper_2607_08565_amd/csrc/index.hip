@@ -11,6 +11,7 @@
 //   [0, 256)                 IndexHdr: entry count, sticky status, pool use
 //   slots                    n_buckets x 128 B: keys[8] then values[8]
 //   pool                     n_records x bitmap_words x 8 B: holder bitmaps
+//   masks                    n_buckets bytes: each chain start's displacement mask
 // A key normally owns one PLAIN slot per holder in its home chain (linear probing over
 // buckets from home_bucket(key)).  When a key gains more than T holders its plain slots
 // are replaced by one HEADER slot pointing at a bitmap record, and every holder becomes a
@@ -89,7 +90,8 @@ bool layout_for(uint64_t capacity, int32_t n_inst, uint64_t n_slots, Layout &L) 
   }
   L.slots_off = sizeof(IndexHdr);
   L.pool_off = L.slots_off + L.n_buckets * BUCKET_WORDS * 8;
-  L.bytes = round_up(L.pool_off + L.n_records * uint64_t(L.words) * 8, 256);
+  // then the displacement masks, one byte per bucket (dev_view finds them after the pool)
+  L.bytes = round_up(L.pool_off + L.n_records * uint64_t(L.words) * 8 + mask_bytes(L.n_buckets), 256);
   return true;
 }
 
@@ -124,8 +126,10 @@ struct Found {
 
 // Find the entry (key, inst), looking through a bitmap record when the key has one.
 __device__ Found find_member(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  uint64_t m = member_bucket(key, inst, ix.n_buckets, ix.nb_inv);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step, m = next_bucket(m, ix.n_buckets)) {
+  ChainWalk w = chain_start(member_bucket(key, inst, ix.n_buckets, ix.nb_inv));
+  bool had_empty;
+  do {
+    const uint64_t m = w.b;
     const uint64_t *mk = ix.slots + m * BUCKET_WORDS;
     const BucketScan sc = scan_bucket(mk, key);
     uint32_t mm = sc.match;
@@ -135,14 +139,16 @@ __device__ Found find_member(const DevIndex &ix, uint64_t key, uint32_t inst) {
       const uint64_t v = mk[SLOTS + t];
       if (val_kind(v) == MEMBER && val_inst(v) == inst) return Found{int64_t(m * SLOTS + t), v};
     }
-    if (sc.empty) break;
-  }
+    had_empty = sc.empty != 0;
+  } while (chain_next(ix, w, had_empty));
   return Found{-1, 0};
 }
 
 __device__ Found find_entry(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  uint64_t b = home_bucket(key, ix.n_buckets);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
+  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets));
+  bool had_empty;
+  do {
+    const uint64_t b = w.b;
     const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
     const BucketScan sc = scan_bucket(bk, key);
     uint32_t mm = sc.match;
@@ -153,13 +159,13 @@ __device__ Found find_entry(const DevIndex &ix, uint64_t key, uint32_t inst) {
       const uint32_t kind = val_kind(v);
       if (kind == PLAIN && val_inst(v) == inst) return Found{int64_t(b * SLOTS + s), v};
       if (kind == HEADER) {
-        const uint64_t w = ix.pool[val_rec(v) * uint64_t(ix.words) + (inst >> 6)];
-        if (!((w >> (inst & 63)) & 1)) return Found{-1, 0};
+        const uint64_t bw = ix.pool[val_rec(v) * uint64_t(ix.words) + (inst >> 6)];
+        if (!((bw >> (inst & 63)) & 1)) return Found{-1, 0};
         return find_member(ix, key, inst);
       }
     }
-    if (sc.empty) break;
-  }
+    had_empty = sc.empty != 0;
+  } while (chain_next(ix, w, had_empty));
   return Found{-1, 0};
 }
 
@@ -185,6 +191,7 @@ struct Claim {
 __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool want_header,
                             uint32_t max_same = 0xFFFFFFFFu) {
   Claim c{-1, -1, 0, false};
+  const uint64_t h = b;  // the chain start whose displacement mask records the claim
   for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
     uint64_t *bk = ix.slots + b * BUCKET_WORDS;
     const BucketScan sc = scan_bucket(bk, key);
@@ -218,6 +225,7 @@ __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool w
       const uint64_t k = atomicCAS(reinterpret_cast<unsigned long long *>(&bk[s]), KEY_EMPTY, key);
       if (k == KEY_EMPTY) {
         c.slot = int64_t(b * SLOTS + s);
+        mask_note(ix, h, b);
         return c;
       }
       if (k == key) {
@@ -654,8 +662,10 @@ __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned l
 // find_member with each bucket read whole (keys and values in one 128-byte request), so
 // a chain step is one round trip.
 __device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  uint64_t m = member_bucket(key, inst, ix.n_buckets, ix.nb_inv);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step, m = next_bucket(m, ix.n_buckets)) {
+  ChainWalk cw = chain_start(member_bucket(key, inst, ix.n_buckets, ix.nb_inv));
+  bool had_empty;
+  do {
+    const uint64_t m = cw.b;
     const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + m * BUCKET_WORDS);
     ulonglong2 kk[SLOTS / 2], vv[SLOTS / 2];
 #pragma unroll
@@ -670,8 +680,8 @@ __device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t ins
       end |= k == KEY_EMPTY;
       if (!end && k == key && val_kind(v) == MEMBER && val_inst(v) == inst) return Found{int64_t(m * SLOTS + s), v};
     }
-    if (end) break;
-  }
+    had_empty = end;
+  } while (chain_next(ix, cw, had_empty));
   return Found{-1, 0};
 }
 
@@ -1519,6 +1529,7 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
   }
   const uint64_t mine = b_lo + 2 * uint64_t(t);  // first of this thread's buckets
   uint32_t used = 0;  // occupancy of the 16 slots of the thread's two buckets
+  uint32_t dm = 0;    // displacement masks of the two buckets (byte 0: mine, byte 1: mine + 1)
 #pragma unroll
   for (int u = 0; u < ME; ++u) {
     if (uint32_t(u) >= n_mine) break;
@@ -1535,6 +1546,7 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
           const int bk = 2 * t + s / SLOTS;
           tb[bk * BUCKET_WORDS + s % SLOTS] = k[u];
           tb[bk * BUCKET_WORDS + SLOTS + s % SLOTS] = v[u];  // a plain value (kind bits 0)
+          if (s / SLOTS > uint32_t(h - mine)) dm |= 2u;  // from bucket mine into mine + 1: displacement 1
           placed = true;
         }
       }
@@ -1542,6 +1554,9 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
     if (!placed)  // for the claim pass
       pos[seg + j_lo + u] = (b_lo * SLOTS + (e & 0x7FFFu)) | (uint64_t(e >> 15) << 63) | (uint64_t(1) << 62);
   }
+  // the two buckets' masks restart from what the tile places; the claim pass adds the rest
+  if (mine + 1 < ix.n_buckets) *reinterpret_cast<uint16_t *>(ix.mask + mine) = uint16_t(dm);
+  else if (mine < ix.n_buckets) ix.mask[mine] = uint8_t(dm);
   __syncthreads();
   const uint64_t nb = ix.n_buckets - b_lo < uint64_t(RT) ? ix.n_buckets - b_lo : uint64_t(RT);
   ulonglong2 *dst = reinterpret_cast<ulonglong2 *>(ix.slots + b_lo * BUCKET_WORDS);

@@ -52,9 +52,10 @@ __device__ Holders probe(const DevIndex &ix, uint64_t key) {
 #pragma unroll
   for (int i = 0; i < LIST_MAX; ++i) H.h[i] = 0xFFFFFFFFu;
   uint32_t cnt = 0;
-  uint64_t b = home_bucket(key, ix.n_buckets);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
-    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets));
+  bool had_empty;
+  do {
+    const uint64_t *bk = ix.slots + w.b * BUCKET_WORDS;
     uint64_t k[SLOTS];
     load_keys(bk, k);
     uint32_t mm = 0, em = 0;
@@ -82,47 +83,54 @@ __device__ Holders probe(const DevIndex &ix, uint64_t key) {
         ++cnt;
       }
     }
-    if (em) break;
-    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
-  }
+    had_empty = em != 0;
+  } while (chain_next(ix, w, had_empty));
   H.kind = cnt == 0 ? H_NONE : (cnt <= LIST_MAX ? H_LIST : H_LONG);
   return H;
 }
 
 // Is (key, inst) a plain entry?  Used for LONG holder sets only.
 __device__ bool chain_has(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  uint64_t b = home_bucket(key, ix.n_buckets);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
-    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+  ChainWalk cw = chain_start(home_bucket(key, ix.n_buckets));
+  bool had_empty;
+  do {
+    const uint64_t *bk = ix.slots + cw.b * BUCKET_WORDS;
+    had_empty = false;
     for (int s = 0; s < SLOTS; ++s) {
       const uint64_t k = bk[s];
-      if (k == KEY_EMPTY) return false;
+      if (k == KEY_EMPTY) {
+        had_empty = true;
+        break;
+      }
       if (k == key) {
         const uint64_t v = bk[SLOTS + s];
         if (val_kind(v) == PLAIN && val_inst(v) == inst) return true;
       }
     }
-    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
-  }
+  } while (chain_next(ix, cw, had_empty));
   return false;
 }
 
 // OR into `m` the bits of every plain holder of `key` that fall in word w.
 __device__ uint64_t chain_word(const DevIndex &ix, uint64_t key, int w) {
   uint64_t m = 0;
-  uint64_t b = home_bucket(key, ix.n_buckets);
-  for (uint64_t step = 0; step < ix.n_buckets; ++step) {
-    const uint64_t *bk = ix.slots + b * BUCKET_WORDS;
+  ChainWalk cw = chain_start(home_bucket(key, ix.n_buckets));
+  bool had_empty;
+  do {
+    const uint64_t *bk = ix.slots + cw.b * BUCKET_WORDS;
+    had_empty = false;
     for (int s = 0; s < SLOTS; ++s) {
       const uint64_t k = bk[s];
-      if (k == KEY_EMPTY) return m;
+      if (k == KEY_EMPTY) {
+        had_empty = true;
+        break;
+      }
       if (k == key) {
         const uint64_t v = bk[SLOTS + s];
         if (val_kind(v) == PLAIN && int(val_inst(v) >> 6) == w) m |= uint64_t(1) << (val_inst(v) & 63);
       }
     }
-    b = (b + 1 == ix.n_buckets) ? 0 : b + 1;
-  }
+  } while (chain_next(ix, cw, had_empty));
   return m;
 }
 

@@ -20,8 +20,10 @@
 //             position, and the inverse index block -> position
 //   probe     a fixed grid of FLAT_WG workgroups walks the region-ordered keys; all
 //             workgroups advance through the regions together, so the live window slides
-//             through the table.  One 128-byte bucket read per chain step (keys and values
-//             at once) gives a 64-bit holder descriptor, written in region order.
+//             through the table.  One 128-byte bucket read (keys and values at once) per
+//             bucket of the key's chain -- its home bucket, and when that is full the
+//             buckets its displacement mask names -- gives a 64-bit holder descriptor,
+//             written in region order.
 // Requests must tile [0, n_blocks): blk_off[0] = 0, non-decreasing, blk_off[n_req] =
 // n_blocks; otherwise the probe state is marked invalid (EINVAL).
 #include "common.h"
@@ -218,35 +220,39 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
 }
 
 // Holder descriptor of a key, built one 128-byte bucket (keys and values at once) per
-// chain step.
+// bucket of the key's chain: its home bucket, and only when that is full the buckets its
+// displacement mask names.
 struct DescWalk {
-  uint64_t key, b, first_slot;
+  uint64_t key, first_slot;
   uint32_t cnt, first_inst;
-  bool done;
+  bool done;     // descriptor final
+  bool pending;  // cw.b is the next bucket to fold
   uint64_t out;
+  ChainWalk cw;
 };
 
-__device__ __forceinline__ void desc_begin(const DevIndex &ix, uint64_t key, DescWalk &w) {
-  w.key = key;
-  w.b = home_bucket(key, ix.n_buckets);
-  w.cnt = 0;
-  w.first_inst = 0;
-  w.first_slot = 0;
-  w.done = false;
-  w.out = 0;
-}
-
-__device__ __forceinline__ void desc_load(const DevIndex &ix, const DescWalk &w, ulonglong2 kk[SLOTS / 2],
+__device__ __forceinline__ void desc_load(const DevIndex &ix, uint64_t b, ulonglong2 kk[SLOTS / 2],
                                           ulonglong2 vv[SLOTS / 2]) {
-  const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + w.b * BUCKET_WORDS);
+  const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + b * BUCKET_WORDS);
 #pragma unroll
   for (int i = 0; i < SLOTS / 2; ++i) kk[i] = p[i];
 #pragma unroll
   for (int i = 0; i < SLOTS / 2; ++i) vv[i] = p[SLOTS / 2 + i];
 }
 
-// Fold one bucket of the chain into the walk; sets done (and out) when the chain ends.
-__device__ __forceinline__ void desc_step(const DevIndex &ix, DescWalk &w, const ulonglong2 kk[SLOTS / 2],
+__device__ __forceinline__ void desc_init(DescWalk &w, uint64_t key, uint64_t h) {
+  w.key = key;
+  w.cnt = 0;
+  w.first_inst = 0;
+  w.first_slot = 0;
+  w.done = false;
+  w.pending = false;
+  w.out = 0;
+  w.cw = chain_start(h);
+}
+
+// Fold bucket w.cw.b into the walk; returns whether the bucket holds an EMPTY slot.
+__device__ __forceinline__ bool desc_fold(DescWalk &w, const ulonglong2 kk[SLOTS / 2],
                                           const ulonglong2 vv[SLOTS / 2]) {
   bool end = false;
 #pragma unroll
@@ -263,50 +269,68 @@ __device__ __forceinline__ void desc_step(const DevIndex &ix, DescWalk &w, const
       if (kind == PLAIN) {
         if (w.cnt == 0) {
           w.first_inst = val_inst(v);
-          w.first_slot = w.b * SLOTS + s;
+          w.first_slot = w.cw.b * SLOTS + s;
         }
         ++w.cnt;
       }
     }
   }
+  return end;
+}
+
+__device__ __forceinline__ void desc_close(DescWalk &w) {
   if (w.done) return;
-  if (end) {
-    w.done = true;
-    w.out = w.cnt == 0 ? make_desc(D_NONE, 0, 0)
-                       : (w.cnt == 1 ? make_desc(D_ONE, w.first_inst, w.first_slot) : make_desc(D_MANY, 0, 0));
-    return;
-  }
-  w.b = next_bucket(w.b, ix.n_buckets);
+  w.done = true;
+  w.out = w.cnt == 0 ? make_desc(D_NONE, 0, 0)
+                     : (w.cnt == 1 ? make_desc(D_ONE, w.first_inst, w.first_slot) : make_desc(D_MANY, 0, 0));
 }
 
-__device__ __forceinline__ uint64_t desc_finish(const DevIndex &ix, DescWalk &w) {
-  for (uint64_t step = 1; step < ix.n_buckets && !w.done; ++step) {
-    ulonglong2 kk[SLOTS / 2], vv[SLOTS / 2];
-    desc_load(ix, w, kk, vv);
-    desc_step(ix, w, kk, vv);
-  }
-  return w.out;
-}
-
-// Each thread describes two keys of the same iteration (i and i + TB); both first buckets
-// are requested before either is examined, so every lane keeps two lines in flight.  The
-// rare chains longer than one bucket are finished one key at a time.
+// Each thread describes two keys of the same iteration (i and i + TB).  Both home buckets
+// are requested before either is examined; a key whose home bucket is full (about a third
+// at 3/4 occupancy) then reads its mask -- both masks requested together -- and the
+// buckets it names (under a fifth of the keys) are read two at a time, one per key.
 __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
   const uint64_t n = pv.hdr->n;
   const uint64_t span = uint64_t(gridDim.x) * 2 * TB;
   for (uint64_t i = uint64_t(blockIdx.x) * 2 * TB + threadIdx.x; i < n; i += span) {
     const uint64_t j = i + TB;
     const bool has_j = j < n;
-    DescWalk a, b;
-    desc_begin(ix, pv.part_key[i], a);
-    desc_begin(ix, has_j ? pv.part_key[j] : pv.part_key[i], b);
+    const uint64_t key_a = pv.part_key[i], key_b = has_j ? pv.part_key[j] : key_a;
+    const uint64_t ha = home_bucket(key_a, ix.n_buckets), hb = home_bucket(key_b, ix.n_buckets);
     ulonglong2 ka[SLOTS / 2], va[SLOTS / 2], kb[SLOTS / 2], vb[SLOTS / 2];
-    desc_load(ix, a, ka, va);
-    desc_load(ix, b, kb, vb);
-    desc_step(ix, a, ka, va);
-    desc_step(ix, b, kb, vb);
-    pv.desc_p[i] = desc_finish(ix, a);
-    if (has_j) pv.desc_p[j] = desc_finish(ix, b);
+    desc_load(ix, ha, ka, va);
+    desc_load(ix, hb, kb, vb);
+    DescWalk a, b;
+    desc_init(a, key_a, ha);
+    desc_init(b, key_b, hb);
+    const bool ea = desc_fold(a, ka, va), eb = desc_fold(b, kb, vb);
+    const bool need_a = !a.done && !ea, need_b = !b.done && !eb;
+    if (need_a || need_b) {
+      const uint32_t ma = ix.mask[need_a ? ha : hb], mb = ix.mask[need_b ? hb : ha];
+      chain_set_mask(a.cw, ma);
+      chain_set_mask(b.cw, mb);
+    }
+    a.pending = need_a && chain_next(ix, a.cw, false);
+    b.pending = need_b && chain_next(ix, b.cw, false);
+    if (!a.pending) desc_close(a);
+    if (!b.pending) desc_close(b);
+    while (a.pending || b.pending) {
+      // both loads unconditional: a finished walk reads the other's bucket
+      desc_load(ix, a.pending ? a.cw.b : b.cw.b, ka, va);
+      desc_load(ix, b.pending ? b.cw.b : a.cw.b, kb, vb);
+      if (a.pending) {
+        const bool e = desc_fold(a, ka, va);
+        a.pending = !a.done && chain_next(ix, a.cw, e);
+        if (!a.pending) desc_close(a);
+      }
+      if (b.pending) {
+        const bool e = desc_fold(b, kb, vb);
+        b.pending = !b.done && chain_next(ix, b.cw, e);
+        if (!b.pending) desc_close(b);
+      }
+    }
+    pv.desc_p[i] = a.out;
+    if (has_j) pv.desc_p[j] = b.out;
   }
 }
 
