@@ -185,7 +185,7 @@ class Setup:
                                       state=self.probe_state)
         rec(1)
         if not self.args.direct:
-            self.index.probe_lookup(self.probe_state, nb)
+            self.index.probe_lookup(self.probe_state, self.keys, d["blk_off"], nb)
         rec(2)
         if self.args.direct:
             self.index.match(self.keys, d["blk_off"], nb, matched=self.matched)
@@ -209,7 +209,7 @@ class Setup:
         d, nb = self.dev[b], self.dev[b]["n_blocks"]
         self.index.hash_partition(d["tokens"], d["tok_off"], d["blk_off"], nb, keys=self.keys2[p],
                                   state=self.state2[p])
-        self.index.probe_lookup(self.state2[p], nb)
+        self.index.probe_lookup(self.state2[p], self.keys2[p], d["blk_off"], nb)
         self.index.match_probed(self.state2[p], self.keys2[p], d["blk_off"], nb, matched=matched)
 
     def path_overlapped(self, batches, matched2):
@@ -234,7 +234,7 @@ class Setup:
                 hashed[k] = e
             with torch.cuda.stream(self.sB):
                 self.sB.wait_event(hashed[k])
-                self.index.probe_lookup(self.state2[p], nb)
+                self.index.probe_lookup(self.state2[p], self.keys2[p], d["blk_off"], nb)
                 self.index.match_probed(self.state2[p], self.keys2[p], d["blk_off"], nb, matched=matched2[p])
                 e = torch.cuda.Event()
                 e.record(self.sB)
@@ -249,8 +249,9 @@ CALL_KERNELS = {
     # then the region partition's scan and scatter
     "hash": ["zero_kernel", "zero_kernel", "req_of_kernel", "hash16_kernel<8, true>", "part_scan_kernel",
              "part_scatter_kernel"],
-    # smetric_probe_lookup: one holder descriptor per block, in region order
-    "probe": ["probe_kernel"],
+    # smetric_probe_lookup: each request's probe bound, then one holder descriptor per block,
+    # in region order
+    "probe": ["zero32_kernel", "zero_kernel", "bound_kernel", "probe_kernel"],
     "match": ["match_kernel<1, true>"],
     "route": ["route_kernel<0>"],
     "insert": ["fill_kernel", "insp_valid_kernel", "insp_classify_kernel", "insp_size_kernel", "insp_bcount_kernel",
@@ -320,7 +321,8 @@ def workload_key(cfg: dict) -> dict:
 def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int, bench_json: str):
     """HBM traffic per timed call from two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE,
     KiB per dispatch), each scaled by what the counter reads for the 1 GiB device copy that
-    --calibrate-copy issues after the timed steps (the largest copy kernel of each run).
+    --calibrate-copy issues after the timed steps (the smallest copy kernel of at least
+    64 MiB in each run: the index snapshot and its restores are larger).
     The result is keyed to the kernel sources and to the workload named by the JSON line of
     one of the runs."""
     import csv
@@ -334,7 +336,10 @@ def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int, b
             rows.append((int(r["Dispatch_Id"]), n, v))
             if "copyBuffer" in n:
                 copies.append((int(r["Dispatch_Id"]), v))
-        return rows, max(v for _, v in copies) if copies else 0.0  # the largest copy: the calibration
+        # the calibration: the smallest copy of at least 1/16 of its size (the index
+        # snapshot and its restores are larger copies, small ones are set-up transfers)
+        big = [v for _, v in copies if v >= copy_bytes / 16]
+        return rows, min(big) if big else 0.0
 
     fr, fcopy = load(fetch_csv, "FETCH_SIZE")
     wr, wcopy = load(write_csv, "WRITE_SIZE")
@@ -368,12 +373,12 @@ def kernel_sources_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(setup, b, matched, I):
+def algorithmic_bytes(setup, b, matched, I, n_probed=None, n_search=None):
     """Bytes the method itself must move for batch b (see the design notes):
     hash: 4 B per token read + 8 B per block key written;
-    probe: 8 B key + one 64 B bucket burst per probed block (the lookup probes every block;
-    only the blocks up to and including each request's first block nobody holds are
-    necessary for the match);
+    probe: 8 B key + one 64 B bucket burst per probe the lookup makes (the blocks before
+    each request's probe bound, and its bound search; the match needs the blocks up to and
+    including each request's first block nobody holds);
     match: the same 72 B per necessary block, I/8 B of holder bitmap per distinct block of a
     widely shared prefix probed in the batch (each bitmap is charged once), 4 B per
     (request, instance) written."""
@@ -391,9 +396,11 @@ def algorithmic_bytes(setup, b, matched, I):
     H = hot_distinct * (I // 8)
     hash_b = 4 * n_tok + 8 * n_blk
     match_b = int(probes.sum()) * (8 + 64) + H + 4 * R * I
-    probe_b = n_blk * (8 + 64)
+    lookups = n_blk if n_probed is None else n_probed + n_search
+    probe_b = lookups * (8 + 64)
     scan_b = int(probes.sum()) * 8 + H + 4 * R * I  # the match from descriptors: one per necessary block
-    return dict(tokens=n_tok, blocks=n_blk, probes=int(probes.sum()), hot_probes=int(hot.sum()),
+    return dict(tokens=n_tok, blocks=n_blk, probes=int(probes.sum()), hot_probes=int(hot.sum()), lookups=lookups,
+                blocks_probed=n_blk if n_probed is None else n_probed, search_probes=n_search or 0,
                 hot_distinct=hot_distinct, H=H, descriptor=8 * n_blk, hash=hash_b, match=match_b, probe=probe_b,
                 match_scan=scan_b, route=4 * R * I + 8 * I + 12 * R + 5 * R)
 
@@ -738,8 +745,9 @@ def main():
     nb_last = setup.dev[last]["n_blocks"]
     gpu_out = (setup.keys[:nb_last].cpu().numpy(), setup.matched.cpu().numpy(), setup.target.cpu().numpy(),
                setup.branch.cpu().numpy())
+    n_probed, n_search = (None, None) if args.direct else setup.index.probe_stats(setup.probe_state, nb_last)
     checks = insert_checks(setup, last, gpu_out[0], gpu_out[1], gpu_out[2], n_after)
-    alg = algorithmic_bytes(setup, last, gpu_out[1], args.n_inst)
+    alg = algorithmic_bytes(setup, last, gpu_out[1], args.n_inst, n_probed, n_search)
     R = args.n_req
     tokens = float(np.mean([setup.host[setup.batch_of(args.warmup + k)].batch.n_tokens for k in range(args.steps)]))
     ms_step = wall * 1e3 / args.steps
@@ -773,9 +781,10 @@ def main():
             "frac": round(gbs.get(dominant, 0.0) / HBM_PEAK_GBS, 4),
             "traffic": round(tr[dominant]) if dominant in tr else None}
     if dominant == "probe" and not args.direct:
-        roof["per_launch"] = {"blocks_probed": alg["blocks"], "bytes_per_probe": 72,
+        roof["per_launch"] = {"blocks": alg["blocks"], "blocks_probed": alg["blocks_probed"],
+                              "bound_search_probes": alg["search_probes"], "bytes_per_probe": 72,
                               "necessary_probes": alg["probes"],
-                              "necessary_fraction": round(alg["probes"] / max(alg["blocks"], 1), 4),
+                              "necessary_fraction_of_blocks": round(alg["probes"] / max(alg["blocks"], 1), 4),
                               "descriptor_bytes_written": alg["descriptor"]}
     # the post-route insert: one bucket burst per pair, 16 B per new entry, 8 B per refresh
     new_pairs = n_after - setup.start_entries

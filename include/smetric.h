@@ -203,13 +203,26 @@ int smetric_probe(const smetric_index *idx, const uint64_t *keys, const int64_t 
  *                            region; it reads only the index geometry, never its contents, so it
  *                            may run while an earlier batch still inserts into the index;
  *   smetric_probe_lookup     reads the index (the descriptors then describe the index as it is
- *                            when this runs), after smetric_probe_partition on the same state.
- * smetric_probe = smetric_probe_partition followed by smetric_probe_lookup on one stream. */
+ *                            when this runs), after smetric_probe_partition on the same state,
+ *                            with the same keys, blk_off, n_req and n_blocks.
+ * smetric_probe = smetric_probe_partition followed by smetric_probe_lookup on one stream.
+ * The lookup first bounds each request's probes: the match never reads past a request's
+ * first block that no instance holds, so a search over the request's blocks (about 30
+ * probes) finds one such block and the blocks from it on are not probed.  They get the
+ * NONE descriptor, which is exact for the bound itself and never read by the match for
+ * the others; smetric_index_insert_probed takes them as new pairs and turns any that are
+ * entries (a block whose ancestors were evicted) into refreshes.  The bound is applied
+ * only while the index cannot overflow whatever those blocks are (entries + n_blocks <=
+ * capacity), so the insert's capacity check stays exact; otherwise every block is probed.
+ * smetric_probe_stats (synchronizes): blocks the last lookup on the state probed, and the
+ * probes its bound's searches made. */
 int smetric_probe_partition(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off,
                             int32_t n_req, int64_t n_blocks, void *probe, uint64_t probe_bytes,
                             hipStream_t stream);
-int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes, int64_t n_blocks,
-                         hipStream_t stream);
+int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes, const uint64_t *keys,
+                         const int64_t *blk_off, int32_t n_req, int64_t n_blocks, hipStream_t stream);
+int smetric_probe_stats(const void *probe, uint64_t probe_bytes, int64_t n_blocks, uint64_t *n_probed /* host */,
+                        uint64_t *n_search /* host */, hipStream_t stream);
 
 /* smetric_hash_partition: smetric_hash_blocks (the block keys, Sec. 3.1 and App. A)
  * followed by smetric_probe_partition on the keys it writes, in one call; for

@@ -30,6 +30,10 @@ __host__ __device__ inline uint32_t val_kind(uint64_t v) { return uint32_t(v >> 
 __host__ __device__ inline uint32_t val_epoch(uint64_t v) { return uint32_t(v >> 24) & 0x3FFFFFu; }
 __host__ __device__ inline uint64_t val_rec(uint64_t v) { return v & ((uint64_t(1) << 46) - 1); }
 __host__ __device__ inline uint64_t header_val(uint64_t rec) { return (uint64_t(HEADER) << 46) | rec; }
+// Value word of an EMPTY slot (kind 3, which no entry has): a slot whose key was just
+// claimed still shows it until its claimant writes the value, so another placer walking
+// the chain never takes it for an entry.
+constexpr uint64_t VAL_UNSET = uint64_t(3) << 46;
 // value with the kind bits cleared: the dump layout inst << 48 | epoch << 24 | session
 __host__ __device__ inline uint64_t val_plain(uint64_t v) { return v & ~(uint64_t(3) << 46); }
 
@@ -239,8 +243,10 @@ inline uint64_t flat_segment(uint64_t n) { return (n + flat_span() - 1) / flat_s
 struct ProbeHdr {
   int err;                          // first input error (EINVAL) found while partitioning
   int bad_key;                      // nonzero if a key is one of the two reserved values
-  unsigned long long n;             // number of blocks probed (0 when invalid)
+  unsigned long long n;             // number of blocks in the state (0 when invalid)
   unsigned long long tot[NREG];     // blocks per region
+  unsigned long long n_skip;        // blocks the lookup did not probe (past their request's bound)
+  unsigned long long n_search;      // probes the bound's search made
 };
 struct ProbeView {
   ProbeHdr *hdr;
@@ -250,9 +256,12 @@ struct ProbeView {
   uint64_t *base;       // [PART_WG][NREG] first region-order position of each (chunk, region)
   uint64_t *part_key;   // region order: key
   uint32_t *part_req;   // region order: request of the block
+  uint32_t *part_blk;   // region order: the block
   uint64_t *desc_p;     // region order: holder descriptor
+  uint32_t *skip;       // block order, one bit per block: past its request's probe bound
   uint64_t cap;         // blocks the buffer holds
 };
+inline uint64_t skip_words(uint64_t n) { return (n + 31) / 32; }
 inline uint64_t probe_layout(int64_t n_blocks, ProbeView *v, void *base) {
   const uint64_t n = uint64_t(n_blocks < 1 ? 1 : n_blocks);
   uint64_t off = 0;
@@ -263,7 +272,7 @@ inline uint64_t probe_layout(int64_t n_blocks, ProbeView *v, void *base) {
   };
   const uint64_t o_hdr = take(sizeof(ProbeHdr)), o_req = take(4 * n), o_inv = take(4 * n),
                  o_hist = take(4ull * NREG * PART_WG), o_base = take(8ull * NREG * PART_WG), o_k = take(8 * n),
-                 o_rq = take(4 * n), o_dp = take(8 * n);
+                 o_rq = take(4 * n), o_bk = take(4 * n), o_dp = take(8 * n), o_sk = take(4 * skip_words(n));
   if (v) {
     char *b = static_cast<char *>(base);
     v->hdr = reinterpret_cast<ProbeHdr *>(b + o_hdr);
@@ -273,7 +282,9 @@ inline uint64_t probe_layout(int64_t n_blocks, ProbeView *v, void *base) {
     v->base = reinterpret_cast<uint64_t *>(b + o_base);
     v->part_key = reinterpret_cast<uint64_t *>(b + o_k);
     v->part_req = reinterpret_cast<uint32_t *>(b + o_rq);
+    v->part_blk = reinterpret_cast<uint32_t *>(b + o_bk);
     v->desc_p = reinterpret_cast<uint64_t *>(b + o_dp);
+    v->skip = reinterpret_cast<uint32_t *>(b + o_sk);
     v->cap = n;
   }
   return off;

@@ -55,6 +55,15 @@ __global__ void fill_kernel(uint64_t *p, uint64_t n_words, uint64_t value) {
 
 __global__ void set_int_kernel(int *p, int v) { *p = v; }
 
+__global__ void unset_values_kernel(uint64_t *slots, uint64_t n_buckets) {
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t b = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; b < n_buckets; b += stride) {
+    ulonglong2 *v = reinterpret_cast<ulonglong2 *>(slots + b * BUCKET_WORDS + SLOTS);
+#pragma unroll
+    for (int i = 0; i < SLOTS / 2; ++i) v[i] = make_ulonglong2(VAL_UNSET, VAL_UNSET);
+  }
+}
+
 int fill(void *p, uint64_t bytes, uint64_t value, hipStream_t s) {
   const uint64_t n = bytes / 8;
   if (n == 0) return SMETRIC_OK;
@@ -182,26 +191,35 @@ __device__ __forceinline__ uint64_t *val_ptr(const DevIndex &ix, int64_t slot) {
 // ahead of any free slot: that key is about to get a bitmap record, and its remaining
 // new holders are entered after the conversion instead of piling up plain slots that
 // would all turn into tombstones.
+// With want_inst, a PLAIN slot of (key, want_inst) met on the way ends the walk instead
+// (existing): the pair is already an entry.
 struct Claim {
-  int64_t slot;    // claimed slot, or -1
-  int64_t header;  // HEADER slot of key when found, else -1
+  int64_t slot;      // claimed slot, or -1
+  int64_t header;    // HEADER slot of key when found, else -1
+  int64_t existing;  // PLAIN slot of (key, want_inst) when found, else -1
   uint32_t same;
   bool capped;
 };
+constexpr uint32_t NO_INST = 0xFFFFFFFFu;
 __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool want_header,
-                            uint32_t max_same = 0xFFFFFFFFu) {
-  Claim c{-1, -1, 0, false};
+                            uint32_t max_same = 0xFFFFFFFFu, uint32_t want_inst = NO_INST) {
+  Claim c{-1, -1, -1, 0, false};
   const uint64_t h = b;  // the chain start whose displacement mask records the claim
   for (uint64_t step = 0; step < ix.n_buckets; ++step, b = next_bucket(b, ix.n_buckets)) {
     uint64_t *bk = ix.slots + b * BUCKET_WORDS;
     const BucketScan sc = scan_bucket(bk, key);
-    if (want_header) {
+    if (want_header || want_inst != NO_INST) {
       uint32_t mm = sc.match;
       while (mm) {
         const int s = __builtin_ctz(mm);
         mm &= mm - 1;
-        if (val_kind(bk[SLOTS + s]) == HEADER) {
+        const uint64_t v = bk[SLOTS + s];
+        if (want_header && val_kind(v) == HEADER) {
           c.header = int64_t(b * SLOTS + s);
+          return c;
+        }
+        if (val_kind(v) == PLAIN && val_inst(v) == want_inst) {
+          c.existing = int64_t(b * SLOTS + s);
           return c;
         }
       }
@@ -228,7 +246,7 @@ __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool w
         mask_note(ix, h, b);
         return c;
       }
-      if (k == key) {
+      if (k == key) {  // claimed meanwhile by another pair of the same key (never this pair)
         if (want_header && val_kind(__hip_atomic_load(&bk[SLOTS + s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == HEADER) {
           c.header = int64_t(b * SLOTS + s);  // cannot happen: headers predate this kernel
           return c;
@@ -240,19 +258,38 @@ __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool w
   return c;
 }
 
-// Enter a distinct new entry.  Returns PLACED, DEFERRED (capped: enter it again after the
-// key's conversion, uncapped) or FAILED (no free slot).  trigger is set when the slot is
-// the key's (T+1)-th plain slot, the last one a key gets before its conversion.
-enum Placed { PLACED = 0, DEFERRED = 1, FAILED = 2 };
+// epoch = max(old, epoch) of the entry at `slot`, session kept (an existing pair).
+__device__ __forceinline__ void refresh_at(const DevIndex &ix, int64_t slot, uint32_t epoch) {
+  uint64_t *vp = val_ptr(ix, slot);
+  const uint64_t v = *vp;
+  if (val_epoch(v) < epoch) *vp = (v & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+}
+
+// Enter a pair that is not known to be an entry (one per pair and call: pairs are
+// distinct).  Returns PLACED, REFRESHED (it was an entry: its epoch is raised instead),
+// DEFERRED (capped: enter it again after the key's conversion, uncapped) or FAILED (no
+// free slot).  trigger is set when the slot is the key's (T+1)-th plain slot, the last
+// one a key gets before its conversion.
+enum Placed { PLACED = 0, DEFERRED = 1, FAILED = 2, REFRESHED = 3 };
 __device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32_t epoch, uint32_t sess,
                          bool &trigger, bool capped) {
   trigger = false;
   const Claim c = claim_slot(ix, home_bucket(key, ix.n_buckets), key, true,
-                             capped ? uint32_t(ix.threshold) + 1 : 0xFFFFFFFFu);
+                             capped ? uint32_t(ix.threshold) + 1 : 0xFFFFFFFFu, inst);
+  if (c.existing >= 0) {
+    refresh_at(ix, c.existing, epoch);
+    return REFRESHED;
+  }
   if (c.header >= 0) {
     const uint64_t rec = val_rec(*val_ptr(ix, c.header));
-    atomicOr(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
-             1ull << (inst & 63));
+    const unsigned long long old = atomicOr(
+        reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]), 1ull << (inst & 63));
+    if ((old >> (inst & 63)) & 1) {  // already a member
+      const Found f = find_member(ix, key, inst);
+      if (f.slot < 0) return FAILED;
+      refresh_at(ix, f.slot, epoch);
+      return REFRESHED;
+    }
     const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, false);
     if (m.slot < 0) return FAILED;
     *val_ptr(ix, m.slot) = make_val(inst, MEMBER, epoch, sess);
@@ -263,6 +300,14 @@ __device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32
   *val_ptr(ix, c.slot) = make_val(inst, PLAIN, epoch, sess);
   trigger = c.same == uint32_t(ix.threshold);
   return PLACED;
+}
+
+// A REFRESHED pair was counted as new by the capacity check: take it back, one atomic
+// per wavefront.
+__device__ __forceinline__ void uncount_refreshed(const DevIndex &ix, bool refreshed) {
+  const uint64_t m = __ballot(refreshed);
+  if (m && (threadIdx.x & 63) == uint32_t(__builtin_ctzll(m)))
+    atomicAdd(&ix.hdr->n_entries, 0ull - (unsigned long long)__popcll(m));
 }
 
 // Replace the plain slots of `key` by a bitmap record (one thread per key).
@@ -614,14 +659,17 @@ __global__ void ins_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
   for (uint64_t i0 = first; i0 < n; i0 += stride) {  // whole wavefronts iterate together
     const uint64_t i = i0 + (threadIdx.x & 63);
     int64_t tk = -1, df = -1;
+    bool rf = false;
     if (i < n) {
       const DSlot d = ws.dd[ws.list[i]];
       bool trig;
       const int pl = place_new(ix, d.key, dd_inst(d.w2), epoch, session[dd_req(d.w2)], trig, true);
       if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
       else if (pl == DEFERRED) df = int64_t(i);
+      else if (pl == REFRESHED) rf = true;
       else if (trig) tk = int64_t(i);
     }
+    uncount_refreshed(ix, rf);
     append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by list index
     append_wave(&ws.hdr->n_def, ws.def, ws.list_cap, df);
   }
@@ -1226,6 +1274,7 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
   for (uint64_t p0 = uint64_t(blockIdx.x) * TB; p0 < n; p0 += span) {  // whole workgroups iterate together
     const uint64_t p = p0 + threadIdx.x;
     int64_t tk = -1, df = -1;
+    bool rf = false;
     if (p < n) {
       const NewPair e = ws.np[p];
       if (e.key != KEY_EMPTY) {
@@ -1234,9 +1283,11 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
         const int pl = place_new(ix, e.key, dd_inst(w2), epoch, session[dd_req(w2)], trig, true);
         if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
         else if (pl == DEFERRED) df = int64_t(p);
+        else if (pl == REFRESHED) rf = true;  // a block past its probe bound that was an entry
         else if (trig) tk = int64_t(p);
       }
     }
+    uncount_refreshed(ix, rf);
     append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by np position
     append_wave(&ws.hdr->n_def, ws.def, ws.list_cap, df);
   }
@@ -1470,7 +1521,7 @@ __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const ui
       if (((want >> j) & 1) && sel_cmp(k[j], v[j], cut) > 0) {
         bool t;
         const int pl = place_new(ix, k[j], val_inst(v[j]), val_epoch(v[j]), uint32_t(v[j] & 0xFFFFFF), t, true);
-        if (pl == FAILED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+        if (pl == FAILED || pl == REFRESHED) set_status(ix.hdr, SMETRIC_EINTERNAL);  // survivors are distinct
         else if (pl == DEFERRED) dmask |= 1u << j;
         else if (t) tmask |= 1u << j;
       }
@@ -1502,7 +1553,7 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
   const uint64_t b_lo = uint64_t(blockIdx.x) * RT;
   const uint64_t seg = toff[blockIdx.x] >> 16;
   const uint32_t cnt = uint32_t(toff[blockIdx.x] & 0xFFFF);  // <= RT * SLOTS
-  for (int i = t; i < RT * BUCKET_WORDS; i += TB) tb[i] = 0;  // KEY_EMPTY
+  for (int i = t; i < RT * BUCKET_WORDS; i += TB) tb[i] = (i % BUCKET_WORDS) < SLOTS ? KEY_EMPTY : VAL_UNSET;
   for (uint32_t i = t; i < cnt; i += TB) {
     const uint64_t ps = pos[seg + i];
     sp[i] = uint16_t(((ps & ((uint64_t(1) << 62) - 1)) - b_lo * SLOTS) | ((ps >> 63) << 15));
@@ -1589,7 +1640,9 @@ __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsign
       const uint64_t v = vals[t];
       pl = place_new(ix, keys[t], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), trig, false);
     }
-    if (pl != PLACED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+    if (pl == REFRESHED && !np && !via) pl = FAILED;  // rebuild survivors are distinct
+    if (pl != PLACED && pl != REFRESHED) set_status(ix.hdr, SMETRIC_EINTERNAL);
+    uncount_refreshed(ix, pl == REFRESHED);
   }
 }
 
@@ -1757,7 +1810,10 @@ extern "C" int smetric_index_init(smetric_index *idx, void *mem, uint64_t mem_by
   if (rc) return rc;
   Layout L;
   layout_for(capacity, n_instances, n_slots, L);
-  return fill(mem, L.bytes, 0, stream);
+  if (int rc2 = fill(mem, L.bytes, 0, stream)) return rc2;
+  // every slot EMPTY with an unset value
+  hipLaunchKernelGGL(unset_values_kernel, dim3(grid_for(L.n_buckets)), dim3(TB), 0, stream, idx->slots, L.n_buckets);
+  return hip_rc(hipGetLastError());
 }
 
 extern "C" int smetric_index_stats(const smetric_index *idx, uint64_t *n_entries, int32_t *status,

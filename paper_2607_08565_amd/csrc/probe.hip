@@ -207,6 +207,7 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
         const uint64_t pos = run[gg] + (p - tstart[gg]);
         pv.part_key[pos] = skey[p];
         pv.part_req[pos] = sreq[p];
+        pv.part_blk[pos] = sblk[p];
         pv.inv[sblk[p]] = uint32_t(pos);
       }
     }
@@ -216,6 +217,92 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
       cnt[t] = 0;
     }
     __syncthreads();
+  }
+}
+
+// Probe bound.  The match reads a request's blocks only up to its first block that no
+// instance holds (c[r][i] = the first block instance i misses, Sec. 4.1), so any block
+// that no instance holds bounds the blocks worth probing.  Each request searches for one:
+// BL lanes test BL evenly spaced blocks of the open interval (lo, hi) -- lo held by some
+// instance (or -1), hi held by none (or the block count) -- and the interval shrinks to
+// the first tested block held by none and the tested block before it.  It ends with hi
+// held by none (or every tested block held, hi = the block count: nothing is skipped), so
+// the first all-miss block lies at or before hi; with whole prompts cached, holding is
+// monotone along a prompt and hi is exactly that block.  Blocks from hi on get their bit
+// in the skip bitmap: the probe gives them the NONE descriptor without reading the table
+// -- right for hi, never read by the match for later ones -- and the insert takes them as
+// candidates, its placement turning any that exist (an entry whose ancestors were
+// evicted) into a refresh.  Only when the insert cannot overflow the index whatever those
+// blocks turn out to be (entries + blocks <= capacity), so that its all-or-nothing
+// capacity check stays exact.
+constexpr int BL = 8;  // lanes per request
+
+// Is `key` in the table at all (any slot of its home chain)?
+__device__ bool key_present(const DevIndex &ix, uint64_t key) {
+  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets));
+  bool had_empty;
+  do {
+    const BucketScan sc = scan_bucket(ix.slots + w.b * BUCKET_WORDS, key);
+    if (sc.match) return true;
+    had_empty = sc.empty != 0;
+  } while (chain_next(ix, w, had_empty));
+  return false;
+}
+
+__global__ void zero32_kernel(uint32_t *p, uint64_t n_words) {
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_words; i += stride) p[i] = 0;
+}
+
+__global__ __launch_bounds__(TB) void bound_kernel(DevIndex ix, ProbeView pv, const uint64_t *__restrict__ keys,
+                                                   const int64_t *__restrict__ blk_off, int32_t n_req,
+                                                   uint64_t n_blocks) {
+  if (pv.hdr->err || pv.hdr->n != n_blocks || ix.hdr->n_entries + n_blocks > ix.capacity) return;
+  const int lane = threadIdx.x & (BL - 1), gbase = (threadIdx.x & 63) & ~(BL - 1);
+  const int64_t r = (int64_t(blockIdx.x) * TB + threadIdx.x) / BL;
+  // a request whose range is not inside [0, n_blocks] is not bounded (its blocks are all probed)
+  int64_t b0 = 0, nb = 0;
+  if (r < n_req) {
+    b0 = blk_off[r];
+    const int64_t b1 = blk_off[r + 1];
+    if (b0 < 0 || b1 < b0 || uint64_t(b1) > n_blocks) b0 = 0;
+    else nb = b1 - b0;
+  }
+  int64_t lo = -1, hi = nb;
+  uint32_t probes = 0;
+  while (__ballot(hi - lo > 1) != 0) {  // whole wavefronts iterate together
+    const int64_t gap = hi - lo - 1, cnt = gap < BL ? gap : BL;
+    const bool mine = lane < cnt;
+    const int64_t p = mine ? lo + (int64_t(lane) + 1) * (gap + 1) / (cnt + 1) : lo;
+    const bool held = mine ? key_present(ix, keys[b0 + p]) : true;
+    probes += mine;
+    const uint32_t miss = uint32_t(__ballot(mine && !held) >> gbase) & ((1u << BL) - 1u);
+    if (gap > 0) {
+      if (miss) {
+        const int t = __builtin_ctz(miss);
+        hi = lo + (int64_t(t) + 1) * (gap + 1) / (cnt + 1);
+        lo = t > 0 ? lo + int64_t(t) * (gap + 1) / (cnt + 1) : lo;
+      } else {
+        lo = lo + cnt * (gap + 1) / (cnt + 1);
+      }
+    }
+  }
+  // bits [b0 + hi, b0 + nb) of the (cleared) skip bitmap; edge words are shared with the
+  // neighbouring requests
+  const uint64_t s0 = uint64_t(b0 + hi), s1 = uint64_t(b0 + nb);
+  if (s0 < s1)
+    for (uint64_t w = s0 / 32 + lane; w <= (s1 - 1) / 32; w += BL) {
+      const uint64_t lo_b = w * 32 > s0 ? w * 32 : s0, hi_b = (w + 1) * 32 < s1 ? (w + 1) * 32 : s1;
+      const uint32_t bits = uint32_t(((uint64_t(1) << (hi_b - lo_b)) - 1) << (lo_b - w * 32));
+      atomicOr(pv.skip + w, bits);
+    }
+  // counts for smetric_probe_stats: one atomic per request
+  const unsigned long long skip = s0 < s1 ? s1 - s0 : 0;
+#pragma unroll
+  for (int d = 1; d < BL; d <<= 1) probes += __shfl_xor(probes, d, 64);
+  if (lane == 0 && r < n_req) {
+    if (s0 < s1) atomicAdd(&pv.hdr->n_skip, skip);
+    if (probes) atomicAdd(&pv.hdr->n_search, (unsigned long long)probes);
   }
 }
 
@@ -285,8 +372,9 @@ __device__ __forceinline__ void desc_close(DescWalk &w) {
                      : (w.cnt == 1 ? make_desc(D_ONE, w.first_inst, w.first_slot) : make_desc(D_MANY, 0, 0));
 }
 
-// Each thread describes two keys of the same iteration (i and i + TB).  Both home buckets
-// are requested before either is examined; a key whose home bucket is full (about a third
+// Each thread describes two keys of the same iteration (i and i + TB); a block past its
+// request's probe bound gets NONE without a read.  Both home buckets are requested
+// before either is examined; a key whose home bucket is full (about a third
 // at 3/4 occupancy) then reads its mask -- both masks requested together -- and the
 // buckets it names (under a fifth of the keys) are read two at a time, one per key.
 __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
@@ -296,14 +384,22 @@ __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
     const uint64_t j = i + TB;
     const bool has_j = j < n;
     const uint64_t key_a = pv.part_key[i], key_b = has_j ? pv.part_key[j] : key_a;
+    const uint32_t blk_a = pv.part_blk[i], blk_b = has_j ? pv.part_blk[j] : blk_a;
+    const bool skip_a = (pv.skip[blk_a >> 5] >> (blk_a & 31)) & 1u;
+    const bool skip_b = !has_j || ((pv.skip[blk_b >> 5] >> (blk_b & 31)) & 1u);
     const uint64_t ha = home_bucket(key_a, ix.n_buckets), hb = home_bucket(key_b, ix.n_buckets);
     ulonglong2 ka[SLOTS / 2], va[SLOTS / 2], kb[SLOTS / 2], vb[SLOTS / 2];
-    desc_load(ix, ha, ka, va);
-    desc_load(ix, hb, kb, vb);
     DescWalk a, b;
     desc_init(a, key_a, ha);
     desc_init(b, key_b, hb);
-    const bool ea = desc_fold(a, ka, va), eb = desc_fold(b, kb, vb);
+    bool ea = true, eb = true;  // a skipped block: no entries, as far as the walk goes
+    if (!(skip_a && skip_b)) {
+      // both loads unconditional: a skipped block reads the other's home bucket
+      desc_load(ix, skip_a ? hb : ha, ka, va);
+      desc_load(ix, skip_b ? ha : hb, kb, vb);
+      if (!skip_a) ea = desc_fold(a, ka, va);
+      if (!skip_b) eb = desc_fold(b, kb, vb);
+    }
     const bool need_a = !a.done && !ea, need_b = !b.done && !eb;
     if (need_a || need_b) {
       const uint32_t ma = ix.mask[need_a ? ha : hb], mb = ix.mask[need_b ? hb : ha];
@@ -393,19 +489,45 @@ extern "C" int smetric_probe_partition(const smetric_index *idx, const uint64_t 
   return partition_tail(ix, pv, keys, uint64_t(n_blocks), false, stream);
 }
 
-extern "C" int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes, int64_t n_blocks,
+extern "C" int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes,
+                                    const uint64_t *keys, const int64_t *blk_off, int32_t n_req, int64_t n_blocks,
                                     hipStream_t stream) {
-  if (!idx || !idx->slots || n_blocks < 0 || n_blocks >= (int64_t(1) << 32)) return SMETRIC_EINVAL;
+  if (!idx || !idx->slots || n_req < 0 || n_blocks < 0 || n_blocks >= (int64_t(1) << 32)) return SMETRIC_EINVAL;
+  if (!blk_off || (n_blocks > 0 && !keys)) return SMETRIC_EINVAL;
   if (!probe || (reinterpret_cast<uintptr_t>(probe) & 255) || probe_bytes < probe_layout(n_blocks, nullptr, nullptr))
     return SMETRIC_EWORKSPACE;
   ProbeView pv;
   probe_layout(n_blocks, &pv, probe);
-  hipLaunchKernelGGL(probe_kernel, dim3(FLAT_WG), dim3(TB), 0, stream, dev_view(idx), pv);
+  const DevIndex ix = dev_view(idx);
+  const uint64_t nw = skip_words(uint64_t(n_blocks < 1 ? 1 : n_blocks));
+  hipLaunchKernelGGL(zero32_kernel, dim3(nw / TB + 1 < 256 ? nw / TB + 1 : 256), dim3(TB), 0, stream, pv.skip, nw);
+  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(64), 0, stream, reinterpret_cast<uint64_t *>(&pv.hdr->n_skip),
+                     uint64_t(2));
+  if (n_req > 0 && n_blocks > 0)
+    hipLaunchKernelGGL(bound_kernel, dim3((uint64_t(n_req) * BL + TB - 1) / TB), dim3(TB), 0, stream, ix, pv, keys,
+                       blk_off, n_req, uint64_t(n_blocks));
+  hipLaunchKernelGGL(probe_kernel, dim3(FLAT_WG), dim3(TB), 0, stream, ix, pv);
   return hip_rc(hipGetLastError());
+}
+
+extern "C" int smetric_probe_stats(const void *probe, uint64_t probe_bytes, int64_t n_blocks, uint64_t *n_probed,
+                                   uint64_t *n_search, hipStream_t stream) {
+  if (n_blocks < 0 || n_blocks >= (int64_t(1) << 32) || !n_probed || !n_search) return SMETRIC_EINVAL;
+  if (!probe || (reinterpret_cast<uintptr_t>(probe) & 255) || probe_bytes < probe_layout(n_blocks, nullptr, nullptr))
+    return SMETRIC_EWORKSPACE;
+  ProbeView pv;
+  probe_layout(n_blocks, &pv, const_cast<void *>(probe));
+  ProbeHdr h;
+  if (hipMemcpyAsync(&h, pv.hdr, sizeof(h), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return SMETRIC_EHIP;
+  *n_probed = h.n >= h.n_skip ? h.n - h.n_skip : 0;
+  *n_search = h.n_search;
+  return SMETRIC_OK;
 }
 
 extern "C" int smetric_probe(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
                              int64_t n_blocks, void *probe, uint64_t probe_bytes, hipStream_t stream) {
   if (int rc = smetric_probe_partition(idx, keys, blk_off, n_req, n_blocks, probe, probe_bytes, stream)) return rc;
-  return smetric_probe_lookup(idx, probe, probe_bytes, n_blocks, stream);
+  return smetric_probe_lookup(idx, probe, probe_bytes, keys, blk_off, n_req, n_blocks, stream);
 }

@@ -81,7 +81,8 @@ def _load() -> C.CDLL:
         "smetric_probe_ws_bytes": [I64, P],
         "smetric_probe": [PIX, P, P, I32, I64, P, U64, P],
         "smetric_probe_partition": [PIX, P, P, I32, I64, P, U64, P],
-        "smetric_probe_lookup": [PIX, P, U64, I64, P],
+        "smetric_probe_lookup": [PIX, P, U64, P, P, I32, I64, P],
+        "smetric_probe_stats": [P, U64, I64, P, P, P],
         "smetric_hash_partition": [P, I64, P, P, I32, I64, I32, U64, P, P, PIX, P, U64, P],
         "smetric_match_probed": [PIX, P, U64, P, P, I32, I64, P, P],
         "smetric_index_insert_probed": [PIX, P, U64, I32, I64, P, P, U32, P, U64, P],
@@ -104,6 +105,7 @@ EXPORTED = (
     "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
     "smetric_probe_partition", "smetric_probe_lookup", "smetric_hash_partition", "smetric_route_seq_coloc",
     "smetric_route_seq_coloc_ws_bytes", "smetric_route_seq_noalloc", "smetric_route_seq_noalloc_max_req",
+    "smetric_probe_stats",
 )
 
 
@@ -479,11 +481,21 @@ class Index:
             self.ref, C.c_void_p(state.data_ptr()), state.numel(), _stream()))
         return keys, state
 
-    def probe_lookup(self, state: torch.Tensor, n_blocks: int):
-        """Second half of probe(): reads the index."""
+    def probe_lookup(self, state: torch.Tensor, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int):
+        """Second half of probe(): reads the index (the keys and offsets of the partition)."""
+        R = blk_off.numel() - 1
         _check("smetric_probe_lookup", _lib.smetric_probe_lookup(
-            self.ref, C.c_void_p(state.data_ptr()), state.numel(), n_blocks, _stream()))
+            self.ref, C.c_void_p(state.data_ptr()), state.numel(), _dev(keys, torch.uint64, "keys"),
+            _dev(blk_off, torch.int64, "blk_off"), R, n_blocks, _stream()))
         return state
+
+    @staticmethod
+    def probe_stats(state: torch.Tensor, n_blocks: int):
+        """(blocks the last lookup on `state` probed, probes of its bound's searches); synchronizes."""
+        a, b = C.c_uint64(), C.c_uint64()
+        _check("smetric_probe_stats", _lib.smetric_probe_stats(C.c_void_p(state.data_ptr()), state.numel(), n_blocks,
+                                                               C.byref(a), C.byref(b), _stream()))
+        return int(a.value), int(b.value)
 
     def match_probed(self, state: torch.Tensor, keys: torch.Tensor, blk_off: torch.Tensor, n_blocks: int,
                      matched: torch.Tensor | None = None) -> torch.Tensor:

@@ -159,7 +159,7 @@ def check_probed_insert_full(gix, batch: W.Batch, blk_off_h, nb: int, keys, stat
     assert n1 - n0 == expect, f"insert added {n1 - n0} entries, expected {expect} distinct new pairs"
     d_boff = to_dev(blk_off_h)
     keys2, state2 = gix.hash_partition(to_dev(batch.tokens), to_dev(batch.tok_off), d_boff, nb)
-    gix.probe_lookup(state2, nb)
+    gix.probe_lookup(state2, keys2, d_boff, nb)
     m2 = gix.match_probed(state2, keys2, d_boff, nb).cpu().numpy()
     whole = m2[np.arange(R), np.asarray(target_h, np.int64)] == np.diff(blk_off_h)
     assert whole.all(), f"{int((~whole).sum())} requests do not see their whole prompt on their target"

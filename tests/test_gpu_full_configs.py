@@ -61,7 +61,7 @@ def _open_loop_last_batch(wl, capacity, n_sample, seed):
     blk_off, nb = S.block_offsets(b.tok_off)
     d_boff = to_dev(blk_off)
     keys, state = gix.hash_partition(to_dev(b.tokens), to_dev(b.tok_off), d_boff, nb)
-    gix.probe_lookup(state, nb)
+    gix.probe_lookup(state, keys, d_boff, nb)
     gm = gix.match_probed(state, keys, d_boff, nb)
     gt, gb = S.route(gm, to_dev(b.prompt_len), to_dev(b.hist_len), to_dev(b.turn), to_dev(b.q), W.DEFAULT_PARAMS,
                      b.rr_base)

@@ -131,7 +131,7 @@ def test_partition_overlaps_previous_insert():
         _, okeys = oracle.hash_blocks(b.tokens, b.tok_off, W.BLOCK, W.DEFAULT_SEED)
         with torch.cuda.stream(sB):
             sB.wait_event(front)
-            pair.gix.probe_lookup(states[p], nb)
+            pair.gix.probe_lookup(states[p], keys[p], d_boff, nb)
             gm = pair.gix.match_probed(states[p], keys[p], d_boff, nb)
             gt, gb = S.route(gm, to_dev(b.prompt_len), to_dev(b.hist_len), to_dev(b.turn), to_dev(b.q),
                              W.DEFAULT_PARAMS, b.rr_base)
@@ -369,7 +369,7 @@ def test_hash_partition_equals_the_separate_calls(B):
                                           status=status)
     assert int(status.item()) == 0
     assert np.array_equal(keys[:nb].cpu().numpy(), okeys), "keys"
-    pair.gix.probe_lookup(state, nb)
+    pair.gix.probe_lookup(state, keys, d_boff, nb)
     gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
     om = pair.oix.match(okeys, blk_off)
     assert np.array_equal(gm, om), "matched rows"
@@ -394,7 +394,7 @@ def test_hash_partition_bad_token_range_invalidates_the_state():
     d_boff = to_dev(blk_off)
     keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(tok_off), d_boff, 40, status=status)
     assert int(status.item()) == S.EINVAL
-    pair.gix.probe_lookup(state, 40)
+    pair.gix.probe_lookup(state, keys, d_boff, 40)
     m = pair.gix.match_probed(state, keys, d_boff, 40).cpu().numpy()
     assert not m.any()
     _, st = pair.gix.stats(reset_status=True)
@@ -418,7 +418,7 @@ def test_hash_partition_with_no_full_block():
     d_boff = to_dev(blk_off)
     keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(tok_off), d_boff, 0, status=status)
     assert int(status.item()) == 0
-    pair.gix.probe_lookup(state, 0)
+    pair.gix.probe_lookup(state, keys, d_boff, 0)
     m = pair.gix.match_probed(state, keys, d_boff, 0).cpu().numpy()
     assert m.shape == (len(lens), 6) and not m.any()
     R = len(lens)
@@ -564,7 +564,7 @@ def test_reserved_marker_keys(B):
     assert np.array_equal(keys[:nb].cpu().numpy(), okeys), "fused hash + partition keys"
     # enter every prompt on its own instance through the probed path, then route the same
     # prompts again: each sees its whole block sequence on that instance
-    pair.gix.probe_lookup(state, nb)
+    pair.gix.probe_lookup(state, keys, d_boff, nb)
     gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
     om = pair.oix.match(okeys, blk_off)
     assert np.array_equal(gm, om) and not gm.any()

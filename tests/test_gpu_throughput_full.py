@@ -75,7 +75,7 @@ def test_throughput_config_full_size():
     # the batch, as bench.py runs it
     d_boff = to_dev(blk0)
     keys, state = gix.hash_partition(to_dev(b0.tokens), to_dev(b0.tok_off), d_boff, nb0)
-    gix.probe_lookup(state, nb0)
+    gix.probe_lookup(state, keys, d_boff, nb0)
     gm = gix.match_probed(state, keys, d_boff, nb0).cpu().numpy()
     gt, gb = S.route(to_dev(gm), to_dev(b0.prompt_len), to_dev(b0.hist_len), to_dev(b0.turn), to_dev(b0.q),
                      W.DEFAULT_PARAMS, b0.rr_base)
