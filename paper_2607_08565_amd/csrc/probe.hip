@@ -306,9 +306,10 @@ __global__ __launch_bounds__(TB) void bound_kernel(DevIndex ix, ProbeView pv, co
   }
 }
 
-// Holder descriptor of a key, built one 128-byte bucket (keys and values at once) per
-// bucket of the key's chain: its home bucket, and only when that is full the buckets its
-// displacement mask names.
+// Holder descriptor of a key, built bucket by bucket over the key's chain -- its home
+// bucket, and only when that is full the buckets its displacement mask names.  A bucket's
+// keys (its first 64 bytes) are read first; the value of a slot that holds the key is then
+// read from the same line (an L2 hit), so a walk keeps only the keys in registers.
 struct DescWalk {
   uint64_t key, first_slot;
   uint32_t cnt, first_inst;
@@ -318,13 +319,10 @@ struct DescWalk {
   ChainWalk cw;
 };
 
-__device__ __forceinline__ void desc_load(const DevIndex &ix, uint64_t b, ulonglong2 kk[SLOTS / 2],
-                                          ulonglong2 vv[SLOTS / 2]) {
+__device__ __forceinline__ void keys_load(const DevIndex &ix, uint64_t b, ulonglong2 kk[SLOTS / 2]) {
   const ulonglong2 *p = reinterpret_cast<const ulonglong2 *>(ix.slots + b * BUCKET_WORDS);
 #pragma unroll
   for (int i = 0; i < SLOTS / 2; ++i) kk[i] = p[i];
-#pragma unroll
-  for (int i = 0; i < SLOTS / 2; ++i) vv[i] = p[SLOTS / 2 + i];
 }
 
 __device__ __forceinline__ void desc_init(DescWalk &w, uint64_t key, uint64_t h) {
@@ -338,31 +336,50 @@ __device__ __forceinline__ void desc_init(DescWalk &w, uint64_t key, uint64_t h)
   w.cw = chain_start(h);
 }
 
-// Fold bucket w.cw.b into the walk; returns whether the bucket holds an EMPTY slot.
-__device__ __forceinline__ bool desc_fold(DescWalk &w, const ulonglong2 kk[SLOTS / 2],
-                                          const ulonglong2 vv[SLOTS / 2]) {
-  bool end = false;
+// Slots of bucket keys kk holding `key` (before the first EMPTY slot) and whether an EMPTY
+// slot is there.
+struct KeyScan {
+  uint32_t match;
+  bool empty;
+};
+__device__ __forceinline__ KeyScan scan_keys(const ulonglong2 kk[SLOTS / 2], uint64_t key) {
+  uint32_t m = 0, e = 0;
 #pragma unroll
-  for (int s = 0; s < SLOTS; ++s) {
-    const uint64_t k = (s & 1) ? kk[s / 2].y : kk[s / 2].x;
-    const uint64_t v = (s & 1) ? vv[s / 2].y : vv[s / 2].x;
-    end |= k == KEY_EMPTY;
-    if (!end && k == w.key) {
-      const uint32_t kind = val_kind(v);
-      if (kind == HEADER && !w.done) {
-        w.out = make_desc(D_HOT, 0, val_rec(v));
-        w.done = true;
+  for (int i = 0; i < SLOTS / 2; ++i) {
+    m |= (uint32_t(kk[i].x == key) << (2 * i)) | (uint32_t(kk[i].y == key) << (2 * i + 1));
+    e |= (uint32_t(kk[i].x == KEY_EMPTY) << (2 * i)) | (uint32_t(kk[i].y == KEY_EMPTY) << (2 * i + 1));
+  }
+  if (e) m &= (e & (0u - e)) - 1u;
+  return KeyScan{m, e != 0};
+}
+
+// The value word the fold of bucket b needs first: the first slot holding the key (slot 0
+// when none does: a read of the same line, then unused).
+__device__ __forceinline__ uint64_t first_val(const DevIndex &ix, uint64_t b, uint32_t match) {
+  return ix.slots[b * BUCKET_WORDS + SLOTS + (match ? __builtin_ctz(match) : 0)];
+}
+
+// Fold bucket w.cw.b (its key matches and the first matching value) into the walk.
+__device__ __forceinline__ void desc_fold(const DevIndex &ix, DescWalk &w, uint32_t match, uint64_t v0) {
+  const uint64_t b = w.cw.b;
+  bool first = true;
+  while (match && !w.done) {
+    const int s = __builtin_ctz(match);
+    match &= match - 1;
+    const uint64_t v = first ? v0 : ix.slots[b * BUCKET_WORDS + SLOTS + s];  // two or more: rare
+    first = false;
+    const uint32_t kind = val_kind(v);
+    if (kind == HEADER) {
+      w.out = make_desc(D_HOT, 0, val_rec(v));
+      w.done = true;
+    } else if (kind == PLAIN) {
+      if (w.cnt == 0) {
+        w.first_inst = val_inst(v);
+        w.first_slot = b * SLOTS + s;
       }
-      if (kind == PLAIN) {
-        if (w.cnt == 0) {
-          w.first_inst = val_inst(v);
-          w.first_slot = w.cw.b * SLOTS + s;
-        }
-        ++w.cnt;
-      }
+      ++w.cnt;
     }
   }
-  return end;
 }
 
 __device__ __forceinline__ void desc_close(DescWalk &w) {
@@ -373,10 +390,11 @@ __device__ __forceinline__ void desc_close(DescWalk &w) {
 }
 
 // Each thread describes two keys of the same iteration (i and i + TB); a block past its
-// request's probe bound gets NONE without a read.  Both home buckets are requested
-// before either is examined; a key whose home bucket is full (about a third
-// at 3/4 occupancy) then reads its mask -- both masks requested together -- and the
-// buckets it names (under a fifth of the keys) are read two at a time, one per key.
+// request's probe bound gets NONE without a read.  Both home buckets' keys are requested
+// before either is examined, then both first matching values; a key whose home bucket is
+// full (about a third at 3/4 occupancy) then reads its mask -- both masks requested
+// together -- and the buckets it names (under a fifth of the keys) are read two at a
+// time, one per key.
 __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
   const uint64_t n = pv.hdr->n;
   const uint64_t span = uint64_t(gridDim.x) * 2 * TB;
@@ -388,17 +406,25 @@ __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
     const bool skip_a = (pv.skip[blk_a >> 5] >> (blk_a & 31)) & 1u;
     const bool skip_b = !has_j || ((pv.skip[blk_b >> 5] >> (blk_b & 31)) & 1u);
     const uint64_t ha = home_bucket(key_a, ix.n_buckets), hb = home_bucket(key_b, ix.n_buckets);
-    ulonglong2 ka[SLOTS / 2], va[SLOTS / 2], kb[SLOTS / 2], vb[SLOTS / 2];
     DescWalk a, b;
     desc_init(a, key_a, ha);
     desc_init(b, key_b, hb);
     bool ea = true, eb = true;  // a skipped block: no entries, as far as the walk goes
     if (!(skip_a && skip_b)) {
+      ulonglong2 ka[SLOTS / 2], kb[SLOTS / 2];
       // both loads unconditional: a skipped block reads the other's home bucket
-      desc_load(ix, skip_a ? hb : ha, ka, va);
-      desc_load(ix, skip_b ? ha : hb, kb, vb);
-      if (!skip_a) ea = desc_fold(a, ka, va);
-      if (!skip_b) eb = desc_fold(b, kb, vb);
+      keys_load(ix, skip_a ? hb : ha, ka);
+      keys_load(ix, skip_b ? ha : hb, kb);
+      const KeyScan sa = scan_keys(ka, key_a), sb = scan_keys(kb, key_b);
+      const uint64_t va = first_val(ix, skip_a ? hb : ha, sa.match), vb = first_val(ix, skip_b ? ha : hb, sb.match);
+      if (!skip_a) {
+        desc_fold(ix, a, sa.match, va);
+        ea = sa.empty;
+      }
+      if (!skip_b) {
+        desc_fold(ix, b, sb.match, vb);
+        eb = sb.empty;
+      }
     }
     const bool need_a = !a.done && !ea, need_b = !b.done && !eb;
     if (need_a || need_b) {
@@ -412,16 +438,20 @@ __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
     if (!b.pending) desc_close(b);
     while (a.pending || b.pending) {
       // both loads unconditional: a finished walk reads the other's bucket
-      desc_load(ix, a.pending ? a.cw.b : b.cw.b, ka, va);
-      desc_load(ix, b.pending ? b.cw.b : a.cw.b, kb, vb);
+      const uint64_t ba = a.pending ? a.cw.b : b.cw.b, bb = b.pending ? b.cw.b : a.cw.b;
+      ulonglong2 ka[SLOTS / 2], kb[SLOTS / 2];
+      keys_load(ix, ba, ka);
+      keys_load(ix, bb, kb);
+      const KeyScan sa = scan_keys(ka, key_a), sb = scan_keys(kb, key_b);
+      const uint64_t va = first_val(ix, ba, sa.match), vb = first_val(ix, bb, sb.match);
       if (a.pending) {
-        const bool e = desc_fold(a, ka, va);
-        a.pending = !a.done && chain_next(ix, a.cw, e);
+        desc_fold(ix, a, sa.match, va);
+        a.pending = !a.done && chain_next(ix, a.cw, sa.empty);
         if (!a.pending) desc_close(a);
       }
       if (b.pending) {
-        const bool e = desc_fold(b, kb, vb);
-        b.pending = !b.done && chain_next(ix, b.cw, e);
+        desc_fold(ix, b, sb.match, vb);
+        b.pending = !b.done && chain_next(ix, b.cw, sb.empty);
         if (!b.pending) desc_close(b);
       }
     }

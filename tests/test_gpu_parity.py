@@ -585,3 +585,48 @@ def test_reserved_marker_keys(B):
         m = pair.oix.match(okeys, blk_off)
         for r in range(R):
             assert m[r][inst[r]] == nbr[r], (r, m[r].tolist())
+
+
+def test_probe_bound_skips_blocks_and_refreshes_orphans():
+    """A prompt whose blocks 16..23 were evicted while the later blocks stayed cached
+    (orphans): the lookup's probe bound search (evenly spaced tests, closer than 8 blocks
+    apart) lands in the evicted run, so the blocks from there on are not probed; the match
+    still equals the oracle's, and the probed insert at the orphans' instance turns the
+    unprobed blocks that are entries into refreshes and re-adds the evicted ones -- the
+    dump and the entry count equal the oracle's."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(90)
+    pair = Pair(10_000, 4)
+    toks = rng.integers(0, W.VOCAB, 50 * 16 + 5, dtype=np.int32)
+    tok_off = np.array([0, len(toks)], np.int64)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, tok_off)
+    # every block on instance 2, blocks 16..23 at epoch 1 (the oldest), the others at 5
+    old = np.zeros(nb, bool)
+    old[16:24] = True
+    for sel, ep in ((~old, 5), (old, 1)):
+        k = okeys[sel]
+        d = torch.from_numpy(k.view(np.int64)).cuda().view(torch.uint64)
+        off = np.array([0, len(k)], np.int64)
+        assert pair.insert_both(d, to_dev(off), len(k), k, off, [2], [9], ep) == 0
+    pair.gix.evict(4, 25)  # ceil(50 * 4 / 25) = 8 entries
+    assert pair.oix.evict(4, 25) == 0
+    pair.compare_index("blocks 16..23 evicted")
+    assert pair.oix.size == nb - 8
+    keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(tok_off), d_boff, nb)
+    pair.gix.probe_lookup(state, keys, d_boff, nb)
+    probed, searched = S.Index.probe_stats(state, nb)
+    assert 16 <= probed < 24 and searched > 0, (probed, searched)
+    gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
+    om = pair.oix.match(okeys, blk_off)
+    assert np.array_equal(gm, om) and gm[0].tolist() == [0, 0, 16, 0]
+    pair.gix.insert_probed(state, 1, nb, to_dev(np.array([2], np.int32)), to_dev(np.array([11], np.uint32)), 7)
+    assert pair.oix.insert(okeys, blk_off, [2], [11], 7) == 0
+    pair.compare_index("orphans refreshed, evicted blocks re-added")
+    assert pair.oix.size == nb
+    # the same prompt again: every block is held, nothing is skipped
+    keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(tok_off), d_boff, nb)
+    pair.gix.probe_lookup(state, keys, d_boff, nb)
+    probed, _ = S.Index.probe_stats(state, nb)
+    assert probed == nb
+    gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
+    assert gm[0].tolist() == [0, 0, nb, 0]
