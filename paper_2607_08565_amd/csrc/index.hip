@@ -402,6 +402,8 @@ constexpr int KCH = 32;                     // chunks per region of the bin part
 // The classify pass runs INS_WG workgroups (as many as the device holds at its register
 // use), each filling one candidate segment.
 constexpr int INS_WG = 1024;
+// Workgroups of the placement's grid.
+constexpr int PLACE_WG = 4096;
 inline uint64_t ins_segment(uint64_t n) {
   const uint64_t span = uint64_t(INS_WG) * WG_THREADS;
   return (n + span - 1) / span * WG_THREADS;
@@ -785,7 +787,7 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
   const bool inl = !pv.hdr->bad_key && !ws.hdr->req_bad && ix.hdr->n_entries + n <= ix.capacity;
   if (blockIdx.x == 0 && tid == 0) ws.hdr->inl = inl;
   Cand *seg = ws.cand + uint64_t(blockIdx.x) * ws.seg;
-  constexpr int CU = 4;
+  constexpr int CU = 2;
   int gcur = 0;  // region of this thread's current position (positions only increase)
   for (uint64_t i0 = uint64_t(blockIdx.x) * TB + tid; i0 < n; i0 += CU * span) {
     // positions past the end read the last position (in bounds) and are dropped below
@@ -2053,7 +2055,7 @@ extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe
   hipLaunchKernelGGL(insp_bdedupe_kernel, flat, dim3(DD_T), 0, stream, ws);
   hipLaunchKernelGGL(insp_check_kernel, dim3(1), blk, 0, stream, ix, ws);
   hipLaunchKernelGGL(insp_refresh_kernel, flat, blk, 0, stream, ix, pv, ws, epoch);
-  hipLaunchKernelGGL(insp_place_kernel, flat, blk, 0, stream, ix, ws, session, epoch);
+  hipLaunchKernelGGL(insp_place_kernel, dim3(PLACE_WG), blk, 0, stream, ix, ws, session, epoch);
   hipLaunchKernelGGL(spill_kernel, dim3(64), blk, 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
                      nullptr, nullptr, nullptr, ws.np);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), blk, 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,
