@@ -238,6 +238,7 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
 constexpr int BL = 4;  // lanes per request
 // Workgroups of the probe kernel's grid (measured: 1,536 -- all resident at its register use -- beat 768, 1,024, 2,048, 3,072 and 4,096).
 constexpr int PROBE_WG = 1536;
+constexpr int PROBE_K = 2;  // keys per thread and iteration
 
 // Is `key` in the table at all (any slot of its home chain)?
 __device__ bool key_present(const DevIndex &ix, uint64_t key) {
@@ -391,74 +392,110 @@ __device__ __forceinline__ void desc_close(DescWalk &w) {
                      : (w.cnt == 1 ? make_desc(D_ONE, w.first_inst, w.first_slot) : make_desc(D_MANY, 0, 0));
 }
 
-// Each thread describes two keys of the same iteration (i and i + TB); a block past its
-// request's probe bound gets NONE without a read.  Both home buckets' keys are requested
-// before either is examined, then both first matching values; a key whose home bucket is
-// full (about a third at 3/4 occupancy) then reads its mask -- both masks requested
-// together -- and the buckets it names (under a fifth of the keys) are read two at a
-// time, one per key.
+// Each thread describes PK keys of the same iteration (positions i + u TB); a block past
+// its request's probe bound gets NONE without a read.  All home buckets' keys are
+// requested before any is examined, then all first matching values; a key whose home
+// bucket is full (about a third at 3/4 occupancy) then reads its mask -- all masks
+// requested together -- and the buckets the masks name (under a fifth of the keys) are
+// read one per key per round.  Loads are unconditional: a lane with nothing to read for a
+// key reads bucket 0 (or its mask), one line that stays cached.
+template <int PK>
 __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
   const uint64_t n = pv.hdr->n;
-  const uint64_t span = uint64_t(gridDim.x) * 2 * TB;
-  for (uint64_t i = uint64_t(blockIdx.x) * 2 * TB + threadIdx.x; i < n; i += span) {
-    const uint64_t j = i + TB;
-    const bool has_j = j < n;
-    const uint64_t key_a = pv.part_key[i], key_b = has_j ? pv.part_key[j] : key_a;
-    const uint32_t blk_a = pv.part_blk[i], blk_b = has_j ? pv.part_blk[j] : blk_a;
-    const bool skip_a = (pv.skip[blk_a >> 5] >> (blk_a & 31)) & 1u;
-    const bool skip_b = !has_j || ((pv.skip[blk_b >> 5] >> (blk_b & 31)) & 1u);
-    const uint64_t ha = home_bucket(key_a, ix.n_buckets), hb = home_bucket(key_b, ix.n_buckets);
-    DescWalk a, b;
-    desc_init(a, key_a, ha);
-    desc_init(b, key_b, hb);
-    bool ea = true, eb = true;  // a skipped block: no entries, as far as the walk goes
-    if (!(skip_a && skip_b)) {
-      ulonglong2 ka[SLOTS / 2], kb[SLOTS / 2];
-      // both loads unconditional: a skipped block reads the other's home bucket
-      keys_load(ix, skip_a ? hb : ha, ka);
-      keys_load(ix, skip_b ? ha : hb, kb);
-      const KeyScan sa = scan_keys(ka, key_a), sb = scan_keys(kb, key_b);
-      const uint64_t va = first_val(ix, skip_a ? hb : ha, sa.match), vb = first_val(ix, skip_b ? ha : hb, sb.match);
-      if (!skip_a) {
-        desc_fold(ix, a, sa.match, va);
-        ea = sa.empty;
-      }
-      if (!skip_b) {
-        desc_fold(ix, b, sb.match, vb);
-        eb = sb.empty;
-      }
+  const uint64_t span = uint64_t(gridDim.x) * PK * TB;
+  for (uint64_t i = uint64_t(blockIdx.x) * PK * TB + threadIdx.x; i < n; i += span) {
+    uint64_t key[PK], h[PK];
+    bool has[PK], skip[PK];
+#pragma unroll
+    for (int u = 0; u < PK; ++u) {
+      const uint64_t q = i + uint64_t(u) * TB;
+      has[u] = q < n;
+      key[u] = pv.part_key[has[u] ? q : i];
     }
-    const bool need_a = !a.done && !ea, need_b = !b.done && !eb;
-    if (need_a || need_b) {
-      const uint32_t ma = ix.mask[need_a ? ha : hb], mb = ix.mask[need_b ? hb : ha];
-      chain_set_mask(a.cw, ma);
-      chain_set_mask(b.cw, mb);
+    uint32_t sw[PK], blk[PK];
+#pragma unroll
+    for (int u = 0; u < PK; ++u) {
+      blk[u] = pv.part_blk[has[u] ? i + uint64_t(u) * TB : i];
+      sw[u] = pv.skip[blk[u] >> 5];
     }
-    a.pending = need_a && chain_next(ix, a.cw, false);
-    b.pending = need_b && chain_next(ix, b.cw, false);
-    if (!a.pending) desc_close(a);
-    if (!b.pending) desc_close(b);
-    while (a.pending || b.pending) {
-      // both loads unconditional: a finished walk reads the other's bucket
-      const uint64_t ba = a.pending ? a.cw.b : b.cw.b, bb = b.pending ? b.cw.b : a.cw.b;
-      ulonglong2 ka[SLOTS / 2], kb[SLOTS / 2];
-      keys_load(ix, ba, ka);
-      keys_load(ix, bb, kb);
-      const KeyScan sa = scan_keys(ka, key_a), sb = scan_keys(kb, key_b);
-      const uint64_t va = first_val(ix, ba, sa.match), vb = first_val(ix, bb, sb.match);
-      if (a.pending) {
-        desc_fold(ix, a, sa.match, va);
-        a.pending = !a.done && chain_next(ix, a.cw, sa.empty);
-        if (!a.pending) desc_close(a);
-      }
-      if (b.pending) {
-        desc_fold(ix, b, sb.match, vb);
-        b.pending = !b.done && chain_next(ix, b.cw, sb.empty);
-        if (!b.pending) desc_close(b);
-      }
+    DescWalk w[PK];
+    bool any = false;
+#pragma unroll
+    for (int u = 0; u < PK; ++u) {
+      skip[u] = !has[u] || ((sw[u] >> (blk[u] & 31)) & 1u);
+      h[u] = home_bucket(key[u], ix.n_buckets);
+      desc_init(w[u], key[u], h[u]);
+      any |= !skip[u];
     }
-    pv.desc_p[i] = a.out;
-    if (has_j) pv.desc_p[j] = b.out;
+    bool e[PK];
+#pragma unroll
+    for (int u = 0; u < PK; ++u) e[u] = true;  // a skipped block: no entries, as far as the walk goes
+    if (any) {
+      ulonglong2 kk[PK][SLOTS / 2];
+#pragma unroll
+      for (int u = 0; u < PK; ++u) keys_load(ix, skip[u] ? 0 : h[u], kk[u]);
+      KeyScan sc[PK];
+      uint64_t v[PK];
+#pragma unroll
+      for (int u = 0; u < PK; ++u) {
+        sc[u] = scan_keys(kk[u], key[u]);
+        v[u] = first_val(ix, skip[u] ? 0 : h[u], skip[u] ? 0u : sc[u].match);
+      }
+#pragma unroll
+      for (int u = 0; u < PK; ++u)
+        if (!skip[u]) {
+          desc_fold(ix, w[u], sc[u].match, v[u]);
+          e[u] = sc[u].empty;
+        }
+    }
+    bool need[PK], any_need = false;
+#pragma unroll
+    for (int u = 0; u < PK; ++u) {
+      need[u] = !w[u].done && !e[u];
+      any_need |= need[u];
+    }
+    if (any_need) {
+      uint32_t m[PK];
+#pragma unroll
+      for (int u = 0; u < PK; ++u) m[u] = ix.mask[need[u] ? h[u] : 0];
+#pragma unroll
+      for (int u = 0; u < PK; ++u) chain_set_mask(w[u].cw, m[u]);
+    }
+    bool pending = false;
+#pragma unroll
+    for (int u = 0; u < PK; ++u) {
+      w[u].pending = need[u] && chain_next(ix, w[u].cw, false);
+      if (!w[u].pending) desc_close(w[u]);
+      pending |= w[u].pending;
+    }
+    while (pending) {
+      uint64_t bb[PK];
+      ulonglong2 kk[PK][SLOTS / 2];
+#pragma unroll
+      for (int u = 0; u < PK; ++u) {
+        bb[u] = w[u].pending ? w[u].cw.b : 0;
+        keys_load(ix, bb[u], kk[u]);
+      }
+      KeyScan sc[PK];
+      uint64_t v[PK];
+#pragma unroll
+      for (int u = 0; u < PK; ++u) {
+        sc[u] = scan_keys(kk[u], key[u]);
+        v[u] = first_val(ix, bb[u], w[u].pending ? sc[u].match : 0u);
+      }
+      pending = false;
+#pragma unroll
+      for (int u = 0; u < PK; ++u)
+        if (w[u].pending) {
+          desc_fold(ix, w[u], sc[u].match, v[u]);
+          w[u].pending = !w[u].done && chain_next(ix, w[u].cw, sc[u].empty);
+          if (!w[u].pending) desc_close(w[u]);
+          pending |= w[u].pending;
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < PK; ++u)
+      if (has[u]) pv.desc_p[i + uint64_t(u) * TB] = w[u].out;
   }
 }
 
@@ -538,7 +575,7 @@ extern "C" int smetric_probe_lookup(const smetric_index *idx, void *probe, uint6
   if (n_req > 0 && n_blocks > 0)
     hipLaunchKernelGGL(bound_kernel, dim3((uint64_t(n_req) * BL + TB - 1) / TB), dim3(TB), 0, stream, ix, pv, keys,
                        blk_off, n_req, uint64_t(n_blocks));
-  hipLaunchKernelGGL(probe_kernel, dim3(PROBE_WG), dim3(TB), 0, stream, ix, pv);
+  hipLaunchKernelGGL(probe_kernel<PROBE_K>, dim3(PROBE_WG), dim3(TB), 0, stream, ix, pv);
   return hip_rc(hipGetLastError());
 }
 
