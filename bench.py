@@ -251,7 +251,7 @@ CALL_KERNELS = {
              "part_scatter_kernel"],
     # smetric_probe_lookup: each request's probe bound, then one holder descriptor per block,
     # in region order
-    "probe": ["zero32_kernel", "zero_kernel", "bound_kernel", "probe_kernel"],
+    "probe": ["zero32_kernel", "zero_kernel", "bound_kernel", "probe_kernel<2>"],
     "match": ["match_kernel<1, true>"],
     "route": ["route_kernel<0>"],
     "insert": ["fill_kernel", "insp_valid_kernel", "insp_classify_kernel", "insp_size_kernel", "insp_bcount_kernel",

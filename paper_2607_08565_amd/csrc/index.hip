@@ -32,7 +32,7 @@
 //              key's (T+1)-th plain slot -- unique, since claims fill a chain in order --
 //              queues the key for conversion
 //   spill      queued keys get a bitmap record, member slots, a header and tombstones
-#include <hipcub/hipcub.hpp>
+#include <rocprim/device/device_radix_sort.hpp>
 
 #include "common.h"
 
@@ -1717,8 +1717,9 @@ struct EvictWs {
 
 size_t sort_temp_bytes(uint64_t n) {
   size_t tb = 0;
-  hipcub::DoubleBuffer<uint64_t> k(nullptr, nullptr), v(nullptr, nullptr);
-  if (hipcub::DeviceRadixSort::SortPairs(nullptr, tb, k, v, int(n < 1 ? 1 : n), 0, 64, 0) != hipSuccess) return 0;
+  rocprim::double_buffer<uint64_t> k(nullptr, nullptr), v(nullptr, nullptr);
+  if (rocprim::radix_sort_pairs(nullptr, tb, k, v, size_t(n < 1 ? 1 : n), 0u, 64u, hipStream_t(nullptr)) != hipSuccess)
+    return 0;
   return tb;
 }
 
@@ -1779,13 +1780,13 @@ int gather_sorted(const smetric_index *idx, const EvictWs &ws, uint64_t n, uint6
   *vals_out = ws.va;
   if (n <= 1) return SMETRIC_OK;
   size_t tb = ws.temp_bytes;
-  hipcub::DoubleBuffer<uint64_t> vk(ws.va, ws.vb), kv(ws.ka, ws.kb);
-  if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, vk, kv, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
-  hipcub::DoubleBuffer<uint64_t> k2(kv.Current(), kv.Alternate()), v2(vk.Current(), vk.Alternate());
+  rocprim::double_buffer<uint64_t> vk(ws.va, ws.vb), kv(ws.ka, ws.kb);
+  if (rocprim::radix_sort_pairs(ws.temp, tb, vk, kv, size_t(n), 0u, 64u, s) != hipSuccess) return SMETRIC_EHIP;
+  rocprim::double_buffer<uint64_t> k2(kv.current(), kv.alternate()), v2(vk.current(), vk.alternate());
   tb = ws.temp_bytes;
-  if (hipcub::DeviceRadixSort::SortPairs(ws.temp, tb, k2, v2, int(n), 0, 64, s) != hipSuccess) return SMETRIC_EHIP;
-  *keys_out = k2.Current();
-  *vals_out = v2.Current();
+  if (rocprim::radix_sort_pairs(ws.temp, tb, k2, v2, size_t(n), 0u, 64u, s) != hipSuccess) return SMETRIC_EHIP;
+  *keys_out = k2.current();
+  *vals_out = v2.current();
   return SMETRIC_OK;
 }
 
