@@ -60,6 +60,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--direct", action="store_true",
                     help="match and insert probe the index themselves instead of sharing one region-ordered probe")
+    ap.add_argument("--overlap-path", action="store_true",
+                    help="also measure the hash + probe path with the next batch's hash beside this batch's "
+                         "lookup and match (two streams); off by default, so that a profile of the default run "
+                         "averages each kernel over the timed steps' launches only")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the timed steps, copy 1 GiB on the device (the counter runs' scale)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
@@ -818,7 +822,7 @@ def main():
                      "names": ["first-turn", "evicted", "stick", "last-resort", "migrate"]},
         "insert_checks": checks,
     }
-    if not args.direct:  # batch k+1's hash beside batch k's lookup and match (no route, no insert)
+    if args.overlap_path and not args.direct:  # batch k+1's hash beside batch k's lookup and match
         setup.restore()
         m2 = [torch.empty_like(setup.matched), torch.empty_like(setup.matched)]
         batches = [setup.batch_of(args.warmup + k) for k in range(args.steps)]
