@@ -281,8 +281,8 @@ def _kname(full: str) -> str:
     return n
 
 
-STEP_SEQ = [k for c in ("hash", "probe", "match", "route", "insert") for k in CALL_KERNELS[c]]
-CALL_OF = {k: c for c in CALL_KERNELS for k in CALL_KERNELS[c]}
+STEP_CALLS = [(c, k) for c in ("hash", "probe", "match", "route", "insert") for k in CALL_KERNELS[c]]
+STEP_SEQ = [k for _, k in STEP_CALLS]
 
 
 def timed_step_dispatches(rows, steps: int):
@@ -307,10 +307,10 @@ def summarize_trace(csv_path: str, steps: int):
     st = timed_step_dispatches(rows, steps)
     out = ["| call | kernel | mean µs | min µs | max µs |", "|---|---|---|---|---|"]
     per_call = {}
-    for j, k in enumerate(STEP_SEQ):
+    for j, (c, k) in enumerate(STEP_CALLS):
         d = [s[j][1] for s in st]
-        out.append(f"| {CALL_OF[k]} | {k} | {np.mean(d):.1f} | {min(d):.1f} | {max(d):.1f} |")
-        per_call[CALL_OF[k]] = per_call.get(CALL_OF[k], 0.0) + float(np.mean(d))
+        out.append(f"| {c} | {k} | {np.mean(d):.1f} | {min(d):.1f} | {max(d):.1f} |")
+        per_call[c] = per_call.get(c, 0.0) + float(np.mean(d))
     out += ["", "| call | sum of kernel means µs |", "|---|---|"]
     out += [f"| {c} | {v:.1f} |" for c, v in per_call.items()]
     return "\n".join(out)
@@ -357,12 +357,12 @@ def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int, b
            "fetch_scale": round(kf, 4), "write_scale": round(kw, 4), "kernels": {}}
     out = [f"Copy calibration: FETCH_SIZE x {kf:.3f}, WRITE_SIZE x {kw:.3f} = bytes of a {copy_bytes >> 20} MiB copy.",
            "", "| call | kernel | fetched MB | written MB | traffic MB |", "|---|---|---|---|---|"]
-    for j, k in enumerate(STEP_SEQ):
+    for j, (c, k) in enumerate(STEP_CALLS):
         f = float(np.mean([s[j][1] for s in fs])) * kf
         w = float(np.mean([s[j][1] for s in ws])) * kw
-        res["kernels"][k] = round(f + w)
-        res[CALL_OF[k]] = res.get(CALL_OF[k], 0) + round(f + w)
-        out.append(f"| {CALL_OF[k]} | {k} | {f / 1e6:.1f} | {w / 1e6:.1f} | {(f + w) / 1e6:.1f} |")
+        res["kernels"][f"{c}:{k}:{j}"] = round(f + w)
+        res[c] = res.get(c, 0) + round(f + w)
+        out.append(f"| {c} | {k} | {f / 1e6:.1f} | {w / 1e6:.1f} | {(f + w) / 1e6:.1f} |")
     out += ["", "| call | traffic MB per launch |", "|---|---|"]
     out += [f"| {c} | {res[c] / 1e6:.1f} |" for c in ("hash", "probe", "match", "route", "insert")]
     return res, "\n".join(out)
