@@ -78,7 +78,7 @@ inline DevIndex dev_view(const smetric_index *ix) {
   return d;
 }
 // Bytes of the displacement masks (whole 32-bit words: they are set with 32-bit atomics).
-inline uint64_t mask_bytes(uint64_t n_buckets) { return (n_buckets + 3) / 4 * 4; }
+inline uint64_t mask_bytes(uint64_t n_buckets) { return (n_buckets + 3) / 4 * 4; }  // room for 8 bits per bucket
 
 // Bucket of a key: a multiplicative mix of the key mapped onto [0, n_buckets) with a
 // 64x64 high product (keys from the hash are already uniform; the mix protects against
@@ -145,28 +145,35 @@ __device__ __forceinline__ BucketScan scan_bucket(const uint64_t *bk, uint64_t k
 }
 __device__ __forceinline__ uint64_t next_bucket(uint64_t b, uint64_t n) { return b + 1 == n ? 0 : b + 1; }
 
-// Displacement mask of a chain start h (a key's home bucket, or a member bucket): bit d,
-// 1 <= d < MASK_FAR, is set once a slot was claimed in bucket h + d by a walk that
-// started at h; bit MASK_FAR once one was claimed at h + MASK_FAR or further.  A walk
-// from h claims the first EMPTY slot it meets and slots never become EMPTY again, so
-// every entry whose chain starts at h lies in bucket h itself, in a bucket h + d of a set
-// bit, or -- under the far bit -- between h + MASK_FAR and the first bucket with an EMPTY
+// Displacement mask of a chain start h (a key's home bucket, or a member bucket), MASK_BITS
+// bits: bit d, 1 <= d < MASK_BITS, is set once a slot was claimed in bucket h + d by a walk
+// that started at h; bit 0 (far) once one was claimed at h + MASK_BITS or further.  A walk
+// from h claims the first EMPTY slot it meets and slots never become EMPTY again, so every
+// entry whose chain starts at h lies in bucket h itself, in a bucket h + d of a set bit,
+// or -- under the far bit -- between h + MASK_BITS and the first bucket with an EMPTY
 // slot; and none lies past a bucket that holds an EMPTY slot.  A lookup therefore reads
-// bucket h, and only when that is full the mask and the buckets it names, instead of
-// every bucket up to the first EMPTY slot (~1.7 buckets on average at 3/4 occupancy,
-// with a long tail).  The mask only grows (tombstones keep their bits); a rebuild
-// recomputes it.
-constexpr int MASK_FAR = 7;
-constexpr uint32_t MASK_NEAR = (1u << MASK_FAR) - 2u;  // bits 1 .. MASK_FAR - 1
+// bucket h, and only when that is full the mask and the buckets it names, instead of every
+// bucket up to the first EMPTY slot (~1.7 buckets on average at 3/4 occupancy, with a long
+// tail).  The mask only grows (tombstones keep their bits); a rebuild recomputes it.
+constexpr int MASK_BITS = 8;
+constexpr int MASK_PER_WORD = 32 / MASK_BITS;
+constexpr uint32_t MASK_ONES = (1u << MASK_BITS) - 1u;
+constexpr uint32_t MASK_NEAR = MASK_ONES & ~1u;  // bits 1 .. MASK_BITS - 1
+constexpr uint32_t MASK_FARBIT = 1u;
 __device__ __forceinline__ uint64_t wrap_bucket(uint64_t b, uint64_t n) { return b >= n ? b - n : b; }
+__device__ __forceinline__ uint32_t mask_get(const DevIndex &ix, uint64_t h) {
+  if (MASK_BITS == 8) return ix.mask[h];
+  const uint32_t byte = ix.mask[h * MASK_BITS / 8];
+  return (byte >> ((h % (8 / MASK_BITS)) * MASK_BITS)) & MASK_ONES;
+}
 // Records a claim in bucket b by a walk from h (nothing for h itself): one atomic only
 // when the bit is new.
 __device__ __forceinline__ void mask_note(const DevIndex &ix, uint64_t h, uint64_t b) {
   const uint64_t d = b >= h ? b - h : b + ix.n_buckets - h;
   if (d == 0) return;
-  const uint32_t bit = d < MASK_FAR ? 1u << d : 1u << MASK_FAR;
-  if (ix.mask[h] & bit) return;
-  atomicOr(reinterpret_cast<unsigned int *>(ix.mask) + (h >> 2), bit << ((h & 3) * 8));
+  const uint32_t bit = d < MASK_BITS ? 1u << d : MASK_FARBIT;
+  if (mask_get(ix, h) & bit) return;
+  atomicOr(reinterpret_cast<unsigned int *>(ix.mask) + h / MASK_PER_WORD, bit << ((h % MASK_PER_WORD) * MASK_BITS));
 }
 
 // The buckets that can hold entries of a chain starting at h, in chain order.  The walk
@@ -178,7 +185,7 @@ struct ChainWalk {
   uint32_t bits;   // near bits still to visit
   bool at_home;    // w.b == h, the mask not consulted yet
   bool have_mask;  // set_mask was called
-  bool far;        // far bit set: walk on from h + MASK_FAR
+  bool far;        // far bit set: walk on from h + MASK_BITS
   bool in_far;
   uint64_t steps;
 };
@@ -187,7 +194,7 @@ __device__ __forceinline__ ChainWalk chain_start(uint64_t h) {
 }
 __device__ __forceinline__ void chain_set_mask(ChainWalk &w, uint32_t m) {
   w.bits = m & MASK_NEAR;
-  w.far = ((m >> MASK_FAR) & 1u) != 0;
+  w.far = (m & MASK_FARBIT) != 0;
   w.have_mask = true;
 }
 __device__ __forceinline__ bool chain_next(const DevIndex &ix, ChainWalk &w, bool had_empty) {
@@ -195,7 +202,7 @@ __device__ __forceinline__ bool chain_next(const DevIndex &ix, ChainWalk &w, boo
   if (had_empty) return false;
   if (w.at_home) {
     w.at_home = false;
-    if (!w.have_mask) chain_set_mask(w, ix.mask[w.h]);
+    if (!w.have_mask) chain_set_mask(w, mask_get(ix, w.h));
   } else if (w.in_far) {
     if (++w.steps >= n) return false;
     w.b = next_bucket(w.b, n);
@@ -206,9 +213,9 @@ __device__ __forceinline__ bool chain_next(const DevIndex &ix, ChainWalk &w, boo
     w.bits &= w.bits - 1;
     return true;
   }
-  if (w.far && n > MASK_FAR) {
+  if (w.far && n > MASK_BITS) {
     w.in_far = true;
-    w.b = wrap_bucket(w.h + MASK_FAR, n);
+    w.b = wrap_bucket(w.h + MASK_BITS, n);
     return true;
   }
   return false;

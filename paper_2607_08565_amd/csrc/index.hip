@@ -1608,8 +1608,12 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
       pos[seg + j_lo + u] = (b_lo * SLOTS + (e & 0x7FFFu)) | (uint64_t(e >> 15) << 63) | (uint64_t(1) << 62);
   }
   // the two buckets' masks restart from what the tile places; the claim pass adds the rest
-  if (mine + 1 < ix.n_buckets) *reinterpret_cast<uint16_t *>(ix.mask + mine) = uint16_t(dm);
-  else if (mine < ix.n_buckets) ix.mask[mine] = uint8_t(dm);
+  if (MASK_BITS == 8) {
+    if (mine + 1 < ix.n_buckets) *reinterpret_cast<uint16_t *>(ix.mask + mine) = uint16_t(dm);
+    else if (mine < ix.n_buckets) ix.mask[mine] = uint8_t(dm);
+  } else if (mine < ix.n_buckets) {  // mine is even: the two buckets share one byte
+    ix.mask[mine * MASK_BITS / 8] = uint8_t(dm & MASK_ONES);
+  }
   __syncthreads();
   const uint64_t nb = ix.n_buckets - b_lo < uint64_t(RT) ? ix.n_buckets - b_lo : uint64_t(RT);
   ulonglong2 *dst = reinterpret_cast<ulonglong2 *>(ix.slots + b_lo * BUCKET_WORDS);

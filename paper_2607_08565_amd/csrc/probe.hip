@@ -457,7 +457,7 @@ __global__ __launch_bounds__(TB) void probe_kernel(DevIndex ix, ProbeView pv) {
     if (any_need) {
       uint32_t m[PK];
 #pragma unroll
-      for (int u = 0; u < PK; ++u) m[u] = ix.mask[need[u] ? h[u] : 0];
+      for (int u = 0; u < PK; ++u) m[u] = mask_get(ix, need[u] ? h[u] : 0);
 #pragma unroll
       for (int u = 0; u < PK; ++u) chain_set_mask(w[u].cw, m[u]);
     }
