@@ -630,3 +630,49 @@ def test_probe_bound_skips_blocks_and_refreshes_orphans():
     assert probed == nb
     gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
     assert gm[0].tolist() == [0, 0, nb, 0]
+
+
+def test_probe_bound_small_and_empty_requests():
+    """Probe bounds over prompts of 0-5 blocks and longer ones, some entered whole, some in
+    part, some not at all, with empty requests between them: the match, the route and the
+    probed insert equal the oracle's, and the lookup probes no more blocks than exist and
+    every block a fully cached prompt has."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(91)
+    I = 6
+    pair = Pair(50_000, I)
+    lens_blk = [0, 1, 2, 3, 0, 5, 1, 40, 0, 2, 17, 64, 65, 0, 3]
+    prompts = [rng.integers(0, W.VOCAB, 16 * n + int(rng.integers(0, 16)), dtype=np.int32) for n in lens_blk]
+    off = np.zeros(len(prompts) + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    toks = np.concatenate(prompts)
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(toks, off)
+    # enter a prefix of each prompt: whole (even r), half (r % 3 == 1), none (others)
+    R = len(prompts)
+    keep = [lens_blk[r] if r % 2 == 0 else (lens_blk[r] // 2 if r % 3 == 1 else 0) for r in range(R)]
+    sel = np.concatenate([np.arange(blk_off[r], blk_off[r] + keep[r]) for r in range(R)]).astype(np.int64)
+    pk = okeys[sel]
+    poff = np.zeros(R + 1, np.int64)
+    poff[1:] = np.cumsum(keep)
+    d_pk = to_dev(pk)
+    inst = (np.arange(R) % I).astype(np.int32)
+    assert pair.insert_both(d_pk, to_dev(poff), int(poff[-1]), pk, poff, inst, np.arange(R, dtype=np.uint32), 1) == 0
+    keys, state = pair.gix.hash_partition(to_dev(toks), to_dev(off), d_boff, nb)
+    pair.gix.probe_lookup(state, keys, d_boff, nb)
+    probed, searched = S.Index.probe_stats(state, nb)
+    assert probed <= nb and probed >= sum(keep[r] for r in range(R) if r % 2 == 0)
+    gm = pair.gix.match_probed(state, keys, d_boff, nb).cpu().numpy()
+    om = pair.oix.match(okeys, blk_off)
+    assert np.array_equal(gm, om)
+    b = W.Batch(tokens=toks, tok_off=off, prompt_len=np.diff(off).astype(np.int32),
+                hist_len=np.diff(off).astype(np.int32), turn=np.ones(R, np.int32),
+                session=np.arange(R, dtype=np.uint32) + 100, q=rng.integers(0, 10**6, I).astype(np.int64),
+                rr_base=3, epoch=2)
+    gt, gb = S.route(to_dev(gm), to_dev(b.prompt_len), to_dev(b.hist_len), to_dev(b.turn), to_dev(b.q),
+                     W.DEFAULT_PARAMS, b.rr_base)
+    ot, ob = oracle.route(om, b.prompt_len, b.hist_len, b.turn, b.q, W.DEFAULT_PARAMS, b.rr_base)
+    assert np.array_equal(gt.cpu().numpy(), ot) and np.array_equal(gb.cpu().numpy(), ob)
+    pair.gix.insert_probed(state, R, nb, to_dev(np.asarray(ot, np.int32)), to_dev(b.session), b.epoch)
+    assert pair.oix.insert(okeys, blk_off, ot, b.session, b.epoch) == 0
+    pair.compare_index("small and empty requests")
+    say(f"  blocks {nb}, probed {probed}, search probes {searched}")
