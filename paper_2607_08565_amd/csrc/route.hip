@@ -685,6 +685,7 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
 //         decided by rescoring its listed candidates on the current state.
 //         The scores est2 x n are compared in 192 bits: over a batch both factors grow.
 // ---------------------------------------------------------------------------------
+typedef unsigned __int128 u128;
 constexpr int SEQC_MAX_I = 4096;  // LDS: 2q (64 KB), n and the step counters (16 KB each)
 
 struct SeqCRec {
@@ -694,8 +695,21 @@ struct SeqCRec {
   int32_t L;
   int32_t start;  // (rr_base + r) mod I
   i128 cost_prev;  // 2 x prefill_cost(req, c[prev])
-  i128 bound;      // SLACK_num x 2 (b + a L)
+  i128 thr;        // prev meets the deadline iff its doubled queue is at most thr
 };
+
+// floor(x / d) for 0 <= x < 2^128 and 0 < d < 2^32, by 32-bit digits
+__device__ __forceinline__ u128 div128_u32(u128 x, uint32_t d) {
+  u128 q = 0;
+  uint64_t rem = 0;
+#pragma unroll
+  for (int k = 3; k >= 0; --k) {
+    const uint64_t cur = (rem << 32) | uint32_t(x >> (32 * k));
+    q |= u128(cur / d) << (32 * k);
+    rem = cur % d;
+  }
+  return q;
+}
 
 __device__ __forceinline__ bool tpot_pass(int64_t slack, i128 cost2) {
   return slack >= NO_DECODE || cost2 <= i128(2) * slack;
@@ -747,12 +761,14 @@ __global__ __launch_bounds__(64 * RW) void route_seqc_prep_kernel(const int32_t 
   out.L = ok ? int32_t(L) : 0;
   out.start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
   out.cost_prev = cost_prev;
-  out.bound = i128(p.slack_num) * (i128(2) * (i128(p.slo_b) + i128(p.slo_a) * (ok ? L : 0)));
+  // (2q + cost_prev) x SLACK_den <= SLACK_num x 2 (b + a L), both sides integers and the
+  // bound non-negative: 2q <= floor(bound / SLACK_den) - cost_prev; SLACK infinite: always
+  const i128 bound = i128(p.slack_num) * (i128(2) * (i128(p.slo_b) + i128(p.slo_a) * (ok ? L : 0)));
+  out.thr = p.slack_den == 0 ? (i128(1) << 126) : i128(div128_u32(u128(bound), uint32_t(p.slack_den))) - cost_prev;
   rec[r] = out;
 }
 
 // a * x for 0 <= a < 2^127, x < 2^32, as (high 128 bits, low 64 bits)
-typedef unsigned __int128 u128;
 struct P192 {
   u128 hi;
   uint64_t lo;
@@ -809,16 +825,29 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
          uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
 }
 
-// Minimum of a 64-bit key over the wavefront by DPP moves toward lane 63; every lane gets it.
+// Minimum of a 32-bit value over the wavefront by DPP moves toward lane 63 (lanes without a
+// source, or outside the row mask, take all ones: the identity of the minimum, which lets
+// the move fold into the minimum's DPP form); every lane gets it.
+template <int CTRL, int RM>
+__device__ __forceinline__ uint32_t dpp_min_u32(uint32_t k) {
+  const uint32_t o = uint32_t(__builtin_amdgcn_update_dpp(-1, int(k), CTRL, RM, 0xF, false));
+  return o < k ? o : k;
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t k) {
+  k = dpp_min_u32<0x111, 0xF>(k);
+  k = dpp_min_u32<0x112, 0xF>(k);
+  k = dpp_min_u32<0x114, 0xF>(k);
+  k = dpp_min_u32<0x118, 0xF>(k);
+  k = dpp_min_u32<0x142, 0xA>(k);  // row_bcast:15 into rows 1 and 3
+  k = dpp_min_u32<0x143, 0xC>(k);  // row_bcast:31 into rows 2 and 3
+  return uint32_t(__builtin_amdgcn_readlane(int(k), 63));
+}
+// Minimum of a 64-bit key over the wavefront: the smallest high word, then the smallest low
+// word among the lanes holding it; every lane gets it.
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
-  uint64_t o;
-  o = dpp_or_own64<0x111, 0xF>(k), k = o < k ? o : k;
-  o = dpp_or_own64<0x112, 0xF>(k), k = o < k ? o : k;
-  o = dpp_or_own64<0x114, 0xF>(k), k = o < k ? o : k;
-  o = dpp_or_own64<0x118, 0xF>(k), k = o < k ? o : k;
-  o = dpp_or_own64<0x142, 0xA>(k), k = o < k ? o : k;  // row_bcast:15 into rows 1 and 3
-  o = dpp_or_own64<0x143, 0xC>(k), k = o < k ? o : k;  // row_bcast:31 into rows 2 and 3
-  return readlane64(k, 63);
+  const uint32_t hi = wave_min_u32(uint32_t(k >> 32));
+  const uint32_t lo = wave_min_u32(uint32_t(k >> 32) == hi ? uint32_t(k) : ~0u);
+  return (uint64_t(hi) << 32) | lo;
 }
 
 // Lexicographic minimum of (k1, k0) over lanes 0..N-1 (N = 64: the wavefront; N <= 16:
@@ -930,14 +959,54 @@ __global__ __launch_bounds__(SQT) void route_seqc_init_kernel(int32_t I, const i
   if (threadIdx.x == 0) *w.st = ok;
 }
 
-// Ranking: request j of block L, on X_L.  Every candidate's key (score x 2^12 + rotation
-// distance; the score is below 2^160, so the key fits three words) goes into LDS, the
-// keys are sorted (bitonic, ascending; non-candidates and padding are all ones), and the
-// first SQK candidates are listed with their costs.
+// A candidate's key as three words compared in order (k2, k1, k0); all ones: no candidate.
+struct Key3 {
+  uint64_t k2, k1, k0;
+};
+__device__ __forceinline__ bool key_less(const Key3 &a, const Key3 &b) {
+  return a.k2 < b.k2 || (a.k2 == b.k2 && (a.k1 < b.k1 || (a.k1 == b.k1 && a.k0 < b.k0)));
+}
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+  const int lo = __shfl(int(uint32_t(v)), src, 64), hi = __shfl(int(uint32_t(v >> 32)), src, 64);
+  return (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo);
+}
+__device__ __forceinline__ Key3 key_shfl(const Key3 &k, int src) {
+  return Key3{shfl64(k.k2, src), shfl64(k.k1, src), shfl64(k.k0, src)};
+}
+// Compare-exchange with lane ^ j: this lane keeps the smaller key iff keep_min.
+__device__ __forceinline__ void key_cx(Key3 &k, int j, bool keep_min) {
+  const int lane = threadIdx.x & 63;
+  const Key3 o = key_shfl(k, lane ^ j);
+  if (key_less(o, k) == keep_min) k = o;
+}
+// The wavefront's 64 keys (one per lane) sorted ascending across the lanes (bitonic network).
+__device__ __forceinline__ void key_sort64(Key3 &k) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int size = 2; size <= 64; size <<= 1)
+#pragma unroll
+    for (int j = size >> 1; j > 0; j >>= 1) key_cx(k, j, ((lane & j) == 0) == ((lane & size) == 0));
+}
+// run and o sorted ascending: run becomes the 64 smallest of both, sorted ascending.
+// min(run[l], o[63 - l]) are those 64 keys in bitonic order; a bitonic merge sorts them.
+__device__ __forceinline__ void key_merge64(Key3 &run, const Key3 &o_rev) {
+  const int lane = threadIdx.x & 63;
+  if (key_less(o_rev, run)) run = o_rev;
+#pragma unroll
+  for (int j = 32; j > 0; j >>= 1) key_cx(run, j, (lane & j) == 0);
+}
+
+// Ranking: request j of block L, on X_L.  Every candidate's key is score x 2^12 + rotation
+// distance (the score is below 2^160, so the key fits three words).  Each wavefront keeps
+// the 64 smallest keys of its instances (w 64 + lane + 1024 m) sorted across its lanes;
+// the 16 wavefronts' lists are then merged pairwise through LDS, and the SQK = 64 smallest
+// keys overall are listed with their costs.  The list need not be in key order: the
+// deciding wavefront rescores every listed candidate.
 __device__ __forceinline__ void seqc_rank(int32_t L, const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
                                           const int64_t *__restrict__ slack, const RouteParams &p, const SeqCWs &w,
                                           uint64_t *smem) {
-  const int tid = threadIdx.x;
+  static_assert(SQK == 64 && SQT == 1024, "one listed candidate per lane, 16 wavefronts");
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int32_t j = int32_t(blockIdx.x) - 1;
   const int32_t r = L * SQW + j;
   if (r >= n_req) return;  // whole workgroup
@@ -953,54 +1022,48 @@ __device__ __forceinline__ void seqc_rank(int32_t L, const int32_t *__restrict__
   const i128 *q2 = w.q2 + uint64_t(L & 1) * I;
   const uint32_t *nr = w.nr + uint64_t(L & 1) * I;
   const int32_t *c = matched + int64_t(r) * I;
-  int NP = 2;
-  while (NP < I) NP <<= 1;
-  uint64_t *k2 = smem, *k1 = smem + SQ_NP, *k0 = smem + 2 * SQ_NP;
-  for (int32_t i = tid; i < NP; i += SQT) {
-    uint64_t a2 = ~uint64_t(0), a1 = ~uint64_t(0), a0 = ~uint64_t(0);
+  constexpr uint64_t ONES = ~uint64_t(0);
+  Key3 run{ONES, ONES, ONES};
+  for (int32_t base = wave * 64; base < I; base += SQT) {  // wavefront-uniform
+    const int32_t i = base + lane;
+    Key3 k{ONES, ONES, ONES};
     if (i < I) {
       const i128 cst = est2(p, Lr, c[i], 0);
       if (!any_pass || tpot_pass(slack[i], cst)) {
         const P192 s = mul192(q2[i] + cst, nr[i]);
         const uint64_t d = uint64_t(i >= start ? i - start : i - start + I);
         const uint64_t h0 = uint64_t(s.hi), h1 = uint64_t(s.hi >> 64);
-        a0 = (s.lo << 12) | d;
-        a1 = (s.lo >> 52) | (h0 << 12);
-        a2 = (h0 >> 52) | (h1 << 12);  // below 2^44: no candidate's key is all ones
+        k.k0 = (s.lo << 12) | d;
+        k.k1 = (s.lo >> 52) | (h0 << 12);
+        k.k2 = (h0 >> 52) | (h1 << 12);  // below 2^44: no candidate's key is all ones
       }
     }
-    k2[i] = a2;
-    k1[i] = a1;
-    k0[i] = a0;
+    key_sort64(k);
+    if (base == wave * 64) {
+      run = k;
+    } else {
+      key_merge64(run, key_shfl(k, 63 - lane));
+    }
   }
-  __syncthreads();
-  for (int size = 2; size <= NP; size <<= 1)
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int u = tid; u < NP / 2; u += SQT) {
-        const int a = ((u & ~(stride - 1)) << 1) | (u & (stride - 1)), b = a + stride;
-        const uint64_t a2 = k2[a], a1 = k1[a], a0 = k0[a], b2 = k2[b], b1 = k1[b], b0 = k0[b];
-        const bool b_less = b2 < a2 || (b2 == a2 && (b1 < a1 || (b1 == a1 && b0 < a0)));
-        if (b_less == ((a & size) == 0)) {
-          k2[a] = b2;
-          k1[a] = b1;
-          k0[a] = b0;
-          k2[b] = a2;
-          k1[b] = a1;
-          k0[b] = a0;
-        }
-      }
-      __syncthreads();
-    }
-  bool listed = false;
-  if (tid < SQK && tid < NP && !(k2[tid] == ~uint64_t(0) && k1[tid] == ~uint64_t(0) && k0[tid] == ~uint64_t(0))) {
-    listed = true;
-    int32_t inst = start + int32_t(k0[tid] & 4095);
+  // pairwise merges: at level h, wavefront w < h takes the list of wavefront w + h
+  Key3 *buf = reinterpret_cast<Key3 *>(smem);  // [8][64]
+#pragma unroll
+  for (int h = 8; h >= 1; h >>= 1) {
+    if (wave >= h && wave < 2 * h) buf[(wave - h) * 64 + lane] = run;
+    __syncthreads();
+    if (wave < h) key_merge64(run, buf[wave * 64 + 63 - lane]);
+    __syncthreads();
+  }
+  if (wave != 0) return;
+  const bool listed = !(run.k2 == ONES && run.k1 == ONES && run.k0 == ONES);
+  if (listed) {  // the listed entries are the first cnt lanes (keys ascending, padding last)
+    int32_t inst = start + int32_t(run.k0 & 4095);
     inst = inst >= I ? inst - I : inst;
-    w.l_inst[le * SQK + tid] = uint32_t(inst);
-    w.l_cst[le * SQK + tid] = est2(p, Lr, c[inst], 0);
+    w.l_inst[le * SQK + lane] = uint32_t(inst);
+    w.l_cst[le * SQK + lane] = est2(p, Lr, c[inst], 0);
   }
-  const int cnt = __syncthreads_count(listed);  // the listed entries are the first cnt
-  if (tid == 0) w.l_cnt[le] = uint32_t(cnt);
+  const int cnt = __popcll(__ballot(listed));
+  if (lane == 0) w.l_cnt[le] = uint32_t(cnt);
 }
 
 // A request to decide with its record and list (entries lane + 64 h, h < SQE).
@@ -1010,17 +1073,23 @@ struct SeqLRow {
   uint32_t inst[SQE];
   i128 cst[SQE];
 };
-__device__ __forceinline__ void seqc_lrow_load(int32_t r, int32_t re, const SeqCWs &w, SeqLRow &row) {
+// The deciding workgroup's copy of block L-1 in LDS: records, list counts and lists.
+struct SeqCStage {
+  int32_t bs;           // the block's first request
+  const SeqCRec *rec;   // [SQW]
+  const uint32_t *cnt;  // [SQW]
+  const uint32_t *inst;  // [SQW][SQK]
+  const i128 *cst;       // [SQW][SQK]
+};
+__device__ __forceinline__ void seqc_lrow_load(int32_t r, int32_t re, const SeqCStage &sg, SeqLRow &row) {
   const int lane = threadIdx.x & 63;
-  int32_t rr = r < re ? r : re - 1;  // clamped, unconditional loads: see seq_load
-  asm volatile("" : "+v"(rr));       // vector loads on purpose: see seq_load
-  row.rec = w.recs[rr];
-  const uint64_t le = uint64_t(((rr / SQW) & 1) * SQW + rr % SQW);
-  row.cnt = w.l_cnt[le];
+  const int32_t x = (r < re ? r : re - 1) - sg.bs;  // clamped, unconditional loads: see seq_load
+  row.rec = sg.rec[x];
+  row.cnt = sg.cnt[x];
 #pragma unroll
   for (int h = 0; h < SQE; ++h) {
-    row.inst[h] = w.l_inst[le * SQK + lane + 64 * h];
-    row.cst[h] = w.l_cst[le * SQK + lane + 64 * h];
+    row.inst[h] = sg.inst[x * SQK + lane + 64 * h];
+    row.cst[h] = sg.cst[x * SQK + lane + 64 * h];
   }
 }
 
@@ -1039,11 +1108,11 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
   }
   const int32_t prev = uni(row.rec.prev);
   const bool cached = flags & 2, follow_up = flags & 4, prev_cand = flags & 8;
-  const bool slack_inf = p.slack_den == 0;
   // the listed instances' queues and counts are read with prev's queue, before the branch
   const int32_t start = uni(row.rec.start);
   const int32_t cnt = uni(int32_t(row.cnt));
   const i128 q_prev = q2[prev];
+  const uint32_t n_prev = nr[prev];
   i128 a[SQE];
   uint32_t n[SQE], d[SQE];
   bool v[SQE], wide = false;
@@ -1056,16 +1125,18 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     d[h] = uint32_t(i >= start ? i - start : i - start + I);
     wide |= v[h] && (a[h] >> 64) != 0;
   }
-  const bool meets_prev = slack_inf || (q_prev + row.rec.cost_prev) * p.slack_den <= row.rec.bound;
+  const bool meets_prev = q_prev <= row.rec.thr;
   int32_t t;
   uint8_t br;
-  bool mine;     // this lane adds the request to t's queue and count
-  i128 cost = 0;
+  bool mine;  // this lane writes t's new queue and count (values it already holds)
+  i128 q_new = 0;
+  uint32_t n_new = 0;
   if (follow_up && cached && meets_prev && prev_cand) {
     t = prev;
     br = SMETRIC_STICK;
     mine = lane == 0;
-    cost = row.rec.cost_prev;
+    q_new = q_prev + row.rec.cost_prev;
+    n_new = n_prev + 1;
   } else {
     int32_t dmin;
     if (__ballot(wide) == 0) {  // every listed queue below 2^64: scores below 2^96, two words
@@ -1106,15 +1177,16 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     mine = false;
 #pragma unroll
     for (int h = 0; h < SQE; ++h)
-      if (lane + 64 * h < cnt && int32_t(row.inst[h]) == t) {
+      if (v[h] && int32_t(row.inst[h]) == t) {
         mine = true;
-        cost = row.cst[h];
+        q_new = a[h];  // its queue plus the request's cost there
+        n_new = n[h] + 1;
       }
   }
   __builtin_amdgcn_wave_barrier();
   if (mine) {  // one lane: the listed instances are distinct
-    q2[t] += cost;
-    nr[t] += 1;
+    q2[t] = q_new;
+    nr[t] = n_new;
     target[r] = t;
     branch[r] = br;
   }
@@ -1129,12 +1201,11 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
 // After two steps that settle nothing, the next 64 requests go one by one with their
 // records and lists loaded D requests ahead.
 template <int D>
-__device__ __forceinline__ void seqc_decide_block(int32_t bs, int32_t be, int32_t I, const RouteParams &p,
-                                                  const SeqCWs &w, i128 *q2, uint32_t *nr, uint32_t *n_on,
+__device__ __forceinline__ void seqc_decide_block(int32_t be, int32_t I, const RouteParams &p, const SeqCStage &sg,
+                                                  bool st_ok, i128 *q2, uint32_t *nr, uint32_t *n_on,
                                                   int32_t *__restrict__ target, uint8_t *__restrict__ branch) {
   const int lane = threadIdx.x & 63;
-  const bool st_ok = *w.st != 0;
-  const bool slack_inf = p.slack_den == 0;
+  const int32_t bs = sg.bs;
   int32_t r0 = bs;
   int streak = 0;
   while (r0 < be) {
@@ -1145,12 +1216,12 @@ __device__ __forceinline__ void seqc_decide_block(int32_t bs, int32_t be, int32_
       // waited for at the join
       SeqLRow ring[D];
 #pragma unroll
-      for (int d = 0; d < D; ++d) seqc_lrow_load(r0 + d, be, w, ring[d]);
+      for (int d = 0; d < D; ++d) seqc_lrow_load(r0 + d, be, sg, ring[d]);
       for (int32_t r = r0; r < re; r += D) {
 #pragma unroll
         for (int d = 0; d < D; ++d) {
           if (r + d < re) seqc_list_decide(ring[d], r + d, I, p, st_ok, q2, nr, target, branch);
-          seqc_lrow_load(r + d + D, be, w, ring[d]);
+          seqc_lrow_load(r + d + D, be, sg, ring[d]);
         }
       }
       r0 = re;
@@ -1159,9 +1230,7 @@ __device__ __forceinline__ void seqc_decide_block(int32_t bs, int32_t be, int32_
     }
     const int32_t nv = be - r0 < 64 ? be - r0 : 64;
     const int32_t r = r0 + lane;
-    int32_t rv = r < be ? r : be - 1;
-    asm volatile("" : "+v"(rv));  // a vector load: see seq_load
-    const SeqCRec rec = w.recs[rv];
+    const SeqCRec rec = sg.rec[(r < be ? r : be - 1) - bs];
     const bool in = lane < nv;
     const bool ok = st_ok && (rec.flags & 1);
     const bool sticky = ok && (rec.flags & 2) && (rec.flags & 4) && (rec.flags & 8);
@@ -1192,14 +1261,14 @@ __device__ __forceinline__ void seqc_decide_block(int32_t bs, int32_t be, int32_
     const i128 q_prev = (mine ? q2[prev] : i128(0)) + excl;
     bool settled = !ok;  // out of domain: settled, nothing queued
     uint8_t br = SMETRIC_INVALID;
-    if (sticky && (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound)) {
+    if (sticky && q_prev <= rec.thr) {
       settled = true;
       br = SMETRIC_STICK;
     }
     const uint64_t open = __ballot(in && !settled);
     const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
     SeqLRow row;
-    if (f < nv) seqc_lrow_load(r0 + f, be, w, row);
+    if (f < nv) seqc_lrow_load(r0 + f, be, sg, row);
     if (lane < f) {
       target[r] = ok ? prev : -1;
       branch[r] = br;
@@ -1226,13 +1295,15 @@ __device__ __forceinline__ void seqc_decide_block(int32_t bs, int32_t be, int32_
 
 // Launch L: workgroup 0 decides block L-1 (L >= 1) and writes X_{L+1}; workgroups 1 ..
 // rank the requests of block L (L < number of blocks).
+constexpr int SQ_STAGE_WORDS = (SQW * SQK * 16 + SQW * int(sizeof(SeqCRec)) + SQW * SQK * 4 + SQW * 4 + 7) / 8;
 __global__ __launch_bounds__(SQT) void route_seqc_block_kernel(int32_t L, const int32_t *__restrict__ matched,
                                                                int32_t n_req, int32_t I,
                                                                const int64_t *__restrict__ slack, RouteParams p,
                                                                SeqCWs w, int32_t *__restrict__ target,
                                                                uint8_t *__restrict__ branch) {
-  // ranking: three key words per instance; deciding: queues (16 B), counts and step counters
-  __shared__ uint64_t smem[3 * SQ_NP];
+  // deciding: queues (16 B), counts and step counters per instance, then block L-1 staged
+  // (costs, records, instances, counts); ranking: the merge buffer
+  __shared__ uint64_t smem[3 * SQ_NP + SQ_STAGE_WORDS];
   if (blockIdx.x > 0) {
     seqc_rank(L, matched, n_req, I, slack, p, w, smem);
     return;
@@ -1240,16 +1311,30 @@ __global__ __launch_bounds__(SQT) void route_seqc_block_kernel(int32_t L, const 
   i128 *q2 = reinterpret_cast<i128 *>(smem);
   uint32_t *nr = reinterpret_cast<uint32_t *>(smem + 2 * SQ_NP);
   uint32_t *n_on = nr + SQ_NP;
+  i128 *s_cst = reinterpret_cast<i128 *>(smem + 3 * SQ_NP);
+  SeqCRec *s_rec = reinterpret_cast<SeqCRec *>(s_cst + SQW * SQK);
+  uint32_t *s_inst = reinterpret_cast<uint32_t *>(s_rec + SQW);
+  uint32_t *s_cnt = s_inst + SQW * SQK;
   const uint64_t sx = uint64_t(L & 1) * I, sy = uint64_t((L + 1) & 1) * I;
   for (int32_t i = threadIdx.x; i < I; i += SQT) {
     q2[i] = w.q2[sx + i];
     nr[i] = w.nr[sx + i];
     n_on[i] = 0;
   }
+  const int32_t bs = (L - 1) * SQW, nb = L >= 1 ? (n_req - bs < SQW ? n_req - bs : SQW) : 0;
+  const uint64_t le0 = uint64_t(((L - 1) & 1) * SQW);
+  for (int32_t x = threadIdx.x; x < nb * SQK; x += SQT) {
+    s_inst[x] = w.l_inst[le0 * SQK + x];
+    s_cst[x] = w.l_cst[le0 * SQK + x];
+  }
+  for (int32_t x = threadIdx.x; x < nb; x += SQT) {
+    s_rec[x] = w.recs[bs + x];
+    s_cnt[x] = w.l_cnt[le0 + x];
+  }
   __syncthreads();
   if (L >= 1 && threadIdx.x < 64) {
-    const int32_t bs = (L - 1) * SQW, be = n_req - bs < SQW ? n_req : bs + SQW;
-    seqc_decide_block<3>(bs, be, I, p, w, q2, nr, n_on, target, branch);
+    const SeqCStage sg{bs, s_rec, s_cnt, s_inst, s_cst};
+    seqc_decide_block<3>(bs + nb, I, p, sg, *w.st != 0, q2, nr, n_on, target, branch);
   }
   __syncthreads();
   for (int32_t i = threadIdx.x; i < I; i += SQT) {
