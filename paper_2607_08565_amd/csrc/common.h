@@ -16,26 +16,44 @@ constexpr int BUCKET_WORDS = 2 * SLOTS;  // u64 words per bucket
 constexpr uint32_t SESSION_LIMIT = 1u << 24;
 constexpr uint32_t EPOCH_LIMIT = 1u << 22;
 
-// Entry value (64 bits): instance:16 | kind:2 | epoch:22 | session:24.
-// HEADER values hold a pool record index in the low 46 bits instead.
+// Entry value (64 bits): epoch:22 | kind:2 | instance:16 | session:24.  The high 32-bit
+// word is epoch:22 | kind:2 | the instance's high byte, so raising an entry's epoch to
+// max(old, e) is one 32-bit atomic maximum on that word, without reading it first: the
+// caller knows the entry's kind and instance, which are the same in both operands.
+// HEADER values hold a pool record index in the low 40 bits instead (epoch 0).
 enum Kind : uint32_t { PLAIN = 0, HEADER = 1, MEMBER = 2 };
 
 __host__ __device__ inline uint64_t make_val(uint32_t inst, uint32_t kind, uint32_t epoch,
                                              uint32_t session) {
-  return (uint64_t(inst) << 48) | (uint64_t(kind) << 46) | (uint64_t(epoch) << 24) |
-         uint64_t(session);
+  return (uint64_t(epoch) << 42) | (uint64_t(kind) << 40) | (uint64_t(inst) << 24) | uint64_t(session);
 }
-__host__ __device__ inline uint32_t val_inst(uint64_t v) { return uint32_t(v >> 48); }
-__host__ __device__ inline uint32_t val_kind(uint64_t v) { return uint32_t(v >> 46) & 3u; }
-__host__ __device__ inline uint32_t val_epoch(uint64_t v) { return uint32_t(v >> 24) & 0x3FFFFFu; }
-__host__ __device__ inline uint64_t val_rec(uint64_t v) { return v & ((uint64_t(1) << 46) - 1); }
-__host__ __device__ inline uint64_t header_val(uint64_t rec) { return (uint64_t(HEADER) << 46) | rec; }
+__host__ __device__ inline uint32_t val_inst(uint64_t v) { return uint32_t(v >> 24) & 0xFFFFu; }
+__host__ __device__ inline uint32_t val_kind(uint64_t v) { return uint32_t(v >> 40) & 3u; }
+__host__ __device__ inline uint32_t val_epoch(uint64_t v) { return uint32_t(v >> 42); }
+__host__ __device__ inline uint32_t val_session(uint64_t v) { return uint32_t(v) & 0xFFFFFFu; }
+__host__ __device__ inline uint64_t val_rec(uint64_t v) { return v & ((uint64_t(1) << 40) - 1); }
+__host__ __device__ inline uint64_t header_val(uint64_t rec) { return (uint64_t(HEADER) << 40) | rec; }
+// v with its epoch replaced by max(its epoch, e)
+__host__ __device__ inline uint64_t val_raise_epoch(uint64_t v, uint32_t e) {
+  return val_epoch(v) < e ? (v & ((uint64_t(1) << 42) - 1)) | (uint64_t(e) << 42) : v;
+}
+// The same on the table, for an entry of the given kind and instance: one atomic on the
+// value's high word (other fields of that word unchanged, the session word untouched).
+__device__ __forceinline__ void raise_epoch_at(uint64_t *vp, uint32_t kind, uint32_t inst, uint32_t e) {
+  atomicMax(reinterpret_cast<unsigned int *>(vp) + 1, (e << 10) | (kind << 8) | (inst >> 8));
+}
 // Value word of an EMPTY slot (kind 3, which no entry has): a slot whose key was just
 // claimed still shows it until its claimant writes the value, so another placer walking
 // the chain never takes it for an entry.
-constexpr uint64_t VAL_UNSET = uint64_t(3) << 46;
-// value with the kind bits cleared: the dump layout inst << 48 | epoch << 24 | session
-__host__ __device__ inline uint64_t val_plain(uint64_t v) { return v & ~(uint64_t(3) << 46); }
+constexpr uint64_t VAL_UNSET = uint64_t(3) << 40;
+// The dump's value layout (instance << 48 | epoch << 24 | session), also the layout of the
+// gathered entries that eviction selects on and rebuilds from.
+__host__ __device__ inline uint64_t val_dump(uint64_t v) {
+  return (uint64_t(val_inst(v)) << 48) | (uint64_t(val_epoch(v)) << 24) | val_session(v);
+}
+__host__ __device__ inline uint32_t dump_inst(uint64_t d) { return uint32_t(d >> 48); }
+__host__ __device__ inline uint32_t dump_epoch(uint64_t d) { return uint32_t(d >> 24) & 0x3FFFFFu; }
+__host__ __device__ inline uint32_t dump_session(uint64_t d) { return uint32_t(d) & 0xFFFFFFu; }
 
 // Device-resident counters, first 256 bytes of the index buffer.
 struct IndexHdr {

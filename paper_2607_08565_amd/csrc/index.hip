@@ -258,11 +258,11 @@ __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool w
   return c;
 }
 
-// epoch = max(old, epoch) of the entry at `slot`, session kept (an existing pair).
-__device__ __forceinline__ void refresh_at(const DevIndex &ix, int64_t slot, uint32_t epoch) {
-  uint64_t *vp = val_ptr(ix, slot);
-  const uint64_t v = *vp;
-  if (val_epoch(v) < epoch) *vp = (v & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+// epoch = max(old, epoch) of the entry at `slot` (kind and instance given), session kept
+// (an existing pair).
+__device__ __forceinline__ void refresh_at(const DevIndex &ix, int64_t slot, uint32_t kind, uint32_t inst,
+                                           uint32_t epoch) {
+  raise_epoch_at(val_ptr(ix, slot), kind, inst, epoch);
 }
 
 // Enter a pair that is not known to be an entry (one per pair and call: pairs are
@@ -277,7 +277,7 @@ __device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32
   const Claim c = claim_slot(ix, home_bucket(key, ix.n_buckets), key, true,
                              capped ? uint32_t(ix.threshold) + 1 : 0xFFFFFFFFu, inst);
   if (c.existing >= 0) {
-    refresh_at(ix, c.existing, epoch);
+    refresh_at(ix, c.existing, PLAIN, inst, epoch);
     return REFRESHED;
   }
   if (c.header >= 0) {
@@ -287,7 +287,7 @@ __device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32
     if ((old >> (inst & 63)) & 1) {  // already a member
       const Found f = find_member(ix, key, inst);
       if (f.slot < 0) return FAILED;
-      refresh_at(ix, f.slot, epoch);
+      refresh_at(ix, f.slot, MEMBER, inst, epoch);
       return REFRESHED;
     }
     const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, false);
@@ -333,7 +333,7 @@ __device__ bool spill_key(const DevIndex &ix, uint64_t key) {
       bm[inst >> 6] |= 1ull << (inst & 63);
       const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, false);
       if (m.slot < 0) return false;
-      *val_ptr(ix, m.slot) = make_val(inst, MEMBER, val_epoch(v), uint32_t(v & 0xFFFFFF));
+      *val_ptr(ix, m.slot) = make_val(inst, MEMBER, val_epoch(v), val_session(v));
       if (first < 0) {
         first = int64_t(b * SLOTS + s);
         bk[SLOTS + s] = header_val(rec);
@@ -649,7 +649,7 @@ __global__ __launch_bounds__(64 * IW) void ins_refresh_kernel(DevIndex ix, InsWs
     if (!p) continue;
     uint64_t *vp = val_ptr(ix, int64_t(p - 1));
     const uint64_t v = *vp;
-    if (val_epoch(v) < epoch) *vp = (v & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+    if (val_epoch(v) < epoch) *vp = val_raise_epoch(v, epoch);
   }
 }
 
@@ -837,15 +837,12 @@ __global__ __launch_bounds__(TB) void insp_classify_kernel(DevIndex ix, ProbeVie
       }
     }
     if (inl) {
-      // epoch = max(old, epoch): every value requested before any is written back (a
-      // position without an entry reads slot 0's value, always present, and drops it)
-      uint64_t v[CU];
-#pragma unroll
-      for (int u = 0; u < CU; ++u) v[u] = *val_ptr(ix, slot[u] >= 0 ? slot[u] : 0);
+      // epoch = max(old, epoch) without a read: the entry is (key, t), a member for a HOT
+      // key and a plain slot otherwise
 #pragma unroll
       for (int u = 0; u < CU; ++u)
-        if (slot[u] >= 0 && val_epoch(v[u]) < epoch)
-          *val_ptr(ix, slot[u]) = (v[u] & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+        if (slot[u] >= 0)
+          raise_epoch_at(val_ptr(ix, slot[u]), desc_kind(d[u]) == D_HOT ? MEMBER : PLAIN, uint32_t(t[u]), epoch);
     } else {
 #pragma unroll
       for (int u = 0; u < CU; ++u)
@@ -1262,7 +1259,7 @@ __global__ __launch_bounds__(TB) void insp_refresh_kernel(DevIndex ix, ProbeView
     if (!p) continue;
     uint64_t *vp = val_ptr(ix, int64_t(p - 1));
     const uint64_t v = *vp;
-    if (val_epoch(v) < epoch) *vp = (v & ~(uint64_t(0x3FFFFF) << 24)) | (uint64_t(epoch) << 24);
+    if (val_epoch(v) < epoch) *vp = val_raise_epoch(v, epoch);
   }
 }
 
@@ -1390,7 +1387,7 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
         if ((live >> (g * SLOTS + s)) & 1) {
           if (at < cap) {
             keys[at] = k[g][s];
-            vals[at] = val_plain(v[g][s]);
+            vals[at] = val_dump(v[g][s]);
             if (pos)
               pos[at] = ((b0 + uint64_t(threadIdx.x) * GB + g) * SLOTS + s) |
                         (uint64_t(val_kind(v[g][s]) == MEMBER) << 63);
@@ -1451,7 +1448,7 @@ struct SelPrefix {
   uint32_t digit[SEL_LEVELS];
 };
 __device__ __forceinline__ uint32_t sel_digit(uint64_t key, uint64_t v, int l) {
-  const uint32_t ep = uint32_t(v >> 24) & 0x3FFFFFu, inst = uint32_t(v >> 48);
+  const uint32_t ep = dump_epoch(v), inst = dump_inst(v);
   switch (l) {
     case 0: return ep >> 11;
     case 1: return ep & 0x7FFu;
@@ -1522,7 +1519,7 @@ __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const ui
     for (int j = 0; j < RS; ++j) {
       if (((want >> j) & 1) && sel_cmp(k[j], v[j], cut) > 0) {
         bool t;
-        const int pl = place_new(ix, k[j], val_inst(v[j]), val_epoch(v[j]), uint32_t(v[j] & 0xFFFFFF), t, true);
+        const int pl = place_new(ix, k[j], dump_inst(v[j]), dump_epoch(v[j]), dump_session(v[j]), t, true);
         if (pl == FAILED || pl == REFRESHED) set_status(ix.hdr, SMETRIC_EINTERNAL);  // survivors are distinct
         else if (pl == DEFERRED) dmask |= 1u << j;
         else if (t) tmask |= 1u << j;
@@ -1598,7 +1595,7 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
           used |= 1u << s;
           const int bk = 2 * t + s / SLOTS;
           tb[bk * BUCKET_WORDS + s % SLOTS] = k[u];
-          tb[bk * BUCKET_WORDS + SLOTS + s % SLOTS] = v[u];  // a plain value (kind bits 0)
+          tb[bk * BUCKET_WORDS + SLOTS + s % SLOTS] = make_val(dump_inst(v[u]), PLAIN, dump_epoch(v[u]), dump_session(v[u]));
           if (s / SLOTS > uint32_t(h - mine)) dm |= 2u;  // from bucket mine into mine + 1: displacement 1
           placed = true;
         }
@@ -1644,7 +1641,7 @@ __global__ void deferred_kernel(DevIndex ix, const uint64_t *items, const unsign
       pl = place_new(ix, d.key, dd_inst(d.w2), epoch, session[dd_req(d.w2)], trig, false);
     } else {
       const uint64_t v = vals[t];
-      pl = place_new(ix, keys[t], val_inst(v), val_epoch(v), uint32_t(v & 0xFFFFFF), trig, false);
+      pl = place_new(ix, keys[t], dump_inst(v), dump_epoch(v), dump_session(v), trig, false);
     }
     if (pl == REFRESHED && !np && !via) pl = FAILED;  // rebuild survivors are distinct
     if (pl != PLACED && pl != REFRESHED) set_status(ix.hdr, SMETRIC_EINTERNAL);
@@ -1677,7 +1674,7 @@ __global__ __launch_bounds__(TB) void evict_tomb_kernel(DevIndex ix, const uint6
         continue;
       }
       const uint64_t rec = val_rec(*val_ptr(ix, h));
-      const uint32_t inst = val_inst(v);
+      const uint32_t inst = dump_inst(v);
       atomicAnd(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
                 ~(1ull << (inst & 63)));
     }
