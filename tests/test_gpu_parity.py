@@ -676,3 +676,37 @@ def test_probe_bound_small_and_empty_requests():
     assert pair.oix.insert(okeys, blk_off, ot, b.session, b.epoch) == 0
     pair.compare_index("small and empty requests")
     say(f"  blocks {nb}, probed {probed}, search probes {searched}")
+
+
+@pytest.mark.parametrize("I,holders", [(4096, [4095, 2055, 300]), (65536, [65535, 40000, 256])])
+def test_refresh_raises_epochs_of_high_instances(I, holders):
+    """Refreshes of existing entries on instances whose id has a high byte (the refresh is
+    a 32-bit atomic maximum over the value's epoch, kind and instance high byte): plain
+    entries and, with I = 4096, bitmap members of a prefix held by more instances than the
+    spill threshold; epochs raised on the probed path, then to the largest epoch on the
+    self-contained insert, then an older epoch that changes nothing.  Every dump equals
+    the oracle's."""
+    rng = np.random.default_rng(17 + I)
+    pair = Pair(100_000, I)
+    pre = rng.integers(0, W.VOCAB, 16 * 32, dtype=np.int32)
+    n0 = 48
+    others = [i for i in rng.choice(I, n0 + len(holders), replace=False) if i not in holders][: n0 - len(holders)]
+    inst = np.array(list(holders) + others, np.int32)
+    tails = [rng.integers(0, W.VOCAB, 16 * 6, dtype=np.int32) for _ in range(n0)]
+    prompts = [np.concatenate([pre, t]) for t in tails]
+    off = np.zeros(n0 + 1, np.int64)
+    off[1:] = np.cumsum([len(p) for p in prompts])
+    d_boff, nb, d_keys, okeys, blk_off = pair.hash_both(np.concatenate(prompts), off)
+    assert pair.insert_both(d_keys, d_boff, nb, okeys, blk_off, inst, np.arange(n0), 5) == 0
+    pair.compare_index("entered")
+    # follow-ups of the holders' sessions: each sticks to its own instance (q = 0)
+    k = len(holders)
+    fol = [np.concatenate([prompts[j], rng.integers(0, W.VOCAB, 40, dtype=np.int32)]) for j in range(k)]
+    foff = np.zeros(k + 1, np.int64)
+    foff[1:] = np.cumsum([len(p) for p in fol])
+    for epoch, probed in [(1000, True), ((1 << 22) - 1, False), (7, True)]:
+        b = W.Batch(tokens=np.concatenate(fol), tok_off=foff, prompt_len=np.diff(foff).astype(np.int32),
+                    hist_len=np.diff(off)[:k].astype(np.int32), turn=np.ones(k, np.int32),
+                    session=np.arange(k, dtype=np.uint32), q=np.zeros(I, np.int64), rr_base=0, epoch=epoch)
+        ot, ob = pair.step(b, what=f"epoch {epoch}", probed=probed)
+        assert list(ot) == list(holders), f"targets {list(ot)}"
