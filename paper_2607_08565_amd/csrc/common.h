@@ -184,13 +184,11 @@ __device__ __forceinline__ uint32_t mask_get(const DevIndex &ix, uint64_t h) {
   const uint32_t byte = ix.mask[h * MASK_BITS / 8];
   return (byte >> ((h % (8 / MASK_BITS)) * MASK_BITS)) & MASK_ONES;
 }
-// Records a claim in bucket b by a walk from h (nothing for h itself): one atomic only
-// when the bit is new.
+// Records a claim in bucket b by a walk from h (nothing for h itself): one atomic OR.
 __device__ __forceinline__ void mask_note(const DevIndex &ix, uint64_t h, uint64_t b) {
   const uint64_t d = b >= h ? b - h : b + ix.n_buckets - h;
   if (d == 0) return;
   const uint32_t bit = d < MASK_BITS ? 1u << d : MASK_FARBIT;
-  if (mask_get(ix, h) & bit) return;
   atomicOr(reinterpret_cast<unsigned int *>(ix.mask) + h / MASK_PER_WORD, bit << ((h % MASK_PER_WORD) * MASK_BITS));
 }
 
