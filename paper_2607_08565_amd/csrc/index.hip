@@ -135,7 +135,7 @@ struct Found {
 
 // Find the entry (key, inst), looking through a bitmap record when the key has one.
 __device__ Found find_member(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  ChainWalk w = chain_start(member_bucket(key, inst, ix.n_buckets, ix.nb_inv));
+  ChainWalk w = chain_start(member_bucket(key, inst, ix.n_buckets, ix.nb_inv), member_cls(key, inst));
   bool had_empty;
   do {
     const uint64_t m = w.b;
@@ -154,7 +154,7 @@ __device__ Found find_member(const DevIndex &ix, uint64_t key, uint32_t inst) {
 }
 
 __device__ Found find_entry(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets));
+  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets), key_cls(key));
   bool had_empty;
   do {
     const uint64_t b = w.b;
@@ -201,7 +201,7 @@ struct Claim {
   bool capped;
 };
 constexpr uint32_t NO_INST = 0xFFFFFFFFu;
-__device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool want_header,
+__device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, uint32_t cls, bool want_header,
                             uint32_t max_same = 0xFFFFFFFFu, uint32_t want_inst = NO_INST) {
   Claim c{-1, -1, -1, 0, false};
   const uint64_t h = b;  // the chain start whose displacement mask records the claim
@@ -243,7 +243,7 @@ __device__ Claim claim_slot(const DevIndex &ix, uint64_t b, uint64_t key, bool w
       const uint64_t k = atomicCAS(reinterpret_cast<unsigned long long *>(&bk[s]), KEY_EMPTY, key);
       if (k == KEY_EMPTY) {
         c.slot = int64_t(b * SLOTS + s);
-        mask_note(ix, h, b);
+        mask_note(ix, h, b, cls);
         return c;
       }
       if (k == key) {  // claimed meanwhile by another pair of the same key (never this pair)
@@ -274,7 +274,7 @@ enum Placed { PLACED = 0, DEFERRED = 1, FAILED = 2, REFRESHED = 3 };
 __device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32_t epoch, uint32_t sess,
                          bool &trigger, bool capped) {
   trigger = false;
-  const Claim c = claim_slot(ix, home_bucket(key, ix.n_buckets), key, true,
+  const Claim c = claim_slot(ix, home_bucket(key, ix.n_buckets), key, key_cls(key), true,
                              capped ? uint32_t(ix.threshold) + 1 : 0xFFFFFFFFu, inst);
   if (c.existing >= 0) {
     refresh_at(ix, c.existing, PLAIN, inst, epoch);
@@ -290,7 +290,7 @@ __device__ int place_new(const DevIndex &ix, uint64_t key, uint32_t inst, uint32
       refresh_at(ix, f.slot, MEMBER, inst, epoch);
       return REFRESHED;
     }
-    const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, false);
+    const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, member_cls(key, inst), false);
     if (m.slot < 0) return FAILED;
     *val_ptr(ix, m.slot) = make_val(inst, MEMBER, epoch, sess);
     return PLACED;
@@ -331,7 +331,7 @@ __device__ bool spill_key(const DevIndex &ix, uint64_t key) {
       if (val_kind(v) != PLAIN) continue;
       const uint32_t inst = val_inst(v);
       bm[inst >> 6] |= 1ull << (inst & 63);
-      const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, false);
+      const Claim m = claim_slot(ix, member_bucket(key, inst, ix.n_buckets, ix.nb_inv), key, member_cls(key, inst), false);
       if (m.slot < 0) return false;
       *val_ptr(ix, m.slot) = make_val(inst, MEMBER, val_epoch(v), val_session(v));
       if (first < 0) {
@@ -712,7 +712,7 @@ __global__ void spill_kernel(DevIndex ix, const uint64_t *trig, const unsigned l
 // find_member with each bucket read whole (keys and values in one 128-byte request), so
 // a chain step is one round trip.
 __device__ Found find_member_line(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  ChainWalk cw = chain_start(member_bucket(key, inst, ix.n_buckets, ix.nb_inv));
+  ChainWalk cw = chain_start(member_bucket(key, inst, ix.n_buckets, ix.nb_inv), member_cls(key, inst));
   bool had_empty;
   do {
     const uint64_t m = cw.b;
@@ -1579,7 +1579,7 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
   }
   const uint64_t mine = b_lo + 2 * uint64_t(t);  // first of this thread's buckets
   uint32_t used = 0;  // occupancy of the 16 slots of the thread's two buckets
-  uint32_t dm = 0;    // displacement masks of the two buckets (byte 0: mine, byte 1: mine + 1)
+  uint32_t dm = 0;    // displacement mask of bucket mine (mine + 1 gets none from the tile)
 #pragma unroll
   for (int u = 0; u < ME; ++u) {
     if (uint32_t(u) >= n_mine) break;
@@ -1596,7 +1596,7 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
           const int bk = 2 * t + s / SLOTS;
           tb[bk * BUCKET_WORDS + s % SLOTS] = k[u];
           tb[bk * BUCKET_WORDS + SLOTS + s % SLOTS] = make_val(dump_inst(v[u]), PLAIN, dump_epoch(v[u]), dump_session(v[u]));
-          if (s / SLOTS > uint32_t(h - mine)) dm |= 2u;  // from bucket mine into mine + 1: displacement 1
+          if (s / SLOTS > uint32_t(h - mine)) dm |= 1u << (2 * key_cls(k[u]));  // from mine into mine + 1
           placed = true;
         }
       }
@@ -1605,11 +1605,12 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
       pos[seg + j_lo + u] = (b_lo * SLOTS + (e & 0x7FFFu)) | (uint64_t(e >> 15) << 63) | (uint64_t(1) << 62);
   }
   // the two buckets' masks restart from what the tile places; the claim pass adds the rest
-  if (MASK_BITS == 8) {
-    if (mine + 1 < ix.n_buckets) *reinterpret_cast<uint16_t *>(ix.mask + mine) = uint16_t(dm);
+  if (MASK_W == 16) {
+    if (mine + 1 < ix.n_buckets) reinterpret_cast<uint32_t *>(ix.mask)[mine / 2] = dm;  // mine is even
+    else if (mine < ix.n_buckets) reinterpret_cast<uint16_t *>(ix.mask)[mine] = uint16_t(dm);
+  } else {
+    if (mine + 1 < ix.n_buckets) reinterpret_cast<uint16_t *>(ix.mask)[mine / 2] = uint16_t(dm);
     else if (mine < ix.n_buckets) ix.mask[mine] = uint8_t(dm);
-  } else if (mine < ix.n_buckets) {  // mine is even: the two buckets share one byte
-    ix.mask[mine * MASK_BITS / 8] = uint8_t(dm & MASK_ONES);
   }
   __syncthreads();
   const uint64_t nb = ix.n_buckets - b_lo < uint64_t(RT) ? ix.n_buckets - b_lo : uint64_t(RT);

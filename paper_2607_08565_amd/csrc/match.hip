@@ -52,7 +52,7 @@ __device__ Holders probe(const DevIndex &ix, uint64_t key) {
 #pragma unroll
   for (int i = 0; i < LIST_MAX; ++i) H.h[i] = 0xFFFFFFFFu;
   uint32_t cnt = 0;
-  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets));
+  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets), key_cls(key));
   bool had_empty;
   do {
     const uint64_t *bk = ix.slots + w.b * BUCKET_WORDS;
@@ -91,7 +91,7 @@ __device__ Holders probe(const DevIndex &ix, uint64_t key) {
 
 // Is (key, inst) a plain entry?  Used for LONG holder sets only.
 __device__ bool chain_has(const DevIndex &ix, uint64_t key, uint32_t inst) {
-  ChainWalk cw = chain_start(home_bucket(key, ix.n_buckets));
+  ChainWalk cw = chain_start(home_bucket(key, ix.n_buckets), key_cls(key));
   bool had_empty;
   do {
     const uint64_t *bk = ix.slots + cw.b * BUCKET_WORDS;
@@ -114,7 +114,7 @@ __device__ bool chain_has(const DevIndex &ix, uint64_t key, uint32_t inst) {
 // OR into `m` the bits of every plain holder of `key` that fall in word w.
 __device__ uint64_t chain_word(const DevIndex &ix, uint64_t key, int w) {
   uint64_t m = 0;
-  ChainWalk cw = chain_start(home_bucket(key, ix.n_buckets));
+  ChainWalk cw = chain_start(home_bucket(key, ix.n_buckets), key_cls(key));
   bool had_empty;
   do {
     const uint64_t *bk = ix.slots + cw.b * BUCKET_WORDS;

@@ -242,7 +242,7 @@ constexpr int PROBE_K = 2;  // keys per thread and iteration
 
 // Is `key` in the table at all (any slot of its home chain)?
 __device__ bool key_present(const DevIndex &ix, uint64_t key) {
-  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets));
+  ChainWalk w = chain_start(home_bucket(key, ix.n_buckets), key_cls(key));
   bool had_empty;
   do {
     const BucketScan sc = scan_bucket(ix.slots + w.b * BUCKET_WORDS, key);
@@ -336,7 +336,7 @@ __device__ __forceinline__ void desc_init(DescWalk &w, uint64_t key, uint64_t h)
   w.done = false;
   w.pending = false;
   w.out = 0;
-  w.cw = chain_start(h);
+  w.cw = chain_start(h, key_cls(key));
 }
 
 // Slots of bucket keys kk holding `key` (before the first EMPTY slot) and whether an EMPTY
