@@ -1311,6 +1311,7 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
   __shared__ uint32_t wt[TB / 64];
   __shared__ unsigned long long wg_base;
   __shared__ uint32_t h1[2048];
+  __shared__ uint64_t stage[TB * GB * SLOTS];  // one round's entries, one array at a time
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t per_round = uint64_t(TB) * GB;
   uint32_t tombs = 0, d0_or = 0, d0_and = ~0u;  // the entries' first selection digit (epoch >> 11)
@@ -1379,22 +1380,30 @@ __global__ __launch_bounds__(TB) void gather_kernel(DevIndex ix, uint64_t *keys,
       if (toff) toff[b0 / per_round] = (uint64_t(wg_base) << 16) | total;  // rounds land anywhere
     }
     __syncthreads();
-    unsigned long long at = wg_base + before + x - c;
+    // the round's entries go out through LDS, one array at a time, so that consecutive
+    // lanes write consecutive words (a lane writing its own entries straight out scatters
+    // every store instruction over 64 lines)
+    const uint32_t lo = before + x - c;  // this thread's first entry in the round
+    const unsigned long long base = wg_base;
+    const uint32_t n_out = base >= cap ? 0u : (cap - base < total ? uint32_t(cap - base) : total);
 #pragma unroll
-    for (int g = 0; g < GB; ++g)
+    for (int a = 0; a < 3; ++a) {
+      if (a == 2 && !pos) break;  // uniform
+      uint32_t j = lo;
 #pragma unroll
-      for (int s = 0; s < SLOTS; ++s)
-        if ((live >> (g * SLOTS + s)) & 1) {
-          if (at < cap) {
-            keys[at] = k[g][s];
-            vals[at] = val_dump(v[g][s]);
-            if (pos)
-              pos[at] = ((b0 + uint64_t(threadIdx.x) * GB + g) * SLOTS + s) |
-                        (uint64_t(val_kind(v[g][s]) == MEMBER) << 63);
-          }
-          ++at;
-        }
-    __syncthreads();  // wt and wg_base are reused by the next round
+      for (int g = 0; g < GB; ++g)
+#pragma unroll
+        for (int s = 0; s < SLOTS; ++s)
+          if ((live >> (g * SLOTS + s)) & 1)
+            stage[j++] = a == 0 ? k[g][s]
+                                : (a == 1 ? val_dump(v[g][s])
+                                          : ((b0 + uint64_t(threadIdx.x) * GB + g) * SLOTS + s) |
+                                                (uint64_t(val_kind(v[g][s]) == MEMBER) << 63));
+      __syncthreads();
+      uint64_t *out = a == 0 ? keys : (a == 1 ? vals : pos);
+      for (uint32_t i = threadIdx.x; i < n_out; i += TB) out[base + i] = stage[i];
+      __syncthreads();  // stage, wt and wg_base are reused
+    }
   }
   if (hist1) {
 #pragma unroll
