@@ -1478,66 +1478,31 @@ __device__ __forceinline__ int sel_cmp(uint64_t key, uint64_t v, const SelPrefix
   }
   return 0;
 }
-// Rebuild, claim pass: enter the entries of (keys, vals)[0, n) that lie above the cut
-// (the eviction's selection prefix) and that the tile pass left (bit 62 of their slot
-// word), by claims from their home buckets.  The entries arrive tile by tile in slot
-// order, where neighbours share buckets, so lane l of a wavefront takes a stretch of RS
-// consecutive entries (one 128-byte line of keys and one of values, loaded at once) and
-// places them one after another: the lanes of one step are RS entries apart and rarely
-// race for a bucket, and a lane's writes land in the same few buckets.
-constexpr int RS = 16;
-__global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const uint64_t *vals, uint64_t n,
-                                     SelPrefix cut, const uint64_t *pos, uint64_t *trig, unsigned long long *n_trig,
-                                     uint64_t *def, unsigned long long *n_def, uint64_t cap) {
-  const int lane = threadIdx.x & 63;
-  const uint64_t wave = (uint64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
-  const uint64_t n_waves = (uint64_t(gridDim.x) * blockDim.x) >> 6;
-  for (uint64_t t0 = wave * 64 * RS; t0 < n; t0 += n_waves * 64 * RS) {  // whole wavefronts iterate together
-    const uint64_t base = t0 + uint64_t(lane) * RS;
-    uint32_t want = base < n ? (base + RS <= n ? 0xFFFFu : (1u << (n - base)) - 1u) : 0u;
-    if (pos) {  // only the entries the tile pass left to claims
-      uint32_t w = 0;
-#pragma unroll
-      for (int j = 0; j < RS; ++j) w |= uint32_t(base + j < n && ((pos[base + j] >> 62) & 1)) << j;
-      want &= w;
+// Rebuild, second pass: the entries the tile pass left, listed by their gathered index,
+// one per thread (all survivors: the tile pass skips evicted entries).  Claims that
+// trigger a key's conversion or are deferred are queued by gathered index for the
+// spill and deferred passes.
+__global__ __launch_bounds__(TB) void rebuild_claim_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
+                                                           const uint64_t *__restrict__ vals, const uint64_t *list,
+                                                           const unsigned long long *n_list, uint64_t *trig,
+                                                           unsigned long long *n_trig, uint64_t *def,
+                                                           unsigned long long *n_def, uint64_t cap) {
+  const uint64_t n = *n_list;
+  const uint64_t span = uint64_t(gridDim.x) * TB;
+  for (uint64_t i0 = uint64_t(blockIdx.x) * TB; i0 < n; i0 += span) {  // whole workgroups iterate together
+    const uint64_t i = i0 + threadIdx.x;
+    int64_t tk = -1, df = -1;
+    if (i < n) {
+      const uint64_t t = list[i];
+      const uint64_t k = keys[t], v = vals[t];
+      bool trg;
+      const int pl = place_new(ix, k, dump_inst(v), dump_epoch(v), dump_session(v), trg, true);
+      if (pl == FAILED || pl == REFRESHED) set_status(ix.hdr, SMETRIC_EINTERNAL);  // survivors are distinct
+      else if (pl == DEFERRED) df = int64_t(t);
+      else if (trg) tk = int64_t(t);
     }
-    uint64_t k[RS], v[RS];  // (no early exit: the appends below are wavefront-wide)
-    if (!want) {
-#pragma unroll
-      for (int j = 0; j < RS; ++j) k[j] = v[j] = 0;
-    } else if (base + RS <= n) {
-      const ulonglong2 *pk = reinterpret_cast<const ulonglong2 *>(keys + base);
-      const ulonglong2 *pv = reinterpret_cast<const ulonglong2 *>(vals + base);
-#pragma unroll
-      for (int j = 0; j < RS / 2; ++j) {
-        const ulonglong2 a = pk[j], b = pv[j];
-        k[2 * j] = a.x;
-        k[2 * j + 1] = a.y;
-        v[2 * j] = b.x;
-        v[2 * j + 1] = b.y;
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < RS; ++j) {
-        k[j] = base + j < n ? keys[base + j] : 0;
-        v[j] = base + j < n ? vals[base + j] : 0;
-      }
-    }
-    uint32_t tmask = 0, dmask = 0;  // entries of the stretch that trigger a conversion / are deferred
-#pragma unroll
-    for (int j = 0; j < RS; ++j) {
-      if (((want >> j) & 1) && sel_cmp(k[j], v[j], cut) > 0) {
-        bool t;
-        const int pl = place_new(ix, k[j], dump_inst(v[j]), dump_epoch(v[j]), dump_session(v[j]), t, true);
-        if (pl == FAILED || pl == REFRESHED) set_status(ix.hdr, SMETRIC_EINTERNAL);  // survivors are distinct
-        else if (pl == DEFERRED) dmask |= 1u << j;
-        else if (t) tmask |= 1u << j;
-      }
-    }
-    // one reservation per wavefront and list for the whole tile (deferred entries are
-    // spread over the table, so a reservation per step made one counter the bottleneck)
-    append_wave_mask(n_trig, trig, cap, tmask, base);
-    append_wave_mask(n_def, def, cap, dmask, base);
+    append_wave(n_trig, trig, cap, tk);
+    append_wave(n_def, def, cap, df);
   }
 }
 
@@ -1552,8 +1517,11 @@ __global__ void rebuild_place_kernel(DevIndex ix, const uint64_t *keys, const ui
 // table as before.
 static_assert(GB == 2, "two buckets per thread");
 __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
-                                                          const uint64_t *__restrict__ vals, uint64_t *__restrict__ pos,
-                                                          const uint64_t *__restrict__ toff, SelPrefix cut) {
+                                                          const uint64_t *__restrict__ vals,
+                                                          const uint64_t *__restrict__ pos,
+                                                          const uint64_t *__restrict__ toff, SelPrefix cut,
+                                                          uint64_t *left_list, unsigned long long *n_left,
+                                                          uint64_t cap) {
   constexpr int RT = TB * GB;
   __shared__ uint64_t tb[RT * BUCKET_WORDS];  // the tile: keys, then values, per bucket
   __shared__ uint16_t sp[RT * SLOTS];         // each entry's old slot in the tile (bit 15: a member)
@@ -1589,6 +1557,7 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
   const uint64_t mine = b_lo + 2 * uint64_t(t);  // first of this thread's buckets
   uint32_t used = 0;  // occupancy of the 16 slots of the thread's two buckets
   uint32_t dm = 0;    // displacement mask of bucket mine (mine + 1 gets none from the tile)
+  uint32_t left = 0;  // this thread's surviving entries left to the claim pass
 #pragma unroll
   for (int u = 0; u < ME; ++u) {
     if (uint32_t(u) >= n_mine) break;
@@ -1610,9 +1579,9 @@ __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uin
         }
       }
     }
-    if (!placed)  // for the claim pass
-      pos[seg + j_lo + u] = (b_lo * SLOTS + (e & 0x7FFFu)) | (uint64_t(e >> 15) << 63) | (uint64_t(1) << 62);
+    if (!placed) left |= 1u << u;  // for the claim pass
   }
+  append_wave_mask(n_left, left_list, cap, left, seg + j_lo);
   // the two buckets' masks restart from what the tile places; the claim pass adds the rest
   if (MASK_W == 16) {
     if (mine + 1 < ix.n_buckets) reinterpret_cast<uint32_t *>(ix.mask)[mine / 2] = dm;  // mine is even
@@ -1991,12 +1960,16 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m), 1);
   // tile pass (writes every bucket: no clear needed), then the claims for what it left
   const uint64_t n_tiles = (ix.n_buckets + TB * GB - 1) / (TB * GB);
-  hipLaunchKernelGGL(rebuild_tile_kernel, dim3(n_tiles), dim3(TB), 0, stream, ix, keys, vals, pos, ws.toff, p);
+  uint64_t *left_list = ws.vb;  // free: the entries the tile pass leaves, by gathered index
+  unsigned long long *n_left = ws.count + 7;
+  if ((rc = fill(n_left, 8, 0, stream))) return rc;
+  hipLaunchKernelGGL(rebuild_tile_kernel, dim3(n_tiles), dim3(TB), 0, stream, ix, keys, vals, pos, ws.toff, p,
+                     left_list, n_left, idx->capacity);
   uint64_t *trig = ws.ea;  // free buffers: the conversion queue and the deferred pairs
   unsigned long long *n_trig = ws.count + 1;
   uint64_t *def = ws.ia;
   unsigned long long *n_def = ws.count + 2;
-  hipLaunchKernelGGL(rebuild_place_kernel, dim3(grid_for(n / RS)), dim3(TB), 0, stream, ix, keys, vals, n, p, pos,
+  hipLaunchKernelGGL(rebuild_claim_kernel, dim3(grid_for(n)), dim3(TB), 0, stream, ix, keys, vals, left_list, n_left,
                      trig, n_trig, def, n_def, idx->capacity);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr, nullptr,
                      nullptr);
