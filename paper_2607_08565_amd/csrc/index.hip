@@ -1478,22 +1478,23 @@ __device__ __forceinline__ int sel_cmp(uint64_t key, uint64_t v, const SelPrefix
   }
   return 0;
 }
-// Rebuild, second pass: the entries the tile pass left, listed by their gathered index,
-// one per thread (all survivors: the tile pass skips evicted entries).  Claims that
-// trigger a key's conversion or are deferred are queued by gathered index for the
-// spill and deferred passes.
+// Rebuild, second pass: the entries the tile pass left (tile k's listed by gathered index
+// in list[seg, seg + count), toff[k] = seg << 16 | count), one per thread (all survivors:
+// the tile pass skips evicted entries).  Claims that trigger a key's conversion or are
+// deferred are queued by gathered index for the spill and deferred passes.
 __global__ __launch_bounds__(TB) void rebuild_claim_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
                                                            const uint64_t *__restrict__ vals, const uint64_t *list,
-                                                           const unsigned long long *n_list, uint64_t *trig,
-                                                           unsigned long long *n_trig, uint64_t *def,
+                                                           const uint64_t *__restrict__ toff, uint64_t n_tiles,
+                                                           uint64_t *trig, unsigned long long *n_trig, uint64_t *def,
                                                            unsigned long long *n_def, uint64_t cap) {
-  const uint64_t n = *n_list;
-  const uint64_t span = uint64_t(gridDim.x) * TB;
-  for (uint64_t i0 = uint64_t(blockIdx.x) * TB; i0 < n; i0 += span) {  // whole workgroups iterate together
-    const uint64_t i = i0 + threadIdx.x;
+  for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x)  // whole workgroups iterate together
+  for (uint32_t i0 = 0; i0 < uint32_t(toff[tile] & 0xFFFF); i0 += TB) {
+    const uint64_t seg = toff[tile] >> 16;
+    const uint32_t n = uint32_t(toff[tile] & 0xFFFF);
+    const uint32_t i = i0 + threadIdx.x;
     int64_t tk = -1, df = -1;
     if (i < n) {
-      const uint64_t t = list[i];
+      const uint64_t t = list[seg + i];
       const uint64_t k = keys[t], v = vals[t];
       bool trg;
       const int pl = place_new(ix, k, dump_inst(v), dump_epoch(v), dump_session(v), trg, true);
@@ -1506,92 +1507,127 @@ __global__ __launch_bounds__(TB) void rebuild_claim_kernel(DevIndex ix, const ui
   }
 }
 
-// Rebuild, first pass, without atomics: workgroup k writes the whole of the cleared
-// table's tile k (the gather's round of TB x GB buckets), assembled in LDS.  Thread t owns
-// buckets 2t, 2t + 1 of the tile and takes the survivors whose old slot lay there (the
-// gather wrote each tile's entries in slot order): a plain entry whose home bucket is one
-// of the two goes to the first free slot from its home bucket on, so every slot between
-// its home and its slot is occupied, as linear probing requires.  Everything else --
-// members, entries whose home is elsewhere, a pair of full buckets -- is marked (bit 62 of
-// its slot word) for the claim pass, which enters it from its home bucket in the written
-// table as before.
-static_assert(GB == 2, "two buckets per thread");
+// Rebuild, first pass: workgroup k writes the whole of the cleared table's tile k (the
+// gather's round of TB x GB buckets), assembled in LDS.  The gather wrote each tile's
+// entries in slot order, so the entries whose old slot lay in the tile are one
+// contiguous run.  The surviving plain entries whose home bucket lies in the tile are
+// placed without a walk: with c(b) of them homed at bucket b, home b's entries take the
+// consecutive slots from S(b) on, S(b) = max(SLOTS b, S(b - 1) + c(b - 1)), i.e. with P
+// the exclusive prefix sum of c, S(b) = P(b) + max over j <= b of (SLOTS j - P(j)).  Every
+// slot from an entry's home bucket up to its own is then taken, as linear probing
+// requires, and the class bit of each entry past its home bucket goes into that bucket's
+// mask.  Everything else -- members (a key's plain slots are capped at T + 1 before its
+// conversion, which the claim pass enforces), entries homed in another tile, entries past
+// the tile's last slot -- is listed for the claim pass, which enters it from its home
+// bucket in the written table: tile k's list takes the gathered indexes of its entries'
+// run, left_list[seg, seg + count), and toff[k] becomes seg << 16 | count.
 __global__ __launch_bounds__(TB) void rebuild_tile_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
                                                           const uint64_t *__restrict__ vals,
-                                                          const uint64_t *__restrict__ pos,
-                                                          const uint64_t *__restrict__ toff, SelPrefix cut,
-                                                          uint64_t *left_list, unsigned long long *n_left,
-                                                          uint64_t cap) {
+                                                          const uint64_t *__restrict__ pos, uint64_t *toff,
+                                                          SelPrefix cut, uint64_t *left_list) {
   constexpr int RT = TB * GB;
+  constexpr int PER = RT * SLOTS / TB;  // entries of the run per thread
+  static_assert(RT == 2 * TB, "two buckets per thread in the scans");
   __shared__ uint64_t tb[RT * BUCKET_WORDS];  // the tile: keys, then values, per bucket
-  __shared__ uint16_t sp[RT * SLOTS];         // each entry's old slot in the tile (bit 15: a member)
-  const int t = threadIdx.x;
+  __shared__ uint32_t tm[RT];                 // the tile's displacement masks
+  __shared__ uint32_t hc[RT];                 // entries homed at each bucket, then S(b)
+  __shared__ uint32_t wsum[TB / 64], wmax[TB / 64];
+  __shared__ uint16_t lo[RT * SLOTS];         // the entries left, as offsets in the run
+  __shared__ uint32_t n_lo;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const uint64_t b_lo = uint64_t(blockIdx.x) * RT;
+  const uint64_t nb = ix.n_buckets - b_lo < uint64_t(RT) ? ix.n_buckets - b_lo : uint64_t(RT);
   const uint64_t seg = toff[blockIdx.x] >> 16;
   const uint32_t cnt = uint32_t(toff[blockIdx.x] & 0xFFFF);  // <= RT * SLOTS
   for (int i = t; i < RT * BUCKET_WORDS; i += TB) tb[i] = (i % BUCKET_WORDS) < SLOTS ? KEY_EMPTY : VAL_UNSET;
-  for (uint32_t i = t; i < cnt; i += TB) {
-    const uint64_t ps = pos[seg + i];
-    sp[i] = uint16_t(((ps & ((uint64_t(1) << 62) - 1)) - b_lo * SLOTS) | ((ps >> 63) << 15));
-  }
+  for (int i = t; i < RT; i += TB) tm[i] = hc[i] = 0;
+  if (t == 0) n_lo = 0;
   __syncthreads();
-  auto lower = [&](uint32_t slot) {  // first entry whose old slot in the tile is >= slot
-    uint32_t lo = 0, hi = cnt;
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if ((sp[mid] & 0x7FFFu) < slot) lo = mid + 1;
-      else hi = mid;
-    }
-    return lo;
-  };
-  const uint32_t j_lo = lower(2 * SLOTS * t), n_mine = lower(2 * SLOTS * (t + 1)) - j_lo;  // <= 16
-  // the thread's entries, all loads first (clamped into its range)
-  constexpr int ME = 2 * SLOTS;
-  uint64_t k[ME], v[ME];
+  // thread t takes entries t + TB u of the run: survivors homed in the tile count
+  // themselves at their home (the count is their rank there), the rest are listed
+  uint64_t k[PER], v[PER];
+  uint32_t home[PER], rank[PER];  // home: offset in the tile, RT when not placed here
+  bool member[PER];
 #pragma unroll
-  for (int u = 0; u < ME; ++u) {  // unconditional loads, every index inside the tile's entries
-    const uint32_t j = j_lo + uint32_t(u) < cnt ? j_lo + uint32_t(u) : (cnt ? cnt - 1 : 0);
-    k[u] = keys[seg + j];
-    v[u] = vals[seg + j];
+  for (int u = 0; u < PER; ++u) {  // every load issued before any is used
+    const uint32_t i = uint32_t(u * TB + t), c = i < cnt ? i : 0u;
+    k[u] = keys[seg + c];
+    v[u] = vals[seg + c];
+    member[u] = pos[seg + c] >> 63;
   }
-  const uint64_t mine = b_lo + 2 * uint64_t(t);  // first of this thread's buckets
-  uint32_t used = 0;  // occupancy of the 16 slots of the thread's two buckets
-  uint32_t dm = 0;    // displacement mask of bucket mine (mine + 1 gets none from the tile)
-  uint32_t left = 0;  // this thread's surviving entries left to the claim pass
 #pragma unroll
-  for (int u = 0; u < ME; ++u) {
-    if (uint32_t(u) >= n_mine) break;
-    if (sel_cmp(k[u], v[u], cut) <= 0) continue;  // evicted
-    const uint32_t e = sp[j_lo + u];
-    bool placed = false;
-    if (!(e >> 15)) {
+  for (int u = 0; u < PER; ++u) {
+    const uint32_t i = uint32_t(u * TB + t);
+    home[u] = RT;
+    rank[u] = 0;
+    if (i < cnt && sel_cmp(k[u], v[u], cut) > 0) {  // survives
       const uint64_t h = home_bucket(k[u], ix.n_buckets);
-      if (h >= mine && h < mine + 2) {
-        const uint32_t free = ~used & (0xFFFFu << (uint32_t(h - mine) * SLOTS)) & 0xFFFFu;
-        if (free) {
-          const int s = __builtin_ctz(free);
-          used |= 1u << s;
-          const int bk = 2 * t + s / SLOTS;
-          tb[bk * BUCKET_WORDS + s % SLOTS] = k[u];
-          tb[bk * BUCKET_WORDS + SLOTS + s % SLOTS] = make_val(dump_inst(v[u]), PLAIN, dump_epoch(v[u]), dump_session(v[u]));
-          if (s / SLOTS > uint32_t(h - mine)) dm |= 1u << (2 * key_cls(k[u]));  // from mine into mine + 1
-          placed = true;
-        }
+      if (!member[u] && h >= b_lo && h < b_lo + nb) {
+        home[u] = uint32_t(h - b_lo);
+        rank[u] = atomicAdd(&hc[home[u]], 1u);
+      } else {
+        lo[atomicAdd(&n_lo, 1u)] = uint16_t(i);
       }
     }
-    if (!placed) left |= 1u << u;  // for the claim pass
-  }
-  append_wave_mask(n_left, left_list, cap, left, seg + j_lo);
-  // the two buckets' masks restart from what the tile places; the claim pass adds the rest
-  if (MASK_W == 16) {
-    if (mine + 1 < ix.n_buckets) reinterpret_cast<uint32_t *>(ix.mask)[mine / 2] = dm;  // mine is even
-    else if (mine < ix.n_buckets) reinterpret_cast<uint16_t *>(ix.mask)[mine] = uint16_t(dm);
-  } else {
-    if (mine + 1 < ix.n_buckets) reinterpret_cast<uint16_t *>(ix.mask)[mine / 2] = uint16_t(dm);
-    else if (mine < ix.n_buckets) ix.mask[mine] = uint8_t(dm);
   }
   __syncthreads();
-  const uint64_t nb = ix.n_buckets - b_lo < uint64_t(RT) ? ix.n_buckets - b_lo : uint64_t(RT);
+  // S(b) over the tile: thread t holds buckets 2t, 2t + 1; exclusive sums P and running
+  // maxima of SLOTS j - P(j) across the workgroup (wavefront scans, then the waves' totals)
+  const uint32_t c0 = hc[2 * t], c1 = hc[2 * t + 1];
+  uint32_t sum = c0 + c1;  // inclusive prefix sum over the threads
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(sum, d, 64);
+    if (lane >= d) sum += y;
+  }
+  if (lane == 63) wsum[wave] = sum;
+  __syncthreads();
+  uint32_t before = 0;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  const uint32_t p0 = before + sum - c0 - c1, p1 = p0 + c0;  // P(2t), P(2t + 1)
+  int32_t m = int32_t(SLOTS * 2 * t) - int32_t(p0);
+  const int32_t m1 = int32_t(SLOTS * (2 * t + 1)) - int32_t(p1);
+  m = m1 > m ? m1 : m;  // this thread's maximum; then inclusive running maxima
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int32_t y = __shfl_up(m, d, 64);
+    if (lane >= d && y > m) m = y;
+  }
+  if (lane == 63) wmax[wave] = uint32_t(m);
+  __syncthreads();
+  int32_t mb = INT32_MIN;  // the maximum over the earlier threads
+  for (int w = 0; w < wave; ++w) mb = int32_t(wmax[w]) > mb ? int32_t(wmax[w]) : mb;
+  {
+    const int32_t prev = __shfl_up(m, 1, 64);
+    if (lane > 0 && prev > mb) mb = prev;
+  }
+  const int32_t a0 = int32_t(SLOTS * 2 * t) - int32_t(p0), a1 = int32_t(SLOTS * (2 * t + 1)) - int32_t(p1);
+  const int32_t m0 = a0 > mb ? a0 : mb, m01 = a1 > m0 ? a1 : m0;
+  __syncthreads();  // every c(b) read before S(b) replaces it
+  hc[2 * t] = uint32_t(int32_t(p0) + m0);
+  hc[2 * t + 1] = uint32_t(int32_t(p1) + m01);
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    if (home[u] == RT) continue;
+    const uint32_t at = hc[home[u]] + rank[u];  // slot index in the tile
+    if (at >= uint32_t(nb) * SLOTS) {           // past the tile's last slot
+      lo[atomicAdd(&n_lo, 1u)] = uint16_t(u * TB + t);
+      continue;
+    }
+    const uint32_t b = at / SLOTS, s = at % SLOTS;
+    tb[b * BUCKET_WORDS + s] = k[u];
+    tb[b * BUCKET_WORDS + SLOTS + s] = make_val(dump_inst(v[u]), PLAIN, dump_epoch(v[u]), dump_session(v[u]));
+    if (b > home[u]) atomicOr(&tm[home[u]], 1u << (2 * key_cls(k[u]) + (b == home[u] + 1 ? 0 : 1)));
+  }
+  __syncthreads();
+  const uint32_t n_left = n_lo;
+  for (uint32_t j = t; j < n_left; j += TB) left_list[seg + j] = seg + lo[j];
+  if (t == 0) toff[blockIdx.x] = (seg << 16) | n_left;
+  for (uint64_t i = t; i < nb; i += TB) {
+    if (MASK_W == 16) reinterpret_cast<uint16_t *>(ix.mask)[b_lo + i] = uint16_t(tm[i]);
+    else ix.mask[b_lo + i] = uint8_t(tm[i]);
+  }
   ulonglong2 *dst = reinterpret_cast<ulonglong2 *>(ix.slots + b_lo * BUCKET_WORDS);
   const ulonglong2 *src = reinterpret_cast<const ulonglong2 *>(tb);
   for (uint64_t w = t; w < nb * (BUCKET_WORDS / 2); w += TB) dst[w] = src[w];
@@ -1961,16 +1997,14 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
   // tile pass (writes every bucket: no clear needed), then the claims for what it left
   const uint64_t n_tiles = (ix.n_buckets + TB * GB - 1) / (TB * GB);
   uint64_t *left_list = ws.vb;  // free: the entries the tile pass leaves, by gathered index
-  unsigned long long *n_left = ws.count + 7;
-  if ((rc = fill(n_left, 8, 0, stream))) return rc;
   hipLaunchKernelGGL(rebuild_tile_kernel, dim3(n_tiles), dim3(TB), 0, stream, ix, keys, vals, pos, ws.toff, p,
-                     left_list, n_left, idx->capacity);
+                     left_list);
   uint64_t *trig = ws.ea;  // free buffers: the conversion queue and the deferred pairs
   unsigned long long *n_trig = ws.count + 1;
   uint64_t *def = ws.ia;
   unsigned long long *n_def = ws.count + 2;
-  hipLaunchKernelGGL(rebuild_claim_kernel, dim3(grid_for(n)), dim3(TB), 0, stream, ix, keys, vals, left_list, n_left,
-                     trig, n_trig, def, n_def, idx->capacity);
+  hipLaunchKernelGGL(rebuild_claim_kernel, dim3(n_tiles < MAX_GRID ? n_tiles : MAX_GRID), dim3(TB), 0, stream, ix,
+                     keys, vals, left_list, ws.toff, n_tiles, trig, n_trig, def, n_def, idx->capacity);
   hipLaunchKernelGGL(spill_kernel, dim3(64), dim3(TB), 0, stream, ix, trig, n_trig, nullptr, keys, nullptr, nullptr,
                      nullptr);
   // every member of a key with a bitmap record is deferred here (millions): the full grid
