@@ -1673,48 +1673,59 @@ __global__ void set_counts_kernel(IndexHdr *h, unsigned long long n_entries, int
 // also leaves its key's bitmap); every other entry keeps its slot.  Tombstones are never
 // reclaimed by inserts, so the caller rebuilds the table instead once they would pass an
 // eighth of the slots.
+__device__ void tomb_entry(const DevIndex &ix, uint64_t k, uint64_t v, uint64_t ps) {
+  const uint64_t slot = ps & ~(uint64_t(1) << 63);
+  ix.slots[(slot / SLOTS) * BUCKET_WORDS + slot % SLOTS] = KEY_TOMB;
+  if (ps >> 63) {
+    const int64_t h = find_header(ix, k);
+    if (h < 0) {
+      set_status(ix.hdr, SMETRIC_EINTERNAL);
+      return;
+    }
+    const uint64_t rec = val_rec(*val_ptr(ix, h));
+    const uint32_t inst = dump_inst(v);
+    atomicAnd(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
+              ~(1ull << (inst & 63)));
+  }
+}
 __global__ __launch_bounds__(TB) void evict_tomb_kernel(DevIndex ix, const uint64_t *__restrict__ keys,
                                                         const uint64_t *__restrict__ vals,
                                                         const uint64_t *__restrict__ pos, uint64_t n, SelPrefix cut) {
   const uint64_t stride = uint64_t(gridDim.x) * TB;
   for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += stride) {
     const uint64_t k = keys[i], v = vals[i];
-    if (sel_cmp(k, v, cut) > 0) continue;  // survives
-    const uint64_t ps = pos[i], slot = ps & ~(uint64_t(1) << 63);
-    ix.slots[(slot / SLOTS) * BUCKET_WORDS + slot % SLOTS] = KEY_TOMB;
-    if (ps >> 63) {
-      const int64_t h = find_header(ix, k);
-      if (h < 0) {
-        set_status(ix.hdr, SMETRIC_EINTERNAL);
-        continue;
-      }
-      const uint64_t rec = val_rec(*val_ptr(ix, h));
-      const uint32_t inst = dump_inst(v);
-      atomicAnd(reinterpret_cast<unsigned long long *>(&ix.pool[rec * uint64_t(ix.words) + (inst >> 6)]),
-                ~(1ull << (inst & 63)));
-    }
+    if (sel_cmp(k, v, cut) <= 0) tomb_entry(ix, k, v, pos[i]);  // at or below the cut
   }
 }
 
 // One selection pass: the histogram of the next digit over the entries on the prefix.
 // With ck non-null those entries are also copied to (ck, cv) (in no particular order; the
-// caller does so only when few are left), so the later passes read them alone.
+// caller does so only when few are left), so the later passes read them alone.  TOMB
+// (eviction in place, on the copying pass, which reads every entry): the entries below
+// the prefix, all of them evicted, become tombstones here, and the copied entries' slot
+// words go to cpos for the last tombstone pass over the copies alone.
+template <bool TOMB>
 __global__ __launch_bounds__(TB) void sel_hist_kernel(const uint64_t *keys, const uint64_t *vals, uint64_t n,
                                                       SelPrefix p, unsigned long long *hist, uint64_t *ck,
-                                                      uint64_t *cv, unsigned long long *n_c) {
+                                                      uint64_t *cv, unsigned long long *n_c, DevIndex ix,
+                                                      const uint64_t *pos, uint64_t *cpos) {
   __shared__ uint32_t h[SEL_BINS];
   for (int b = threadIdx.x; b < SEL_BINS; b += TB) h[b] = 0;
   __syncthreads();
   const uint64_t stride = uint64_t(gridDim.x) * TB;
   for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += stride) {
     const uint64_t k = keys[i], v = vals[i];
-    if (sel_cmp(k, v, p) == 0) {
+    const int c = sel_cmp(k, v, p);
+    if (c == 0) {
       atomicAdd(&h[sel_digit(k, v, p.level)], 1u);
       if (ck) {
         const unsigned long long at = atomicAdd(n_c, 1ull);
         ck[at] = k;
         cv[at] = v;
+        if (TOMB) cpos[at] = pos[i];
       }
+    } else if (TOMB && c < 0) {
+      tomb_entry(ix, k, v, pos[i]);
     }
   }
   __syncthreads();
@@ -1942,7 +1953,16 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
       on_prefix = hh[b];
     }
   }
-  const uint64_t *sk = ws.ka, *sv = ws.va;  // the entries the passes read
+  // few tombstones: evict in place, the survivors keep their slots.  Tombstones may take
+  // an eighth of the slots, and at most half of what stays free with the live entries at
+  // capacity (the same eighth under the default 3/4 sizing), so every chain keeps
+  // reaching an EMPTY slot
+  const uint64_t n_slots = ix.n_buckets * SLOTS;
+  const uint64_t reserved = idx->capacity + uint64_t(ix.threshold) * ix.n_records;
+  const uint64_t tomb_cap_free = n_slots > reserved ? (n_slots - reserved) / 2 : 0;
+  const uint64_t tomb_cap = tomb_cap_free < n_slots / 8 ? tomb_cap_free : n_slots / 8;
+  const bool in_place = n_tomb + m <= tomb_cap;
+  const uint64_t *sk = ws.ka, *sv = ws.va, *sp = pos;  // the entries the passes read, and their slots
   uint64_t sn = n;
   for (int l = l0; l < SEL_LEVELS && rem < on_prefix; ++l) {
     p.level = l;
@@ -1952,8 +1972,12 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
     if ((rc = fill(ws.hist, 8 * SEL_BINS, 0, stream))) return rc;
     if (compact && (rc = fill(ws.count + 6, 8, 0, stream))) return rc;
     const int grid = grid_for(sn) < 1024 ? grid_for(sn) : 1024;
-    hipLaunchKernelGGL(sel_hist_kernel, dim3(grid), dim3(TB), 0, stream, sk, sv, sn, p, ws.hist,
-                       compact ? ws.ea : nullptr, compact ? ws.ia : nullptr, ws.count + 6);
+    if (in_place && compact)  // the last pass over every entry also writes the tombstones below the prefix
+      hipLaunchKernelGGL(sel_hist_kernel<true>, dim3(grid), dim3(TB), 0, stream, sk, sv, sn, p, ws.hist, ws.ea,
+                         ws.ia, ws.count + 6, ix, pos, ws.vb);
+    else
+      hipLaunchKernelGGL(sel_hist_kernel<false>, dim3(grid), dim3(TB), 0, stream, sk, sv, sn, p, ws.hist,
+                         compact ? ws.ea : nullptr, compact ? ws.ia : nullptr, ws.count + 6, ix, nullptr, nullptr);
     unsigned long long n_c = 0;
     if (hipMemcpyAsync(hh, ws.hist, 8 * SEL_BINS, hipMemcpyDeviceToHost, stream) != hipSuccess ||
         (compact && hipMemcpyAsync(&n_c, ws.count + 6, 8, hipMemcpyDeviceToHost, stream) != hipSuccess) ||
@@ -1964,6 +1988,7 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
       sk = ws.ea;
       sv = ws.ia;
       sn = n_c;
+      if (in_place) sp = ws.vb;  // and everything below the copies is a tombstone already
     }
     uint64_t below = 0;
     int b = 0;
@@ -1975,16 +2000,8 @@ extern "C" int smetric_index_evict(smetric_index *idx, uint32_t frac_num, uint32
     on_prefix = hh[b];  // rem == on_prefix: the whole bin goes, the prefix itself is the cut
     if (rem < on_prefix && l + 1 == SEL_LEVELS) return SMETRIC_EINTERNAL;  // the full tuple is unique
   }
-  // few tombstones: evict in place, the survivors keep their slots.  Tombstones may take
-  // an eighth of the slots, and at most half of what stays free with the live entries at
-  // capacity (the same eighth under the default 3/4 sizing), so every chain keeps
-  // reaching an EMPTY slot
-  const uint64_t n_slots = ix.n_buckets * SLOTS;
-  const uint64_t reserved = idx->capacity + uint64_t(ix.threshold) * ix.n_records;
-  const uint64_t tomb_cap_free = n_slots > reserved ? (n_slots - reserved) / 2 : 0;
-  const uint64_t tomb_cap = tomb_cap_free < n_slots / 8 ? tomb_cap_free : n_slots / 8;
-  if (n_tomb + m <= tomb_cap) {
-    hipLaunchKernelGGL(evict_tomb_kernel, dim3(grid_for(n)), dim3(TB), 0, stream, ix, ws.ka, ws.va, pos, n, p);
+  if (in_place) {  // the entries still to decide: every one, or the copies of the last full pass
+    hipLaunchKernelGGL(evict_tomb_kernel, dim3(grid_for(sn)), dim3(TB), 0, stream, ix, sk, sv, sp, sn, p);
     hipLaunchKernelGGL(set_counts_kernel, dim3(1), dim3(1), 0, stream, ix.hdr, (unsigned long long)(n - m), 0);
     if ((rc = hip_rc(hipGetLastError()))) return rc;
     return hip_rc(hipStreamSynchronize(stream));
