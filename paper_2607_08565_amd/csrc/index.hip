@@ -11,7 +11,7 @@
 //   [0, 256)                 IndexHdr: entry count, sticky status, pool use
 //   slots                    n_buckets x 128 B: keys[8] then values[8]
 //   pool                     n_records x bitmap_words x 8 B: holder bitmaps
-//   masks                    n_buckets bytes: each chain start's displacement mask
+//   masks                    n_buckets x 16 bits: each chain start's displacement mask
 // A key normally owns one PLAIN slot per holder in its home chain (linear probing over
 // buckets from home_bucket(key)).  When a key gains more than T holders its plain slots
 // are replaced by one HEADER slot pointing at a bitmap record, and every holder becomes a
@@ -19,7 +19,9 @@
 // bucket line plus the bitmap instead of walking T+ slots.  If the pool runs out, keys
 // simply stay plain.  Slots are only ever claimed (EMPTY -> key by compare-and-swap) or
 // turned into tombstones, so every slot of a key lies before the first EMPTY slot of its
-// chain; eviction rebuilds the table from the surviving entries.
+// chain.  Eviction selects the oldest entries by (epoch, key, instance) digit by digit
+// over a gathered copy of the entries, then turns them into tombstones in place, or --
+// once tombstones would take too many slots -- rebuilds the table from the survivors.
 //
 // Insert pipeline (no sort, no host synchronisation):
 //   clear      scratch dedupe table
