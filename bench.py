@@ -557,6 +557,23 @@ def measure_variants(setup, b: int, reps: int = 20):
                         "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist(),
                         "targets_differing_from_batch_snapshot": int((st != snap_t).sum())}
     inputs["route_seq"] = (st, br.cpu().numpy(), q_out.cpu().numpy(), b)
+    # the same rows as first turns: every decision is the sequential argmin over the
+    # running loads (no stick, no last-resort shortcut)
+    turn0 = torch.zeros_like(d["turn"])
+    call = lambda: S.route_seq(setup.matched, d["prompt_len"], d["hist_len"], turn0, d["q"], W.DEFAULT_PARAMS,
+                               tb.batch.rr_base, target=tgt, branch=br, q_out=q_out, workspace=ws)
+    call()
+    e0.record()
+    for _ in range(seq_reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / seq_reps
+    out["route_seq_all_scans"] = {"rule": "as route_seq, every request a first turn (each decision scans the "
+                                          "running loads)",
+                                  "ms": round(ms, 4), "requests_per_s": round(R / (ms / 1e3), 1),
+                                  "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist()}
+    inputs["route_seq_all_scans"] = (tgt.cpu().numpy(), br.cpu().numpy(), q_out.cpu().numpy(), b)
     # the colocated rule, one request at a time: the queue and the request counts update
     n_out = torch.empty(I, dtype=torch.int64, device="cuda")
     ws = torch.empty(S.route_seq_coloc_ws_bytes(R, I), dtype=torch.uint8, device="cuda")
@@ -651,6 +668,11 @@ def variants_parity(setup, inputs) -> dict:
                                   setup.W.DEFAULT_PARAMS, bt.rr_base)
     res["route_seq"] = {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb)
                                                                     and np.array_equal(oq, gq))}
+    gt, gb, gq, b = inputs["route_seq_all_scans"]
+    ot, ob, oq = oracle.route_seq(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, np.zeros_like(bt.turn),
+                                  bt.q, setup.W.DEFAULT_PARAMS, bt.rr_base)
+    res["route_seq_all_scans"] = {"requests": int(len(ot)), "bit_exact": bool(
+        np.array_equal(ot, gt) and np.array_equal(ob, gb) and np.array_equal(oq, gq))}
     gt, gb, gq, gn, b = inputs["route_seq_coloc"]
     bt = setup.host[b].batch
     slack, n_run = inputs["route_coloc"][0], inputs["route_coloc"][1]

@@ -434,13 +434,75 @@ __device__ __forceinline__ i128 readlane128(i128 v, int l) {
   return (i128((uint64_t(w3) << 32) | w2) << 64) | i128((uint64_t(w1) << 32) | w0);
 }
 
+// Minimum of a 32-bit value over the wavefront by DPP moves toward lane 63 (lanes without a
+// source, or outside the row mask, take all ones: the identity of the minimum, which lets
+// the move fold into the minimum's DPP form); every lane gets it.
+template <int CTRL, int RM>
+__device__ __forceinline__ uint32_t dpp_min_u32(uint32_t k) {
+  const uint32_t o = uint32_t(__builtin_amdgcn_update_dpp(-1, int(k), CTRL, RM, 0xF, false));
+  return o < k ? o : k;
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t k) {
+  k = dpp_min_u32<0x111, 0xF>(k);
+  k = dpp_min_u32<0x112, 0xF>(k);
+  k = dpp_min_u32<0x114, 0xF>(k);
+  k = dpp_min_u32<0x118, 0xF>(k);
+  k = dpp_min_u32<0x142, 0xA>(k);  // row_bcast:15 into rows 1 and 3
+  k = dpp_min_u32<0x143, 0xC>(k);  // row_bcast:31 into rows 2 and 3
+  return uint32_t(__builtin_amdgcn_readlane(int(k), 63));
+}
+// Minimum of a 64-bit key over the wavefront: the smallest high word, then the smallest low
+// word among the lanes holding it; every lane gets it.
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
+  const uint32_t hi = wave_min_u32(uint32_t(k >> 32));
+  const uint32_t lo = wave_min_u32(uint32_t(k >> 32) == hi ? uint32_t(k) : ~0u);
+  return (uint64_t(hi) << 32) | lo;
+}
+
+// The running state of the online route, held by its one wavefront (all fields uniform but
+// the LDS arrays).  Besides the exact loads 2q it keeps them as doubles for the scan's fast
+// path: exact while q_small (every 2q below 2^50), which stops holding for good once any
+// load reaches it.  With a1 = 2 C_LIN B and a2 = C_ATT B^2, Eq. (1) doubled is
+// est2(c) = C0 - c (a1 + a2 c) on the request's domain 0 <= c <= L / B, C0 = est2(0).
+constexpr double SEQ_PAD_2Q = 3377699720527872.0;  // 3 x 2^50
+
+struct SeqState {
+  i128 *q2;      // LDS: 2q per instance (exact)
+  double *q2d;   // LDS: the same values as doubles (exact while q_small)
+  i128 qmin;     // a lower bound of min(2q), exact unless qmin_stale
+  bool qmin_stale;
+  bool q_small;  // every 2q < 2^50
+  bool a_ok;     // a1, a2 < 2^53: exact as doubles
+  double a1, a2;
+};
+
+// The last-resort test of a cached follow-up whose prev misses its deadline: every other
+// instance i has est2(i) >= min(2q) + cost_rest and est2(i) >= m0, so if either misses the
+// deadline nobody can meet it.  qmin is a lower bound of min(2q) (loads only grow), exact
+// unless qmin_stale; a stale bound that does not settle the test is refreshed first, so the
+// minimum is recomputed only when a request needs it.
+__device__ __forceinline__ bool seq_none_meets(const SeqRec &rec, const RouteParams &p, int32_t I, SeqState &st) {
+  const i128 bound = rec.bound;
+  if (rec.m0 * p.slack_den > bound || (st.qmin + rec.cost_rest) * p.slack_den > bound) return true;
+  if (!st.qmin_stale) return false;
+  st.qmin = seq_qmin(st.q2, I);
+  st.qmin_stale = false;
+  return (st.qmin + rec.cost_rest) * p.slack_den > bound;
+}
+
+// A load update: the exact value, its double, and whether the doubles stay exact.
+__device__ __forceinline__ void seq_store(SeqState &st, int32_t i, i128 v) {
+  st.q2[i] = v;
+  st.q2d[i] = double(int64_t(v < (i128(1) << 62) ? v : i128(0)));
+}
+
 // Decide request r.  Every branch below is on wavefront-uniform values (read with
 // readfirstlane), and every lane performs the identical stores, so the code has no divergent
 // regions: the compiler can then wait for exactly the prefetched loads it uses.
 template <int K>
 __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *__restrict__ matched, int32_t r,
-                                           int32_t I, const RouteParams &p, bool q_ok, i128 *q2,
-                                           i128 &qmin, int32_t *__restrict__ target, uint8_t *__restrict__ branch) {
+                                           int32_t I, const RouteParams &p, bool q_ok, SeqState &st,
+                                           int32_t *__restrict__ target, uint8_t *__restrict__ branch) {
   const int lane = threadIdx.x;
   const int32_t flags = uni(row.rec.flags);
   if (!q_ok || !(flags & 1)) {
@@ -452,7 +514,8 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
   const bool cached = flags & 2, follow_up = flags & 4;
   const bool slack_inf = p.slack_den == 0;
   const i128 cost_prev = row.rec.cost_prev, bound = row.rec.bound;  // uniform across lanes
-  const bool meets_prev = slack_inf || (q2[prev] + cost_prev) * p.slack_den <= bound;
+  i128 *q2 = st.q2;
+  const bool meets_prev = follow_up && cached && (slack_inf || (q2[prev] + cost_prev) * p.slack_den <= bound);
   int32_t t;
   uint8_t br;
   i128 cost_t;
@@ -460,8 +523,7 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
     t = prev;
     br = SMETRIC_STICK;
     cost_t = cost_prev;
-  } else if (follow_up && cached && !slack_inf &&
-             ((qmin + row.rec.cost_rest) * p.slack_den > bound || row.rec.m0 * p.slack_den > bound)) {
+  } else if (follow_up && cached && !slack_inf && seq_none_meets(row.rec, p, I, st)) {
     // prev misses its deadline, and every other instance i has est2(i) >= min(2q) +
     // cost_rest and est2(i) >= m0: nobody can meet it
     t = prev;
@@ -473,20 +535,67 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
     const int32_t start = uni(row.rec.start);
     const int32_t *c = matched + int64_t(r) * I;
     MinSD best{0, 0x7FFFFFFF};
-    if (K > 0) {
+    // Fast path, while every 2q < 2^50 and C0 < 2^50: each candidate's score
+    // 2q + est2 = 2q + C0 - c (a1 + a2 c) is an integer below 2^51, and two fused
+    // multiply-adds in double precision give it exactly, offset by 2^52 so that its bit
+    // pattern holds the score in the low 52 bits under a fixed exponent field.  Shifting the
+    // exponent out leaves room for the rotation distance (I <= 4096): one 64-bit key per
+    // instance, minimised with two 32-bit DPP minima.
+    bool fast = false;
+    if (st.q_small && st.a_ok) {
+      const i128 c0 = est2(p, L, 0, 0);
+      if (c0 < (i128(1) << 50)) {
+        fast = true;
+        const double off = double(int64_t(c0)) + 4503599627370496.0;  // C0 + 2^52, exact
+        const double a1 = st.a1, a2 = st.a2;
+        const double *q2d = st.q2d;
+        uint64_t kmin = ~uint64_t(0);
+        int32_t d = lane >= start ? lane - start : lane - start + I;  // rotation distance of i
+        auto scan_one = [&](int32_t ci, double q2i) {
+          const double cd = double(ci);
+          const double s2 = __builtin_fma(-cd, __builtin_fma(a2, cd, a1), q2i + off);
+          const uint64_t key = (__builtin_bit_cast(uint64_t, s2) << 12) | uint32_t(d);
+          kmin = key < kmin ? key : kmin;
+        };
+        if (K > 0) {
+          // Slots past the last instance hold 2q = 3 x 2^50 (SEQ_PAD_2Q): their scores fall
+          // in [2^51, 2^52) under the same exponent, above every real one, so the loop has
+          // no per-lane conditions and all its LDS reads go out before the first is used.
+          double qv[K > 0 ? K : 1];
 #pragma unroll
-      for (int k = 0; k < (K > 0 ? K : 1); ++k) {
-        const int32_t i = lane + 64 * k;
-        const int32_t ii = i < I ? i : I - 1;
-        const i128 e = q2[ii] + est2(p, L, row.v[k], 0);
-        min_sd(best, e, i < I ? (i >= start ? i - start : i - start + I) : 0x7FFFFFFF);
+          for (int k = 0; k < (K > 0 ? K : 1); ++k) qv[k] = q2d[lane + 64 * k];
+#pragma unroll
+          for (int k = 0; k < (K > 0 ? K : 1); ++k) {
+            scan_one(row.v[k], qv[k]);
+            d = d + 64 >= I ? d + 64 - I : d + 64;  // I > 64 whenever K > 1
+          }
+        } else {
+          for (int32_t i = lane; i < I; i += 64) {
+            scan_one(c[i], q2d[i]);
+            d = d + 64 >= I ? d + 64 - I : d + 64;
+          }
+        }
+        const uint64_t m = wave_min_u64(kmin);
+        best.s = i128(m >> 12);
+        best.d = int32_t(m & 4095u);
       }
-    } else {
-      for (int32_t i = lane; i < I; i += 64)
-        min_sd(best, q2[i] + est2(p, L, c[i], 0), i >= start ? i - start : i - start + I);
     }
+    if (!fast) {
+      if (K > 0) {
 #pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) min_sd(best, shfl_xor128(best.s, m), __shfl_xor(best.d, m, 64));
+        for (int k = 0; k < (K > 0 ? K : 1); ++k) {
+          const int32_t i = lane + 64 * k;
+          const int32_t ii = i < I ? i : I - 1;
+          const i128 e = q2[ii] + est2(p, L, row.v[k], 0);
+          min_sd(best, e, i < I ? (i >= start ? i - start : i - start + I) : 0x7FFFFFFF);
+        }
+      } else {
+        for (int32_t i = lane; i < I; i += 64)
+          min_sd(best, q2[i] + est2(p, L, c[i], 0), i >= start ? i - start : i - start + I);
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) min_sd(best, shfl_xor128(best.s, m), __shfl_xor(best.d, m, 64));
+    }
     const int32_t bal0 = start + uni(best.d);  // start, d < I
     const int32_t bal = bal0 >= I ? bal0 - I : bal0;
     if (tr == 0) {
@@ -520,15 +629,16 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
   const i128 old = q2[t];
   target[r] = t;
   branch[r] = br;
-  q2[t] = old + cost_t;  // the request's prefill joins its target's queue
-  if (old == qmin && cost_t != 0) qmin = seq_qmin(q2, I);
+  seq_store(st, t, old + cost_t);  // the request's prefill joins its target's queue
+  st.q_small = st.q_small && old + cost_t < (i128(1) << 50);
+  if (old == st.qmin && cost_t != 0) st.qmin_stale = true;
 }
 
 // Requests [rs, re) one at a time, rows and records prefetched D requests ahead.
 template <int K, int D>
 __device__ __forceinline__ void seq_exact_block(const int32_t *__restrict__ matched, int32_t n_req, int32_t I,
                                                 const RouteParams &p, bool q_ok,
-                                                const SeqRec *__restrict__ recs, i128 *q2, i128 &qmin,
+                                                const SeqRec *__restrict__ recs, SeqState &st,
                                                 int32_t *__restrict__ target, uint8_t *__restrict__ branch,
                                                 int32_t rs, int32_t re) {
   SeqRow<K> ring[D];
@@ -539,7 +649,7 @@ __device__ __forceinline__ void seq_exact_block(const int32_t *__restrict__ matc
     for (int d = 0; d < D; ++d) {
       const int32_t r = r0 + d;
       if (r < re) {
-        seq_decide<K>(ring[d], matched, r, I, p, q_ok, q2, qmin, target, branch);
+        seq_decide<K>(ring[d], matched, r, I, p, q_ok, st, target, branch);
         seq_load<K>(matched, I, r + D, n_req, recs, ring[d]);
       }
     }
@@ -563,25 +673,38 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
                                                        int32_t *__restrict__ target, uint8_t *__restrict__ branch,
                                                        int64_t *__restrict__ q_out) {
   __shared__ i128 q2[SEQ_MAX_I];
+  __shared__ double q2d[SEQ_MAX_I];
   __shared__ uint32_t n_on[SEQ_MAX_I];  // block requests per prev (0 between blocks)
   const int lane = threadIdx.x;
-  bool q_ok = true;
+  bool q_ok = true, small = true;
   for (int32_t i = lane; i < I; i += 64) {
     const int64_t qi = q[i];
     if (qi < 0 || qi >= (int64_t(1) << 62)) q_ok = false;
+    if (qi >= (int64_t(1) << 49)) small = false;
     q2[i] = i128(2) * qi;
+    q2d[i] = 2.0 * double(qi < 0 ? 0 : qi);
     n_on[i] = 0;
   }
+  for (int32_t i = I + lane; i < 64 * K; i += 64) q2d[i] = SEQ_PAD_2Q;
   q_ok = __ballot(!q_ok) == 0;
   __syncthreads();
-  i128 qmin = seq_qmin(q2, I);  // a lower bound of min(2q) from here on (loads only grow)
+  SeqState st;
+  st.q2 = q2;
+  st.q2d = q2d;
+  st.qmin = seq_qmin(q2, I);  // a lower bound of min(2q) from here on (loads only grow)
+  st.qmin_stale = false;
+  st.q_small = __ballot(!small) == 0;
+  const i128 a1 = i128(2) * p.c_lin * p.B, a2 = i128(p.c_att) * p.B * p.B;
+  st.a_ok = a1 < (i128(1) << 53) && a2 < (i128(1) << 53);
+  st.a1 = double(int64_t(st.a_ok ? a1 : 0));
+  st.a2 = double(int64_t(st.a_ok ? a2 : 0));
   const bool slack_inf = p.slack_den == 0;
   int32_t r0 = 0;
   int streak = 0;
   while (r0 < n_req) {
     if (streak >= 2) {
       const int32_t re = n_req - r0 < 64 ? n_req : r0 + 64;
-      seq_exact_block<K, D>(matched, n_req, I, p, q_ok, recs, q2, qmin, target, branch, r0, re);
+      seq_exact_block<K, D>(matched, n_req, I, p, q_ok, recs, st, target, branch, r0, re);
       r0 = re;
       streak = 0;
       continue;
@@ -624,14 +747,21 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
     const i128 q_prev = q_pre + excl;
     bool settled = !ok;  // out of domain: settled, nothing queued
     uint8_t br = SMETRIC_INVALID;
-    if (sticky) {
-      if (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound) {
-        settled = true;
-        br = SMETRIC_STICK;
-      } else if ((qmin + rec.cost_rest) * p.slack_den > rec.bound || rec.m0 * p.slack_den > rec.bound) {
-        settled = true;
-        br = SMETRIC_LAST_RESORT;
-      }
+    const bool stick = sticky && (slack_inf || (q_prev + rec.cost_prev) * p.slack_den <= rec.bound);
+    bool none = sticky && !stick &&
+                ((st.qmin + rec.cost_rest) * p.slack_den > rec.bound || rec.m0 * p.slack_den > rec.bound);
+    if (st.qmin_stale && __ballot(in && sticky && !stick && !none)) {  // a stale bound left one open
+      st.qmin = seq_qmin(q2, I);
+      st.qmin_stale = false;
+      none = sticky && !stick && (st.qmin + rec.cost_rest) * p.slack_den > rec.bound;
+      none |= sticky && !stick && rec.m0 * p.slack_den > rec.bound;
+    }
+    if (stick) {
+      settled = true;
+      br = SMETRIC_STICK;
+    } else if (none) {
+      settled = true;
+      br = SMETRIC_LAST_RESORT;
     }
     const uint64_t open = __ballot(in && !settled);
     const int32_t f = open ? __builtin_ctzll(open) : nv;  // requests [r0, r0 + f) are decided
@@ -647,14 +777,15 @@ __global__ __launch_bounds__(64) void route_seq_kernel(const int32_t *__restrict
     const uint64_t after_me = lane == 63 ? uint64_t(0) : ~((uint64_t(2) << lane) - 1);
     const bool last = mine && lane < f && (group & after_me & decided) == 0;
     __builtin_amdgcn_wave_barrier();
-    if (last) q2[prev] = q_prev + rec.cost_prev;
+    if (last) seq_store(st, prev, q_prev + rec.cost_prev);
+    st.q_small = st.q_small && __ballot(last && q_prev + rec.cost_prev >= (i128(1) << 50)) == 0;
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     // the minimum can only have moved if an instance at the minimum took load
-    if (__ballot(mine && lane < f && q_pre == qmin)) qmin = seq_qmin(q2, I);
+    if (__ballot(mine && lane < f && q_pre == st.qmin)) st.qmin_stale = true;
     r0 += f;
     if (f < nv) {  // the first request not settled: the sequential rule
-      seq_decide<K>(row, matched, r0, I, p, q_ok, q2, qmin, target, branch);
+      seq_decide<K>(row, matched, r0, I, p, q_ok, st, target, branch);
       r0 += 1;
       streak = f == 0 ? streak + 1 : 0;
     }
@@ -823,31 +954,6 @@ __device__ __forceinline__ void dpp_min_key(uint64_t &k1, uint64_t &k0) {
 __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
   return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), l))) << 32) |
          uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
-}
-
-// Minimum of a 32-bit value over the wavefront by DPP moves toward lane 63 (lanes without a
-// source, or outside the row mask, take all ones: the identity of the minimum, which lets
-// the move fold into the minimum's DPP form); every lane gets it.
-template <int CTRL, int RM>
-__device__ __forceinline__ uint32_t dpp_min_u32(uint32_t k) {
-  const uint32_t o = uint32_t(__builtin_amdgcn_update_dpp(-1, int(k), CTRL, RM, 0xF, false));
-  return o < k ? o : k;
-}
-__device__ __forceinline__ uint32_t wave_min_u32(uint32_t k) {
-  k = dpp_min_u32<0x111, 0xF>(k);
-  k = dpp_min_u32<0x112, 0xF>(k);
-  k = dpp_min_u32<0x114, 0xF>(k);
-  k = dpp_min_u32<0x118, 0xF>(k);
-  k = dpp_min_u32<0x142, 0xA>(k);  // row_bcast:15 into rows 1 and 3
-  k = dpp_min_u32<0x143, 0xC>(k);  // row_bcast:31 into rows 2 and 3
-  return uint32_t(__builtin_amdgcn_readlane(int(k), 63));
-}
-// Minimum of a 64-bit key over the wavefront: the smallest high word, then the smallest low
-// word among the lanes holding it; every lane gets it.
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t k) {
-  const uint32_t hi = wave_min_u32(uint32_t(k >> 32));
-  const uint32_t lo = wave_min_u32(uint32_t(k >> 32) == hi ? uint32_t(k) : ~0u);
-  return (uint64_t(hi) << 32) | lo;
 }
 
 // Lexicographic minimum of (k1, k0) over lanes 0..N-1 (N = 64: the wavefront; N <= 16:

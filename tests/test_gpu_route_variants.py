@@ -213,6 +213,25 @@ def test_seq_extremes_invalid_and_limits():
     assert gq.cpu().numpy().tolist() == list(range(5))
 
 
+@pytest.mark.parametrize("I", [64, 1000])
+def test_seq_loads_crossing_2_pow_49(I):
+    """Loads that start just under 2^49 ns and grow past it within the batch: scans move
+    from the range where every score 2q + est2 stays below 2^51 (computed in double
+    precision) to the 128-bit one mid-batch; first turns only (a scan per request), then the
+    random mix of turns."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(500 + I)
+    R = 2000
+    m, L, hist, turn, _, _, _ = _coloc_inputs(rng, R, I)
+    q = rng.integers((1 << 49) - 3 * (1 << 38), (1 << 49) - (1 << 38), I).astype(np.int64)
+    # first turns on small hits (costly), with the costs scaled to cross within the batch
+    for over in (dict(c_lin=(1 << 24) * (I // 64)), dict(c_lin=(1 << 23) * (I // 64), c_att=(1 << 12) * (I // 64))):
+        _, ob = _seq_both(S, m // 4, L, hist, np.zeros_like(turn), q, dict(W.DEFAULT_PARAMS, **over), 77)
+        assert set(ob.tolist()) <= {0, 255}
+    for over in (dict(c_lin=1 << 28), dict(c_lin=1 << 27, c_att=1 << 16)):
+        _seq_both(S, m, L, hist, turn, q, dict(W.DEFAULT_PARAMS, **over), 78)
+
+
 def test_seq_on_matched_rows_of_a_session_workload():
     """Online routing of the real c rows of a scaled long-context workload, closed loop."""
     from paper_2607_08565_amd import smetric as S
