@@ -1221,7 +1221,12 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
   const uint32_t n_prev = nr[prev];
   i128 a[SQE];
   uint32_t n[SQE], d[SQE];
-  bool v[SQE], wide = false;
+  bool v[SQE], big = false;
+  // Each lane's best one-word key, formed before any branch: while every listed queue is
+  // below 2^64 and every score below 2^52, (score, d) is score 2^12 + d in one word.  The
+  // ballot below cannot move into a branch, so the listed entries' loads are waited for
+  // together with prev's, one LDS round trip for both.
+  uint64_t k1w = ~uint64_t(0);
 #pragma unroll
   for (int h = 0; h < SQE; ++h) {
     v[h] = lane + 64 * h < cnt;
@@ -1229,8 +1234,15 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     a[h] = q2[i] + row.cst[h];
     n[h] = nr[i];
     d[h] = uint32_t(i >= start ? i - start : i - start + I);
-    wide |= v[h] && (a[h] >> 64) != 0;
+    const uint64_t lo = uint64_t(a[h]);
+    const uint64_t p0 = uint64_t(uint32_t(lo)) * n[h];
+    const uint64_t p1 = (lo >> 32) * n[h] + (p0 >> 32);  // score = p1 2^32 + low word of p0
+    const bool b = (a[h] >> 64) != 0 || p1 >= (uint64_t(1) << 20);
+    big |= v[h] && b;
+    const uint64_t k = (p1 << 44) | (uint64_t(uint32_t(p0)) << 12) | d[h];
+    k1w = v[h] && k < k1w ? k : k1w;
   }
+  const bool one_word = __ballot(big) == 0;
   const bool meets_prev = q_prev <= row.rec.thr;
   int32_t t;
   uint8_t br;
@@ -1245,9 +1257,13 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     n_new = n_prev + 1;
   } else {
     int32_t dmin;
-    if (__ballot(wide) == 0) {  // every listed queue below 2^64: scores below 2^96, two words
+    bool wide = false;
+#pragma unroll
+    for (int h = 0; h < SQE; ++h) wide |= v[h] && (a[h] >> 64) != 0;
+    if (one_word) {
+      dmin = int32_t(uint32_t(wave_min_u64(k1w)) & 4095u);
+    } else if (__ballot(wide) == 0) {  // every listed queue below 2^64: scores below 2^96, two words
       uint64_t k1 = ~uint64_t(0), k0 = ~uint64_t(0);
-      bool big = false;
 #pragma unroll
       for (int h = 0; h < SQE; ++h)
         if (v[h]) {
@@ -1255,19 +1271,13 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
           const uint64_t p0 = uint64_t(uint32_t(lo)) * n[h];
           const uint64_t p1 = (lo >> 32) * n[h] + (p0 >> 32);  // score = p1 2^32 + low word of p0
           const uint64_t c0 = (p0 << 32) | d[h];
-          big |= p1 >= (uint64_t(1) << 20);
           if (p1 < k1 || (p1 == k1 && c0 < k0)) {
             k1 = p1;
             k0 = c0;
           }
         }
-      if (__ballot(big) == 0) {  // and below 2^52: (score, d) in one word, score 2^12 + d
-        const uint64_t k = k1 == ~uint64_t(0) ? ~uint64_t(0) : (k1 << 44) | ((k0 >> 32) << 12) | (k0 & 4095u);
-        dmin = int32_t(uint32_t(wave_min_u64(k)) & 4095u);
-      } else {
-        wave_min_key<64>(k1, k0);
-        dmin = int32_t(uint32_t(k0));
-      }
+      wave_min_key<64>(k1, k0);
+      dmin = int32_t(uint32_t(k0));
     } else {
       MinPD best{{0, 0}, 0x7FFFFFFF};
 #pragma unroll
