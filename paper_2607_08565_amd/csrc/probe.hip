@@ -208,8 +208,25 @@ __global__ __launch_bounds__(TB) void part_scatter_kernel(DevIndex ix, ProbeView
         pv.part_key[pos] = skey[p];
         pv.part_req[pos] = sreq[p];
         pv.part_blk[pos] = sblk[p];
-        pv.inv[sblk[p]] = uint32_t(pos);
       }
+    }
+    __syncthreads();
+    // the inverse map in block order through LDS (the keys' space is free now), so its
+    // stores are coalesced rather than one line per lane
+    uint32_t *sinv = reinterpret_cast<uint32_t *>(skey);
+#pragma unroll
+    for (int u = 0; u < UW; ++u) {
+      const uint32_t p = u * TB + t;
+      if (p < total) {
+        const uint32_t gg = sg[p];
+        sinv[sblk[p] - uint32_t(t0)] = uint32_t(run[gg] + (p - tstart[gg]));
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < UW; ++u) {
+      const uint32_t p = u * TB + t;
+      if (p < total) pv.inv[t0 + p] = sinv[p];
     }
     __syncthreads();
     if (t < NREG) {
