@@ -44,6 +44,11 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t v) {
   return (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo);
 }
 
+__device__ __forceinline__ uint64_t readlane64u(uint64_t v, int l) {
+  return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), l))) << 32) |
+         uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
+}
+
 __device__ __forceinline__ uint64_t remap(uint64_t k) {
   if (k == KEY_EMPTY) return 1;
   if (k == KEY_TOMB) return KEY_TOMB - 1;
@@ -185,7 +190,11 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
     return;  // the whole workgroup leaves before any barrier
   }
   const ChainConsts cc = chain_consts(seed, 16);
-  const uint64_t M64 = cc.Mpow[5] * cc.Mpow[5];
+  static_assert(NW == 8, "the step's carries are an affine scan over the eight lanes of row 0");
+  // powers of a tile's map M^64: M64^1, ^2, ^4 for the scan over the waves' aggregates,
+  // M64^wave for this wave's carry-in and M64^8 for the next step's
+  const uint64_t M64 = cc.Mpow[5] * cc.Mpow[5], M128 = M64 * M64, M256 = M128 * M128, M512 = M256 * M256;
+  const uint64_t Mw = ((wave & 1) ? M64 : 1ull) * ((wave & 2) ? M128 : 1ull) * ((wave & 4) ? M256 : 1ull);
   // this lane's four offset constants: K[4q .. 4q+3], q = lane % 4
   const int q = lane & 3;
   const uint32_t k0 = uint32_t(splitmix_out(seed, 4 * q + 0));
@@ -220,8 +229,14 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
     const uint64_t v = affine_scan64(lane < n_valid ? finalise(dig[wave][lane] + uint64_t(j0 + lane)) : 0, cc);
     if (lane == 63) agg[wave] = v;
     __syncthreads();
-    uint64_t c = carry;
-    for (int w = 0; w < wave; ++w) c = M64 * c + agg[w];
+    // inclusive scan of the tiles' aggregates over lanes 0..7: lane w holds
+    // sum_{k <= w} M64^(w-k) agg[k]; wave w starts from M64^w carry + (lane w-1's value)
+    uint64_t a = lane < NW ? agg[lane] : 0;
+    a += M64 * dpp_take64<0x111>(a);   // row_shr:1
+    a += M128 * dpp_take64<0x112>(a);  // row_shr:2
+    a += M256 * dpp_take64<0x114>(a);  // row_shr:4
+    const uint64_t before = wave == 0 ? 0 : readlane64u(a, wave - 1);
+    const uint64_t c = Mw * carry + before;
     if (lane < n_valid) {
       const uint64_t key = remap(finalise(cc.Mlane * c + v));
       keys[b0 + j0 + lane] = key;
@@ -232,10 +247,7 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
         else atomicAdd(&hist[(b / clen) * NREG + g], 1u);
       }
     }
-    uint64_t next = carry;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) next = M64 * next + agg[w];
-    carry = next;  // used only when every tile of this step was full
+    carry = M512 * carry + readlane64u(a, NW - 1);  // used only when every tile of this step was full
     __syncthreads();
     cur = nxt;
   }
