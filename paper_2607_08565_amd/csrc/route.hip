@@ -483,11 +483,11 @@ struct SeqState {
 // minimum is recomputed only when a request needs it.
 __device__ __forceinline__ bool seq_none_meets(const SeqRec &rec, const RouteParams &p, int32_t I, SeqState &st) {
   const i128 bound = rec.bound;
-  if (rec.m0 * p.slack_den > bound || (st.qmin + rec.cost_rest) * p.slack_den > bound) return true;
+  if (uni(int32_t(rec.m0 * p.slack_den > bound || (st.qmin + rec.cost_rest) * p.slack_den > bound)) != 0) return true;
   if (!st.qmin_stale) return false;
   st.qmin = seq_qmin(st.q2, I);
   st.qmin_stale = false;
-  return (st.qmin + rec.cost_rest) * p.slack_den > bound;
+  return uni(int32_t((st.qmin + rec.cost_rest) * p.slack_den > bound)) != 0;
 }
 
 // A load update: the exact value, its double, and whether the doubles stay exact.
@@ -515,7 +515,8 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
   const bool slack_inf = p.slack_den == 0;
   const i128 cost_prev = row.rec.cost_prev, bound = row.rec.bound;  // uniform across lanes
   i128 *q2 = st.q2;
-  const bool meets_prev = follow_up && cached && (slack_inf || (q2[prev] + cost_prev) * p.slack_den <= bound);
+  const bool meets_prev =
+      follow_up && cached && (slack_inf || uni(int32_t((q2[prev] + cost_prev) * p.slack_den <= bound)) != 0);
   int32_t t;
   uint8_t br;
   i128 cost_t;
@@ -604,7 +605,7 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
     } else if (!cached) {
       t = bal;
       br = SMETRIC_EVICTED;
-    } else if (!slack_inf && best.s * p.slack_den > bound) {
+    } else if (!slack_inf && uni(int32_t(best.s * p.slack_den > bound)) != 0) {
       t = prev;
       br = SMETRIC_LAST_RESORT;
     } else {
@@ -1243,7 +1244,9 @@ __device__ __forceinline__ void seqc_list_decide(const SeqLRow &row, int32_t r, 
     k1w = v[h] && k < k1w ? k : k1w;
   }
   const bool one_word = __ballot(big) == 0;
-  const bool meets_prev = q_prev <= row.rec.thr;
+  // the same on every lane (prev's queue and the record are); read as one scalar so that the
+  // branches below are uniform ones, with no exec-mask bookkeeping
+  const bool meets_prev = uni(int32_t(q_prev <= row.rec.thr)) != 0;
   int32_t t;
   uint8_t br;
   bool mine;  // this lane writes t's new queue and count (values it already holds)
