@@ -631,8 +631,9 @@ __device__ __forceinline__ void seq_decide(const SeqRow<K> &row, const int32_t *
   target[r] = t;
   branch[r] = br;
   seq_store(st, t, old + cost_t);  // the request's prefill joins its target's queue
-  st.q_small = st.q_small && old + cost_t < (i128(1) << 50);
-  if (old == st.qmin && cost_t != 0) st.qmin_stale = true;
+  // both flags stay wavefront-uniform (every lane holds the same values): read as scalars
+  st.q_small = st.q_small && uni(int32_t(old + cost_t < (i128(1) << 50))) != 0;
+  if (uni(int32_t(old == st.qmin && cost_t != 0)) != 0) st.qmin_stale = true;
 }
 
 // Requests [rs, re) one at a time, rows and records prefetched D requests ahead.
