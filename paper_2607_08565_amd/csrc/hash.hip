@@ -72,7 +72,8 @@ __device__ __forceinline__ uint64_t mpow(const uint64_t Mpow[6], uint32_t e) {
   return r;
 }
 
-__device__ ChainConsts chain_consts(uint64_t seed, int B) {
+// The constants every lane shares (kernel arguments only: scalar registers).
+__device__ ChainConsts chain_uniform(uint64_t seed, int B) {
   ChainConsts c;
   c.M = splitmix_out(seed, B) | 1ull;
   c.s_init = splitmix_out(seed, B + 1);
@@ -81,11 +82,18 @@ __device__ ChainConsts chain_consts(uint64_t seed, int B) {
     c.Mpow[k] = p;
     p *= p;
   }
-  // per-lane powers by binary exponentiation (exponents 1..64)
+  return c;
+}
+// This lane's powers, by binary exponentiation (exponents 1..64).
+__device__ void chain_lanes(ChainConsts &c) {
   const uint32_t lane = threadIdx.x & 63;
   c.Mlane = lane == 63 ? c.Mpow[5] * c.Mpow[5] : mpow(c.Mpow, lane + 1);
   c.Mrow = mpow(c.Mpow, (lane & 15) + 1);
   c.Mhalf = mpow(c.Mpow, lane >= 32 ? lane - 31 : 1);
+}
+__device__ ChainConsts chain_consts(uint64_t seed, int B) {
+  ChainConsts c = chain_uniform(seed, B);
+  chain_lanes(c);
   return c;
 }
 
@@ -189,25 +197,38 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
     if (COUNT && threadIdx.x == 0) atomicCAS(probe_err, 0, SMETRIC_EINVAL);
     return;  // the whole workgroup leaves before any barrier
   }
-  const ChainConsts cc = chain_consts(seed, 16);
   static_assert(NW == 8, "the step's carries are an affine scan over the eight lanes of row 0");
+  // The chain and digest constants depend on the seed and the lane only: wavefront 0 forms
+  // them while every wavefront's first tile is in flight, and the others read them from LDS.
+  // (the powers common to all lanes are formed by every wavefront in scalar registers)
+  __shared__ uint64_t s_lane[3][64];  // M^(l+1), M^(l % 16 + 1), M^(l - 31)
+  __shared__ uint32_t s_k[16];        // K[0 .. 15]
+  const int q = lane & 3;
+  const int32_t *x = tokens + t0;
+  Tile16 cur, nxt;
+  load_tile16(x, wave, nb, q, lane, cur);
+  ChainConsts cc = chain_uniform(seed, 16);
+  if (wave == 0) {
+    chain_lanes(cc);
+    s_lane[0][lane] = cc.Mlane;
+    s_lane[1][lane] = cc.Mrow;
+    s_lane[2][lane] = cc.Mhalf;
+    if (lane < 16) s_k[lane] = uint32_t(splitmix_out(seed, lane));
+  }
+  __syncthreads();
+  cc.Mlane = s_lane[0][lane];
+  cc.Mrow = s_lane[1][lane];
+  cc.Mhalf = s_lane[2][lane];
   // powers of a tile's map M^64: M64^1, ^2, ^4 for the scan over the waves' aggregates,
   // M64^wave for this wave's carry-in and M64^8 for the next step's
   const uint64_t M64 = cc.Mpow[5] * cc.Mpow[5], M128 = M64 * M64, M256 = M128 * M128, M512 = M256 * M256;
   const uint64_t Mw = ((wave & 1) ? M64 : 1ull) * ((wave & 2) ? M128 : 1ull) * ((wave & 4) ? M256 : 1ull);
   // this lane's four offset constants: K[4q .. 4q+3], q = lane % 4
-  const int q = lane & 3;
-  const uint32_t k0 = uint32_t(splitmix_out(seed, 4 * q + 0));
-  const uint32_t k1 = uint32_t(splitmix_out(seed, 4 * q + 1));
-  const uint32_t k2 = uint32_t(splitmix_out(seed, 4 * q + 2));
-  const uint32_t k3 = uint32_t(splitmix_out(seed, 4 * q + 3));
-  const int32_t *x = tokens + t0;
+  const uint32_t k0 = s_k[4 * q + 0], k1 = s_k[4 * q + 1], k2 = s_k[4 * q + 2], k3 = s_k[4 * q + 3];
   const int64_t n_tiles = (nb + 63) / 64;
   uint64_t carry = cc.s_init;  // chain state before the step's first block
   const uint64_t c_lo = COUNT ? uint64_t(b0) / clen : 0, B1 = (c_lo + 1) * clen, B2 = B1 + clen;
   if (COUNT && threadIdx.x < 2 * NREG) lh[threadIdx.x] = 0;  // first used after the step's barrier
-  Tile16 cur, nxt;
-  load_tile16(x, wave, nb, q, lane, cur);
   for (int64_t step0 = 0; step0 < n_tiles; step0 += NW) {
     const int64_t tile = step0 + wave;
     load_tile16(x, tile + NW, nb, q, lane, nxt);
