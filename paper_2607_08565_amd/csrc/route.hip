@@ -285,17 +285,20 @@ __global__ __launch_bounds__(64 * RW) void route_coloc_kernel(
 //         the best other hit, the deadline, and the smallest other est2 on the starting
 //         loads -- into an 80-byte record.
 //   seq   ONE wavefront routes the batch in index order; the running loads 2q[i] live in
-//         LDS as 128-bit integers, with a lower bound of their minimum.  Per request:
+//         LDS as 128-bit integers (and as doubles, exact while they stay below 2^50),
+//         with a lower bound of their minimum.  Per request:
 //           * cached follow-up whose prev meets its deadline: stick (no scan);
 //           * cached follow-up for which min(2q) + cost(best other hit), or the smallest
 //             other est2 on the starting loads, is past the deadline: no instance can meet
 //             it, last-resort stick (no scan);
-//           * otherwise the row is scanned for the argmin with the current loads.
+//           * otherwise the row is scanned for the argmin with the current loads (in
+//             double precision while every score is an integer below 2^51, else in 128
+//             bits).
 //         The first two need only prev's load, so 64 requests are settled per step (see
 //         route_seq_kernel); the rest go one at a time, their rows (for <= 1024 instances)
 //         and records loaded into registers ahead of use.
 // ---------------------------------------------------------------------------------
-constexpr int SEQ_MAX_I = 4096;  // 64 KB of LDS for the loads
+constexpr int SEQ_MAX_I = 4096;  // LDS: the loads (64 KB), as doubles (32 KB), step counters (16 KB)
 
 struct SeqRec {
   int32_t prev;    // argmax c, lowest id
