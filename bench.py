@@ -68,6 +68,9 @@ def parse():
                     help="after the timed steps, copy 1 GiB on the device (the counter runs' scale)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print the per-kernel summary of a rocprofv3 --kernel-trace run of this script and exit")
+    ap.add_argument("--summarize-sq", nargs=2, metavar=("SQ_CSV", "BENCH_JSON"),
+                    help="print the per-kernel instruction counts of a rocprofv3 --pmc run of this script with "
+                         "the SQ counters (and the JSON line of that run, which gives the tokens per batch) and exit")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_JSON"),
                     help="write the traffic file from two rocprofv3 --pmc runs of this script (and the JSON "
                          "line of one of them, which names the workload) and exit")
@@ -366,6 +369,37 @@ def summarize_pmc(fetch_csv: str, write_csv: str, steps: int, copy_bytes: int, b
     out += ["", "| call | traffic MB per launch |", "|---|---|"]
     out += [f"| {c} | {res[c] / 1e6:.1f} |" for c in ("hash", "probe", "match", "route", "insert")]
     return res, "\n".join(out)
+
+
+SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_LDS", "SQ_INSTS_VMEM_RD", "SQ_INSTS_VMEM_WR",
+               "SQ_WAVE_CYCLES")
+
+
+def summarize_sq(csv_path: str, steps: int, bench_json: str):
+    """Per-kernel instruction counts over the timed steps from one rocprofv3 --pmc run with
+    the SQ counters (wavefront instructions per launch; a VALU instruction covers 64 lanes),
+    and the counting hash's VALU lane operations per prompt token."""
+    import csv
+    per = {c: [] for c in SQ_COUNTERS}
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] in per:
+            per[r["Counter_Name"]].append((int(r["Dispatch_Id"]), _kname(r["Kernel_Name"]), float(r["Counter_Value"])))
+    st = {c: timed_step_dispatches(rows, steps) for c, rows in per.items() if rows}
+    line = [x for x in open(bench_json).read().splitlines() if x.startswith("{")][-1]
+    tokens = json.loads(line)["config"]["tokens_per_batch"]
+    cols = [c for c in SQ_COUNTERS if c in st]
+    out = ["| call | kernel | " + " | ".join(c[3:] for c in cols) + " |", "|---|---|" + "---|" * len(cols)]
+    mean = {}
+    for j, (c, k) in enumerate(STEP_CALLS):
+        vals = {q: float(np.mean([s[j][1] for s in st[q]])) for q in cols}
+        mean[(c, k)] = vals
+        out.append(f"| {c} | {k} | " + " | ".join(f"{vals[q]:.4g}" for q in cols) + " |")
+    hk = [key for key in mean if key[0] == "hash" and key[1].startswith("hash16_kernel")]
+    if hk and "SQ_INSTS_VALU" in cols:
+        v = mean[hk[0]]["SQ_INSTS_VALU"]
+        out += ["", f"Counting hash: {v:.4g} VALU instructions x 64 lanes / {tokens:,} tokens = "
+                    f"{v * 64 / tokens:.1f} VALU lane operations per token."]
+    return "\n".join(out)
 
 
 def kernel_sources_hash() -> str:
@@ -732,6 +766,9 @@ def main():
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.steps))
         return
+    if args.summarize_sq:
+        print(summarize_sq(args.summarize_sq[0], args.steps, args.summarize_sq[1]))
+        return
     if args.summarize_pmc:
         res, md = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.steps, COPY_BYTES,
                                 args.summarize_pmc[2])
@@ -741,7 +778,7 @@ def main():
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU: the matching/routing path is "
-                                   "not sharded across GPUs in this build (pass --gpus 1)"}))
+                                   "not sharded across GPUs (pass --gpus 1)"}))
         sys.exit(2)
     import torch
 

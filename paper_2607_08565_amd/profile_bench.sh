@@ -1,12 +1,15 @@
 #!/bin/bash
-# The profiles under profiles/: a rocprofv3 kernel trace of the benchmark as the round-end
-# driver runs it, then one FETCH_SIZE and one WRITE_SIZE counter run of the same command
-# with --calibrate-copy (a 1 GiB device copy after the timed steps fixes the counters'
-# scale), summarised by bench.py itself.  Run from the repository root on an MI355X machine;
-# raw output goes to gpurun_out/profile/.  Usage: profile_bench.sh [trace|counters|all]
+# The profiles under profiles/: a rocprofv3 kernel trace of the benchmark command
+# (bench.py --gpus 1 --steps 20 --warmup 5), then one FETCH_SIZE and one WRITE_SIZE counter
+# run of the same command with --calibrate-copy (a 1 GiB device copy after the timed steps
+# fixes the counters' scale), summarised by bench.py itself.  Run from the repository root
+# on an MI355X; raw output goes to $PROFILE_OUT (default: profile_out/ in the repository).
+# Usage: profile_bench.sh [trace|counters|all|sq]  (sq: one run with the SQ instruction
+# counters, summarised per kernel).
 set -o pipefail
 R=$(pwd)
-O=$R/gpurun_out/profile
+O=${PROFILE_OUT:-$R/profile_out}
+case $O in /*) ;; *) O=$R/$O ;; esac
 mkdir -p $O
 CMD="$R/bench.py --gpus 1 --steps 20 --warmup 5"
 STAGE=${1:-all}
@@ -33,5 +36,13 @@ cd $R
 F=$(find $O/fetch -name "*counter_collection.csv" | head -1)
 W=$(find $O/write -name "*counter_collection.csv" | head -1)
 python3 bench.py --summarize-pmc $F $W $O/fetch_bench.log --steps 20 --traffic $O/traffic.json > $O/traffic_summary.md || exit 6
+fi
+if [ $STAGE = sq ]; then
+echo "== SQ instruction counters"
+timeout -s KILL 900 rocprofv3 --pmc SQ_WAVES SQ_INSTS_VALU SQ_INSTS_SALU SQ_INSTS_LDS SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR \
+  SQ_WAVE_CYCLES --output-format csv -d $O/sq -o run -- python3 $CMD > $O/sq_bench.log 2>&1 || { tail -5 $O/sq_bench.log; exit 7; }
+cd $R
+Q=$(find $O/sq -name "*counter_collection.csv" | head -1)
+python3 bench.py --summarize-sq $Q $O/sq_bench.log --steps 20 > $O/sq_summary.md || exit 8
 fi
 echo "done"
