@@ -64,6 +64,9 @@ def parse():
                     help="also measure the hash + probe path with the next batch's hash beside this batch's "
                          "lookup and match (two streams); off by default, so that a profile of the default run "
                          "averages each kernel over the timed steps' launches only")
+    ap.add_argument("--overlap-step", action="store_true",
+                    help="also measure whole steps with the next batch's hash + partition beside this batch's "
+                         "lookup, match, route and insert (two streams, the index restored between steps)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the timed steps, copy 1 GiB on the device (the counter runs' scale)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
@@ -248,6 +251,45 @@ class Setup:
                 matched_done[k] = e
         torch.cuda.synchronize()
         return time.perf_counter() - t0
+
+    def step_overlapped(self, batches):
+        """Whole steps over consecutive batches with the next batch's hash and partition
+        (stream A; it reads no index contents) beside this batch's lookup, match, route and
+        insert (stream B), buffer sets alternating; the index is restored between steps,
+        untimed, after both streams finished.  Batch 0's hash is timed alone.  Returns the
+        timed seconds (one hash, lookup, match, route and insert per batch)."""
+        torch = self.torch
+        total = 0.0
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        with torch.cuda.stream(self.sA):
+            d = self.dev[batches[0]]
+            self.index.hash_partition(d["tokens"], d["tok_off"], d["blk_off"], d["n_blocks"], keys=self.keys2[0],
+                                      state=self.state2[0])
+        torch.cuda.synchronize()
+        total += time.perf_counter() - t0
+        for k, b in enumerate(batches):
+            p, d, tb = k % 2, self.dev[b], self.host[b]
+            nb = d["n_blocks"]
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            with torch.cuda.stream(self.sB):
+                self.index.probe_lookup(self.state2[p], self.keys2[p], d["blk_off"], nb)
+                self.index.match_probed(self.state2[p], self.keys2[p], d["blk_off"], nb, matched=self.matched)
+                self.S.route(self.matched, d["prompt_len"], d["hist_len"], d["turn"], d["q"], self.W.DEFAULT_PARAMS,
+                             tb.batch.rr_base, target=self.target, branch=self.branch)
+                self.index.insert_probed(self.state2[p], self.args.n_req, nb, self.target, d["session"],
+                                         tb.batch.epoch, workspace=self.ws)
+            if k + 1 < len(batches):  # set 1 - p was last read by the previous step, which has finished
+                with torch.cuda.stream(self.sA):
+                    dn = self.dev[batches[k + 1]]
+                    self.index.hash_partition(dn["tokens"], dn["tok_off"], dn["blk_off"], dn["n_blocks"],
+                                              keys=self.keys2[1 - p], state=self.state2[1 - p])
+            torch.cuda.synchronize()
+            total += time.perf_counter() - t0
+            self.restore()
+            torch.cuda.synchronize()
+        return total
 
 
 # kernels each timed call launches, in order (names as rocprofv3 reports them)
@@ -894,6 +936,18 @@ def main():
             "how": "two streams: the next batch's hash + partition beside this batch's lookup + match; "
                    "wall time over the timed batches"}
         del m2
+    if args.overlap_step and not args.direct:  # batch k+1's hash beside batch k's lookup .. insert
+        setup.restore()
+        batches = [setup.batch_of(args.warmup + k) for k in range(args.steps)]
+        setup.step_overlapped(batches[:2])  # warm
+        dt = setup.step_overlapped(batches)
+        ms = dt * 1e3 / len(batches)
+        out["step_overlapped"] = {
+            "ms_per_step": round(ms, 4), "requests_per_s": round(R / (ms / 1e3), 1),
+            "how": "two streams: the next batch's hash + partition beside this batch's lookup, match, route and "
+                   "insert; the index restored between steps (untimed, after both streams finished); wall time "
+                   "over the timed batches, the first batch's hash included"}
+        setup.restore()
     if args.calibrate_copy:  # a device copy of known size, for the HBM counters' scale
         src = torch.ones(COPY_BYTES, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
