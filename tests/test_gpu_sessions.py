@@ -90,3 +90,19 @@ def test_tiny_batches():
         off = np.zeros(len(prompts) + 1, np.int64)
         off[1:] = np.cumsum([len(p) for p in prompts])
         _check(S, toks, off, np.asarray(user, np.uint32), np.asarray(turn, np.int32))
+
+
+def test_random_trace_shapes():
+    """Seeded random trace shapes: 1-59 users, 1-7 sessions each, 1-8 turns, prompts from
+    empty to thousands of tokens, no or short or long shared prefixes, compactions and
+    retries from never to often."""
+    from paper_2607_08565_amd import smetric as S
+    for case in range(60000, 60030):
+        rng = np.random.default_rng(case)
+        tr = W.session_trace(n_users=int(rng.integers(1, 60)), sessions_per_user=int(rng.integers(1, 8)),
+                             turns=int(rng.integers(1, 9)), l0=int(rng.choice([0, 8, 24, 300, 2048])),
+                             prefix_len=int(rng.choice([0, 16, 100, 1024])),
+                             app=tuple(sorted(rng.integers(0, 3000, 2).tolist())),
+                             p_compact=float(rng.choice([0, 0.05, 0.3])), p_retry=float(rng.choice([0, 0.03, 0.3])),
+                             compact_len=int(rng.choice([0, 8, 1024])), seed=case)
+        _check(S, tr.tokens, tr.tok_off, tr.user, tr.turn)
