@@ -197,7 +197,7 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
     if (COUNT && threadIdx.x == 0) atomicCAS(probe_err, 0, SMETRIC_EINVAL);
     return;  // the whole workgroup leaves before any barrier
   }
-  static_assert(NW == 8, "the step's carries are an affine scan over the eight lanes of row 0");
+  static_assert(NW == 2 || NW == 4 || NW == 8 || NW == 16, "the step's carries: an affine scan inside row 0");
   // The chain and digest constants depend on the seed and the lane only: wavefront 0 forms
   // them while every wavefront's first tile is in flight, and the others read them from LDS.
   // (the powers common to all lanes are formed by every wavefront in scalar registers)
@@ -219,10 +219,13 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
   cc.Mlane = s_lane[0][lane];
   cc.Mrow = s_lane[1][lane];
   cc.Mhalf = s_lane[2][lane];
-  // powers of a tile's map M^64: M64^1, ^2, ^4 for the scan over the waves' aggregates,
-  // M64^wave for this wave's carry-in and M64^8 for the next step's
-  const uint64_t M64 = cc.Mpow[5] * cc.Mpow[5], M128 = M64 * M64, M256 = M128 * M128, M512 = M256 * M256;
-  const uint64_t Mw = ((wave & 1) ? M64 : 1ull) * ((wave & 2) ? M128 : 1ull) * ((wave & 4) ? M256 : 1ull);
+  // powers of a tile's map M^64: M64^1, ^2, ^4, ^8 for the scan over the waves' aggregates,
+  // M64^wave for this wave's carry-in and M64^NW for the next step's
+  const uint64_t M64 = cc.Mpow[5] * cc.Mpow[5], M128 = M64 * M64, M256 = M128 * M128, M512 = M256 * M256,
+                 M1024 = M512 * M512;
+  const uint64_t Mw = ((wave & 1) ? M64 : 1ull) * ((wave & 2) ? M128 : 1ull) * ((wave & 4) ? M256 : 1ull) *
+                      ((wave & 8) ? M512 : 1ull);
+  const uint64_t Mstep = NW == 2 ? M128 : (NW == 4 ? M256 : (NW == 8 ? M512 : M1024));
   // this lane's four offset constants: K[4q .. 4q+3], q = lane % 4
   const uint32_t k0 = s_k[4 * q + 0], k1 = s_k[4 * q + 1], k2 = s_k[4 * q + 2], k3 = s_k[4 * q + 3];
   const int64_t n_tiles = (nb + 63) / 64;
@@ -250,12 +253,13 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
     const uint64_t v = affine_scan64(lane < n_valid ? finalise(dig[wave][lane] + uint64_t(j0 + lane)) : 0, cc);
     if (lane == 63) agg[wave] = v;
     __syncthreads();
-    // inclusive scan of the tiles' aggregates over lanes 0..7: lane w holds
+    // inclusive scan of the tiles' aggregates over lanes 0..NW-1: lane w holds
     // sum_{k <= w} M64^(w-k) agg[k]; wave w starts from M64^w carry + (lane w-1's value)
     uint64_t a = lane < NW ? agg[lane] : 0;
-    a += M64 * dpp_take64<0x111>(a);   // row_shr:1
-    a += M128 * dpp_take64<0x112>(a);  // row_shr:2
-    a += M256 * dpp_take64<0x114>(a);  // row_shr:4
+    a += M64 * dpp_take64<0x111>(a);                   // row_shr:1
+    if (NW > 2) a += M128 * dpp_take64<0x112>(a);      // row_shr:2
+    if (NW > 4) a += M256 * dpp_take64<0x114>(a);      // row_shr:4
+    if (NW > 8) a += M512 * dpp_take64<0x118>(a);      // row_shr:8
     const uint64_t before = wave == 0 ? 0 : readlane64u(a, wave - 1);
     const uint64_t c = Mw * carry + before;
     if (lane < n_valid) {
@@ -268,7 +272,7 @@ __global__ __launch_bounds__(64 * NW) void hash16_kernel(const int32_t *__restri
         else atomicAdd(&hist[(b / clen) * NREG + g], 1u);
       }
     }
-    carry = M512 * carry + readlane64u(a, NW - 1);  // used only when every tile of this step was full
+    carry = Mstep * carry + readlane64u(a, NW - 1);  // used only when every tile of this step was full
     __syncthreads();
     cur = nxt;
   }
