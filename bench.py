@@ -911,6 +911,8 @@ def main():
         "path": ("direct" if args.direct else "hash + region partition in one call, then the region-ordered lookup")
                 + "; one batch at a time, the index restored (untimed) before every step",
         "prompt_tokens_matched_per_s": round(tokens / ((per["hash"] + probe_match_ms) / 1e3), 1),
+        # the decision alone (hash, lookup, match, route: the insert follows it), by event time
+        "requests_routed_per_s_before_insert": round(R / ((per["hash"] + probe_match_ms + per["route"]) / 1e3), 1),
         "kernel_ms": {show(k): round(per[k], 4) for k in Setup.CALLS if not (args.direct and k == "probe")},
         "algorithmic_GBs": {show(k): round(v, 1) for k, v in gbs.items()},
         "hash_probe_path": {"GBs": round(path_gbs, 1), "frac_of_peak": round(path_gbs / HBM_PEAK_GBS, 4),
