@@ -89,6 +89,8 @@ def _load():
     lib.orc_test_prod_less.argtypes = [C.c_int64, C.c_uint64, C.c_uint64, C.c_int64, C.c_uint64, C.c_uint64]
     lib.orc_route_seq_coloc.argtypes = [P, C.c_int32, C.c_int32, P, P, P, P, P, P, C.POINTER(_Params), C.c_uint64,
                                         P, P, P, P]
+    lib.orc_route_score.argtypes = [C.c_int32, P, C.c_int32, C.c_int32, P, P, P, C.c_int32, C.c_int32, C.c_int32,
+                                    C.c_uint64, P, P]
     _lib = lib
     return lib
 
@@ -354,3 +356,26 @@ def imbalance(inst, t0, t1, n_inst: int, window: int, n_windows: int):
     if rc != OK:
         raise ValueError(f"orc_imbalance rc={rc}")
     return out_sum[:n_windows], out_max[:n_windows], bad.value
+
+
+SCORE_LOAD, SCORE_TOKENS, SCORE_PRODUCT, SCORE_LINEAR, SCORE_HIT_FILTER = range(5)
+
+
+def route_score(kind, matched, prompt_len, q, load, block_size, lam=(0, 1), rr_base: int = 0):
+    """The scoring template's comparison scorers (Sec. 4.1, Sec. 5): argmin over instances of
+    f(kind), ties in rotation order. q: int64[I] queued prefill tokens; load: int32[I] batch
+    sizes; lam = (num, den) for the weighted sum (kinds 3 and 4). Returns (target int32[R],
+    branch uint8[R]: 6 scored, 7 hit filter, 255 out of domain); raises on bad scalars."""
+    matched = _arr(matched, np.int32)
+    R, I = matched.shape
+    prompt_len = _arr(prompt_len, np.int32)
+    q = _arr(q, np.int64)
+    load = _arr(load, np.int32)
+    target = np.zeros(max(R, 1), np.int32)
+    branch = np.zeros(max(R, 1), np.uint8)
+    rc = _load().orc_route_score(int(kind), _ptr(matched) if matched.size else None, R, I,
+                                 _ptr(prompt_len) if R else None, _ptr(q), _ptr(load), int(block_size),
+                                 int(lam[0]), int(lam[1]), C.c_uint64(rr_base), _ptr(target), _ptr(branch))
+    if rc != OK:
+        raise ValueError(f"orc_route_score rc={rc}")
+    return target[:R], branch[:R]

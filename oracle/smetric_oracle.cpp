@@ -18,6 +18,7 @@
 //   route_loadaware  the Sec. 5.4 ablation's load-aware filter        (Sec. 5.4)
 //   imbalance    per-window max / mean load                            (Sec. 4.1 analysis)
 //   route_coloc  the same rule under PD colocation                    (App. B pseudocode)
+//   route_score  the comparison scorers of the scoring template        (Sec. 4.1, Sec. 5)
 //
 // Where the paper is silent (hash function, tie-breaks, integer units, batch semantics,
 // eviction order) the choices are the readings recorded with the design notes; each is
@@ -27,7 +28,8 @@
 // hash itself is pinned only by its structural properties (chained prefix identity,
 // closed-form == sequential), since the paper specifies no hash.  Match is pinned by a
 // hash-free brute-force longest-common-prefix model, route by hand-built decision tables
-// and closed forms of Eq. (1), insert/evict by a brute-force dictionary model.
+// and closed forms of Eq. (1), insert/evict by a brute-force dictionary model, the
+// comparison scorers by hand-worked tables and the textbook rules they reduce to.
 
 #include <algorithm>
 #include <climits>
@@ -864,6 +866,97 @@ int orc_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t I, const 
     }
   if (n_out)
     for (int32_t i = 0; i < I; ++i) n_out[i] = n[i];
+  return ORC_OK;
+}
+
+// The Sec. 4.1 scoring template: each request goes to the instance that minimises a score
+// f(req, i) built from the request's KV$ hit c[i] (blocks), its prompt length L, the
+// prefill work q[i] already queued at i (tokens) and the instance's load l[i] (its batch
+// size, i.e. requests running there).  The scorers are the ones the paper compares against
+// (Sec. 4.1 motivating analysis, Sec. 5 baselines); kind selects f:
+//   0 load-balance only (join the shortest queue):  f = l[i]
+//   1 fewest tokens left to prefill (Dynamo):        f = q[i] + L - B c[i]
+//   2 multiplicative (LMetric):                      f = (q[i] + L - B c[i]) * l[i]
+//   3 weighted sum (the production scheduler):       f = (1 - lam) lhat[i] + lam (1 - chat[i])
+//        lhat[i] = l[i] / max_j l[j]  (reading: normalised by the cluster maximum; an idle
+//                                      cluster, max 0, has lhat = 0)
+//        chat[i] = B c[i] / L         (the hit ratio; reading: 0 for an empty prompt)
+//        lam = lam_num / lam_den
+//   4 hit filter, then score (Preble): if some instance caches more than half the prompt
+//        (2 B c[i] > L, strict), the least loaded such instance (argmin l[i]); otherwise
+//        kind 3's weighted sum with the same lam
+// Every argmin breaks ties by the rotation order of orc_route (the earliest of
+// start, start+1, ... mod I, start = (rr_base + r) mod I; reading: the paper gives no
+// tie-break for these scorers).  Kind 3's fractions are compared exactly: every f[i] of one
+// request is multiplied by the same positive constant lam_den * Dl * Dc (Dl = max l or 1,
+// Dc = L or 1), leaving integers.
+// branch: 6 scored, 7 the hit filter chose (kind 4); 255 out of domain (target -1): L < 0
+// or > 2^24, some c[i] < 0 or > L / B, some q[i] < 0 or >= 2^62, some l[i] < 0.
+int orc_route_score(int32_t kind, const int32_t *matched, int32_t n_req, int32_t I, const int32_t *prompt_len,
+                    const int64_t *q, const int32_t *load, int32_t block_size, int32_t lam_num, int32_t lam_den,
+                    uint64_t rr_base, int32_t *target, uint8_t *branch) {
+  typedef __int128 i128;
+  if (kind < 0 || kind > 4 || n_req < 0 || I < 1 || I > 65536) return ORC_EINVAL;
+  if (block_size < 2 || block_size > 256 || (block_size & 1)) return ORC_EINVAL;
+  if ((kind == 3 || kind == 4) && (lam_den <= 0 || lam_num < 0 || lam_num > lam_den)) return ORC_EINVAL;
+  const int64_t B = block_size;
+  bool inst_ok = true;
+  int64_t lmax = 0;
+  for (int32_t i = 0; i < I; ++i) {
+    if (q[i] < 0 || q[i] >= (int64_t(1) << 62) || load[i] < 0) inst_ok = false;
+    lmax = std::max<int64_t>(lmax, load[i]);
+  }
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int32_t *c = matched + int64_t(r) * I;
+    const int64_t L = prompt_len[r];
+    bool ok = inst_ok && L >= 0 && L <= (int64_t(1) << 24);
+    for (int32_t i = 0; ok && i < I; ++i) ok = c[i] >= 0 && c[i] <= L / B;
+    if (!ok) {
+      target[r] = -1;
+      branch[r] = 255;
+      continue;
+    }
+    // the weighted sum's terms as fractions over Dl and Dc
+    const int64_t Dl = lmax > 0 ? lmax : 1;
+    const int64_t Dc = L > 0 ? L : 1;
+    auto lhat_num = [&](int32_t i) -> i128 { return lmax > 0 ? load[i] : 0; };
+    auto miss_num = [&](int32_t i) -> i128 { return L > 0 ? L - B * c[i] : 1; };  // (1 - chat) Dc
+    auto score = [&](int32_t k, int32_t i) -> i128 {
+      switch (k) {
+        case 0: return load[i];
+        case 1: return i128(q[i]) + L - B * c[i];
+        case 2: return (i128(q[i]) + L - B * c[i]) * load[i];
+        default:  // (1 - lam) lhat + lam (1 - chat), times lam_den Dl Dc
+          return i128(lam_den - lam_num) * lhat_num(i) * Dc + i128(lam_num) * miss_num(i) * Dl;
+      }
+    };
+    const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
+    // argmin of score kind k over the instances with keep(i), rotation order on ties
+    auto argmin = [&](int32_t k, auto keep) -> int32_t {
+      int32_t best = -1;
+      for (int32_t s = 0; s < I; ++s) {
+        const int32_t i = (start + s) % I;
+        if (!keep(i)) continue;
+        if (best < 0 || score(k, i) < score(k, best)) best = i;  // strict: earlier position wins
+      }
+      return best;
+    };
+    auto all = [](int32_t) { return true; };
+    if (kind == 4) {
+      auto holds_half = [&](int32_t i) { return 2 * B * c[i] > L; };
+      const int32_t h = argmin(0, holds_half);
+      if (h >= 0) {
+        target[r] = h;
+        branch[r] = 7;
+      } else {
+        target[r] = argmin(3, all);
+        branch[r] = 6;
+      }
+    } else {
+      target[r] = argmin(kind, all);
+      branch[r] = 6;
+    }
+  }
   return ORC_OK;
 }
 
