@@ -18,6 +18,7 @@
  *   smetric_sessions      session reconstruction from block hashes        (App. A)
  *   smetric_route_loadaware  the Sec. 5.4 ablation's load-aware filter
  *   smetric_imbalance     per-window max / mean load                      (Sec. 4.1)
+ *   smetric_route_score   the comparison scorers of the scoring template  (Sec. 4.1, Sec. 5)
  *   smetric_index_insert  post-route insert of every full block on the target
  *   smetric_index_evict   LRU eviction of a fraction of the entries
  *
@@ -287,7 +288,8 @@ typedef struct smetric_params {
 } smetric_params;
 
 enum { SMETRIC_FIRST_TURN = 0, SMETRIC_EVICTED = 1, SMETRIC_STICK = 2, SMETRIC_LAST_RESORT = 3,
-       SMETRIC_MIGRATE = 4, SMETRIC_MIGRATE_TPOT = 5, SMETRIC_INVALID = 255 };
+       SMETRIC_MIGRATE = 4, SMETRIC_MIGRATE_TPOT = 5, SMETRIC_SCORED = 6, SMETRIC_HIT_FILTER = 7,
+       SMETRIC_INVALID = 255 };
 
 int smetric_route(const int32_t *matched, int32_t n_req, int32_t n_instances,
                   const int32_t *prompt_len, const int32_t *hist_len, const int32_t *turn,
@@ -448,6 +450,45 @@ int smetric_route_seq_coloc(const int32_t *matched, int32_t n_req, int32_t n_ins
                             const smetric_params *params /* host */, uint64_t rr_base, int32_t *target,
                             uint8_t *branch, int64_t *q_out, int64_t *n_out, void *workspace,
                             uint64_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------------
+ * The scoring template's comparison scorers (Sec. 4.1: a request goes to the instance
+ * with the lowest score f of its load and the request's KV$ hit; the scorers of the
+ * Sec. 4.1 motivating analysis and the Sec. 5 baselines).  Per request r with prompt
+ * length L, hit c[i] (blocks of B tokens), queued prefill q[i] and load l[i]:
+ *   SMETRIC_SCORE_LOAD       f = l[i]                         load balance only (JSQ)
+ *   SMETRIC_SCORE_TOKENS     f = q[i] + L - B c[i]            fewest tokens left to
+ *                                                             prefill (Dynamo)
+ *   SMETRIC_SCORE_PRODUCT    f = (q[i] + L - B c[i]) * l[i]   LMetric
+ *   SMETRIC_SCORE_LINEAR     f = (1 - lam) l[i] / max_j l[j] + lam (1 - B c[i] / L)
+ *                            the production scheduler's weighted sum of normalised load
+ *                            and miss ratio, lam = lam_num / lam_den; an idle cluster
+ *                            (max load 0) has normalised load 0, an empty prompt hit
+ *                            ratio 0; compared exactly (times lam_den * max l * L)
+ *   SMETRIC_SCORE_HIT_FILTER Preble: when some instance holds more than half the prompt
+ *                            (2 B c[i] > L), the least loaded such instance (argmin l);
+ *                            otherwise the weighted sum with the same lam
+ * Every argmin breaks ties by smetric_route's rotation order: the first instance met
+ * walking start, start + 1, ... (mod n_instances), start = (rr_base + r) mod n_instances.
+ *   matched     int32[n_req * n_instances]  from smetric_match
+ *   prompt_len  int32[n_req]                L, tokens
+ *   q           int64[n_instances]          queued prefill per instance, tokens
+ *   load        int32[n_instances]          the instance's load: its batch size (requests
+ *                                           running there)
+ *   target      int32[n_req] (out); branch uint8[n_req] (out): SMETRIC_SCORED, or
+ *               SMETRIC_HIT_FILTER when the hit filter chose
+ * A request with L < 0 or > 2^24, some c[i] < 0 or > L / B, some q[i] < 0 or >= 2^62, or
+ * some load[i] < 0 gets target -1, branch SMETRIC_INVALID.
+ * Host errors: EINVAL for kind outside the five, n_req < 0, n_instances outside
+ * [1, 65536], block_size not even in [2, 256], and (LINEAR and HIT_FILTER only)
+ * lam_den <= 0 or lam_num outside [0, lam_den].
+ * --------------------------------------------------------------------------------- */
+enum { SMETRIC_SCORE_LOAD = 0, SMETRIC_SCORE_TOKENS = 1, SMETRIC_SCORE_PRODUCT = 2, SMETRIC_SCORE_LINEAR = 3,
+       SMETRIC_SCORE_HIT_FILTER = 4 };
+int smetric_route_score(int32_t kind, const int32_t *matched, int32_t n_req, int32_t n_instances,
+                        const int32_t *prompt_len, const int64_t *q, const int32_t *load, int32_t block_size,
+                        int32_t lam_num, int32_t lam_den, uint64_t rr_base, int32_t *target, uint8_t *branch,
+                        hipStream_t stream);
 
 /* ---------------------------------------------------------------------------------
  * Post-route insert: every full block of request r goes on instance[r] (the routed

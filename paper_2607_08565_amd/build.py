@@ -11,7 +11,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsmetric.so")
-SOURCES = ["hash.hip", "probe.hip", "match.hip", "route.hip", "index.hip", "session.hip", "metrics.hip"]
+SOURCES = ["hash.hip", "probe.hip", "match.hip", "route.hip", "index.hip", "session.hip", "metrics.hip", "score.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

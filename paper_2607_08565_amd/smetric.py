@@ -86,6 +86,7 @@ def _load() -> C.CDLL:
         "smetric_hash_partition": [P, I64, P, P, I32, I64, I32, U64, P, P, PIX, P, U64, P],
         "smetric_match_probed": [PIX, P, U64, P, P, I32, I64, P, P],
         "smetric_index_insert_probed": [PIX, P, U64, I32, I64, P, P, U32, P, U64, P],
+        "smetric_route_score": [I32, P, I32, I32, P, P, P, I32, I32, I32, U64, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -105,7 +106,7 @@ EXPORTED = (
     "smetric_sessions", "smetric_route_loadaware", "smetric_imbalance_ws_bytes", "smetric_imbalance",
     "smetric_probe_partition", "smetric_probe_lookup", "smetric_hash_partition", "smetric_route_seq_coloc",
     "smetric_route_seq_coloc_ws_bytes", "smetric_route_seq_noalloc", "smetric_route_seq_noalloc_max_req",
-    "smetric_probe_stats",
+    "smetric_probe_stats", "smetric_route_score",
 )
 
 
@@ -332,6 +333,26 @@ def route_coloc(matched: torch.Tensor, prompt_len: torch.Tensor, hist_len: torch
         C.byref(p), C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"),
         _stream()))
     return target[:R], branch[:R]
+
+# Scorer kinds of smetric_route_score (Sec. 4.1 scoring template).
+SCORE_LOAD, SCORE_TOKENS, SCORE_PRODUCT, SCORE_LINEAR, SCORE_HIT_FILTER = range(5)
+
+
+def route_score(kind: int, matched: torch.Tensor, prompt_len: torch.Tensor, q: torch.Tensor, load: torch.Tensor,
+                block_size: int, lam: tuple[int, int] = (0, 1), rr_base: int = 0,
+                target: torch.Tensor | None = None, branch: torch.Tensor | None = None):
+    """smetric_route_score: argmin of a comparison scorer (q in tokens, load int32 batch
+    sizes, lam = (num, den) for the weighted sum and the hit filter)."""
+    R, I = matched.shape
+    dev = matched.device
+    target = torch.empty(max(R, 1), dtype=torch.int32, device=dev) if target is None else target
+    branch = torch.empty(max(R, 1), dtype=torch.uint8, device=dev) if branch is None else branch
+    _check("smetric_route_score", _lib.smetric_route_score(
+        int(kind), _dev(matched, torch.int32, "matched"), R, I, _dev(prompt_len, torch.int32, "prompt_len"),
+        _dev(q, torch.int64, "q"), _dev(load, torch.int32, "load"), int(block_size), int(lam[0]), int(lam[1]),
+        C.c_uint64(rr_base), _dev(target, torch.int32, "target"), _dev(branch, torch.uint8, "branch"), _stream()))
+    return target[:R], branch[:R]
+
 
 def insert_ws_bytes(n_blocks: int) -> int:
     b = C.c_uint64()
