@@ -685,6 +685,33 @@ def measure_variants(setup, b: int, reps: int = 20):
     out["route_loadaware"] = {"rule": "Sec. 5.4 ablation: stick unless prev's load > 1.5 x mean",
                               "ms": round(ms, 4), "branches": np.bincount(br.cpu().numpy(), minlength=5).tolist()}
     inputs["route_loadaware"] = (load.cpu().numpy(), la_t, br.cpu().numpy(), b)
+    # the comparison scorers of the scoring template (Sec. 4.1, Sec. 5) on the same rows:
+    # queued prefill in tokens (the queue's ns over C_LIN), load = requests running,
+    # lam = 9/10 (a weight that favours reuse, as set for agentic workloads)
+    q_tok = d["q"] // W.DEFAULT_PARAMS["c_lin"]
+    B = W.DEFAULT_PARAMS["block_size"]
+    lam = (9, 10)
+    names = {S.SCORE_LOAD: "load_only", S.SCORE_TOKENS: "tokens_left_dynamo", S.SCORE_PRODUCT: "product_lmetric",
+             S.SCORE_LINEAR: "weighted_sum", S.SCORE_HIT_FILTER: "hit_filter_preble"}
+    sc_out, sc_in, sc_targets = {}, {}, {}
+    for kind, name in names.items():
+        call = lambda: S.route_score(kind, setup.matched, d["prompt_len"], q_tok, d_run, B, lam, tb.batch.rr_base,
+                                     target=tgt, branch=br)
+        call()
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        st, sb = tgt.cpu().numpy(), br.cpu().numpy()
+        sc_out[name] = {"ms": round(ms, 4), "same_target_as_smetric_batch": int((st == snap_t).sum()),
+                        "hit_filter_decisions": int((sb == 7).sum())}
+        sc_in[kind] = (st, sb)
+        sc_targets[name] = st
+    out["route_score"] = {"rule": "Sec. 4.1 scoring template: argmin of a comparison scorer, lam = 9/10",
+                          "scorers": sc_out}
+    inputs["route_score"] = (q_tok.cpu().numpy(), lam, sc_in, b)
     # load imbalance (Sec. 4.1) of the batch-snapshot and the load-aware decisions: arrivals
     # spread over 10 min, each request running 20 s, 30 s windows
     rng = np.random.default_rng(b)
@@ -692,7 +719,7 @@ def measure_variants(setup, b: int, reps: int = 20):
     d_t0 = torch.from_numpy(t0).cuda()
     d_t1 = d_t0 + 20_000
     imb = {}
-    for name, tg in (("smetric_batch", snap_t), ("loadaware", la_t)):
+    for name, tg in (("smetric_batch", snap_t), ("loadaware", la_t), *sc_targets.items()):
         gs, gm, _ = S.imbalance(torch.from_numpy(tg.astype(np.int32)).cuda(), d_t0, d_t1, I, 30_000, 21)
         gs, gm = gs.cpu().numpy(), gm.cpu().numpy()
         ratio = gm * I / np.maximum(gs, 1)
@@ -761,6 +788,16 @@ def variants_parity(setup, inputs) -> dict:
     ot, ob = oracle.route_loadaware(setup.matched.cpu().numpy(), bt.prompt_len, bt.hist_len, bt.turn, bt.q, load,
                                     (1, 2), setup.W.DEFAULT_PARAMS, bt.rr_base)
     res["route_loadaware"] = {"requests": int(len(ot)), "bit_exact": bool(np.array_equal(ot, gt) and np.array_equal(ob, gb))}
+    q_tok, lam, sc_in, b = inputs["route_score"]
+    bt = setup.host[b].batch
+    n_run = inputs["route_coloc"][1]
+    m = setup.matched.cpu().numpy()
+    exact = True
+    for kind, (gt, gb) in sc_in.items():
+        ot, ob = oracle.route_score(kind, m, bt.prompt_len, q_tok, n_run, setup.W.DEFAULT_PARAMS["block_size"], lam,
+                                    bt.rr_base)
+        exact = exact and bool(np.array_equal(ot, gt) and np.array_equal(ob, gb))
+    res["route_score"] = {"requests": int(len(bt.prompt_len)), "scorers": len(sc_in), "bit_exact": exact}
     tr, blk_off, gp, gs = inputs["sessions"]
     ob, ok = oracle.hash_blocks(tr.tokens, tr.tok_off, setup.W.BLOCK, setup.W.DEFAULT_SEED)
     op, os_ = oracle.sessions(ok, ob, tr.user, tr.turn)
