@@ -4,9 +4,10 @@ batches that vary everything at once: instance counts around the 64-lane wave an
 empty prompts), hit rows from none to whole prompts (one instance holding most of a prompt,
 an out-of-domain hit), loads from a few queued requests to just under 2^62 ns, every cost
 and SLO parameter from 0 to its 2^32 limit, SLACK from 0 to unbounded, and 64-bit
-round-robin bases.  The batch rule and its colocation variant, and both online rules
-(final loads and request counts included); a batch the online rules cannot take within
-their 128-bit bound is refused with EINVAL on both sides of the check."""
+round-robin bases.  The batch rule and its colocation variant, both online rules (final
+loads and request counts included), and the five comparison scorers with a random lam; a
+batch the online rules cannot take within their 128-bit bound is refused with EINVAL on
+both sides of the check."""
 import numpy as np
 import pytest
 
@@ -74,6 +75,12 @@ def test_route_rules_on_random_batches(chunk):
         _online(S.route_seq, oracle.route_seq, (args, (m, L, hist, turn, q)), (), p, rr, R, f"route_seq, seed {seed}")
         _online(S.route_seq_coloc, oracle.route_seq_coloc, (args, (m, L, hist, turn, q)),
                 ((to_dev(slack), to_dev(n_run)), (slack, n_run)), p, rr, R, f"route_seq_coloc, seed {seed}")
+        lam_den = 1 + seed % 97
+        lam = ((seed * 7) % (lam_den + 1), lam_den)
+        for kind in range(5):
+            assert _same(R, S.route_score(kind, args[0], args[1], args[4], to_dev(n_run), p["block_size"], lam, rr),
+                         oracle.route_score(kind, m, L, q, n_run, p["block_size"], lam, rr)), \
+                f"route_score kind {kind}, seed {seed}"
 
 
 def _online(gpu_fn, oracle_fn, base, extra, p, rr, R, what):
