@@ -11,8 +11,10 @@
 // stays integral, and products are formed in 128 bits.
 //
 // Mapping to gfx950: one wavefront per request; lane l scans instances l, l+64, ...,
-// keeping (max c, lowest id) and (min est2, rotation distance); two butterfly
-// reductions across the wavefront finish the argmax and the argmin; lane 0 decides.
+// keeping (max c, lowest id, its est2) and (min est2, rotation distance); two butterfly
+// reductions across the wavefront finish the argmax and the argmin; lane 0 decides.  The
+// main rule's scan runs in double precision while that is exact (every score an integer
+// below 2^51), which cuts the kernel's vector instructions by more than a third.
 #include <mutex>
 
 #include "common.h"
@@ -38,6 +40,13 @@ __device__ __forceinline__ i128 est2(const RouteParams &p, int64_t L, int32_t c,
   const uint64_t w = n * (uint64_t(2 * L) - n);
   typedef unsigned __int128 u128_;
   return i128(2) * q + i128(uint64_t(2 * p.c_lin) * n) + i128(u128_(uint64_t(p.c_att)) * w);
+}
+
+__device__ __forceinline__ double shfl_xor_f64(double v, int m) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = uint32_t(__shfl_xor(int(uint32_t(b)), m, 64));
+  const uint32_t hi = uint32_t(__shfl_xor(int(uint32_t(b >> 32)), m, 64));
+  return __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
 }
 
 __device__ __forceinline__ i128 shfl_xor128(i128 v, int m) {
@@ -75,11 +84,82 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
   const int32_t start = int32_t((rr_base % uint64_t(I) + uint64_t(r) % uint64_t(I)) % uint64_t(I));
 
   int32_t best_c = -1, best_ci = 0x7FFFFFFF;  // argmax c, lowest id
+  i128 prev_e = 0;                            // est2 of that instance
   i128 best_e = 0;
   int32_t best_d = 0x7FFFFFFF;                // argmin (est2, rotation distance)
   i128 load_sum = 0;                          // RULE 1
+  // Fast scan, exact in doubles: with n = L - B c, est2 = 2q + C0 - c (a1 + a2 c) where
+  // C0 = 2 C_LIN L + C_ATT L^2, a1 = 2 C_LIN B and a2 = C_ATT B^2 (at most 2^41 and 2^48 for
+  // parameters in range).  While C0 and every 2q stay below 2^50, each in-domain score is an
+  // integer below 2^51 (and c (a1 + a2 c) <= C0), so two fused multiply-adds give it
+  // exactly and doubles compare it exactly.  A wavefront that meets a larger queue scans
+  // again in 128 bits.
+  const i128 c0 = i128(2) * p.c_lin * L + i128(p.c_att) * L * L;
+  bool fast = RULE == 0 && ok && c0 < (i128(1) << 50);
+  if (fast) {
+    const double a1 = double(2 * p.c_lin * p.B), a2 = double(p.c_att * p.B * p.B), c0d = double(int64_t(c0));
+    double bs = 0.0, ps = 0.0;
+    bool small = true;
+    for (int32_t i0 = lane; i0 < I; i0 += 64 * RU) {
+      int32_t cv[RU];
+      int64_t qv[RU];
+#pragma unroll
+      for (int u = 0; u < RU; ++u) {
+        const int32_t ii = i0 + 64 * u < I ? i0 + 64 * u : I - 1;
+        cv[u] = c[ii];
+        qv[u] = q[ii];
+      }
+#pragma unroll
+      for (int u = 0; u < RU; ++u) {
+        const int32_t i = i0 + 64 * u;
+        if (i >= I) break;
+        const int32_t ci = cv[u];
+        const int64_t qi = qv[u];
+        if (ci < 0 || ci > max_c || qi < 0 || qi >= (int64_t(1) << 62)) ok = false;
+        small = small && uint64_t(qi) < (uint64_t(1) << 49);
+        const double cd = double(ci);
+        const double sc = __builtin_fma(-cd, __builtin_fma(a2, cd, a1), c0d + 2.0 * double(qi));
+        if (ci > best_c) {
+          best_c = ci;
+          best_ci = i;
+          ps = sc;
+        }
+        const int32_t d = i >= start ? i - start : i - start + I;
+        if (best_d == 0x7FFFFFFF || sc < bs || (sc == bs && d < best_d)) {
+          bs = sc;
+          best_d = d;
+        }
+      }
+    }
+    fast = __ballot(!small) == 0;
+    if (fast) {
+      ok = __ballot(!ok) == 0;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const int32_t oc = __shfl_xor(best_c, m, 64), oi = __shfl_xor(best_ci, m, 64);
+        const double ops = shfl_xor_f64(ps, m), obs = shfl_xor_f64(bs, m);
+        const int32_t od = __shfl_xor(best_d, m, 64);
+        if (oc > best_c || (oc == best_c && oi < best_ci)) {
+          best_c = oc;
+          best_ci = oi;
+          ps = ops;
+        }
+        if (od != 0x7FFFFFFF && (best_d == 0x7FFFFFFF || obs < bs || (obs == bs && od < best_d))) {
+          bs = obs;
+          best_d = od;
+        }
+      }
+      prev_e = i128(int64_t(ps));
+      best_e = i128(int64_t(bs));
+    } else {  // back to the 128-bit scan from the start
+      ok = L >= 0 && L <= (int64_t(1) << 24) && hist >= 0 && tr >= 0;
+      best_c = -1;
+      best_ci = 0x7FFFFFFF;
+      best_d = 0x7FFFFFFF;
+    }
+  }
   // RU instances per lane at a time, their loads issued first (clamped, so branch-free)
-  for (int32_t i0 = lane; i0 < I; i0 += 64 * RU) {
+  for (int32_t i0 = lane; !fast && i0 < I; i0 += 64 * RU) {
     int32_t cv[RU];
     int64_t qv[RU], lv[RU];
 #pragma unroll
@@ -101,11 +181,12 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
         if (li < 0 || li >= (int64_t(1) << 62)) ok = false;
         load_sum += li;
       }
+      const i128 e = est2(p, L, ci, qi);
       if (ci > best_c) {
         best_c = ci;
         best_ci = i;
+        prev_e = e;
       }
-      const i128 e = est2(p, L, ci, qi);
       const int32_t d = i >= start ? i - start : i - start + I;
       if (best_d == 0x7FFFFFFF || e < best_e || (e == best_e && d < best_d)) {
         best_e = e;
@@ -113,13 +194,15 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
       }
     }
   }
-  ok = __ballot(!ok) == 0;
+  if (!fast) ok = __ballot(!ok) == 0;
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
+  for (int m = 32; m >= 1 && !fast; m >>= 1) {
     const int32_t oc = __shfl_xor(best_c, m, 64), oi = __shfl_xor(best_ci, m, 64);
+    const i128 ope = shfl_xor128(prev_e, m);
     if (oc > best_c || (oc == best_c && oi < best_ci)) {
       best_c = oc;
       best_ci = oi;
+      prev_e = ope;
     }
     const i128 oe = shfl_xor128(best_e, m);
     const int32_t od = __shfl_xor(best_d, m, 64);
@@ -139,10 +222,9 @@ __global__ __launch_bounds__(64 * RW) void route_kernel(const int32_t *__restric
   const int32_t bal = (start + best_d) % I;
   const i128 bound2 = i128(2) * (i128(p.slo_b) + i128(p.slo_a) * L);
   const bool slack_inf = p.slack_den == 0;
-  const i128 e_prev = est2(p, L, c[prev], q[prev]);
-  const bool meets_prev = slack_inf || e_prev * p.slack_den <= i128(p.slack_num) * bound2;
+  const bool meets_prev = slack_inf || prev_e * p.slack_den <= i128(p.slack_num) * bound2;
   const bool none_meets = !slack_inf && best_e * p.slack_den > i128(p.slack_num) * bound2;
-  const bool cached = i128(p.B) * c[prev] * p.hit_den > i128(p.hit_num) * hist;
+  const bool cached = i128(p.B) * best_c * p.hit_den > i128(p.hit_num) * hist;
   int32_t t;
   uint8_t br;
   if (RULE == 1) {

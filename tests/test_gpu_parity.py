@@ -509,6 +509,46 @@ def test_route_edge_parameters():
         S.route(to_dev(m), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), dict(W.DEFAULT_PARAMS, hit_num=2, hit_den=2))
 
 
+def test_route_scan_precision_boundaries():
+    """The route scans in doubles while C0 = 2 C_LIN L + C_ATT L^2 and every 2q stay below
+    2^50 (each score is then an integer below 2^51) and in 128 bits otherwise: prompts whose
+    C0 falls just under and at 2^50 (C_ATT = C_LIN = 2^32, L around 511-512), queues just
+    under and at 2^49 on some instances, exact ties between instances, and wavefronts that
+    switch to 128 bits with an out-of-domain request among them."""
+    from paper_2607_08565_amd import smetric as S
+    rng = np.random.default_rng(14)
+    big = dict(W.DEFAULT_PARAMS, c_lin=1 << 32, c_att=1 << 32, slo_b=1 << 32, slo_a=1 << 32,
+               slack_num=1 << 20, slack_den=1, block_size=16)
+    for I in (1, 37, 64, 65, 1024, 1500):
+        R = 400
+        L = rng.integers(500, 520, R).astype(np.int32)
+        m = rng.integers(0, 33, (R, I))
+        m = np.minimum(m, (L // 16)[:, None]).astype(np.int32)
+        m[:, ::3] = m[:, :1]  # ties on c, so ties on the scores
+        hist = rng.integers(0, 520, R).astype(np.int32)
+        turn = rng.integers(0, 3, R).astype(np.int32)
+        for qcase in range(4):
+            if qcase == 0:    # all far below 2^49
+                q = rng.integers(0, 1 << 30, I)
+            elif qcase == 1:  # up to 2^49 - 1: the double scan
+                q = rng.integers((1 << 49) - 4096, 1 << 49, I)
+            elif qcase == 2:  # one instance at 2^49: the 128-bit scan
+                q = rng.integers((1 << 49) - 4096, 1 << 49, I)
+                q[rng.integers(0, I)] = 1 << 49
+            else:             # equal queues, every tie down to the rotation
+                q = np.full(I, (1 << 49) - 1)
+            q = q.astype(np.int64)
+            for p in (big, dict(big, c_att=(1 << 32) - 1), dict(big, c_lin=0), W.DEFAULT_PARAMS):
+                m2 = m.copy()
+                m2[7, 0] = 1 << 20  # an out-of-domain request
+                for rr in (0, 2**64 - 1):
+                    gt, gb = S.route(to_dev(m2), to_dev(L), to_dev(hist), to_dev(turn), to_dev(q), p, rr)
+                    ot, ob = oracle.route(m2, L, hist, turn, q, p, rr)
+                    assert np.array_equal(gt.cpu().numpy(), ot) and np.array_equal(gb.cpu().numpy(), ob), \
+                        (I, qcase, p["c_lin"], p["c_att"], rr)
+                assert ob[7] == 255
+
+
 def test_probed_path_rejects_untiled_requests():
     """The region-ordered path needs requests that tile the keys; otherwise every row is
     zero, the status is EINVAL and the insert changes nothing."""
