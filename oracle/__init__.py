@@ -24,7 +24,8 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 _LIB_OVERRIDE = os.environ.get("SMETRIC_ORACLE_LIB")
 
 OK, EINVAL, EFULL = 0, -1, -2
-BRANCH_NAMES = {0: "first-turn", 1: "evicted", 2: "stick", 3: "last-resort", 4: "migrate", 255: "invalid"}
+BRANCH_NAMES = {0: "first-turn", 1: "evicted", 2: "stick", 3: "last-resort", 4: "migrate", 5: "migrate-tpot",
+                6: "scored", 7: "hit-filter", 255: "invalid"}
 
 
 def build(extra_flags: tuple[str, ...] = (), out: str | None = None) -> str:
