@@ -294,10 +294,9 @@ class Setup:
 
 # kernels each timed call launches, in order (names as rocprofv3 reports them)
 CALL_KERNELS = {
-    # smetric_hash_partition: the block keys, the hash itself taking the region counts,
-    # then the region partition's scan and scatter
-    "hash": ["zero_kernel", "zero_kernel", "req_of_kernel", "hash16_kernel<8, true>", "part_scan_kernel",
-             "part_scatter_kernel"],
+    # smetric_hash_partition: the state cleared, the block keys (the hash itself taking the
+    # region counts), each block's request, then the region partition's scan and scatter
+    "hash": ["zero2_kernel", "hash16_kernel<8, true>", "req_of_kernel", "part_scan_kernel", "part_scatter_kernel"],
     # smetric_probe_lookup: each request's probe bound, then one holder descriptor per block,
     # in region order
     "probe": ["zero32_kernel", "zero_kernel", "bound_kernel", "probe_kernel<2>"],

@@ -323,14 +323,14 @@ inline uint64_t probe_layout(int64_t n_blocks, ProbeView *v, void *base) {
 
 // Region partition of a probe state, shared by smetric_probe_partition and the hash call
 // that counts the regions itself (defined with the probe).  partition_head clears the
-// state (and the [chunk][region] counts when the hash is to add into them) and checks the
-// tiling; partition_tail counts (unless counted), scans and scatters.
+// state (and the [chunk][region] counts when the hash is to add into them) in one launch;
+// partition_tail checks the tiling and maps blocks to requests, counts (unless counted),
+// scans and scatters.
 int probe_state_args(const smetric_index *idx, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
                      int64_t n_blocks, void *probe, uint64_t probe_bytes);
-void partition_head(ProbeView &pv, const int64_t *blk_off, int32_t n_req, int64_t n_blocks, bool clear_hist,
-                    hipStream_t stream);
-int partition_tail(const DevIndex &ix, ProbeView &pv, const uint64_t *keys, uint64_t n, bool counted,
-                   hipStream_t stream);
+void partition_head(ProbeView &pv, bool clear_hist, hipStream_t stream);
+int partition_tail(const DevIndex &ix, ProbeView &pv, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                   uint64_t n, bool counted, hipStream_t stream);
 inline uint64_t partition_chunk(uint64_t n) { return n ? (n + PART_WG - 1) / PART_WG : 1; }
 
 // Sizing shared by host code.

@@ -351,7 +351,7 @@ extern "C" int smetric_hash_partition(const int32_t *tokens, int64_t n_tokens, c
   probe_layout(n_blocks, &pv, probe);
   const DevIndex ix = dev_view(idx);  // geometry only
   const bool counted = block_size == 16 && n_req > 0;
-  partition_head(pv, blk_off, n_req, n_blocks, counted, stream);
+  partition_head(pv, counted, stream);
   if (counted)
     hipLaunchKernelGGL((hash16_kernel<HASH_NW, true>), dim3(n_req), dim3(64 * HASH_NW), 0, stream, tokens, n_tokens,
                        tok_off, blk_off, n_req, n_blocks, seed, keys, status, pv.hist, ix.n_buckets, ix.nb_inv,
@@ -359,7 +359,7 @@ extern "C" int smetric_hash_partition(const int32_t *tokens, int64_t n_tokens, c
   else if (n_req > 0)
     hipLaunchKernelGGL(hash_generic_kernel, dim3((n_req + WAVES - 1) / WAVES), dim3(64 * WAVES), 0, stream, tokens,
                        n_tokens, tok_off, blk_off, n_req, n_blocks, int(block_size), seed, keys, status);
-  return partition_tail(ix, pv, keys, uint64_t(n_blocks), counted, stream);
+  return partition_tail(ix, pv, keys, blk_off, n_req, uint64_t(n_blocks), counted, stream);
 }
 
 extern "C" int smetric_block_offsets(const int64_t *tok_off, int32_t n_req, int32_t block_size,

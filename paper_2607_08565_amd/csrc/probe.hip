@@ -38,6 +38,15 @@ __global__ void zero_kernel(uint64_t *p, uint64_t n_words) {
   for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_words; i += stride) p[i] = 0;
 }
 
+// two ranges cleared by one launch
+__global__ void zero2_kernel(uint64_t *p, uint64_t n_words, uint64_t *p2, uint64_t n_words2) {
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_words + n_words2; i += stride) {
+    if (i < n_words) p[i] = 0;
+    else p2[i - n_words] = 0;
+  }
+}
+
 __global__ __launch_bounds__(64) void req_of_kernel(ProbeView pv, const int64_t *__restrict__ blk_off, int32_t n_req,
                                                     int64_t n_blocks) {
   const int r = blockIdx.x, lane = threadIdx.x;
@@ -544,19 +553,17 @@ int probe_state_args(const smetric_index *idx, const uint64_t *keys, const int64
   return probe_args(idx, keys, blk_off, n_req, n_blocks, probe, probe_bytes);
 }
 
-void partition_head(ProbeView &pv, const int64_t *blk_off, int32_t n_req, int64_t n_blocks, bool clear_hist,
-                    hipStream_t stream) {
-  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hdr),
-                     uint64_t(sizeof(ProbeHdr) / 8));
-  if (clear_hist)
-    hipLaunchKernelGGL(zero_kernel, dim3(16), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hist),
-                       uint64_t(PART_WG) * NREG / 2);
-  if (n_req > 0)
-    hipLaunchKernelGGL(req_of_kernel, dim3(n_req), dim3(64), 0, stream, pv, blk_off, n_req, n_blocks);
+void partition_head(ProbeView &pv, bool clear_hist, hipStream_t stream) {
+  hipLaunchKernelGGL(zero2_kernel, dim3(16), dim3(TB), 0, stream, reinterpret_cast<uint64_t *>(pv.hdr),
+                     uint64_t(sizeof(ProbeHdr) / 8), reinterpret_cast<uint64_t *>(pv.hist),
+                     clear_hist ? uint64_t(PART_WG) * NREG / 2 : uint64_t(0));
 }
 
-int partition_tail(const DevIndex &ix, ProbeView &pv, const uint64_t *keys, uint64_t n, bool counted,
-                   hipStream_t stream) {
+int partition_tail(const DevIndex &ix, ProbeView &pv, const uint64_t *keys, const int64_t *blk_off, int32_t n_req,
+                   uint64_t n, bool counted, hipStream_t stream) {
+  // launched after the hash in the fused call, so that the hash starts right after the clear
+  if (n_req > 0)
+    hipLaunchKernelGGL(req_of_kernel, dim3(n_req), dim3(64), 0, stream, pv, blk_off, n_req, int64_t(n));
   if (!counted) hipLaunchKernelGGL(part_count_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
   hipLaunchKernelGGL(part_scan_kernel, dim3(NREG), dim3(TB), 0, stream, pv);
   hipLaunchKernelGGL(part_scatter_kernel, dim3(PART_WG), dim3(TB), 0, stream, ix, pv, keys, n);
@@ -571,8 +578,8 @@ extern "C" int smetric_probe_partition(const smetric_index *idx, const uint64_t 
   ProbeView pv;
   probe_layout(n_blocks, &pv, probe);
   const DevIndex ix = dev_view(idx);  // geometry only: the table's contents are not read here
-  partition_head(pv, blk_off, n_req, n_blocks, false, stream);
-  return partition_tail(ix, pv, keys, uint64_t(n_blocks), false, stream);
+  partition_head(pv, false, stream);
+  return partition_tail(ix, pv, keys, blk_off, n_req, uint64_t(n_blocks), false, stream);
 }
 
 extern "C" int smetric_probe_lookup(const smetric_index *idx, void *probe, uint64_t probe_bytes,

@@ -8,10 +8,10 @@
 // that weighted sum.  The exact integer forms are stated with smetric_route_score.
 //
 // Mapping to gfx950: one wavefront per request, as in the main route.  Lane l scores
-// instances l, l + 64, ... (four rows' loads issued together) and keeps the minimum of
-// (score, rotation distance) -- and, for the hit filter, of (load, rotation distance) over
-// the instances holding more than half the prompt; a butterfly across the wavefront
-// finishes both and lane 0 writes the decision.  The weighted sum's normaliser (the
+// instances l, l + 64, ... (the loads of four of them issued together) and keeps the
+// minimum of (score, rotation distance) -- and, for the hit filter, of (load, rotation
+// distance) over the instances holding more than half the prompt; a butterfly across the
+// wavefront finishes both and lane 0 writes the decision.  The weighted sum's normaliser (the
 // cluster's largest load) is reduced once per workgroup into LDS.  Scores that fit 64 bits
 // (load, tokens) stay 64-bit; the product and the weighted sum are formed in 128 bits.
 #include <type_traits>
