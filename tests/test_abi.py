@@ -64,3 +64,19 @@ def test_host_side_errors_without_gpu():
     for bad in ((-1, 8), (10, 0), (10, 4097)):
         with pytest.raises(S.SmetricError):
             S.route_seq_coloc_ws_bytes(*bad)
+
+
+def test_route_score_host_checks_without_gpu():
+    """smetric_route_score rejects bad scalars on the host, before any launch, and an empty
+    batch returns at once (nothing is enqueued, so no GPU is needed)."""
+    from paper_2607_08565_amd import smetric as S
+    f = S._lib.smetric_route_score
+    call = lambda kind, n_req, I, B, lam: f(kind, None, n_req, I, None, None, None, B, lam[0], lam[1], 0, None, None,
+                                           None)
+    assert call(0, 0, 8, 16, (0, 0)) == S.OK                   # empty batch; lam unused by kind 0
+    assert call(3, 0, 8, 16, (1, 2)) == S.OK
+    for args in ((5, 0, 8, 16, (0, 1)), (-1, 0, 8, 16, (0, 1)), (0, -1, 8, 16, (0, 1)), (0, 0, 0, 16, (0, 1)),
+                 (0, 0, 65537, 16, (0, 1)), (0, 0, 8, 3, (0, 1)), (0, 0, 8, 258, (0, 1)), (3, 0, 8, 16, (2, 1)),
+                 (4, 0, 8, 16, (0, 0)), (3, 0, 8, 16, (-1, 2))):
+        assert call(*args) == S.EINVAL, args
+    assert call(1, 4, 8, 16, (0, 1)) == S.EINVAL               # null device pointers
