@@ -299,12 +299,12 @@ CALL_KERNELS = {
     "hash": ["zero2_kernel", "hash16_kernel<8, true>", "req_of_kernel", "part_scan_kernel", "part_scatter_kernel"],
     # smetric_probe_lookup: each request's probe bound, then one holder descriptor per block,
     # in region order
-    "probe": ["zero32_kernel", "zero_kernel", "bound_kernel", "probe_kernel<2>"],
+    "probe": ["zero2_kernel", "bound_kernel", "probe_kernel<2>"],
     "match": ["match_kernel<1, true>"],
     "route": ["route_kernel<0>"],
     "insert": ["fill_kernel", "insp_valid_kernel", "insp_classify_kernel", "insp_size_kernel", "insp_bcount_kernel",
-               "insp_bscan_kernel", "insp_size2_kernel", "dd_clear_kernel", "insp_bscatter_kernel",
-               "insp_bdedupe_kernel", "insp_check_kernel", "insp_refresh_kernel", "insp_place_kernel", "spill_kernel",
+               "insp_bscan_kernel", "insp_size2_kernel", "insp_bscatter_kernel",
+               "insp_bdedupe_kernel", "insp_check_kernel", "insp_place_kernel", "spill_kernel",
                "deferred_kernel"],
 }
 

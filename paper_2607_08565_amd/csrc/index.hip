@@ -1026,7 +1026,8 @@ __global__ __launch_bounds__(SCAN_T) void insp_bscan_kernel(InsWs ws) {
   }
 }
 
-// fallback pair-table size for the oversized bins: a power of two >= 2 x their candidates
+// fallback pair-table size for the oversized bins: a power of two >= 2 x their candidates;
+// every thread sizes it (no separate launch), the first records it, all clear its slots
 __global__ void insp_size2_kernel(InsWs ws) {
   const unsigned long long c = ws.hdr->n_over;
   uint64_t nd = 0;
@@ -1034,7 +1035,10 @@ __global__ void insp_size2_kernel(InsWs ws) {
     nd = 64;
     while (nd < 2 * c && nd < ws.n_dedupe) nd <<= 1;
   }
-  ws.hdr->n_dd2 = nd;
+  const uint64_t t0 = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t0 == 0) ws.hdr->n_dd2 = nd;
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
+  for (uint64_t h = t0; h < nd; h += stride) ws.dd[h] = DSlot{0, 0};
 }
 
 __global__ void dd_clear_kernel(DSlot *dd, uint64_t n, const unsigned long long *n_dev) {
@@ -1252,8 +1256,10 @@ __global__ __launch_bounds__(TB) void insp_check_kernel(DevIndex ix, InsWs ws) {
   }
 }
 
-__global__ __launch_bounds__(TB) void insp_refresh_kernel(DevIndex ix, ProbeView pv, InsWs ws, uint32_t epoch) {
-  if (ws.hdr->abort || ws.hdr->inl) return;
+// The refreshes, when the classify pass could not do them (run by the placement's grid
+// after its pairs: placement claims only empty slots, so the two never touch one value
+// except an entry that both raise to the same epoch).
+__device__ void refresh_pass(const DevIndex &ix, const ProbeView &pv, const InsWs &ws, uint32_t epoch) {
   const uint64_t n = pv.hdr->n;
   const uint64_t span = uint64_t(gridDim.x) * TB;
   for (uint64_t i = uint64_t(blockIdx.x) * TB + threadIdx.x; i < n; i += span) {
@@ -1267,8 +1273,8 @@ __global__ __launch_bounds__(TB) void insp_refresh_kernel(DevIndex ix, ProbeView
 
 // place: the distinct new pairs in bin order (so in region order), all FLAT_WG
 // workgroups advancing through it together
-__global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, const uint32_t *session,
-                                                        uint32_t epoch) {
+__global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, ProbeView pv, InsWs ws,
+                                                        const uint32_t *session, uint32_t epoch) {
   if (ws.hdr->abort) return;
   const uint64_t n = ws.hdr->n_cand;
   const uint64_t span = uint64_t(gridDim.x) * TB;
@@ -1292,6 +1298,7 @@ __global__ __launch_bounds__(TB) void insp_place_kernel(DevIndex ix, InsWs ws, c
     append_wave(&ws.hdr->n_trig, ws.trig, ws.list_cap, tk);  // queue by np position
     append_wave(&ws.hdr->n_def, ws.def, ws.list_cap, df);
   }
+  if (!ws.hdr->inl) refresh_pass(ix, pv, ws, epoch);
 }
 
 // ---------------------------------------------------------------------------------
@@ -2086,14 +2093,11 @@ extern "C" int smetric_index_insert_probed(smetric_index *idx, const void *probe
   hipLaunchKernelGGL(insp_size_kernel, dim3(1), blk, 0, stream, ws);
   hipLaunchKernelGGL(insp_bcount_kernel, chunks, blk, 0, stream, ix, ws);
   hipLaunchKernelGGL(insp_bscan_kernel, dim3(NREG), dim3(SCAN_T), 0, stream, ws);
-  hipLaunchKernelGGL(insp_size2_kernel, dim3(1), dim3(1), 0, stream, ws);
-  hipLaunchKernelGGL(dd_clear_kernel, dim3(grid_for(ws.n_dedupe)), blk, 0, stream, ws.dd, ws.n_dedupe,
-                     &ws.hdr->n_dd2);
+  hipLaunchKernelGGL(insp_size2_kernel, dim3(grid_for(ws.n_dedupe)), blk, 0, stream, ws);
   hipLaunchKernelGGL(insp_bscatter_kernel, chunks, blk, 0, stream, ix, ws);
   hipLaunchKernelGGL(insp_bdedupe_kernel, flat, dim3(DD_T), 0, stream, ws);
   hipLaunchKernelGGL(insp_check_kernel, dim3(1), blk, 0, stream, ix, ws);
-  hipLaunchKernelGGL(insp_refresh_kernel, flat, blk, 0, stream, ix, pv, ws, epoch);
-  hipLaunchKernelGGL(insp_place_kernel, dim3(PLACE_WG), blk, 0, stream, ix, ws, session, epoch);
+  hipLaunchKernelGGL(insp_place_kernel, dim3(PLACE_WG), blk, 0, stream, ix, pv, ws, session, epoch);
   hipLaunchKernelGGL(spill_kernel, dim3(64), blk, 0, stream, ix, ws.trig, &ws.hdr->n_trig, &ws.hdr->abort,
                      nullptr, nullptr, nullptr, ws.np);
   hipLaunchKernelGGL(deferred_kernel, dim3(64), blk, 0, stream, ix, ws.def, &ws.hdr->n_def, &ws.hdr->abort,

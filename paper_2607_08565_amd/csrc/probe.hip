@@ -278,11 +278,6 @@ __device__ bool key_present(const DevIndex &ix, uint64_t key) {
   return false;
 }
 
-__global__ void zero32_kernel(uint32_t *p, uint64_t n_words) {
-  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x;
-  for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_words; i += stride) p[i] = 0;
-}
-
 __global__ __launch_bounds__(TB) void bound_kernel(DevIndex ix, ProbeView pv, const uint64_t *__restrict__ keys,
                                                    const int64_t *__restrict__ blk_off, int32_t n_req,
                                                    uint64_t n_blocks) {
@@ -593,9 +588,11 @@ extern "C" int smetric_probe_lookup(const smetric_index *idx, void *probe, uint6
   probe_layout(n_blocks, &pv, probe);
   const DevIndex ix = dev_view(idx);
   const uint64_t nw = skip_words(uint64_t(n_blocks < 1 ? 1 : n_blocks));
-  hipLaunchKernelGGL(zero32_kernel, dim3(nw / TB + 1 < 256 ? nw / TB + 1 : 256), dim3(TB), 0, stream, pv.skip, nw);
-  hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(64), 0, stream, reinterpret_cast<uint64_t *>(&pv.hdr->n_skip),
-                     uint64_t(2));
+  // the skip bitmap (whole 64-bit words: its allocation is rounded up to 256 bytes) and
+  // the probe counters, one launch
+  hipLaunchKernelGGL(zero2_kernel, dim3(nw / TB + 1 < 256 ? nw / TB + 1 : 256), dim3(TB), 0, stream,
+                     reinterpret_cast<uint64_t *>(pv.skip), (nw + 1) / 2,
+                     reinterpret_cast<uint64_t *>(&pv.hdr->n_skip), uint64_t(2));
   if (n_req > 0 && n_blocks > 0)
     hipLaunchKernelGGL(bound_kernel, dim3((uint64_t(n_req) * BL + TB - 1) / TB), dim3(TB), 0, stream, ix, pv, keys,
                        blk_off, n_req, uint64_t(n_blocks));
